@@ -1,0 +1,225 @@
+"""CPU oracle for HillInfer's per-decode-step token-importance path.
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py`` may import this module.  It shares no
+code with the GPU library (``paper_2602_18750_amd``) and never imports it.
+
+This is a thin ctypes/numpy wrapper around ``hill_oracle.c`` (plain C, fp64
+accumulation over exactly widened fp16/bf16 inputs).  Every function follows
+one definition of the paper (arxiv 2602.18750):
+
+* :func:`logits`      -- the raw inner product q.K^T (Sec. 4.4 "Algorithmic
+                         Simplification"; Sec. 2.1 Eq. 1 for the product).
+* :func:`update`      -- per-step attention weights softmax(q.K^T / sqrt(d))
+                         (Eq. 1) or raw logits (Sec. 4.4), summed column-wise
+                         into the cumulative importance S (Sec. 4.1).
+* :func:`topk`        -- the top-alpha selection (Sec. 3.1, Sec. 4.2 HIE),
+                         brute force by full sort, ties to the lower index.
+* :func:`sparse_attn` -- Eq. 1 restricted to the selected tokens (Sec. 4.1,
+                         workflow step 6).
+* :func:`step`        -- the three in the workflow's order.
+
+16-bit inputs are passed as ``numpy.uint16`` bit patterns; the oracle decodes
+them itself (:func:`decode16`).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "hill_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libhill_oracle.so")
+
+F16, BF16 = 0, 1
+ATTN, RAW = 0, 1
+TOKEN, KVHEAD = 0, 1
+
+_DTYPES = {"fp16": F16, "f16": F16, "float16": F16, "bf16": BF16, "bfloat16": BF16}
+_MODES = {"attn": ATTN, "raw": RAW}
+_GRANS = {"token": TOKEN, "kvhead": KVHEAD}
+
+_lock = threading.Lock()
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math)."""
+    if force or not os.path.exists(_LIB_PATH) or (
+        os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
+    ):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+               "-D_POSIX_C_SOURCE=200809L", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        build()
+        lib = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        I = ctypes.c_int
+        I64 = ctypes.c_int64
+        Dd = ctypes.c_double
+        lib.hor_decode16.argtypes = [P, I64, I, P]
+        lib.hor_decode16.restype = None
+        lib.hor_num_threads.argtypes = []
+        lib.hor_num_threads.restype = I
+        lib.hor_logits.argtypes = [I, I, I, I, I, I, P, P, P]
+        lib.hor_logits.restype = I
+        lib.hor_update.argtypes = [I, I, I, I, I, I, Dd, P, P]
+        lib.hor_update.restype = I
+        lib.hor_topk.argtypes = [I64, I, I, P, P]
+        lib.hor_topk.restype = I
+        lib.hor_sparse_attn.argtypes = [I, I, I, I, I, I, I, Dd, P, P, P, I, P, P]
+        lib.hor_sparse_attn.restype = I
+        lib.hor_step.argtypes = [I, I, I, I, I, I, I, I, Dd, P, P, P, P, P, I, P, P, P]
+        lib.hor_step.restype = I
+        _lib = lib
+        return lib
+
+
+def _ptr(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def _u16(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.uint16:
+        raise TypeError("16-bit inputs must be passed as uint16 bit patterns")
+    return a
+
+
+def _code(table, key):
+    if isinstance(key, int):
+        return key
+    return table[key.lower()]
+
+
+def num_threads() -> int:
+    return int(_load().hor_num_threads())
+
+
+def default_scale(D: int) -> float:
+    """1/sqrt(d), the scale of Eq. 1."""
+    return 1.0 / float(np.sqrt(D))
+
+
+def decode16(bits, dtype) -> np.ndarray:
+    """Widen fp16/bf16 bit patterns to float64 exactly."""
+    lib = _load()
+    bits = _u16(bits)
+    out = np.empty(bits.shape, dtype=np.float64)
+    lib.hor_decode16(_ptr(bits), bits.size, _code(_DTYPES, dtype), _ptr(out))
+    return out
+
+
+def logits(q, k, dtype) -> np.ndarray:
+    """l[b,h,j] = q[b,h,:] . K[b,h//G,j,:] in float64.  q [B,Hq,D], K [B,Hkv,n,D]."""
+    lib = _load()
+    q, k = _u16(q), _u16(k)
+    B, Hq, D = q.shape
+    Bk, Hkv, n, Dk = k.shape
+    assert Bk == B and Dk == D
+    out = np.empty((B, Hq, n), dtype=np.float64)
+    rc = lib.hor_logits(B, Hq, Hkv, D, n, _code(_DTYPES, dtype), _ptr(q), _ptr(k), _ptr(out))
+    if rc:
+        raise ValueError("hor_logits failed (%d)" % rc)
+    return out
+
+
+def update(l, S, n_kv_heads: int, mode="attn", granularity="token", scale=None) -> np.ndarray:
+    """Return S + column-wise sum of this step's weights (a new array)."""
+    lib = _load()
+    l = np.ascontiguousarray(l, dtype=np.float64)
+    B, Hq, n = l.shape
+    S = np.array(S, dtype=np.float64, copy=True, order="C")
+    gran = _code(_GRANS, granularity)
+    R = 1 if gran == TOKEN else n_kv_heads
+    assert S.shape == (B, R, n), (S.shape, (B, R, n))
+    if scale is None:
+        raise ValueError("scale is required (1/sqrt(D) for Eq. 1)")
+    rc = lib.hor_update(B, Hq, n_kv_heads, n, _code(_MODES, mode), gran, float(scale), _ptr(l), _ptr(S))
+    if rc:
+        raise ValueError("hor_update failed (%d)" % rc)
+    return S
+
+
+def topk(S, k: int) -> np.ndarray:
+    """k largest per row of S [..., n]; ties to the lower index; ascending."""
+    lib = _load()
+    S = np.ascontiguousarray(S, dtype=np.float64)
+    n = S.shape[-1]
+    rows = int(np.prod(S.shape[:-1])) if S.ndim > 1 else 1
+    out = np.empty(S.shape[:-1] + (k,), dtype=np.int32)
+    rc = lib.hor_topk(rows, n, int(k), _ptr(S), _ptr(out))
+    if rc:
+        raise ValueError("hor_topk failed (%d)" % rc)
+    return out
+
+
+def sparse_attn(q, k, v, idx, dtype, granularity="token", scale=None) -> np.ndarray:
+    """Eq. 1 over the selected tokens; out [B,Hq,D] float64."""
+    lib = _load()
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    B, Hq, D = q.shape
+    _, Hkv, n, _ = k.shape
+    assert v.shape == k.shape
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    kk = idx.shape[-1]
+    gran = _code(_GRANS, granularity)
+    R = 1 if gran == TOKEN else Hkv
+    assert idx.shape == (B, R, kk), (idx.shape, (B, R, kk))
+    if scale is None:
+        scale = default_scale(D)
+    out = np.empty((B, Hq, D), dtype=np.float64)
+    rc = lib.hor_sparse_attn(B, Hq, Hkv, D, n, _code(_DTYPES, dtype), gran, float(scale),
+                             _ptr(q), _ptr(k), _ptr(v), kk, _ptr(idx), _ptr(out))
+    if rc:
+        raise ValueError("hor_sparse_attn failed (%d)" % rc)
+    return out
+
+
+def step(q, k, v, S, k_sel: int, dtype, mode="attn", granularity="token", scale=None,
+         return_times: bool = False):
+    """One decode step: update S with q, select k on the new S, attend.
+
+    Returns (S_new, idx, out[, (t_score, t_select, t_attn)])."""
+    lib = _load()
+    q, k, v = _u16(q), _u16(k), _u16(v)
+    B, Hq, D = q.shape
+    _, Hkv, n, _ = k.shape
+    gran = _code(_GRANS, granularity)
+    R = 1 if gran == TOKEN else Hkv
+    S = np.array(S, dtype=np.float64, copy=True, order="C")
+    assert S.shape == (B, R, n)
+    if scale is None:
+        scale = default_scale(D)
+    l = np.empty((B, Hq, n), dtype=np.float64)
+    idx = np.empty((B, R, k_sel), dtype=np.int32)
+    out = np.empty((B, Hq, D), dtype=np.float64)
+    t = np.zeros(3, dtype=np.float64)
+    rc = lib.hor_step(B, Hq, Hkv, D, n, _code(_DTYPES, dtype), _code(_MODES, mode), gran,
+                      float(scale), _ptr(q), _ptr(k), _ptr(v), _ptr(S), _ptr(l), int(k_sel),
+                      _ptr(idx), _ptr(out), _ptr(t))
+    if rc:
+        raise ValueError("hor_step failed (%d)" % rc)
+    if return_times:
+        return S, idx, out, tuple(float(x) for x in t)
+    return S, idx, out
+
+
+def budget_k(n: int, alpha: float) -> int:
+    """Token budget k = floor(alpha * n), clamped to [1, n] (top-alpha percent, Sec. 3.1)."""
+    import math
+    return max(1, min(n, int(math.floor(alpha * n + 1e-9))))

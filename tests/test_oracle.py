@@ -1,0 +1,317 @@
+"""Pins for the CPU oracle (run without a GPU).
+
+Each test checks the oracle against something other than itself: a library
+routine (torch / numpy), a closed form, an invariant the paper's definitions
+imply, or brute force on tiny inputs.  The oracle is the yard-stick of the GPU
+parity tests, so every function here is chosen so that a plausible slip in
+it (a dropped term, a wrong sign, a wrong GQA index, a transposed operand,
+a wrong scale, an off-by-one in selection) fails at least one test.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+from hypothesis import given, settings, strategies as st
+
+from oracle import oracle as O
+from paper_2602_18750_amd import workloads as W
+from util import bits, dname
+
+
+
+# ---------------------------------------------------------------- decoding --
+
+@pytest.mark.parametrize("tdt", [torch.float16, torch.bfloat16])
+def test_decode16_exhaustive_matches_torch(tdt):
+    """All 65536 bit patterns widen exactly as torch's .double() does."""
+    pats = np.arange(65536, dtype=np.uint16)
+    ref = torch.from_numpy(pats.view(np.int16).copy()).view(tdt).double().numpy()
+    got = O.decode16(pats, "fp16" if tdt == torch.float16 else "bf16")
+    nan = np.isnan(ref)
+    assert np.array_equal(nan, np.isnan(got))
+    assert np.array_equal(got[~nan], ref[~nan])
+    # signed zeros keep their sign
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+# ------------------------------------------------------------------ logits --
+
+def _dense_logits_library(x):
+    """q.K^T via torch.matmul with KV heads repeated per GQA group."""
+    q = x.q[0].double()                      # [B,Hq,D]
+    k = x.k.double()                         # [B,Hkv,n,D]
+    G = q.shape[1] // k.shape[1]
+    kr = k.repeat_interleave(G, dim=1)       # [B,Hq,n,D]
+    return torch.matmul(kr, q.unsqueeze(-1)).squeeze(-1).numpy()
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,D,n,dt", [
+    (1, 4, 4, 8, 5, "fp16"), (2, 8, 2, 16, 33, "bf16"), (1, 32, 1, 128, 7, "fp16"),
+    (3, 6, 3, 4, 11, "bf16"),
+])
+def test_logits_match_library_matmul(B, Hq, Hkv, D, n, dt):
+    x = W.make_random(B, Hq, Hkv, D, n, dt, seed=B * 100 + n)
+    got = O.logits(bits(x.q[0]), bits(x.k), dt)
+    ref = _dense_logits_library(x)
+    np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-12)
+
+
+def test_logits_one_hot_keys_closed_form():
+    """K rows equal to unit vectors e_i make l[h,j] = q[h, i_j] exactly."""
+    B, Hq, Hkv, D, n = 1, 4, 2, 8, 8
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=3)
+    k = torch.zeros(B, Hkv, n, D, dtype=torch.float16)
+    for g in range(Hkv):
+        for j in range(n):
+            k[0, g, j, (j + 3 * g) % D] = 1.0
+    l = O.logits(bits(x.q[0]), bits(k), "fp16")
+    q = x.q[0].double().numpy()
+    for h in range(Hq):
+        g = h // (Hq // Hkv)
+        for j in range(n):
+            assert l[0, h, j] == q[0, h, (j + 3 * g) % D]
+
+
+def test_logits_gqa_mapping_is_contiguous_groups():
+    """kv(h) = h // G, not h % G: the two differ and the oracle follows the first."""
+    B, Hq, Hkv, D, n = 1, 8, 2, 16, 9
+    x = W.make_random(B, Hq, Hkv, D, n, "bf16", seed=5)
+    got = O.logits(bits(x.q[0]), bits(x.k), "bf16")
+    q, k = x.q[0].double().numpy(), x.k.double().numpy()
+    G = Hq // Hkv
+    right = np.stack([k[0, h // G] @ q[0, h] for h in range(Hq)])
+    wrong = np.stack([k[0, h % Hkv] @ q[0, h] for h in range(Hq)])
+    np.testing.assert_allclose(got[0], right, rtol=1e-13, atol=1e-12)
+    assert not np.allclose(got[0], wrong)
+
+
+# ----------------------------------------------------------------- weights --
+
+@pytest.mark.parametrize("gran", ["token", "kvhead"])
+@pytest.mark.parametrize("Hq,Hkv", [(4, 4), (8, 2), (8, 1)])
+def test_attn_update_matches_torch_softmax(gran, Hq, Hkv):
+    B, D, n = 2, 16, 29
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=Hq * 10 + Hkv)
+    l = O.logits(bits(x.q[0]), bits(x.k), "fp16")
+    R = 1 if gran == "token" else Hkv
+    S0 = np.random.default_rng(0).random((B, R, n))
+    s = 1 / math.sqrt(D)
+    got = O.update(l, S0, Hkv, "attn", gran, s)
+    w = torch.softmax(torch.from_numpy(l) * s, dim=-1).numpy()     # [B,Hq,n]
+    if gran == "token":
+        ref = S0 + w.sum(axis=1, keepdims=True)
+    else:
+        ref = S0 + w.reshape(B, Hkv, Hq // Hkv, n).sum(axis=2)
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("gran", ["token", "kvhead"])
+def test_attn_update_column_mass_invariant(gran):
+    """Each head's weights sum to one, so one step adds |heads(r)| to each row's total."""
+    B, Hq, Hkv, D, n = 2, 32, 8, 128, 300
+    x = W.make_random(B, Hq, Hkv, D, n, "bf16", seed=9, keys="outlier")
+    l = O.logits(bits(x.q[0]), bits(x.k), "bf16")
+    R = 1 if gran == "token" else Hkv
+    S0 = np.zeros((B, R, n))
+    S1 = O.update(l, S0, Hkv, "attn", gran, 1 / math.sqrt(128))
+    per_row = Hq if gran == "token" else Hq // Hkv
+    np.testing.assert_allclose(S1.sum(axis=-1), per_row, rtol=1e-12)
+    assert (S1 > 0).all()
+
+
+def test_attn_scale_is_inverse_sqrt_d():
+    """A scale of 1/sqrt(D) (Eq. 1) gives softmax(l/sqrt(D)); 1/D or 1 give something else."""
+    B, Hq, Hkv, D, n = 1, 2, 2, 64, 17
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=2)
+    l = O.logits(bits(x.q[0]), bits(x.k), "fp16")
+    S = O.update(l, np.zeros((B, Hkv, n)), Hkv, "attn", "kvhead", 1 / 8.0)
+    for h in range(Hq):
+        e = np.exp(l[0, h] / 8.0 - (l[0, h] / 8.0).max())
+        np.testing.assert_allclose(S[0, h], e / e.sum(), rtol=1e-12)
+        e2 = np.exp(l[0, h] / 64.0 - (l[0, h] / 64.0).max())
+        assert not np.allclose(S[0, h], e2 / e2.sum())
+
+
+def test_raw_update_linearity_closed_form():
+    """RAW: S_T - S_0 = sum_{h in r} (sum_t q_{t,h}) . K_{kv(h)}^T (linear in q)."""
+    B, Hq, Hkv, D, n, T = 2, 8, 2, 32, 19, 4
+    x = W.make_random(B, Hq, Hkv, D, n, "bf16", steps=T, seed=4)
+    S = np.zeros((B, Hkv, n))
+    for t in range(T):
+        l = O.logits(bits(x.q[t]), bits(x.k), "bf16")
+        S = O.update(l, S, Hkv, "raw", "kvhead", 1 / math.sqrt(D))
+    qs = x.q.double().sum(dim=0)                          # [B,Hq,D]
+    k = x.k.double()
+    G = Hq // Hkv
+    ref = torch.einsum("bgjd,bgd->bgj", k, qs.view(B, Hkv, G, D).sum(dim=2)).numpy()
+    np.testing.assert_allclose(S, ref, rtol=1e-11, atol=1e-10)
+
+
+def test_multistep_is_sum_of_independent_steps():
+    """The per-step softmax runs over all tokens, so S_T = sum_t (one-step S from zero)."""
+    B, Hq, Hkv, D, n, T = 1, 8, 2, 16, 40, 5
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", steps=T, seed=6)
+    S = np.zeros((B, 1, n))
+    acc = np.zeros((B, 1, n))
+    for t in range(T):
+        S, idx, out = O.step(bits(x.q[t]), bits(x.k), bits(x.v), S, 7, "fp16")
+        l = O.logits(bits(x.q[t]), bits(x.k), "fp16")
+        acc += O.update(l, np.zeros((B, 1, n)), Hkv, "attn", "token", 1 / 4.0)
+    np.testing.assert_allclose(S, acc, rtol=1e-12)
+
+
+def test_raw_and_attn_select_the_same_tokens_for_one_mha_head_one_step():
+    """Softmax is monotone: for one head, one step, from S=0, ranking is unchanged (Sec. 4.4)."""
+    B, Hq, Hkv, D, n = 2, 4, 4, 64, 200
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=8)
+    S0 = np.zeros((B, Hkv, n))
+    _, ia, _ = O.step(bits(x.q[0]), bits(x.k), bits(x.v), S0, 37, "fp16", "attn", "kvhead")
+    _, ir, _ = O.step(bits(x.q[0]), bits(x.k), bits(x.v), S0, 37, "fp16", "raw", "kvhead")
+    assert np.array_equal(ia, ir)
+
+
+def test_raw_and_attn_rank_differently_when_heads_are_summed():
+    """Summed over heads the monotonicity argument breaks: token mode RAW != ATTN in general."""
+    B, Hq, Hkv, D, n = 1, 32, 8, 128, 512
+    x = W.make_random(B, Hq, Hkv, D, n, "bf16", seed=11, keys="outlier")
+    S0 = np.zeros((B, 1, n))
+    _, ia, _ = O.step(bits(x.q[0]), bits(x.k), bits(x.v), S0, 51, "bf16", "attn", "token")
+    _, ir, _ = O.step(bits(x.q[0]), bits(x.k), bits(x.v), S0, 51, "bf16", "raw", "token")
+    assert not np.array_equal(ia, ir)
+
+
+# -------------------------------------------------------------------- top-k --
+
+def _brute_topk(S, k):
+    """numpy lexsort: primary key -S (NaN last), secondary token index."""
+    out = []
+    for row in S.reshape(-1, S.shape[-1]):
+        n = row.size
+        key = np.where(np.isnan(row), np.inf, -row)
+        key = np.where(key == 0.0, 0.0, key)                      # -0 ties +0
+        order = np.lexsort((np.arange(n), key))
+        out.append(np.sort(order[:k]))
+    return np.array(out, dtype=np.int32).reshape(S.shape[:-1] + (k,))
+
+
+@settings(max_examples=150, deadline=None)
+@given(st.data())
+def test_topk_matches_full_sort_on_tie_heavy_rows(data):
+    rows = data.draw(st.integers(1, 4))
+    n = data.draw(st.integers(1, 300))
+    k = data.draw(st.integers(1, n))
+    grid = data.draw(st.sampled_from([2, 5, 17, 1000]))
+    vals = data.draw(st.lists(st.integers(-grid, grid), min_size=rows * n, max_size=rows * n))
+    S = np.array(vals, dtype=np.float64).reshape(rows, n) / 7.0
+    assert np.array_equal(O.topk(S, k), _brute_topk(S, k))
+
+
+def test_topk_special_cases():
+    rng = np.random.default_rng(1)
+    S = rng.standard_normal((3, 101))
+    # k = 1 is argmax with the first occurrence winning
+    S[1, 10] = S[1, 70] = S[1].max() + 1
+    got = O.topk(S, 1)[:, 0]
+    assert np.array_equal(got, np.argmax(S, axis=1))
+    assert got[1] == 10
+    # k = n is every index
+    assert np.array_equal(O.topk(S, 101), np.tile(np.arange(101), (3, 1)))
+    # all equal -> the lowest k indices
+    assert np.array_equal(O.topk(np.full((2, 50), 0.25), 13), np.tile(np.arange(13), (2, 1)))
+    # -0.0 and +0.0 tie: the lower index wins regardless of sign
+    z = np.array([[1.0, -0.0, 0.0, -1.0, -0.0]])
+    assert np.array_equal(O.topk(z, 2), [[0, 1]])
+    assert np.array_equal(O.topk(z, 4), [[0, 1, 2, 4]])
+    # NaN ranks below everything, -inf above NaN
+    w = np.array([[np.nan, -np.inf, 3.0, np.nan, np.inf]])
+    assert np.array_equal(O.topk(w, 3), [[1, 2, 4]])
+    # output is ascending by token index
+    big = rng.standard_normal((1, 1000))
+    t = O.topk(big, 100)[0]
+    assert np.all(np.diff(t) > 0)
+    assert set(t) == set(np.argsort(-big[0])[:100])
+
+
+def test_topk_off_by_one_is_caught():
+    """The k-th largest is in, the (k+1)-th is out."""
+    S = np.arange(20, dtype=np.float64)[None, ::-1].copy()      # 19..0
+    got = O.topk(S, 5)[0]
+    assert np.array_equal(got, [0, 1, 2, 3, 4])
+
+
+# ---------------------------------------------------------------- attention --
+
+def _sdpa_dense(x, scale=None):
+    q = x.q[0].double().unsqueeze(2)                          # [B,Hq,1,D]
+    G = x.q.shape[2] // x.k.shape[1]
+    k = x.k.double().repeat_interleave(G, dim=1)
+    v = x.v.double().repeat_interleave(G, dim=1)
+    return torch.nn.functional.scaled_dot_product_attention(q, k, v, scale=scale).squeeze(2).numpy()
+
+
+@pytest.mark.parametrize("gran", ["token", "kvhead"])
+@pytest.mark.parametrize("B,Hq,Hkv,D,n,dt", [(1, 4, 4, 32, 23, "fp16"), (2, 8, 2, 64, 50, "bf16"),
+                                            (1, 32, 8, 128, 64, "bf16")])
+def test_full_budget_reproduces_dense_sdpa(gran, B, Hq, Hkv, D, n, dt):
+    x = W.make_random(B, Hq, Hkv, D, n, dt, seed=n)
+    R = 1 if gran == "token" else Hkv
+    _, idx, out = O.step(bits(x.q[0]), bits(x.k), bits(x.v), np.zeros((B, R, n)), n, dt, "attn", gran)
+    assert np.array_equal(idx, np.tile(np.arange(n), (B, R, 1)))
+    np.testing.assert_allclose(out, _sdpa_dense(x), rtol=1e-12, atol=1e-13)
+
+
+def test_single_token_budget_returns_that_value_row():
+    B, Hq, Hkv, D, n = 2, 8, 2, 16, 30
+    x = W.make_random(B, Hq, Hkv, D, n, "bf16", seed=12)
+    idx = np.array([[[7]], [[29]]], dtype=np.int32)
+    out = O.sparse_attn(bits(x.q[0]), bits(x.k), bits(x.v), idx, "bf16", "token")
+    v = x.v.double().numpy()
+    for b in range(B):
+        for h in range(Hq):
+            assert np.array_equal(out[b, h], v[b, h // 4, idx[b, 0, 0]])
+
+
+def test_sparse_attention_matches_library_on_subset_and_is_order_free():
+    """Attention over I equals SDPA on the gathered rows, for any order of I."""
+    B, Hq, Hkv, D, n = 1, 8, 2, 32, 60
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=13)
+    I = np.array([3, 5, 11, 12, 40, 59], dtype=np.int32)
+    out = O.sparse_attn(bits(x.q[0]), bits(x.k), bits(x.v), I[None, None], "fp16", "token")
+    perm = O.sparse_attn(bits(x.q[0]), bits(x.k), bits(x.v), I[::-1].copy()[None, None], "fp16", "token")
+    np.testing.assert_allclose(out, perm, rtol=1e-13, atol=1e-14)
+    sub = W.LayerInputs(q=x.q, k=x.k[:, :, I], v=x.v[:, :, I], heavy=None)
+    np.testing.assert_allclose(out, _sdpa_dense(sub), rtol=1e-12, atol=1e-13)
+
+
+def test_kvhead_mode_attends_each_group_over_its_own_set():
+    B, Hq, Hkv, D, n = 1, 4, 2, 16, 20
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=14)
+    idx = np.array([[[0, 1, 2], [17, 18, 19]]], dtype=np.int32)
+    out = O.sparse_attn(bits(x.q[0]), bits(x.k), bits(x.v), idx, "fp16", "kvhead")
+    for g, I in enumerate(idx[0]):
+        sub = W.LayerInputs(q=x.q[:, :, 2 * g:2 * g + 2], k=x.k[:, g:g + 1, I], v=x.v[:, g:g + 1, I],
+                            heavy=None)
+        np.testing.assert_allclose(out[:, 2 * g:2 * g + 2], _sdpa_dense(sub), rtol=1e-12, atol=1e-13)
+
+
+# --------------------------------------------------------------- workflow --
+
+def test_step_orders_update_before_selection():
+    """Selection uses S after this step's update (Sec. 4.1 workflow steps 5 then 6)."""
+    B, Hq, Hkv, D, n = 1, 4, 4, 16, 50
+    x = W.make_random(B, Hq, Hkv, D, n, "fp16", seed=15)
+    S0 = np.zeros((B, 1, n))
+    S1, idx, _ = O.step(bits(x.q[0]), bits(x.k), bits(x.v), S0, 10, "fp16")
+    assert np.array_equal(idx, O.topk(S1, 10))
+
+
+def test_budget_rounding():
+    assert O.budget_k(4096, 0.20) == 819
+    assert O.budget_k(32768, 0.10) == 3276
+    assert O.budget_k(131072, 0.05) == 6553
+    assert O.budget_k(65536, 0.20) == 13107
+    assert O.budget_k(3, 0.05) == 1
+    for n, a in itertools.product([8192, 32768, 65536], [0.05, 0.10, 0.20]):
+        assert O.budget_k(n, a) == W.budget_tokens(n, a)
