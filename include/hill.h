@@ -1,0 +1,155 @@
+/*
+ * hill.h -- C ABI of libhill: the per-decode-step token-importance path of
+ * HillInfer (arxiv 2602.18750) on AMD Instinct MI355X (gfx950).
+ *
+ * One decode step of one layer, for a batch of sequences that each own a
+ * KV cache (Sec. 2.1, "KV Cache Mechanism"):
+ *
+ *   score      l[b,h,j] = q[b,h,:] . K[b,kv(h),j,:]           (Sec. 4.4, Eq. 1)
+ *              ATTN: w = softmax_j(sm_scale * l)  (Eq. 1 weights)
+ *              RAW:  w = l                        (Sec. 4.4 simplification)
+ *              S[b,r,j] += sum_{h in heads(r)} w[b,h,j]         (Sec. 4.1)
+ *   select     idx[b,r,:] = the k largest S[b,r,:], ascending token order,
+ *              ties to the lower token index    (Sec. 3.1 top-alpha; Sec. 4.2)
+ *   attention  out[b,h,:] = softmax over I of sm_scale * q.K_j, times V_j,
+ *              I = idx[b,r(h),:]                 (Eq. 1 over the selection;
+ *                                                 Sec. 4.1 workflow step 6)
+ *
+ * kv(h) = h / G with G = n_q_heads / n_kv_heads (contiguous GQA groups; MHA is
+ * G = 1, MQA is n_kv_heads = 1).  Granularity: HILL_SEL_TOKEN keeps one
+ * importance row and one index set per sequence (R = 1, summed over all query
+ * heads); HILL_SEL_KVHEAD keeps one per (sequence, KV head) (R = n_kv_heads,
+ * summed over that head's G query heads); r(h) = 0 or kv(h) respectively.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Every data pointer is a DEVICE pointer owned by the caller; the
+ *   library never allocates, frees or synchronises.  Scratch memory is the
+ *   caller's workspace `ws` of at least hill_workspace_bytes() bytes, 16-byte
+ *   aligned; its contents on entry are irrelevant and on return undefined.
+ * Streams.  `stream` is a hipStream_t (NULL = the default stream).  All work
+ *   is enqueued on it in order and the call returns without waiting.
+ * Layouts.  q: fp16/bf16 [B, Hq, D] with strides (q_stride_b, q_stride_h),
+ *   D contiguous.  K, V: fp16/bf16 [B, Hkv, Ncap, D] with strides
+ *   (*_stride_b, *_stride_h, *_stride_n), D contiguous, only the first
+ *   n_tokens rows read.  S: fp32 [B, R, >= n_tokens] with strides
+ *   (s_stride_b, s_stride_r), token index contiguous.  idx: int32
+ *   [B, R, k_sel] contiguous.  out: fp32 [B, Hq, D] contiguous.  Strides are
+ *   in elements.
+ * Alignment.  q, K, V, S, out and ws base addresses 16-byte aligned; q, K, V
+ *   strides multiples of 8 elements; S strides multiples of 4 elements.
+ * Supported.  head_dim == 128; dtype fp16 or bf16; n_q_heads % n_kv_heads
+ *   == 0; 1 <= k_sel <= n_tokens.
+ * Errors.  All arguments are checked on the host before anything is
+ *   enqueued; on any error nothing is enqueued and no output is written.
+ *   HILL_ERR_INVALID_ARG: null/misaligned pointer, bad shape, stride or k_sel.
+ *   HILL_ERR_UNSUPPORTED: a valid but unimplemented head_dim or dtype.
+ *   HILL_ERR_WORKSPACE:   ws too small.
+ *   HILL_ERR_HIP:         a kernel launch failed (enqueued work before it in
+ *                         the same call may still run).
+ *   Device-side faults surface at the caller's next synchronisation.
+ *   hill_last_error() returns a message for the calling thread's last error.
+ * Determinism.  No floating-point atomics: results are bitwise reproducible
+ *   for identical inputs and shapes.
+ * Inputs containing Inf/NaN are outside the contract; they never cause an
+ *   out-of-bounds access (NaN importance ranks below every number).
+ */
+#ifndef HILL_H
+#define HILL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define HILL_ABI_VERSION 1
+
+typedef enum hill_status {
+    HILL_OK = 0,
+    HILL_ERR_INVALID_ARG = 1,
+    HILL_ERR_UNSUPPORTED = 2,
+    HILL_ERR_WORKSPACE = 3,
+    HILL_ERR_HIP = 4
+} hill_status;
+
+typedef enum hill_dtype { HILL_F16 = 0, HILL_BF16 = 1 } hill_dtype;
+
+/* ATTN: column sums of softmax(sm_scale * q.K^T) (Sec. 4.1 importance metric).
+ * RAW: column sums of the raw q.K^T (Sec. 4.4 simplification; no scale). */
+typedef enum hill_score_mode { HILL_SCORE_ATTN = 0, HILL_SCORE_RAW = 1 } hill_score_mode;
+
+typedef enum hill_granularity { HILL_SEL_TOKEN = 0, HILL_SEL_KVHEAD = 1 } hill_granularity;
+
+/* Problem descriptor.  Set struct_size = sizeof(hill_desc). */
+typedef struct hill_desc {
+    uint32_t struct_size;
+    int32_t batch;        /* B  >= 1 */
+    int32_t n_q_heads;    /* Hq >= 1 */
+    int32_t n_kv_heads;   /* Hkv >= 1, divides Hq */
+    int32_t head_dim;     /* D == 128 */
+    int32_t n_tokens;     /* n >= 1: cached tokens scored this step */
+    int32_t dtype;        /* hill_dtype of q, K, V */
+    int32_t score_mode;   /* hill_score_mode */
+    int32_t granularity;  /* hill_granularity */
+    float sm_scale;       /* softmax scale; 0 selects 1/sqrt(head_dim) */
+    int64_t q_stride_b, q_stride_h;
+    int64_t k_stride_b, k_stride_h, k_stride_n;
+    int64_t v_stride_b, v_stride_h, v_stride_n;
+    int64_t s_stride_b, s_stride_r;
+} hill_desc;
+
+/* ABI version of the loaded library (HILL_ABI_VERSION it was built with). */
+int hill_abi_version(void);
+
+/* Static description of a status code. */
+const char* hill_status_str(int status);
+
+/* Message describing the calling thread's most recent failed call (empty
+ * string if none).  Valid until the next libhill call on this thread. */
+const char* hill_last_error(void);
+
+/* Workspace bytes that hill_score / hill_topk / hill_gather_attn / hill_step
+ * need for this descriptor and token budget (the maximum over the four).
+ * Pure host function; writes *bytes.  k_sel is only used by the attention
+ * and select parts and may be any value in [1, n_tokens]. */
+hill_status hill_workspace_bytes(const hill_desc* d, int32_t k_sel, size_t* bytes);
+
+/* Importance scoring (Sec. 4.1 metric; Sec. 4.4 raw variant):
+ * S[b,r,j] += sum_{h in heads(r)} w[b,h,j] for every j < n_tokens.
+ * q, k: inputs.  s: in/out, the caller's cumulative importance (zero it
+ * before the first step and for newly appended tokens). */
+hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* s,
+                       void* ws, size_t ws_bytes, void* stream);
+
+/* Top-k selection (Sec. 3.1 top-alpha; Sec. 4.2 global top-alpha indices):
+ * for each row (b, r), the k_sel tokens with the largest S, ties broken toward
+ * the lower token index, NaN below every number, -0.0 equal to +0.0.
+ * idx_out: [B, R, k_sel] int32, ascending within a row.
+ * val_out: nullable; if given, [B, R, k_sel] fp32 with S at those tokens. */
+hill_status hill_topk(const hill_desc* d, const float* s, int32_t k_sel,
+                      int32_t* idx_out, float* val_out,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* Sparse decode attention over the selected tokens (Eq. 1 restricted to I,
+ * softmax renormalised over I).  idx: [B, R, k_sel] int32, each row k_sel
+ * distinct indices in [0, n_tokens) in any order (not checked on device;
+ * out-of-range indices are undefined behaviour).  out: [B, Hq, D] fp32. */
+hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v,
+                             const int32_t* idx, int32_t k_sel, float* out,
+                             void* ws, size_t ws_bytes, void* stream);
+
+/* One full decode step in the paper's order (Sec. 4.1 workflow, steps 5-6):
+ * update S with this query, select k_sel tokens on the updated S, attend over
+ * them.  Equivalent to hill_score, hill_topk (val_out = NULL) and
+ * hill_gather_attn in sequence, with fewer launches. */
+hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v,
+                      float* s, int32_t k_sel, int32_t* idx_out, float* out,
+                      void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HILL_H */

@@ -1,0 +1,402 @@
+// C-ABI host layer of libhill: argument validation, workspace layout and
+// kernel orchestration.  Every check runs before the first HIP call, so an
+// invalid call enqueues nothing and touches no output.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "hill.h"
+#include "hill_internal.h"
+
+using namespace hill;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+hill_status fail(hill_status st, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return st;
+}
+
+// Shape facts derived from a validated descriptor.
+struct Shape {
+    int B, Hq, Hkv, G, D, n, R, ntiles;
+    int dtype, mode, gran;
+    float scale;
+};
+
+// Workspace regions, in this order, each 256-byte aligned:
+//   logits  ATTN [B,Hq,n] fp32 | RAW token rows with Hkv > 1: [B,Hkv,n] fp32
+//   part    ATTN [B,Hq,ntiles] float2
+//   stats   ATTN [B,Hq] float2
+//   hist    [B*R, 4096] u32
+//   apart_o [B,Hq,nsplit,D] fp32, apart_ml [B,Hq,nsplit] float2
+// The scoring and selection regions do not depend on k_sel.
+struct Layout {
+    size_t logits, part, stats, hist, apart_o, apart_ml;
+    size_t end_score, end_topk, end_all;
+    int nsplit, per_split;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+Layout layout_for(const Shape& s, int ksel)
+{
+    Layout L{};
+    size_t off = 0;
+    const bool attn = s.mode == HILL_SCORE_ATTN;
+    const bool raw_groups = !attn && s.gran == HILL_SEL_TOKEN && s.Hkv > 1;
+    L.logits = off;
+    if (attn) off += align256((size_t)s.B * s.Hq * s.n * sizeof(float));
+    else if (raw_groups) off += align256((size_t)s.B * s.Hkv * s.n * sizeof(float));
+    L.part = off;
+    if (attn) off += align256((size_t)s.B * s.Hq * s.ntiles * sizeof(float2));
+    L.stats = off;
+    if (attn) off += align256((size_t)s.B * s.Hq * sizeof(float2));
+    L.hist = off;
+    off += align256((size_t)s.B * s.R * kHistBins * sizeof(uint32_t));
+    L.end_score = off;   // scoring uses the hist region only inside hill_step
+    L.end_topk = off;
+    L.nsplit = attn_splits((int64_t)s.B * s.Hkv, ksel, &L.per_split);
+    L.apart_o = off;
+    off += align256((size_t)s.B * s.Hq * L.nsplit * kHeadDim * sizeof(float));
+    L.apart_ml = off;
+    off += align256((size_t)s.B * s.Hq * L.nsplit * sizeof(float2));
+    L.end_all = off;
+    return L;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
+{
+    if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
+    if (d->struct_size != sizeof(hill_desc))
+        return fail(HILL_ERR_INVALID_ARG, "struct_size %u != sizeof(hill_desc) %zu", d->struct_size,
+                    sizeof(hill_desc));
+    if (d->batch < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1 || d->n_tokens < 1 || d->head_dim < 1)
+        return fail(HILL_ERR_INVALID_ARG, "batch, heads, head_dim and n_tokens must be >= 1");
+    if (d->n_q_heads % d->n_kv_heads)
+        return fail(HILL_ERR_INVALID_ARG, "n_q_heads %d is not a multiple of n_kv_heads %d", d->n_q_heads,
+                    d->n_kv_heads);
+    if (d->dtype != HILL_F16 && d->dtype != HILL_BF16)
+        return fail(HILL_ERR_UNSUPPORTED, "dtype %d is not fp16 (0) or bf16 (1)", d->dtype);
+    if (d->score_mode != HILL_SCORE_ATTN && d->score_mode != HILL_SCORE_RAW)
+        return fail(HILL_ERR_INVALID_ARG, "score_mode %d is not ATTN (0) or RAW (1)", d->score_mode);
+    if (d->granularity != HILL_SEL_TOKEN && d->granularity != HILL_SEL_KVHEAD)
+        return fail(HILL_ERR_INVALID_ARG, "granularity %d is not TOKEN (0) or KVHEAD (1)", d->granularity);
+    if (d->head_dim != kHeadDim)
+        return fail(HILL_ERR_UNSUPPORTED, "head_dim %d is not supported (only 128)", d->head_dim);
+    if (!std::isfinite(d->sm_scale)) return fail(HILL_ERR_INVALID_ARG, "sm_scale is not finite");
+    const int64_t D = d->head_dim;
+    const int64_t strides16[] = {d->q_stride_b, d->q_stride_h, d->k_stride_b, d->k_stride_h,
+                                 d->k_stride_n, d->v_stride_b, d->v_stride_h, d->v_stride_n};
+    for (int64_t st : strides16)
+        if (st < 0 || st % 8)
+            return fail(HILL_ERR_INVALID_ARG, "q/K/V strides must be non-negative multiples of 8 elements");
+    if (d->q_stride_h < D && d->n_q_heads > 1) return fail(HILL_ERR_INVALID_ARG, "q_stride_h < head_dim");
+    if (d->k_stride_n < D || d->v_stride_n < D)
+        return fail(HILL_ERR_INVALID_ARG, "k_stride_n / v_stride_n < head_dim");
+    const int R = d->granularity == HILL_SEL_TOKEN ? 1 : d->n_kv_heads;
+    if (uses_s) {
+        if (d->s_stride_r < d->n_tokens || d->s_stride_r % 4)
+            return fail(HILL_ERR_INVALID_ARG, "s_stride_r must be >= n_tokens and a multiple of 4");
+        if (d->s_stride_b % 4 || (d->batch > 1 && d->s_stride_b < (int64_t)R * d->s_stride_r))
+            return fail(HILL_ERR_INVALID_ARG, "s_stride_b must be a multiple of 4 and >= R * s_stride_r");
+    }
+    s->B = d->batch;
+    s->Hq = d->n_q_heads;
+    s->Hkv = d->n_kv_heads;
+    s->G = d->n_q_heads / d->n_kv_heads;
+    s->D = d->head_dim;
+    s->n = d->n_tokens;
+    s->R = R;
+    s->ntiles = (d->n_tokens + kScoreTile - 1) / kScoreTile;
+    s->dtype = d->dtype;
+    s->mode = d->score_mode;
+    s->gran = d->granularity;
+    s->scale = d->sm_scale != 0.0f ? d->sm_scale : 1.0f / std::sqrt((float)d->head_dim);
+    return HILL_OK;
+}
+
+hill_status check_ptr(const void* p, const char* name)
+{
+    if (!p) return fail(HILL_ERR_INVALID_ARG, "%s is NULL", name);
+    if (!aligned16(p)) return fail(HILL_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+    return HILL_OK;
+}
+
+hill_status check_ksel(const Shape& s, int32_t ksel)
+{
+    if (ksel < 1 || ksel > s.n) return fail(HILL_ERR_INVALID_ARG, "k_sel %d not in [1, n_tokens=%d]", ksel, s.n);
+    return HILL_OK;
+}
+
+hill_status check_ws(const void* ws, size_t ws_bytes, size_t need)
+{
+    if (ws_bytes < need)
+        return fail(HILL_ERR_WORKSPACE, "workspace of %zu bytes is smaller than the %zu needed", ws_bytes, need);
+    if (need && !ws) return fail(HILL_ERR_INVALID_ARG, "workspace is NULL");
+    if (need && !aligned16(ws)) return fail(HILL_ERR_INVALID_ARG, "workspace is not 16-byte aligned");
+    return HILL_OK;
+}
+
+#define HILL_TRY(expr)                            \
+    do {                                          \
+        hill_status st_ = (expr);                 \
+        if (st_ != HILL_OK) return st_;           \
+    } while (0)
+
+#define HIP_TRY(expr)                                                                              \
+    do {                                                                                           \
+        hipError_t e_ = (expr);                                                                    \
+        if (e_ != hipSuccess) return fail(HILL_ERR_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+    } while (0)
+
+// Compute units of the current device, cached per device.
+int device_cus()
+{
+    static int cache[64] = {0};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+    if (v > 0) return v;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
+    return v;
+}
+
+template <typename T>
+T* at(void* ws, size_t off)
+{
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// Scoring; if `hist` is given the first selection digit is counted as a side
+// effect (hill_step) and the counts are cleared by the first kernel.
+hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, float* sacc,
+                      void* ws, bool with_hist, hipStream_t st)
+{
+    uint32_t* hist = with_hist ? at<uint32_t>(ws, L.hist) : nullptr;
+    const int64_t hist_words = (int64_t)s.B * s.R * kHistBins;
+    ScoreArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.q_sb = d->q_stride_b;
+    a.q_sh = d->q_stride_h;
+    a.k_sb = d->k_stride_b;
+    a.k_sh = d->k_stride_h;
+    a.k_sn = d->k_stride_n;
+    a.B = s.B;
+    a.Hq = s.Hq;
+    a.Hkv = s.Hkv;
+    a.G = s.G;
+    a.n = s.n;
+    a.ntiles = s.ntiles;
+    a.s2 = s.scale * 1.4426950408889634f;
+    a.s = sacc;
+    a.s_sb = d->s_stride_b;
+    a.s_sr = d->s_stride_r;
+    a.zero_ptr = hist;
+    a.zero_words = with_hist ? hist_words : 0;
+    const int grid_cap = device_cus() * 4;
+
+    UpdateArgs u{};
+    u.s = sacc;
+    u.s_sb = d->s_stride_b;
+    u.s_sr = d->s_stride_r;
+    u.B = s.B;
+    u.Hq = s.Hq;
+    u.Hkv = s.Hkv;
+    u.G = s.G;
+    u.R = s.R;
+    u.n = s.n;
+    u.s2 = a.s2;
+    u.hist = hist;
+
+    if (s.mode == HILL_SCORE_ATTN) {
+        a.logits = at<float>(ws, L.logits);
+        a.part = at<float2>(ws, L.part);
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutLogits, grid_cap, st));
+        float2* stats = at<float2>(ws, L.stats);
+        HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.ntiles, st));
+        u.logits = a.logits;
+        u.stats = stats;
+        HIP_TRY(launch_update_attn(u, st));
+    } else if (s.R == s.Hkv) {
+        // one row per KV head (or a single KV head): the scan adds straight into S
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawS, grid_cap, st));
+        if (with_hist) HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, hist, st));
+    } else {
+        a.logits = at<float>(ws, L.logits);
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawGroups, grid_cap, st));
+        u.logits = a.logits;
+        HIP_TRY(launch_update_raw_groups(u, st));
+    }
+    return HILL_OK;
+}
+
+hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, const float* sacc, int32_t ksel,
+                       int32_t* idx, float* val, void* ws, bool hist_ready, hipStream_t st)
+{
+    uint32_t* hist = at<uint32_t>(ws, L.hist);
+    if (!hist_ready) {
+        HIP_TRY(launch_fill_zero(hist, (int64_t)s.B * s.R * kHistBins, st));
+        HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, hist, st));
+    }
+    SelectArgs a{};
+    a.s = sacc;
+    a.s_sb = d->s_stride_b;
+    a.s_sr = d->s_stride_r;
+    a.R = s.R;
+    a.n = s.n;
+    a.k = ksel;
+    a.hist = hist;
+    a.idx = idx;
+    a.val = val;
+    HIP_TRY(launch_topk_select(a, s.B * s.R, st));
+    return HILL_OK;
+}
+
+hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, const void* v,
+                     const int32_t* idx, int32_t ksel, float* out, void* ws, hipStream_t st)
+{
+    AttnArgs a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.q_sb = d->q_stride_b;
+    a.q_sh = d->q_stride_h;
+    a.k_sb = d->k_stride_b;
+    a.k_sh = d->k_stride_h;
+    a.k_sn = d->k_stride_n;
+    a.v_sb = d->v_stride_b;
+    a.v_sh = d->v_stride_h;
+    a.v_sn = d->v_stride_n;
+    a.idx = idx;
+    a.B = s.B;
+    a.Hq = s.Hq;
+    a.Hkv = s.Hkv;
+    a.G = s.G;
+    a.R = s.R;
+    a.n = s.n;
+    a.ksel = ksel;
+    a.nsplit = L.nsplit;
+    a.per_split = L.per_split;
+    a.s2 = s.scale * 1.4426950408889634f;
+    a.part_o = at<float>(ws, L.apart_o);
+    a.part_ml = at<float2>(ws, L.apart_ml);
+    a.out = out;
+    HIP_TRY(launch_attn_split(a, s.dtype, st));
+    HIP_TRY(launch_attn_combine(a, st));
+    return HILL_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int hill_abi_version(void) { return HILL_ABI_VERSION; }
+
+const char* hill_status_str(int status)
+{
+    switch (status) {
+    case HILL_OK: return "HILL_OK";
+    case HILL_ERR_INVALID_ARG: return "HILL_ERR_INVALID_ARG";
+    case HILL_ERR_UNSUPPORTED: return "HILL_ERR_UNSUPPORTED";
+    case HILL_ERR_WORKSPACE: return "HILL_ERR_WORKSPACE";
+    case HILL_ERR_HIP: return "HILL_ERR_HIP";
+    default: return "HILL_ERR_UNKNOWN";
+    }
+}
+
+const char* hill_last_error(void) { return g_last_error.c_str(); }
+
+hill_status hill_workspace_bytes(const hill_desc* d, int32_t k_sel, size_t* bytes)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s, false));
+    HILL_TRY(check_ksel(s, k_sel));
+    if (!bytes) return fail(HILL_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = layout_for(s, k_sel).end_all;
+    return HILL_OK;
+}
+
+hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* s_acc, void* ws, size_t ws_bytes,
+                       void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    const Layout L = layout_for(s, 1);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_score));
+    return run_score(d, s, L, q, k, s_acc, ws, false, static_cast<hipStream_t>(stream));
+}
+
+hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int32_t* idx_out, float* val_out,
+                      void* ws, size_t ws_bytes, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s));
+    HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
+    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
+    if (val_out && ((uintptr_t)val_out & 3u)) return fail(HILL_ERR_INVALID_ARG, "val_out is not 4-byte aligned");
+    const Layout L = layout_for(s, k_sel);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_topk));
+    return run_select(d, s, L, s_acc, k_sel, idx_out, val_out, ws, false, static_cast<hipStream_t>(stream));
+}
+
+hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v, const int32_t* idx,
+                             int32_t k_sel, float* out, void* ws, size_t ws_bytes, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s, false));
+    HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_ptr(v, "v"));
+    HILL_TRY(check_ptr(out, "out"));
+    if (!idx) return fail(HILL_ERR_INVALID_ARG, "idx is NULL");
+    if ((uintptr_t)idx & 3u) return fail(HILL_ERR_INVALID_ARG, "idx is not 4-byte aligned");
+    const Layout L = layout_for(s, k_sel);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
+    return run_attn(d, s, L, q, k, v, idx, k_sel, out, ws, static_cast<hipStream_t>(stream));
+}
+
+hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc, int32_t k_sel,
+                      int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s));
+    HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_ptr(v, "v"));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    HILL_TRY(check_ptr(out, "out"));
+    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
+    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
+    const Layout L = layout_for(s, k_sel);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    HILL_TRY(run_score(d, s, L, q, k, s_acc, ws, true, st));
+    HILL_TRY(run_select(d, s, L, s_acc, k_sel, idx_out, nullptr, ws, true, st));
+    return run_attn(d, s, L, q, k, v, idx_out, k_sel, out, ws, st);
+}
+
+}  // extern "C"

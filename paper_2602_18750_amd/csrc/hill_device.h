@@ -1,0 +1,147 @@
+// Device helpers for the gfx950 kernels: 16-bit dot products, 16-lane DPP
+// reductions, wave reductions/scans and the order-preserving key map used
+// by the selection.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hill {
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf162_t __attribute__((ext_vector_type(2)));
+
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte load that bypasses cache retention (streamed once per step).
+__device__ __forceinline__ uint4 load_stream16(const void* p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+// fp32 += a.lo*b.lo + a.hi*b.hi over packed 16-bit pairs (v_dot2c_f32_{f16,bf16}).
+template <int DT>
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c);
+
+template <>
+__device__ __forceinline__ float dot2<0>(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, a), __builtin_bit_cast(half2_t, b), c, false);
+}
+
+template <>
+__device__ __forceinline__ float dot2<1>(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf162_t, a), __builtin_bit_cast(bf162_t, b),
+                                           c, false);
+}
+
+// Dot product of 8 packed 16-bit elements (one 16-byte load each side).
+template <int DT>
+__device__ __forceinline__ float dot8(const uint4& k, const uint4& q)
+{
+    float acc = dot2<DT>(k.x, q.x, 0.0f);
+    acc = dot2<DT>(k.y, q.y, acc);
+    acc = dot2<DT>(k.z, q.z, acc);
+    acc = dot2<DT>(k.w, q.w, acc);
+    return acc;
+}
+
+// Widen a packed pair to two floats.
+template <int DT>
+__device__ __forceinline__ void widen2(uint32_t x, float& lo, float& hi);
+
+template <>
+__device__ __forceinline__ void widen2<0>(uint32_t x, float& lo, float& hi)
+{
+    half2_t h = __builtin_bit_cast(half2_t, x);
+    lo = (float)h[0];
+    hi = (float)h[1];
+}
+
+template <>
+__device__ __forceinline__ void widen2<1>(uint32_t x, float& lo, float& hi)
+{
+    lo = __uint_as_float(x << 16);
+    hi = __uint_as_float(x & 0xffff0000u);
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF,
+                                                                  false));
+}
+
+// Sum over each aligned group of 16 lanes; every lane of the group gets the sum.
+// quad_perm[1,0,3,2], quad_perm[2,3,0,1], row_half_mirror, row_mirror.
+__device__ __forceinline__ float sum16(float v)
+{
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0x141>(v);
+    v += dpp<0x140>(v);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum(float v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        uint32_t t = __shfl_up(v, o, 64);
+        if (lane >= o) v += t;
+    }
+    return v;
+}
+
+// Exclusive prefix sum over a block of NT threads (NT a multiple of 64, <= 1024).
+// `scratch` holds at least NT/64 + 1 words of LDS.  Returns the block total in *total.
+template <int NT>
+__device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratch, uint32_t* total)
+{
+    constexpr int NW = NT / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    uint32_t inc = wave_incl_scan(v);
+    if (lane == 63) scratch[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        uint32_t x = lane < NW ? scratch[lane] : 0u;
+        uint32_t xi = wave_incl_scan(x);
+        if (lane < NW) scratch[lane] = xi - x;
+        if (lane == NW - 1) scratch[NW] = xi;
+    }
+    __syncthreads();
+    uint32_t r = scratch[w] + inc - v;
+    *total = scratch[NW];
+    __syncthreads();
+    return r;
+}
+
+// Order-preserving map of fp32 to uint32: larger float -> larger key.
+// -0.0 is folded onto +0.0; every NaN maps to 0, below -inf.
+__device__ __forceinline__ uint32_t order_key(float f)
+{
+    if (f != f) return 0u;
+    uint32_t u = __float_as_uint(f);
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+}  // namespace hill

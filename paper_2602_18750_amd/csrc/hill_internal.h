@@ -1,0 +1,98 @@
+// Internal interface between the C-ABI host layer (hill_api.cpp) and the
+// kernel translation units.  Not installed; not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hill {
+
+constexpr int kHeadDim = 128;      // D supported by every kernel
+constexpr int kScoreTile = 128;    // tokens per scoring tile (one K1 work item)
+constexpr int kHistBits = 12;      // first radix digit of the selection keys
+constexpr int kHistBins = 1 << kHistBits;
+constexpr int kUpdChunk = 512;     // tokens per importance-update workgroup
+constexpr int kHistChunk = 2048;   // tokens per standalone histogram workgroup
+
+enum ScoreOut : int {
+    kOutLogits = 0,    // ATTN: logits [B,Hq,n] + per-tile softmax partials
+    kOutRawS = 1,      // RAW, one row per KV head: add head-group sums into S
+    kOutRawGroups = 2  // RAW, token rows with Hkv > 1: head-group sums [B,Hkv,n]
+};
+
+struct ScoreArgs {
+    const uint16_t* q;
+    const uint16_t* k;
+    int64_t q_sb, q_sh;
+    int64_t k_sb, k_sh, k_sn;
+    int B, Hq, Hkv, G, n, ntiles;
+    float s2;                // sm_scale * log2(e): logits are kept in the exp2 domain
+    float* logits;           // kOutLogits / kOutRawGroups destination
+    float2* part;            // kOutLogits: [B,Hq,ntiles] (max, sum exp2) per tile
+    float* s;                // kOutRawS: importance rows
+    int64_t s_sb, s_sr;
+    uint32_t* zero_ptr;      // nullable: words to clear for a later kernel
+    int64_t zero_words;
+};
+
+struct UpdateArgs {
+    const float* logits;     // ATTN: [B,Hq,n]; RAW: group sums [B,Hkv,n]
+    const float2* stats;     // ATTN: [B,Hq] (max, 1/sum) in the exp2 domain
+    float* s;
+    int64_t s_sb, s_sr;
+    int B, Hq, Hkv, G, R, n;
+    float s2;
+    uint32_t* hist;          // nullable: [B*R, kHistBins] first-digit counts
+};
+
+struct SelectArgs {
+    const float* s;
+    int64_t s_sb, s_sr;
+    int R, n, k;
+    const uint32_t* hist;    // [rows, kHistBins] first-digit counts
+    int32_t* idx;            // [rows, k]
+    float* val;              // nullable [rows, k]
+};
+
+struct AttnArgs {
+    const uint16_t* q;
+    const uint16_t* k;
+    const uint16_t* v;
+    int64_t q_sb, q_sh;
+    int64_t k_sb, k_sh, k_sn;
+    int64_t v_sb, v_sh, v_sn;
+    const int32_t* idx;      // [B, R, ksel]
+    int B, Hq, Hkv, G, R, n, ksel, nsplit, per_split;
+    float s2;
+    float* part_o;           // [B,Hq,nsplit,D]
+    float2* part_ml;         // [B,Hq,nsplit] (max, sum) in the exp2 domain
+    float* out;              // [B,Hq,D]
+};
+
+// Splits of the selected set per (sequence, KV head) for the attention pass.
+// A pure function of the shape so that workspace sizing needs no device query.
+inline int attn_splits(int64_t b_hkv, int ksel, int* per_split)
+{
+    const int64_t target_wgs = 1024;
+    const int min_tokens = 32;
+    int64_t s = (target_wgs + b_hkv - 1) / b_hkv;
+    int64_t cap = (ksel + min_tokens - 1) / min_tokens;
+    if (s > cap) s = cap;
+    if (s < 1) s = 1;
+    int p = (int)((ksel + s - 1) / s);
+    *per_split = p;
+    return (ksel + p - 1) / p;   // every split non-empty
+}
+
+hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
+hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int grid_cap, hipStream_t st);
+hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int ntiles, hipStream_t st);
+hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st);
+hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st);
+hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n,
+                            uint32_t* hist, hipStream_t st);
+hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st);
+hipError_t launch_attn_split(const AttnArgs& a, int dtype, hipStream_t st);
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st);
+
+}  // namespace hill

@@ -1,0 +1,283 @@
+"""Python binding of libhill (ctypes).  Argument marshalling only: every step
+of the path runs in the library's HIP kernels; torch supplies device memory
+and the current stream.
+
+The functions mirror the C-ABI entry points of ``include/hill.h``:
+
+    hill_score(q, k, s, ...)                    S += column sums of this step's weights
+    hill_topk(s, k_sel, ...)         -> idx[, val]
+    hill_gather_attn(q, k, v, idx, ...) -> out
+    hill_step(q, k, v, s, k_sel, ...)  -> (idx, out)
+
+Shapes: q [B, Hq, D]; k, v [B, Hkv, Ncap, D] (any strides with D contiguous);
+s [B, R, >= n] fp32 with R = 1 (granularity "token") or Hkv ("kvhead");
+idx [B, R, k_sel] int32; out [B, Hq, D] fp32.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+from typing import Optional, Tuple
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhill.so")
+
+HILL_OK = 0
+STATUS = {0: "HILL_OK", 1: "HILL_ERR_INVALID_ARG", 2: "HILL_ERR_UNSUPPORTED", 3: "HILL_ERR_WORKSPACE",
+          4: "HILL_ERR_HIP"}
+DTYPES = {torch.float16: 0, torch.bfloat16: 1}
+MODES = {"attn": 0, "raw": 1}
+GRANS = {"token": 0, "kvhead": 1}
+
+EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
+           "hill_topk", "hill_gather_attn", "hill_step")
+
+
+class HillError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("%s: %s" % (STATUS.get(status, status), msg))
+        self.status = status
+
+
+class HillDesc(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", ctypes.c_uint32),
+        ("batch", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("n_tokens", ctypes.c_int32),
+        ("dtype", ctypes.c_int32),
+        ("score_mode", ctypes.c_int32),
+        ("granularity", ctypes.c_int32),
+        ("sm_scale", ctypes.c_float),
+        ("q_stride_b", ctypes.c_int64),
+        ("q_stride_h", ctypes.c_int64),
+        ("k_stride_b", ctypes.c_int64),
+        ("k_stride_h", ctypes.c_int64),
+        ("k_stride_n", ctypes.c_int64),
+        ("v_stride_b", ctypes.c_int64),
+        ("v_stride_h", ctypes.c_int64),
+        ("v_stride_n", ctypes.c_int64),
+        ("s_stride_b", ctypes.c_int64),
+        ("s_stride_r", ctypes.c_int64),
+    ]
+
+
+_lock = threading.Lock()
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libhill.so (built in-tree by ``__graft_entry__.build()``).  Raises if absent:
+    there is no fallback implementation."""
+    global _lib
+    with _lock:
+        if _lib is not None:
+            return _lib
+        if not os.path.exists(path):
+            raise RuntimeError("libhill.so is not built (%s); run __graft_entry__.build()" % path)
+        lib = ctypes.CDLL(path)
+        P, I32, SZ = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        D = ctypes.POINTER(HillDesc)
+        lib.hill_abi_version.argtypes = []
+        lib.hill_abi_version.restype = ctypes.c_int
+        lib.hill_status_str.argtypes = [ctypes.c_int]
+        lib.hill_status_str.restype = ctypes.c_char_p
+        lib.hill_last_error.argtypes = []
+        lib.hill_last_error.restype = ctypes.c_char_p
+        lib.hill_workspace_bytes.argtypes = [D, I32, ctypes.POINTER(SZ)]
+        lib.hill_workspace_bytes.restype = ctypes.c_int
+        lib.hill_score.argtypes = [D, P, P, P, P, SZ, P]
+        lib.hill_score.restype = ctypes.c_int
+        lib.hill_topk.argtypes = [D, P, I32, P, P, P, SZ, P]
+        lib.hill_topk.restype = ctypes.c_int
+        lib.hill_gather_attn.argtypes = [D, P, P, P, P, I32, P, P, SZ, P]
+        lib.hill_gather_attn.restype = ctypes.c_int
+        lib.hill_step.argtypes = [D, P, P, P, P, I32, P, P, P, SZ, P]
+        lib.hill_step.restype = ctypes.c_int
+        _lib = lib
+        return lib
+
+
+def _check(status: int):
+    if status != HILL_OK:
+        raise HillError(status, _lib.hill_last_error().decode())
+
+
+def budget_k(n: int, budget: float) -> int:
+    """Token budget: floor(budget * n), at least 1 and at most n."""
+    return max(1, min(n, int(math.floor(budget * n + 1e-9))))
+
+
+def make_desc(q: Optional[torch.Tensor], k: Optional[torch.Tensor], v: Optional[torch.Tensor],
+              s: Optional[torch.Tensor], *, mode: str = "attn", granularity: str = "token",
+              n_tokens: Optional[int] = None, sm_scale: float = 0.0,
+              shape: Optional[Tuple[int, int, int, int]] = None, dtype=None) -> HillDesc:
+    """Descriptor from tensors.  ``shape`` = (B, Hq, Hkv, D) stands in when q/k are absent."""
+    d = HillDesc()
+    d.struct_size = ctypes.sizeof(HillDesc)
+    if q is not None:
+        B, Hq, D = q.shape
+    else:
+        B, Hq, _, D = shape
+    if k is not None:
+        _, Hkv, ncap, _ = k.shape
+    else:
+        Hkv = shape[2]
+        ncap = s.shape[-1]
+    n = ncap if n_tokens is None else int(n_tokens)
+    d.batch, d.n_q_heads, d.n_kv_heads, d.head_dim, d.n_tokens = B, Hq, Hkv, D, n
+    tdt = dtype if dtype is not None else (q.dtype if q is not None else k.dtype)
+    d.dtype = DTYPES.get(tdt, -1)
+    d.score_mode = MODES[mode]
+    d.granularity = GRANS[granularity]
+    d.sm_scale = float(sm_scale)
+    if q is not None:
+        d.q_stride_b, d.q_stride_h = q.stride(0), q.stride(1)
+        _require_unit_last(q, "q")
+    else:
+        d.q_stride_b, d.q_stride_h = Hq * D, D
+    if k is not None:
+        d.k_stride_b, d.k_stride_h, d.k_stride_n = k.stride(0), k.stride(1), k.stride(2)
+        _require_unit_last(k, "k")
+    else:
+        d.k_stride_b, d.k_stride_h, d.k_stride_n = Hkv * n * D, n * D, D
+    if v is not None:
+        d.v_stride_b, d.v_stride_h, d.v_stride_n = v.stride(0), v.stride(1), v.stride(2)
+        _require_unit_last(v, "v")
+    else:
+        d.v_stride_b, d.v_stride_h, d.v_stride_n = d.k_stride_b, d.k_stride_h, d.k_stride_n
+    if s is not None:
+        d.s_stride_b, d.s_stride_r = s.stride(0), s.stride(1)
+        if s.stride(2) != 1:
+            raise ValueError("s must have a contiguous token axis")
+    return d
+
+
+def _require_unit_last(t: torch.Tensor, name: str):
+    if t.stride(-1) != 1:
+        raise ValueError("%s must have a contiguous last (head_dim) axis" % name)
+
+
+def workspace_bytes(desc: HillDesc, k_sel: int) -> int:
+    lib = load_library()
+    out = ctypes.c_size_t(0)
+    _check(lib.hill_workspace_bytes(ctypes.byref(desc), int(k_sel), ctypes.byref(out)))
+    return int(out.value)
+
+
+_ws_cache = {}
+
+
+def workspace(desc: HillDesc, k_sel: int, device) -> torch.Tensor:
+    """A cached per-device workspace, grown on demand.  Calls that share it must be
+    ordered on one stream; pass ``ws=`` explicitly otherwise."""
+    need = max(workspace_bytes(desc, k_sel), 256)
+    dev = torch.device(device)
+    buf = _ws_cache.get(dev)
+    if buf is None or buf.numel() < need:
+        buf = torch.empty(need, dtype=torch.uint8, device=dev)
+        _ws_cache[dev] = buf
+    return buf
+
+
+def _stream_ptr(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _device_check(*ts):
+    for t in ts:
+        if t is not None and t.device.type != "cuda":
+            raise ValueError("libhill works on GPU tensors only (got %s)" % t.device)
+
+
+def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0, ws=None,
+               stream=None):
+    """S += column-wise sum over this step's weights (in place)."""
+    lib = load_library()
+    _device_check(q, k, s)
+    desc = make_desc(q, k, None, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
+    if ws is None:
+        ws = workspace(desc, 1, q.device)
+    _check(lib.hill_score(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(s), _ptr(ws), ws.numel(),
+                          _stream_ptr(stream)))
+    return s
+
+
+def hill_topk(s, k_sel, *, granularity="token", n_tokens=None, n_kv_heads=None, with_values=False,
+              idx_out=None, val_out=None, ws=None, stream=None):
+    """Indices [B, R, k_sel] (int32, ascending) of the k_sel largest S per row."""
+    lib = load_library()
+    _device_check(s)
+    B, R, _ = s.shape
+    hkv = n_kv_heads if n_kv_heads is not None else R
+    desc = make_desc(None, None, None, s, granularity=granularity, n_tokens=n_tokens,
+                     shape=(B, hkv, hkv, 128), dtype=torch.float16)
+    if idx_out is None:
+        idx_out = torch.empty((B, R, k_sel), dtype=torch.int32, device=s.device)
+    if with_values and val_out is None:
+        val_out = torch.empty((B, R, k_sel), dtype=torch.float32, device=s.device)
+    if ws is None:
+        ws = workspace(desc, k_sel, s.device)
+    _check(lib.hill_topk(ctypes.byref(desc), _ptr(s), int(k_sel), _ptr(idx_out), _ptr(val_out), _ptr(ws),
+                         ws.numel(), _stream_ptr(stream)))
+    return (idx_out, val_out) if with_values else idx_out
+
+
+def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_scale=0.0, out=None, ws=None,
+                     stream=None):
+    """Attention over the selected tokens; out [B, Hq, D] fp32."""
+    lib = load_library()
+    _device_check(q, k, v, idx)
+    k_sel = idx.shape[-1]
+    desc = make_desc(q, k, v, None, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
+    if not idx.is_contiguous() or idx.dtype != torch.int32:
+        raise ValueError("idx must be a contiguous int32 tensor")
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(desc, k_sel, q.device)
+    _check(lib.hill_gather_attn(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(idx), int(k_sel),
+                                _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
+    return out
+
+
+def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
+              sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None):
+    """One decode step: S update, top-k on the new S, attention.  Returns (idx, out)."""
+    lib = load_library()
+    _device_check(q, k, v, s)
+    desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
+    if k_sel is None:
+        if budget is None:
+            raise ValueError("give k_sel or budget")
+        k_sel = budget_k(desc.n_tokens, budget)
+    B, R = s.shape[0], s.shape[1]
+    if idx_out is None:
+        idx_out = torch.empty((B, R, k_sel), dtype=torch.int32, device=s.device)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(desc, k_sel, q.device)
+    _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
+                         _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
+    return idx_out, out
+
+
+def new_importance(B: int, R: int, n_cap: int, device) -> torch.Tensor:
+    """Zeroed fp32 importance buffer [B, R, n_cap] whose row stride is a multiple of 4."""
+    pad = (n_cap + 3) // 4 * 4
+    return torch.zeros((B, R, pad), dtype=torch.float32, device=device)[:, :, :n_cap]

@@ -1,0 +1,179 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/hill.h declares, and every argument error is reported by its status
+code before anything is enqueued.
+
+No call here is valid as a whole, so no kernel is ever launched: each case
+breaks exactly one rule, and the pointers are fake (never dereferenced,
+because validation fails first)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hill.h")
+
+
+@pytest.fixture(scope="module")
+def H():
+    import paper_2602_18750_amd as H
+    if not os.path.exists(H.hill.LIB_PATH):
+        from paper_2602_18750_amd import _build
+        _build.build()
+    H.load_library()
+    return H
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hill_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    fns = declared_functions()
+    for f in ("hill_score", "hill_topk", "hill_gather_attn", "hill_step", "hill_workspace_bytes",
+              "hill_status_str", "hill_abi_version", "hill_last_error"):
+        assert f in fns
+
+
+def test_library_exports_every_declared_symbol(H):
+    lib = H.load_library()
+    for f in declared_functions():
+        assert hasattr(lib, f), f
+    assert sorted(H.hill.EXPORTS) == declared_functions()
+
+
+def test_abi_version_and_status_strings(H):
+    lib = H.load_library()
+    assert lib.hill_abi_version() == 1
+    assert lib.hill_status_str(0) == b"HILL_OK"
+    assert lib.hill_status_str(3) == b"HILL_ERR_WORKSPACE"
+    assert lib.hill_status_str(99) == b"HILL_ERR_UNKNOWN"
+
+
+def test_desc_layout_matches_header(H):
+    # 10 x 4-byte fields, then 10 x int64 strides
+    assert ctypes.sizeof(H.HillDesc) == 40 + 80
+    assert H.HillDesc.q_stride_b.offset == 40
+
+
+FAKE = 0x10000          # 16-byte aligned, never dereferenced
+
+
+def base_desc(H, B=2, Hq=8, Hkv=2, D=128, n=1000, mode=0, gran=0, dtype=1):
+    d = H.HillDesc()
+    d.struct_size = ctypes.sizeof(d)
+    d.batch, d.n_q_heads, d.n_kv_heads, d.head_dim, d.n_tokens = B, Hq, Hkv, D, n
+    d.dtype, d.score_mode, d.granularity, d.sm_scale = dtype, mode, gran, 0.0
+    d.q_stride_b, d.q_stride_h = Hq * D, D
+    d.k_stride_b, d.k_stride_h, d.k_stride_n = Hkv * n * D, n * D, D
+    d.v_stride_b, d.v_stride_h, d.v_stride_n = Hkv * n * D, n * D, D
+    R = 1 if gran == 0 else Hkv
+    sr = (n + 3) // 4 * 4
+    d.s_stride_r, d.s_stride_b = sr, R * sr
+    return d
+
+
+def ws_need(H, d, k):
+    lib = H.load_library()
+    out = ctypes.c_size_t()
+    assert lib.hill_workspace_bytes(ctypes.byref(d), k, ctypes.byref(out)) == 0
+    return out.value
+
+
+def call_step(H, d, k=10, q=FAKE, kp=FAKE, v=FAKE, s=FAKE, idx=FAKE, out=FAKE, ws=FAKE, ws_bytes=None):
+    lib = H.load_library()
+    if ws_bytes is None:
+        ws_bytes = ws_need(H, d, k)
+    return lib.hill_step(ctypes.byref(d), q, kp, v, s, k, idx, out, ws, ws_bytes, None)
+
+
+INVALID, UNSUPPORTED, WORKSPACE = 1, 2, 3
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("struct_size", 12, INVALID),
+    ("batch", 0, INVALID),
+    ("n_q_heads", 7, INVALID),          # not a multiple of n_kv_heads=2
+    ("n_kv_heads", 0, INVALID),
+    ("n_tokens", 0, INVALID),
+    ("head_dim", 64, UNSUPPORTED),
+    ("dtype", 2, UNSUPPORTED),
+    ("score_mode", 5, INVALID),
+    ("granularity", -1, INVALID),
+    ("k_stride_n", 100, INVALID),       # not a multiple of 8
+    ("v_stride_n", 64, INVALID),        # < head_dim
+    ("q_stride_h", 4, INVALID),
+    ("s_stride_r", 999, INVALID),       # < n_tokens
+    ("s_stride_r", 1002, INVALID),      # not a multiple of 4
+    ("s_stride_b", 1001, INVALID),      # not a multiple of 4
+])
+def test_descriptor_errors(H, field, value, code):
+    d = base_desc(H)
+    setattr(d, field, value)
+    lib = H.load_library()
+    st = call_step(H, d, ws_bytes=1 << 40)
+    assert st == code, (field, lib.hill_last_error())
+    assert lib.hill_last_error() != b""
+
+
+def test_overlapping_importance_rows(H):
+    d = base_desc(H, gran=1)            # R = 2 rows per sequence
+    d.s_stride_b = d.s_stride_r         # second row of b would alias b+1
+    assert call_step(H, d, ws_bytes=1 << 40) == INVALID
+
+
+def test_sm_scale_must_be_finite(H):
+    d = base_desc(H)
+    d.sm_scale = float("nan")
+    assert call_step(H, d, ws_bytes=1 << 40) == INVALID
+
+
+@pytest.mark.parametrize("ksel", [0, -3, 1001])
+def test_budget_out_of_range(H, ksel):
+    d = base_desc(H)
+    assert call_step(H, d, k=ksel, ws_bytes=1 << 40) == INVALID
+
+
+@pytest.mark.parametrize("which", ["q", "kp", "v", "s", "idx", "out", "ws"])
+def test_null_pointers(H, which):
+    d = base_desc(H)
+    assert call_step(H, d, **{which: None}) == INVALID
+
+
+@pytest.mark.parametrize("which", ["q", "kp", "v", "s", "out", "ws"])
+def test_misaligned_pointers(H, which):
+    d = base_desc(H)
+    assert call_step(H, d, **{which: FAKE + 8}) == INVALID
+
+
+def test_workspace_too_small(H):
+    d = base_desc(H)
+    need = ws_need(H, d, 10)
+    assert call_step(H, d, ws_bytes=need - 1) == WORKSPACE
+
+
+def test_entry_points_validate_independently(H):
+    lib = H.load_library()
+    d = base_desc(H)
+    need = ws_need(H, d, 10)
+    assert lib.hill_score(ctypes.byref(d), FAKE, None, FAKE, FAKE, need, None) == INVALID
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 0, FAKE, None, FAKE, need, None) == INVALID
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 5, FAKE + 2, None, FAKE, need, None) == INVALID
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 5, FAKE, None, FAKE, 16, None) == WORKSPACE
+    assert lib.hill_gather_attn(ctypes.byref(d), FAKE, FAKE, FAKE, None, 5, FAKE, FAKE, need, None) == INVALID
+    assert lib.hill_gather_attn(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 5, FAKE + 4, FAKE, need, None) == INVALID
+    assert lib.hill_workspace_bytes(None, 1, None) == INVALID
+
+
+def test_workspace_sizes_are_pure_functions_of_shape(H):
+    # 32K-token Llama-3-8B-shaped layer: logits dominate (32 heads x 32768 x 4 B)
+    d = base_desc(H, B=1, Hq=32, Hkv=8, n=32768)
+    a = ws_need(H, d, 3276)
+    assert a == ws_need(H, d, 3276)
+    assert a >= 32 * 32768 * 4
+    # RAW with one row per KV head needs no logits buffer
+    d_raw = base_desc(H, B=1, Hq=32, Hkv=8, n=32768, mode=1, gran=1)
+    assert ws_need(H, d_raw, 3276) < a

@@ -1,0 +1,371 @@
+"""GPU parity: libhill (through its C ABI) against the CPU oracle on seeded
+synthetic inputs.  Runs only on an MI355X with the library built."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2602_18750_amd import workloads as W
+from parity import check_outputs, check_scores, check_selection
+from util import bits, dname
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_18750_amd as H
+    H.load_library()
+    yield
+
+
+def H():
+    import paper_2602_18750_amd as H
+    return H
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def gpu_inputs(x):
+    return x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+
+
+def R_of(gran, Hkv):
+    return 1 if gran == "token" else Hkv
+
+
+# ------------------------------------------------------------------ scoring --
+
+SCORE_CASES = [
+    # B, Hq, Hkv, n, dtype, mode, gran
+    (1, 32, 32, 4096, "fp16", "attn", "token"),
+    (2, 8, 2, 1000, "bf16", "attn", "kvhead"),
+    (1, 4, 4, 129, "fp16", "raw", "token"),
+    (2, 8, 2, 1, "bf16", "attn", "token"),
+    (1, 32, 1, 777, "bf16", "raw", "token"),
+    (3, 6, 2, 300, "fp16", "attn", "kvhead"),
+    (1, 16, 2, 5000, "bf16", "raw", "kvhead"),
+    (1, 32, 8, 2049, "bf16", "attn", "token"),
+    (2, 32, 8, 3000, "bf16", "raw", "token"),
+    (1, 64, 2, 640, "fp16", "attn", "token"),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,dt,mode,gran", SCORE_CASES)
+def test_score_matches_oracle_over_steps(B, Hq, Hkv, n, dt, mode, gran):
+    say("score case", B, Hq, Hkv, n, dt, mode, gran)
+    T = 3
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=T, seed=n + 7 * Hq)
+    q, k, v = gpu_inputs(x)
+    R = R_of(gran, Hkv)
+    s = H().new_importance(B, R, n, DEV)
+    s_ref = np.zeros((B, R, n))
+    for t in range(T):
+        H().hill_score(q[t], k, s, mode=mode, granularity=gran)
+        l = O.logits(bits(x.q[t]), bits(x.k), dt)
+        s_ref = O.update(l, s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        torch.cuda.synchronize()
+        check_scores(s.cpu().numpy(), s_ref, "step %d" % t)
+
+
+# -------------------------------------------------------------------- top-k --
+
+def _rows(kind, rows, n, seed):
+    g = np.random.default_rng(seed)
+    if kind == "normal":
+        return g.standard_normal((rows, n)).astype(np.float32)
+    if kind == "grid":          # heavy ties
+        return (g.integers(-6, 7, (rows, n)) / 4.0).astype(np.float32)
+    if kind == "equal":
+        return np.full((rows, n), 0.125, dtype=np.float32)
+    if kind == "signed":        # +-0, negatives, tiny and huge magnitudes
+        a = g.choice(np.array([0.0, -0.0, -1.0, 1e-30, -1e-30, 3e38, -3e38, 2.5], dtype=np.float32),
+                     size=(rows, n))
+        return a.astype(np.float32)
+    if kind == "nan":
+        a = g.standard_normal((rows, n)).astype(np.float32)
+        a[:, ::7] = np.nan
+        a[:, 3::11] = -np.inf
+        return a
+    if kind == "lognormal":     # the shape of summed attention weights
+        return np.exp(g.standard_normal((rows, n)) - 8).astype(np.float32)
+    raise ValueError(kind)
+
+
+TOPK_CASES = [
+    ("normal", 1, 1, 1), ("normal", 2, 3, 2), ("normal", 1, 100, 37), ("grid", 3, 4096, 819),
+    ("grid", 2, 4097, 4097), ("equal", 2, 5000, 17), ("signed", 2, 3000, 1500), ("nan", 2, 2000, 1999),
+    ("lognormal", 1, 32768, 3276), ("lognormal", 4, 131072, 6553), ("grid", 1, 65536, 13107),
+    ("normal", 8, 8192, 1), ("lognormal", 16, 9000, 450), ("nan", 1, 300, 300),
+]
+
+
+@pytest.mark.parametrize("kind,rows,n,k", TOPK_CASES)
+@pytest.mark.parametrize("values", [False, True])
+def test_topk_is_exact_on_identical_input(kind, rows, n, k, values):
+    say("topk case", kind, rows, n, k, values)
+    a = _rows(kind, rows, n, seed=n + rows)
+    s = H().new_importance(rows, 1, n, DEV)
+    s[:, 0, :] = torch.from_numpy(a).to(DEV)
+    res = H().hill_topk(s, k, granularity="token", with_values=values)
+    idx, val = res if values else (res, None)
+    torch.cuda.synchronize()
+    ref = O.topk(a.astype(np.float64), k)
+    assert np.array_equal(idx.cpu().numpy()[:, 0, :], ref)
+    if values:
+        got = val.cpu().numpy()[:, 0, :]
+        want = np.take_along_axis(a, ref, axis=1)
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+def test_topk_kvhead_rows():
+    B, Hkv, n, k = 3, 4, 1500, 200
+    a = _rows("grid", B * Hkv, n, seed=5).reshape(B, Hkv, n)
+    s = H().new_importance(B, Hkv, n, DEV)
+    s.copy_(torch.from_numpy(a))
+    idx = H().hill_topk(s, k, granularity="kvhead")
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), O.topk(a.astype(np.float64), k))
+
+
+# ---------------------------------------------------------------- attention --
+
+ATTN_CASES = [
+    # B, Hq, Hkv, n, k, dtype, gran
+    (1, 32, 32, 4096, 819, "fp16", "token"),
+    (2, 32, 8, 3000, 300, "bf16", "token"),
+    (2, 8, 2, 500, 1, "bf16", "kvhead"),
+    (1, 8, 8, 64, 64, "fp16", "token"),
+    (1, 32, 1, 1000, 77, "fp16", "token"),
+    (3, 6, 3, 333, 100, "bf16", "kvhead"),
+    (1, 16, 2, 7000, 5000, "bf16", "token"),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,k,dt,gran", ATTN_CASES)
+def test_gather_attn_matches_oracle(B, Hq, Hkv, n, k, dt, gran):
+    say("attn case", B, Hq, Hkv, n, k, dt, gran)
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, seed=k + n)
+    q, kk, v = gpu_inputs(x)
+    R = R_of(gran, Hkv)
+    g = np.random.default_rng(k)
+    idx = np.stack([np.stack([g.permutation(n)[:k] for _ in range(R)]) for _ in range(B)]).astype(np.int32)
+    out = H().hill_gather_attn(q[0], kk, v, torch.from_numpy(idx).to(DEV), granularity=gran)
+    torch.cuda.synchronize()
+    ref = O.sparse_attn(bits(x.q[0]), bits(x.k), bits(x.v), idx, dt, gran)
+    check_outputs(out.cpu().numpy(), ref, "attn")
+
+
+def test_single_token_attention_returns_value_rows():
+    B, Hq, Hkv, n = 2, 8, 2, 100
+    x = W.make_random(B, Hq, Hkv, 128, n, "bf16", seed=3)
+    q, k, v = gpu_inputs(x)
+    idx = torch.tensor([[[13]], [[99]]], dtype=torch.int32, device=DEV)
+    out = H().hill_gather_attn(q[0], k, v, idx)
+    torch.cuda.synchronize()
+    want = torch.stack([x.v[0, :, 13].float().repeat_interleave(4, 0), x.v[1, :, 99].float().repeat_interleave(4, 0)])
+    assert torch.equal(out.cpu(), want)
+
+
+# --------------------------------------------------------------- full steps --
+
+def run_steps(x, k_sel, mode, gran, steps, check_every=1, where=""):
+    """hill_step over `steps` queries vs the oracle; returns final GPU (S, idx, out)."""
+    B, Hkv, n = x.k.shape[0], x.k.shape[1], x.k.shape[2]
+    dt = dname(x.k)
+    q, k, v = gpu_inputs(x)
+    R = R_of(gran, Hkv)
+    s = H().new_importance(B, R, n, DEV)
+    s_ref = np.zeros((B, R, n))
+    for t in range(steps):
+        idx, out = H().hill_step(q[t], k, v, s, k_sel, mode=mode, granularity=gran)
+        s_ref, idx_ref, out_ref = O.step(bits(x.q[t]), bits(x.k), bits(x.v), s_ref, k_sel, dt, mode, gran)
+        if t % check_every == 0 or t == steps - 1:
+            torch.cuda.synchronize()
+            idx_g = idx.cpu().numpy()
+            check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t))
+            check_selection(idx_g, s_ref, k_sel, "%s step %d sel" % (where, t))
+            out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, gran)
+            check_outputs(out.cpu().numpy(), out_own, "%s step %d out" % (where, t))
+            if np.array_equal(idx_g, idx_ref):
+                check_outputs(out.cpu().numpy(), out_ref, "%s step %d out(direct)" % (where, t))
+    return s, idx, out
+
+
+@pytest.mark.parametrize("mode,gran", [("attn", "token"), ("attn", "kvhead"), ("raw", "token"),
+                                       ("raw", "kvhead")])
+def test_step_config1_full_size(mode, gran):
+    w = W.WORKLOADS[1]
+    say("config 1", mode, gran)
+    x = W.make_layer(w, 0)
+    run_steps(x, w.k_sel, mode, gran, 1, where="cfg1")
+
+
+def test_step_config2_layers_full_size():
+    w = W.WORKLOADS[2]
+    for layer in (0, 31):
+        say("config 2 layer", layer)
+        x = W.make_layer(w, layer)
+        s, idx, _ = run_steps(x, w.k_sel, "attn", "token", 1, where="cfg2 L%d" % layer)
+        idx = idx.cpu().numpy()
+        recall = np.mean([np.isin(x.heavy[b].numpy(), idx[b, 0]).mean() for b in range(w.batch)])
+        say("config 2 layer %d heavy-hitter recall %.3f" % (layer, recall))
+
+
+def test_step_config3_multistep_full_size():
+    w = W.WORKLOADS[3]
+    say("config 3 layer 0, 6 steps")
+    x = W.make_layer(w.replace(steps=6), 0)
+    run_steps(x, w.k_sel, "attn", "token", 6, where="cfg3")
+
+
+def test_step_config4_full_size():
+    w = W.WORKLOADS[4]
+    say("config 4, 2 steps")
+    x = W.make_layer(w.replace(steps=2), 0, device=DEV)
+    x = W.LayerInputs(q=x.q.cpu(), k=x.k.cpu(), v=x.v.cpu(), heavy=None)
+    run_steps(x, w.k_sel, "attn", "token", 2, where="cfg4")
+
+
+@pytest.mark.parametrize("cell", [0, 4, 8, 13, 26])
+def test_step_sweep_cells_sampled(cell):
+    """Sweep cells at full size; batch rows are independent, so the oracle checks two of them."""
+    w = W.sweep_workloads()[cell]
+    say("sweep", w.name)
+    x = W.make_layer(w, 0, device=DEV, seed=5000 + cell)
+    q, k, v = x.q, x.k, x.v
+    s = H().new_importance(w.batch, 1, w.n_tokens, DEV)
+    idx, out = H().hill_step(q[0], k, v, s, w.k_sel)
+    torch.cuda.synchronize()
+    for b in sorted({0, w.batch - 1}):
+        xb = W.LayerInputs(q=q[:, b:b + 1].cpu(), k=k[b:b + 1].cpu(), v=v[b:b + 1].cpu(), heavy=None)
+        s_ref, idx_ref, out_ref = O.step(bits(xb.q[0]), bits(xb.k), bits(xb.v), np.zeros((1, 1, w.n_tokens)),
+                                         w.k_sel, "bf16")
+        check_scores(s[b:b + 1].cpu().numpy(), s_ref, "sweep b%d" % b)
+        idx_b = idx[b:b + 1].cpu().numpy()
+        check_selection(idx_b, s_ref, w.k_sel, "sweep b%d" % b)
+        own = O.sparse_attn(bits(xb.q[0]), bits(xb.k), bits(xb.v), idx_b, "bf16", "token")
+        check_outputs(out[b:b + 1].cpu().numpy(), own, "sweep b%d" % b)
+
+
+# ---------------------------------------------------------- layout / state --
+
+def test_strided_cache_query_and_scores():
+    """K/V are views into a larger cache (Ncap > n), q a strided view, S padded rows."""
+    B, Hq, Hkv, n, ncap, kk = 2, 8, 2, 900, 1024, 90
+    x = W.make_random(B, Hq, Hkv, 128, n, "bf16", steps=2, seed=21)
+    kc = torch.zeros(B, Hkv, ncap, 128, dtype=torch.bfloat16, device=DEV)
+    vc = torch.zeros(B, Hkv, ncap, 128, dtype=torch.bfloat16, device=DEV)
+    kc[:, :, :n] = x.k.to(DEV)
+    vc[:, :, :n] = x.v.to(DEV)
+    qbig = torch.zeros(2, B, Hq, 256, dtype=torch.bfloat16, device=DEV)
+    qbig[:, :, :, 64:192] = x.q.to(DEV)
+    q = qbig[:, :, :, 64:192]
+    s = H().new_importance(B, 1, ncap + 12, DEV)
+    s_ref = np.zeros((B, 1, n))
+    for t in range(2):
+        idx, out = H().hill_step(q[t], kc, vc, s, kk, n_tokens=n)
+        s_ref, idx_ref, out_ref = O.step(bits(x.q[t]), bits(x.k), bits(x.v), s_ref, kk, "bf16")
+        torch.cuda.synchronize()
+        check_scores(s[:, :, :n].cpu().numpy(), s_ref, "strided S")
+        assert float(s[:, :, n:].abs().max()) == 0.0        # untouched beyond n
+        check_selection(idx.cpu().numpy(), s_ref, kk, "strided sel")
+        own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx.cpu().numpy(), "bf16", "token")
+        check_outputs(out.cpu().numpy(), own, "strided out")
+
+
+def test_append_one_token_per_step():
+    """The context grows by one token per step; new tokens enter with S = 0."""
+    B, Hq, Hkv, n0, T, kk = 1, 32, 8, 2000, 4, 200
+    x = W.make_random(B, Hq, Hkv, 128, n0 + T, "bf16", steps=T, seed=31)
+    q, k, v = gpu_inputs(x)
+    s = H().new_importance(B, 1, n0 + T, DEV)
+    s_ref = np.zeros((B, 1, n0 + T))
+    for t in range(T):
+        n = n0 + t + 1
+        idx, out = H().hill_step(q[t], k, v, s, kk, n_tokens=n)
+        sr, _, _ = O.step(bits(x.q[t]), bits(x.k[:, :, :n]), bits(x.v[:, :, :n]), s_ref[:, :, :n], kk, "bf16")
+        s_ref[:, :, :n] = sr
+        torch.cuda.synchronize()
+        check_scores(s[:, :, :n].cpu().numpy(), sr, "append S")
+        check_selection(idx.cpu().numpy(), sr, kk, "append sel")
+
+
+def test_step_is_deterministic_and_resumable():
+    w = W.WORKLOADS[3]
+    x = W.make_layer(w.replace(steps=4, n_tokens=8192), 0)
+    q, k, v = gpu_inputs(x)
+
+    def run(s, ts):
+        res = None
+        for t in ts:
+            res = H().hill_step(q[t], k, v, s, 819)
+        torch.cuda.synchronize()
+        return res
+
+    s1 = H().new_importance(1, 1, 8192, DEV)
+    i1, o1 = run(s1, range(4))
+    s2 = H().new_importance(1, 1, 8192, DEV)
+    run(s2, range(2))
+    saved = s2.cpu().clone()
+    s3 = H().new_importance(1, 1, 8192, DEV)
+    s3.copy_(saved)
+    i3, o3 = run(s3, range(2, 4))
+    assert torch.equal(s1.cpu(), s3.cpu())
+    assert torch.equal(i1.cpu(), i3.cpu())
+    assert torch.equal(o1.cpu(), o3.cpu())
+    s4 = H().new_importance(1, 1, 8192, DEV)
+    i4, o4 = run(s4, range(4))
+    assert torch.equal(s1.cpu(), s4.cpu()) and torch.equal(i1.cpu(), i4.cpu()) and torch.equal(o1.cpu(), o4.cpu())
+
+
+@pytest.mark.parametrize("mode,gran", [("attn", "token"), ("raw", "kvhead"), ("raw", "token")])
+def test_step_equals_score_topk_attn_in_sequence(mode, gran):
+    B, Hq, Hkv, n, kk = 2, 32, 8, 3000, 300
+    x = W.make_random(B, Hq, Hkv, 128, n, "bf16", seed=41)
+    q, k, v = gpu_inputs(x)
+    R = R_of(gran, Hkv)
+    s1 = H().new_importance(B, R, n, DEV)
+    i1, o1 = H().hill_step(q[0], k, v, s1, kk, mode=mode, granularity=gran)
+    s2 = H().new_importance(B, R, n, DEV)
+    H().hill_score(q[0], k, s2, mode=mode, granularity=gran)
+    i2 = H().hill_topk(s2, kk, granularity=gran, n_kv_heads=Hkv)
+    o2 = H().hill_gather_attn(q[0], k, v, i2, granularity=gran)
+    torch.cuda.synchronize()
+    assert torch.equal(s1.cpu(), s2.cpu())
+    assert torch.equal(i1.cpu(), i2.cpu())
+    assert torch.equal(o1.cpu(), o2.cpu())
+
+
+@pytest.mark.parametrize("gran", ["token", "kvhead"])
+def test_full_budget_equals_dense_attention(gran):
+    B, Hq, Hkv, n = 1, 32, 8, 1000
+    x = W.make_random(B, Hq, Hkv, 128, n, "fp16", seed=51)
+    q, k, v = gpu_inputs(x)
+    s = H().new_importance(B, R_of(gran, Hkv), n, DEV)
+    idx, out = H().hill_step(q[0], k, v, s, n, granularity=gran)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy()[0, 0], np.arange(n))
+    qd = x.q[0].double().unsqueeze(2)
+    kd = x.k.double().repeat_interleave(4, 1)
+    vd = x.v.double().repeat_interleave(4, 1)
+    dense = torch.nn.functional.scaled_dot_product_attention(qd, kd, vd).squeeze(2).numpy()
+    check_outputs(out.cpu().numpy(), dense, "dense")
+
+
+def test_errors_raise_and_enqueue_nothing():
+    x = W.make_random(1, 8, 2, 128, 100, "fp16", seed=1)
+    q, k, v = gpu_inputs(x)
+    s = H().new_importance(1, 1, 100, DEV)
+    with pytest.raises(H().HillError):
+        H().hill_step(q[0], k, v, s, 101)
+    torch.cuda.synchronize()
+    assert float(s.abs().max()) == 0.0
