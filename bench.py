@@ -1,0 +1,407 @@
+#!/usr/bin/env python3
+"""Benchmark of one decode step of HillInfer's token-importance path on one
+MI355X: for every layer, score all cached keys against the step's query and
+update the cumulative importance, select the top-k tokens, and attend over
+them (libhill ``hill_step``).
+
+Default workload: the Llama-3-8B-shaped 32K-context decode -- 32 layers, GQA
+32 query / 8 KV heads, head_dim 128, batch 1, 32768 cached bf16 tokens per
+layer, keys with LogNormal(0,1) per-channel outlier scales, budget 10%
+(3276 tokens), importance carried across the decode steps.  A "step" is one
+decode step through all 32 layers.  Inputs are synthetic (seeded), resident
+in HBM before timing starts; the 4 GiB of K+V exceed the 256 MB Infinity
+Cache, so every layer's keys come from HBM.
+
+Prints one JSON line:
+  value        GB/s of keys scanned by the whole step (all layers, scoring +
+               selection + attention): K bytes per step / step time
+  roofline     the key-scan kernel (score_tiles): algorithmic bytes per
+               launch / its mean duration, from start/stop timestamps that
+               the kernel's own dispatch stamps into HIP events
+               (hill_step_profiled, on the library's stream), vs 8 TB/s
+  scoring_*    the scoring stage (scan + normaliser + S update)
+  select_attn_us_per_layer_step   selection + gather attention, per layer-step
+  cpu_baseline the CPU oracle on a bounded sample of the same workload
+
+Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
+``--copy-calib`` (plain copy of known size, for counter calibration),
+``--summarize DIR`` (condense rocprofv3 output under DIR into text).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "scoring GB/s of K scanned (% HBM peak) + select+attn µs/layer-step at 32K ctx"
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "score_tiles_counters.json")
+SCORE_SRC = os.path.join(ROOT, "paper_2602_18750_amd", "csrc", "score.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------- HIP events --
+
+class HipEvents:
+    """hipEvent_t handles created through the HIP runtime (ctypes)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.made = []
+
+    def create(self):
+        e = ctypes.c_void_p()
+        rc = self.hip.hipEventCreate(ctypes.byref(e))
+        if rc != 0:
+            raise RuntimeError("hipEventCreate failed (%d)" % rc)
+        self.made.append(e)
+        return e
+
+    def ms(self, a, b) -> float:
+        out = ctypes.c_float()
+        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        if rc != 0:
+            raise RuntimeError("hipEventElapsedTime failed (%d)" % rc)
+        return float(out.value)
+
+    def close(self):
+        for e in self.made:
+            self.hip.hipEventDestroy(e)
+        self.made = []
+
+
+# ------------------------------------------------------------ byte counts --
+
+def scan_kernel_bytes(B, Hq, Hkv, D, n, mode="attn"):
+    """Algorithmic bytes of one score_tiles launch: every key read once, plus
+    (ATTN) the fp32 logits and per-32-token (max, sum) pairs written."""
+    kbytes = B * Hkv * n * D * 2
+    if mode != "attn":
+        return kbytes + B * n * 4 * 2
+    ntiles = (n + 31) // 32
+    return kbytes + B * Hq * n * 4 + B * Hq * ntiles * 8
+
+
+def load_traffic(per_launch_bytes_hint=None):
+    """HBM traffic of score_tiles from committed counter runs, only while the
+    kernel source is unchanged since the counters were taken."""
+    try:
+        rec = json.load(open(COUNTERS_FILE))
+        src = hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest()
+        if rec.get("source_sha256") != src:
+            return None
+        return rec.get("hbm_bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+# ------------------------------------------------------------- CPU oracle --
+
+def cpu_baseline(w, seconds: float):
+    """The oracle, as it stands, on a bounded sample: consecutive decode steps
+    of layer 0 of the same workload (full context), S carried."""
+    import numpy as np
+    import torch
+    from oracle import oracle as O
+    from paper_2602_18750_amd import workloads as W
+
+    x = W.make_layer(w.replace(steps=max(2, min(w.steps, 64))), 0)
+
+    def u16(t):
+        return t.contiguous().view(torch.int16).numpy().view(np.uint16)
+
+    kb, vb = u16(x.k), u16(x.v)
+    R = 1
+    S = np.zeros((w.batch, R, w.n_tokens))
+    done, t_total, phases = 0, 0.0, np.zeros(3)
+    while done < x.q.shape[0]:
+        t0 = time.perf_counter()
+        S, _, _, ph = O.step(u16(x.q[done]), kb, vb, S, w.k_sel, w.dtype, "attn", "token", return_times=True)
+        t_total += time.perf_counter() - t0
+        phases += ph
+        done += 1
+        if t_total >= seconds and done >= 2:
+            break
+    kbytes = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
+    per = t_total / done
+    return {
+        "value": round(kbytes / per / 1e9, 4),
+        "unit": "GB/s",
+        "cores": O.num_threads(),
+        "kind": "oracle",
+        "sample": "%d decode steps of layer 0 (B=%d, n=%d, GQA %d/%d, %s, k=%d), S carried; "
+                  "%.1f ms per layer-step (score %.1f, select %.1f, attention %.1f)" % (
+                      done, w.batch, w.n_tokens, w.n_q_heads, w.n_kv_heads, w.dtype, w.k_sel, per * 1e3,
+                      phases[0] / done * 1e3, phases[1] / done * 1e3, phases[2] / done * 1e3),
+    }
+
+
+# ------------------------------------------------------------- main bench --
+
+def run_bench(args):
+    import torch
+    import paper_2602_18750_amd as H
+    from paper_2602_18750_amd import workloads as W
+
+    w = W.WORKLOADS[int(args.workload)]
+    if args.layers:
+        w = w.replace(layers=args.layers)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    nl, T = w.layers, w.steps
+    log("bench: %s, %d layers, %d query steps, k=%d" % (w.name, nl, T, w.k_sel))
+
+    layers = []
+    for L in range(nl):
+        x = W.make_layer(w, L, device=dev)
+        s = H.new_importance(w.batch, 1, w.n_tokens, dev)
+        layers.append((x, s))
+    ws = H.workspace(H.make_desc(layers[0][0].q[0], layers[0][0].k, layers[0][0].v, layers[0][1]), w.k_sel, dev)
+    calls = [H.StepCall(x.q[0], x.k, x.v, s, w.k_sel, ws=ws, stream=stream) for (x, s) in layers]
+    qptrs = [[x.q[t].data_ptr() for t in range(T)] for (x, _) in layers]
+    torch.cuda.synchronize()
+
+    hip = HipEvents()
+    ev_sets = []
+    for _ in range(args.steps):
+        e = [hip.create() for _ in range(6)]
+        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+
+    for i in range(args.warmup):
+        for L in range(nl):
+            calls[L](qptrs[L][i % T])
+    torch.cuda.synchronize()
+
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        t = (args.warmup + i) % T
+        probe = i % nl            # one timestamped layer per step, rotating
+        for L in range(nl):
+            if L == probe:
+                calls[L](qptrs[L][t], ev_sets[i][1])
+            else:
+                calls[L](qptrs[L][t])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    # e: scan_start, scan_stop, score_stop, select_start, select_stop, attn_stop
+    scan, score, sel, selattn, total = [], [], [], [], []
+    for e, _ in ev_sets:
+        scan.append(hip.ms(e[0], e[1]))
+        score.append(hip.ms(e[0], e[2]))
+        sel.append(hip.ms(e[3], e[4]))
+        selattn.append(hip.ms(e[2], e[5]))
+        total.append(hip.ms(e[0], e[5]))
+    hip.close()
+
+    def mean(xs):
+        return sum(xs) / len(xs)
+
+    ms_step = (t1 - t0) * 1e3 / args.steps
+    kbytes_layer = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
+    value = kbytes_layer * nl / (ms_step * 1e-3) / 1e9
+    scan_bytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
+    scan_us = mean(scan) * 1e3
+    achieved = scan_bytes / (scan_us * 1e-6) / 1e9
+    score_us = mean(score) * 1e3
+    scoring_gbs = kbytes_layer / (score_us * 1e-6) / 1e9
+    traffic = load_traffic()
+
+    res = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+            "n_tokens": w.n_tokens, "budget": w.budget, "k_sel": w.k_sel, "layers": nl,
+            "query_steps": T, "score_mode": "attn", "granularity": "token", "parallelism": "none (1 GPU)",
+        },
+        "roofline": {
+            "kernel": "score_tiles",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": scan_bytes,
+            "mean_launch_us": round(scan_us, 3),
+        },
+        "scoring_gbps": round(scoring_gbs, 1),
+        "scoring_frac_hbm": round(scoring_gbs / HBM_PEAK_GBS, 4),
+        "scoring_us_per_layer_step": round(score_us, 3),
+        "select_kernel_us": round(mean(sel) * 1e3, 3),
+        "select_attn_us_per_layer_step": round(mean(selattn) * 1e3, 3),
+        "layer_step_us_probe": round(mean(total) * 1e3, 3),
+        "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle (%.0f s budget)" % args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(W.WORKLOADS[int(args.workload)], args.cpu_seconds)
+    else:
+        res["cpu_baseline"] = None
+    print(json.dumps(res), flush=True)
+
+
+# ------------------------------------------------------------------ sweep --
+
+def run_sweep(args):
+    """Throughput sweep: one decode step per cell, K rotated through enough
+    replicas to exceed 1 GiB so that the scan reads HBM, not the Infinity Cache."""
+    import torch
+    import paper_2602_18750_amd as H
+    from paper_2602_18750_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    hip = HipEvents()
+    for w in W.sweep_workloads():
+        kv_bytes = 2 * w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
+        reps = max(1, min(16, -(-(1 << 30) // kv_bytes)))
+        x = W.make_layer(w, 0, device=dev, seed=7000)
+        ks = [x.k] + [x.k.clone() for _ in range(reps - 1)]
+        vs = [x.v] + [x.v.clone() for _ in range(reps - 1)]
+        s = H.new_importance(w.batch, 1, w.n_tokens, dev)
+        ws = H.workspace(H.make_desc(x.q[0], x.k, x.v, s), w.k_sel, dev)
+        calls = [H.StepCall(x.q[0], ks[r], vs[r], s, w.k_sel, ws=ws, stream=stream) for r in range(reps)]
+        iters = max(20, reps)
+        evs = [[hip.create() for _ in range(6)] for _ in range(iters)]
+        for r in range(reps):
+            calls[r](x.q[0].data_ptr())
+        torch.cuda.synchronize()
+        for i in range(iters):
+            calls[i % reps](x.q[0].data_ptr(), H.HillStepEvents(*[e.value for e in evs[i]]))
+        torch.cuda.synchronize()
+        scan = sorted(hip.ms(e[0], e[1]) for e in evs)[iters // 2]
+        score = sorted(hip.ms(e[0], e[2]) for e in evs)[iters // 2]
+        selattn = sorted(hip.ms(e[2], e[5]) for e in evs)[iters // 2]
+        nbytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
+        kbytes = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
+        print(json.dumps({
+            "cell": w.name, "batch": w.batch, "n_tokens": w.n_tokens, "budget": w.budget, "k_sel": w.k_sel,
+            "scan_us": round(scan * 1e3, 2), "scan_gbps": round(nbytes / (scan * 1e-3) / 1e9, 1),
+            "scan_frac_hbm": round(nbytes / (scan * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "scoring_us": round(score * 1e3, 2),
+            "scoring_kgbps": round(kbytes / (score * 1e-3) / 1e9, 1),
+            "select_attn_us": round(selattn * 1e3, 2), "replicas": reps}), flush=True)
+        del calls, ks, vs, x, s
+        hip.close()
+        torch.cuda.empty_cache()
+
+
+def run_copy_calib(args):
+    """A plain device copy of known size (counter calibration: FETCH_SIZE and
+    WRITE_SIZE of this copy are compared with its 1 GiB read and write)."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda:0")
+    a.fill_(1)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "repeats": 3}), flush=True)
+
+
+# -------------------------------------------------------- profile summary --
+
+def _short(name: str) -> str:
+    name = name.replace("(anonymous namespace)::", "").replace("void ", "")
+    depth, out = 0, []
+    for ch in name:            # drop the argument list, keep template arguments
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out)[:80]
+
+
+def summarize(directory: str):
+    """Condense rocprofv3 --stats / --pmc CSV output found under `directory`."""
+    import csv
+    lines = []
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*kernel_stats.csv"), recursive=True)):
+        lines.append("## %s" % os.path.relpath(path, directory))
+        lines.append("| kernel | calls | mean us | total % |")
+        lines.append("|---|---|---|---|")
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                short = _short(r.get("Name", ""))
+                lines.append("| %s | %s | %.3f | %.2f |" % (short, r.get("Calls"), float(r.get("AverageNs", 0)) / 1e3,
+                                                          float(r.get("Percentage", 0))))
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
+        agg = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                name = _short(r.get("Kernel_Name", ""))
+                key = (name, r.get("Counter_Name"))
+                agg.setdefault(key, []).append(float(r.get("Counter_Value", 0)))
+        lines.append("## %s" % os.path.relpath(path, directory))
+        lines.append("| kernel | counter | dispatches | mean per dispatch |")
+        lines.append("|---|---|---|---|")
+        for (name, ctr), vals in sorted(agg.items()):
+            lines.append("| %s | %s | %d | %.1f |" % (name, ctr, len(vals), sum(vals) / len(vals)))
+    print("\n".join(lines))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=64)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="3", help="1..4 (default 3: the 32K-context Llama-3-8B-shaped decode)")
+    ap.add_argument("--layers", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--copy-calib", action="store_true")
+    ap.add_argument("--summarize", metavar="DIR")
+    args = ap.parse_args()
+
+    if args.summarize:
+        summarize(args.summarize)
+        return 0
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this path has no multi-GPU mode "
+              "(--gpus %d, WORLD_SIZE %d requested)" % (args.gpus, world), file=sys.stderr)
+        return 2
+    if args.copy_calib:
+        run_copy_calib(args)
+    elif args.sweep:
+        run_sweep(args)
+    else:
+        run_bench(args)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -148,6 +148,26 @@ hill_status hill_step(const hill_desc* d, const void* q, const void* k, const vo
                       float* s, int32_t k_sel, int32_t* idx_out, float* out,
                       void* ws, size_t ws_bytes, void* stream);
 
+/* Kernel timestamps for profiling hill_step.  Each non-NULL member is a
+ * caller-created hipEvent_t (hipEventCreate, timing enabled) that the named
+ * kernel boundary stamps: the kernels are launched with hipExtLaunchKernel's
+ * start/stop events, so no extra work is enqueued and elapsed times between
+ * members are GPU execution times. */
+typedef struct hill_step_events {
+    void* scan_start;    /* start of the kernel that streams the keys (q.K^T) */
+    void* scan_stop;     /* end of that kernel */
+    void* score_stop;    /* end of the last kernel that updates S */
+    void* select_start;  /* start of the selection kernel that writes the indices */
+    void* select_stop;   /* end of it */
+    void* attn_stop;     /* end of the last attention kernel (output written) */
+} hill_step_events;
+
+/* hill_step with kernel timestamps (ev may be NULL: then identical to hill_step).
+ * Same arguments, validation and results as hill_step. */
+hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k, const void* v,
+                               float* s, int32_t k_sel, int32_t* idx_out, float* out,
+                               void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
+
 #ifdef __cplusplus
 }
 #endif

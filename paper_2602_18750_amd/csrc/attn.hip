@@ -12,6 +12,8 @@
 //  attn_combine  merges the split partials of each query head.
 //
 // Softmax arithmetic runs in the exp2 domain (scale pre-multiplied by log2 e).
+#include <hip/hip_ext.h>
+
 #include "hill_device.h"
 #include "hill_internal.h"
 
@@ -57,22 +59,22 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a)
         }
 
         for (int tb = t0 + rg; tb < t1; tb += 16 * kTokBatch) {
+            // indices first (clamped into the split, so every load is in bounds),
+            // then every K and V row of the batch, then the arithmetic
+            int jj[kTokBatch];
+#pragma unroll
+            for (int u = 0; u < kTokBatch; ++u) jj[u] = I[min(tb + u * 16, t1 - 1)];
             uint4 kr[kTokBatch], vr[kTokBatch];
-            bool ok[kTokBatch];
 #pragma unroll
             for (int u = 0; u < kTokBatch; ++u) {
-                const int t = tb + u * 16;
-                ok[u] = t < t1;
-                if (ok[u]) {
-                    // clamped: an out-of-range index reads a valid row instead of faulting
-                    const int64_t j = min(max(I[t], 0), a.n - 1);
-                    kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
-                    vr[u] = *reinterpret_cast<const uint4*>(vb + j * a.v_sn);
-                }
+                // clamped: an out-of-range index reads a valid row instead of faulting
+                const int64_t j = min(max(jj[u], 0), a.n - 1);
+                kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
+                vr[u] = *reinterpret_cast<const uint4*>(vb + j * a.v_sn);
             }
 #pragma unroll
             for (int u = 0; u < kTokBatch; ++u) {
-                if (!ok[u]) continue;   // uniform within the 16-lane group
+                if (tb + u * 16 >= t1) break;   // uniform within the 16-lane group
                 float vf[8];
                 widen2<DT>(vr[u].x, vf[0], vf[1]);
                 widen2<DT>(vr[u].y, vf[2], vf[3]);
@@ -123,21 +125,50 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a)
     }
 }
 
-// out[b,h,:] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s, splits in order.
+// out[b,h,:] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s.  The split
+// weights are formed once in LDS; each thread then accumulates one output
+// dimension over the splits with several loads in flight.
 __global__ __launch_bounds__(kHeadDim) void attn_combine_kernel(AttnArgs a)
 {
+    __shared__ float wsplit[kMaxSplits];
+    __shared__ float red[kHeadDim / 64];
     const int bh = blockIdx.x;
     const int d = threadIdx.x;
+    const int lane = d & 63, w = d >> 6;
     const float2* ml = a.part_ml + (int64_t)bh * a.nsplit;
-    const float* po = a.part_o + (int64_t)bh * a.nsplit * kHeadDim + d;
     float mx = -INFINITY;
-    for (int s = 0; s < a.nsplit; ++s) mx = fmaxf(mx, ml[s].x);
-    float L = 0.0f, O = 0.0f;
-    for (int s = 0; s < a.nsplit; ++s) {
-        const float w = exp2f(ml[s].x - mx);
-        L += w * ml[s].y;
-        O += w * po[(int64_t)s * kHeadDim];
+    for (int s = d; s < a.nsplit; s += kHeadDim) mx = fmaxf(mx, ml[s].x);
+    mx = wave_max(mx);
+    if (lane == 0) red[w] = mx;
+    __syncthreads();
+    mx = red[0];
+#pragma unroll
+    for (int i = 1; i < kHeadDim / 64; ++i) mx = fmaxf(mx, red[i]);
+    __syncthreads();
+    float lsum = 0.0f;
+    for (int s = d; s < a.nsplit; s += kHeadDim) {
+        const float2 v = ml[s];
+        const float ws = exp2f(v.x - mx);
+        wsplit[s] = ws;
+        lsum += ws * v.y;
     }
+    lsum = wave_sum(lsum);
+    if (lane == 0) red[w] = lsum;
+    __syncthreads();
+    float L = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kHeadDim / 64; ++i) L += red[i];
+    const float* po = a.part_o + (int64_t)bh * a.nsplit * kHeadDim + d;
+    float O = 0.0f;
+    int s = 0;
+    for (; s + 8 <= a.nsplit; s += 8) {
+        float x[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[i] = po[(int64_t)(s + i) * kHeadDim];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) O += wsplit[s + i] * x[i];
+    }
+    for (; s < a.nsplit; ++s) O += wsplit[s] * po[(int64_t)s * kHeadDim];
     a.out[(int64_t)bh * kHeadDim + d] = O / L;
 }
 
@@ -163,9 +194,9 @@ hipError_t launch_attn_split(const AttnArgs& a, int dtype, hipStream_t st)
     return launch_attn_dt<0>(a, grid, st);
 }
 
-hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st)
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st, Stamp ts)
 {
-    hipLaunchKernelGGL(attn_combine_kernel, dim3(a.B * a.Hq), dim3(kHeadDim), 0, st, a);
+    hipExtLaunchKernelGGL(attn_combine_kernel, dim3(a.B * a.Hq), dim3(kHeadDim), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 

@@ -32,12 +32,13 @@ hill_status fail(hill_status st, const char* fmt, ...)
 // Shape facts derived from a validated descriptor.
 struct Shape {
     int B, Hq, Hkv, G, D, n, R, ntiles;
+    int64_t ld;
     int dtype, mode, gran;
     float scale;
 };
 
 // Workspace regions, in this order, each 256-byte aligned:
-//   logits  ATTN [B,Hq,n] fp32 | RAW token rows with Hkv > 1: [B,Hkv,n] fp32
+//   logits  ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
 //   part    ATTN [B,Hq,ntiles] float2
 //   stats   ATTN [B,Hq] float2
 //   hist    [B*R, 4096] u32
@@ -58,8 +59,8 @@ Layout layout_for(const Shape& s, int ksel)
     const bool attn = s.mode == HILL_SCORE_ATTN;
     const bool raw_groups = !attn && s.gran == HILL_SEL_TOKEN && s.Hkv > 1;
     L.logits = off;
-    if (attn) off += align256((size_t)s.B * s.Hq * s.n * sizeof(float));
-    else if (raw_groups) off += align256((size_t)s.B * s.Hkv * s.n * sizeof(float));
+    if (attn) off += align256((size_t)s.B * s.Hq * s.ld * sizeof(float));
+    else if (raw_groups) off += align256((size_t)s.B * s.Hkv * s.ld * sizeof(float));
     L.part = off;
     if (attn) off += align256((size_t)s.B * s.Hq * s.ntiles * sizeof(float2));
     L.stats = off;
@@ -123,6 +124,7 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     s->n = d->n_tokens;
     s->R = R;
     s->ntiles = (d->n_tokens + kScoreTile - 1) / kScoreTile;
+    s->ld = ((int64_t)d->n_tokens + 3) / 4 * 4;
     s->dtype = d->dtype;
     s->mode = d->score_mode;
     s->gran = d->granularity;
@@ -177,6 +179,11 @@ int device_cus()
     return v;
 }
 
+hipError_t mark(void* ev, hipStream_t st)
+{
+    return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), st) : hipSuccess;
+}
+
 template <typename T>
 T* at(void* ws, size_t off)
 {
@@ -186,8 +193,10 @@ T* at(void* ws, size_t off)
 // Scoring; if `hist` is given the first selection digit is counted as a side
 // effect (hill_step) and the counts are cleared by the first kernel.
 hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, float* sacc,
-                      void* ws, bool with_hist, hipStream_t st)
+                      void* ws, bool with_hist, hipStream_t st, const hill_step_events& ev)
 {
+    const Stamp scan{static_cast<hipEvent_t>(ev.scan_start), static_cast<hipEvent_t>(ev.scan_stop)};
+    const Stamp last{nullptr, static_cast<hipEvent_t>(ev.score_stop)};
     uint32_t* hist = with_hist ? at<uint32_t>(ws, L.hist) : nullptr;
     const int64_t hist_words = (int64_t)s.B * s.R * kHistBins;
     ScoreArgs a{};
@@ -204,13 +213,14 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.G = s.G;
     a.n = s.n;
     a.ntiles = s.ntiles;
+    a.ld = s.ld;
     a.s2 = s.scale * 1.4426950408889634f;
     a.s = sacc;
     a.s_sb = d->s_stride_b;
     a.s_sr = d->s_stride_r;
     a.zero_ptr = hist;
     a.zero_words = with_hist ? hist_words : 0;
-    const int grid_cap = device_cus() * 4;
+    const int ncu = device_cus();
 
     UpdateArgs u{};
     u.s = sacc;
@@ -222,33 +232,36 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     u.G = s.G;
     u.R = s.R;
     u.n = s.n;
+    u.ld = s.ld;
     u.s2 = a.s2;
     u.hist = hist;
 
     if (s.mode == HILL_SCORE_ATTN) {
         a.logits = at<float>(ws, L.logits);
         a.part = at<float2>(ws, L.part);
-        HIP_TRY(launch_score_tiles(a, s.dtype, kOutLogits, grid_cap, st));
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutLogits, ncu, st, scan));
         float2* stats = at<float2>(ws, L.stats);
         HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.ntiles, st));
         u.logits = a.logits;
         u.stats = stats;
-        HIP_TRY(launch_update_attn(u, st));
+        HIP_TRY(launch_update_attn(u, st, last));
     } else if (s.R == s.Hkv) {
         // one row per KV head (or a single KV head): the scan adds straight into S
-        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawS, grid_cap, st));
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawS, ncu, st, scan));
+        HIP_TRY(mark(ev.score_stop, st));
         if (with_hist) HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, hist, st));
     } else {
         a.logits = at<float>(ws, L.logits);
-        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawGroups, grid_cap, st));
+        HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawGroups, ncu, st, scan));
         u.logits = a.logits;
-        HIP_TRY(launch_update_raw_groups(u, st));
+        HIP_TRY(launch_update_raw_groups(u, st, last));
     }
     return HILL_OK;
 }
 
 hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, const float* sacc, int32_t ksel,
-                       int32_t* idx, float* val, void* ws, bool hist_ready, hipStream_t st)
+                       int32_t* idx, float* val, void* ws, bool hist_ready, hipStream_t st,
+                       const hill_step_events& ev)
 {
     uint32_t* hist = at<uint32_t>(ws, L.hist);
     if (!hist_ready) {
@@ -265,12 +278,13 @@ hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, cons
     a.hist = hist;
     a.idx = idx;
     a.val = val;
-    HIP_TRY(launch_topk_select(a, s.B * s.R, st));
+    HIP_TRY(launch_topk_select(a, s.B * s.R, st,
+                               Stamp{static_cast<hipEvent_t>(ev.select_start), static_cast<hipEvent_t>(ev.select_stop)}));
     return HILL_OK;
 }
 
 hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, const void* v,
-                     const int32_t* idx, int32_t ksel, float* out, void* ws, hipStream_t st)
+                     const int32_t* idx, int32_t ksel, float* out, void* ws, hipStream_t st, const hill_step_events& ev)
 {
     AttnArgs a{};
     a.q = static_cast<const uint16_t*>(q);
@@ -299,7 +313,7 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
     a.part_ml = at<float2>(ws, L.apart_ml);
     a.out = out;
     HIP_TRY(launch_attn_split(a, s.dtype, st));
-    HIP_TRY(launch_attn_combine(a, st));
+    HIP_TRY(launch_attn_combine(a, st, Stamp{nullptr, static_cast<hipEvent_t>(ev.attn_stop)}));
     return HILL_OK;
 }
 
@@ -343,7 +357,7 @@ hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* 
     HILL_TRY(check_ptr(s_acc, "s"));
     const Layout L = layout_for(s, 1);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_score));
-    return run_score(d, s, L, q, k, s_acc, ws, false, static_cast<hipStream_t>(stream));
+    return run_score(d, s, L, q, k, s_acc, ws, false, static_cast<hipStream_t>(stream), hill_step_events{});
 }
 
 hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int32_t* idx_out, float* val_out,
@@ -358,7 +372,8 @@ hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int
     if (val_out && ((uintptr_t)val_out & 3u)) return fail(HILL_ERR_INVALID_ARG, "val_out is not 4-byte aligned");
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_topk));
-    return run_select(d, s, L, s_acc, k_sel, idx_out, val_out, ws, false, static_cast<hipStream_t>(stream));
+    return run_select(d, s, L, s_acc, k_sel, idx_out, val_out, ws, false, static_cast<hipStream_t>(stream),
+                      hill_step_events{});
 }
 
 hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v, const int32_t* idx,
@@ -375,11 +390,18 @@ hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, c
     if ((uintptr_t)idx & 3u) return fail(HILL_ERR_INVALID_ARG, "idx is not 4-byte aligned");
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
-    return run_attn(d, s, L, q, k, v, idx, k_sel, out, ws, static_cast<hipStream_t>(stream));
+    return run_attn(d, s, L, q, k, v, idx, k_sel, out, ws, static_cast<hipStream_t>(stream), hill_step_events{});
 }
 
 hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc, int32_t k_sel,
                       int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream)
+{
+    return hill_step_profiled(d, q, k, v, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, nullptr);
+}
+
+hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc,
+                               int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
+                               const hill_step_events* ev)
 {
     Shape s;
     HILL_TRY(check_desc(d, &s));
@@ -394,9 +416,11 @@ hill_status hill_step(const hill_desc* d, const void* q, const void* k, const vo
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
     hipStream_t st = static_cast<hipStream_t>(stream);
-    HILL_TRY(run_score(d, s, L, q, k, s_acc, ws, true, st));
-    HILL_TRY(run_select(d, s, L, s_acc, k_sel, idx_out, nullptr, ws, true, st));
-    return run_attn(d, s, L, q, k, v, idx_out, k_sel, out, ws, st);
+    const hill_step_events none{};
+    const hill_step_events& e = ev ? *ev : none;
+    HILL_TRY(run_score(d, s, L, q, k, s_acc, ws, true, st, e));
+    HILL_TRY(run_select(d, s, L, s_acc, k_sel, idx_out, nullptr, ws, true, st, e));
+    return run_attn(d, s, L, q, k, v, idx_out, k_sel, out, ws, st, e);
 }
 
 }  // extern "C"

@@ -74,6 +74,16 @@ __device__ __forceinline__ float dpp(float v)
                                                                   false));
 }
 
+// Sum over each aligned group of 8 lanes; every lane of the group gets the sum.
+// quad_perm[1,0,3,2], quad_perm[2,3,0,1], row_half_mirror.
+__device__ __forceinline__ float sum8(float v)
+{
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    v += dpp<0x141>(v);
+    return v;
+}
+
 // Sum over each aligned group of 16 lanes; every lane of the group gets the sum.
 // quad_perm[1,0,3,2], quad_perm[2,3,0,1], row_half_mirror, row_mirror.
 __device__ __forceinline__ float sum16(float v)
@@ -132,6 +142,47 @@ __device__ __forceinline__ uint32_t block_excl_scan(uint32_t v, uint32_t* scratc
     *total = scratch[NW];
     __syncthreads();
     return r;
+}
+
+// Exclusive prefix sums of two counters at once over a block of NT threads.
+// `scratch` holds at least NT/64 + 1 uint2 of LDS.
+template <int NT>
+__device__ __forceinline__ uint2 block_excl_scan2(uint2 v, uint2* scratch, uint2* total)
+{
+    constexpr int NW = NT / 64;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    uint2 inc = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t tx = __shfl_up(inc.x, o, 64);
+        const uint32_t ty = __shfl_up(inc.y, o, 64);
+        if (lane >= o) {
+            inc.x += tx;
+            inc.y += ty;
+        }
+    }
+    if (lane == 63) scratch[w] = inc;
+    __syncthreads();
+    if (w == 0) {
+        uint2 x = lane < NW ? scratch[lane] : make_uint2(0u, 0u);
+        uint2 xi = x;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t tx = __shfl_up(xi.x, o, 64);
+            const uint32_t ty = __shfl_up(xi.y, o, 64);
+            if (lane >= o) {
+                xi.x += tx;
+                xi.y += ty;
+            }
+        }
+        if (lane < NW) scratch[lane] = make_uint2(xi.x - x.x, xi.y - x.y);
+        if (lane == NW - 1) scratch[NW] = xi;
+    }
+    __syncthreads();
+    const uint2 base = scratch[w];
+    *total = scratch[NW];
+    __syncthreads();
+    return make_uint2(base.x + inc.x - v.x, base.y + inc.y - v.y);
 }
 
 // Order-preserving map of fp32 to uint32: larger float -> larger key.

@@ -8,10 +8,10 @@
 namespace hill {
 
 constexpr int kHeadDim = 128;      // D supported by every kernel
-constexpr int kScoreTile = 128;    // tokens per scoring tile (one K1 work item)
+constexpr int kScoreTile = 32;     // tokens per scoring wave-tile (softmax partial granularity)
 constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
-constexpr int kUpdChunk = 512;     // tokens per importance-update workgroup
+constexpr int kUpdChunk = 256;     // tokens per importance-update workgroup
 constexpr int kHistChunk = 2048;   // tokens per standalone histogram workgroup
 
 enum ScoreOut : int {
@@ -26,8 +26,9 @@ struct ScoreArgs {
     int64_t q_sb, q_sh;
     int64_t k_sb, k_sh, k_sn;
     int B, Hq, Hkv, G, n, ntiles;
+    int64_t ld;              // row stride of the logits buffer (n rounded up to 4)
     float s2;                // sm_scale * log2(e): logits are kept in the exp2 domain
-    float* logits;           // kOutLogits / kOutRawGroups destination
+    float* logits;           // kOutLogits: [B,Hq,ld]; kOutRawGroups: [B,Hkv,ld]
     float2* part;            // kOutLogits: [B,Hq,ntiles] (max, sum exp2) per tile
     float* s;                // kOutRawS: importance rows
     int64_t s_sb, s_sr;
@@ -36,7 +37,8 @@ struct ScoreArgs {
 };
 
 struct UpdateArgs {
-    const float* logits;     // ATTN: [B,Hq,n]; RAW: group sums [B,Hkv,n]
+    const float* logits;     // ATTN: [B,Hq,ld]; RAW: group sums [B,Hkv,ld]
+    int64_t ld;
     const float2* stats;     // ATTN: [B,Hq] (max, 1/sum) in the exp2 domain
     float* s;
     int64_t s_sb, s_sr;
@@ -73,26 +75,33 @@ struct AttnArgs {
 // A pure function of the shape so that workspace sizing needs no device query.
 inline int attn_splits(int64_t b_hkv, int ksel, int* per_split)
 {
-    const int64_t target_wgs = 1024;
-    const int min_tokens = 32;
+    const int64_t target_wgs = 512;   // about two workgroups per CU
+    const int min_tokens = 64;
     int64_t s = (target_wgs + b_hkv - 1) / b_hkv;
     int64_t cap = (ksel + min_tokens - 1) / min_tokens;
     if (s > cap) s = cap;
     if (s < 1) s = 1;
     int p = (int)((ksel + s - 1) / s);
     *per_split = p;
-    return (ksel + p - 1) / p;   // every split non-empty
+    return (ksel + p - 1) / p;   // every split non-empty; at most target_wgs
 }
+constexpr int kMaxSplits = 512;
+
+// Optional start/stop timestamps of one launch (hipExtLaunchKernel events).
+struct Stamp {
+    hipEvent_t start = nullptr;
+    hipEvent_t stop = nullptr;
+};
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
-hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int grid_cap, hipStream_t st);
+hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int ntiles, hipStream_t st);
-hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st);
-hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st);
+hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
+hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n,
-                            uint32_t* hist, hipStream_t st);
-hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st);
+                            uint32_t* hist, hipStream_t st, Stamp ts = {});
+hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st, Stamp ts = {});
 hipError_t launch_attn_split(const AttnArgs& a, int dtype, hipStream_t st);
-hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st);
+hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st, Stamp ts = {});
 
 }  // namespace hill

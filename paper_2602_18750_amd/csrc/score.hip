@@ -11,10 +11,19 @@
 //                to the cumulative importance S (Sec. 4.1 metric), and counts
 //                the first radix digit of the new S for the selection.
 //
-// Key rows are 256 bytes (D = 128 x 16 bit).  A group of 16 lanes reads one
-// row with 16-byte loads, so a wave reads 4 contiguous rows (1 KiB) per load;
-// each lane keeps 8 rows in flight.  Partial dot products are combined with
-// four DPP adds inside the 16-lane group.
+// score_tiles layout.  A key row is 256 bytes (D = 128 x 16 bit).  Eight
+// lanes share a row: lane l8 reads elements [8*l8, 8*l8+8) with one 16-byte
+// load and [64+8*l8, 64+8*l8+8) with a second, so each load instruction of a
+// wave covers whole 128-byte lines of 8 rows.  The work item is a wave-tile
+// of 32 consecutive tokens of one (sequence, KV head): row group rg (lanes
+// 8*rg .. 8*rg+7) owns tokens j0 + 4*rg .. j0 + 4*rg + 3.  Waves run
+// independently (no LDS, no barriers); each wave walks a contiguous range of
+// wave-tiles and keeps the group's queries in registers while (b, g) stays
+// the same.  Latency is hidden by occupancy (several waves per SIMD) rather
+// than by double-buffering, which costs more registers than it returns.
+// Partial dot products are combined by three DPP adds.
+#include <hip/hip_ext.h>
+
 #include "hill_device.h"
 #include "hill_internal.h"
 
@@ -22,8 +31,8 @@ namespace hill {
 
 namespace {
 
-constexpr int kRowsPerLane = kScoreTile / 16;  // 8 key rows in flight per lane
-constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kRowsPerLane = kScoreTile / 8;   // 4 rows per row group
+constexpr int kLoadsPerTile = 2 * kRowsPerLane;
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, int64_t words)
 {
@@ -32,220 +41,362 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, int64_t wor
         p[i] = 0u;
 }
 
+struct TileCoord {
+    int b, g, tile, j0;
+};
+
+__device__ __forceinline__ TileCoord coord(const ScoreArgs& a, int t)
+{
+    TileCoord c;
+    c.tile = t % a.ntiles;
+    const int bg = t / a.ntiles;
+    c.g = bg % a.Hkv;
+    c.b = bg / a.Hkv;
+    c.j0 = c.tile * kScoreTile;
+    return c;
+}
+
+__device__ __forceinline__ void load_tile(const ScoreArgs& a, int t, int rg, int l8, uint4 (&kr)[kLoadsPerTile])
+{
+    const TileCoord c = coord(a, t);
+    const uint16_t* kb = a.k + (int64_t)c.b * a.k_sb + (int64_t)c.g * a.k_sh + l8 * 8;
+#pragma unroll
+    for (int u = 0; u < kRowsPerLane; ++u) {
+        const int j = c.j0 + rg * kRowsPerLane + u;
+        if (j < a.n) {
+            const uint16_t* row = kb + (int64_t)j * a.k_sn;
+            kr[2 * u] = load_stream16(row);
+            kr[2 * u + 1] = load_stream16(row + 64);
+        } else {
+            kr[2 * u] = make_uint4(0u, 0u, 0u, 0u);
+            kr[2 * u + 1] = make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+}
+
+template <int DT, int GC, int OUT>
+__device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, int l8, const uint4 (&kr)[kLoadsPerTile],
+                                             uint4 (&qa)[GC], uint4 (&qb)[GC], int& q_tag)
+{
+    const TileCoord c = coord(a, t);
+    const int jr = c.j0 + rg * kRowsPerLane;   // first token of this row group
+    float rawsum[kRowsPerLane];
+#pragma unroll
+    for (int u = 0; u < kRowsPerLane; ++u) rawsum[u] = 0.0f;
+
+    for (int hc = 0; hc < a.G; hc += GC) {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag != q_tag) {
+#pragma unroll
+            for (int hh = 0; hh < GC; ++hh) {
+                const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + hc + hh) * a.q_sh + l8 * 8;
+                qa[hh] = *reinterpret_cast<const uint4*>(qr);
+                qb[hh] = *reinterpret_cast<const uint4*>(qr + 64);
+            }
+            q_tag = tag;
+        }
+        float mine[kRowsPerLane];   // lane l8 == hh keeps head hh's logits
+#pragma unroll
+        for (int u = 0; u < kRowsPerLane; ++u) {
+            mine[u] = 0.0f;
+#pragma unroll
+            for (int hh = 0; hh < GC; ++hh) {
+                float d = dot8<DT>(kr[2 * u], qa[hh]);
+                d += dot8<DT>(kr[2 * u + 1], qb[hh]);
+                d = sum8(d);
+                if constexpr (OUT == kOutLogits)
+                    mine[u] = (l8 == hh) ? d : mine[u];
+                else
+                    rawsum[u] += d;
+            }
+        }
+        if constexpr (OUT == kOutLogits) {
+            const int h = c.g * a.G + hc + l8;   // valid for l8 < GC
+            float* lrow = a.logits + ((int64_t)c.b * a.Hq + h) * a.ld + jr;
+            float x[kRowsPerLane];
+            float m = -INFINITY;
+#pragma unroll
+            for (int u = 0; u < kRowsPerLane; ++u) {
+                x[u] = jr + u < a.n ? a.s2 * mine[u] : -INFINITY;
+                m = fmaxf(m, x[u]);
+            }
+            if (l8 < GC) {
+                if (jr + kRowsPerLane <= a.n) {
+                    *reinterpret_cast<float4*>(lrow) = make_float4(mine[0], mine[1], mine[2], mine[3]);
+                } else {
+#pragma unroll
+                    for (int u = 0; u < kRowsPerLane; ++u)
+                        if (jr + u < a.n) lrow[u] = mine[u];
+                }
+            }
+            // tile max and sum of exp2 over the 8 row groups (lanes l8 + 8*rg)
+            m = fmaxf(m, __shfl_xor(m, 8, 64));
+            m = fmaxf(m, __shfl_xor(m, 16, 64));
+            m = fmaxf(m, __shfl_xor(m, 32, 64));
+            float z = 0.0f;
+#pragma unroll
+            for (int u = 0; u < kRowsPerLane; ++u) z += jr + u < a.n ? exp2f(x[u] - m) : 0.0f;
+            z += __shfl_xor(z, 8, 64);
+            z += __shfl_xor(z, 16, 64);
+            z += __shfl_xor(z, 32, 64);
+            if (rg == 0 && l8 < GC)
+                a.part[((int64_t)c.b * a.Hq + h) * a.ntiles + c.tile] = make_float2(m, z);
+        }
+    }
+
+    if constexpr (OUT != kOutLogits) {
+        if (l8 == 0 && jr < a.n) {
+            float* dst = OUT == kOutRawS ? a.s + (int64_t)c.b * a.s_sb + (int64_t)c.g * a.s_sr + jr
+                                         : a.logits + ((int64_t)c.b * a.Hkv + c.g) * a.ld + jr;
+            if (jr + kRowsPerLane <= a.n) {
+                float4 v = make_float4(rawsum[0], rawsum[1], rawsum[2], rawsum[3]);
+                if constexpr (OUT == kOutRawS) {
+                    const float4 o = *reinterpret_cast<const float4*>(dst);
+                    v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+                }
+                *reinterpret_cast<float4*>(dst) = v;
+            } else {
+#pragma unroll
+                for (int u = 0; u < kRowsPerLane; ++u)
+                    if (jr + u < a.n) dst[u] = (OUT == kOutRawS ? dst[u] : 0.0f) + rawsum[u];
+            }
+        }
+    }
+}
+
 template <int DT, int GC, int OUT>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
-    __shared__ float tile_logit[OUT == kOutLogits ? GC : 1][kScoreTile];
-
-    const int tid = threadIdx.x;
-    const int rg = tid >> 4;    // row group: which of the 16 rows of a load slot
-    const int l16 = tid & 15;   // 16-byte column within the row
+    const int lane = threadIdx.x & 63;
+    const int rg = lane >> 3;
+    const int l8 = lane & 7;
 
     if (a.zero_ptr) {
-        for (int64_t i = (int64_t)blockIdx.x * 256 + tid; i < a.zero_words; i += (int64_t)gridDim.x * 256)
+        for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < a.zero_words; i += (int64_t)gridDim.x * 256)
             a.zero_ptr[i] = 0u;
     }
 
+    // contiguous range of wave-tiles per wave
+    const int nwaves = gridDim.x * 4;
+    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
     const int total = a.B * a.Hkv * a.ntiles;
-    for (int t = blockIdx.x; t < total; t += gridDim.x) {
-        const int tile = t % a.ntiles;
-        const int bg = t / a.ntiles;
-        const int g = bg % a.Hkv;
-        const int b = bg / a.Hkv;
-        const int j0 = tile * kScoreTile;
-        const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
+    const int per = (total + nwaves - 1) / nwaves;
+    int t = w * per;
+    const int t_end = min(t + per, total);
+    if (t >= t_end) return;
 
-        uint4 kr[kRowsPerLane];
-#pragma unroll
-        for (int u = 0; u < kRowsPerLane; ++u) {
-            const int j = j0 + u * 16 + rg;
-            if (j < a.n)
-                kr[u] = load_stream16(kb + (int64_t)j * a.k_sn);
-            else
-                kr[u] = make_uint4(0u, 0u, 0u, 0u);
-        }
-
-        float rawsum[kRowsPerLane];
-#pragma unroll
-        for (int u = 0; u < kRowsPerLane; ++u) rawsum[u] = 0.0f;
-
-        for (int hc = 0; hc < a.G; hc += GC) {
-            uint4 qv[GC];
-#pragma unroll
-            for (int hh = 0; hh < GC; ++hh) {
-                const int h = g * a.G + hc + hh;
-                qv[hh] = *reinterpret_cast<const uint4*>(a.q + (int64_t)b * a.q_sb + (int64_t)h * a.q_sh + l16 * 8);
-            }
-#pragma unroll
-            for (int u = 0; u < kRowsPerLane; ++u) {
-#pragma unroll
-                for (int hh = 0; hh < GC; ++hh) {
-                    float d = sum16(dot8<DT>(kr[u], qv[hh]));
-                    if constexpr (OUT == kOutLogits) {
-                        if (l16 == hh) tile_logit[hh][u * 16 + rg] = d;
-                    } else {
-                        rawsum[u] += d;
-                    }
-                }
-            }
-            if constexpr (OUT == kOutLogits) {
-                __syncthreads();
-                // coalesced logits store: GC rows of kScoreTile floats
-                for (int e = tid; e < GC * kScoreTile; e += 256) {
-                    const int hh = e / kScoreTile, c = e % kScoreTile;
-                    const int j = j0 + c;
-                    if (j < a.n) {
-                        const int h = g * a.G + hc + hh;
-                        a.logits[((int64_t)b * a.Hq + h) * a.n + j] = tile_logit[hh][c];
-                    }
-                }
-                // per-tile softmax partials in the exp2 domain: one wave per head
-                const int w = tid >> 6, lane = tid & 63;
-                for (int hh = w; hh < GC; hh += 4) {
-                    const int c0 = lane, c1 = lane + 64;
-                    const bool v0 = j0 + c0 < a.n, v1 = j0 + c1 < a.n;
-                    const float x0 = v0 ? a.s2 * tile_logit[hh][c0] : -INFINITY;
-                    const float x1 = v1 ? a.s2 * tile_logit[hh][c1] : -INFINITY;
-                    const float m = wave_max(fmaxf(x0, x1));
-                    float z = (v0 ? exp2f(x0 - m) : 0.0f) + (v1 ? exp2f(x1 - m) : 0.0f);
-                    z = wave_sum(z);
-                    if (lane == 0) {
-                        const int h = g * a.G + hc + hh;
-                        a.part[((int64_t)b * a.Hq + h) * a.ntiles + tile] = make_float2(m, z);
-                    }
-                }
-                __syncthreads();
-            }
-        }
-
-        if constexpr (OUT != kOutLogits) {
-            if (l16 == 0) {
-#pragma unroll
-                for (int u = 0; u < kRowsPerLane; ++u) {
-                    const int j = j0 + u * 16 + rg;
-                    if (j < a.n) {
-                        if constexpr (OUT == kOutRawS)
-                            a.s[(int64_t)b * a.s_sb + (int64_t)g * a.s_sr + j] += rawsum[u];
-                        else
-                            a.logits[((int64_t)b * a.Hkv + g) * a.n + j] = rawsum[u];
-                    }
-                }
-            }
-        }
+    uint4 qa[GC], qb[GC];
+    int q_tag = -1;
+    uint4 kr[kLoadsPerTile];
+    for (; t < t_end; ++t) {
+        load_tile(a, t, rg, l8, kr);
+        compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag);
     }
 }
 
-// One wave per (b, h): combine the tile pairs into (max, 1/sum) in a fixed order.
+// One workgroup per (b, h): combine the tile pairs into (max, 1/sum), each
+// thread over a fixed strided subset, then waves in a fixed order.
 __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __restrict__ part,
-                                                            float2* __restrict__ stats, int bh_total, int ntiles)
+                                                            float2* __restrict__ stats, int ntiles)
 {
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int bh = blockIdx.x * 4 + w;
-    if (bh >= bh_total) return;
+    __shared__ float red_m[4], red_z[4];
+    const int bh = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const float2* p = part + (int64_t)bh * ntiles;
-    float m = -INFINITY;
-    for (int i = lane; i < ntiles; i += 64) m = fmaxf(m, p[i].x);
-    m = wave_max(m);
-    float z = 0.0f;
-    for (int i = lane; i < ntiles; i += 64) {
-        const float2 pi = p[i];
-        z += pi.y * exp2f(pi.x - m);
+    constexpr int kBatch = 8;
+    float m = -INFINITY, z = 0.0f;
+    for (int i0 = tid; i0 < ntiles; i0 += 256 * kBatch) {
+        float2 v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int i = i0 + u * 256;
+            v[u] = i < ntiles ? p[i] : make_float2(-INFINITY, 0.0f);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            if (v[u].x == -INFINITY) continue;
+            const float mn = fmaxf(m, v[u].x);
+            z = z * exp2f(m - mn) + v[u].y * exp2f(v[u].x - mn);
+            m = mn;
+        }
     }
+    const float mw = wave_max(m);
+    z = m > -INFINITY ? z * exp2f(m - mw) : 0.0f;
     z = wave_sum(z);
-    if (lane == 0) stats[bh] = make_float2(m, 1.0f / z);
+    if (lane == 0) {
+        red_m[w] = mw;
+        red_z[w] = z;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float M = red_m[0];
+        for (int i = 1; i < 4; ++i) M = fmaxf(M, red_m[i]);
+        float Z = 0.0f;
+        for (int i = 0; i < 4; ++i) Z += red_m[i] > -INFINITY ? red_z[i] * exp2f(red_m[i] - M) : 0.0f;
+        stats[bh] = make_float2(M, 1.0f / Z);
+    }
 }
 
-// Local histogram of the first radix digit of the new S values, merged into
-// the row's global histogram (integer atomics: order-independent result).
-__device__ __forceinline__ void hist_flush(uint32_t* lds_hist, uint32_t* ghist)
+// Merges a workgroup's LDS histogram into the row's global histogram: one
+// integer atomic per non-empty bin (order-independent result).
+__device__ __forceinline__ void hist_merge(const uint32_t* lds_hist, uint32_t* ghist)
 {
-    __syncthreads();
-    for (int i = threadIdx.x; i < kHistBins; i += blockDim.x) {
+    for (int i = threadIdx.x; i < kHistBins; i += 256) {
         const uint32_t c = lds_hist[i];
         if (c) atomicAdd(ghist + i, c);
     }
 }
 
-// S[b,r,j] += sum_{h in heads(r)} exp2(s2*l - max_h) / sum_h   (softmax weights)
+constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
+
+// S[b,r,j] += sum_{h in heads(r)} exp2(s2*l - max_h) / sum_h   (softmax weights).
+// kUpdChunk = 256 tokens per workgroup: lane l of wave w loads tokens
+// [4l, 4l+4) of heads w, w+4, ... as float4; the four wave partials are added
+// in wave order, then each thread finishes one token and counts its first
+// selection digit in an LDS histogram.
 __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 {
+    __shared__ float4 wsum[4][64];
     __shared__ uint32_t lds_hist[kHistBins];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
     const int nh = a.R == 1 ? a.Hq : a.G;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
-    if (do_hist) {
-        for (int i = threadIdx.x; i < kHistBins; i += 256) lds_hist[i] = 0u;
-        __syncthreads();
-    }
-    float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
-    const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.n;
+    if (do_hist)
+        for (int i = tid; i < kHistBins; i += 256) lds_hist[i] = 0u;
+    const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
+    const int jc = min(j4, (int)(a.ld - 4));              // rows are padded to ld (multiple of 4)
+    const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
     const float2* st = a.stats + (int64_t)b * a.Hq + h0;
-    constexpr int kPer = kUpdChunk / 256;
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int hb = w; hb < nh; hb += 4 * kHeadBatch) {
+        float4 x[kHeadBatch];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        const int j = blockIdx.x * kUpdChunk + i * 256 + threadIdx.x;
-        if (j < a.n) {
-            float acc = 0.0f;
-            for (int h = 0; h < nh; ++h) {
+        for (int i = 0; i < kHeadBatch; ++i) {
+            const int h = hb + 4 * i;
+            x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < kHeadBatch; ++i) {
+            const int h = hb + 4 * i;
+            if (h < nh) {
                 const float2 ms = st[h];
-                acc += exp2f(a.s2 * lg[(int64_t)h * a.n + j] - ms.x) * ms.y;
+                acc.x += exp2f(a.s2 * x[i].x - ms.x) * ms.y;
+                acc.y += exp2f(a.s2 * x[i].y - ms.x) * ms.y;
+                acc.z += exp2f(a.s2 * x[i].z - ms.x) * ms.y;
+                acc.w += exp2f(a.s2 * x[i].w - ms.x) * ms.y;
             }
-            const float s_new = srow[j] + acc;
-            srow[j] = s_new;
-            if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
         }
     }
-    if (do_hist) hist_flush(lds_hist, a.hist + (int64_t)row * kHistBins);
+    wsum[w][lane] = acc;
+    __syncthreads();
+    const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
+    const int j = blockIdx.x * kUpdChunk + tid;
+    if (j < a.n) {
+        const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
+        float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
+        const float s_new = srow[j] + tot;
+        srow[j] = s_new;
+        if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
+    }
+    if (do_hist) {
+        __syncthreads();
+        hist_merge(lds_hist, a.hist + (int64_t)row * kHistBins);
+    }
 }
 
-// Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j].
+// Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j] (same layout).
 __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
 {
+    __shared__ float4 wsum[4][64];
     __shared__ uint32_t lds_hist[kHistBins];
     const int b = blockIdx.y;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
-    if (do_hist) {
-        for (int i = threadIdx.x; i < kHistBins; i += 256) lds_hist[i] = 0u;
-        __syncthreads();
-    }
-    float* srow = a.s + (int64_t)b * a.s_sb;
-    const float* gs = a.logits + (int64_t)b * a.Hkv * a.n;
-    constexpr int kPer = kUpdChunk / 256;
+    if (do_hist)
+        for (int i = tid; i < kHistBins; i += 256) lds_hist[i] = 0u;
+    const int j4 = blockIdx.x * kUpdChunk + 4 * lane;
+    const int jc = min(j4, (int)(a.ld - 4));
+    const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int gb = w; gb < a.Hkv; gb += 4 * kHeadBatch) {
+        float4 x[kHeadBatch];
 #pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-        const int j = blockIdx.x * kUpdChunk + i * 256 + threadIdx.x;
-        if (j < a.n) {
-            float acc = 0.0f;
-            for (int g = 0; g < a.Hkv; ++g) acc += gs[(int64_t)g * a.n + j];
-            const float s_new = srow[j] + acc;
-            srow[j] = s_new;
-            if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
+        for (int i = 0; i < kHeadBatch; ++i) {
+            const int g = gb + 4 * i;
+            x[i] = g < a.Hkv ? *reinterpret_cast<const float4*>(gs + (int64_t)g * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < kHeadBatch; ++i) {
+            acc.x += x[i].x;
+            acc.y += x[i].y;
+            acc.z += x[i].z;
+            acc.w += x[i].w;
         }
     }
-    if (do_hist) hist_flush(lds_hist, a.hist + (int64_t)b * kHistBins);
+    wsum[w][lane] = acc;
+    __syncthreads();
+    const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
+    const int j = blockIdx.x * kUpdChunk + tid;
+    if (j < a.n) {
+        const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
+        float* srow = a.s + (int64_t)b * a.s_sb;
+        const float s_new = srow[j] + tot;
+        srow[j] = s_new;
+        if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
+    }
+    if (do_hist) {
+        __syncthreads();
+        hist_merge(lds_hist, a.hist + (int64_t)b * kHistBins);
+    }
 }
 
-template <int DT, int OUT>
-hipError_t launch_score_gc(const ScoreArgs& a, int gc, dim3 grid, hipStream_t st)
+// Workgroups of `kernel` that stay resident on one CU (queried once per instantiation).
+template <typename K>
+int resident_per_cu(K kernel)
 {
-    switch (gc) {
-    case 8: hipLaunchKernelGGL((score_tiles_kernel<DT, 8, OUT>), grid, dim3(256), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((score_tiles_kernel<DT, 4, OUT>), grid, dim3(256), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((score_tiles_kernel<DT, 2, OUT>), grid, dim3(256), 0, st, a); break;
-    default: hipLaunchKernelGGL((score_tiles_kernel<DT, 1, OUT>), grid, dim3(256), 0, st, a); break;
-    }
+    static const int v = [kernel] {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, 256, 0) != hipSuccess || nb < 1) nb = 1;
+        return nb;
+    }();
+    return v;
+}
+
+// Persistent grid: every workgroup resident at once, each wave with at least one tile.
+template <int DT, int GC, int OUT>
+hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp ts)
+{
+    auto kernel = score_tiles_kernel<DT, GC, OUT>;
+    const int64_t total = (int64_t)a.B * a.Hkv * a.ntiles;
+    int64_t grid = (total + 3) / 4;
+    const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+    if (grid > cap) grid = cap;
+    if (grid < 1) grid = 1;
+    hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 
+template <int DT, int OUT>
+hipError_t launch_score_gc(const ScoreArgs& a, int gc, int ncu, hipStream_t st, Stamp ts)
+{
+    switch (gc) {
+    case 8: return launch_score_inst<DT, 8, OUT>(a, ncu, st, ts);
+    case 4: return launch_score_inst<DT, 4, OUT>(a, ncu, st, ts);
+    case 2: return launch_score_inst<DT, 2, OUT>(a, ncu, st, ts);
+    default: return launch_score_inst<DT, 1, OUT>(a, ncu, st, ts);
+    }
+}
+
 template <int DT>
-hipError_t launch_score_dt(const ScoreArgs& a, ScoreOut out, int gc, dim3 grid, hipStream_t st)
+hipError_t launch_score_dt(const ScoreArgs& a, ScoreOut out, int gc, int ncu, hipStream_t st, Stamp ts)
 {
     switch (out) {
-    case kOutLogits: return launch_score_gc<DT, kOutLogits>(a, gc, grid, st);
-    case kOutRawS: return launch_score_gc<DT, kOutRawS>(a, gc, grid, st);
-    default: return launch_score_gc<DT, kOutRawGroups>(a, gc, grid, st);
+    case kOutLogits: return launch_score_gc<DT, kOutLogits>(a, gc, ncu, st, ts);
+    case kOutRawS: return launch_score_gc<DT, kOutRawS>(a, gc, ncu, st, ts);
+    default: return launch_score_gc<DT, kOutRawGroups>(a, gc, ncu, st, ts);
     }
 }
 
@@ -260,34 +411,31 @@ hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st)
     return hipGetLastError();
 }
 
-hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int grid_cap, hipStream_t st)
+hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts)
 {
     // heads per pass over the key registers: the largest of 8, 4, 2, 1 dividing G
     const int gc = (a.G % 8 == 0) ? 8 : (a.G % 4 == 0) ? 4 : (a.G % 2 == 0) ? 2 : 1;
-    int64_t total = (int64_t)a.B * a.Hkv * a.ntiles;
-    int64_t grid = total < grid_cap ? total : grid_cap;
-    if (grid < 1) grid = 1;
-    if (dtype == 1) return launch_score_dt<1>(a, out, gc, dim3((unsigned)grid), st);
-    return launch_score_dt<0>(a, out, gc, dim3((unsigned)grid), st);
+    if (dtype == 1) return launch_score_dt<1>(a, out, gc, ncu, st, ts);
+    return launch_score_dt<0>(a, out, gc, ncu, st, ts);
 }
 
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int ntiles, hipStream_t st)
 {
-    hipLaunchKernelGGL(softmax_stats_kernel, dim3((bh + 3) / 4), dim3(256), 0, st, part, stats, bh, ntiles);
+    hipLaunchKernelGGL(softmax_stats_kernel, dim3(bh), dim3(256), 0, st, part, stats, ntiles);
     return hipGetLastError();
 }
 
-hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st)
+hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts)
 {
     dim3 grid((a.n + kUpdChunk - 1) / kUpdChunk, a.B * a.R);
-    hipLaunchKernelGGL(update_attn_kernel, grid, dim3(256), 0, st, a);
+    hipExtLaunchKernelGGL(update_attn_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 
-hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st)
+hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts)
 {
     dim3 grid((a.n + kUpdChunk - 1) / kUpdChunk, a.B);
-    hipLaunchKernelGGL(update_raw_groups_kernel, grid, dim3(256), 0, st, a);
+    hipExtLaunchKernelGGL(update_raw_groups_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 

@@ -3,15 +3,20 @@
 //
 //  topk_hist     many workgroups per row count the first 12-bit digit of the
 //                keys (also fused into the importance update).
-//  topk_select   one 1024-thread workgroup per row: finds the threshold key
-//                digit by digit (12 + 12 + 8 bits; later digits only look at
-//                keys that still tie on the earlier ones), then emits every
-//                key above the threshold plus the lowest-index keys equal to
-//                it, in ascending token order, with one ordered block scan
-//                per 4096-key tile.
+//  topk_select   one 1024-thread workgroup per row.  Each thread holds a
+//                contiguous 32-key segment of the row in registers (32768
+//                keys per chunk, loaded with coalesced reads and transposed
+//                through LDS; rows up to that length are read once).  The
+//                threshold key is found digit by digit (12 + 12 + 8 bits;
+//                later digits only count keys that still tie on the earlier
+//                ones), then every key above it plus the lowest-index keys
+//                equal to it are written in ascending token order, placed by
+//                one block-wide scan of (greater, equal) counts per chunk.
 //
 // The result is exactly the k largest S with ties to the lower index: the
 // keys are integers, so no floating-point rounding is involved.
+#include <hip/hip_ext.h>
+
 #include "hill_device.h"
 #include "hill_internal.h"
 
@@ -20,7 +25,8 @@ namespace hill {
 namespace {
 
 constexpr int kSelThreads = 1024;
-constexpr int kSelTile = kSelThreads * 4;
+constexpr int kSelPer = 32;                         // keys per thread per chunk
+constexpr int kSelChunk = kSelThreads * kSelPer;    // 32768 keys
 
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict__ s, int64_t s_sb, int64_t s_sr,
                                                         int R, int n, uint32_t* __restrict__ hist)
@@ -45,21 +51,41 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict_
     }
 }
 
-// Reads 4 consecutive keys starting at j (j a multiple of 4); keys past n are
-// reported invalid.  The row base is 16-byte aligned.
-__device__ __forceinline__ void load4(const float* srow, int j, int n, float v[4], bool ok[4])
+constexpr int kSelPitch = kSelPer + 1;             // LDS words per thread segment (bank-conflict free)
+
+// Stage chunk c of the row through LDS: coalesced 16-byte global loads, then
+// each thread takes its contiguous segment of tokens [c*kSelChunk + 32*tid, +32)
+// as order keys.  Returns how many of those tokens are inside the row.
+// Row bases are 16-byte aligned.  Every thread of the block must call this.
+__device__ __forceinline__ int load_segment(const float* srow, int c, int n, uint32_t* stage,
+                                            uint32_t (&key)[kSelPer])
 {
-    if (j + 3 < n) {
-        const float4 x = *reinterpret_cast<const float4*>(srow + j);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-        ok[0] = ok[1] = ok[2] = ok[3] = true;
-    } else {
+    const int tid = threadIdx.x;
+    const int c0 = c * kSelChunk;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            ok[e] = j + e < n;
-            v[e] = ok[e] ? srow[j + e] : 0.0f;
+    for (int i = 0; i < kSelPer / 4; ++i) {
+        const int pl = 4 * (i * kSelThreads + tid);     // position within the chunk
+        const int p = c0 + pl;
+        uint32_t k4[4];
+        if (p + 3 < n) {
+            const float4 x = *reinterpret_cast<const float4*>(srow + p);
+            k4[0] = order_key(x.x);
+            k4[1] = order_key(x.y);
+            k4[2] = order_key(x.z);
+            k4[3] = order_key(x.w);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) k4[e] = p + e < n ? order_key(srow[p + e]) : 0u;
         }
+        uint32_t* dst = stage + (pl / kSelPer) * kSelPitch + (pl % kSelPer);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = k4[e];
     }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kSelPer; ++i) key[i] = stage[tid * kSelPitch + i];
+    __syncthreads();
+    return min(max(n - (c0 + tid * kSelPer), 0), kSelPer);
 }
 
 // Given a histogram of `nb` bins (nb in {256, 4096}) in LDS, find the bin
@@ -98,8 +124,10 @@ __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* 
 
 __global__ __launch_bounds__(kSelThreads) void topk_select_kernel(SelectArgs a)
 {
+    __shared__ uint32_t stage[kSelThreads * kSelPitch];
     __shared__ uint32_t hist[kHistBins];
     __shared__ uint32_t scan_scratch[kSelThreads / 64 + 1];
+    __shared__ uint2 scan2_scratch[kSelThreads / 64 + 1];
     __shared__ uint32_t res[2];
 
     const int tid = threadIdx.x;
@@ -107,6 +135,11 @@ __global__ __launch_bounds__(kSelThreads) void topk_select_kernel(SelectArgs a)
     const int b = row / a.R, r = row % a.R;
     const float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
     const int n = a.n;
+    const int nchunks = (n + kSelChunk - 1) / kSelChunk;
+
+    uint32_t key[kSelPer];
+    int valid = 0;
+    if (nchunks == 1) valid = load_segment(srow, 0, n, stage, key);
 
     // digit 1 (bits 31..20): counts come from the multi-workgroup histogram
     const uint32_t* gh = a.hist + (int64_t)row * kHistBins;
@@ -126,16 +159,12 @@ __global__ __launch_bounds__(kSelThreads) void topk_select_kernel(SelectArgs a)
         __syncthreads();
         for (int i = tid; i < nb; i += kSelThreads) hist[i] = 0u;
         __syncthreads();
-        for (int base = 0; base < n; base += kSelTile) {
-            float v[4];
-            bool ok[4];
-            load4(srow, base + tid * 4, n, v, ok);
+        for (int c = 0; c < nchunks; ++c) {
+            if (nchunks > 1) valid = load_segment(srow, c, n, stage, key);
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const uint32_t key = order_key(v[e]);
-                if (ok[e] && (key >> shift) == prefix)
-                    atomicAdd(&hist[(key >> next_shift) & (uint32_t)(nb - 1)], 1u);
-            }
+            for (int i = 0; i < kSelPer; ++i)
+                if (i < valid && (key[i] >> shift) == prefix)
+                    atomicAdd(&hist[(key[i] >> next_shift) & (uint32_t)(nb - 1)], 1u);
         }
         __syncthreads();
         find_bin(hist, nb, need, scan_scratch, res);
@@ -151,55 +180,50 @@ __global__ __launch_bounds__(kSelThreads) void topk_select_kernel(SelectArgs a)
     int32_t* out_idx = a.idx + (int64_t)row * a.k;
     float* out_val = a.val ? a.val + (int64_t)row * a.k : nullptr;
     uint32_t carry_gt = 0, carry_eq = 0;
-    for (int base = 0; base < n; base += kSelTile) {
-        const int j = base + tid * 4;
-        float v[4];
-        bool ok[4];
-        load4(srow, j, n, v, ok);
-        uint32_t gt_mask = 0, eq_mask = 0;
+    for (int c = 0; c < nchunks; ++c) {
+        if (nchunks > 1) valid = load_segment(srow, c, n, stage, key);
+        uint32_t gtm = 0u, eqm = 0u;   // bit i: token 32*tid + i is above / at the threshold
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t key = order_key(v[e]) >> shift;
-            if (ok[e] && key > prefix) gt_mask |= 1u << e;
-            if (ok[e] && key == prefix) eq_mask |= 1u << e;
+        for (int i = 0; i < kSelPer; ++i) {
+            const uint32_t kd = key[i] >> shift;
+            gtm |= (i < valid && kd > prefix) ? (1u << i) : 0u;
+            eqm |= (i < valid && kd == prefix) ? (1u << i) : 0u;
         }
-        const uint32_t packed = ((uint32_t)__builtin_popcount(gt_mask) << 16) | (uint32_t)__builtin_popcount(eq_mask);
-        uint32_t total;
-        const uint32_t before = block_excl_scan<kSelThreads>(packed, scan_scratch, &total);
-        uint32_t gt_b = carry_gt + (before >> 16);
-        uint32_t eq_b = carry_eq + (before & 0xffffu);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const bool is_gt = (gt_mask >> e) & 1u;
-            const bool is_eq = (eq_mask >> e) & 1u;
-            if (is_gt || (is_eq && eq_b < need)) {
+        uint2 total;
+        const uint2 before = block_excl_scan2<kSelThreads>(
+            make_uint2((uint32_t)__builtin_popcount(gtm), (uint32_t)__builtin_popcount(eqm)), scan2_scratch, &total);
+        const int j0 = c * kSelChunk + tid * kSelPer;
+        for (uint32_t m = gtm | eqm; m; m &= m - 1u) {
+            const int i = __builtin_ctz(m);
+            const uint32_t below = (1u << i) - 1u;
+            const uint32_t gt_b = carry_gt + before.x + (uint32_t)__builtin_popcount(gtm & below);
+            const uint32_t eq_b = carry_eq + before.y + (uint32_t)__builtin_popcount(eqm & below);
+            if (((gtm >> i) & 1u) || eq_b < need) {
                 const uint32_t pos = gt_b + (eq_b < need ? eq_b : need);
                 if (pos < (uint32_t)a.k) {
-                    out_idx[pos] = j + e;
-                    if (out_val) out_val[pos] = v[e];
+                    out_idx[pos] = j0 + i;
+                    if (out_val) out_val[pos] = srow[j0 + i];
                 }
             }
-            gt_b += is_gt;
-            eq_b += is_eq;
         }
-        carry_gt += total >> 16;
-        carry_eq += total & 0xffffu;
+        carry_gt += total.x;
+        carry_eq += total.y;
     }
 }
 
 }  // namespace
 
 hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n, uint32_t* hist,
-                            hipStream_t st)
+                            hipStream_t st, Stamp ts)
 {
     dim3 grid((n + kHistChunk - 1) / kHistChunk, B * R);
-    hipLaunchKernelGGL(topk_hist_kernel, grid, dim3(256), 0, st, s, s_sb, s_sr, R, n, hist);
+    hipExtLaunchKernelGGL(topk_hist_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, s, s_sb, s_sr, R, n, hist);
     return hipGetLastError();
 }
 
-hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st)
+hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st, Stamp ts)
 {
-    hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, a);
+    hipExtLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 

@@ -24,7 +24,7 @@ from typing import Optional, Tuple
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libhill.so")
+LIB_PATH = os.environ.get("HILL_LIBRARY") or os.path.join(_PKG, "libhill.so")
 
 HILL_OK = 0
 STATUS = {0: "HILL_OK", 1: "HILL_ERR_INVALID_ARG", 2: "HILL_ERR_UNSUPPORTED", 3: "HILL_ERR_WORKSPACE",
@@ -34,7 +34,7 @@ MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
-           "hill_topk", "hill_gather_attn", "hill_step")
+           "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled")
 
 
 class HillError(RuntimeError):
@@ -66,6 +66,13 @@ class HillDesc(ctypes.Structure):
         ("s_stride_b", ctypes.c_int64),
         ("s_stride_r", ctypes.c_int64),
     ]
+
+
+class HillStepEvents(ctypes.Structure):
+    """Kernel timestamps for hill_step_profiled: hipEvent_t handles or None."""
+    _fields_ = [("scan_start", ctypes.c_void_p), ("scan_stop", ctypes.c_void_p), ("score_stop", ctypes.c_void_p),
+                ("select_start", ctypes.c_void_p), ("select_stop", ctypes.c_void_p),
+                ("attn_stop", ctypes.c_void_p)]
 
 
 _lock = threading.Lock()
@@ -100,6 +107,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_gather_attn.restype = ctypes.c_int
         lib.hill_step.argtypes = [D, P, P, P, P, I32, P, P, P, SZ, P]
         lib.hill_step.restype = ctypes.c_int
+        lib.hill_step_profiled.argtypes = [D, P, P, P, P, I32, P, P, P, SZ, P, ctypes.POINTER(HillStepEvents)]
+        lib.hill_step_profiled.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -256,8 +265,10 @@ def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_sca
 
 
 def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
-              sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None):
-    """One decode step: S update, top-k on the new S, attention.  Returns (idx, out)."""
+              sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None):
+    """One decode step: S update, top-k on the new S, attention.  Returns (idx, out).
+
+    ``events``: optional HillStepEvents; then hill_step_profiled records them."""
     lib = load_library()
     _device_check(q, k, v, s)
     desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
@@ -272,8 +283,13 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     if ws is None:
         ws = workspace(desc, k_sel, q.device)
-    _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
-                         _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
+    if events is None:
+        _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
+                             _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
+    else:
+        _check(lib.hill_step_profiled(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel),
+                                      _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
+                                      ctypes.byref(events)))
     return idx_out, out
 
 
@@ -281,3 +297,36 @@ def new_importance(B: int, R: int, n_cap: int, device) -> torch.Tensor:
     """Zeroed fp32 importance buffer [B, R, n_cap] whose row stride is a multiple of 4."""
     pad = (n_cap + 3) // 4 * 4
     return torch.zeros((B, R, pad), dtype=torch.float32, device=device)[:, :, :n_cap]
+
+
+class StepCall:
+    """hill_step with its arguments marshalled once, for hot loops that call it
+    repeatedly on the same buffers (only the query pointer changes per call)."""
+
+    def __init__(self, q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
+                 ws=None, stream=None):
+        lib = load_library()
+        _device_check(q, k, v, s)
+        self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
+                              sm_scale=sm_scale)
+        B, R = s.shape[0], s.shape[1]
+        self.k_sel = int(k_sel)
+        self.idx = torch.empty((B, R, self.k_sel), dtype=torch.int32, device=s.device)
+        self.out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
+        P = ctypes.c_void_p
+        self._fn = lib.hill_step
+        self._fn_ev = lib.hill_step_profiled
+        self._pre = (ctypes.byref(self.desc),)
+        self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
+                      P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
+                      ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        self._keep = (k, v, s)
+
+    def __call__(self, q_ptr: int, events=None):
+        if events is None:
+            st = self._fn(*self._pre, ctypes.c_void_p(q_ptr), *self._post)
+        else:
+            st = self._fn_ev(*self._pre, ctypes.c_void_p(q_ptr), *self._post, ctypes.byref(events))
+        if st != HILL_OK:
+            _check(st)
