@@ -38,16 +38,23 @@ struct Shape {
 };
 
 // Workspace regions, in this order, each 256-byte aligned:
-//   logits  ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
-//   part    ATTN [B,Hq,ntiles] float2
-//   stats   ATTN [B,Hq] float2
-//   hist    [B*R, 4096] u32
-//   apart_o [B,Hq,nsplit,D] fp32, apart_ml [B,Hq,nsplit] float2
-// The scoring and selection regions do not depend on k_sel.
+//   logits   ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
+//   part     ATTN [B,Hq,ntiles] float2;  stats ATTN [B,Hq] float2
+//   zeroed   hist1 [rows,4096] | hist2 [rows,4096] (u32; cleared by the first kernel of every call
+//            that accumulates into them)
+//   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
+//   sel_list [rows,n] i32 | sel_n [rows,nchunks] u32
+//   slots: attention partials [B,Hq,nslots,D] fp32 and [B,Hq,nslots] float2, nslots =
+//          max(nchunks, splits of the standalone attention)
+// Only the last region depends on k_sel.
 struct Layout {
-    size_t logits, part, stats, hist, apart_o, apart_ml;
+    size_t logits, part, stats;
+    size_t zero, hist1, hist2;
+    int64_t zero_words;
+    size_t cand_key, cand_n, state, sel_list, sel_n;
+    size_t slot_o, slot_ml;
     size_t end_score, end_topk, end_all;
-    int nsplit, per_split;
+    int nchunks, nsplit, per_split, nslots;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -58,6 +65,7 @@ Layout layout_for(const Shape& s, int ksel)
     size_t off = 0;
     const bool attn = s.mode == HILL_SCORE_ATTN;
     const bool raw_groups = !attn && s.gran == HILL_SEL_TOKEN && s.Hkv > 1;
+    const size_t rows = (size_t)s.B * s.R;
     L.logits = off;
     if (attn) off += align256((size_t)s.B * s.Hq * s.ld * sizeof(float));
     else if (raw_groups) off += align256((size_t)s.B * s.Hkv * s.ld * sizeof(float));
@@ -65,15 +73,31 @@ Layout layout_for(const Shape& s, int ksel)
     if (attn) off += align256((size_t)s.B * s.Hq * s.ntiles * sizeof(float2));
     L.stats = off;
     if (attn) off += align256((size_t)s.B * s.Hq * sizeof(float2));
-    L.hist = off;
-    off += align256((size_t)s.B * s.R * kHistBins * sizeof(uint32_t));
-    L.end_score = off;   // scoring uses the hist region only inside hill_step
+    L.end_score = off;
+    L.zero = off;
+    L.hist1 = off;
+    L.hist2 = L.hist1 + rows * kHistBins * sizeof(uint32_t);
+    const size_t zero_end = L.hist2 + rows * kHistBins * sizeof(uint32_t);
+    L.zero_words = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
+    off = align256(zero_end);
+    L.nchunks = (s.n + kSelChunk - 1) / kSelChunk;
+    L.cand_key = off;
+    off += align256(rows * (size_t)s.n * sizeof(uint32_t));
+    L.cand_n = off;
+    off += align256(rows * L.nchunks * sizeof(uint32_t));
+    L.state = off;
+    off += align256(rows * sizeof(uint4));
+    L.sel_list = off;
+    off += align256(rows * (size_t)s.n * sizeof(int32_t));
+    L.sel_n = off;
+    off += align256(rows * L.nchunks * sizeof(uint32_t));
     L.end_topk = off;
     L.nsplit = attn_splits((int64_t)s.B * s.Hkv, ksel, &L.per_split);
-    L.apart_o = off;
-    off += align256((size_t)s.B * s.Hq * L.nsplit * kHeadDim * sizeof(float));
-    L.apart_ml = off;
-    off += align256((size_t)s.B * s.Hq * L.nsplit * sizeof(float2));
+    L.nslots = L.nsplit > L.nchunks ? L.nsplit : L.nchunks;
+    L.slot_o = off;
+    off += align256((size_t)s.B * s.Hq * L.nslots * kHeadDim * sizeof(float));
+    L.slot_ml = off;
+    off += align256((size_t)s.B * s.Hq * L.nslots * sizeof(float2));
     L.end_all = off;
     return L;
 }
@@ -99,6 +123,8 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
         return fail(HILL_ERR_INVALID_ARG, "granularity %d is not TOKEN (0) or KVHEAD (1)", d->granularity);
     if (d->head_dim != kHeadDim)
         return fail(HILL_ERR_UNSUPPORTED, "head_dim %d is not supported (only 128)", d->head_dim);
+    if ((int64_t)d->n_tokens > (int64_t)kMaxSlots * kSelChunk)
+        return fail(HILL_ERR_UNSUPPORTED, "n_tokens %d exceeds the supported %d", d->n_tokens, kMaxSlots * kSelChunk);
     if (!std::isfinite(d->sm_scale)) return fail(HILL_ERR_INVALID_ARG, "sm_scale is not finite");
     const int64_t D = d->head_dim;
     const int64_t strides16[] = {d->q_stride_b, d->q_stride_h, d->k_stride_b, d->k_stride_h,
@@ -197,8 +223,7 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
 {
     const Stamp scan{static_cast<hipEvent_t>(ev.scan_start), static_cast<hipEvent_t>(ev.scan_stop)};
     const Stamp last{nullptr, static_cast<hipEvent_t>(ev.score_stop)};
-    uint32_t* hist = with_hist ? at<uint32_t>(ws, L.hist) : nullptr;
-    const int64_t hist_words = (int64_t)s.B * s.R * kHistBins;
+    uint32_t* hist = with_hist ? at<uint32_t>(ws, L.hist1) : nullptr;
     ScoreArgs a{};
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
@@ -218,8 +243,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.s = sacc;
     a.s_sb = d->s_stride_b;
     a.s_sr = d->s_stride_r;
-    a.zero_ptr = hist;
-    a.zero_words = with_hist ? hist_words : 0;
+    a.zero_ptr = with_hist ? at<uint32_t>(ws, L.zero) : nullptr;
+    a.zero_words = with_hist ? L.zero_words : 0;
     const int ncu = device_cus();
 
     UpdateArgs u{};
@@ -259,32 +284,40 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     return HILL_OK;
 }
 
-hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, const float* sacc, int32_t ksel,
-                       int32_t* idx, float* val, void* ws, bool hist_ready, hipStream_t st,
-                       const hill_step_events& ev)
+RefineArgs refine_args(const hill_desc* d, const Shape& s, const Layout& L, const float* sacc, int32_t ksel, void* ws)
 {
-    uint32_t* hist = at<uint32_t>(ws, L.hist);
-    if (!hist_ready) {
-        HIP_TRY(launch_fill_zero(hist, (int64_t)s.B * s.R * kHistBins, st));
-        HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, hist, st));
-    }
-    SelectArgs a{};
-    a.s = sacc;
-    a.s_sb = d->s_stride_b;
-    a.s_sr = d->s_stride_r;
-    a.R = s.R;
-    a.n = s.n;
-    a.k = ksel;
-    a.hist = hist;
-    a.idx = idx;
-    a.val = val;
-    HIP_TRY(launch_topk_select(a, s.B * s.R, st,
-                               Stamp{static_cast<hipEvent_t>(ev.select_start), static_cast<hipEvent_t>(ev.select_stop)}));
+    RefineArgs r{};
+    r.s = sacc;
+    r.s_sb = d->s_stride_b;
+    r.s_sr = d->s_stride_r;
+    r.R = s.R;
+    r.n = s.n;
+    r.k = ksel;
+    r.nchunks = L.nchunks;
+    r.hist1 = at<uint32_t>(ws, L.hist1);
+    r.hist2 = at<uint32_t>(ws, L.hist2);
+    r.cand_key = at<uint32_t>(ws, L.cand_key);
+    r.cand_n = at<uint32_t>(ws, L.cand_n);
+    r.state = at<uint4>(ws, L.state);
+    r.sel_list = at<int32_t>(ws, L.sel_list);
+    r.sel_n = at<uint32_t>(ws, L.sel_n);
+    return r;
+}
+
+// Standalone selection: clear the counters, count the first digit, refine, emit.
+hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, const float* sacc, int32_t ksel,
+                       int32_t* idx, float* val, void* ws, hipStream_t st)
+{
+    const RefineArgs r = refine_args(d, s, L, sacc, ksel, ws);
+    HIP_TRY(launch_fill_zero(at<uint32_t>(ws, L.zero), L.zero_words, st));
+    HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, at<uint32_t>(ws, L.hist1), st));
+    HIP_TRY(launch_topk_refine(r, s.B * s.R, st));
+    HIP_TRY(launch_topk_emit_indices(r, s.B * s.R, idx, val, st));
     return HILL_OK;
 }
 
-hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, const void* v,
-                     const int32_t* idx, int32_t ksel, float* out, void* ws, hipStream_t st, const hill_step_events& ev)
+AttnArgs attn_args(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, const void* v,
+                   const int32_t* idx, int32_t ksel, float* out, void* ws)
 {
     AttnArgs a{};
     a.q = static_cast<const uint16_t*>(q);
@@ -309,11 +342,18 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
     a.nsplit = L.nsplit;
     a.per_split = L.per_split;
     a.s2 = s.scale * 1.4426950408889634f;
-    a.part_o = at<float>(ws, L.apart_o);
-    a.part_ml = at<float2>(ws, L.apart_ml);
+    a.part_o = at<float>(ws, L.slot_o);
+    a.part_ml = at<float2>(ws, L.slot_ml);
     a.out = out;
+    return a;
+}
+
+hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, const void* v,
+                     const int32_t* idx, int32_t ksel, float* out, void* ws, hipStream_t st)
+{
+    const AttnArgs a = attn_args(d, s, L, q, k, v, idx, ksel, out, ws);
     HIP_TRY(launch_attn_split(a, s.dtype, st));
-    HIP_TRY(launch_attn_combine(a, st, Stamp{nullptr, static_cast<hipEvent_t>(ev.attn_stop)}));
+    HIP_TRY(launch_attn_combine(a, st));
     return HILL_OK;
 }
 
@@ -372,8 +412,7 @@ hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int
     if (val_out && ((uintptr_t)val_out & 3u)) return fail(HILL_ERR_INVALID_ARG, "val_out is not 4-byte aligned");
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_topk));
-    return run_select(d, s, L, s_acc, k_sel, idx_out, val_out, ws, false, static_cast<hipStream_t>(stream),
-                      hill_step_events{});
+    return run_select(d, s, L, s_acc, k_sel, idx_out, val_out, ws, static_cast<hipStream_t>(stream));
 }
 
 hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v, const int32_t* idx,
@@ -390,7 +429,7 @@ hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, c
     if ((uintptr_t)idx & 3u) return fail(HILL_ERR_INVALID_ARG, "idx is not 4-byte aligned");
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
-    return run_attn(d, s, L, q, k, v, idx, k_sel, out, ws, static_cast<hipStream_t>(stream), hill_step_events{});
+    return run_attn(d, s, L, q, k, v, idx, k_sel, out, ws, static_cast<hipStream_t>(stream));
 }
 
 hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc, int32_t k_sel,
@@ -419,8 +458,15 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
     const hill_step_events none{};
     const hill_step_events& e = ev ? *ev : none;
     HILL_TRY(run_score(d, s, L, q, k, s_acc, ws, true, st, e));
-    HILL_TRY(run_select(d, s, L, s_acc, k_sel, idx_out, nullptr, ws, true, st, e));
-    return run_attn(d, s, L, q, k, v, idx_out, k_sel, out, ws, st, e);
+    // selection and attention: refine the threshold, then emit the indices and
+    // attend over each chunk's picks in the same kernel
+    const RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
+    HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
+                               Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
+    const AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
+    HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
+    HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, Stamp{nullptr, static_cast<hipEvent_t>(e.attn_stop)}));
+    return HILL_OK;
 }
 
 }  // extern "C"

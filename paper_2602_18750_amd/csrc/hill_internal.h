@@ -13,6 +13,7 @@ constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kUpdChunk = 256;     // tokens per importance-update workgroup
 constexpr int kHistChunk = 2048;   // tokens per standalone histogram workgroup
+constexpr int kSelChunk = 512;     // tokens per selection chunk (256 threads x 2)
 
 enum ScoreOut : int {
     kOutLogits = 0,    // ATTN: logits [B,Hq,n] + per-tile softmax partials
@@ -47,15 +48,6 @@ struct UpdateArgs {
     uint32_t* hist;          // nullable: [B*R, kHistBins] first-digit counts
 };
 
-struct SelectArgs {
-    const float* s;
-    int64_t s_sb, s_sr;
-    int R, n, k;
-    const uint32_t* hist;    // [rows, kHistBins] first-digit counts
-    int32_t* idx;            // [rows, k]
-    float* val;              // nullable [rows, k]
-};
-
 struct AttnArgs {
     const uint16_t* q;
     const uint16_t* k;
@@ -69,6 +61,21 @@ struct AttnArgs {
     float* part_o;           // [B,Hq,nsplit,D]
     float2* part_ml;         // [B,Hq,nsplit] (max, sum) in the exp2 domain
     float* out;              // [B,Hq,D]
+};
+
+// Exact top-k over 512-token chunks of each importance row (rows = B*R).
+// Counts and lists live in the workspace.
+struct RefineArgs {
+    const float* s;
+    int64_t s_sb, s_sr;
+    int R, n, k, nchunks;
+    const uint32_t* hist1;   // [rows, kHistBins] first-digit counts (bits 31..20)
+    uint32_t* hist2;         // [rows, kHistBins] second-digit counts (bits 19..8), zeroed before
+    uint32_t* cand_key;      // [rows, n] keys inside the first-digit bin, chunk c at offset c*kSelChunk
+    uint32_t* cand_n;        // [rows, nchunks]
+    uint4* state;            // [rows] (first-digit bin, keys still needed from it, keys in it, 0)
+    int32_t* sel_list;       // [rows, n] each chunk's selected tokens in order, chunk c at c*kSelChunk
+    uint32_t* sel_n;         // [rows, nchunks]
 };
 
 // Splits of the selected set per (sequence, KV head) for the attention pass.
@@ -86,6 +93,7 @@ inline int attn_splits(int64_t b_hkv, int ksel, int* per_split)
     return (ksel + p - 1) / p;   // every split non-empty; at most target_wgs
 }
 constexpr int kMaxSplits = 512;
+constexpr int kMaxSlots = 4096;   // partial slots merged per head (splits or chunks)
 
 // Optional start/stop timestamps of one launch (hipExtLaunchKernel events).
 struct Stamp {
@@ -100,7 +108,17 @@ hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {}
 hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n,
                             uint32_t* hist, hipStream_t st, Stamp ts = {});
-hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st, Stamp ts = {});
+hipError_t launch_topk_refine(const RefineArgs& a, int rows, hipStream_t st, Stamp ts = {});
+// Selects per chunk and writes the ordered indices (and values, if val).
+hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx, float* val, hipStream_t st,
+                                    Stamp ts = {});
+// Selects per chunk and attends over each chunk's selected tokens: one
+// partial per (query head, chunk) in at.part_o / at.part_ml ([B*Hq, nchunks]
+// slots).  launch_merge_write then merges the partials into at.out and
+// writes the ordered indices.
+hipError_t launch_topk_emit_attn(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts = {});
+hipError_t launch_merge_write(const RefineArgs& r, const AttnArgs& at, int32_t* idx, int rows, hipStream_t st,
+                              Stamp ts = {});
 hipError_t launch_attn_split(const AttnArgs& a, int dtype, hipStream_t st);
 hipError_t launch_attn_combine(const AttnArgs& a, hipStream_t st, Stamp ts = {});
 

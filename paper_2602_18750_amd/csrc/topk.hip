@@ -1,32 +1,46 @@
-// Top-k token selection on gfx950 (Sec. 3.1 top-alpha; Sec. 4.2 global
-// top-alpha indices) as an exact radix select on order-preserving 32-bit keys.
+// Exact top-k token selection on gfx950 (Sec. 3.1 top-alpha; Sec. 4.2 global
+// top-alpha indices) as a radix select on order-preserving 32-bit keys, split
+// over 512-token chunks of each importance row so that every step runs on
+// many CUs -- the GPU form of the paper's chunked evaluation whose per-chunk
+// results are merged into one global threshold (Sec. 4.2, HIE).
 //
-//  topk_hist     many workgroups per row count the first 12-bit digit of the
-//                keys (also fused into the importance update).
-//  topk_select   one 1024-thread workgroup per row.  Each thread holds a
-//                contiguous 32-key segment of the row in registers (32768
-//                keys per chunk, loaded with coalesced reads and transposed
-//                through LDS; rows up to that length are read once).  The
-//                threshold key is found digit by digit (12 + 12 + 8 bits;
-//                later digits only count keys that still tie on the earlier
-//                ones), then every key above it plus the lowest-index keys
-//                equal to it are written in ascending token order, placed by
-//                one block-wide scan of (greater, equal) counts per chunk.
+//  topk_hist    first-digit (bits 31..20) histogram of every row; in hill_step
+//               the importance update counts it as it writes S.
+//  topk_refine  per chunk: finds the first-digit bin holding the k-th key,
+//               histograms the second digit (bits 19..8) of the chunk's keys
+//               inside that bin and keeps those keys in a compact candidate
+//               list.
+//  topk_emit    per chunk: resolves the exact threshold key from the row's
+//               second-digit histogram (and, when keys still tie on 24 bits,
+//               the third digit from the candidate lists), marks the chunk's
+//               selected tokens -- every key above the threshold plus, among
+//               keys equal to it, the lowest token indices that fit the
+//               budget -- and stores them in token order with their count.
+//               With attention, every 16-lane row group then attends over the
+//               selected tokens among its own 32 (fused gather + online
+//               softmax) for one KV head, and one partial per query head is
+//               written.
+//  topk_write   places each chunk's list at its ascending-order offset (the
+//               counts of the chunks before it) in the output; in hill_step
+//               this runs inside the merge of the attention partials.
 //
-// The result is exactly the k largest S with ties to the lower index: the
-// keys are integers, so no floating-point rounding is involved.
+// Cross-chunk results always pass through a kernel boundary: on this
+// multi-XCD part an agent-scope fence per workgroup (needed by a
+// last-workgroup-done merge) costs far more than a launch.  The selection is
+// exactly the k largest S with ties to the lower index: keys are integers, so
+// no floating-point rounding takes part.
 #include <hip/hip_ext.h>
 
-#include "hill_device.h"
-#include "hill_internal.h"
+#include "attn_device.h"
 
 namespace hill {
 
 namespace {
 
-constexpr int kSelThreads = 1024;
-constexpr int kSelPer = 32;                         // keys per thread per chunk
-constexpr int kSelChunk = kSelThreads * kSelPer;    // 32768 keys
+constexpr int kThreads = 256;
+constexpr int kPerThread = kSelChunk / kThreads;   // 2 consecutive tokens per thread
+static_assert(kPerThread == 2, "load_keys reads float2");
+static_assert(kSelChunk == 16 * 32, "16 row groups of 32 tokens");
 
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict__ s, int64_t s_sb, int64_t s_sr,
                                                         int R, int n, uint32_t* __restrict__ hist)
@@ -51,46 +65,42 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict_
     }
 }
 
-constexpr int kSelPitch = kSelPer + 1;             // LDS words per thread segment (bank-conflict free)
-
-// Stage chunk c of the row through LDS: coalesced 16-byte global loads, then
-// each thread takes its contiguous segment of tokens [c*kSelChunk + 32*tid, +32)
-// as order keys.  Returns how many of those tokens are inside the row.
-// Row bases are 16-byte aligned.  Every thread of the block must call this.
-__device__ __forceinline__ int load_segment(const float* srow, int c, int n, uint32_t* stage,
-                                            uint32_t (&key)[kSelPer])
+__device__ __forceinline__ const float* row_ptr(const RefineArgs& a, int row)
 {
-    const int tid = threadIdx.x;
-    const int c0 = c * kSelChunk;
-#pragma unroll
-    for (int i = 0; i < kSelPer / 4; ++i) {
-        const int pl = 4 * (i * kSelThreads + tid);     // position within the chunk
-        const int p = c0 + pl;
-        uint32_t k4[4];
-        if (p + 3 < n) {
-            const float4 x = *reinterpret_cast<const float4*>(srow + p);
-            k4[0] = order_key(x.x);
-            k4[1] = order_key(x.y);
-            k4[2] = order_key(x.z);
-            k4[3] = order_key(x.w);
-        } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e) k4[e] = p + e < n ? order_key(srow[p + e]) : 0u;
-        }
-        uint32_t* dst = stage + (pl / kSelPer) * kSelPitch + (pl % kSelPer);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) dst[e] = k4[e];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < kSelPer; ++i) key[i] = stage[tid * kSelPitch + i];
-    __syncthreads();
-    return min(max(n - (c0 + tid * kSelPer), 0), kSelPer);
+    const int b = row / a.R, r = row % a.R;
+    return a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
 }
 
-// Given a histogram of `nb` bins (nb in {256, 4096}) in LDS, find the bin
-// holding the need-th largest key: the largest d with count(bins >= d) >= need.
-// Writes the bin and count(bins > d) to res[0], res[1].
+// Keys of this thread's 2 consecutive tokens of chunk c (row bases 16-byte aligned).
+__device__ __forceinline__ void load_keys(const float* srow, int c, int n, uint32_t (&key)[kPerThread],
+                                          bool (&ok)[kPerThread])
+{
+    const int j = c * kSelChunk + threadIdx.x * kPerThread;
+    if (j + kPerThread <= n) {
+        const float2 x = *reinterpret_cast<const float2*>(srow + j);
+        key[0] = order_key(x.x);
+        key[1] = order_key(x.y);
+        ok[0] = ok[1] = true;
+    } else {
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e) {
+            ok[e] = j + e < n;
+            key[e] = ok[e] ? order_key(srow[j + e]) : 0u;
+        }
+    }
+}
+
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
+{
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+
+// Histogram of `nb` bins in LDS: the bin holding the need-th largest key,
+// i.e. the largest d with count(bins >= d) >= need.  res[0] = d,
+// res[1] = count(bins > d).  Every thread of the NT-thread block must call this.
+template <int NT>
 __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* scan_scratch, uint32_t* res)
 {
     const int tid = threadIdx.x;
@@ -98,15 +108,15 @@ __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* 
         res[0] = 0u;
         res[1] = 0u;
     }
-    const int per = nb / kSelThreads > 0 ? nb / kSelThreads : 1;
-    const int nthreads = nb / per;
+    const int per = nb >= NT ? nb / NT : 1;
+    const int nt = nb / per;
     // thread t owns bins [nb - (t+1)*per, nb - t*per), visited from the top
     uint32_t local = 0;
-    if (tid < nthreads)
+    if (tid < nt)
         for (int i = 0; i < per; ++i) local += hist[nb - 1 - (tid * per + i)];
     uint32_t total;
-    const uint32_t before = block_excl_scan<kSelThreads>(local, scan_scratch, &total);
-    if (tid < nthreads && before < need && before + local >= need) {
+    const uint32_t before = block_excl_scan<NT>(local, scan_scratch, &total);
+    if (tid < nt && before < need && before + local >= need) {
         uint32_t c = before;
         for (int i = 0; i < per; ++i) {
             const int bin = nb - 1 - (tid * per + i);
@@ -122,93 +132,271 @@ __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* 
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kSelThreads) void topk_select_kernel(SelectArgs a)
+__global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
 {
-    __shared__ uint32_t stage[kSelThreads * kSelPitch];
     __shared__ uint32_t hist[kHistBins];
-    __shared__ uint32_t scan_scratch[kSelThreads / 64 + 1];
-    __shared__ uint2 scan2_scratch[kSelThreads / 64 + 1];
+    __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t res[2];
+    __shared__ uint32_t n_cand;
 
-    const int tid = threadIdx.x;
-    const int row = blockIdx.x;
-    const int b = row / a.R, r = row % a.R;
-    const float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
-    const int n = a.n;
-    const int nchunks = (n + kSelChunk - 1) / kSelChunk;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int c = blockIdx.x, row = blockIdx.y;
+    const float* srow = row_ptr(a, row);
 
-    uint32_t key[kSelPer];
-    int valid = 0;
-    if (nchunks == 1) valid = load_segment(srow, 0, n, stage, key);
-
-    // digit 1 (bits 31..20): counts come from the multi-workgroup histogram
-    const uint32_t* gh = a.hist + (int64_t)row * kHistBins;
-    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = gh[i];
+    // the chunk's keys and the row's first-digit histogram are loaded together
+    uint32_t key[kPerThread];
+    bool ok[kPerThread];
+    load_keys(srow, c, a.n, key, ok);
+    const uint32_t* h1 = a.hist1 + (int64_t)row * kHistBins;
+    uint32_t hv[kHistBins / kThreads];
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) hv[i] = h1[i * kThreads + tid];
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) hist[i * kThreads + tid] = hv[i];
+    if (tid == 0) n_cand = 0u;
     __syncthreads();
-    uint32_t need = (uint32_t)a.k;
-    find_bin(hist, kHistBins, need, scan_scratch, res);
-    uint32_t prefix = res[0] & (kHistBins - 1);
+    // first digit: the bin of the k-th key
+    find_bin<kThreads>(hist, kHistBins, (uint32_t)a.k, scan_scratch, res);
+    const uint32_t b1 = res[0] & (kHistBins - 1);
+    const uint32_t need1 = (uint32_t)a.k - res[1];
+    const uint32_t in1 = hist[b1];
+    const bool refine = need1 < in1;
+    if (c == 0 && tid == 0) a.state[row] = make_uint4(b1, need1, in1, 0u);
+    __syncthreads();
+
+    for (int i = tid; i < kHistBins; i += kThreads) hist[i] = 0u;
+    __syncthreads();
+    // keys inside the bin are the candidates: their second digit is
+    // histogrammed and they are appended (wave-compacted) to the chunk's
+    // candidate list, whose order does not matter
+    uint32_t* cand = a.cand_key + (int64_t)row * a.n + (int64_t)c * kSelChunk;
+#pragma unroll
+    for (int e = 0; e < kPerThread; ++e) {
+        const bool is_c = ok[e] && (key[e] >> 20) == b1;
+        if (is_c && refine) atomicAdd(&hist[(key[e] >> 8) & (kHistBins - 1)], 1u);
+        const uint64_t mask = __ballot(is_c);
+        if (mask) {
+            const int leader = __ffsll((unsigned long long)mask) - 1;
+            uint32_t base = 0;
+            if (lane == leader) base = atomicAdd(&n_cand, (uint32_t)__popcll(mask));
+            base = __shfl(base, leader, 64);
+            if (is_c) cand[base + __popcll(mask & ((1ull << lane) - 1ull))] = key[e];
+        }
+    }
+    __syncthreads();
+    if (refine) {
+        uint32_t* h2 = a.hist2 + (int64_t)row * kHistBins;
+        for (int i = tid; i < kHistBins; i += kThreads) {
+            const uint32_t v = hist[i];
+            if (v) atomicAdd(h2 + i, v);
+        }
+    }
+    if (tid == 0) a.cand_n[(int64_t)row * a.nchunks + c] = n_cand;
+}
+
+// Calls f(key) for every candidate of chunks [c0, c1) of a row, all threads
+// of the block in parallel (one chunk list per wave pass).
+template <typename F>
+__device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int c0, int c1, F f)
+{
+    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const uint32_t* cn = a.cand_n + (int64_t)row * a.nchunks;
+    const uint32_t* cl = a.cand_key + (int64_t)row * a.n;
+    for (int cc = c0 + w; cc < c1; cc += kThreads / 64) {
+        const uint32_t m = cn[cc];
+        for (uint32_t i = lane; i < m; i += 64) f(cl[(int64_t)cc * kSelChunk + i]);
+    }
+}
+
+template <int DT, int GC, bool ATTN>
+__global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnArgs at)
+{
+    __shared__ uint32_t hist[kHistBins];
+    __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
+    __shared__ uint32_t red[kThreads / 64];
+    __shared__ uint32_t res[2];
+    __shared__ AttnLds<ATTN ? GC : 1> sh;
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int c = blockIdx.x;
+    int row, b = 0, g = 0;
+    if constexpr (ATTN) {
+        b = blockIdx.y / at.Hkv;
+        g = blockIdx.y % at.Hkv;
+        row = r.R == 1 ? b : blockIdx.y;
+    } else {
+        row = blockIdx.y;
+    }
+    // one workgroup per chunk stores the list (token rows: KV head 0)
+    const bool writer = !ATTN || r.R != 1 || g == 0;
+
+    // independent loads first: queries, this chunk's keys, the row's state and histogram
+    uint4 qv[ATTN ? GC : 1];
+    if constexpr (ATTN) load_queries<GC>(at, b, g, 0, qv);
+    uint32_t key[kPerThread];
+    bool ok[kPerThread];
+    load_keys(row_ptr(r, row), c, r.n, key, ok);
+    const uint4 s1 = r.state[row];
+    const uint32_t b1 = s1.x, need1 = s1.y, in1 = s1.z;
+    const uint32_t* h2 = r.hist2 + (int64_t)row * kHistBins;
+    uint32_t hv[kHistBins / kThreads];
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) hv[i] = need1 < in1 ? h2[i * kThreads + tid] : 0u;
+
+    // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
+    uint32_t prefix = b1, need = need1;
     int shift = 20;
-    need -= res[1];
-    uint32_t in_bin = hist[prefix];
-
-    // digits 2 (bits 19..8) and 3 (bits 7..0), only while the threshold bin is split
-    for (int pass = 0; pass < 2 && need < in_bin; ++pass) {
-        const int nb = pass == 0 ? kHistBins : 256;
-        const int next_shift = pass == 0 ? 8 : 0;
-        __syncthreads();
-        for (int i = tid; i < nb; i += kSelThreads) hist[i] = 0u;
-        __syncthreads();
-        for (int c = 0; c < nchunks; ++c) {
-            if (nchunks > 1) valid = load_segment(srow, c, n, stage, key);
+    bool all_eq = need1 == in1;
+    if (!all_eq) {
 #pragma unroll
-            for (int i = 0; i < kSelPer; ++i)
-                if (i < valid && (key[i] >> shift) == prefix)
-                    atomicAdd(&hist[(key[i] >> next_shift) & (uint32_t)(nb - 1)], 1u);
-        }
+        for (int i = 0; i < kHistBins / kThreads; ++i) hist[i * kThreads + tid] = hv[i];
         __syncthreads();
-        find_bin(hist, nb, need, scan_scratch, res);
-        const uint32_t d = res[0] & (uint32_t)(nb - 1);
-        need -= res[1];
-        in_bin = hist[d];
-        prefix = (prefix << (shift - next_shift)) | d;
-        shift = next_shift;
+        find_bin<kThreads>(hist, kHistBins, need1, scan_scratch, res);
+        const uint32_t b2 = res[0] & (kHistBins - 1);
+        const uint32_t need2 = need1 - res[1];
+        const uint32_t in2 = hist[b2];
+        prefix = (b1 << 12) | b2;
+        shift = 8;
+        need = need2;
+        all_eq = need2 == in2;
+        __syncthreads();
+        if (!all_eq) {   // third digit (bits 7..0) from the candidate lists
+            for (int i = tid; i < 256; i += kThreads) hist[i] = 0u;
+            __syncthreads();
+            const uint32_t p2 = prefix;
+            for_candidates(r, row, 0, r.nchunks, [p2](uint32_t kk) {
+                if ((kk >> 8) == p2) atomicAdd(&hist[kk & 0xffu], 1u);
+            });
+            __syncthreads();
+            find_bin<kThreads>(hist, 256, need2, scan_scratch, res);
+            const uint32_t b3 = res[0] & 0xffu;
+            prefix = (p2 << 8) | b3;
+            shift = 0;
+            need = need2 - res[1];
+            all_eq = need == hist[b3];
+            __syncthreads();
+        }
     }
-    // Selection rule: (key >> shift) > prefix, or == prefix and among the
-    // first `need` such keys in token order.
 
-    int32_t* out_idx = a.idx + (int64_t)row * a.k;
-    float* out_val = a.val ? a.val + (int64_t)row * a.k : nullptr;
-    uint32_t carry_gt = 0, carry_eq = 0;
-    for (int c = 0; c < nchunks; ++c) {
-        if (nchunks > 1) valid = load_segment(srow, c, n, stage, key);
-        uint32_t gtm = 0u, eqm = 0u;   // bit i: token 32*tid + i is above / at the threshold
+    bool gt[kPerThread], eq[kPerThread], sel[kPerThread];
+    uint32_t neq = 0;
 #pragma unroll
-        for (int i = 0; i < kSelPer; ++i) {
-            const uint32_t kd = key[i] >> shift;
-            gtm |= (i < valid && kd > prefix) ? (1u << i) : 0u;
-            eqm |= (i < valid && kd == prefix) ? (1u << i) : 0u;
-        }
-        uint2 total;
-        const uint2 before = block_excl_scan2<kSelThreads>(
-            make_uint2((uint32_t)__builtin_popcount(gtm), (uint32_t)__builtin_popcount(eqm)), scan2_scratch, &total);
-        const int j0 = c * kSelChunk + tid * kSelPer;
-        for (uint32_t m = gtm | eqm; m; m &= m - 1u) {
-            const int i = __builtin_ctz(m);
-            const uint32_t below = (1u << i) - 1u;
-            const uint32_t gt_b = carry_gt + before.x + (uint32_t)__builtin_popcount(gtm & below);
-            const uint32_t eq_b = carry_eq + before.y + (uint32_t)__builtin_popcount(eqm & below);
-            if (((gtm >> i) & 1u) || eq_b < need) {
-                const uint32_t pos = gt_b + (eq_b < need ? eq_b : need);
-                if (pos < (uint32_t)a.k) {
-                    out_idx[pos] = j0 + i;
-                    if (out_val) out_val[pos] = srow[j0 + i];
-                }
-            }
-        }
-        carry_gt += total.x;
-        carry_eq += total.y;
+    for (int e = 0; e < kPerThread; ++e) {
+        const uint32_t kd = key[e] >> shift;
+        gt[e] = ok[e] && kd > prefix;
+        eq[e] = ok[e] && kd == prefix;
+        neq += eq[e];
     }
+    if (all_eq) {
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e) sel[e] = gt[e] || eq[e];
+    } else {
+        // the budget cuts through keys equal to the threshold: rank them by
+        // token index (equal keys in the chunks before, then in this chunk)
+        uint32_t before_chunks = 0;
+        const uint32_t pf = prefix;
+        for_candidates(r, row, 0, c, [&before_chunks, pf](uint32_t kk) { before_chunks += kk == pf; });
+        before_chunks = wave_sum_u32(before_chunks);
+        if (lane == 0) red[tid >> 6] = before_chunks;
+        __syncthreads();
+        uint32_t eq_rank = 0;
+        for (int i = 0; i < kThreads / 64; ++i) eq_rank += red[i];
+        uint32_t tot;
+        eq_rank += block_excl_scan<kThreads>(neq, scan_scratch, &tot);
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e) {
+            sel[e] = gt[e] || (eq[e] && eq_rank < need);
+            eq_rank += eq[e];
+        }
+    }
+
+    // the chunk's selected tokens in token order, and their count
+    const uint32_t nsel = (uint32_t)sel[0] + (uint32_t)sel[1];
+    uint32_t tot;
+    const uint32_t pos = block_excl_scan<kThreads>(nsel, scan_scratch, &tot);
+    if (writer) {
+        int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
+        const int j0 = c * kSelChunk + tid * kPerThread;
+        uint32_t p = pos;
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e)
+            if (sel[e]) list[p++] = j0 + e;
+        if (tid == 0) r.sel_n[(int64_t)row * r.nchunks + c] = tot;
+    }
+
+    if constexpr (ATTN) {
+        // row group rg owns tokens [32*rg, 32*rg + 32) of the chunk: both
+        // tokens of each of its 16 lanes
+        const int rg = tid >> 4;
+        const uint64_t m0 = __ballot(sel[0]), m1 = __ballot(sel[1]);
+        const int sh16 = (rg & 3) * 16;
+        const uint32_t a0 = (uint32_t)(m0 >> sh16) & 0xffffu, a1 = (uint32_t)(m1 >> sh16) & 0xffffu;
+        uint32_t mask = 0;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mask |= (((a0 >> i) & 1u) << (2 * i)) | (((a1 >> i) & 1u) << (2 * i + 1));
+        const int jbase = c * kSelChunk + rg * 32;
+        for (int hc = 0; hc < at.G; hc += GC) {
+            if (hc) load_queries<GC>(at, b, g, hc, qv);
+            attend_masked<DT, GC>(at, b, g, hc, qv, jbase, mask, c, r.nchunks, sh);
+        }
+    }
+}
+
+// Copies the list of chunk c of a row to the output at its ascending-order
+// offset (the selected counts of the chunks before it).
+__device__ __forceinline__ void write_chunk(const RefineArgs& r, int row, int c, int32_t* idx, float* val,
+                                            uint32_t* red)
+{
+    const int tid = threadIdx.x, lane = tid & 63;
+    const uint32_t* sn = r.sel_n + (int64_t)row * r.nchunks;
+    uint32_t before = 0;
+    for (int cc = tid; cc < c; cc += kThreads) before += sn[cc];
+    before = wave_sum_u32(before);
+    if (lane == 0) red[tid >> 6] = before;
+    __syncthreads();
+    uint32_t base = 0;
+    for (int i = 0; i < kThreads / 64; ++i) base += red[i];
+    const uint32_t m = sn[c];
+    const int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
+    const float* srow = row_ptr(r, row);
+    for (uint32_t i = tid; i < m; i += kThreads) {
+        const uint32_t p = base + i;
+        if (p < (uint32_t)r.k) {
+            const int32_t j = list[i];
+            idx[(int64_t)row * r.k + p] = j;
+            if (val) val[(int64_t)row * r.k + p] = srow[j];
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void topk_write_kernel(RefineArgs r, int32_t* idx, float* val)
+{
+    __shared__ uint32_t red[kThreads / 64];
+    write_chunk(r, blockIdx.y, blockIdx.x, idx, val, red);
+}
+
+// hill_step's last kernel: workgroups [0, B*Hq) merge the chunk partials of one
+// query head each; the rest copy one chunk list each into the index output.
+__global__ __launch_bounds__(kThreads) void merge_write_kernel(RefineArgs r, AttnArgs at, int32_t* idx)
+{
+    __shared__ float wsl[kMaxSlots];
+    __shared__ float red[kThreads / 64 + 1];
+    __shared__ float osum[kThreads];
+    __shared__ uint32_t ured[kThreads / 64];
+    const int nheads = at.B * at.Hq;
+    if ((int)blockIdx.x < nheads) {
+        merge_head<kThreads>(at, blockIdx.x / at.Hq, blockIdx.x % at.Hq, r.nchunks, wsl, red, osum);
+    } else {
+        const int t = blockIdx.x - nheads;
+        write_chunk(r, t / r.nchunks, t % r.nchunks, idx, nullptr, ured);
+    }
+}
+
+template <int DT, int GC>
+void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
+{
+    dim3 grid(r.nchunks, at.B * at.Hkv);
+    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at);
 }
 
 }  // namespace
@@ -221,9 +409,48 @@ hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, i
     return hipGetLastError();
 }
 
-hipError_t launch_topk_select(const SelectArgs& a, int rows, hipStream_t st, Stamp ts)
+hipError_t launch_topk_refine(const RefineArgs& a, int rows, hipStream_t st, Stamp ts)
 {
-    hipExtLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, ts.start, ts.stop, 0, a);
+    dim3 grid(a.nchunks, rows);
+    hipExtLaunchKernelGGL(topk_refine_kernel, grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx, float* val, hipStream_t st, Stamp ts)
+{
+    dim3 grid(r.nchunks, rows);
+    hipExtLaunchKernelGGL((topk_emit_kernel<0, 1, false>), grid, dim3(kThreads), 0, st, ts.start, nullptr, 0, r,
+                          AttnArgs{});
+    hipExtLaunchKernelGGL(topk_write_kernel, grid, dim3(kThreads), 0, st, nullptr, ts.stop, 0, r, idx, val);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_emit_attn(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
+{
+    const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
+    if (dtype == 1) {
+        switch (gc) {
+        case 8: emit_attn_launch<1, 8>(r, at, st, ts); break;
+        case 4: emit_attn_launch<1, 4>(r, at, st, ts); break;
+        case 2: emit_attn_launch<1, 2>(r, at, st, ts); break;
+        default: emit_attn_launch<1, 1>(r, at, st, ts); break;
+        }
+    } else {
+        switch (gc) {
+        case 8: emit_attn_launch<0, 8>(r, at, st, ts); break;
+        case 4: emit_attn_launch<0, 4>(r, at, st, ts); break;
+        case 2: emit_attn_launch<0, 2>(r, at, st, ts); break;
+        default: emit_attn_launch<0, 1>(r, at, st, ts); break;
+        }
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_write(const RefineArgs& r, const AttnArgs& at, int32_t* idx, int rows, hipStream_t st,
+                              Stamp ts)
+{
+    const int blocks = at.B * at.Hq + rows * r.nchunks;
+    hipExtLaunchKernelGGL(merge_write_kernel, dim3(blocks), dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at, idx);
     return hipGetLastError();
 }
 
