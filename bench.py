@@ -25,7 +25,8 @@ Prints one JSON line:
 
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
 ``--copy-calib`` (plain copy of known size, for counter calibration),
-``--summarize DIR`` (condense rocprofv3 output under DIR into text).
+``--summarize DIR`` (condense rocprofv3 output under DIR into text),
+``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs).
 """
 from __future__ import annotations
 
@@ -316,8 +317,10 @@ def run_sweep(args):
 
 
 def run_copy_calib(args):
-    """A plain device copy of known size (counter calibration: FETCH_SIZE and
-    WRITE_SIZE of this copy are compared with its 1 GiB read and write)."""
+    """A plain elementwise copy of known size (counter calibration): 1 GiB
+    read and 1 GiB written by one kernel (bitwise_not of uint8), three times.
+    FETCH_SIZE and WRITE_SIZE of these dispatches against their known bytes
+    give the factors that turn the counters into HBM bytes."""
     import torch
     n = 1 << 30
     a = torch.empty(n, dtype=torch.uint8, device="cuda:0")
@@ -325,9 +328,57 @@ def run_copy_calib(args):
     a.fill_(1)
     torch.cuda.synchronize()
     for _ in range(3):
-        b.copy_(a)
+        torch.bitwise_not(a, out=b)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes": n, "repeats": 3}), flush=True)
+
+
+def _counter_rows(directory: str, counter: str, name_part: str):
+    """Per-dispatch values of `counter` for kernels whose name contains name_part."""
+    import csv
+    vals = []
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
+        with open(path) as f:
+            per = {}
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name") != counter or name_part not in r.get("Kernel_Name", ""):
+                    continue
+                key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+                per[key] = per.get(key, 0.0) + float(r.get("Counter_Value", 0))
+            vals.extend(per.values())
+    return vals
+
+
+def make_counters(directory: str, command: str):
+    """Writes the score_tiles HBM-traffic record from four rocprofv3 --pmc runs
+    under `directory`: fetch/ and write/ (FETCH_SIZE, WRITE_SIZE of the bench),
+    calib_fetch/ and calib_write/ (the same counters of --copy-calib)."""
+    def mean(xs):
+        if not xs:
+            raise SystemExit("no dispatches found under %s" % directory)
+        return sum(xs) / len(xs)
+
+    copy_bytes = 1 << 30
+    f_kib = mean(_counter_rows(os.path.join(directory, "fetch"), "FETCH_SIZE", "score_tiles"))
+    w_kib = mean(_counter_rows(os.path.join(directory, "write"), "WRITE_SIZE", "score_tiles"))
+    cf_kib = mean(_counter_rows(os.path.join(directory, "calib_fetch"), "FETCH_SIZE", "bitwise_not"))
+    cw_kib = mean(_counter_rows(os.path.join(directory, "calib_write"), "WRITE_SIZE", "bitwise_not"))
+    ff = copy_bytes / (cf_kib * 1024.0)
+    wf = copy_bytes / (cw_kib * 1024.0)
+    rec = {
+        "kernel": "score_tiles",
+        "source_sha256": hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest(),
+        "fetch_kib_per_dispatch": round(f_kib, 1),
+        "write_kib_per_dispatch": round(w_kib, 1),
+        "copy_bytes": copy_bytes,
+        "copy_fetch_kib": round(cf_kib, 1),
+        "copy_write_kib": round(cw_kib, 1),
+        "fetch_factor": round(ff, 4),
+        "write_factor": round(wf, 4),
+        "hbm_bytes_per_launch": int(round(f_kib * 1024.0 * ff + w_kib * 1024.0 * wf)),
+        "command": command,
+    }
+    print(json.dumps(rec, indent=1))
 
 
 # -------------------------------------------------------- profile summary --
@@ -384,7 +435,13 @@ def main():
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")
     ap.add_argument("--summarize", metavar="DIR")
+    ap.add_argument("--counters", metavar="DIR", help="write the score_tiles traffic record from --pmc runs under DIR")
+    ap.add_argument("--counters-command", default="", help="command line recorded with --counters")
     args = ap.parse_args()
+
+    if args.counters:
+        make_counters(args.counters, args.counters_command)
+        return 0
 
     if args.summarize:
         summarize(args.summarize)
