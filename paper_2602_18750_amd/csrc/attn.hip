@@ -28,7 +28,16 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a)
     for (int hc = 0; hc < a.G; hc += GC) {
         uint4 qv[GC];
         load_queries<GC>(a, b, g, hc, qv);
-        attend_partial<DT, GC>(a, b, g, hc, qv, t0, t1, [I](int t) { return I[t]; }, split, a.nsplit, sh);
+        AttnAcc<GC> acc;
+        attn_begin<GC>(acc, sh);
+        for (int tb = t0; tb < t1; tb += kAttnBlock) {
+            const int cnt = min(kAttnBlock, t1 - tb);
+            __syncthreads();   // the previous block's list reads are done
+            for (int i = threadIdx.x; i < cnt; i += 256) sh.tok[i] = I[tb + i];
+            __syncthreads();
+            attn_block<DT, GC>(a, b, g, qv, cnt, acc, sh);
+        }
+        attn_finish<GC>(a, b, g, hc, acc, split, a.nsplit, sh);
     }
 }
 

@@ -3,14 +3,22 @@
 // shared by the standalone split-K kernel and the fused select+attend kernel.
 //
 // A 256-thread workgroup handles one (sequence b, KV head g) and GC query
-// heads of its group over a list of selected tokens.  Sixteen 16-lane row
-// groups each take every 16th token of the list: lane l16 loads elements
-// [8*l16, 8*l16+8) of the token's K and V rows (16-byte loads, read in place
-// from the cache), the dot products are summed by four DPP adds, and each
-// row group keeps an online softmax (running max m, sum l, and 8 of the 128
-// output dims per lane) per head.  The 16 row groups are then merged in LDS
-// and one partial (m, l, o[D]) per head is written to a slot of the partial
-// buffer; partials of all slots are merged by merge_head().
+// heads of its group over a list of selected tokens, in blocks of at most
+// kAttnBlock list entries held in LDS:
+//   A  logits: sixteen 16-lane row groups take every 16th entry; lane l16
+//      loads elements [8*l16, 8*l16+8) of the token's K row (16-byte loads,
+//      read in place from the cache) and four DPP adds finish each dot
+//      product.  The logits of the block go to LDS.
+//   B  softmax: one wave per head takes the block maximum, folds it into the
+//      head's running maximum and turns the logits into exp2 weights (one
+//      exp2 per head and token) and their sum.
+//   C  values: wave w takes entries w, w+4, ...; lane l reads elements
+//      (2l, 2l+1) of the V row (one 4-byte load per lane: a whole 256-byte
+//      row per wave instruction) and accumulates weight * V for every head.
+//      The V loads of the first batch are issued before phase A.
+// The four waves' outputs are added in LDS at the end, and one partial
+// (m, l, o[D]) per head is written to a slot of the partial buffer; partials
+// of all slots are merged by merge_head().
 #pragma once
 
 #include "hill_device.h"
@@ -18,16 +26,19 @@
 
 namespace hill {
 
-constexpr int kTokBatch = 4;   // tokens per row group whose rows are loaded together
+constexpr int kAttnBlock = 512;   // list entries per LDS block
+constexpr int kKBatch = 8;        // K rows in flight per row group (phase A)
+constexpr int kVBatch = 16;       // V rows in flight per wave (phase C)
 
 template <int GC>
 struct AttnLds {
-    float m[16][GC];
-    float l[16][GC];
-    float o[16][GC][kHeadDim];
+    int32_t tok[kAttnBlock];          // token index of each entry of the block
+    float p[kAttnBlock][GC];          // logits, then exp2 weights
+    float mrun[GC], lrun[GC], alpha[GC];
+    float o[4][GC][kHeadDim];         // per-wave outputs, added at the end
 };
 
-// This lane's 8 query elements of heads g*G+hc .. +GC.
+// This lane's 8 query elements of heads g*G+hc .. +GC (16-lane row layout).
 template <int GC>
 __device__ __forceinline__ void load_queries(const AttnArgs& a, int b, int g, int hc, uint4 (&qv)[GC])
 {
@@ -39,173 +50,190 @@ __device__ __forceinline__ void load_queries(const AttnArgs& a, int b, int g, in
     }
 }
 
-// Merges the 16 row groups' online-softmax states (m, l, o) in LDS and writes
-// one partial (m, l, o[D]) per head to slot `slot` of `nslots`.
+// Running state of one workgroup's attention: this lane's two output
+// elements (2*lane, 2*lane+1) per head, summed over its wave's entries.
 template <int GC>
-__device__ __forceinline__ void merge_row_groups(const AttnArgs& a, int b, int g, int hc, const float (&m)[GC],
-                                                 const float (&l)[GC], const float (&o)[GC][8], int slot, int nslots,
-                                                 AttnLds<GC>& sh)
+struct AttnAcc {
+    float o[GC][2];
+};
+
+template <int GC>
+__device__ __forceinline__ void attn_begin(AttnAcc<GC>& acc, AttnLds<GC>& sh)
 {
-    const int tid = threadIdx.x;
+#pragma unroll
+    for (int hh = 0; hh < GC; ++hh) acc.o[hh][0] = acc.o[hh][1] = 0.0f;
+    if (threadIdx.x < GC) {
+        sh.mrun[threadIdx.x] = -INFINITY;
+        sh.lrun[threadIdx.x] = 0.0f;
+    }
+}
+
+// This lane's V element pair of token j, clamped into [0, n) so that a bad
+// index reads a valid row instead of faulting (lists hold valid tokens).
+__device__ __forceinline__ uint32_t load_v2(const AttnArgs& a, const uint16_t* vb, int j)
+{
+    j = min(max(j, 0), a.n - 1);
+    return *reinterpret_cast<const uint32_t*>(vb + (int64_t)j * a.v_sn);
+}
+
+// Folds list entries [0, cnt) of sh.tok (1 <= cnt <= kAttnBlock, written and
+// made visible by a barrier before the call) into the running state.  Every
+// thread of the workgroup must call this; it ends with the block's LDS
+// reads done only after a barrier of the next call or of attn_finish.
+template <int DT, int GC>
+__device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, const uint4 (&qv)[GC], int cnt,
+                                           AttnAcc<GC>& acc, AttnLds<GC>& sh)
+{
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int rg = tid >> 4, l16 = tid & 15;
+    const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
+    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
+
+    // first V batch of this wave, in flight during phase A
+    uint32_t vr[kVBatch];
 #pragma unroll
-    for (int hh = 0; hh < GC; ++hh) {
+    for (int i = 0; i < kVBatch; ++i) {
+        const int t = w + 4 * i;
+        vr[i] = t < cnt ? load_v2(a, vb, sh.tok[t]) : 0u;
+    }
+
+    // A: logits of every entry, into sh.p
+    for (int t0 = rg; t0 < cnt; t0 += 16 * kKBatch) {
+        uint4 kr[kKBatch];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) sh.o[rg][hh][l16 * 8 + i] = o[hh][i];
-        if (l16 == 0) {
-            sh.m[rg][hh] = m[hh];
-            sh.l[rg][hh] = l[hh];
+        for (int u = 0; u < kKBatch; ++u) {
+            const int t = min(t0 + 16 * u, cnt - 1);
+            const int64_t j = min(max(sh.tok[t], 0), a.n - 1);
+            kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
+        }
+#pragma unroll
+        for (int u = 0; u < kKBatch; ++u) {
+            const int t = t0 + 16 * u;
+            if (t >= cnt) break;   // uniform within the row group
+            float mine = 0.0f;     // lane l16 == hh keeps head hh's dot product
+#pragma unroll
+            for (int hh = 0; hh < GC; ++hh) {
+                const float d = sum16(dot8<DT>(kr[u], qv[hh]));
+                mine = l16 == hh ? d : mine;
+            }
+            if (l16 < GC) sh.p[t][l16] = a.s2 * mine;
         }
     }
+    __syncthreads();
+
+    // B: per head, block maximum -> running maximum, weights and their sum
+    for (int hh = w; hh < GC; hh += 4) {
+        float mx = -INFINITY;
+        for (int t = lane; t < cnt; t += 64) mx = fmaxf(mx, sh.p[t][hh]);
+        mx = wave_max(mx);
+        const float m_old = sh.mrun[hh];
+        const float m_new = fmaxf(m_old, mx);
+        float ls = 0.0f;
+        for (int t = lane; t < cnt; t += 64) {
+            const float e = exp2f(sh.p[t][hh] - m_new);
+            sh.p[t][hh] = e;
+            ls += e;
+        }
+        ls = wave_sum(ls);
+        if (lane == 0) {
+            const float al = m_old == -INFINITY ? 0.0f : exp2f(m_old - m_new);
+            sh.alpha[hh] = al;
+            sh.lrun[hh] = sh.lrun[hh] * al + ls;
+            sh.mrun[hh] = m_new;
+        }
+    }
+    __syncthreads();
+
+    // C: weight * V over this wave's entries
+#pragma unroll
+    for (int hh = 0; hh < GC; ++hh) {
+        const float al = sh.alpha[hh];
+        acc.o[hh][0] *= al;
+        acc.o[hh][1] *= al;
+    }
+    for (int i0 = 0;; i0 += kVBatch) {
+#pragma unroll
+        for (int i = 0; i < kVBatch; ++i) {
+            const int t = w + 4 * (i0 + i);
+            if (t >= cnt) break;   // uniform within the wave
+            float v0, v1;
+            widen2<DT>(vr[i], v0, v1);
+            float pw[GC];
+            if constexpr (GC % 4 == 0) {
+#pragma unroll
+                for (int h4 = 0; h4 < GC; h4 += 4) {
+                    const float4 x = *reinterpret_cast<const float4*>(&sh.p[t][h4]);
+                    pw[h4] = x.x;
+                    pw[h4 + 1] = x.y;
+                    pw[h4 + 2] = x.z;
+                    pw[h4 + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int hh = 0; hh < GC; ++hh) pw[hh] = sh.p[t][hh];
+            }
+#pragma unroll
+            for (int hh = 0; hh < GC; ++hh) {
+                acc.o[hh][0] += pw[hh] * v0;
+                acc.o[hh][1] += pw[hh] * v1;
+            }
+        }
+        if (w + 4 * (i0 + kVBatch) >= cnt) break;
+#pragma unroll
+        for (int i = 0; i < kVBatch; ++i) {
+            const int t = w + 4 * (i0 + kVBatch + i);
+            vr[i] = t < cnt ? load_v2(a, vb, sh.tok[t]) : 0u;
+        }
+    }
+}
+
+// Adds the four waves' outputs and writes the partial (m, l, o[D]) of heads
+// g*G+hc .. +GC to slot `slot` of `nslots`.  An empty list gives m = -inf,
+// l = 0, o = 0 (weight 0 in the merge).  Every thread must call this.
+template <int GC>
+__device__ __forceinline__ void attn_finish(const AttnArgs& a, int b, int g, int hc, const AttnAcc<GC>& acc, int slot,
+                                            int nslots, AttnLds<GC>& sh)
+{
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll
+    for (int hh = 0; hh < GC; ++hh)
+        *reinterpret_cast<float2*>(&sh.o[w][hh][2 * lane]) = make_float2(acc.o[hh][0], acc.o[hh][1]);
     __syncthreads();
     for (int e = tid; e < GC * kHeadDim; e += 256) {
         const int hh = e / kHeadDim, d = e % kHeadDim;
-        float mx = -INFINITY;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) mx = fmaxf(mx, sh.m[q][hh]);
-        float accl = 0.0f, acco = 0.0f;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const float w = sh.l[q][hh] > 0.0f ? exp2f(sh.m[q][hh] - mx) : 0.0f;
-            accl += w * sh.l[q][hh];
-            acco += w * sh.o[q][hh][d];
-        }
-        const int h = g * a.G + hc + hh;
-        const int64_t pi = ((int64_t)b * a.Hq + h) * nslots + slot;
-        a.part_o[pi * kHeadDim + d] = acco;
-        if (d == 0) a.part_ml[pi] = make_float2(mx, accl);
+        const float o = ((sh.o[0][hh][d] + sh.o[1][hh][d]) + sh.o[2][hh][d]) + sh.o[3][hh][d];
+        const int64_t pi = ((int64_t)b * a.Hq + g * a.G + hc + hh) * nslots + slot;
+        a.part_o[pi * kHeadDim + d] = o;
+        if (d == 0) a.part_ml[pi] = make_float2(sh.mrun[hh], sh.lrun[hh]);
     }
     __syncthreads();
 }
 
-
-// One token's K and V row (this lane's 8 elements) folded into the online
-// softmax state of each head.
-template <int DT, int GC>
-__device__ __forceinline__ void fold_token(const AttnArgs& a, const uint4 (&qv)[GC], const uint4& kr, const uint4& vr,
-                                           float (&m)[GC], float (&l)[GC], float (&o)[GC][8])
-{
-    float vf[8];
-    widen2<DT>(vr.x, vf[0], vf[1]);
-    widen2<DT>(vr.y, vf[2], vf[3]);
-    widen2<DT>(vr.z, vf[4], vf[5]);
-    widen2<DT>(vr.w, vf[6], vf[7]);
-#pragma unroll
-    for (int hh = 0; hh < GC; ++hh) {
-        const float x = a.s2 * sum16(dot8<DT>(kr, qv[hh]));
-        const float mn = fmaxf(m[hh], x);
-        const float sc = exp2f(m[hh] - mn);
-        const float p = exp2f(x - mn);
-        l[hh] = l[hh] * sc + p;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[hh][i] = o[hh][i] * sc + p * vf[i];
-        m[hh] = mn;
-    }
-}
-
-// Partial attention where every row group attends over its own tokens:
-// bit i of `mask` selects token jbase + i (mask and jbase uniform within the
-// 16-lane group).  Rows are loaded kTokBatch at a time.
-template <int DT, int GC>
-__device__ __forceinline__ void attend_masked(const AttnArgs& a, int b, int g, int hc, const uint4 (&qv)[GC], int jbase,
-                                              uint32_t mask, int slot, int nslots, AttnLds<GC>& sh)
-{
-    const int l16 = threadIdx.x & 15;
-    const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
-    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + l16 * 8;
-    float m[GC], l[GC], o[GC][8];
-#pragma unroll
-    for (int hh = 0; hh < GC; ++hh) {
-        m[hh] = -INFINITY;
-        l[hh] = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[hh][i] = 0.0f;
-    }
-    while (mask) {
-        int jj[kTokBatch];
-        int cnt = 0;
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u) {
-            jj[u] = jbase + (mask ? __builtin_ctz(mask) : 0);
-            cnt += mask ? 1 : 0;
-            mask &= mask - 1u;
-        }
-        uint4 kr[kTokBatch], vr[kTokBatch];
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u) {
-            // clamped: an out-of-range index reads a valid row instead of faulting
-            const int64_t j = min(max(jj[u], 0), a.n - 1);
-            kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
-            vr[u] = *reinterpret_cast<const uint4*>(vb + j * a.v_sn);
-        }
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u)
-            if (u < cnt) fold_token<DT, GC>(a, qv, kr[u], vr[u], m, l, o);
-    }
-    merge_row_groups<GC>(a, b, g, hc, m, l, o, slot, nslots, sh);
-}
-
-// Partial attention of heads g*G+hc .. +GC (queries qv from load_queries) over
-// list entries [t0, t1), written to slot `slot` of `nslots`.  idx_at(t)
-// returns the token index of entry t.  Every thread of the workgroup must
-// call this.
-template <int DT, int GC, typename IdxAt>
-__device__ __forceinline__ void attend_partial(const AttnArgs& a, int b, int g, int hc, const uint4 (&qv)[GC], int t0,
-                                               int t1, IdxAt idx_at, int slot, int nslots, AttnLds<GC>& sh)
-{
-    const int tid = threadIdx.x;
-    const int rg = tid >> 4, l16 = tid & 15;
-    const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
-    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + l16 * 8;
-
-    float m[GC], l[GC], o[GC][8];
-#pragma unroll
-    for (int hh = 0; hh < GC; ++hh) {
-        m[hh] = -INFINITY;
-        l[hh] = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) o[hh][i] = 0.0f;
-    }
-
-    for (int tb = t0 + rg; tb < t1; tb += 16 * kTokBatch) {
-        // indices first (clamped into the list, so every load is in bounds),
-        // then every K and V row of the batch, then the arithmetic
-        int jj[kTokBatch];
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u) jj[u] = idx_at(min(tb + u * 16, t1 - 1));
-        uint4 kr[kTokBatch], vr[kTokBatch];
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u) {
-            // clamped: an out-of-range index reads a valid row instead of faulting
-            const int64_t j = min(max(jj[u], 0), a.n - 1);
-            kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
-            vr[u] = *reinterpret_cast<const uint4*>(vb + j * a.v_sn);
-        }
-#pragma unroll
-        for (int u = 0; u < kTokBatch; ++u) {
-            if (tb + u * 16 >= t1) break;   // uniform within the 16-lane group
-            fold_token<DT, GC>(a, qv, kr[u], vr[u], m, l, o);
-        }
-    }
-
-    merge_row_groups<GC>(a, b, g, hc, m, l, o, slot, nslots, sh);
-}
-
 // out[b,h,:] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s over the nslots
-// partials of head h (empty slots have l = 0 and weigh 0).  The slot weights
-// are formed once in LDS (wsl holds nslots floats); thread t then sums output
-// dimension t % D over every (blockDim/D)-th slot with eight loads in flight,
-// and the slot groups are added in order.  red holds blockDim/64 + 1 floats,
-// osum blockDim floats.  Called by one workgroup of NT threads per (b, h).
+// partials of head h (empty slots have l = 0 and weigh 0).  Thread t sums
+// output dimension t % D over every (NT/D)-th slot; its partial loads are
+// issued before the maximum is known.  The slot weights are formed once in
+// LDS (wsl holds nslots floats), and the slot groups are added in order.
+// red holds NT/64 + 1 floats, osum NT floats.  One workgroup of NT threads
+// per (b, h).
 template <int NT>
 __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int nslots, float* wsl, float* red,
                                            float* osum)
 {
-    constexpr int NW = NT / 64, NG = NT / kHeadDim;
+    constexpr int NW = NT / 64, NG = NT / kHeadDim, kPre = 32;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int d = tid % kHeadDim, grp = tid / kHeadDim;
     const int64_t bh = (int64_t)b * a.Hq + h;
     const float2* ml = a.part_ml + bh * nslots;
+    const float* po = a.part_o + bh * nslots * kHeadDim + d;
+
+    // the first kPre of this thread's slots: loads in flight during the reductions
+    float x[kPre];
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) {
+        const int s = grp + i * NG;
+        x[i] = s < nslots ? po[(int64_t)s * kHeadDim] : 0.0f;
+    }
     float mx = -INFINITY;
     for (int s = tid; s < nslots; s += NT) {
         const float2 v = ml[s];
@@ -231,17 +259,24 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
     float L = 0.0f;
 #pragma unroll
     for (int i = 0; i < NW; ++i) L += red[i];
-    const float* po = a.part_o + bh * nslots * kHeadDim + d;
     float O = 0.0f;
-    int s = grp;
-    for (; s + 8 * NG <= nslots; s += 8 * NG) {
-        float x[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) x[i] = po[(int64_t)(s + i * NG) * kHeadDim];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) O += wsl[s + i * NG] * x[i];
+    for (int i = 0; i < kPre; ++i) {
+        const int s = grp + i * NG;
+        if (s < nslots) O += wsl[s] * x[i];
     }
-    for (; s < nslots; s += NG) O += wsl[s] * po[(int64_t)s * kHeadDim];
+    for (int s0 = grp + kPre * NG; s0 < nslots; s0 += kPre * NG) {
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) {
+            const int s = s0 + i * NG;
+            x[i] = s < nslots ? po[(int64_t)s * kHeadDim] : 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) {
+            const int s = s0 + i * NG;
+            if (s < nslots) O += wsl[s] * x[i];
+        }
+    }
     osum[tid] = O;
     __syncthreads();
     if (grp == 0) {

@@ -40,7 +40,7 @@ struct Shape {
 // Workspace regions, in this order, each 256-byte aligned:
 //   logits   ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
 //   part     ATTN [B,Hq,ntiles] float2;  stats ATTN [B,Hq] float2
-//   zeroed   hist1 [rows,4096] | hist2 [rows,4096] (u32; cleared by the first kernel of every call
+//   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins; cleared by the first kernel of every call
 //            that accumulates into them)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
 //   sel_list [rows,n] i32 | sel_n [rows,nchunks] u32
@@ -76,8 +76,8 @@ Layout layout_for(const Shape& s, int ksel)
     L.end_score = off;
     L.zero = off;
     L.hist1 = off;
-    L.hist2 = L.hist1 + rows * kHistBins * sizeof(uint32_t);
-    const size_t zero_end = L.hist2 + rows * kHistBins * sizeof(uint32_t);
+    L.hist2 = L.hist1 + rows * kHistRow * sizeof(uint32_t);
+    const size_t zero_end = L.hist2 + rows * kHistRow * sizeof(uint32_t);
     L.zero_words = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
     off = align256(zero_end);
     L.nchunks = (s.n + kSelChunk - 1) / kSelChunk;

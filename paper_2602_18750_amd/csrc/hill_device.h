@@ -121,6 +121,40 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
     return v;
 }
 
+// 64 histogram bins held one per lane (lane l: count of bin l; higher bins
+// hold larger keys).  Finds the bin L holding the need-th largest key
+// (need >= 1) and the number of keys in the bins above L.  Wave-uniform
+// results; L = 0 if the bins hold fewer than need keys.
+__device__ __forceinline__ void wave_find_bin(uint32_t cnt, uint32_t need, int& L, uint32_t& above)
+{
+    const uint32_t incl = wave_incl_scan(cnt);
+    const uint32_t total = __shfl(incl, 63, 64);
+    const uint32_t suffix = total - incl + cnt;   // keys in bins >= this lane's
+    const uint64_t m = __ballot(suffix >= need);  // lanes 0 .. L
+    L = m ? 63 - __clzll((long long)m) : 0;
+    above = __shfl(suffix - cnt, L, 64);
+}
+
+// Exclusive prefix sum over a 256-thread block with a single barrier.  The
+// four wave totals stay in scratch[0..3], which must not be rewritten before
+// the next barrier.
+__device__ __forceinline__ uint32_t block_excl_scan_1b(uint32_t v, uint32_t* scratch, uint32_t* total)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint32_t inc = wave_incl_scan(v);
+    if (lane == 63) scratch[w] = inc;
+    __syncthreads();
+    uint32_t base = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t s = scratch[i];
+        base += i < w ? s : 0u;
+        tot += s;
+    }
+    *total = tot;
+    return base + inc - v;
+}
+
 // Exclusive prefix sum over a block of NT threads (NT a multiple of 64, <= 1024).
 // `scratch` holds at least NT/64 + 1 words of LDS.  Returns the block total in *total.
 template <int NT>

@@ -11,6 +11,8 @@ constexpr int kHeadDim = 128;      // D supported by every kernel
 constexpr int kScoreTile = 32;     // tokens per scoring wave-tile (softmax partial granularity)
 constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
+constexpr int kCoarseBins = 64;    // each 12-bit digit histogram also counts its top 6 bits
+constexpr int kHistRow = kHistBins + kCoarseBins;   // words per histogram row: fine, then coarse
 constexpr int kUpdChunk = 256;     // tokens per importance-update workgroup
 constexpr int kHistChunk = 2048;   // tokens per standalone histogram workgroup
 constexpr int kSelChunk = 512;     // tokens per selection chunk (256 threads x 2)
@@ -45,7 +47,7 @@ struct UpdateArgs {
     int64_t s_sb, s_sr;
     int B, Hq, Hkv, G, R, n;
     float s2;
-    uint32_t* hist;          // nullable: [B*R, kHistBins] first-digit counts
+    uint32_t* hist;          // nullable: [B*R, kHistRow] first-digit counts (fine, coarse)
 };
 
 struct AttnArgs {
@@ -69,8 +71,8 @@ struct RefineArgs {
     const float* s;
     int64_t s_sb, s_sr;
     int R, n, k, nchunks;
-    const uint32_t* hist1;   // [rows, kHistBins] first-digit counts (bits 31..20)
-    uint32_t* hist2;         // [rows, kHistBins] second-digit counts (bits 19..8), zeroed before
+    const uint32_t* hist1;   // [rows, kHistRow] first-digit counts (bits 31..20; coarse: bits 31..26)
+    uint32_t* hist2;         // [rows, kHistRow] second-digit counts (bits 19..8; coarse: bits 19..14), zeroed before
     uint32_t* cand_key;      // [rows, n] keys inside the first-digit bin, chunk c at offset c*kSelChunk
     uint32_t* cand_n;        // [rows, nchunks]
     uint4* state;            // [rows] (first-digit bin, keys still needed from it, keys in it, 0)

@@ -237,11 +237,19 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
     }
 }
 
+// Counts a selection key in the first-digit histogram (bits 31..20) and its
+// coarse bins (bits 31..26).
+__device__ __forceinline__ void count_key(uint32_t* lds_hist, uint32_t key)
+{
+    atomicAdd(&lds_hist[key >> (32 - kHistBits)], 1u);
+    atomicAdd(&lds_hist[kHistBins + (key >> 26)], 1u);
+}
+
 // Merges a workgroup's LDS histogram into the row's global histogram: one
 // integer atomic per non-empty bin (order-independent result).
 __device__ __forceinline__ void hist_merge(const uint32_t* lds_hist, uint32_t* ghist)
 {
-    for (int i = threadIdx.x; i < kHistBins; i += 256) {
+    for (int i = threadIdx.x; i < kHistRow; i += 256) {
         const uint32_t c = lds_hist[i];
         if (c) atomicAdd(ghist + i, c);
     }
@@ -257,7 +265,7 @@ constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 {
     __shared__ float4 wsum[4][64];
-    __shared__ uint32_t lds_hist[kHistBins];
+    __shared__ uint32_t lds_hist[kHistRow];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
@@ -265,7 +273,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
     if (do_hist)
-        for (int i = tid; i < kHistBins; i += 256) lds_hist[i] = 0u;
+        for (int i = tid; i < kHistRow; i += 256) lds_hist[i] = 0u;
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
     const int jc = min(j4, (int)(a.ld - 4));              // rows are padded to ld (multiple of 4)
     const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
@@ -299,11 +307,11 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
         float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
         const float s_new = srow[j] + tot;
         srow[j] = s_new;
-        if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
+        if (do_hist) count_key(lds_hist, order_key(s_new));
     }
     if (do_hist) {
         __syncthreads();
-        hist_merge(lds_hist, a.hist + (int64_t)row * kHistBins);
+        hist_merge(lds_hist, a.hist + (int64_t)row * kHistRow);
     }
 }
 
@@ -311,12 +319,12 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
 {
     __shared__ float4 wsum[4][64];
-    __shared__ uint32_t lds_hist[kHistBins];
+    __shared__ uint32_t lds_hist[kHistRow];
     const int b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
     if (do_hist)
-        for (int i = tid; i < kHistBins; i += 256) lds_hist[i] = 0u;
+        for (int i = tid; i < kHistRow; i += 256) lds_hist[i] = 0u;
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;
     const int jc = min(j4, (int)(a.ld - 4));
     const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
@@ -345,11 +353,11 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
         float* srow = a.s + (int64_t)b * a.s_sb;
         const float s_new = srow[j] + tot;
         srow[j] = s_new;
-        if (do_hist) atomicAdd(&lds_hist[order_key(s_new) >> (32 - kHistBits)], 1u);
+        if (do_hist) count_key(lds_hist, order_key(s_new));
     }
     if (do_hist) {
         __syncthreads();
-        hist_merge(lds_hist, a.hist + (int64_t)b * kHistBins);
+        hist_merge(lds_hist, a.hist + (int64_t)b * kHistRow);
     }
 }
 

@@ -45,21 +45,25 @@ static_assert(kSelChunk == 16 * 32, "16 row groups of 32 tokens");
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict__ s, int64_t s_sb, int64_t s_sr,
                                                         int R, int n, uint32_t* __restrict__ hist)
 {
-    __shared__ uint32_t lds_hist[kHistBins];
+    __shared__ uint32_t lds_hist[kHistRow];
     const int row = blockIdx.y;
     const int b = row / R, r = row % R;
-    for (int i = threadIdx.x; i < kHistBins; i += 256) lds_hist[i] = 0u;
+    for (int i = threadIdx.x; i < kHistRow; i += 256) lds_hist[i] = 0u;
     __syncthreads();
     const float* srow = s + (int64_t)b * s_sb + (int64_t)r * s_sr;
     constexpr int kPer = kHistChunk / 256;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
         const int j = blockIdx.x * kHistChunk + i * 256 + threadIdx.x;
-        if (j < n) atomicAdd(&lds_hist[order_key(srow[j]) >> (32 - kHistBits)], 1u);
+        if (j < n) {
+            const uint32_t kk = order_key(srow[j]);
+            atomicAdd(&lds_hist[kk >> (32 - kHistBits)], 1u);
+            atomicAdd(&lds_hist[kHistBins + (kk >> 26)], 1u);
+        }
     }
     __syncthreads();
-    uint32_t* gh = hist + (int64_t)row * kHistBins;
-    for (int i = threadIdx.x; i < kHistBins; i += 256) {
+    uint32_t* gh = hist + (int64_t)row * kHistRow;
+    for (int i = threadIdx.x; i < kHistRow; i += 256) {
         const uint32_t c = lds_hist[i];
         if (c) atomicAdd(gh + i, c);
     }
@@ -95,6 +99,49 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
     return v;
+}
+
+// A histogram row of one 12-bit digit, loaded so that thread t holds fine
+// bins i*256 + t (i < 16) and every lane holds coarse bin `lane` (the bin's
+// top 6 bits).  Fine bins 64*C .. 64*C+63 of coarse bin C then sit in
+// register C/4 of wave C%4, one per lane.
+struct DigitHist {
+    uint32_t fine[kHistBins / kThreads];
+    uint32_t coarse;
+};
+
+__device__ __forceinline__ void load_digit_hist(const uint32_t* h, DigitHist& d)
+{
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) d.fine[i] = h[i * kThreads + threadIdx.x];
+    d.coarse = h[kHistBins + (threadIdx.x & 63)];
+}
+
+// The bin holding the need-th largest key of the row (1 <= need <= keys in
+// the row): res[0] = bin, res[1] = keys still needed from it (need minus the
+// keys in higher bins), res[2] = keys in it.  Every wave finds the coarse bin;
+// the wave holding its fine bins finishes and publishes the result.  The
+// caller reads res after a barrier.
+__device__ __forceinline__ void find_digit(const DigitHist& d, uint32_t need, uint32_t* res)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    int C;
+    uint32_t above_c;
+    wave_find_bin(d.coarse, need, C, above_c);
+    if (w == (C & 3)) {
+        uint32_t v = 0u;
+#pragma unroll
+        for (int i = 0; i < kHistBins / kThreads; ++i) v = i == (C >> 2) ? d.fine[i] : v;
+        int L;
+        uint32_t above_f;
+        wave_find_bin(v, need - above_c, L, above_f);
+        const uint32_t in_bin = __shfl(v, L, 64);
+        if (lane == 0) {
+            res[0] = (uint32_t)(64 * C + L);
+            res[1] = need - above_c - above_f;
+            res[2] = in_bin;
+        }
+    }
 }
 
 // Histogram of `nb` bins in LDS: the bin holding the need-th largest key,
@@ -134,9 +181,8 @@ __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* 
 
 __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
 {
-    __shared__ uint32_t hist[kHistBins];
-    __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
-    __shared__ uint32_t res[2];
+    __shared__ uint32_t hist[kHistRow];
+    __shared__ uint32_t res[3];
     __shared__ uint32_t n_cand;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -147,25 +193,19 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     uint32_t key[kPerThread];
     bool ok[kPerThread];
     load_keys(srow, c, a.n, key, ok);
-    const uint32_t* h1 = a.hist1 + (int64_t)row * kHistBins;
-    uint32_t hv[kHistBins / kThreads];
-#pragma unroll
-    for (int i = 0; i < kHistBins / kThreads; ++i) hv[i] = h1[i * kThreads + tid];
-#pragma unroll
-    for (int i = 0; i < kHistBins / kThreads; ++i) hist[i * kThreads + tid] = hv[i];
+    DigitHist h1;
+    load_digit_hist(a.hist1 + (int64_t)row * kHistRow, h1);
+    for (int i = tid; i < kHistRow; i += kThreads) hist[i] = 0u;
     if (tid == 0) n_cand = 0u;
-    __syncthreads();
     // first digit: the bin of the k-th key
-    find_bin<kThreads>(hist, kHistBins, (uint32_t)a.k, scan_scratch, res);
+    find_digit(h1, (uint32_t)a.k, res);
+    __syncthreads();
     const uint32_t b1 = res[0] & (kHistBins - 1);
-    const uint32_t need1 = (uint32_t)a.k - res[1];
-    const uint32_t in1 = hist[b1];
+    const uint32_t need1 = res[1];
+    const uint32_t in1 = res[2];
     const bool refine = need1 < in1;
     if (c == 0 && tid == 0) a.state[row] = make_uint4(b1, need1, in1, 0u);
-    __syncthreads();
 
-    for (int i = tid; i < kHistBins; i += kThreads) hist[i] = 0u;
-    __syncthreads();
     // keys inside the bin are the candidates: their second digit is
     // histogrammed and they are appended (wave-compacted) to the chunk's
     // candidate list, whose order does not matter
@@ -173,7 +213,10 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
 #pragma unroll
     for (int e = 0; e < kPerThread; ++e) {
         const bool is_c = ok[e] && (key[e] >> 20) == b1;
-        if (is_c && refine) atomicAdd(&hist[(key[e] >> 8) & (kHistBins - 1)], 1u);
+        if (is_c && refine) {
+            atomicAdd(&hist[(key[e] >> 8) & (kHistBins - 1)], 1u);
+            atomicAdd(&hist[kHistBins + ((key[e] >> 14) & (kCoarseBins - 1))], 1u);
+        }
         const uint64_t mask = __ballot(is_c);
         if (mask) {
             const int leader = __ffsll((unsigned long long)mask) - 1;
@@ -185,8 +228,8 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     }
     __syncthreads();
     if (refine) {
-        uint32_t* h2 = a.hist2 + (int64_t)row * kHistBins;
-        for (int i = tid; i < kHistBins; i += kThreads) {
+        uint32_t* h2 = a.hist2 + (int64_t)row * kHistRow;
+        for (int i = tid; i < kHistRow; i += kThreads) {
             const uint32_t v = hist[i];
             if (v) atomicAdd(h2 + i, v);
         }
@@ -211,10 +254,10 @@ __device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int
 template <int DT, int GC, bool ATTN>
 __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnArgs at)
 {
-    __shared__ uint32_t hist[kHistBins];
+    __shared__ uint32_t hist3[256];
     __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t red[kThreads / 64];
-    __shared__ uint32_t res[2];
+    __shared__ uint32_t res[3];
     __shared__ AttnLds<ATTN ? GC : 1> sh;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -230,50 +273,46 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     // one workgroup per chunk stores the list (token rows: KV head 0)
     const bool writer = !ATTN || r.R != 1 || g == 0;
 
-    // independent loads first: queries, this chunk's keys, the row's state and histogram
+    // independent loads first: queries, this chunk's keys, the row's state and
+    // second-digit histogram
     uint4 qv[ATTN ? GC : 1];
     if constexpr (ATTN) load_queries<GC>(at, b, g, 0, qv);
     uint32_t key[kPerThread];
     bool ok[kPerThread];
     load_keys(row_ptr(r, row), c, r.n, key, ok);
     const uint4 s1 = r.state[row];
+    DigitHist h2;
+    load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
     const uint32_t b1 = s1.x, need1 = s1.y, in1 = s1.z;
-    const uint32_t* h2 = r.hist2 + (int64_t)row * kHistBins;
-    uint32_t hv[kHistBins / kThreads];
-#pragma unroll
-    for (int i = 0; i < kHistBins / kThreads; ++i) hv[i] = need1 < in1 ? h2[i * kThreads + tid] : 0u;
 
     // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
     uint32_t prefix = b1, need = need1;
     int shift = 20;
     bool all_eq = need1 == in1;
     if (!all_eq) {
-#pragma unroll
-        for (int i = 0; i < kHistBins / kThreads; ++i) hist[i * kThreads + tid] = hv[i];
+        find_digit(h2, need1, res);
         __syncthreads();
-        find_bin<kThreads>(hist, kHistBins, need1, scan_scratch, res);
         const uint32_t b2 = res[0] & (kHistBins - 1);
-        const uint32_t need2 = need1 - res[1];
-        const uint32_t in2 = hist[b2];
+        const uint32_t need2 = res[1];
+        const uint32_t in2 = res[2];
         prefix = (b1 << 12) | b2;
         shift = 8;
         need = need2;
         all_eq = need2 == in2;
-        __syncthreads();
         if (!all_eq) {   // third digit (bits 7..0) from the candidate lists
-            for (int i = tid; i < 256; i += kThreads) hist[i] = 0u;
+            for (int i = tid; i < 256; i += kThreads) hist3[i] = 0u;
             __syncthreads();
             const uint32_t p2 = prefix;
             for_candidates(r, row, 0, r.nchunks, [p2](uint32_t kk) {
-                if ((kk >> 8) == p2) atomicAdd(&hist[kk & 0xffu], 1u);
+                if ((kk >> 8) == p2) atomicAdd(&hist3[kk & 0xffu], 1u);
             });
             __syncthreads();
-            find_bin<kThreads>(hist, 256, need2, scan_scratch, res);
+            find_bin<kThreads>(hist3, 256, need2, scan_scratch, res);
             const uint32_t b3 = res[0] & 0xffu;
             prefix = (p2 << 8) | b3;
             shift = 0;
             need = need2 - res[1];
-            all_eq = need == hist[b3];
+            all_eq = need == hist3[b3];
             __syncthreads();
         }
     }
@@ -313,10 +352,10 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     // the chunk's selected tokens in token order, and their count
     const uint32_t nsel = (uint32_t)sel[0] + (uint32_t)sel[1];
     uint32_t tot;
-    const uint32_t pos = block_excl_scan<kThreads>(nsel, scan_scratch, &tot);
+    const uint32_t pos = block_excl_scan_1b(nsel, scan_scratch, &tot);
+    const int j0 = c * kSelChunk + tid * kPerThread;
     if (writer) {
         int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
-        const int j0 = c * kSelChunk + tid * kPerThread;
         uint32_t p = pos;
 #pragma unroll
         for (int e = 0; e < kPerThread; ++e)
@@ -325,19 +364,19 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     }
 
     if constexpr (ATTN) {
-        // row group rg owns tokens [32*rg, 32*rg + 32) of the chunk: both
-        // tokens of each of its 16 lanes
-        const int rg = tid >> 4;
-        const uint64_t m0 = __ballot(sel[0]), m1 = __ballot(sel[1]);
-        const int sh16 = (rg & 3) * 16;
-        const uint32_t a0 = (uint32_t)(m0 >> sh16) & 0xffffu, a1 = (uint32_t)(m1 >> sh16) & 0xffffu;
-        uint32_t mask = 0;
+        // attention of the group's heads over the chunk's selected tokens:
+        // one partial per head in slot c
+        uint32_t p = pos;
 #pragma unroll
-        for (int i = 0; i < 16; ++i) mask |= (((a0 >> i) & 1u) << (2 * i)) | (((a1 >> i) & 1u) << (2 * i + 1));
-        const int jbase = c * kSelChunk + rg * 32;
+        for (int e = 0; e < kPerThread; ++e)
+            if (sel[e]) sh.tok[p++] = j0 + e;
+        __syncthreads();
         for (int hc = 0; hc < at.G; hc += GC) {
             if (hc) load_queries<GC>(at, b, g, hc, qv);
-            attend_masked<DT, GC>(at, b, g, hc, qv, jbase, mask, c, r.nchunks, sh);
+            AttnAcc<GC> acc;
+            attn_begin<GC>(acc, sh);
+            if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
+            attn_finish<GC>(at, b, g, hc, acc, c, r.nchunks, sh);
         }
     }
 }
