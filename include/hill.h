@@ -39,11 +39,14 @@
  * Alignment.  q, K, V, S, out and ws base addresses 16-byte aligned; q, K, V
  *   strides multiples of 8 elements; S strides multiples of 4 elements.
  * Supported.  head_dim == 128; dtype fp16 or bf16; n_q_heads % n_kv_heads
- *   == 0; 1 <= k_sel <= n_tokens.
+ *   == 0, n_q_heads <= 256, n_q_heads / n_kv_heads <= 128; 1 <= k_sel <=
+ *   n_tokens; n_tokens <= 2097152; k_stride_n and v_stride_n below 2^31
+ *   elements.
  * Errors.  All arguments are checked on the host before anything is
  *   enqueued; on any error nothing is enqueued and no output is written.
  *   HILL_ERR_INVALID_ARG: null/misaligned pointer, bad shape, stride or k_sel.
- *   HILL_ERR_UNSUPPORTED: a valid but unimplemented head_dim or dtype.
+ *   HILL_ERR_UNSUPPORTED: a valid but unimplemented head_dim, dtype, head
+ *                         count, context length or token stride.
  *   HILL_ERR_WORKSPACE:   ws too small.
  *   HILL_ERR_HIP:         a kernel launch failed (enqueued work before it in
  *                         the same call may still run).

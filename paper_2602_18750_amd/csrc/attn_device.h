@@ -27,7 +27,7 @@
 namespace hill {
 
 constexpr int kAttnBlock = 512;   // list entries per LDS block
-constexpr int kKBatch = 8;        // K rows in flight per row group (phase A)
+constexpr int kKBatch = 4;        // K rows in flight per row group (phase A)
 constexpr int kVBatch = 16;       // V rows in flight per wave (phase C)
 
 template <int GC>
@@ -68,56 +68,85 @@ __device__ __forceinline__ void attn_begin(AttnAcc<GC>& acc, AttnLds<GC>& sh)
     }
 }
 
-// This lane's V element pair of token j, clamped into [0, n) so that a bad
-// index reads a valid row instead of faulting (lists hold valid tokens).
-__device__ __forceinline__ uint32_t load_v2(const AttnArgs& a, const uint16_t* vb, int j)
+// Row offset of token j (clamped into [0, n) so that a bad index reads a
+// valid row instead of faulting; lists hold valid tokens).  Row strides are
+// below 2^31 elements (checked on the host): one 32x32->64-bit multiply.
+__device__ __forceinline__ uint64_t row_off(int j, int n, int64_t stride)
 {
-    j = min(max(j, 0), a.n - 1);
-    return *reinterpret_cast<const uint32_t*>(vb + (int64_t)j * a.v_sn);
+    j = min(max(j, 0), n - 1);
+    return (uint64_t)(uint32_t)j * (uint32_t)stride;
+}
+
+// K rows of entries t0, t0+16, ... (kKBatch of them, clamped to the last
+// entry) for this lane's 16-byte slice.
+__device__ __forceinline__ void load_k_batch(const AttnArgs& a, const uint16_t* kb, const int32_t* tok, int t0,
+                                             int cnt, uint4 (&kr)[kKBatch])
+{
+#pragma unroll
+    for (int u = 0; u < kKBatch; ++u) {
+        const int t = min(t0 + 16 * u, cnt - 1);
+        kr[u] = *reinterpret_cast<const uint4*>(kb + row_off(tok[t], a.n, a.k_sn));
+    }
+}
+
+// V element pairs of entries w + 4*(i0 + i), i < kVBatch (clamped to the
+// last entry).
+__device__ __forceinline__ void load_v_batch(const AttnArgs& a, const uint16_t* vb, const int32_t* tok, int w,
+                                             int i0, int cnt, uint32_t (&vr)[kVBatch])
+{
+#pragma unroll
+    for (int i = 0; i < kVBatch; ++i) {
+        const int t = min(w + 4 * (i0 + i), cnt - 1);
+        vr[i] = *reinterpret_cast<const uint32_t*>(vb + row_off(tok[t], a.n, a.v_sn));
+    }
+}
+
+// Logits of the batch's entries into sh.p (lane l16 == hh of the row group
+// writes head hh; entries past cnt are computed on the clamped row and not
+// stored).
+template <int DT, int GC>
+__device__ __forceinline__ void logits_batch(const AttnArgs& a, const uint4 (&qv)[GC], const uint4 (&kr)[kKBatch],
+                                             int t0, int cnt, float (*p)[GC])
+{
+    const int l16 = threadIdx.x & 15;
+#pragma unroll
+    for (int u = 0; u < kKBatch; ++u) {
+        const int t = t0 + 16 * u;
+        float mine = 0.0f;   // lane l16 == hh keeps head hh's dot product
+#pragma unroll
+        for (int hh = 0; hh < GC; ++hh) {
+            const float d = sum16(dot8<DT>(kr[u], qv[hh]));
+            mine = l16 == hh ? d : mine;
+        }
+        if (l16 < GC && t < cnt) p[t][l16] = a.s2 * mine;
+    }
 }
 
 // Folds list entries [0, cnt) of sh.tok (1 <= cnt <= kAttnBlock, written and
 // made visible by a barrier before the call) into the running state.  Every
-// thread of the workgroup must call this; it ends with the block's LDS
-// reads done only after a barrier of the next call or of attn_finish.
+// thread of the workgroup must call this.  The first K batch is issued
+// before the first V batch so that the logits wait for K only; all loads are
+// unconditional (clamped) so the counters stay exact.
 template <int DT, int GC>
 __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, const uint4 (&qv)[GC], int cnt,
                                            AttnAcc<GC>& acc, AttnLds<GC>& sh)
 {
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar control flow
     const int rg = tid >> 4, l16 = tid & 15;
     const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
     const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
 
-    // first V batch of this wave, in flight during phase A
+    // A: logits of every entry, into sh.p; the first V batch is in flight meanwhile
+    uint4 kr[kKBatch];
+    load_k_batch(a, kb, sh.tok, rg, cnt, kr);
+    __builtin_amdgcn_sched_barrier(0);   // keep the K loads ahead of the V loads in the queue
     uint32_t vr[kVBatch];
-#pragma unroll
-    for (int i = 0; i < kVBatch; ++i) {
-        const int t = w + 4 * i;
-        vr[i] = t < cnt ? load_v2(a, vb, sh.tok[t]) : 0u;
-    }
-
-    // A: logits of every entry, into sh.p
-    for (int t0 = rg; t0 < cnt; t0 += 16 * kKBatch) {
-        uint4 kr[kKBatch];
-#pragma unroll
-        for (int u = 0; u < kKBatch; ++u) {
-            const int t = min(t0 + 16 * u, cnt - 1);
-            const int64_t j = min(max(sh.tok[t], 0), a.n - 1);
-            kr[u] = *reinterpret_cast<const uint4*>(kb + j * a.k_sn);
-        }
-#pragma unroll
-        for (int u = 0; u < kKBatch; ++u) {
-            const int t = t0 + 16 * u;
-            if (t >= cnt) break;   // uniform within the row group
-            float mine = 0.0f;     // lane l16 == hh keeps head hh's dot product
-#pragma unroll
-            for (int hh = 0; hh < GC; ++hh) {
-                const float d = sum16(dot8<DT>(kr[u], qv[hh]));
-                mine = l16 == hh ? d : mine;
-            }
-            if (l16 < GC) sh.p[t][l16] = a.s2 * mine;
-        }
+    load_v_batch(a, vb, sh.tok, w, 0, cnt, vr);
+    logits_batch<DT, GC>(a, qv, kr, rg, cnt, sh.p);
+    for (int t0 = rg + 16 * kKBatch; t0 < cnt; t0 += 16 * kKBatch) {
+        load_k_batch(a, kb, sh.tok, t0, cnt, kr);
+        logits_batch<DT, GC>(a, qv, kr, t0, cnt, sh.p);
     }
     __syncthreads();
 
@@ -152,17 +181,18 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
         acc.o[hh][1] *= al;
     }
     for (int i0 = 0;; i0 += kVBatch) {
+        // branch-free over the batch: entries past cnt weigh 0
 #pragma unroll
         for (int i = 0; i < kVBatch; ++i) {
             const int t = w + 4 * (i0 + i);
-            if (t >= cnt) break;   // uniform within the wave
+            const int tc = min(t, cnt - 1);
             float v0, v1;
             widen2<DT>(vr[i], v0, v1);
             float pw[GC];
             if constexpr (GC % 4 == 0) {
 #pragma unroll
                 for (int h4 = 0; h4 < GC; h4 += 4) {
-                    const float4 x = *reinterpret_cast<const float4*>(&sh.p[t][h4]);
+                    const float4 x = *reinterpret_cast<const float4*>(&sh.p[tc][h4]);
                     pw[h4] = x.x;
                     pw[h4 + 1] = x.y;
                     pw[h4 + 2] = x.z;
@@ -170,20 +200,17 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
                 }
             } else {
 #pragma unroll
-                for (int hh = 0; hh < GC; ++hh) pw[hh] = sh.p[t][hh];
+                for (int hh = 0; hh < GC; ++hh) pw[hh] = sh.p[tc][hh];
             }
 #pragma unroll
             for (int hh = 0; hh < GC; ++hh) {
-                acc.o[hh][0] += pw[hh] * v0;
-                acc.o[hh][1] += pw[hh] * v1;
+                const float pv = t < cnt ? pw[hh] : 0.0f;
+                acc.o[hh][0] += pv * v0;
+                acc.o[hh][1] += pv * v1;
             }
         }
         if (w + 4 * (i0 + kVBatch) >= cnt) break;
-#pragma unroll
-        for (int i = 0; i < kVBatch; ++i) {
-            const int t = w + 4 * (i0 + kVBatch + i);
-            vr[i] = t < cnt ? load_v2(a, vb, sh.tok[t]) : 0u;
-        }
+        load_v_batch(a, vb, sh.tok, w, i0 + kVBatch, cnt, vr);
     }
 }
 

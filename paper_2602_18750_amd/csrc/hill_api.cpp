@@ -31,7 +31,7 @@ hill_status fail(hill_status st, const char* fmt, ...)
 
 // Shape facts derived from a validated descriptor.
 struct Shape {
-    int B, Hq, Hkv, G, D, n, R, ntiles;
+    int B, Hq, Hkv, G, D, n, R, ntiles, npart;
     int64_t ld;
     int dtype, mode, gran;
     float scale;
@@ -39,7 +39,7 @@ struct Shape {
 
 // Workspace regions, in this order, each 256-byte aligned:
 //   logits   ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
-//   part     ATTN [B,Hq,ntiles] float2;  stats ATTN [B,Hq] float2
+//   part     ATTN [B,Hq,npart] float2 (per 128-token unit);  stats ATTN [B,Hq] float2
 //   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins; cleared by the first kernel of every call
 //            that accumulates into them)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
@@ -70,7 +70,7 @@ Layout layout_for(const Shape& s, int ksel)
     if (attn) off += align256((size_t)s.B * s.Hq * s.ld * sizeof(float));
     else if (raw_groups) off += align256((size_t)s.B * s.Hkv * s.ld * sizeof(float));
     L.part = off;
-    if (attn) off += align256((size_t)s.B * s.Hq * s.ntiles * sizeof(float2));
+    if (attn) off += align256((size_t)s.B * s.Hq * s.npart * sizeof(float2));
     L.stats = off;
     if (attn) off += align256((size_t)s.B * s.Hq * sizeof(float2));
     L.end_score = off;
@@ -115,6 +115,8 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     if (d->n_q_heads % d->n_kv_heads)
         return fail(HILL_ERR_INVALID_ARG, "n_q_heads %d is not a multiple of n_kv_heads %d", d->n_q_heads,
                     d->n_kv_heads);
+    if (d->n_q_heads > 256 || d->n_q_heads / d->n_kv_heads > kMaxGroup)
+        return fail(HILL_ERR_UNSUPPORTED, "more than 256 query heads or %d query heads per KV head", kMaxGroup);
     if (d->dtype != HILL_F16 && d->dtype != HILL_BF16)
         return fail(HILL_ERR_UNSUPPORTED, "dtype %d is not fp16 (0) or bf16 (1)", d->dtype);
     if (d->score_mode != HILL_SCORE_ATTN && d->score_mode != HILL_SCORE_RAW)
@@ -135,6 +137,8 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     if (d->q_stride_h < D && d->n_q_heads > 1) return fail(HILL_ERR_INVALID_ARG, "q_stride_h < head_dim");
     if (d->k_stride_n < D || d->v_stride_n < D)
         return fail(HILL_ERR_INVALID_ARG, "k_stride_n / v_stride_n < head_dim");
+    if (d->k_stride_n > INT32_MAX || d->v_stride_n > INT32_MAX)
+        return fail(HILL_ERR_UNSUPPORTED, "k_stride_n / v_stride_n above 2^31 - 1 elements");
     const int R = d->granularity == HILL_SEL_TOKEN ? 1 : d->n_kv_heads;
     if (uses_s) {
         if (d->s_stride_r < d->n_tokens || d->s_stride_r % 4)
@@ -150,6 +154,7 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     s->n = d->n_tokens;
     s->R = R;
     s->ntiles = (d->n_tokens + kScoreTile - 1) / kScoreTile;
+    s->npart = (s->ntiles + kUnitTiles - 1) / kUnitTiles;
     s->ld = ((int64_t)d->n_tokens + 3) / 4 * 4;
     s->dtype = d->dtype;
     s->mode = d->score_mode;
@@ -238,6 +243,7 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.G = s.G;
     a.n = s.n;
     a.ntiles = s.ntiles;
+    a.npart = s.npart;
     a.ld = s.ld;
     a.s2 = s.scale * 1.4426950408889634f;
     a.s = sacc;
@@ -265,10 +271,15 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         a.logits = at<float>(ws, L.logits);
         a.part = at<float2>(ws, L.part);
         HIP_TRY(launch_score_tiles(a, s.dtype, kOutLogits, ncu, st, scan));
-        float2* stats = at<float2>(ws, L.stats);
-        HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.ntiles, st));
         u.logits = a.logits;
-        u.stats = stats;
+        u.part = a.part;
+        u.npart = s.npart;
+        u.stats = nullptr;
+        if (!update_reduces_stats(s.R == 1 ? s.Hq : s.G, s.npart)) {
+            float2* stats = at<float2>(ws, L.stats);
+            HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.npart, st));
+            u.stats = stats;
+        }
         HIP_TRY(launch_update_attn(u, st, last));
     } else if (s.R == s.Hkv) {
         // one row per KV head (or a single KV head): the scan adds straight into S

@@ -95,30 +95,55 @@ __device__ __forceinline__ float sum16(float v)
     return v;
 }
 
+__device__ __forceinline__ float readlane_f(float v, int lane)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), lane));
+}
+
+// Max over the 64 lanes of a wave (every lane active): a 16-lane DPP
+// reduction, then the four row results read as scalars.
 __device__ __forceinline__ float wave_max(float v)
 {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-    return v;
+    v = fmaxf(v, dpp<0xB1>(v));
+    v = fmaxf(v, dpp<0x4E>(v));
+    v = fmaxf(v, dpp<0x141>(v));
+    v = fmaxf(v, dpp<0x140>(v));
+    return fmaxf(fmaxf(readlane_f(v, 0), readlane_f(v, 16)), fmaxf(readlane_f(v, 32), readlane_f(v, 48)));
 }
 
+// Sum over the 64 lanes of a wave (every lane active), in a fixed order.
 __device__ __forceinline__ float wave_sum(float v)
 {
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+    v = sum16(v);
+    return (readlane_f(v, 0) + readlane_f(v, 16)) + (readlane_f(v, 32) + readlane_f(v, 48));
+}
+
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v)
+{
+    // lanes that the control does not write (masked rows, shifted-in lanes) read 0
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROW_MASK, 0xF, false);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave, all in DPP: shifts by
+// 1, 2, 4, 8 within each 16-lane row (row_shr), then the last lane of row 0
+// added to row 1 and of row 2 to row 3 (row_bcast:15), then the last lane of
+// row 1 added to rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+{
+    v += dpp_u32<0x111, 0xF>(v);   // row_shr:1
+    v += dpp_u32<0x112, 0xF>(v);   // row_shr:2
+    v += dpp_u32<0x114, 0xF>(v);   // row_shr:4
+    v += dpp_u32<0x118, 0xF>(v);   // row_shr:8
+    v += dpp_u32<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3
+    v += dpp_u32<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3
     return v;
 }
 
-// Inclusive prefix sum over the 64 lanes of a wave.
-__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v)
+// Sum over the 64 lanes of a wave (every lane active), as a scalar.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
 {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        uint32_t t = __shfl_up(v, o, 64);
-        if (lane >= o) v += t;
-    }
-    return v;
+    return (uint32_t)__builtin_amdgcn_readlane((int)wave_incl_scan(v), 63);
 }
 
 // 64 histogram bins held one per lane (lane l: count of bin l; higher bins

@@ -8,7 +8,10 @@
 namespace hill {
 
 constexpr int kHeadDim = 128;      // D supported by every kernel
-constexpr int kScoreTile = 32;     // tokens per scoring wave-tile (softmax partial granularity)
+constexpr int kScoreTile = 32;     // tokens per scoring wave-tile
+constexpr int kUnitTiles = 4;      // wave-tiles per scoring workgroup unit (softmax partial granularity)
+constexpr int kMaxGroup = 128;     // query heads per KV head supported
+constexpr int kStatLoads = 32;     // softmax partials per thread when the update reduces them itself
 constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;    // each 12-bit digit histogram also counts its top 6 bits
@@ -29,10 +32,11 @@ struct ScoreArgs {
     int64_t q_sb, q_sh;
     int64_t k_sb, k_sh, k_sn;
     int B, Hq, Hkv, G, n, ntiles;
+    int npart;               // workgroup units per (b, g): ceil(ntiles / kUnitTiles)
     int64_t ld;              // row stride of the logits buffer (n rounded up to 4)
     float s2;                // sm_scale * log2(e): logits are kept in the exp2 domain
     float* logits;           // kOutLogits: [B,Hq,ld]; kOutRawGroups: [B,Hkv,ld]
-    float2* part;            // kOutLogits: [B,Hq,ntiles] (max, sum exp2) per tile
+    float2* part;            // kOutLogits: [B,Hq,npart] (max, sum exp2) per unit of kUnitTiles tiles
     float* s;                // kOutRawS: importance rows
     int64_t s_sb, s_sr;
     uint32_t* zero_ptr;      // nullable: words to clear for a later kernel
@@ -42,7 +46,9 @@ struct ScoreArgs {
 struct UpdateArgs {
     const float* logits;     // ATTN: [B,Hq,ld]; RAW: group sums [B,Hkv,ld]
     int64_t ld;
-    const float2* stats;     // ATTN: [B,Hq] (max, 1/sum) in the exp2 domain
+    const float2* stats;     // ATTN: [B,Hq] (max, 1/sum) in the exp2 domain, or null: then
+    const float2* part;      //   the kernel reduces the [B,Hq,npart] unit partials itself
+    int npart;
     float* s;
     int64_t s_sb, s_sr;
     int B, Hq, Hkv, G, R, n;
@@ -105,7 +111,15 @@ struct Stamp {
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
-hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int ntiles, hipStream_t st);
+hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st);
+// Whether update_attn can reduce the softmax partials itself (no separate
+// softmax_stats launch): every thread then loads at most kStatLoads of them.
+inline bool update_reduces_stats(int nheads_per_row, int npart)
+{
+    if (nheads_per_row < 1 || nheads_per_row > 256) return false;
+    const int tph = 256 / nheads_per_row;
+    return (int64_t)npart <= (int64_t)kStatLoads * tph;
+}
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n,

@@ -76,7 +76,7 @@ __device__ __forceinline__ void load_tile(const ScoreArgs& a, int t, int rg, int
 
 template <int DT, int GC, int OUT>
 __device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, int l8, const uint4 (&kr)[kLoadsPerTile],
-                                             uint4 (&qa)[GC], uint4 (&qb)[GC], int& q_tag)
+                                             uint4 (&qa)[GC], uint4 (&qb)[GC], int& q_tag, float2* tile_part)
 {
     const TileCoord c = coord(a, t);
     const int jr = c.j0 + rg * kRowsPerLane;   // first token of this row group
@@ -139,8 +139,7 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, 
             z += __shfl_xor(z, 8, 64);
             z += __shfl_xor(z, 16, 64);
             z += __shfl_xor(z, 32, 64);
-            if (rg == 0 && l8 < GC)
-                a.part[((int64_t)c.b * a.Hq + h) * a.ntiles + c.tile] = make_float2(m, z);
+            if (rg == 0 && l8 < GC) tile_part[hc + l8] = make_float2(m, z);
         }
     }
 
@@ -164,10 +163,31 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, 
     }
 }
 
+// Merges the four waves' tile pairs of every head of the group into the
+// unit's pair (fixed order), by threads 0 .. G-1.
+__device__ __forceinline__ void merge_unit(const ScoreArgs& a, int bg, int unit, const float2 (*tp)[kMaxGroup])
+{
+    const int h = threadIdx.x;
+    if (h >= a.G) return;
+    float m = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kUnitTiles; ++w) m = fmaxf(m, tp[w][h].x);
+    float z = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kUnitTiles; ++w)
+        z += tp[w][h].x == -INFINITY ? 0.0f : tp[w][h].y * exp2f(tp[w][h].x - m);
+    const int b = bg / a.Hkv, g = bg % a.Hkv;
+    a.part[((int64_t)b * a.Hq + g * a.G + h) * a.npart + unit] = make_float2(m, z);
+}
+
+// Work unit: kUnitTiles consecutive wave-tiles of one (b, g), one per wave;
+// each workgroup walks a contiguous range of units.
 template <int DT, int GC, int OUT>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
+    __shared__ float2 tile_part[kUnitTiles][kMaxGroup];   // ATTN: per wave, per head of the group
     const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int rg = lane >> 3;
     const int l8 = lane & 7;
 
@@ -176,41 +196,50 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
             a.zero_ptr[i] = 0u;
     }
 
-    // contiguous range of wave-tiles per wave
-    const int nwaves = gridDim.x * 4;
-    const int w = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int total = a.B * a.Hkv * a.ntiles;
-    const int per = (total + nwaves - 1) / nwaves;
-    int t = w * per;
-    const int t_end = min(t + per, total);
-    if (t >= t_end) return;
+    const int total = a.B * a.Hkv * a.npart;
+    const int per = (total + gridDim.x - 1) / gridDim.x;
+    int u = blockIdx.x * per;
+    const int u_end = min(u + per, total);
 
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
     uint4 kr[kLoadsPerTile];
-    for (; t < t_end; ++t) {
-        load_tile(a, t, rg, l8, kr);
-        compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag);
+    for (; u < u_end; ++u) {
+        const int bg = u / a.npart, unit = u % a.npart;
+        const int tile = unit * kUnitTiles + wv;
+        if (tile < a.ntiles) {
+            const int t = bg * a.ntiles + tile;
+            load_tile(a, t, rg, l8, kr);
+            compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag, tile_part[wv]);
+        } else if constexpr (OUT == kOutLogits) {
+            for (int h = lane; h < a.G; h += 64) tile_part[wv][h] = make_float2(-INFINITY, 0.0f);
+        }
+        if constexpr (OUT == kOutLogits) {
+            __syncthreads();
+            merge_unit(a, bg, unit, tile_part);
+            __syncthreads();
+        }
     }
 }
 
-// One workgroup per (b, h): combine the tile pairs into (max, 1/sum), each
-// thread over a fixed strided subset, then waves in a fixed order.
+// One workgroup per (b, h): combine the unit pairs into (max, 1/sum), each
+// thread over a fixed strided subset, then waves in a fixed order.  Used when
+// the update cannot reduce them itself (long contexts).
 __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __restrict__ part,
-                                                            float2* __restrict__ stats, int ntiles)
+                                                            float2* __restrict__ stats, int npart)
 {
     __shared__ float red_m[4], red_z[4];
     const int bh = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const float2* p = part + (int64_t)bh * ntiles;
+    const float2* p = part + (int64_t)bh * npart;
     constexpr int kBatch = 8;
     float m = -INFINITY, z = 0.0f;
-    for (int i0 = tid; i0 < ntiles; i0 += 256 * kBatch) {
+    for (int i0 = tid; i0 < npart; i0 += 256 * kBatch) {
         float2 v[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int i = i0 + u * 256;
-            v[u] = i < ntiles ? p[i] : make_float2(-INFINITY, 0.0f);
+            v[u] = i < npart ? p[i] : make_float2(-INFINITY, 0.0f);
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
@@ -257,27 +286,115 @@ __device__ __forceinline__ void hist_merge(const uint32_t* lds_hist, uint32_t* g
 
 constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 
+// (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
+// stats kernel's output, or reduced here from the unit partials.  Thread t
+// works for head t / tph (tph = 256 / nh threads per head) and folds
+// partials t % tph, + tph, ... (at most kStatLoads); the tph results of a
+// head are then folded across lanes (DPP within a wave when tph is a power of
+// two up to 64, else in order through LDS).  The partial loads
+// are issued by load_head_parts() before the logits; every thread calls
+// finish_head_stats(), which ends with a barrier.
+struct HeadParts {
+    float2 v[kStatLoads];
+};
+
+__device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int h0, int nh, HeadParts& hp)
+{
+    const int tph = nh <= 256 ? 256 / nh : 1;
+    const int t = threadIdx.x, hh = t / tph, sub = t % tph;
+    const bool active = a.stats == nullptr && hh < nh;
+    const float2* p = a.part + ((int64_t)b * a.Hq + h0 + (active ? hh : 0)) * a.npart;
+#pragma unroll
+    for (int i = 0; i < kStatLoads; ++i) {
+        const int idx = sub + i * tph;   // consecutive lanes read consecutive partials
+        hp.v[i] = active && idx < a.npart ? p[idx] : make_float2(-INFINITY, 0.0f);
+    }
+}
+
+// (m, z) of two disjoint sets of exp2 terms merged (z relative to m).
+__device__ __forceinline__ void merge_mz(float& m, float& z, float mo, float zo)
+{
+    const float M = fmaxf(m, mo);
+    const float a = m == -INFINITY ? 0.0f : z * exp2f(m - M);
+    const float c = mo == -INFINITY ? 0.0f : zo * exp2f(mo - M);
+    m = M;
+    z = a + c;
+}
+
+template <int CTRL>
+__device__ __forceinline__ void merge_mz_dpp(float& m, float& z)
+{
+    const float mo = dpp<CTRL>(m), zo = dpp<CTRL>(z);
+    merge_mz(m, z, mo, zo);
+}
+
+__device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, int h0, int nh, const HeadParts& hp,
+                                                  float2* red, float2* ms)
+{
+    const int t = threadIdx.x;
+    if (a.stats) {
+        if (t < nh) ms[t] = a.stats[(int64_t)b * a.Hq + h0 + t];
+        __syncthreads();
+        return;
+    }
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kStatLoads; ++i) m = fmaxf(m, hp.v[i].x);
+    float z = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2f(hp.v[i].x - m);
+    const int tph = 256 / nh;
+    if ((tph & (tph - 1)) == 0 && tph >= 2 && tph <= 64) {
+        // every lane is active here; groups of tph lanes are aligned
+        merge_mz_dpp<0xB1>(m, z);                      // lane ^ 1
+        if (tph >= 4) merge_mz_dpp<0x4E>(m, z);        // lane ^ 2
+        if (tph >= 8) merge_mz_dpp<0x141>(m, z);       // mirror within 8
+        if (tph >= 16) merge_mz_dpp<0x140>(m, z);      // mirror within 16
+        if (tph >= 32) merge_mz(m, z, __shfl_xor(m, 16, 64), __shfl_xor(z, 16, 64));
+        if (tph >= 64) merge_mz(m, z, __shfl_xor(m, 32, 64), __shfl_xor(z, 32, 64));
+        if (t % tph == 0 && t / tph < nh) ms[t / tph] = make_float2(m, 1.0f / z);
+    } else {
+        red[t] = make_float2(m, z);
+        __syncthreads();
+        if (t < nh) {
+            float M = -INFINITY, Z = 0.0f;
+            for (int i = 0; i < tph; ++i) merge_mz(M, Z, red[t * tph + i].x, red[t * tph + i].y);
+            ms[t] = make_float2(M, 1.0f / Z);
+        }
+    }
+    __syncthreads();
+}
+
 // S[b,r,j] += sum_{h in heads(r)} exp2(s2*l - max_h) / sum_h   (softmax weights).
 // kUpdChunk = 256 tokens per workgroup: lane l of wave w loads tokens
 // [4l, 4l+4) of heads w, w+4, ... as float4; the four wave partials are added
 // in wave order, then each thread finishes one token and counts its first
-// selection digit in an LDS histogram.
+// selection digit in an LDS histogram.  The head statistics come from the
+// stats kernel or, for short rows, from the unit partials reduced here.
 __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 {
     __shared__ float4 wsum[4][64];
     __shared__ uint32_t lds_hist[kHistRow];
+    __shared__ float2 red[256];
+    __shared__ float2 ms[256];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
     const int nh = a.R == 1 ? a.Hq : a.G;
-    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool do_hist = a.hist != nullptr;
     if (do_hist)
         for (int i = tid; i < kHistRow; i += 256) lds_hist[i] = 0u;
+    HeadParts hp;
+    load_head_parts(a, b, h0, nh, hp);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
     const int jc = min(j4, (int)(a.ld - 4));              // rows are padded to ld (multiple of 4)
     const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
-    const float2* st = a.stats + (int64_t)b * a.Hq + h0;
+    // this thread's old importance, loaded with the logits
+    const int j = blockIdx.x * kUpdChunk + tid;
+    float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
+    const float s_old = j < a.n ? srow[j] : 0.0f;
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (int hb = w; hb < nh; hb += 4 * kHeadBatch) {
         float4 x[kHeadBatch];
@@ -286,26 +403,26 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
             const int h = hb + 4 * i;
             x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
+        if (hb == w) finish_head_stats(a, b, h0, nh, hp, red, ms);
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
             const int h = hb + 4 * i;
             if (h < nh) {
-                const float2 ms = st[h];
-                acc.x += exp2f(a.s2 * x[i].x - ms.x) * ms.y;
-                acc.y += exp2f(a.s2 * x[i].y - ms.x) * ms.y;
-                acc.z += exp2f(a.s2 * x[i].z - ms.x) * ms.y;
-                acc.w += exp2f(a.s2 * x[i].w - ms.x) * ms.y;
+                const float2 st = ms[h];
+                acc.x += exp2f(a.s2 * x[i].x - st.x) * st.y;
+                acc.y += exp2f(a.s2 * x[i].y - st.x) * st.y;
+                acc.z += exp2f(a.s2 * x[i].z - st.x) * st.y;
+                acc.w += exp2f(a.s2 * x[i].w - st.x) * st.y;
             }
         }
     }
+    if (w >= nh) finish_head_stats(a, b, h0, nh, hp, red, ms);   // waves without a head still join the barriers
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
-    const int j = blockIdx.x * kUpdChunk + tid;
     if (j < a.n) {
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
-        float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
-        const float s_new = srow[j] + tot;
+        const float s_new = s_old + tot;
         srow[j] = s_new;
         if (do_hist) count_key(lds_hist, order_key(s_new));
     }
@@ -328,6 +445,9 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;
     const int jc = min(j4, (int)(a.ld - 4));
     const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
+    const int j = blockIdx.x * kUpdChunk + tid;
+    float* srow = a.s + (int64_t)b * a.s_sb;
+    const float s_old = j < a.n ? srow[j] : 0.0f;
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (int gb = w; gb < a.Hkv; gb += 4 * kHeadBatch) {
         float4 x[kHeadBatch];
@@ -347,11 +467,9 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
-    const int j = blockIdx.x * kUpdChunk + tid;
     if (j < a.n) {
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
-        float* srow = a.s + (int64_t)b * a.s_sb;
-        const float s_new = srow[j] + tot;
+        const float s_new = s_old + tot;
         srow[j] = s_new;
         if (do_hist) count_key(lds_hist, order_key(s_new));
     }
@@ -373,13 +491,13 @@ int resident_per_cu(K kernel)
     return v;
 }
 
-// Persistent grid: every workgroup resident at once, each wave with at least one tile.
+// Persistent grid: every workgroup resident at once, each with at least one unit.
 template <int DT, int GC, int OUT>
 hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp ts)
 {
     auto kernel = score_tiles_kernel<DT, GC, OUT>;
-    const int64_t total = (int64_t)a.B * a.Hkv * a.ntiles;
-    int64_t grid = (total + 3) / 4;
+    const int64_t total = (int64_t)a.B * a.Hkv * a.npart;
+    int64_t grid = total;
     const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
     if (grid > cap) grid = cap;
     if (grid < 1) grid = 1;
@@ -427,9 +545,9 @@ hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int n
     return launch_score_dt<0>(a, out, gc, ncu, st, ts);
 }
 
-hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int ntiles, hipStream_t st)
+hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st)
 {
-    hipLaunchKernelGGL(softmax_stats_kernel, dim3(bh), dim3(256), 0, st, part, stats, ntiles);
+    hipLaunchKernelGGL(softmax_stats_kernel, dim3(bh), dim3(256), 0, st, part, stats, npart);
     return hipGetLastError();
 }
 

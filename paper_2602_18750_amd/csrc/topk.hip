@@ -94,13 +94,6 @@ __device__ __forceinline__ void load_keys(const float* srow, int c, int n, uint3
     }
 }
 
-__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v)
-{
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-}
-
 // A histogram row of one 12-bit digit, loaded so that thread t holds fine
 // bins i*256 + t (i < 16) and every lane holds coarse bin `lane` (the bin's
 // top 6 bits).  Fine bins 64*C .. 64*C+63 of coarse bin C then sit in
@@ -354,30 +347,38 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     uint32_t tot;
     const uint32_t pos = block_excl_scan_1b(nsel, scan_scratch, &tot);
     const int j0 = c * kSelChunk + tid * kPerThread;
-    if (writer) {
-        int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
-        uint32_t p = pos;
-#pragma unroll
-        for (int e = 0; e < kPerThread; ++e)
-            if (sel[e]) list[p++] = j0 + e;
-        if (tid == 0) r.sel_n[(int64_t)row * r.nchunks + c] = tot;
-    }
-
+    int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
     if constexpr (ATTN) {
-        // attention of the group's heads over the chunk's selected tokens:
-        // one partial per head in slot c
+        // attention of the group's heads over the chunk's selected tokens
+        // (one partial per head in slot c), then the list is stored
         uint32_t p = pos;
 #pragma unroll
         for (int e = 0; e < kPerThread; ++e)
             if (sel[e]) sh.tok[p++] = j0 + e;
         __syncthreads();
-        for (int hc = 0; hc < at.G; hc += GC) {
-            if (hc) load_queries<GC>(at, b, g, hc, qv);
+        {
+            AttnAcc<GC> acc;
+            attn_begin<GC>(acc, sh);
+            if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
+            attn_finish<GC>(at, b, g, 0, acc, c, r.nchunks, sh);
+        }
+        for (int hc = GC; hc < at.G; hc += GC) {
+            load_queries<GC>(at, b, g, hc, qv);
             AttnAcc<GC> acc;
             attn_begin<GC>(acc, sh);
             if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
             attn_finish<GC>(at, b, g, hc, acc, c, r.nchunks, sh);
         }
+        if (writer) {
+            for (uint32_t i = tid; i < tot; i += kThreads) list[i] = sh.tok[i];
+            if (tid == 0) r.sel_n[(int64_t)row * r.nchunks + c] = tot;
+        }
+    } else {
+        uint32_t p = pos;
+#pragma unroll
+        for (int e = 0; e < kPerThread; ++e)
+            if (sel[e]) list[p++] = j0 + e;
+        if (tid == 0) r.sel_n[(int64_t)row * r.nchunks + c] = tot;
     }
 }
 

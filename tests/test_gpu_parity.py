@@ -56,6 +56,10 @@ SCORE_CASES = [
     (1, 32, 8, 2049, "bf16", "attn", "token"),
     (2, 32, 8, 3000, "bf16", "raw", "token"),
     (1, 64, 2, 640, "fp16", "attn", "token"),
+    # head counts that do not divide the update's 256 threads; a row just past
+    # the length whose softmax partials the update reduces itself
+    (1, 6, 3, 2000, "fp16", "attn", "token"),
+    (1, 32, 8, 32768 + 129, "bf16", "attn", "token"),
 ]
 
 
