@@ -39,7 +39,7 @@ struct Shape {
 
 // Workspace regions, in this order, each 256-byte aligned:
 //   logits   ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
-//   part     ATTN [B,Hq,npart] float2 (per 128-token unit);  stats ATTN [B,Hq] float2
+//   part     ATTN [B,Hq,npart] float2 (per 256-token unit);  stats ATTN [B,Hq] float2
 //   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins; cleared by the first kernel of every call
 //            that accumulates into them)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
@@ -154,7 +154,7 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     s->n = d->n_tokens;
     s->R = R;
     s->ntiles = (d->n_tokens + kScoreTile - 1) / kScoreTile;
-    s->npart = (s->ntiles + kUnitTiles - 1) / kUnitTiles;
+    s->npart = ((s->ntiles + kUnitTiles - 1) / kUnitTiles + 1) / 2 * 2;   // even: the update reads pairs
     s->ld = ((int64_t)d->n_tokens + 3) / 4 * 4;
     s->dtype = d->dtype;
     s->mode = d->score_mode;

@@ -244,6 +244,25 @@ __device__ __forceinline__ uint2 block_excl_scan2(uint2 v, uint2* scratch, uint2
     return make_uint2(base.x + inc.x - v.x, base.y + inc.y - v.y);
 }
 
+// Workgroup histogram in LDS that also lists the bins it touched, so that
+// only those are added to the global histogram.  `bins` starts zeroed and
+// *nlist at 0; `list` holds at least as many entries as distinct bins can
+// be touched.
+__device__ __forceinline__ void hist_add(uint32_t* bins, uint32_t* list, uint32_t* nlist, uint32_t bin)
+{
+    if (atomicAdd(&bins[bin], 1u) == 0u) list[atomicAdd(nlist, 1u)] = bin;
+}
+
+// Adds the touched bins to the global histogram (one integer atomic each:
+// order-independent).  Called by every thread after a barrier.
+__device__ __forceinline__ void hist_flush(const uint32_t* bins, const uint32_t* list, uint32_t nlist, uint32_t* ghist)
+{
+    for (uint32_t i = threadIdx.x; i < nlist; i += blockDim.x) {
+        const uint32_t b = list[i];
+        atomicAdd(ghist + b, bins[b]);
+    }
+}
+
 // Order-preserving map of fp32 to uint32: larger float -> larger key.
 // -0.0 is folded onto +0.0; every NaN maps to 0, below -inf.
 __device__ __forceinline__ uint32_t order_key(float f)

@@ -9,9 +9,9 @@ namespace hill {
 
 constexpr int kHeadDim = 128;      // D supported by every kernel
 constexpr int kScoreTile = 32;     // tokens per scoring wave-tile
-constexpr int kUnitTiles = 4;      // wave-tiles per scoring workgroup unit (softmax partial granularity)
+constexpr int kUnitTiles = 8;      // wave-tiles per scoring workgroup unit (softmax partial granularity)
 constexpr int kMaxGroup = 128;     // query heads per KV head supported
-constexpr int kStatLoads = 32;     // softmax partials per thread when the update reduces them itself
+constexpr int kStatLoads = 16;     // softmax partials per thread when the update reduces them itself
 constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;    // each 12-bit digit histogram also counts its top 6 bits
@@ -32,7 +32,7 @@ struct ScoreArgs {
     int64_t q_sb, q_sh;
     int64_t k_sb, k_sh, k_sn;
     int B, Hq, Hkv, G, n, ntiles;
-    int npart;               // workgroup units per (b, g): ceil(ntiles / kUnitTiles)
+    int npart;               // workgroup units per (b, g): ceil(ntiles / kUnitTiles) rounded up to even
     int64_t ld;              // row stride of the logits buffer (n rounded up to 4)
     float s2;                // sm_scale * log2(e): logits are kept in the exp2 domain
     float* logits;           // kOutLogits: [B,Hq,ld]; kOutRawGroups: [B,Hkv,ld]

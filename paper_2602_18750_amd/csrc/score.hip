@@ -163,29 +163,30 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, 
     }
 }
 
-// Merges the four waves' tile pairs of every head of the group into the
-// unit's pair (fixed order), by threads 0 .. G-1.
+// Merges the unit's tile pairs of every head of the group into the unit's
+// pair (tile order), by threads 0 .. G-1.
 __device__ __forceinline__ void merge_unit(const ScoreArgs& a, int bg, int unit, const float2 (*tp)[kMaxGroup])
 {
     const int h = threadIdx.x;
     if (h >= a.G) return;
     float m = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < kUnitTiles; ++w) m = fmaxf(m, tp[w][h].x);
+    for (int i = 0; i < kUnitTiles; ++i) m = fmaxf(m, tp[i][h].x);
     float z = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kUnitTiles; ++w)
-        z += tp[w][h].x == -INFINITY ? 0.0f : tp[w][h].y * exp2f(tp[w][h].x - m);
+    for (int i = 0; i < kUnitTiles; ++i)
+        z += tp[i][h].x == -INFINITY ? 0.0f : tp[i][h].y * exp2f(tp[i][h].x - m);
     const int b = bg / a.Hkv, g = bg % a.Hkv;
     a.part[((int64_t)b * a.Hq + g * a.G + h) * a.npart + unit] = make_float2(m, z);
 }
 
-// Work unit: kUnitTiles consecutive wave-tiles of one (b, g), one per wave;
-// each workgroup walks a contiguous range of units.
+// Work unit: kUnitTiles consecutive wave-tiles of one (b, g); wave w takes
+// tiles w, w+4, ... of the unit.  Each workgroup walks a contiguous range of
+// units.
 template <int DT, int GC, int OUT>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
-    __shared__ float2 tile_part[kUnitTiles][kMaxGroup];   // ATTN: per wave, per head of the group
+    __shared__ float2 tile_part[kUnitTiles][kMaxGroup];   // ATTN: per tile of the unit, per head of the group
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int rg = lane >> 3;
@@ -206,13 +207,16 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
     uint4 kr[kLoadsPerTile];
     for (; u < u_end; ++u) {
         const int bg = u / a.npart, unit = u % a.npart;
-        const int tile = unit * kUnitTiles + wv;
-        if (tile < a.ntiles) {
-            const int t = bg * a.ntiles + tile;
-            load_tile(a, t, rg, l8, kr);
-            compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag, tile_part[wv]);
-        } else if constexpr (OUT == kOutLogits) {
-            for (int h = lane; h < a.G; h += 64) tile_part[wv][h] = make_float2(-INFINITY, 0.0f);
+#pragma unroll
+        for (int i = wv; i < kUnitTiles; i += 4) {
+            const int tile = unit * kUnitTiles + i;
+            if (tile < a.ntiles) {
+                const int t = bg * a.ntiles + tile;
+                load_tile(a, t, rg, l8, kr);
+                compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag, tile_part[i]);
+            } else if constexpr (OUT == kOutLogits) {
+                for (int h = lane; h < a.G; h += 64) tile_part[i][h] = make_float2(-INFINITY, 0.0f);
+            }
         }
         if constexpr (OUT == kOutLogits) {
             __syncthreads();
@@ -266,30 +270,33 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
     }
 }
 
-// Counts a selection key in the first-digit histogram (bits 31..20) and its
-// coarse bins (bits 31..26).
-__device__ __forceinline__ void count_key(uint32_t* lds_hist, uint32_t key)
+// First-digit histogram of the importance keys a workgroup writes (bits
+// 31..20, and the coarse bins of bits 31..26), merged sparsely.
+struct KeyHist {
+    uint32_t bins[kHistRow];
+    uint32_t list[2 * kUpdChunk];
+    uint32_t nlist;
+};
+
+__device__ __forceinline__ void key_hist_clear(KeyHist& h)
 {
-    atomicAdd(&lds_hist[key >> (32 - kHistBits)], 1u);
-    atomicAdd(&lds_hist[kHistBins + (key >> 26)], 1u);
+    for (int i = threadIdx.x; i < kHistRow; i += 256) h.bins[i] = 0u;
+    if (threadIdx.x == 0) h.nlist = 0u;
 }
 
-// Merges a workgroup's LDS histogram into the row's global histogram: one
-// integer atomic per non-empty bin (order-independent result).
-__device__ __forceinline__ void hist_merge(const uint32_t* lds_hist, uint32_t* ghist)
+__device__ __forceinline__ void count_key(KeyHist& h, uint32_t key)
 {
-    for (int i = threadIdx.x; i < kHistRow; i += 256) {
-        const uint32_t c = lds_hist[i];
-        if (c) atomicAdd(ghist + i, c);
-    }
+    hist_add(h.bins, h.list, &h.nlist, key >> (32 - kHistBits));
+    hist_add(h.bins, h.list, &h.nlist, kHistBins + (key >> 26));
 }
 
 constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
 // stats kernel's output, or reduced here from the unit partials.  Thread t
-// works for head t / tph (tph = 256 / nh threads per head) and folds
-// partials t % tph, + tph, ... (at most kStatLoads); the tph results of a
+// works for head t / tph (tph = 256 / nh threads per head) and folds the
+// partial pairs t % tph, + tph, ... (at most kStatLoads partials); the tph
+// results of a
 // head are then folded across lanes (DPP within a wave when tph is a power of
 // two up to 64, else in order through LDS).  The partial loads
 // are issued by load_head_parts() before the logits; every thread calls
@@ -303,11 +310,18 @@ __device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int 
     const int tph = nh <= 256 ? 256 / nh : 1;
     const int t = threadIdx.x, hh = t / tph, sub = t % tph;
     const bool active = a.stats == nullptr && hh < nh;
-    const float2* p = a.part + ((int64_t)b * a.Hq + h0 + (active ? hh : 0)) * a.npart;
+    // npart is even and the rows 16-byte aligned: pairs of partials per load
+    const float4* p = reinterpret_cast<const float4*>(a.part + ((int64_t)b * a.Hq + h0 + (active ? hh : 0)) * a.npart);
+    const int npair = a.npart / 2;
 #pragma unroll
-    for (int i = 0; i < kStatLoads; ++i) {
-        const int idx = sub + i * tph;   // consecutive lanes read consecutive partials
-        hp.v[i] = active && idx < a.npart ? p[idx] : make_float2(-INFINITY, 0.0f);
+    for (int i = 0; i < kStatLoads / 2; ++i) {
+        // consecutive lanes read consecutive pairs; unconditional (clamped)
+        // loads, invalid ones replaced afterwards
+        const int idx = sub + i * tph;
+        const float4 v = p[min(idx, npair - 1)];
+        const bool ok = active && idx < npair;
+        hp.v[2 * i] = ok ? make_float2(v.x, v.y) : make_float2(-INFINITY, 0.0f);
+        hp.v[2 * i + 1] = ok ? make_float2(v.z, v.w) : make_float2(-INFINITY, 0.0f);
     }
 }
 
@@ -374,7 +388,7 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
 __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 {
     __shared__ float4 wsum[4][64];
-    __shared__ uint32_t lds_hist[kHistRow];
+    __shared__ KeyHist kh;
     __shared__ float2 red[256];
     __shared__ float2 ms[256];
     const int row = blockIdx.y;          // b * R + r
@@ -384,8 +398,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool do_hist = a.hist != nullptr;
-    if (do_hist)
-        for (int i = tid; i < kHistRow; i += 256) lds_hist[i] = 0u;
+    if (do_hist) key_hist_clear(kh);
     HeadParts hp;
     load_head_parts(a, b, h0, nh, hp);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
@@ -395,15 +408,17 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int j = blockIdx.x * kUpdChunk + tid;
     float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
     const float s_old = j < a.n ? srow[j] : 0.0f;
-    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int hb = w; hb < nh; hb += 4 * kHeadBatch) {
-        float4 x[kHeadBatch];
+    // the first batch of logits is issued before the statistics are folded
+    float4 x[kHeadBatch];
 #pragma unroll
-        for (int i = 0; i < kHeadBatch; ++i) {
-            const int h = hb + 4 * i;
-            x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
-        if (hb == w) finish_head_stats(a, b, h0, nh, hp, red, ms);
+    for (int i = 0; i < kHeadBatch; ++i) {
+        const int h = w + 4 * i;
+        x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    finish_head_stats(a, b, h0, nh, hp, red, ms);
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int hb = w;;) {
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
             const int h = hb + 4 * i;
@@ -415,8 +430,14 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
                 acc.w += exp2f(a.s2 * x[i].w - st.x) * st.y;
             }
         }
+        hb += 4 * kHeadBatch;
+        if (hb >= nh) break;
+#pragma unroll
+        for (int i = 0; i < kHeadBatch; ++i) {
+            const int h = hb + 4 * i;
+            x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
-    if (w >= nh) finish_head_stats(a, b, h0, nh, hp, red, ms);   // waves without a head still join the barriers
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
@@ -424,11 +445,11 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
-        if (do_hist) count_key(lds_hist, order_key(s_new));
+        if (do_hist) count_key(kh, order_key(s_new));
     }
     if (do_hist) {
         __syncthreads();
-        hist_merge(lds_hist, a.hist + (int64_t)row * kHistRow);
+        hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)row * kHistRow);
     }
 }
 
@@ -436,12 +457,11 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
 {
     __shared__ float4 wsum[4][64];
-    __shared__ uint32_t lds_hist[kHistRow];
+    __shared__ KeyHist kh;
     const int b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
-    if (do_hist)
-        for (int i = tid; i < kHistRow; i += 256) lds_hist[i] = 0u;
+    if (do_hist) key_hist_clear(kh);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;
     const int jc = min(j4, (int)(a.ld - 4));
     const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
@@ -471,11 +491,11 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
-        if (do_hist) count_key(lds_hist, order_key(s_new));
+        if (do_hist) count_key(kh, order_key(s_new));
     }
     if (do_hist) {
         __syncthreads();
-        hist_merge(lds_hist, a.hist + (int64_t)b * kHistRow);
+        hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)b * kHistRow);
     }
 }
 

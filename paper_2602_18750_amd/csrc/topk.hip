@@ -46,9 +46,12 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict_
                                                         int R, int n, uint32_t* __restrict__ hist)
 {
     __shared__ uint32_t lds_hist[kHistRow];
+    __shared__ uint32_t list[kHistRow];
+    __shared__ uint32_t nlist;
     const int row = blockIdx.y;
     const int b = row / R, r = row % R;
     for (int i = threadIdx.x; i < kHistRow; i += 256) lds_hist[i] = 0u;
+    if (threadIdx.x == 0) nlist = 0u;
     __syncthreads();
     const float* srow = s + (int64_t)b * s_sb + (int64_t)r * s_sr;
     constexpr int kPer = kHistChunk / 256;
@@ -57,16 +60,12 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict_
         const int j = blockIdx.x * kHistChunk + i * 256 + threadIdx.x;
         if (j < n) {
             const uint32_t kk = order_key(srow[j]);
-            atomicAdd(&lds_hist[kk >> (32 - kHistBits)], 1u);
-            atomicAdd(&lds_hist[kHistBins + (kk >> 26)], 1u);
+            hist_add(lds_hist, list, &nlist, kk >> (32 - kHistBits));
+            hist_add(lds_hist, list, &nlist, kHistBins + (kk >> 26));
         }
     }
     __syncthreads();
-    uint32_t* gh = hist + (int64_t)row * kHistRow;
-    for (int i = threadIdx.x; i < kHistRow; i += 256) {
-        const uint32_t c = lds_hist[i];
-        if (c) atomicAdd(gh + i, c);
-    }
+    hist_flush(lds_hist, list, nlist, hist + (int64_t)row * kHistRow);
 }
 
 __device__ __forceinline__ const float* row_ptr(const RefineArgs& a, int row)
@@ -175,8 +174,9 @@ __device__ void find_bin(const uint32_t* hist, int nb, uint32_t need, uint32_t* 
 __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
 {
     __shared__ uint32_t hist[kHistRow];
+    __shared__ uint32_t list[2 * kSelChunk];
     __shared__ uint32_t res[3];
-    __shared__ uint32_t n_cand;
+    __shared__ uint32_t n_cand, nlist;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int c = blockIdx.x, row = blockIdx.y;
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     DigitHist h1;
     load_digit_hist(a.hist1 + (int64_t)row * kHistRow, h1);
     for (int i = tid; i < kHistRow; i += kThreads) hist[i] = 0u;
-    if (tid == 0) n_cand = 0u;
+    if (tid == 0) n_cand = nlist = 0u;
     // first digit: the bin of the k-th key
     find_digit(h1, (uint32_t)a.k, res);
     __syncthreads();
@@ -207,8 +207,8 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     for (int e = 0; e < kPerThread; ++e) {
         const bool is_c = ok[e] && (key[e] >> 20) == b1;
         if (is_c && refine) {
-            atomicAdd(&hist[(key[e] >> 8) & (kHistBins - 1)], 1u);
-            atomicAdd(&hist[kHistBins + ((key[e] >> 14) & (kCoarseBins - 1))], 1u);
+            hist_add(hist, list, &nlist, (key[e] >> 8) & (kHistBins - 1));
+            hist_add(hist, list, &nlist, kHistBins + ((key[e] >> 14) & (kCoarseBins - 1)));
         }
         const uint64_t mask = __ballot(is_c);
         if (mask) {
@@ -220,13 +220,7 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
         }
     }
     __syncthreads();
-    if (refine) {
-        uint32_t* h2 = a.hist2 + (int64_t)row * kHistRow;
-        for (int i = tid; i < kHistRow; i += kThreads) {
-            const uint32_t v = hist[i];
-            if (v) atomicAdd(h2 + i, v);
-        }
-    }
+    if (refine) hist_flush(hist, list, nlist, a.hist2 + (int64_t)row * kHistRow);
     if (tid == 0) a.cand_n[(int64_t)row * a.nchunks + c] = n_cand;
 }
 
