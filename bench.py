@@ -90,12 +90,14 @@ class HipEvents:
 
 def scan_kernel_bytes(B, Hq, Hkv, D, n, mode="attn"):
     """Algorithmic bytes of one score_tiles launch: every key read once, plus
-    (ATTN) the fp32 logits and per-32-token (max, sum) pairs written."""
+    (ATTN) the fp32 logits and the per-256-token (max, sum) pairs of every
+    head written (an even number of pairs per head)."""
     kbytes = B * Hkv * n * D * 2
     if mode != "attn":
         return kbytes + B * n * 4 * 2
-    ntiles = (n + 31) // 32
-    return kbytes + B * Hq * n * 4 + B * Hq * ntiles * 8
+    units = (n + 255) // 256
+    npart = (units + 1) // 2 * 2
+    return kbytes + B * Hq * n * 4 + B * Hq * npart * 8
 
 
 def load_traffic(per_launch_bytes_hint=None):
