@@ -27,8 +27,8 @@
 namespace hill {
 
 constexpr int kAttnBlock = 512;   // list entries per LDS block
-constexpr int kKBatch = 4;        // K rows in flight per row group (phase A)
-constexpr int kVBatch = 16;       // V rows in flight per wave (phase C)
+constexpr int kKBatch = 4;        // K rows per row group per batch (64 entries)
+constexpr int kVBatch = 16;       // V rows per wave per batch (64 entries)
 
 template <int GC>
 struct AttnLds {
@@ -77,10 +77,11 @@ __device__ __forceinline__ uint64_t row_off(int j, int n, int64_t stride)
     return (uint64_t)(uint32_t)j * (uint32_t)stride;
 }
 
-// K rows of entries t0, t0+16, ... (kKBatch of them, clamped to the last
-// entry) for this lane's 16-byte slice.
-__device__ __forceinline__ void load_k_batch(const AttnArgs& a, const uint16_t* kb, const int32_t* tok, int t0,
-                                             int cnt, uint4 (&kr)[kKBatch])
+// K rows of entries t0, t0+16, ... (kKBatch of them) for this lane's
+// 16-byte slice; entries past cnt are clamped to the last one (their logits
+// are not stored).  Unconditional loads keep the wait counters exact.
+__device__ __forceinline__ void load_k_rows(const AttnArgs& a, const uint16_t* kb, const int32_t* tok, int t0, int cnt,
+                                            uint4 (&kr)[kKBatch])
 {
 #pragma unroll
     for (int u = 0; u < kKBatch; ++u) {
@@ -89,28 +90,29 @@ __device__ __forceinline__ void load_k_batch(const AttnArgs& a, const uint16_t* 
     }
 }
 
-// V element pairs of entries w + 4*(i0 + i), i < kVBatch (clamped to the
-// last entry).
-__device__ __forceinline__ void load_v_batch(const AttnArgs& a, const uint16_t* vb, const int32_t* tok, int w,
-                                             int i0, int cnt, uint32_t (&vr)[kVBatch])
+// V element pairs of entries t0, t0+4, ... (kVBatch of them); entries past
+// cnt are clamped to the last one (they weigh 0).
+__device__ __forceinline__ void load_v_rows(const AttnArgs& a, const uint16_t* vb, const int32_t* tok, int t0, int cnt,
+                                            uint32_t (&vr)[kVBatch])
 {
 #pragma unroll
     for (int i = 0; i < kVBatch; ++i) {
-        const int t = min(w + 4 * (i0 + i), cnt - 1);
+        const int t = min(t0 + 4 * i, cnt - 1);
         vr[i] = *reinterpret_cast<const uint32_t*>(vb + row_off(tok[t], a.n, a.v_sn));
     }
 }
 
-// Logits of the batch's entries into sh.p (lane l16 == hh of the row group
-// writes head hh; entries past cnt are computed on the clamped row and not
-// stored).
+// Logits of entries t0, t0+16, ... into sh.p (lane l16 == hh of the row group
+// writes head hh).  nu (wave-uniform) bounds the batches that hold an entry
+// of any row group of the wave; entries past cnt are not stored.
 template <int DT, int GC>
-__device__ __forceinline__ void logits_batch(const AttnArgs& a, const uint4 (&qv)[GC], const uint4 (&kr)[kKBatch],
-                                             int t0, int cnt, float (*p)[GC])
+__device__ __forceinline__ void logits_rows(const AttnArgs& a, const uint4 (&qv)[GC], const uint4 (&kr)[kKBatch], int t0,
+                                            int cnt, int nu, float (*p)[GC])
 {
     const int l16 = threadIdx.x & 15;
 #pragma unroll
     for (int u = 0; u < kKBatch; ++u) {
+        if (u >= nu) break;
         const int t = t0 + 16 * u;
         float mine = 0.0f;   // lane l16 == hh keeps head hh's dot product
 #pragma unroll
@@ -122,11 +124,50 @@ __device__ __forceinline__ void logits_batch(const AttnArgs& a, const uint4 (&qv
     }
 }
 
+// weight * V of this wave's entries idx0 .. idx0+N-1 (entry w + 4*idx) into
+// the accumulators; entries at or past nmine weigh 0.
+template <int DT, int GC>
+__device__ __forceinline__ void values_rows(const uint32_t (&vr)[kVBatch], int w, int idx0, int nmine, int cnt,
+                                            const float (*p)[GC], AttnAcc<GC>& acc)
+{
+#pragma unroll
+    for (int c0 = 0; c0 < kVBatch; c0 += 8) {
+        if (idx0 + c0 >= nmine) break;   // wave-uniform
+#pragma unroll
+        for (int i = c0; i < c0 + 8; ++i) {
+            const int idx = idx0 + i;
+            const int tc = min(w + 4 * idx, cnt - 1);
+            float v0, v1;
+            widen2<DT>(vr[i], v0, v1);
+            float pw[GC];
+            if constexpr (GC % 4 == 0) {
+#pragma unroll
+                for (int h4 = 0; h4 < GC; h4 += 4) {
+                    const float4 x = *reinterpret_cast<const float4*>(&p[tc][h4]);
+                    pw[h4] = x.x;
+                    pw[h4 + 1] = x.y;
+                    pw[h4 + 2] = x.z;
+                    pw[h4 + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int hh = 0; hh < GC; ++hh) pw[hh] = p[tc][hh];
+            }
+#pragma unroll
+            for (int hh = 0; hh < GC; ++hh) {
+                const float pv = idx < nmine ? pw[hh] : 0.0f;
+                acc.o[hh][0] += pv * v0;
+                acc.o[hh][1] += pv * v1;
+            }
+        }
+    }
+}
+
 // Folds list entries [0, cnt) of sh.tok (1 <= cnt <= kAttnBlock, written and
 // made visible by a barrier before the call) into the running state.  Every
-// thread of the workgroup must call this.  The first K batch is issued
-// before the first V batch so that the logits wait for K only; all loads are
-// unconditional (clamped) so the counters stay exact.
+// thread of the workgroup must call this.  The K rows are issued before the
+// V rows, so that the logits wait for K only; every loop bound is
+// wave-uniform.
 template <int DT, int GC>
 __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, const uint4 (&qv)[GC], int cnt,
                                            AttnAcc<GC>& acc, AttnLds<GC>& sh)
@@ -137,16 +178,24 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
     const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
     const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
 
-    // A: logits of every entry, into sh.p; the first V batch is in flight meanwhile
-    uint4 kr[kKBatch];
-    load_k_batch(a, kb, sh.tok, rg, cnt, kr);
+    // A: logits of every entry, into sh.p.  Up to 128 entries take one round
+    // trip: the K rows of entries < 64 (and < 128 when the list is longer),
+    // then the V rows of this wave's first 16 (and 32) entries.
+    const int nmine = cnt > w ? (cnt - w + 3) / 4 : 0;   // this wave's entries w, w+4, ...
+    const bool two = cnt > 16 * kKBatch;                 // block-uniform
+    uint4 kr[kKBatch], kr2[kKBatch];
+    load_k_rows(a, kb, sh.tok, rg, cnt, kr);
+    if (two) load_k_rows(a, kb, sh.tok, rg + 16 * kKBatch, cnt, kr2);
     __builtin_amdgcn_sched_barrier(0);   // keep the K loads ahead of the V loads in the queue
-    uint32_t vr[kVBatch];
-    load_v_batch(a, vb, sh.tok, w, 0, cnt, vr);
-    logits_batch<DT, GC>(a, qv, kr, rg, cnt, sh.p);
-    for (int t0 = rg + 16 * kKBatch; t0 < cnt; t0 += 16 * kKBatch) {
-        load_k_batch(a, kb, sh.tok, t0, cnt, kr);
-        logits_batch<DT, GC>(a, qv, kr, t0, cnt, sh.p);
+    uint32_t vr[kVBatch], vr2[kVBatch];
+    load_v_rows(a, vb, sh.tok, w, cnt, vr);
+    if (two) load_v_rows(a, vb, sh.tok, w + 4 * kVBatch, cnt, vr2);
+    logits_rows<DT, GC>(a, qv, kr, rg, cnt, (cnt - 4 * w + 15) / 16, sh.p);
+    if (two) logits_rows<DT, GC>(a, qv, kr2, rg + 16 * kKBatch, cnt, (cnt - 16 * kKBatch - 4 * w + 15) / 16, sh.p);
+    for (int base = 32 * kKBatch; base < cnt; base += 16 * kKBatch) {   // lists longer than 128
+        uint4 kx[kKBatch];
+        load_k_rows(a, kb, sh.tok, base + rg, cnt, kx);
+        logits_rows<DT, GC>(a, qv, kx, base + rg, cnt, (cnt - base - 4 * w + 15) / 16, sh.p);
     }
     __syncthreads();
 
@@ -173,44 +222,19 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
     }
     __syncthreads();
 
-    // C: weight * V over this wave's entries
+    // C: weight * V over this wave's entries w, w+4, ...
 #pragma unroll
     for (int hh = 0; hh < GC; ++hh) {
         const float al = sh.alpha[hh];
         acc.o[hh][0] *= al;
         acc.o[hh][1] *= al;
     }
-    for (int i0 = 0;; i0 += kVBatch) {
-        // branch-free over the batch: entries past cnt weigh 0
-#pragma unroll
-        for (int i = 0; i < kVBatch; ++i) {
-            const int t = w + 4 * (i0 + i);
-            const int tc = min(t, cnt - 1);
-            float v0, v1;
-            widen2<DT>(vr[i], v0, v1);
-            float pw[GC];
-            if constexpr (GC % 4 == 0) {
-#pragma unroll
-                for (int h4 = 0; h4 < GC; h4 += 4) {
-                    const float4 x = *reinterpret_cast<const float4*>(&sh.p[tc][h4]);
-                    pw[h4] = x.x;
-                    pw[h4 + 1] = x.y;
-                    pw[h4 + 2] = x.z;
-                    pw[h4 + 3] = x.w;
-                }
-            } else {
-#pragma unroll
-                for (int hh = 0; hh < GC; ++hh) pw[hh] = sh.p[tc][hh];
-            }
-#pragma unroll
-            for (int hh = 0; hh < GC; ++hh) {
-                const float pv = t < cnt ? pw[hh] : 0.0f;
-                acc.o[hh][0] += pv * v0;
-                acc.o[hh][1] += pv * v1;
-            }
-        }
-        if (w + 4 * (i0 + kVBatch) >= cnt) break;
-        load_v_batch(a, vb, sh.tok, w, i0 + kVBatch, cnt, vr);
+    values_rows<DT, GC>(vr, w, 0, nmine, cnt, sh.p, acc);
+    if (two) values_rows<DT, GC>(vr2, w, kVBatch, nmine, cnt, sh.p, acc);
+    for (int i0 = 2 * kVBatch; i0 < nmine; i0 += kVBatch) {   // lists longer than 128
+        uint32_t vx[kVBatch];
+        load_v_rows(a, vb, sh.tok, w + 4 * i0, cnt, vx);
+        values_rows<DT, GC>(vx, w, i0, nmine, cnt, sh.p, acc);
     }
 }
 
