@@ -352,6 +352,7 @@ AttnArgs attn_args(const hill_desc* d, const Shape& s, const Layout& L, const vo
     a.ksel = ksel;
     a.nsplit = L.nsplit;
     a.per_split = L.per_split;
+    a.kv_per_wg = emit_kv_per_wg(s.B, s.Hkv, L.nchunks, s.R);
     a.s2 = s.scale * 1.4426950408889634f;
     a.part_o = at<float>(ws, L.slot_o);
     a.part_ml = at<float2>(ws, L.slot_ml);

@@ -65,6 +65,7 @@ struct AttnArgs {
     int64_t v_sb, v_sh, v_sn;
     const int32_t* idx;      // [B, R, ksel]
     int B, Hq, Hkv, G, R, n, ksel, nsplit, per_split;
+    int kv_per_wg;           // fused select+attend, token rows: KV heads per workgroup (divides Hkv)
     float s2;
     float* part_o;           // [B,Hq,nsplit,D]
     float2* part_ml;         // [B,Hq,nsplit] (max, sum) in the exp2 domain
@@ -101,6 +102,18 @@ inline int attn_splits(int64_t b_hkv, int ksel, int* per_split)
     return (ksel + p - 1) / p;   // every split non-empty; at most target_wgs
 }
 constexpr int kMaxSplits = 512;
+
+// KV heads per fused select+attend workgroup for token rows: the largest
+// power of two dividing Hkv that still leaves about eight workgroups per CU,
+// so that large batches stop repeating the chunk's selection per KV head.
+inline int emit_kv_per_wg(int B, int Hkv, int nchunks, int R)
+{
+    if (R != 1) return 1;
+    const int64_t target = 2048;
+    int h = 1;
+    while (h * 2 <= Hkv && Hkv % (h * 2) == 0 && (int64_t)B * nchunks * (Hkv / (h * 2)) >= target) h *= 2;
+    return h;
+}
 constexpr int kMaxSlots = 4096;   // partial slots merged per head (splits or chunks)
 
 // Optional start/stop timestamps of one launch (hipExtLaunchKernel events).

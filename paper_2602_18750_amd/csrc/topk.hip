@@ -249,15 +249,18 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int c = blockIdx.x;
-    int row, b = 0, g = 0;
+    int row, b = 0, g = 0, ng = 1;
     if constexpr (ATTN) {
-        b = blockIdx.y / at.Hkv;
-        g = blockIdx.y % at.Hkv;
-        row = r.R == 1 ? b : blockIdx.y;
+        // KV heads g .. g+ng-1 of sequence b (ng > 1 only for token rows)
+        ng = at.kv_per_wg;
+        const int groups = at.Hkv / ng;
+        b = blockIdx.y / groups;
+        g = (blockIdx.y % groups) * ng;
+        row = r.R == 1 ? b : b * at.Hkv + g;
     } else {
         row = blockIdx.y;
     }
-    // one workgroup per chunk stores the list (token rows: KV head 0)
+    // one workgroup per chunk stores the list (token rows: the one with KV head 0)
     const bool writer = !ATTN || r.R != 1 || g == 0;
 
     // independent loads first: queries, this chunk's keys, the row's state and
@@ -350,18 +353,19 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         for (int e = 0; e < kPerThread; ++e)
             if (sel[e]) sh.tok[p++] = j0 + e;
         __syncthreads();
-        {
+        {   // the first head chunk with the queries loaded at the start
             AttnAcc<GC> acc;
             attn_begin<GC>(acc, sh);
             if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
             attn_finish<GC>(at, b, g, 0, acc, c, r.nchunks, sh);
         }
-        for (int hc = GC; hc < at.G; hc += GC) {
-            load_queries<GC>(at, b, g, hc, qv);
+        for (int i = 1; i < ng * (at.G / GC); ++i) {   // further head chunks and KV heads
+            const int gg = g + i / (at.G / GC), hc = (i % (at.G / GC)) * GC;
+            load_queries<GC>(at, b, gg, hc, qv);
             AttnAcc<GC> acc;
             attn_begin<GC>(acc, sh);
-            if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
-            attn_finish<GC>(at, b, g, hc, acc, c, r.nchunks, sh);
+            if (tot) attn_block<DT, GC>(at, b, gg, qv, (int)tot, acc, sh);
+            attn_finish<GC>(at, b, gg, hc, acc, c, r.nchunks, sh);
         }
         if (writer) {
             for (uint32_t i = tid; i < tot; i += kThreads) list[i] = sh.tok[i];
@@ -429,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void merge_write_kernel(RefineArgs r, Att
 template <int DT, int GC>
 void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
 {
-    dim3 grid(r.nchunks, at.B * at.Hkv);
+    dim3 grid(r.nchunks, at.B * (at.Hkv / at.kv_per_wg));
     hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at);
 }
 
