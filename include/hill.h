@@ -137,8 +137,9 @@ hill_status hill_topk(const hill_desc* d, const float* s, int32_t k_sel,
 
 /* Sparse decode attention over the selected tokens (Eq. 1 restricted to I,
  * softmax renormalised over I).  idx: [B, R, k_sel] int32, each row k_sel
- * distinct indices in [0, n_tokens) in any order (not checked on device;
- * out-of-range indices are undefined behaviour).  out: [B, Hq, D] fp32. */
+ * distinct indices in [0, n_tokens) in any order (not checked on device: an
+ * out-of-range index is clamped into [0, n_tokens), so it never reads out of
+ * bounds, and the result is then unspecified).  out: [B, Hq, D] fp32. */
 hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v,
                              const int32_t* idx, int32_t k_sel, float* out,
                              void* ws, size_t ws_bytes, void* stream);
@@ -160,7 +161,7 @@ typedef struct hill_step_events {
     void* scan_start;    /* start of the kernel that streams the keys (q.K^T) */
     void* scan_stop;     /* end of that kernel */
     void* score_stop;    /* end of the last kernel that updates S */
-    void* select_start;  /* start of the selection kernel that writes the indices */
+    void* select_start;  /* start of the first selection kernel (threshold refinement) */
     void* select_stop;   /* end of it */
     void* attn_stop;     /* end of the last attention kernel (output written) */
 } hill_step_events;

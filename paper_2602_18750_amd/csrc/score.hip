@@ -3,10 +3,11 @@
 //  score_tiles   streams every cached key row once and forms the raw logits
 //                q.K^T of all query heads that share it (GQA group)
 //                (Sec. 4.4 raw inner product; Eq. 1).  ATTN keeps the logits
-//                and a per-tile (max, sum of exp2) pair per head; RAW sums
-//                each head group per token.
-//  softmax_stats reduces the tile pairs to one (max, 1/sum) per head: the
-//                softmax normaliser over all n tokens of Eq. 1.
+//                and, per 256-token unit, a (max, sum of exp2) pair per head;
+//                RAW sums each head group per token.
+//  softmax_stats reduces the unit pairs to one (max, 1/sum) per head: the
+//                softmax normaliser over all n tokens of Eq. 1.  Only for
+//                rows longer than the update can reduce itself.
 //  update_*      turns logits into weights and adds their per-row column sum
 //                to the cumulative importance S (Sec. 4.1 metric), and counts
 //                the first radix digit of the new S for the selection.
@@ -14,14 +15,14 @@
 // score_tiles layout.  A key row is 256 bytes (D = 128 x 16 bit).  Eight
 // lanes share a row: lane l8 reads elements [8*l8, 8*l8+8) with one 16-byte
 // load and [64+8*l8, 64+8*l8+8) with a second, so each load instruction of a
-// wave covers whole 128-byte lines of 8 rows.  The work item is a wave-tile
-// of 32 consecutive tokens of one (sequence, KV head): row group rg (lanes
-// 8*rg .. 8*rg+7) owns tokens j0 + 4*rg .. j0 + 4*rg + 3.  Waves run
-// independently (no LDS, no barriers); each wave walks a contiguous range of
-// wave-tiles and keeps the group's queries in registers while (b, g) stays
-// the same.  Latency is hidden by occupancy (several waves per SIMD) rather
-// than by double-buffering, which costs more registers than it returns.
-// Partial dot products are combined by three DPP adds.
+// wave covers whole 128-byte lines of 8 rows.  A wave-tile is 32 consecutive
+// tokens of one (sequence, KV head): row group rg (lanes 8*rg .. 8*rg+7) owns
+// tokens j0 + 4*rg .. j0 + 4*rg + 3.  A workgroup unit is 8 wave-tiles (256
+// tokens; each wave takes two); the tiles' pairs are merged in LDS into one
+// pair per head.  Queries stay in registers while (b, g) stays the same.
+// Latency is hidden by occupancy (four workgroups per CU) rather than by
+// double-buffering, which costs more registers than it returns.  Partial dot
+// products are combined by three DPP adds.
 #include <hip/hip_ext.h>
 
 #include "hill_device.h"

@@ -16,19 +16,23 @@
 //               selected tokens -- every key above the threshold plus, among
 //               keys equal to it, the lowest token indices that fit the
 //               budget -- and stores them in token order with their count.
-//               With attention, every 16-lane row group then attends over the
-//               selected tokens among its own 32 (fused gather + online
-//               softmax) for one KV head, and one partial per query head is
-//               written.
+//               With attention, the workgroup then attends over the chunk's
+//               selected tokens for one or more KV heads (fused gather +
+//               softmax over the list, attn_device.h) and writes one partial
+//               per query head.
 //  topk_write   places each chunk's list at its ascending-order offset (the
 //               counts of the chunks before it) in the output; in hill_step
-//               this runs inside the merge of the attention partials.
+//               this runs inside merge_write, with the merge of the attention
+//               partials.
 //
-// Cross-chunk results always pass through a kernel boundary: on this
-// multi-XCD part an agent-scope fence per workgroup (needed by a
-// last-workgroup-done merge) costs far more than a launch.  The selection is
-// exactly the k largest S with ties to the lower index: keys are integers, so
-// no floating-point rounding takes part.
+// Every histogram is a 12-bit digit whose top 6 bits are also counted, so the
+// bin of the k-th key is found in registers: every wave scans the 64 coarse
+// bins (one per lane), and the wave that holds the 64 fine bins of the chosen
+// coarse bin finishes.  Cross-chunk results always pass through a kernel
+// boundary: on this multi-XCD part an agent-scope fence per workgroup (needed
+// by a last-workgroup-done merge) costs far more than a launch.  The
+// selection is exactly the k largest S with ties to the lower index: keys are
+// integers, so no floating-point rounding takes part.
 #include <hip/hip_ext.h>
 
 #include "attn_device.h"
