@@ -331,6 +331,47 @@ def test_step_is_deterministic_and_resumable():
     assert torch.equal(s1.cpu(), s4.cpu()) and torch.equal(i1.cpu(), i4.cpu()) and torch.equal(o1.cpu(), o4.cpu())
 
 
+@pytest.mark.parametrize("mode,gran", [("attn", "token"), ("raw", "kvhead")])
+def test_step_graph_replays_match_eager(mode, gran):
+    """hill_step captured in a HIP graph: every replay (with eager work and
+    synchronisation between replays) equals the eager call sequence bit for
+    bit -- the library enqueues kernels only, no memsets or allocations."""
+    B, Hq, Hkv, n, kk = 2, 32, 8, 5000, 500
+    say("graph replay", mode, gran)
+    x = W.make_random(B, Hq, Hkv, 128, n, "bf16", steps=1, seed=4242)
+    q, k, v = gpu_inputs(x)
+    R = R_of(gran, Hkv)
+    s_e = H().new_importance(B, R, n, DEV)
+    eager = []
+    for _ in range(4):
+        i, o = H().hill_step(q[0], k, v, s_e, kk, mode=mode, granularity=gran)
+        torch.cuda.synchronize()
+        eager.append((i.cpu().clone(), o.cpu().clone(), s_e.cpu().clone()))
+    cs = torch.cuda.Stream()
+    s_g = H().new_importance(B, R, n, DEV)
+    call = H().StepCall(q[0], k, v, s_g, kk, mode=mode, granularity=gran, stream=cs)
+    qp = q[0].data_ptr()
+    with torch.cuda.stream(cs):          # one-time host initialisation outside the capture
+        call(qp)
+    torch.cuda.synchronize()
+    s_g.zero_()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=cs):
+        call(qp)
+    torch.cuda.synchronize()
+    assert torch.count_nonzero(s_g).item() == 0   # capturing executed nothing
+    junk = torch.randn(256, 256, device=DEV)
+    for r in range(4):
+        g.replay()
+        torch.cuda.synchronize()
+        got = (call.idx.cpu(), call.out.cpu(), s_g.cpu())
+        for a, e, name in zip(got, eager[r], ("idx", "out", "S")):
+            assert torch.equal(a, e), "replay %d: %s differs from the eager call" % (r, name)
+        junk = torch.mm(junk, junk.t().contiguous()) / 256.0   # eager work between replays
+        torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("mode,gran", [("attn", "token"), ("raw", "kvhead"), ("raw", "token")])
 def test_step_equals_score_topk_attn_in_sequence(mode, gran):
     B, Hq, Hkv, n, kk = 2, 32, 8, 3000, 300
