@@ -27,6 +27,17 @@
  *   (5) attention    Eq. 1 restricted to the selected set I, softmax
  *                    renormalised over I (Sec. 4.1 workflow step 6)
  *
+ *   (6) asymmetric   scoring-only int8 casts of the keys and the query
+ *       precision    (Sec. 4.4 "Streaming Execution and Asymmetric
+ *                    Precision": Q.K^T in low precision for the evaluation
+ *                    only; attention keeps the 16-bit K, V).  Readings where
+ *                    the paper is silent: one power-of-two scale 2^e per key
+ *                    row (sequence, KV head, token) and per query head, the
+ *                    smallest e with max|x| * 2^-e <= 127; codes rounded to
+ *                    nearest, ties to even; e clamped to [-128, 127] (an
+ *                    all-zero row has e = -128); the score is the exact
+ *                    integer dot product times 2^(e_q + e_k).
+ *
  * kv(h) = floor(h / G) with G = Hq / Hkv (contiguous GQA groups).
  * Row granularity: token mode (gran 0) has one row per batch element summing
  * all Hq heads; KV-head mode (gran 1) has one row per (batch, KV head) summing
@@ -141,6 +152,65 @@ int hor_logits(int B, int Hq, int Hkv, int D, int n, int dtype,
         }
     }
     free(tab);
+    return 0;
+}
+
+/* (6) int8 sketch of `rows` rows of D 16-bit values: codes[r, i] and one
+ * exponent per row, by the rule in the header.  Every operation is exact
+ * (scaling by a power of two, round-to-nearest-even of a value <= 127). */
+int hor_sketch(int64_t rows, int D, int dtype, const uint16_t *x, int8_t *codes, int8_t *exps)
+{
+    if (rows < 0 || D < 1) return -1;
+    double *tab = (double *)malloc(65536 * sizeof(double));
+    if (!tab) return -2;
+    build_table(dtype, tab);
+    #pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) {
+        const uint16_t *xr = x + r * D;
+        double amax = 0.0;
+        for (int i = 0; i < D; ++i) {
+            const double a = fabs(tab[xr[i]]);
+            if (a > amax) amax = a;
+        }
+        int e = -128;
+        if (amax > 0.0) {
+            int E;
+            const double m = frexp(amax, &E);       /* amax = m * 2^E, m in [0.5, 1) */
+            e = m * 128.0 <= 127.0 ? E - 7 : E - 6; /* smallest e with amax * 2^-e <= 127 */
+            if (e < -128) e = -128;
+            if (e > 127) e = 127;
+        }
+        exps[r] = (int8_t)e;
+        for (int i = 0; i < D; ++i) {
+            double c = nearbyint(ldexp(tab[xr[i]], -e));   /* default rounding: to nearest, ties to even */
+            if (c > 127.0) c = 127.0;
+            if (c < -127.0) c = -127.0;
+            codes[r * D + i] = (int8_t)c;
+        }
+    }
+    free(tab);
+    return 0;
+}
+
+/* (6) sketch logits l[b,h,j] = (sum_i q8[b,h,i] * k8[b,kv(h),j,i]) * 2^(eq[b,h] + ek[b,kv(h),j]):
+ * the integer dot product is exact (int64), the scaling exact in double. */
+int hor_logits_i8(int B, int Hq, int Hkv, int D, int n, const int8_t *q8, const int8_t *eq,
+                  const int8_t *k8, const int8_t *ek, double *l)
+{
+    if (check_shape(B, Hq, Hkv, D, n)) return -1;
+    const int G = Hq / Hkv;
+    const int64_t rows = (int64_t)B * Hq;
+    #pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t bh = 0; bh < rows; ++bh) {
+        for (int j = 0; j < n; ++j) {
+            int64_t b = bh / Hq;
+            int h = (int)(bh % Hq);
+            int64_t krow = ((int64_t)b * Hkv + h / G) * n + j;
+            int64_t acc = 0;
+            for (int i = 0; i < D; ++i) acc += (int64_t)q8[bh * D + i] * (int64_t)k8[krow * D + i];
+            l[bh * n + j] = ldexp((double)acc, (int)eq[bh] + (int)ek[krow]);
+        }
+    }
     return 0;
 }
 

@@ -85,6 +85,10 @@ def _load():
         lib.hor_sparse_attn.restype = I
         lib.hor_step.argtypes = [I, I, I, I, I, I, I, I, Dd, P, P, P, P, P, I, P, P, P]
         lib.hor_step.restype = I
+        lib.hor_sketch.argtypes = [I64, I, I, P, P, P]
+        lib.hor_sketch.restype = I
+        lib.hor_logits_i8.argtypes = [I, I, I, I, I, P, P, P, P, P]
+        lib.hor_logits_i8.restype = I
         _lib = lib
         return lib
 
@@ -135,6 +139,38 @@ def logits(q, k, dtype) -> np.ndarray:
     rc = lib.hor_logits(B, Hq, Hkv, D, n, _code(_DTYPES, dtype), _ptr(q), _ptr(k), _ptr(out))
     if rc:
         raise ValueError("hor_logits failed (%d)" % rc)
+    return out
+
+
+def sketch(x, dtype):
+    """int8 scoring sketch of the last axis of x (16-bit patterns, D = last
+    dimension): (codes int8 of x's shape, exponents int8 of x.shape[:-1]).
+    Sec. 4.4 asymmetric precision, with the power-of-two per-row scale reading."""
+    lib = _load()
+    x = _u16(x)
+    D = x.shape[-1]
+    rows = x.size // D
+    codes = np.empty(x.shape, dtype=np.int8)
+    exps = np.empty(x.shape[:-1], dtype=np.int8)
+    rc = lib.hor_sketch(rows, D, _code(_DTYPES, dtype), _ptr(x), _ptr(codes), _ptr(exps))
+    if rc:
+        raise ValueError("hor_sketch failed (%d)" % rc)
+    return codes, exps
+
+
+def logits_i8(q8, eq, k8, ek) -> np.ndarray:
+    """Sketch logits: exact integer q8.k8 scaled by 2^(eq + ek), float64.
+    q8 [B,Hq,D], eq [B,Hq], k8 [B,Hkv,n,D], ek [B,Hkv,n]."""
+    lib = _load()
+    q8, k8 = np.ascontiguousarray(q8, dtype=np.int8), np.ascontiguousarray(k8, dtype=np.int8)
+    eq, ek = np.ascontiguousarray(eq, dtype=np.int8), np.ascontiguousarray(ek, dtype=np.int8)
+    B, Hq, D = q8.shape
+    Bk, Hkv, n, Dk = k8.shape
+    assert Bk == B and Dk == D and eq.shape == (B, Hq) and ek.shape == (B, Hkv, n)
+    out = np.empty((B, Hq, n), dtype=np.float64)
+    rc = lib.hor_logits_i8(B, Hq, Hkv, D, n, _ptr(q8), _ptr(eq), _ptr(k8), _ptr(ek), _ptr(out))
+    if rc:
+        raise ValueError("hor_logits_i8 failed (%d)" % rc)
     return out
 
 

@@ -315,3 +315,103 @@ def test_budget_rounding():
     assert O.budget_k(3, 0.05) == 1
     for n, a in itertools.product([8192, 32768, 65536], [0.05, 0.10, 0.20]):
         assert O.budget_k(n, a) == W.budget_tokens(n, a)
+
+
+# ------------------------------------------ asymmetric-precision scoring --
+# Sec. 4.4 (asymmetric precision): int8 casts of keys and query for scoring
+# only.  The pins check the sketch against the bounds the power-of-two
+# rounding rule implies and against the fp64 logits where the cast is exact.
+
+def _decoded(t):
+    return t.detach().double().numpy()
+
+
+@pytest.mark.parametrize("dt", ["bf16", "fp16"])
+def test_sketch_rounding_bound_range_and_minimal_exponent(dt):
+    g = torch.Generator().manual_seed(11)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float16
+    x = torch.randn(64, 128, generator=g)
+    x = x * torch.exp(torch.randn(1, 128, generator=g))          # per-channel outliers
+    x = x * torch.logspace(-3, 3, 64).unsqueeze(1)               # rows of very different size
+    x = x.to(tdt)
+    codes, exps = O.sketch(bits(x), dt)
+    xd = _decoded(x)
+    amax = np.abs(xd).max(axis=1)
+    e = exps.astype(np.float64)
+    step = np.exp2(e)[:, None]
+    assert np.all(np.abs(xd - codes * step) <= step / 2)         # round to nearest
+    assert np.all(np.abs(codes) <= 127)
+    assert np.all(amax * np.exp2(-e) <= 127)                     # e large enough ...
+    assert np.all(amax * np.exp2(-(e - 1)) > 127)                # ... and the smallest such
+    assert np.all(np.abs(codes).max(axis=1) >= 64)               # half the code range at least
+
+
+def test_sketch_ties_to_even_zero_and_tiny_rows():
+    s = 8.0   # 2^3
+    row = [127 * s, 2.5 * s, 3.5 * s, -2.5 * s, 0.5 * s, -0.5 * s, 1.5 * s, -1.5 * s] + [0.0] * 120
+    zero = [0.0] * 128
+    tiny = [2.0 ** -130] + [0.0] * 127                           # bf16 subnormal: exponent clamped
+    x = torch.tensor([row, zero, tiny], dtype=torch.float32).to(torch.bfloat16)
+    codes, exps = O.sketch(bits(x), "bf16")
+    assert exps.tolist() == [3, -128, -128]
+    assert codes[0, :8].tolist() == [127, 2, 4, -2, 0, 0, 2, -2]
+    assert not codes[1].any() and not codes[2].any()
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n", [(1, 4, 4, 9), (2, 8, 2, 17), (1, 32, 8, 5)])
+def test_sketch_logits_exact_when_the_cast_is_lossless(B, Hq, Hkv, n):
+    """Integers in [-127, 127] times 2^s with a row maximum of 127 * 2^s are
+    cast without loss, so the sketch logits equal the fp64 logits exactly
+    (including the GQA head mapping)."""
+    g = np.random.default_rng(B * 31 + n)
+
+    def rows(shape):
+        v = g.integers(-127, 128, size=shape + (128,)).astype(np.float64)
+        v[..., 0] = 127.0
+        return v * np.exp2(g.integers(-6, 7, size=shape + (1,)))
+
+    q = torch.from_numpy(rows((B, Hq))).to(torch.bfloat16)
+    k = torch.from_numpy(rows((B, Hkv, n))).to(torch.bfloat16)
+    q8, eq = O.sketch(bits(q), "bf16")
+    k8, ek = O.sketch(bits(k), "bf16")
+    l8 = O.logits_i8(q8, eq, k8, ek)
+    l = O.logits(bits(q), bits(k), "bf16")
+    assert np.array_equal(l8, l)
+
+
+def test_sketch_logits_error_bound():
+    """|l8 - l| <= sum_i |q_i| dk + |k_i| dq + dq dk with d = half a code step."""
+    x = W.make_random(1, 8, 2, 128, 300, "bf16", seed=5)
+    q8, eq = O.sketch(bits(x.q[0]), "bf16")
+    k8, ek = O.sketch(bits(x.k), "bf16")
+    l8 = O.logits_i8(q8, eq, k8, ek)
+    l = O.logits(bits(x.q[0]), bits(x.k), "bf16")
+    qd, kd = _decoded(x.q[0]), _decoded(x.k)                     # [1,8,128], [1,2,300,128]
+    dq = np.exp2(eq.astype(np.float64) - 1)                      # [1,8]
+    dk = np.exp2(ek.astype(np.float64) - 1)                      # [1,2,300]
+    for h in range(8):
+        g = h // 4
+        bound = (np.abs(qd[0, h]).sum() * dk[0, g] + np.abs(kd[0, g]).sum(axis=1) * dq[0, h]
+                 + 128 * dq[0, h] * dk[0, g])
+        assert np.all(np.abs(l8[0, h] - l[0, h]) <= bound * (1 + 1e-12))
+
+
+@pytest.mark.parametrize("wid,floor", [(3, 0.93), (1, 0.98)])
+def test_sketch_selection_recall_vs_full_precision(wid, floor):
+    """Quality statistic, not exactness: the top-alpha sets selected on sketch
+    scores overlap the full-precision sets (4 steps, S carried).  Per-token
+    scales lose most on the per-channel outlier keys of workload 3."""
+    w = W.WORKLOADS[wid].replace(n_tokens=4096, steps=4, layers=1)
+    x = W.make_layer(w, 0)
+    k8, ek = O.sketch(bits(x.k), w.dtype)
+    S = np.zeros((w.batch, 1, w.n_tokens))
+    S8 = np.zeros_like(S)
+    k = O.budget_k(w.n_tokens, w.budget)
+    for t in range(w.steps):
+        q8, eq = O.sketch(bits(x.q[t]), w.dtype)
+        S = O.update(O.logits(bits(x.q[t]), bits(x.k), w.dtype), S, w.n_kv_heads, "attn", "token",
+                     O.default_scale(128))
+        S8 = O.update(O.logits_i8(q8, eq, k8, ek), S8, w.n_kv_heads, "attn", "token", O.default_scale(128))
+        for b in range(w.batch):
+            ov = len(np.intersect1d(O.topk(S[b:b + 1], k), O.topk(S8[b:b + 1], k))) / k
+            assert ov >= floor, (t, b, ov)
