@@ -221,10 +221,28 @@ T* at(void* ws, size_t off)
     return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
 }
 
+// Optional int8 key sketch scored in place of the 16-bit keys.
+struct Sketch {
+    const int8_t* k8 = nullptr;
+    const int8_t* k_exp = nullptr;
+    int64_t cap = 0;
+};
+
+hill_status check_sketch(const Shape& s, const int8_t* k8, const int8_t* k_exp, int64_t cap)
+{
+    if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
+    if ((uintptr_t)k8 & 15u) return fail(HILL_ERR_INVALID_ARG, "sketch codes are not 16-byte aligned");
+    if ((uintptr_t)k_exp & 3u) return fail(HILL_ERR_INVALID_ARG, "sketch exponents are not 4-byte aligned");
+    if (cap < s.n || cap % 4) return fail(HILL_ERR_INVALID_ARG, "sketch capacity %lld must be >= n_tokens and a multiple of 4",
+                                          (long long)cap);
+    return HILL_OK;
+}
+
 // Scoring; if `hist` is given the first selection digit is counted as a side
 // effect (hill_step) and the counts are cleared by the first kernel.
-hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k, float* sacc,
-                      void* ws, bool with_hist, hipStream_t st, const hill_step_events& ev)
+hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k,
+                      const Sketch& sk, float* sacc, void* ws, bool with_hist, hipStream_t st,
+                      const hill_step_events& ev)
 {
     const Stamp scan{static_cast<hipEvent_t>(ev.scan_start), static_cast<hipEvent_t>(ev.scan_stop)};
     const Stamp last{nullptr, static_cast<hipEvent_t>(ev.score_stop)};
@@ -251,6 +269,9 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.s_sr = d->s_stride_r;
     a.zero_ptr = with_hist ? at<uint32_t>(ws, L.zero) : nullptr;
     a.zero_words = with_hist ? L.zero_words : 0;
+    a.k8 = sk.k8;
+    a.k_exp = sk.k_exp;
+    a.cap = sk.cap;
     const int ncu = device_cus();
 
     UpdateArgs u{};
@@ -369,6 +390,38 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
     return HILL_OK;
 }
 
+// One decode step: score (16-bit keys or the sketch), refine the threshold,
+// then emit the indices and attend over each chunk's picks in the same kernel.
+hill_status run_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk, float* s_acc,
+                     int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
+                     const hill_step_events* ev)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s));
+    HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_ptr(v, "v"));
+    if (sk.k8) HILL_TRY(check_sketch(s, sk.k8, sk.k_exp, sk.cap));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    HILL_TRY(check_ptr(out, "out"));
+    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
+    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
+    const Layout L = layout_for(s, k_sel);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const hill_step_events none{};
+    const hill_step_events& e = ev ? *ev : none;
+    HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e));
+    const RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
+    HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
+                               Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
+    const AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
+    HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
+    HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, Stamp{nullptr, static_cast<hipEvent_t>(e.attn_stop)}));
+    return HILL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -409,7 +462,46 @@ hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* 
     HILL_TRY(check_ptr(s_acc, "s"));
     const Layout L = layout_for(s, 1);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_score));
-    return run_score(d, s, L, q, k, s_acc, ws, false, static_cast<hipStream_t>(stream), hill_step_events{});
+    return run_score(d, s, L, q, k, Sketch{}, s_acc, ws, false, static_cast<hipStream_t>(stream), hill_step_events{});
+}
+
+hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap,
+                             int32_t token_begin, int32_t token_end, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s, false));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_sketch(s, k8, k_exp, cap));
+    if (token_begin < 0 || token_begin > token_end || token_end > s.n)
+        return fail(HILL_ERR_INVALID_ARG, "token range [%d, %d) not inside [0, n_tokens=%d)", token_begin, token_end, s.n);
+    SketchArgs a{};
+    a.k = static_cast<const uint16_t*>(k);
+    a.k_sb = d->k_stride_b;
+    a.k_sh = d->k_stride_h;
+    a.k_sn = d->k_stride_n;
+    a.B = s.B;
+    a.Hkv = s.Hkv;
+    a.t0 = token_begin;
+    a.t1 = token_end;
+    a.cap = cap;
+    a.k8 = k8;
+    a.k_exp = k_exp;
+    HIP_TRY(launch_sketch_keys(a, s.dtype, static_cast<hipStream_t>(stream)));
+    return HILL_OK;
+}
+
+hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp, int64_t cap,
+                              float* s_acc, void* ws, size_t ws_bytes, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_sketch(s, k8, k_exp, cap));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    const Layout L = layout_for(s, 1);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end_score));
+    return run_score(d, s, L, q, nullptr, Sketch{k8, k_exp, cap}, s_acc, ws, false, static_cast<hipStream_t>(stream),
+                     hill_step_events{});
 }
 
 hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int32_t* idx_out, float* val_out,
@@ -454,31 +546,15 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
                                int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                                const hill_step_events* ev)
 {
-    Shape s;
-    HILL_TRY(check_desc(d, &s));
-    HILL_TRY(check_ksel(s, k_sel));
-    HILL_TRY(check_ptr(q, "q"));
-    HILL_TRY(check_ptr(k, "k"));
-    HILL_TRY(check_ptr(v, "v"));
-    HILL_TRY(check_ptr(s_acc, "s"));
-    HILL_TRY(check_ptr(out, "out"));
-    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
-    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
-    const Layout L = layout_for(s, k_sel);
-    HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
-    hipStream_t st = static_cast<hipStream_t>(stream);
-    const hill_step_events none{};
-    const hill_step_events& e = ev ? *ev : none;
-    HILL_TRY(run_score(d, s, L, q, k, s_acc, ws, true, st, e));
-    // selection and attention: refine the threshold, then emit the indices and
-    // attend over each chunk's picks in the same kernel
-    const RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
-    HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
-                               Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
-    const AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
-    HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
-    HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, Stamp{nullptr, static_cast<hipEvent_t>(e.attn_stop)}));
-    return HILL_OK;
+    return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
+}
+
+hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v, const int8_t* k8,
+                             const int8_t* k_exp, int64_t cap, float* s_acc, int32_t k_sel, int32_t* idx_out,
+                             float* out, void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev)
+{
+    if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
+    return run_step(d, q, k, v, Sketch{k8, k_exp, cap}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
 }
 
 }  // extern "C"

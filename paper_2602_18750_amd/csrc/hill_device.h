@@ -84,6 +84,51 @@ __device__ __forceinline__ float sum8(float v)
     return v;
 }
 
+// Integer sum over each aligned group of 8 lanes (exact); every lane of the
+// group gets the sum.
+__device__ __forceinline__ int isum8(int v)
+{
+    v += __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+    v += __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false);
+    return v;
+}
+
+// Max over each aligned group of 8 / 16 lanes; every lane of the group gets it.
+__device__ __forceinline__ float max8(float v)
+{
+    v = fmaxf(v, dpp<0xB1>(v));
+    v = fmaxf(v, dpp<0x4E>(v));
+    v = fmaxf(v, dpp<0x141>(v));
+    return v;
+}
+
+__device__ __forceinline__ float max16(float v)
+{
+    v = max8(v);
+    return fmaxf(v, dpp<0x140>(v));
+}
+
+// Exponent of the int8 scoring sketch of a row whose largest magnitude is
+// amax: the smallest e with amax * 2^-e <= 127, clamped to [-128, 127]
+// (-128 for an all-zero row).  frexp is exact.
+__device__ __forceinline__ int sketch_exponent(float amax)
+{
+    if (!(amax > 0.0f)) return -128;
+    int E;
+    const float m = frexpf(amax, &E);   // amax = m * 2^E, m in [0.5, 1)
+    const int e = m <= 0.9921875f ? E - 7 : E - 6;
+    return e < -128 ? -128 : (e > 127 ? 127 : e);
+}
+
+// int8 code of x under exponent e: x * 2^-e (exact) rounded to nearest, ties
+// to even, clamped to [-127, 127].
+__device__ __forceinline__ int sketch_code(float x, int e)
+{
+    const float r = rintf(ldexpf(x, -e));
+    return (int)fminf(fmaxf(r, -127.0f), 127.0f);
+}
+
 // Sum over each aligned group of 16 lanes; every lane of the group gets the sum.
 // quad_perm[1,0,3,2], quad_perm[2,3,0,1], row_half_mirror, row_mirror.
 __device__ __forceinline__ float sum16(float v)

@@ -41,6 +41,19 @@ struct ScoreArgs {
     int64_t s_sb, s_sr;
     uint32_t* zero_ptr;      // nullable: words to clear for a later kernel
     int64_t zero_words;
+    const int8_t* k8;        // nullable: int8 key sketch [B,Hkv,cap,128] scored instead of k
+    const int8_t* k_exp;     //   its per-row exponents [B,Hkv,cap]
+    int64_t cap;             //   tokens per (b, g) in the sketch, a multiple of 4
+};
+
+// int8 key sketch: codes and one power-of-two exponent per key row
+struct SketchArgs {
+    const uint16_t* k;
+    int64_t k_sb, k_sh, k_sn;
+    int B, Hkv, t0, t1;
+    int64_t cap;
+    int8_t* k8;
+    int8_t* k_exp;
 };
 
 struct UpdateArgs {
@@ -123,6 +136,7 @@ struct Stamp {
 };
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
+hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st);
 // Whether update_attn can reduce the softmax partials itself (no separate

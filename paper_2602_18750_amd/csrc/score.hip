@@ -57,54 +57,147 @@ __device__ __forceinline__ TileCoord coord(const ScoreArgs& a, int t)
     return c;
 }
 
-__device__ __forceinline__ void load_tile(const ScoreArgs& a, int t, int rg, int l8, uint4 (&kr)[kLoadsPerTile])
-{
-    const TileCoord c = coord(a, t);
-    const uint16_t* kb = a.k + (int64_t)c.b * a.k_sb + (int64_t)c.g * a.k_sh + l8 * 8;
+// Key sources of the scan.  Each provides: load(a, c, rg, l8) -- issue the
+// tile's key loads of this lane; query(a, c, hc, l8) -- make the queries of
+// heads hc .. hc+GC of group (c.b, c.g) ready (kept while the group stays the
+// same); dot(a, u, hh, l8) -- the raw logit q_hh . K_row of this lane's row u,
+// complete in every lane of the 8-lane row group.
+
+// 16-bit keys: lane l8 holds elements [8*l8, 8*l8+8) and [64+8*l8, 64+8*l8+8)
+// of each of its 4 rows (two 16-byte non-temporal loads per row).
+template <int DT, int GC>
+struct KeysF16 {
+    uint4 kr[2 * kRowsPerLane];
+    uint4 qa[GC], qb[GC];
+    int q_tag = -1;
+
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const uint16_t* kb = a.k + (int64_t)c.b * a.k_sb + (int64_t)c.g * a.k_sh + l8 * 8;
 #pragma unroll
-    for (int u = 0; u < kRowsPerLane; ++u) {
-        const int j = c.j0 + rg * kRowsPerLane + u;
-        if (j < a.n) {
-            const uint16_t* row = kb + (int64_t)j * a.k_sn;
-            kr[2 * u] = load_stream16(row);
-            kr[2 * u + 1] = load_stream16(row + 64);
-        } else {
-            kr[2 * u] = make_uint4(0u, 0u, 0u, 0u);
-            kr[2 * u + 1] = make_uint4(0u, 0u, 0u, 0u);
+        for (int u = 0; u < kRowsPerLane; ++u) {
+            const int j = c.j0 + rg * kRowsPerLane + u;
+            if (j < a.n) {
+                const uint16_t* row = kb + (int64_t)j * a.k_sn;
+                kr[2 * u] = load_stream16(row);
+                kr[2 * u + 1] = load_stream16(row + 64);
+            } else {
+                kr[2 * u] = make_uint4(0u, 0u, 0u, 0u);
+                kr[2 * u + 1] = make_uint4(0u, 0u, 0u, 0u);
+            }
         }
     }
-}
 
-template <int DT, int GC, int OUT>
-__device__ __forceinline__ void compute_tile(const ScoreArgs& a, int t, int rg, int l8, const uint4 (&kr)[kLoadsPerTile],
-                                             uint4 (&qa)[GC], uint4 (&qb)[GC], int& q_tag, float2* tile_part)
+    __device__ __forceinline__ void query(const ScoreArgs& a, const TileCoord& c, int hc, int l8)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+#pragma unroll
+        for (int hh = 0; hh < GC; ++hh) {
+            const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + hc + hh) * a.q_sh + l8 * 8;
+            qa[hh] = *reinterpret_cast<const uint4*>(qr);
+            qb[hh] = *reinterpret_cast<const uint4*>(qr + 64);
+        }
+        q_tag = tag;
+    }
+
+    __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
+    {
+        float d = dot8<DT>(kr[2 * u], qa[hh]);
+        d += dot8<DT>(kr[2 * u + 1], qb[hh]);
+        return sum8(d);
+    }
+};
+
+// int8 sketch (Sec. 4.4 asymmetric precision): lane l8 holds codes
+// [16*l8, 16*l8+16) of each of its 4 rows (one 16-byte load per row) and the
+// rows' exponents; the queries are cast to int8 the same way (power-of-two
+// scale per head, round to nearest even) when the group changes.  The dot
+// product is exact in int32 (|sum| < 2^24) and scaled by 2^(e_q + e_k).
+template <int DT, int GC>
+struct KeysI8 {
+    uint4 kr[kRowsPerLane];
+    uint32_t ek4;   // exponents of the 4 rows, one byte each
+    uint4 q8[GC];
+    int eq[GC];
+    int q_tag = -1;
+
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
+        const int jr = c.j0 + rg * kRowsPerLane;
+        const int8_t* kb = a.k8 + bg * a.cap * kHeadDim + l8 * 16;
+#pragma unroll
+        for (int u = 0; u < kRowsPerLane; ++u) {
+            const int j = jr + u;
+            kr[u] = j < a.n ? load_stream16(kb + (int64_t)j * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+        }
+        // jr is a multiple of 4 and cap too: the 4 exponents are one aligned word inside the row
+        ek4 = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
+    }
+
+    __device__ __forceinline__ void query(const ScoreArgs& a, const TileCoord& c, int hc, int l8)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+#pragma unroll
+        for (int hh = 0; hh < GC; ++hh) {
+            const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + hc + hh) * a.q_sh + l8 * 16;
+            const uint4 w0 = *reinterpret_cast<const uint4*>(qr);
+            const uint4 w1 = *reinterpret_cast<const uint4*>(qr + 8);
+            const uint32_t pw[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+            float x[16];
+            float amax = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                widen2<DT>(pw[i], x[2 * i], x[2 * i + 1]);
+                amax = fmaxf(amax, fmaxf(fabsf(x[2 * i]), fabsf(x[2 * i + 1])));
+            }
+            const int e = sketch_exponent(max8(amax));   // the head's 128 elements sit in 8 lanes
+            uint32_t packed[4];
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                uint32_t v = 0u;
+#pragma unroll
+                for (int b = 0; b < 4; ++b) v |= ((uint32_t)sketch_code(x[4 * w + b], e) & 0xffu) << (8 * b);
+                packed[w] = v;
+            }
+            q8[hh] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
+            eq[hh] = e;
+        }
+        q_tag = tag;
+    }
+
+    __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
+    {
+        int d = __builtin_amdgcn_sdot4((int)kr[u].x, (int)q8[hh].x, 0, false);
+        d = __builtin_amdgcn_sdot4((int)kr[u].y, (int)q8[hh].y, d, false);
+        d = __builtin_amdgcn_sdot4((int)kr[u].z, (int)q8[hh].z, d, false);
+        d = __builtin_amdgcn_sdot4((int)kr[u].w, (int)q8[hh].w, d, false);
+        d = isum8(d);
+        const int ek = (int)(int8_t)(ek4 >> (8 * u));
+        return ldexpf((float)d, eq[hh] + ek);
+    }
+};
+
+template <int GC, int OUT, typename Keys>
+__device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord& c, int rg, int l8, Keys& ks,
+                                             float2* tile_part)
 {
-    const TileCoord c = coord(a, t);
     const int jr = c.j0 + rg * kRowsPerLane;   // first token of this row group
     float rawsum[kRowsPerLane];
 #pragma unroll
     for (int u = 0; u < kRowsPerLane; ++u) rawsum[u] = 0.0f;
 
     for (int hc = 0; hc < a.G; hc += GC) {
-        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
-        if (tag != q_tag) {
-#pragma unroll
-            for (int hh = 0; hh < GC; ++hh) {
-                const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + hc + hh) * a.q_sh + l8 * 8;
-                qa[hh] = *reinterpret_cast<const uint4*>(qr);
-                qb[hh] = *reinterpret_cast<const uint4*>(qr + 64);
-            }
-            q_tag = tag;
-        }
+        ks.query(a, c, hc, l8);
         float mine[kRowsPerLane];   // lane l8 == hh keeps head hh's logits
 #pragma unroll
         for (int u = 0; u < kRowsPerLane; ++u) {
             mine[u] = 0.0f;
 #pragma unroll
             for (int hh = 0; hh < GC; ++hh) {
-                float d = dot8<DT>(kr[2 * u], qa[hh]);
-                d += dot8<DT>(kr[2 * u + 1], qb[hh]);
-                d = sum8(d);
+                const float d = ks.dot(a, u, hh, l8);
                 if constexpr (OUT == kOutLogits)
                     mine[u] = (l8 == hh) ? d : mine[u];
                 else
@@ -183,8 +276,8 @@ __device__ __forceinline__ void merge_unit(const ScoreArgs& a, int bg, int unit,
 
 // Work unit: kUnitTiles consecutive wave-tiles of one (b, g); wave w takes
 // tiles w, w+4, ... of the unit.  Each workgroup walks a contiguous range of
-// units.
-template <int DT, int GC, int OUT>
+// units.  Keys = KeysF16 (16-bit cache) or KeysI8 (int8 sketch).
+template <int GC, int OUT, typename Keys>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
     __shared__ float2 tile_part[kUnitTiles][kMaxGroup];   // ATTN: per tile of the unit, per head of the group
@@ -203,18 +296,16 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
     int u = blockIdx.x * per;
     const int u_end = min(u + per, total);
 
-    uint4 qa[GC], qb[GC];
-    int q_tag = -1;
-    uint4 kr[kLoadsPerTile];
+    Keys ks;
     for (; u < u_end; ++u) {
         const int bg = u / a.npart, unit = u % a.npart;
 #pragma unroll
         for (int i = wv; i < kUnitTiles; i += 4) {
             const int tile = unit * kUnitTiles + i;
             if (tile < a.ntiles) {
-                const int t = bg * a.ntiles + tile;
-                load_tile(a, t, rg, l8, kr);
-                compute_tile<DT, GC, OUT>(a, t, rg, l8, kr, qa, qb, q_tag, tile_part[i]);
+                const TileCoord c = coord(a, bg * a.ntiles + tile);
+                ks.load(a, c, rg, l8);
+                compute_tile<GC, OUT>(a, c, rg, l8, ks, tile_part[i]);
             } else if constexpr (OUT == kOutLogits) {
                 for (int h = lane; h < a.G; h += 64) tile_part[i][h] = make_float2(-INFINITY, 0.0f);
             }
@@ -516,13 +607,18 @@ int resident_per_cu(K kernel)
 template <int DT, int GC, int OUT>
 hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp ts)
 {
-    auto kernel = score_tiles_kernel<DT, GC, OUT>;
     const int64_t total = (int64_t)a.B * a.Hkv * a.npart;
-    int64_t grid = total;
-    const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
-    if (grid > cap) grid = cap;
-    if (grid < 1) grid = 1;
-    hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+    if (a.k8) {
+        auto kernel = score_tiles_kernel<GC, OUT, KeysI8<DT, GC>>;
+        const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+        const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+    } else {
+        auto kernel = score_tiles_kernel<GC, OUT, KeysF16<DT, GC>>;
+        const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+        const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+    }
     return hipGetLastError();
 }
 

@@ -8,6 +8,8 @@ The functions mirror the C-ABI entry points of ``include/hill.h``:
     hill_topk(s, k_sel, ...)         -> idx[, val]
     hill_gather_attn(q, k, v, idx, ...) -> out
     hill_step(q, k, v, s, k_sel, ...)  -> (idx, out)
+    sketch_keys(k, ...)              -> Sketch (int8 codes + exponents, Sec. 4.4)
+    hill_score / hill_step(..., sketch=...)   score on the int8 sketch
 
 Shapes: q [B, Hq, D]; k, v [B, Hkv, Ncap, D] (any strides with D contiguous);
 s [B, R, >= n] fp32 with R = 1 (granularity "token") or Hkv ("kvhead");
@@ -34,7 +36,8 @@ MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
-           "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled")
+           "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
+           "hill_score_sketch", "hill_step_sketch")
 
 
 class HillError(RuntimeError):
@@ -109,6 +112,14 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step.restype = ctypes.c_int
         lib.hill_step_profiled.argtypes = [D, P, P, P, P, I32, P, P, P, SZ, P, ctypes.POINTER(HillStepEvents)]
         lib.hill_step_profiled.restype = ctypes.c_int
+        I64 = ctypes.c_int64
+        lib.hill_sketch_keys.argtypes = [D, P, P, P, I64, I32, I32, P]
+        lib.hill_sketch_keys.restype = ctypes.c_int
+        lib.hill_score_sketch.argtypes = [D, P, P, P, I64, P, P, SZ, P]
+        lib.hill_score_sketch.restype = ctypes.c_int
+        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, P, I32, P, P, P, SZ, P,
+                                         ctypes.POINTER(HillStepEvents)]
+        lib.hill_step_sketch.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -213,16 +224,58 @@ def _device_check(*ts):
             raise ValueError("libhill works on GPU tensors only (got %s)" % t.device)
 
 
+class Sketch:
+    """int8 scoring sketch of a key cache (Sec. 4.4 asymmetric precision):
+    codes [B, Hkv, cap, 128] int8 and one exponent per row [B, Hkv, cap] int8."""
+
+    def __init__(self, codes: torch.Tensor, exps: torch.Tensor):
+        self.codes, self.exps = codes, exps
+        self.cap = codes.shape[2]
+
+
+def new_sketch(B: int, Hkv: int, cap: int, device) -> Sketch:
+    cap = (cap + 3) // 4 * 4
+    return Sketch(torch.zeros((B, Hkv, cap, 128), dtype=torch.int8, device=device),
+                  torch.full((B, Hkv, cap), -128, dtype=torch.int8, device=device))
+
+
+def sketch_keys(k, sketch: Optional[Sketch] = None, *, token_begin=0, token_end=None, n_tokens=None,
+                stream=None) -> Sketch:
+    """Write the sketch of key rows [token_begin, token_end) (default: all)."""
+    lib = load_library()
+    _device_check(k)
+    B, Hkv, ncap, D = k.shape
+    if sketch is None:
+        sketch = new_sketch(B, Hkv, ncap, k.device)
+    n = ncap if n_tokens is None else int(n_tokens)
+    t1 = n if token_end is None else int(token_end)
+    desc = make_desc(None, k, None, None, n_tokens=n, shape=(B, Hkv, Hkv, D), dtype=k.dtype)
+    _check(lib.hill_sketch_keys(ctypes.byref(desc), _ptr(k), _ptr(sketch.codes), _ptr(sketch.exps), sketch.cap,
+                                int(token_begin), t1, _stream_ptr(stream)))
+    return sketch
+
+
 def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0, ws=None,
-               stream=None):
-    """S += column-wise sum over this step's weights (in place)."""
+               stream=None, sketch: Optional[Sketch] = None):
+    """S += column-wise sum over this step's weights (in place).  With
+    ``sketch`` the scores come from the int8 sketch (k may then be None)."""
     lib = load_library()
     _device_check(q, k, s)
-    desc = make_desc(q, k, None, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
+    if sketch is not None and k is None:
+        B, Hkv, cap, D = sketch.codes.shape
+        desc = make_desc(q, None, None, s, mode=mode, granularity=granularity,
+                         n_tokens=s.shape[-1] if n_tokens is None else n_tokens, sm_scale=sm_scale,
+                         shape=(B, q.shape[1], Hkv, D))
+    else:
+        desc = make_desc(q, k, None, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
     if ws is None:
         ws = workspace(desc, 1, q.device)
-    _check(lib.hill_score(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(s), _ptr(ws), ws.numel(),
-                          _stream_ptr(stream)))
+    if sketch is None:
+        _check(lib.hill_score(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(s), _ptr(ws), ws.numel(),
+                              _stream_ptr(stream)))
+    else:
+        _check(lib.hill_score_sketch(ctypes.byref(desc), _ptr(q), _ptr(sketch.codes), _ptr(sketch.exps),
+                                     sketch.cap, _ptr(s), _ptr(ws), ws.numel(), _stream_ptr(stream)))
     return s
 
 
@@ -265,10 +318,12 @@ def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_sca
 
 
 def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
-              sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None):
+              sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None,
+              sketch: Optional[Sketch] = None):
     """One decode step: S update, top-k on the new S, attention.  Returns (idx, out).
 
-    ``events``: optional HillStepEvents; then hill_step_profiled records them."""
+    ``events``: optional HillStepEvents; then hill_step_profiled records them.
+    ``sketch``: score on the int8 sketch (hill_step_sketch)."""
     lib = load_library()
     _device_check(q, k, v, s)
     desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
@@ -283,7 +338,12 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     if ws is None:
         ws = workspace(desc, k_sel, q.device)
-    if events is None:
+    if sketch is not None:
+        _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
+                                    _ptr(sketch.exps), sketch.cap, _ptr(s), int(k_sel), _ptr(idx_out), _ptr(out),
+                                    _ptr(ws), ws.numel(), _stream_ptr(stream),
+                                    None if events is None else ctypes.byref(events)))
+    elif events is None:
         _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
                              _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
     else:
@@ -304,7 +364,7 @@ class StepCall:
     repeatedly on the same buffers (only the query pointer changes per call)."""
 
     def __init__(self, q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
-                 ws=None, stream=None):
+                 ws=None, stream=None, sketch: Optional[Sketch] = None):
         lib = load_library()
         _device_check(q, k, v, s)
         self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
@@ -315,16 +375,27 @@ class StepCall:
         self.out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
         self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
         P = ctypes.c_void_p
-        self._fn = lib.hill_step
-        self._fn_ev = lib.hill_step_profiled
         self._pre = (ctypes.byref(self.desc),)
-        self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
-                      P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
-                      ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
-        self._keep = (k, v, s)
+        if sketch is None:
+            self._fn = lib.hill_step
+            self._fn_ev = lib.hill_step_profiled
+            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
+                          P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
+                          ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        else:
+            self._fn = None
+            self._fn_ev = lib.hill_step_sketch   # events may be NULL
+            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
+                          ctypes.c_int64(sketch.cap), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
+                          P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
+                          ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        self._keep = (k, v, s, sketch)
 
     def __call__(self, q_ptr: int, events=None):
-        if events is None:
+        if self._fn is None:
+            st = self._fn_ev(*self._pre, ctypes.c_void_p(q_ptr), *self._post,
+                             None if events is None else ctypes.byref(events))
+        elif events is None:
             st = self._fn(*self._pre, ctypes.c_void_p(q_ptr), *self._post)
         else:
             st = self._fn_ev(*self._pre, ctypes.c_void_p(q_ptr), *self._post, ctypes.byref(events))

@@ -177,3 +177,41 @@ def test_workspace_sizes_are_pure_functions_of_shape(H):
     # RAW with one row per KV head needs no logits buffer
     d_raw = base_desc(H, B=1, Hq=32, Hkv=8, n=32768, mode=1, gran=1)
     assert ws_need(H, d_raw, 3276) < a
+
+
+# ------------------------------------------------------------- key sketch --
+
+def test_sketch_entry_points_validate(H):
+    lib = H.load_library()
+    d = base_desc(H)                     # n = 1000
+    need = ws_need(H, d, 10)
+    ok_cap = 1000
+    # sketch_keys: pointers, capacity, token range
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, None, FAKE, ok_cap, 0, 10, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, None, ok_cap, 0, 10, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE + 8, FAKE, ok_cap, 0, 10, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE + 2, ok_cap, 0, 10, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 996, 0, 10, None) == INVALID    # cap < n
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 1002, 0, 10, None) == INVALID   # cap % 4
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, 5, 4, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, -1, 4, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, 0, 1001, None) == INVALID
+    assert lib.hill_sketch_keys(ctypes.byref(d), None, FAKE, FAKE, ok_cap, 0, 10, None) == INVALID
+    # score / step on the sketch
+    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, None, FAKE, ok_cap, FAKE, FAKE, need, None) == INVALID
+    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, 996, FAKE, FAKE, need, None) == INVALID
+    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, FAKE, FAKE, 16, None) == WORKSPACE
+    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, FAKE, 10, FAKE, FAKE,
+                                FAKE, need, None, None) == INVALID
+    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, FAKE, 10, FAKE, FAKE,
+                                FAKE, need, None, None) == INVALID
+    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, FAKE, 0, FAKE, FAKE,
+                                FAKE, need, None, None) == INVALID
+    assert lib.hill_last_error() != b""
+
+
+def test_head_count_limits(H):
+    d = base_desc(H, Hq=512, Hkv=2)
+    assert call_step(H, d, ws_bytes=1 << 40) == UNSUPPORTED
+    d = base_desc(H, Hq=256, Hkv=1)      # 256 heads per KV head
+    assert call_step(H, d, ws_bytes=1 << 40) == UNSUPPORTED

@@ -417,3 +417,96 @@ def test_errors_raise_and_enqueue_nothing():
         H().hill_step(q[0], k, v, s, 101)
     torch.cuda.synchronize()
     assert float(s.abs().max()) == 0.0
+
+
+# ----------------------------------------------- asymmetric-precision sketch --
+
+def _sketch_ref(x_k, dt):
+    codes, exps = O.sketch(bits(x_k), dt)
+    return codes, exps
+
+
+@pytest.mark.parametrize("dt,B,Hkv,n,t0,t1", [
+    ("bf16", 1, 8, 4096, 0, 4096), ("fp16", 2, 4, 777, 0, 777), ("bf16", 2, 2, 1000, 123, 517),
+    ("bf16", 1, 1, 5, 4, 5),
+])
+def test_sketch_keys_bit_exact(dt, B, Hkv, n, t0, t1):
+    say("sketch keys", dt, B, Hkv, n, t0, t1)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float16
+    g = torch.Generator().manual_seed(n + t0)
+    k = torch.randn(B, Hkv, n, 128, generator=g) * torch.exp(torch.randn(1, Hkv, 1, 128, generator=g))
+    k[:, :, ::97] = 0.0                                   # all-zero rows
+    k[:, :, 1::89] *= 1e-30                               # tiny rows (exponent clamp)
+    k[:, :, 2::53, :5] = 0.5                              # ties at half a code step in some rows
+    k = k.to(tdt)
+    sk = H().sketch_keys(k.to(DEV), token_begin=t0, token_end=t1)
+    torch.cuda.synchronize()
+    codes, exps = _sketch_ref(k, dt)
+    got_c, got_e = sk.codes.cpu().numpy(), sk.exps.cpu().numpy()
+    assert np.array_equal(got_c[:, :, t0:t1], codes[:, :, t0:t1])
+    assert np.array_equal(got_e[:, :, t0:t1], exps[:, :, t0:t1])
+    assert not got_c[:, :, :t0].any() and not got_c[:, :, t1:].any()          # untouched outside the range
+    assert (got_e[:, :, :t0] == -128).all() and (got_e[:, :, t1:] == -128).all()
+
+
+SKETCH_SCORE_CASES = [
+    # B, Hq, Hkv, n, dtype, mode, gran
+    (1, 32, 8, 4096, "bf16", "attn", "token"),
+    (2, 8, 2, 1001, "fp16", "attn", "kvhead"),
+    (1, 32, 32, 777, "fp16", "raw", "token"),
+    (2, 16, 4, 2049, "bf16", "raw", "kvhead"),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,dt,mode,gran", SKETCH_SCORE_CASES)
+def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran):
+    say("sketch score", B, Hq, Hkv, n, dt, mode, gran)
+    T = 2
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=T, seed=n + 3 * Hq)
+    q, k, v = gpu_inputs(x)
+    sk = H().sketch_keys(k)
+    k8, ek = _sketch_ref(x.k, dt)
+    R = R_of(gran, Hkv)
+    s = H().new_importance(B, R, n, DEV)
+    s_ref = np.zeros((B, R, n))
+    for t in range(T):
+        H().hill_score(q[t], None, s, mode=mode, granularity=gran, sketch=sk)
+        q8, eq = O.sketch(bits(x.q[t]), dt)
+        s_ref = O.update(O.logits_i8(q8, eq, k8, ek), s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        torch.cuda.synchronize()
+        check_scores(s.cpu().numpy(), s_ref, "sketch step %d" % t)
+
+
+def _run_sketch_steps(x, k_sel, mode, gran, steps, where):
+    B, Hkv, n = x.k.shape[0], x.k.shape[1], x.k.shape[2]
+    dt = dname(x.k)
+    q, k, v = gpu_inputs(x)
+    sk = H().sketch_keys(k)
+    k8, ek = _sketch_ref(x.k, dt)
+    R = R_of(gran, Hkv)
+    s = H().new_importance(B, R, n, DEV)
+    s_ref = np.zeros((B, R, n))
+    for t in range(steps):
+        idx, out = H().hill_step(q[t], k, v, s, k_sel, mode=mode, granularity=gran, sketch=sk)
+        q8, eq = O.sketch(bits(x.q[t]), dt)
+        s_ref = O.update(O.logits_i8(q8, eq, k8, ek), s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        torch.cuda.synchronize()
+        idx_g = idx.cpu().numpy()
+        check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t))
+        check_selection(idx_g, s_ref, k_sel, "%s step %d sel" % (where, t))
+        # attention reads the 16-bit K and V of the selected tokens
+        out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, gran)
+        check_outputs(out.cpu().numpy(), out_own, "%s step %d out" % (where, t))
+
+
+@pytest.mark.parametrize("mode,gran", [("attn", "token"), ("attn", "kvhead"), ("raw", "token")])
+def test_step_on_sketch_matches_oracle(mode, gran):
+    x = W.make_random(2, 32, 8, 128, 3000, "bf16", steps=3, seed=77)
+    _run_sketch_steps(x, 300, mode, gran, 3, "sketch %s/%s" % (mode, gran))
+
+
+def test_step_on_sketch_config3_full_size():
+    w = W.WORKLOADS[3]
+    say("sketch config 3 layer 0, 2 steps")
+    x = W.make_layer(w.replace(steps=2), 0)
+    _run_sketch_steps(x, w.k_sel, "attn", "token", 2, "sketch cfg3")
