@@ -21,6 +21,9 @@ Prints one JSON line:
                (hill_step_profiled, on the library's stream), vs 8 TB/s
   scoring_*    the scoring stage (scan + normaliser + S update)
   select_attn_us_per_layer_step   selection + gather attention, per layer-step
+  sketch       the same steps scored on the int8 key sketch (Sec. 4.4
+               asymmetric precision): step time, scan roofline on its own
+               bytes, selection agreement with the 16-bit path
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
@@ -278,12 +281,81 @@ def run_bench(args):
         "layer_step_us_probe": round(mean(total) * 1e3, 3),
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
     }
+    if not args.no_sketch:
+        res["sketch"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (%.0f s budget)" % args.cpu_seconds)
         res["cpu_baseline"] = cpu_baseline(W.WORKLOADS[int(args.workload)], args.cpu_seconds)
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
+
+
+def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
+    """The same decode steps scored on the int8 key sketch (Sec. 4.4
+    asymmetric precision; selection and attention unchanged).  The sketches
+    are written once before timing, as when the cache is filled; in a decode
+    loop only the appended row is sketched per step."""
+    import torch
+    import paper_2602_18750_amd as H
+
+    dev = torch.device("cuda:0")
+    sks = [H.sketch_keys(x.k) for (x, _) in layers]
+    ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
+    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L])
+             for L, (x, _) in enumerate(layers)]
+    hip = HipEvents()
+    ev_sets = []
+    for _ in range(args.steps):
+        e = [hip.create() for _ in range(6)]
+        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+    for i in range(args.warmup):
+        for L in range(nl_run):
+            calls[L](qptrs[L][i % T])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        t = (args.warmup + i) % T
+        probe = i % nl_run
+        for L in range(nl_run):
+            if L == probe:
+                calls[L](qptrs[L][t], ev_sets[i][1])
+            else:
+                calls[L](qptrs[L][t])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    scan = sum(hip.ms(e[0], e[1]) for e, _ in ev_sets) / len(ev_sets)
+    score = sum(hip.ms(e[0], e[2]) for e, _ in ev_sets) / len(ev_sets)
+    selattn = sum(hip.ms(e[2], e[5]) for e, _ in ev_sets) / len(ev_sets)
+    hip.close()
+    ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
+    units = (w.n_tokens + 255) // 256
+    npart = (units + 1) // 2 * 2
+    scan_bytes = (w.batch * w.n_kv_heads * w.n_tokens * (128 + 1) + w.batch * w.n_q_heads * w.n_tokens * 4
+                  + w.batch * w.n_q_heads * npart * 8)
+    scan_gbs = scan_bytes / (scan * 1e-3) / 1e9
+    # selection agreement with the 16-bit path: one step from zero importance on layer 0
+    x = layers[0][0]
+    s16 = H.new_importance(w.batch, 1, w.n_tokens, dev)
+    s8 = H.new_importance(w.batch, 1, w.n_tokens, dev)
+    i16, _ = H.hill_step(x.q[0], x.k, x.v, s16, w.k_sel, ws=ws, stream=stream)
+    i8, _ = H.hill_step(x.q[0], x.k, x.v, s8, w.k_sel, ws=ws, stream=stream, sketch=sks[0])
+    torch.cuda.synchronize()
+    a, b = i16.cpu(), i8.cpu()
+    recall = sum(len(set(a[r, 0].tolist()) & set(b[r, 0].tolist())) for r in range(w.batch)) / (w.batch * w.k_sel)
+    del calls, sks, ss
+    return {
+        "ms_per_step": round(ms_step, 4),
+        "value_gbps_of_16bit_keys": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl /
+                                          (ms_step * 1e-3) / 1e9, 2),
+        "scan_us": round(scan * 1e3, 3),
+        "scan_algorithmic_bytes": scan_bytes,
+        "scan_gbps": round(scan_gbs, 1),
+        "scan_frac_hbm": round(scan_gbs / HBM_PEAK_GBS, 4),
+        "scoring_us_per_layer_step": round(score * 1e3, 3),
+        "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
+        "selection_recall_vs_16bit": round(recall, 4),
+    }
 
 
 # ------------------------------------------------------------------ sweep --
@@ -447,6 +519,7 @@ def main():
     ap.add_argument("--workload", default="3", help="1..4 (default 3: the 32K-context Llama-3-8B-shaped decode)")
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sketch", action="store_true", help="skip the int8-sketch variant of the step")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")

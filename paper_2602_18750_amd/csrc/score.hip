@@ -25,6 +25,8 @@
 // products are combined by three DPP adds.
 #include <hip/hip_ext.h>
 
+#include <type_traits>
+
 #include "hill_device.h"
 #include "hill_internal.h"
 
@@ -67,10 +69,13 @@ __device__ __forceinline__ TileCoord coord(const ScoreArgs& a, int t)
 // of each of its 4 rows (two 16-byte non-temporal loads per row).
 template <int DT, int GC>
 struct KeysF16 {
+    static constexpr int kSlots = 1;   // tiles whose loads are in flight together
+    static constexpr bool kGroupQuery = false;
     uint4 kr[2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
 
+    template <int SLOT>
     __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
     {
         const uint16_t* kb = a.k + (int64_t)c.b * a.k_sb + (int64_t)c.g * a.k_sh + l8 * 8;
@@ -101,6 +106,7 @@ struct KeysF16 {
         q_tag = tag;
     }
 
+    template <int SLOT>
     __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
     {
         float d = dot8<DT>(kr[2 * u], qa[hh]);
@@ -111,17 +117,28 @@ struct KeysF16 {
 
 // int8 sketch (Sec. 4.4 asymmetric precision): lane l8 holds codes
 // [16*l8, 16*l8+16) of each of its 4 rows (one 16-byte load per row) and the
-// rows' exponents; the queries are cast to int8 the same way (power-of-two
-// scale per head, round to nearest even) when the group changes.  The dot
-// product is exact in int32 (|sum| < 2^24) and scaled by 2^(e_q + e_k).
+// rows' exponents.  The queries of the group are cast to int8 the same way
+// (power-of-two scale per head, round to nearest even) once per workgroup
+// when the group changes: wave w casts heads w, w+4, ... into LDS
+// (group_query), and every wave reads its slices from there (query).  The
+// dot product is exact in int32 (|sum| < 2^24) and scaled by 2^(e_q + e_k).
+struct QueryLds {
+    int8_t q8[kMaxGroup][kHeadDim];
+    int eq[kMaxGroup];
+};
+
 template <int DT, int GC>
 struct KeysI8 {
-    uint4 kr[kRowsPerLane];
-    uint32_t ek4;   // exponents of the 4 rows, one byte each
+    static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
+    static constexpr bool kGroupQuery = true;
+    uint4 kr[kSlots][kRowsPerLane];
+    uint32_t ek4[kSlots];   // exponents of the 4 rows, one byte each
     uint4 q8[GC];
     int eq[GC];
     int q_tag = -1;
+    QueryLds* ql = nullptr;
 
+    template <int SLOT>
     __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
     {
         const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
@@ -130,10 +147,27 @@ struct KeysI8 {
 #pragma unroll
         for (int u = 0; u < kRowsPerLane; ++u) {
             const int j = jr + u;
-            kr[u] = j < a.n ? load_stream16(kb + (int64_t)j * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+            kr[SLOT][u] = j < a.n ? load_stream16(kb + (int64_t)j * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
         }
         // jr is a multiple of 4 and cap too: the 4 exponents are one aligned word inside the row
-        ek4 = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
+        ek4[SLOT] = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
+    }
+
+    // Casts the G queries of group (b, g) into ql; wave w takes heads w, w+4, ...
+    // and lane l elements 2l, 2l+1.  Called by every wave; the caller orders
+    // it with a barrier before the reads.
+    __device__ __forceinline__ void group_query(const ScoreArgs& a, int b, int g, int w, int lane)
+    {
+        for (int h = w; h < a.G; h += 4) {
+            const uint16_t* qr = a.q + (int64_t)b * a.q_sb + (int64_t)(g * a.G + h) * a.q_sh;
+            float x0, x1;
+            widen2<DT>(*reinterpret_cast<const uint32_t*>(qr + 2 * lane), x0, x1);
+            const int e = sketch_exponent(wave_max(fmaxf(fabsf(x0), fabsf(x1))));
+            const uint32_t c2 = ((uint32_t)sketch_code(x0, e) & 0xffu) | (((uint32_t)sketch_code(x1, e) & 0xffu) << 8);
+            *reinterpret_cast<uint16_t*>(&ql->q8[h][2 * lane]) = (uint16_t)c2;
+            if (lane == 0) ql->eq[h] = e;
+        }
+        q_tag = -1;
     }
 
     __device__ __forceinline__ void query(const ScoreArgs& a, const TileCoord& c, int hc, int l8)
@@ -142,45 +176,27 @@ struct KeysI8 {
         if (tag == q_tag) return;
 #pragma unroll
         for (int hh = 0; hh < GC; ++hh) {
-            const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + hc + hh) * a.q_sh + l8 * 16;
-            const uint4 w0 = *reinterpret_cast<const uint4*>(qr);
-            const uint4 w1 = *reinterpret_cast<const uint4*>(qr + 8);
-            const uint32_t pw[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
-            float x[16];
-            float amax = 0.0f;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                widen2<DT>(pw[i], x[2 * i], x[2 * i + 1]);
-                amax = fmaxf(amax, fmaxf(fabsf(x[2 * i]), fabsf(x[2 * i + 1])));
-            }
-            const int e = sketch_exponent(max8(amax));   // the head's 128 elements sit in 8 lanes
-            uint32_t packed[4];
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                uint32_t v = 0u;
-#pragma unroll
-                for (int b = 0; b < 4; ++b) v |= ((uint32_t)sketch_code(x[4 * w + b], e) & 0xffu) << (8 * b);
-                packed[w] = v;
-            }
-            q8[hh] = make_uint4(packed[0], packed[1], packed[2], packed[3]);
-            eq[hh] = e;
+            q8[hh] = *reinterpret_cast<const uint4*>(&ql->q8[hc + hh][16 * l8]);
+            eq[hh] = ql->eq[hc + hh];
         }
         q_tag = tag;
     }
 
+    template <int SLOT>
     __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
     {
-        int d = __builtin_amdgcn_sdot4((int)kr[u].x, (int)q8[hh].x, 0, false);
-        d = __builtin_amdgcn_sdot4((int)kr[u].y, (int)q8[hh].y, d, false);
-        d = __builtin_amdgcn_sdot4((int)kr[u].z, (int)q8[hh].z, d, false);
-        d = __builtin_amdgcn_sdot4((int)kr[u].w, (int)q8[hh].w, d, false);
+        const uint4 k = kr[SLOT][u];
+        int d = __builtin_amdgcn_sdot4((int)k.x, (int)q8[hh].x, 0, false);
+        d = __builtin_amdgcn_sdot4((int)k.y, (int)q8[hh].y, d, false);
+        d = __builtin_amdgcn_sdot4((int)k.z, (int)q8[hh].z, d, false);
+        d = __builtin_amdgcn_sdot4((int)k.w, (int)q8[hh].w, d, false);
         d = isum8(d);
-        const int ek = (int)(int8_t)(ek4 >> (8 * u));
+        const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * u));
         return ldexpf((float)d, eq[hh] + ek);
     }
 };
 
-template <int GC, int OUT, typename Keys>
+template <int GC, int OUT, int SLOT, typename Keys>
 __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord& c, int rg, int l8, Keys& ks,
                                              float2* tile_part)
 {
@@ -197,7 +213,7 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord
             mine[u] = 0.0f;
 #pragma unroll
             for (int hh = 0; hh < GC; ++hh) {
-                const float d = ks.dot(a, u, hh, l8);
+                const float d = ks.template dot<SLOT>(a, u, hh, l8);
                 if constexpr (OUT == kOutLogits)
                     mine[u] = (l8 == hh) ? d : mine[u];
                 else
@@ -281,6 +297,7 @@ template <int GC, int OUT, typename Keys>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
     __shared__ float2 tile_part[kUnitTiles][kMaxGroup];   // ATTN: per tile of the unit, per head of the group
+    __shared__ typename std::conditional<Keys::kGroupQuery, QueryLds, int>::type qlds;
     const int lane = threadIdx.x & 63;
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int rg = lane >> 3;
@@ -296,19 +313,38 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
     int u = blockIdx.x * per;
     const int u_end = min(u + per, total);
 
+    static_assert(kUnitTiles == 8, "each wave takes two tiles of a unit");
     Keys ks;
+    int cur_bg = -1;
     for (; u < u_end; ++u) {
         const int bg = u / a.npart, unit = u % a.npart;
-#pragma unroll
-        for (int i = wv; i < kUnitTiles; i += 4) {
-            const int tile = unit * kUnitTiles + i;
-            if (tile < a.ntiles) {
-                const TileCoord c = coord(a, bg * a.ntiles + tile);
-                ks.load(a, c, rg, l8);
-                compute_tile<GC, OUT>(a, c, rg, l8, ks, tile_part[i]);
-            } else if constexpr (OUT == kOutLogits) {
-                for (int h = lane; h < a.G; h += 64) tile_part[i][h] = make_float2(-INFINITY, 0.0f);
+        if constexpr (Keys::kGroupQuery) {
+            if (bg != cur_bg) {   // workgroup-uniform
+                if (cur_bg >= 0 && OUT != kOutLogits) __syncthreads();   // earlier reads of the casts are done
+                ks.ql = &qlds;
+                ks.group_query(a, bg / a.Hkv, bg % a.Hkv, wv, lane);
+                __syncthreads();
+                cur_bg = bg;
             }
+        }
+        const int i0 = wv, i1 = wv + 4;   // this wave's tiles of the unit
+        const int t0 = unit * kUnitTiles + i0, t1 = unit * kUnitTiles + i1;
+        const TileCoord c0 = coord(a, bg * a.ntiles + min(t0, a.ntiles - 1));
+        const TileCoord c1 = coord(a, bg * a.ntiles + min(t1, a.ntiles - 1));
+        if (t0 < a.ntiles) ks.template load<0>(a, c0, rg, l8);
+        if constexpr (Keys::kSlots == 2) {   // both tiles in flight at once
+            if (t1 < a.ntiles) ks.template load<1>(a, c1, rg, l8);
+        }
+        if (t0 < a.ntiles) {
+            compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
+        } else if constexpr (OUT == kOutLogits) {
+            for (int h = lane; h < a.G; h += 64) tile_part[i0][h] = make_float2(-INFINITY, 0.0f);
+        }
+        if (t1 < a.ntiles) {
+            if constexpr (Keys::kSlots == 1) ks.template load<0>(a, c1, rg, l8);
+            compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
+        } else if constexpr (OUT == kOutLogits) {
+            for (int h = lane; h < a.G; h += 64) tile_part[i1][h] = make_float2(-INFINITY, 0.0f);
         }
         if constexpr (OUT == kOutLogits) {
             __syncthreads();
