@@ -51,6 +51,7 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "scoring GB/s of K scanned (% HBM peak) + select+attn µs/layer-step at 32K ctx"
 COUNTERS_FILE = os.path.join(ROOT, "profiles", "score_tiles_counters.json")
 SCORE_SRC = os.path.join(ROOT, "paper_2602_18750_amd", "csrc", "score.hip")
+COUNTERS_WORKLOAD = 3   # the counters are taken on the default workload (Llama-3-8B-shaped 32K)
 
 
 def log(*a):
@@ -104,14 +105,18 @@ def scan_kernel_bytes(B, Hq, Hkv, D, n, mode="attn"):
     return kbytes + B * Hq * n * 4 + B * Hq * npart * 8
 
 
-def load_traffic(per_launch_bytes_hint=None):
-    """HBM traffic of score_tiles from committed counter runs, only while the
-    kernel source is unchanged since the counters were taken."""
+def load_traffic(which="keys16"):
+    """HBM traffic of one score_tiles launch (which = "keys16" for the scan of
+    the 16-bit keys, "sketch" for the scan of the int8 sketch) from committed
+    counter runs, only while the kernel source is unchanged since the counters
+    were taken."""
     try:
         rec = json.load(open(COUNTERS_FILE))
         src = hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest()
         if rec.get("source_sha256") != src:
             return None
+        if which == "sketch":
+            return (rec.get("sketch") or {}).get("hbm_bytes_per_launch")
         return rec.get("hbm_bytes_per_launch")
     except (OSError, ValueError):
         return None
@@ -240,7 +245,7 @@ def run_bench(args):
     achieved = scan_bytes / (scan_us * 1e-6) / 1e9
     score_us = mean(score) * 1e3
     scoring_gbs = kbytes_layer / (score_us * 1e-6) / 1e9
-    traffic = load_traffic()
+    traffic = load_traffic() if w.id == COUNTERS_WORKLOAD else None
 
     res = {
         "metric": METRIC,
@@ -334,6 +339,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     scan_bytes = (w.batch * w.n_kv_heads * w.n_tokens * (128 + 1) + w.batch * w.n_q_heads * w.n_tokens * 4
                   + w.batch * w.n_q_heads * npart * 8)
     scan_gbs = scan_bytes / (scan * 1e-3) / 1e9
+    traffic = load_traffic("sketch")
     # selection agreement with the 16-bit path: one step from zero importance on layer 0
     x = layers[0][0]
     s16 = H.new_importance(w.batch, 1, w.n_tokens, dev)
@@ -352,6 +358,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
         "scan_algorithmic_bytes": scan_bytes,
         "scan_gbps": round(scan_gbs, 1),
         "scan_frac_hbm": round(scan_gbs / HBM_PEAK_GBS, 4),
+        "scan_traffic": traffic if w.id == COUNTERS_WORKLOAD else None,
         "scoring_us_per_layer_step": round(score * 1e3, 3),
         "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
         "selection_recall_vs_16bit": round(recall, 4),
@@ -447,25 +454,29 @@ def make_counters(directory: str, command: str):
         return sum(xs) / len(xs)
 
     copy_bytes = 1 << 30
-    f_kib = mean(_counter_rows(os.path.join(directory, "fetch"), "FETCH_SIZE", "score_tiles"))
-    w_kib = mean(_counter_rows(os.path.join(directory, "write"), "WRITE_SIZE", "score_tiles"))
     cf_kib = mean(_counter_rows(os.path.join(directory, "calib_fetch"), "FETCH_SIZE", "bitwise_not"))
     cw_kib = mean(_counter_rows(os.path.join(directory, "calib_write"), "WRITE_SIZE", "bitwise_not"))
     ff = copy_bytes / (cf_kib * 1024.0)
     wf = copy_bytes / (cw_kib * 1024.0)
-    rec = {
-        "kernel": "score_tiles",
-        "source_sha256": hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest(),
-        "fetch_kib_per_dispatch": round(f_kib, 1),
-        "write_kib_per_dispatch": round(w_kib, 1),
+
+    def scan(keys):   # the score_tiles instantiation over `keys` (KeysF16 or KeysI8)
+        f_kib = mean(_counter_rows(os.path.join(directory, "fetch"), "FETCH_SIZE", keys))
+        w_kib = mean(_counter_rows(os.path.join(directory, "write"), "WRITE_SIZE", keys))
+        return {"fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1),
+                "hbm_bytes_per_launch": int(round(f_kib * 1024.0 * ff + w_kib * 1024.0 * wf))}
+
+    rec = {"kernel": "score_tiles (16-bit keys)",
+           "source_sha256": hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest()}
+    rec.update(scan("KeysF16"))
+    rec.update({
         "copy_bytes": copy_bytes,
         "copy_fetch_kib": round(cf_kib, 1),
         "copy_write_kib": round(cw_kib, 1),
         "fetch_factor": round(ff, 4),
         "write_factor": round(wf, 4),
-        "hbm_bytes_per_launch": int(round(f_kib * 1024.0 * ff + w_kib * 1024.0 * wf)),
+        "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan("KeysI8")),
         "command": command,
-    }
+    })
     print(json.dumps(rec, indent=1))
 
 
