@@ -428,6 +428,44 @@ def run_copy_calib(args):
     print(json.dumps({"copy_bytes": n, "repeats": 3}), flush=True)
 
 
+def run_read_ceiling(args):
+    """What a single plain streaming-read launch reaches at the scan's sizes:
+    the library's calibration read (hill_calib_read: 16-byte non-temporal
+    loads, eight in flight per lane, one contiguous share per workgroup) over
+    16 MiB .. 1 GiB, the best of a few grid sizes, rotated through replicas so
+    that at least 1 GiB is touched between reuses; event-timed like the scan."""
+    import torch
+    import paper_2602_18750_amd as H
+    stream = torch.cuda.current_stream()
+    sink = torch.empty(65536, dtype=torch.int32, device="cuda:0")
+    for mib in (16, 32, 64, 256, 1024):
+        reps = max(1, min(16, 1024 // mib))
+        xs = [torch.empty(mib << 20, dtype=torch.uint8, device="cuda:0").fill_(r + 1) for r in range(reps)]
+        best = None
+        for grid in (1024, 2048, 4096, 8192):
+            for x in xs:
+                H.calib_read(x, grid, sink, stream=stream)
+            torch.cuda.synchronize()
+            iters = max(20, reps)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+            for i in range(iters):
+                ev[i][0].record(stream)
+                H.calib_read(xs[i % reps], grid, sink, stream=stream)
+                ev[i][1].record(stream)
+            torch.cuda.synchronize()
+            ts = sorted(a.elapsed_time(b) for a, b in ev)
+            med = ts[len(ts) // 2]
+            if best is None or med < best[0]:
+                best = (med, grid)
+        med, grid = best
+        gbs = (mib << 20) / (med * 1e-3) / 1e9
+        print(json.dumps({"read_mib": mib, "kernel": "hill_calib_read", "grid": grid, "median_us": round(med * 1e3, 2),
+                          "gbps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "replicas": reps}),
+              flush=True)
+        del xs
+        torch.cuda.empty_cache()
+
+
 def _counter_rows(directory: str, counter: str, name_part: str):
     """Per-dispatch values of `counter` for kernels whose name contains name_part."""
     import csv
@@ -534,6 +572,7 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")
+    ap.add_argument("--read-ceiling", action="store_true", help="time a plain library streaming read at the scan's sizes")
     ap.add_argument("--summarize", metavar="DIR")
     ap.add_argument("--counters", metavar="DIR", help="write the score_tiles traffic record from --pmc runs under DIR")
     ap.add_argument("--counters-command", default="", help="command line recorded with --counters")
@@ -553,6 +592,8 @@ def main():
         return 2
     if args.copy_calib:
         run_copy_calib(args)
+    elif args.read_ceiling:
+        run_read_ceiling(args)
     elif args.sweep:
         run_sweep(args)
     else:

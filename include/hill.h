@@ -203,6 +203,14 @@ hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, c
                              int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                              const hill_step_events* ev);
 
+/* Roofline calibration (measurement aid, computes nothing of the method):
+ * one launch of `grid` workgroups that reads `bytes` bytes of the device
+ * buffer `buf` once, each workgroup a contiguous share, with 16-byte
+ * non-temporal loads.  buf 16-byte aligned, bytes a positive multiple of 16,
+ * 1 <= grid <= 65536; sink is a device array of `grid` words that the kernel
+ * may write (its contents are meaningless).  Errors as for every call. */
+hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

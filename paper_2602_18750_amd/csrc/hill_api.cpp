@@ -490,6 +490,17 @@ hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8
     return HILL_OK;
 }
 
+hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream)
+{
+    HILL_TRY(check_ptr(buf, "buf"));
+    if (!sink) return fail(HILL_ERR_INVALID_ARG, "sink is NULL");
+    if (bytes < 16 || bytes % 16) return fail(HILL_ERR_INVALID_ARG, "bytes %lld not a positive multiple of 16",
+                                              static_cast<long long>(bytes));
+    if (grid < 1 || grid > 65536) return fail(HILL_ERR_INVALID_ARG, "grid %d not in [1, 65536]", grid);
+    HIP_TRY(launch_calib_read(buf, bytes, grid, sink, static_cast<hipStream_t>(stream)));
+    return HILL_OK;
+}
+
 hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp, int64_t cap,
                               float* s_acc, void* ws, size_t ws_bytes, void* stream)
 {

@@ -137,6 +137,7 @@ struct Stamp {
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
 hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
+hipError_t launch_calib_read(const void* p, int64_t bytes, int grid, uint32_t* sink, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st);
 // Whether update_attn can reduce the softmax partials itself (no separate

@@ -153,20 +153,46 @@ struct KeysI8 {
         ek4[SLOT] = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
     }
 
+    // The raw query words of the group's first heads (wave w: heads w and
+    // w + 4, lane l: elements 2l, 2l+1), fetched before the key loads so that
+    // the cast waits only for them.
+    static constexpr int kQPre = 2;
+    uint32_t qpre[kQPre];
+
+    __device__ __forceinline__ const uint32_t* qword(const ScoreArgs& a, int b, int g, int h, int lane) const
+    {
+        return reinterpret_cast<const uint32_t*>(a.q + (int64_t)b * a.q_sb + (int64_t)(g * a.G + h) * a.q_sh +
+                                                 2 * lane);
+    }
+
+    __device__ __forceinline__ void group_query_fetch(const ScoreArgs& a, int b, int g, int w, int lane)
+    {
+#pragma unroll
+        for (int i = 0; i < kQPre; ++i) {
+            const int h = w + 4 * i;
+            qpre[i] = h < a.G ? *qword(a, b, g, h, lane) : 0u;
+        }
+    }
+
+    __device__ __forceinline__ void cast_head(uint32_t word, int h, int lane)
+    {
+        float x0, x1;
+        widen2<DT>(word, x0, x1);
+        const int e = sketch_exponent(wave_max(fmaxf(fabsf(x0), fabsf(x1))));
+        const uint32_t c2 = ((uint32_t)sketch_code(x0, e) & 0xffu) | (((uint32_t)sketch_code(x1, e) & 0xffu) << 8);
+        *reinterpret_cast<uint16_t*>(&ql->q8[h][2 * lane]) = (uint16_t)c2;
+        if (lane == 0) ql->eq[h] = e;
+    }
+
     // Casts the G queries of group (b, g) into ql; wave w takes heads w, w+4, ...
-    // and lane l elements 2l, 2l+1.  Called by every wave; the caller orders
-    // it with a barrier before the reads.
+    // (the first kQPre of them from group_query_fetch).  Called by every wave;
+    // the caller orders it with a barrier before the reads.
     __device__ __forceinline__ void group_query(const ScoreArgs& a, int b, int g, int w, int lane)
     {
-        for (int h = w; h < a.G; h += 4) {
-            const uint16_t* qr = a.q + (int64_t)b * a.q_sb + (int64_t)(g * a.G + h) * a.q_sh;
-            float x0, x1;
-            widen2<DT>(*reinterpret_cast<const uint32_t*>(qr + 2 * lane), x0, x1);
-            const int e = sketch_exponent(wave_max(fmaxf(fabsf(x0), fabsf(x1))));
-            const uint32_t c2 = ((uint32_t)sketch_code(x0, e) & 0xffu) | (((uint32_t)sketch_code(x1, e) & 0xffu) << 8);
-            *reinterpret_cast<uint16_t*>(&ql->q8[h][2 * lane]) = (uint16_t)c2;
-            if (lane == 0) ql->eq[h] = e;
-        }
+#pragma unroll
+        for (int i = 0; i < kQPre; ++i)
+            if (w + 4 * i < a.G) cast_head(qpre[i], w + 4 * i, lane);
+        for (int h = w + 4 * kQPre; h < a.G; h += 4) cast_head(*qword(a, b, g, h, lane), h, lane);
         q_tag = -1;
     }
 
@@ -318,22 +344,31 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
     int cur_bg = -1;
     for (; u < u_end; ++u) {
         const int bg = u / a.npart, unit = u % a.npart;
+        const int i0 = wv, i1 = wv + 4;   // this wave's tiles of the unit
+        const int t0 = unit * kUnitTiles + i0, t1 = unit * kUnitTiles + i1;
+        const TileCoord c0 = coord(a, bg * a.ntiles + min(t0, a.ntiles - 1));
+        const TileCoord c1 = coord(a, bg * a.ntiles + min(t1, a.ntiles - 1));
         if constexpr (Keys::kGroupQuery) {
-            if (bg != cur_bg) {   // workgroup-uniform
+            // query words first, then both tiles' keys (clamped coordinates: no
+            // branch between them), then the cast, which waits only for the query
+            const bool fresh = bg != cur_bg;   // workgroup-uniform
+            if (fresh) {
                 if (cur_bg >= 0 && OUT != kOutLogits) __syncthreads();   // earlier reads of the casts are done
+                ks.group_query_fetch(a, bg / a.Hkv, bg % a.Hkv, wv, lane);
+            }
+            ks.template load<0>(a, c0, rg, l8);
+            ks.template load<1>(a, c1, rg, l8);
+            if (fresh) {
                 ks.ql = &qlds;
                 ks.group_query(a, bg / a.Hkv, bg % a.Hkv, wv, lane);
                 __syncthreads();
                 cur_bg = bg;
             }
-        }
-        const int i0 = wv, i1 = wv + 4;   // this wave's tiles of the unit
-        const int t0 = unit * kUnitTiles + i0, t1 = unit * kUnitTiles + i1;
-        const TileCoord c0 = coord(a, bg * a.ntiles + min(t0, a.ntiles - 1));
-        const TileCoord c1 = coord(a, bg * a.ntiles + min(t1, a.ntiles - 1));
-        if (t0 < a.ntiles) ks.template load<0>(a, c0, rg, l8);
-        if constexpr (Keys::kSlots == 2) {   // both tiles in flight at once
-            if (t1 < a.ntiles) ks.template load<1>(a, c1, rg, l8);
+        } else {
+            if (t0 < a.ntiles) ks.template load<0>(a, c0, rg, l8);
+            if constexpr (Keys::kSlots == 2) {   // both tiles in flight at once
+                if (t1 < a.ntiles) ks.template load<1>(a, c1, rg, l8);
+            }
         }
         if (t0 < a.ntiles) {
             compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);

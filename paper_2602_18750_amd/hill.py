@@ -37,7 +37,7 @@ GRANS = {"token": 0, "kvhead": 1}
 
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
-           "hill_score_sketch", "hill_step_sketch")
+           "hill_score_sketch", "hill_step_sketch", "hill_calib_read")
 
 
 class HillError(RuntimeError):
@@ -120,6 +120,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, P, I32, P, P, P, SZ, P,
                                          ctypes.POINTER(HillStepEvents)]
         lib.hill_step_sketch.restype = ctypes.c_int
+        lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
+        lib.hill_calib_read.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -253,6 +255,18 @@ def sketch_keys(k, sketch: Optional[Sketch] = None, *, token_begin=0, token_end=
     _check(lib.hill_sketch_keys(ctypes.byref(desc), _ptr(k), _ptr(sketch.codes), _ptr(sketch.exps), sketch.cap,
                                 int(token_begin), t1, _stream_ptr(stream)))
     return sketch
+
+
+def calib_read(buf, grid: int, sink, stream=None) -> None:
+    """One launch of the library's plain streaming read over the bytes of
+    ``buf`` (roofline calibration; computes nothing of the method).  ``sink``
+    is a device int32/uint32 tensor of at least ``grid`` words."""
+    lib = load_library()
+    _device_check(buf, sink)
+    if sink.numel() < grid or sink.element_size() != 4:
+        raise ValueError("sink needs at least grid 4-byte words")
+    _check(lib.hill_calib_read(_ptr(buf), buf.numel() * buf.element_size(), int(grid), _ptr(sink),
+                               _stream_ptr(stream)))
 
 
 def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0, ws=None,

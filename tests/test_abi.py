@@ -215,3 +215,14 @@ def test_head_count_limits(H):
     assert call_step(H, d, ws_bytes=1 << 40) == UNSUPPORTED
     d = base_desc(H, Hq=256, Hkv=1)      # 256 heads per KV head
     assert call_step(H, d, ws_bytes=1 << 40) == UNSUPPORTED
+
+
+def test_calib_read_validates(H):
+    lib = H.load_library()
+    assert lib.hill_calib_read(None, 1024, 4, FAKE, None) == INVALID
+    assert lib.hill_calib_read(FAKE + 8, 1024, 4, FAKE, None) == INVALID     # misaligned buffer
+    assert lib.hill_calib_read(FAKE, 1024, 4, None, None) == INVALID          # no sink
+    assert lib.hill_calib_read(FAKE, 1000, 4, FAKE, None) == INVALID          # not a multiple of 16
+    assert lib.hill_calib_read(FAKE, 0, 4, FAKE, None) == INVALID
+    assert lib.hill_calib_read(FAKE, 1024, 0, FAKE, None) == INVALID
+    assert lib.hill_calib_read(FAKE, 1024, 65537, FAKE, None) == INVALID

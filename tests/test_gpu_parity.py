@@ -477,6 +477,26 @@ def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran):
         check_scores(s.cpu().numpy(), s_ref, "sketch step %d" % t)
 
 
+@pytest.mark.parametrize("B,nh,n,dt", [(1, 16, 1000, "bf16"), (2, 8, 4099, "fp16")])
+def test_sketch_logits_bit_exact(B, nh, n, dt):
+    """A sketch logit is an integer dot product (at most 128 * 127 * 127 < 2^24
+    in magnitude) times a power of two, so in fp32 it is exact.  RAW, KV-head
+    rows of one head each, one step from S = 0: S is the logit itself, and the
+    GPU's must equal the oracle's exact value bit for bit."""
+    say("sketch logits exact", B, nh, n, dt)
+    x = W.make_random(B, nh, nh, 128, n, dt, steps=1, seed=4242 + n)
+    q, k, v = gpu_inputs(x)
+    sk = H().sketch_keys(k)
+    k8, ek = _sketch_ref(x.k, dt)
+    q8, eq = O.sketch(bits(x.q[0]), dt)
+    ref = O.logits_i8(q8, eq, k8, ek).astype(np.float32)   # exact in fp64, hence in fp32
+    s = H().new_importance(B, nh, n, DEV)
+    H().hill_score(q[0], None, s, mode="raw", granularity="kvhead", sketch=sk)
+    torch.cuda.synchronize()
+    got = s.cpu().numpy()[:, :, :n]
+    assert np.array_equal(got, ref.reshape(B, nh, n))
+
+
 def _run_sketch_steps(x, k_sel, mode, gran, steps, where):
     B, Hkv, n = x.k.shape[0], x.k.shape[1], x.k.shape[2]
     dt = dname(x.k)
