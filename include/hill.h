@@ -203,6 +203,52 @@ hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, c
                              int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                              const hill_step_events* ev);
 
+/* Bidirectional KV Cache Pools (Sec. 4.2, HKM / BKP): the per-token hit-rate
+ * table and the hot/cold pool policy, run once after each decoding step (the
+ * paper's background maintenance pass).  On one GPU both pools live in HBM;
+ * the call returns which tokens move between them, for a caller that keeps
+ * the cold pool in a slower tier.
+ *
+ * Per importance row (b, r) over its first N = n_tokens tokens:
+ *  1. hits[j] += 1 (saturating at 65535) for every j of this step's
+ *     selected set idx[b, r, 0..k_sel);
+ *  2. the most recent min(n_recent, N) tokens are hot (temporal pinning);
+ *  3. the other min(capacity, N) - min(n_recent, N) hot slots go to the
+ *     remaining tokens with the most hits; a token hot before the call wins a
+ *     tie in hits, then the lower index wins (frequency tracking: a cold
+ *     token is promoted only when it strictly exceeds the lowest-ranked hot
+ *     token, which is then demoted);
+ *  4. promote[b, r, :] lists the tokens that became hot and demote[b, r, :]
+ *     those that became cold, each ascending; counts[b, r, 0..1] are their
+ *     numbers (which may exceed list_cap: only the first list_cap entries of
+ *     each list are written).
+ * Positions at and beyond N are neither read nor written. */
+typedef struct hill_bkp_desc {
+    uint32_t struct_size;    /* sizeof(hill_bkp_desc) */
+    int32_t batch;           /* B >= 1 */
+    int32_t rows;            /* R >= 1 importance rows per sequence (1 in token mode, n_kv_heads in KV-head mode);
+                                B * R <= 65535 */
+    int32_t n_tokens;        /* N, 1 <= N <= 2097152 */
+    int32_t n_recent;        /* >= 0: recent tokens pinned hot */
+    int32_t capacity;        /* >= n_recent: hot pool size in tokens */
+    int64_t stride_b;        /* elements between sequences of hits and hot (>= R * stride_r when B > 1) */
+    int64_t stride_r;        /* elements between rows of hits and hot (>= N) */
+} hill_bkp_desc;
+
+/* Workspace bytes for hill_bkp_update (a pure function of the descriptor). */
+hill_status hill_bkp_workspace_bytes(const hill_bkp_desc* d, size_t* bytes);
+
+/* One BKP pass.  idx: int32 [B, R, k_sel] (the layout of hill_step's
+ * idx_out), indices unique within a row; entries outside [0, N) are skipped;
+ * k_sel in [0, N] (idx may be NULL when 0).  hits: uint16 [B, R, >= N] and
+ * hot: uint8 [B, R, >= N] (1 = hot, 0 = cold; bit 0 is read, 0 or 1 is
+ * written), both with the descriptor's strides, caller-owned, zero at the
+ * start of a sequence.  promote, demote: int32 [B, R, list_cap]; counts:
+ * int32 [B, R, 2].  All device pointers, asynchronous on `stream`. */
+hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t k_sel, uint16_t* hits,
+                            uint8_t* hot, int32_t* promote, int32_t* demote, int32_t list_cap, int32_t* counts,
+                            void* ws, size_t ws_bytes, void* stream);
+
 /* Roofline calibration (measurement aid, computes nothing of the method):
  * one launch of `grid` workgroups that reads `bytes` bytes of the device
  * buffer `buf` once, each workgroup a contiguous share, with 16-byte

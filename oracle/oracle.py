@@ -18,6 +18,12 @@ one definition of the paper (arxiv 2602.18750):
 * :func:`sparse_attn` -- Eq. 1 restricted to the selected tokens (Sec. 4.1,
                          workflow step 6).
 * :func:`step`        -- the three in the workflow's order.
+* :func:`sketch`, :func:`logits_i8` -- the int8 key/query casts and the
+                         integer logits of asymmetric-precision scoring
+                         (Sec. 4.4).
+* :func:`bkp_update`  -- the hit-rate table and the hot/cold pool policy of
+                         the Bidirectional KV Cache Pools (Sec. 4.2 HKM,
+                         BKP (1)-(3)), plain numpy on integers.
 
 16-bit inputs are passed as ``numpy.uint16`` bit patterns; the oracle decodes
 them itself (:func:`decode16`).
@@ -259,3 +265,53 @@ def budget_k(n: int, alpha: float) -> int:
     """Token budget k = floor(alpha * n), clamped to [1, n] (top-alpha percent, Sec. 3.1)."""
     import math
     return max(1, min(n, int(math.floor(alpha * n + 1e-9))))
+
+
+HIT_MAX = 65535   # the hit-rate table holds 2 bytes per token (Sec. 5.4 overhead analysis)
+
+
+def bkp_update(hits, hot, idx, n_tokens: int, n_recent: int, capacity: int):
+    """One maintenance pass of the Bidirectional KV Cache Pools after a
+    decoding step (Sec. 4.2 BKP), per row (b, r) of a [B, R, Ncap] table:
+
+    1. frequency tracking: every token of this step's selected set ``idx``
+       ([B, R, k]) gains one hit, saturating at 65535 (a 2-byte table);
+    2. temporal pinning: the ``n_recent`` most recent tokens of the first
+       ``n_tokens`` (all of them if fewer) are hot;
+    3. the remaining ``min(capacity, n_tokens) - n_recent`` hot slots go to
+       the other tokens with the most hits; a token already hot wins a tie in
+       hits (a cold token is promoted only when it strictly exceeds the
+       lowest-ranked hot token), then the lower token index wins;
+    4. promotions are tokens hot now and cold before, demotions the reverse,
+       each in ascending token order.
+
+    ``hits`` uint16 and ``hot`` bool/uint8 of shape [B, R, >= n_tokens].
+    Returns (hits, hot, promote, demote): updated copies and two nested lists
+    [B][R] of int arrays.  Positions at and beyond n_tokens are left as they
+    are."""
+    hits = np.array(hits, dtype=np.int64, copy=True)
+    hot_old = np.array(hot, dtype=bool, copy=True)
+    idx = np.asarray(idx, dtype=np.int64)
+    B, R = hits.shape[0], hits.shape[1]
+    N = int(n_tokens)
+    W = min(int(n_recent), N)
+    F = max(0, min(int(capacity), N) - W)
+    hot_new = hot_old.copy()
+    promote = [[None] * R for _ in range(B)]
+    demote = [[None] * R for _ in range(B)]
+    for b in range(B):
+        for r in range(R):
+            h = hits[b, r]
+            for j in idx[b, r]:                                  # step 1
+                h[j] = min(h[j] + 1, HIT_MAX)
+            new = np.zeros(N, dtype=bool)
+            new[N - W:] = True                                   # step 2
+            rest = np.arange(N - W)
+            old = hot_old[b, r, :N]
+            # step 3: order by hits (more first), incumbency (hot first), index
+            order = rest[np.lexsort((rest, ~old[rest], -h[rest]))]
+            new[order[:F]] = True
+            promote[b][r] = np.nonzero(new & ~old)[0]            # step 4
+            demote[b][r] = np.nonzero(old & ~new)[0]
+            hot_new[b, r, :N] = new
+    return hits.astype(np.uint16), hot_new, promote, demote

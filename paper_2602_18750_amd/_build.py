@@ -16,7 +16,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhill.so")
 
-SOURCES = ["hill_api.cpp", "score.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip"]
+SOURCES = ["hill_api.cpp", "score.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip", "bkp.hip"]
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

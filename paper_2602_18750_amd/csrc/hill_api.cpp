@@ -490,6 +490,139 @@ hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8
     return HILL_OK;
 }
 
+// ---------------------------------------------------------------- BKP pools --
+
+struct BkpLayout {
+    size_t v, flist, zero, hist1, hist2, cand_key, cand_n, state, sel_list, sel_n, end;
+    int64_t zero_words, ld;
+    int nchunks;
+};
+
+BkpLayout bkp_layout(const hill_bkp_desc* d)
+{
+    BkpLayout L{};
+    const size_t rows = (size_t)d->batch * d->rows;
+    const size_t n = (size_t)d->n_tokens;
+    L.ld = ((int64_t)n + 3) / 4 * 4;
+    L.nchunks = (int)((n + kSelChunk - 1) / kSelChunk);
+    size_t off = 0;
+    L.v = off;
+    off += align256(rows * (size_t)L.ld * sizeof(float));
+    L.flist = off;
+    off += align256(rows * n * sizeof(int32_t));
+    L.zero = L.hist1 = off;
+    L.hist2 = L.hist1 + rows * kHistRow * sizeof(uint32_t);
+    const size_t zero_end = L.hist2 + rows * kHistRow * sizeof(uint32_t);
+    L.zero_words = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
+    off = align256(zero_end);
+    L.cand_key = off;
+    off += align256(rows * n * sizeof(uint32_t));
+    L.cand_n = off;
+    off += align256(rows * L.nchunks * sizeof(uint32_t));
+    L.state = off;
+    off += align256(rows * sizeof(uint4));
+    L.sel_list = off;
+    off += align256(rows * n * sizeof(int32_t));
+    L.sel_n = off;
+    off += align256(rows * L.nchunks * sizeof(uint32_t));
+    L.end = off;
+    return L;
+}
+
+hill_status check_bkp(const hill_bkp_desc* d)
+{
+    if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
+    if (d->struct_size != sizeof(hill_bkp_desc))
+        return fail(HILL_ERR_INVALID_ARG, "struct_size %u != sizeof(hill_bkp_desc) %zu", d->struct_size,
+                    sizeof(hill_bkp_desc));
+    if (d->batch < 1 || d->rows < 1 || d->n_tokens < 1)
+        return fail(HILL_ERR_INVALID_ARG, "batch, rows and n_tokens must be >= 1");
+    if ((int64_t)d->batch * d->rows > 65535)
+        return fail(HILL_ERR_UNSUPPORTED, "batch * rows %lld exceeds 65535", (long long)d->batch * d->rows);
+    if ((int64_t)d->n_tokens > (int64_t)kMaxSlots * kSelChunk)
+        return fail(HILL_ERR_UNSUPPORTED, "n_tokens %d exceeds the supported %d", d->n_tokens, kMaxSlots * kSelChunk);
+    if (d->n_recent < 0 || d->capacity < d->n_recent)
+        return fail(HILL_ERR_INVALID_ARG, "need 0 <= n_recent (%d) <= capacity (%d)", d->n_recent, d->capacity);
+    if (d->stride_r < d->n_tokens) return fail(HILL_ERR_INVALID_ARG, "stride_r must be >= n_tokens");
+    if (d->batch > 1 && d->stride_b < (int64_t)d->rows * d->stride_r)
+        return fail(HILL_ERR_INVALID_ARG, "stride_b must be >= rows * stride_r");
+    return HILL_OK;
+}
+
+hill_status hill_bkp_workspace_bytes(const hill_bkp_desc* d, size_t* bytes)
+{
+    HILL_TRY(check_bkp(d));
+    if (!bytes) return fail(HILL_ERR_INVALID_ARG, "bytes is NULL");
+    *bytes = bkp_layout(d).end;
+    return HILL_OK;
+}
+
+hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t k_sel, uint16_t* hits, uint8_t* hot,
+                            int32_t* promote, int32_t* demote, int32_t list_cap, int32_t* counts, void* ws,
+                            size_t ws_bytes, void* stream)
+{
+    HILL_TRY(check_bkp(d));
+    if (k_sel < 0 || k_sel > d->n_tokens)
+        return fail(HILL_ERR_INVALID_ARG, "k_sel %d not in [0, n_tokens=%d]", k_sel, d->n_tokens);
+    if (k_sel > 0 && (!idx || ((uintptr_t)idx & 3u)))
+        return fail(HILL_ERR_INVALID_ARG, "idx is NULL or not 4-byte aligned");
+    if (!hits || ((uintptr_t)hits & 1u)) return fail(HILL_ERR_INVALID_ARG, "hits is NULL or not 2-byte aligned");
+    if (!hot) return fail(HILL_ERR_INVALID_ARG, "hot is NULL");
+    if (list_cap < 0) return fail(HILL_ERR_INVALID_ARG, "list_cap %d < 0", list_cap);
+    if (list_cap > 0 && (!promote || !demote || ((uintptr_t)promote & 3u) || ((uintptr_t)demote & 3u)))
+        return fail(HILL_ERR_INVALID_ARG, "promote / demote NULL or not 4-byte aligned");
+    if (!counts || ((uintptr_t)counts & 3u)) return fail(HILL_ERR_INVALID_ARG, "counts is NULL or not 4-byte aligned");
+    const BkpLayout L = bkp_layout(d);
+    HILL_TRY(check_ws(ws, ws_bytes, L.end));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int rows = d->batch * d->rows;
+    const int n = d->n_tokens;
+    BkpArgs a{};
+    a.idx = idx;
+    a.k = k_sel;
+    a.hits = hits;
+    a.hot = hot;
+    a.sb = d->stride_b;
+    a.sr = d->stride_r;
+    a.R = d->rows;
+    a.n = n;
+    a.w = d->n_recent < n ? d->n_recent : n;
+    a.f = (d->capacity < n ? d->capacity : n) - a.w;
+    a.v = at<float>(ws, L.v);
+    a.ld = L.ld;
+    a.flist = at<int32_t>(ws, L.flist);
+    a.promote = promote;
+    a.demote = demote;
+    a.list_cap = list_cap;
+    a.counts = counts;
+    HIP_TRY(launch_bkp_hits(a, rows, st));
+    HIP_TRY(launch_bkp_rank(a, rows, st));
+    if (a.f > 0) {   // frequency slots: the exact top-f of the rank values, ties to the lower index
+        RefineArgs r{};
+        r.s = a.v;
+        r.s_sb = (int64_t)d->rows * L.ld;
+        r.s_sr = L.ld;
+        r.R = d->rows;
+        r.n = n;
+        r.k = a.f;
+        r.nchunks = L.nchunks;
+        r.hist1 = at<uint32_t>(ws, L.hist1);
+        r.hist2 = at<uint32_t>(ws, L.hist2);
+        r.cand_key = at<uint32_t>(ws, L.cand_key);
+        r.cand_n = at<uint32_t>(ws, L.cand_n);
+        r.state = at<uint4>(ws, L.state);
+        r.sel_list = at<int32_t>(ws, L.sel_list);
+        r.sel_n = at<uint32_t>(ws, L.sel_n);
+        HIP_TRY(launch_fill_zero(at<uint32_t>(ws, L.zero), L.zero_words, st));
+        HIP_TRY(launch_topk_hist(a.v, r.s_sb, r.s_sr, d->batch, d->rows, n, at<uint32_t>(ws, L.hist1), st));
+        HIP_TRY(launch_topk_refine(r, rows, st));
+        HIP_TRY(launch_topk_emit_indices(r, rows, at<int32_t>(ws, L.flist), nullptr, st));
+        HIP_TRY(launch_bkp_mark(a, rows, st));
+    }
+    HIP_TRY(launch_bkp_lists(a, rows, st));
+    return HILL_OK;
+}
+
 hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream)
 {
     HILL_TRY(check_ptr(buf, "buf"));

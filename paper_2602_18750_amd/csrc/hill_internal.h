@@ -137,6 +137,27 @@ struct Stamp {
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
 hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
+// Bidirectional KV cache pools (bkp.hip).
+struct BkpArgs {
+    const int32_t* idx;   // [rows, k]
+    int k;
+    uint16_t* hits;       // [B, R, >= n] strided
+    uint8_t* hot;         // same strides as hits
+    int64_t sb, sr;
+    int R, n, w, f;       // w = min(n_recent, n); f = frequency slots
+    float* v;             // [rows, ld] rank values for the selection
+    int64_t ld;
+    const int32_t* flist; // [rows, f] frequency-hot tokens
+    int32_t* promote;     // [rows, list_cap]
+    int32_t* demote;
+    int list_cap;
+    int32_t* counts;      // [rows, 2]
+    __host__ __device__ int64_t off(int row) const { return (int64_t)(row / R) * sb + (int64_t)(row % R) * sr; }
+};
+hipError_t launch_bkp_hits(const BkpArgs& a, int rows, hipStream_t st);
+hipError_t launch_bkp_rank(const BkpArgs& a, int rows, hipStream_t st);
+hipError_t launch_bkp_mark(const BkpArgs& a, int rows, hipStream_t st);
+hipError_t launch_bkp_lists(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_calib_read(const void* p, int64_t bytes, int grid, uint32_t* sink, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st);

@@ -37,7 +37,8 @@ GRANS = {"token": 0, "kvhead": 1}
 
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
-           "hill_score_sketch", "hill_step_sketch", "hill_calib_read")
+           "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
+           "hill_bkp_update")
 
 
 class HillError(RuntimeError):
@@ -76,6 +77,13 @@ class HillStepEvents(ctypes.Structure):
     _fields_ = [("scan_start", ctypes.c_void_p), ("scan_stop", ctypes.c_void_p), ("score_stop", ctypes.c_void_p),
                 ("select_start", ctypes.c_void_p), ("select_stop", ctypes.c_void_p),
                 ("attn_stop", ctypes.c_void_p)]
+
+
+class BkpDesc(ctypes.Structure):
+    """hill_bkp_desc (include/hill.h)."""
+    _fields_ = [("struct_size", ctypes.c_uint32), ("batch", ctypes.c_int32), ("rows", ctypes.c_int32),
+                ("n_tokens", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("stride_b", ctypes.c_int64), ("stride_r", ctypes.c_int64)]
 
 
 _lock = threading.Lock()
@@ -122,6 +130,10 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_sketch.restype = ctypes.c_int
         lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
         lib.hill_calib_read.restype = ctypes.c_int
+        lib.hill_bkp_workspace_bytes.argtypes = [ctypes.POINTER(BkpDesc), ctypes.POINTER(SZ)]
+        lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
+        lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
+        lib.hill_bkp_update.restype = ctypes.c_int
         _lib = lib
         return lib
 
@@ -371,6 +383,56 @@ def new_importance(B: int, R: int, n_cap: int, device) -> torch.Tensor:
     """Zeroed fp32 importance buffer [B, R, n_cap] whose row stride is a multiple of 4."""
     pad = (n_cap + 3) // 4 * 4
     return torch.zeros((B, R, pad), dtype=torch.float32, device=device)[:, :, :n_cap]
+
+
+class BkpState:
+    """Per-token state of the Bidirectional KV Cache Pools for [B, R, n_cap]
+    tokens: the 2-byte hit table (held as int16, read as uint16 bit
+    patterns) and one pool byte per token (1 = hot)."""
+
+    def __init__(self, B: int, R: int, n_cap: int, device):
+        self.hits = torch.zeros((B, R, n_cap), dtype=torch.int16, device=device)
+        self.hot = torch.zeros((B, R, n_cap), dtype=torch.uint8, device=device)
+
+
+def bkp_desc(state: BkpState, n_tokens: int, n_recent: int, capacity: int) -> BkpDesc:
+    B, R, n_cap = state.hits.shape
+    if state.hits.stride() != state.hot.stride() or state.hits.stride(2) != 1:
+        raise ValueError("hits and hot need the same strides with tokens contiguous")
+    return BkpDesc(ctypes.sizeof(BkpDesc), B, R, int(n_tokens), int(n_recent), int(capacity),
+                   state.hits.stride(0), state.hits.stride(1))
+
+
+def bkp_update(state: BkpState, idx, *, n_tokens: int, n_recent: int, capacity: int, list_cap=None, ws=None,
+               stream=None):
+    """One BKP pass after a decoding step (Sec. 4.2): hits of the selected
+    tokens ``idx`` ([B, R, k] int32, or None) go up by one, the pool is
+    rebuilt from the recent window and the most-hit tokens; returns
+    (promote, demote, counts) device tensors ([B, R, list_cap] int32 each,
+    only the first counts[..., 0] / counts[..., 1] entries meaningful)."""
+    lib = load_library()
+    _device_check(state.hits, state.hot)
+    B, R, _ = state.hits.shape
+    d = bkp_desc(state, n_tokens, n_recent, capacity)
+    if list_cap is None:
+        list_cap = min(int(capacity), int(n_tokens))
+    dev = state.hits.device
+    if ws is None:
+        need = ctypes.c_size_t(0)
+        _check(lib.hill_bkp_workspace_bytes(ctypes.byref(d), ctypes.byref(need)))
+        ws = torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=dev)
+    k = 0 if idx is None else int(idx.shape[-1])
+    if idx is not None:
+        _device_check(idx)
+        if idx.dtype != torch.int32 or tuple(idx.shape) != (B, R, k) or not idx.is_contiguous():
+            raise ValueError("idx must be a contiguous int32 [B, R, k] tensor")
+    promote = torch.empty((B, R, max(list_cap, 1)), dtype=torch.int32, device=dev)
+    demote = torch.empty_like(promote)
+    counts = torch.empty((B, R, 2), dtype=torch.int32, device=dev)
+    _check(lib.hill_bkp_update(ctypes.byref(d), _ptr(idx) if idx is not None else None, k, _ptr(state.hits),
+                               _ptr(state.hot), _ptr(promote), _ptr(demote), int(list_cap), _ptr(counts), _ptr(ws),
+                               ws.numel(), _stream_ptr(stream)))
+    return promote[..., :list_cap], demote[..., :list_cap], counts
 
 
 class StepCall:

@@ -226,3 +226,63 @@ def test_calib_read_validates(H):
     assert lib.hill_calib_read(FAKE, 0, 4, FAKE, None) == INVALID
     assert lib.hill_calib_read(FAKE, 1024, 0, FAKE, None) == INVALID
     assert lib.hill_calib_read(FAKE, 1024, 65537, FAKE, None) == INVALID
+
+
+def _bkp_desc(H, **kw):
+    f = dict(batch=2, rows=3, n_tokens=1000, n_recent=10, capacity=100, stride_b=3 * 1000, stride_r=1000)
+    f.update(kw)
+    return H.BkpDesc(ctypes.sizeof(H.BkpDesc), f["batch"], f["rows"], f["n_tokens"], f["n_recent"],
+                     f["capacity"], f["stride_b"], f["stride_r"])
+
+
+def test_bkp_desc_layout_matches_header(H):
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct hill_bkp_desc \{(.*?)\} hill_bkp_desc;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = re.findall(r"\b(\w+);", body)
+    assert names == [f[0] for f in H.BkpDesc._fields_]
+    assert ctypes.sizeof(H.BkpDesc) == 40
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, INVALID), ("rows", 0, INVALID), ("n_tokens", 0, INVALID), ("n_recent", -1, INVALID),
+    ("capacity", 5, INVALID), ("stride_r", 999, INVALID), ("stride_b", 2999, INVALID),
+    ("n_tokens", (1 << 21) + 1, UNSUPPORTED), ("batch", 30000, UNSUPPORTED),
+])
+def test_bkp_descriptor_errors(H, field, value, code):
+    lib = H.load_library()
+    kw = {field: value}
+    if field == "n_tokens" and value > 1000:
+        kw.update(stride_r=value, stride_b=3 * value)
+    d = _bkp_desc(H, **kw)
+    need = ctypes.c_size_t()
+    assert lib.hill_bkp_workspace_bytes(ctypes.byref(d), ctypes.byref(need)) == code
+    assert lib.hill_bkp_update(ctypes.byref(d), FAKE, 10, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, 1 << 40,
+                               None) == code
+    assert lib.hill_last_error() != b""
+
+
+def test_bkp_arguments_validate(H):
+    lib = H.load_library()
+    d = _bkp_desc(H)
+    need = ctypes.c_size_t()
+    assert lib.hill_bkp_workspace_bytes(ctypes.byref(d), ctypes.byref(need)) == 0 and need.value > 0
+    ok = dict(idx=FAKE, k=10, hits=FAKE, hot=FAKE, pro=FAKE, dem=FAKE, cap=10, cnt=FAKE, ws=FAKE, wsb=need.value)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.hill_bkp_update(ctypes.byref(d), a["idx"], a["k"], a["hits"], a["hot"], a["pro"], a["dem"],
+                                   a["cap"], a["cnt"], a["ws"], a["wsb"], None)
+
+    assert call(k=-1) == INVALID and call(k=1001) == INVALID
+    assert call(idx=None) == INVALID and call(idx=FAKE + 2) == INVALID
+    assert call(hits=None) == INVALID and call(hits=FAKE + 1) == INVALID
+    assert call(hot=None) == INVALID
+    assert call(cap=-1) == INVALID and call(pro=None) == INVALID and call(dem=FAKE + 2) == INVALID
+    assert call(cnt=None) == INVALID and call(cnt=FAKE + 1) == INVALID
+    assert call(ws=None) == INVALID and call(ws=FAKE + 8) == INVALID
+    assert call(wsb=need.value - 1) == WORKSPACE
+    # the workspace size is a pure function of the descriptor
+    need2 = ctypes.c_size_t()
+    lib.hill_bkp_workspace_bytes(ctypes.byref(_bkp_desc(H)), ctypes.byref(need2))
+    assert need2.value == need.value

@@ -1,0 +1,126 @@
+"""GPU parity of the Bidirectional KV Cache Pools pass (Sec. 4.2 BKP,
+hill_bkp_update) against the oracle's bkp_update: integer work, compared bit
+for bit (hit table, pool bytes, promotion and demotion lists, counts) over
+several consecutive steps."""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2602_18750_amd import workloads as W
+from util import bits
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_18750_amd as H
+    H.load_library()
+    yield
+
+
+def H():
+    import paper_2602_18750_amd as H
+    return H
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _padded_state(B, R, n_cap, pad):
+    """BkpState whose rows are padded (strides larger than the row)."""
+    st = H().BkpState(B, R, n_cap + pad, DEV)
+    st.hits = st.hits[:, :, :n_cap]
+    st.hot = st.hot[:, :, :n_cap]
+    return st
+
+
+def _seed_state(st, rng, hits_hi):
+    B, R, n_cap = st.hits.shape
+    h = rng.integers(0, hits_hi + 1, (B, R, n_cap)).astype(np.uint16)
+    o = (rng.random((B, R, n_cap)) < 0.2)
+    st.hits.copy_(torch.from_numpy(h.view(np.int16)))
+    st.hot.copy_(torch.from_numpy(o.astype(np.uint8)))
+    return h, o
+
+
+def _compare(st, promote, demote, counts, ref, list_cap, where):
+    h_ref, o_ref, pr_ref, de_ref = ref
+    torch.cuda.synchronize()
+    h = st.hits.cpu().numpy().view(np.uint16)
+    o = st.hot.cpu().numpy()
+    assert np.array_equal(h, h_ref), where + ": hits"
+    assert np.array_equal(o, o_ref.astype(np.uint8)), where + ": hot"
+    c = counts.cpu().numpy()
+    pr, de = promote.cpu().numpy(), demote.cpu().numpy()
+    B, R = c.shape[0], c.shape[1]
+    for b in range(B):
+        for r in range(R):
+            assert c[b, r, 0] == len(pr_ref[b][r]) and c[b, r, 1] == len(de_ref[b][r]), (where, b, r)
+            m = min(len(pr_ref[b][r]), list_cap)
+            assert np.array_equal(pr[b, r, :m], pr_ref[b][r][:m]), (where, b, r, "promote")
+            m = min(len(de_ref[b][r]), list_cap)
+            assert np.array_equal(de[b, r, :m], de_ref[b][r][:m]), (where, b, r, "demote")
+
+
+BKP_CASES = [
+    # B, R, n_cap, n per step, n_recent, capacity, k, list_cap, pad, hits_hi
+    (1, 1, 4096, [4096] * 6, 409, 1228, 819, None, 0, 0),
+    (2, 3, 1500, [1000, 1100, 1200, 1300, 1400], 50, 300, 150, None, 12, 3),     # growing context, padded rows
+    (1, 1, 777, [777] * 4, 100, 100, 77, None, 0, 2),                            # no frequency slots
+    (1, 2, 300, [300] * 4, 10, 400, 30, None, 4, 1),                             # pool larger than the context
+    (1, 1, 5000, [5000] * 3, 0, 1000, 500, 5, 0, 1),                             # truncated lists
+    (1, 1, 2000, [2000] * 3, 30, 200, 0, None, 0, 6),                            # no selected tokens
+    (1, 8, 32768, [32768] * 3, 3276, 6553, 3276, None, 0, 0),                    # full size, 8 rows
+    (4, 1, 131072, [131072] * 2, 6553, 13107, 6553, None, 0, 1),                 # 128K context, 4 sequences
+]
+
+
+@pytest.mark.parametrize("B,R,n_cap,ns,w,c,k,list_cap,pad,hits_hi", BKP_CASES)
+def test_bkp_matches_oracle(B, R, n_cap, ns, w, c, k, list_cap, pad, hits_hi):
+    say("bkp", B, R, n_cap, ns[0], w, c, k, list_cap, pad)
+    rng = np.random.default_rng(n_cap + 7 * R + k)
+    st = _padded_state(B, R, n_cap, pad)
+    h_ref, o_ref = _seed_state(st, rng, hits_hi)
+    for t, n in enumerate(ns):
+        kk = min(k, n)
+        idx = np.stack([np.stack([np.sort(rng.permutation(n)[:kk]) for _ in range(R)]) for _ in range(B)])
+        idx = idx.astype(np.int32).reshape(B, R, kk)
+        cap = list_cap if list_cap is not None else min(c, n)
+        gidx = torch.from_numpy(idx).to(DEV) if kk else None
+        promote, demote, counts = H().bkp_update(st, gidx, n_tokens=n, n_recent=w, capacity=c, list_cap=cap)
+        ref = O.bkp_update(h_ref, o_ref, idx, n, w, c)
+        _compare(st, promote, demote, counts, ref, cap, "step %d" % t)
+        h_ref, o_ref = ref[0], ref[1]
+
+
+def test_bkp_driven_by_hill_step():
+    """The pool pass fed with hill_step's own index output (token rows,
+    [B, 1, k]) over consecutive decode steps of a Llama-3-8B-shaped layer."""
+    w = W.WORKLOADS[3].replace(n_tokens=8192, steps=6, layers=1)
+    say("bkp from hill_step", w.n_tokens)
+    x = W.make_layer(w, 0)
+    q, kk, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    k_sel = H().budget_k(w.n_tokens, w.budget)
+    s = H().new_importance(w.batch, 1, w.n_tokens, DEV)
+    st = H().BkpState(w.batch, 1, w.n_tokens, DEV)
+    h_ref = np.zeros((w.batch, 1, w.n_tokens), dtype=np.uint16)
+    o_ref = np.zeros((w.batch, 1, w.n_tokens), dtype=bool)
+    n_recent, cap = k_sel // 2, 2 * k_sel
+    moves = []
+    for t in range(w.steps):
+        idx, _ = H().hill_step(q[t], kk, v, s, k_sel)
+        promote, demote, counts = H().bkp_update(st, idx, n_tokens=w.n_tokens, n_recent=n_recent, capacity=cap)
+        ref = O.bkp_update(h_ref, o_ref, idx.cpu().numpy(), w.n_tokens, n_recent, cap)
+        _compare(st, promote, demote, counts, ref, min(cap, w.n_tokens), "step %d" % t)
+        h_ref, o_ref = ref[0], ref[1]
+        moves.append(int(counts[0, 0, 0]))
+    assert moves[0] == cap            # the empty pool fills at the first pass
+    assert all(m < cap for m in moves[1:])

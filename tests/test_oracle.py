@@ -415,3 +415,121 @@ def test_sketch_selection_recall_vs_full_precision(wid, floor):
         for b in range(w.batch):
             ov = len(np.intersect1d(O.topk(S[b:b + 1], k), O.topk(S8[b:b + 1], k))) / k
             assert ov >= floor, (t, b, ov)
+
+
+# ------------------------------------------- BKP hot/cold pools (Sec. 4.2) --
+
+def _bkp(hits, hot, idx, n, w, c):
+    h = np.array(hits, dtype=np.uint16)[None, None]
+    o = np.array(hot, dtype=bool)[None, None]
+    i = np.array(idx, dtype=np.int64).reshape(1, 1, -1)
+    h2, o2, pr, de = O.bkp_update(h, o, i, n, w, c)
+    return h2[0, 0], o2[0, 0], list(pr[0][0]), list(de[0][0])
+
+
+def test_bkp_worked_cases():
+    # N=10, window W=2 (tokens 8, 9), capacity 5: three frequency slots.
+    # Hits after the step: token 2 -> 4, token 4 -> 1; non-recent ranking 0 (5), 2 (4), 3 (3).
+    h, o, pr, de = _bkp([5, 0, 3, 3, 0, 1, 0, 0, 9, 9], [1, 0, 0, 1, 0, 0, 0, 0, 1, 1], [2, 4], 10, 2, 5)
+    assert list(h) == [5, 0, 4, 3, 1, 1, 0, 0, 9, 9]
+    assert list(np.nonzero(o)[0]) == [0, 2, 3, 8, 9] and pr == [2] and de == []
+    # Full pool: token 6 reaches 4 hits and displaces token 3 (3 hits), the lowest-ranked hot one.
+    h, o, pr, de = _bkp([5, 0, 4, 3, 1, 1, 3, 0, 9, 9], [1, 0, 1, 1, 0, 0, 0, 0, 1, 1], [6], 10, 2, 5)
+    assert list(np.nonzero(o)[0]) == [0, 2, 6, 8, 9] and pr == [6] and de == [3]
+    # Equal hits: the incumbent keeps its slot even though the cold token has the lower index.
+    h, o, pr, de = _bkp([0, 2, 2, 0], [0, 0, 1, 0], [1], 4, 0, 1)
+    assert list(h) == [0, 3, 2, 0] and pr == [1] and de == [2]          # 3 > 2: strict, promoted
+    h, o, pr, de = _bkp([0, 2, 3, 0], [0, 0, 1, 0], [1], 4, 0, 1)
+    assert list(h) == [0, 3, 3, 0] and pr == [] and de == []            # tie: incumbent stays
+    # The window moves as the context grows: token 5 enters it, token 3 leaves and must compete.
+    h, o, pr, de = _bkp([1, 0, 0, 0, 9, 0, 7, 7], [1, 0, 0, 1, 1, 0, 0, 0], [], 6, 2, 3)
+    assert list(np.nonzero(o[:6])[0]) == [0, 4, 5] and pr == [5] and de == [3]
+    assert list(h) == [1, 0, 0, 0, 9, 0, 7, 7] and list(o[6:]) == [False, False]   # beyond n untouched
+    # Saturation of the 2-byte table.
+    h, o, pr, de = _bkp([65535, 65534, 0], [0, 0, 0], [0, 1], 3, 0, 2)
+    assert list(h) == [65535, 65535, 0] and pr == [0, 1]
+
+
+def _rank_key(h, old, j):
+    return (int(h[j]), bool(old[j]), -j)   # larger is better
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.integers(1, 40), st.data())
+def test_bkp_invariants(n, data):
+    cap_n = n + data.draw(st.integers(0, 3))
+    w = data.draw(st.integers(0, n + 2))
+    c = data.draw(st.integers(w, n + 5))
+    hits = np.array(data.draw(st.lists(st.integers(0, 65535) | st.integers(0, 4), min_size=cap_n, max_size=cap_n)))
+    old = np.array(data.draw(st.lists(st.booleans(), min_size=cap_n, max_size=cap_n)))
+    k = data.draw(st.integers(0, n))
+    idx = np.sort(np.array(data.draw(st.permutations(list(range(n))))[:k], dtype=np.int64))
+    h2, o2, pr, de = _bkp(hits, old, idx, n, w, c)
+    sel = np.zeros(n, dtype=bool)
+    sel[idx] = True
+    assert np.array_equal(h2[:n], np.minimum(hits[:n] + sel, 65535))
+    assert np.array_equal(h2[n:], hits[n:]) and np.array_equal(o2[n:], old[n:])
+    W_ = min(w, n)
+    assert o2[n - W_:n].all()                                         # recent tokens are hot
+    assert o2[:n].sum() == min(c, n)                                  # the pool is full (or holds all)
+    prs, des = set(pr), set(de)
+    assert not prs & des and all(not old[j] for j in prs) and all(old[j] for j in des)
+    assert set(np.nonzero(o2[:n])[0]) == (set(np.nonzero(old[:n])[0]) | prs) - des
+    assert pr == sorted(pr) and de == sorted(de)
+    rest = range(n - W_)
+    hot_keys = [_rank_key(h2, old, j) for j in rest if o2[j]]
+    cold_keys = [_rank_key(h2, old, j) for j in rest if not o2[j]]
+    if hot_keys and cold_keys:
+        assert min(hot_keys) > max(cold_keys)                         # every hot token outranks every cold one
+
+
+def test_bkp_brute_force_by_enumeration():
+    """On tiny rows, the frequency slots are the one subset of the non-recent
+    tokens whose every member outranks every non-member; enumerate them all."""
+    rng = np.random.default_rng(5)
+    for _ in range(300):
+        n = int(rng.integers(1, 9))
+        w = int(rng.integers(0, n + 1))
+        c = int(rng.integers(w, n + 2))
+        hits = rng.integers(0, 3, n)
+        old = rng.random(n) < 0.5
+        h2, o2, _, _ = _bkp(hits, old, [], n, w, c)
+        rest = list(range(n - w))
+        F = max(0, min(c, n) - w)
+        good = [set(s) for s in itertools.combinations(rest, F)
+                if all(_rank_key(hits, old, a) > _rank_key(hits, old, b) for a in s for b in rest if b not in s)]
+        assert len(good) == 1
+        assert set(j for j in rest if o2[j]) == good[0]
+
+
+def test_bkp_suppresses_ping_pong():
+    """Two tokens selected alternately with one frequency slot: with the
+    incumbent winning ties, the slot changes hands once, not every step."""
+    n, moves = 6, 0
+    hits = np.zeros(n, dtype=np.uint16)
+    hot = np.zeros(n, dtype=bool)
+    for t in range(20):
+        sel = [1] if t % 2 == 0 else [0]
+        hits, hot, pr, de = _bkp(hits, hot, sel, n, 0, 1)
+        moves += len(pr)
+    assert moves == 1 and hot[1] and not hot[0]
+
+
+def test_bkp_recurring_sink_stays_hot():
+    """A token selected at every step (an attention sink, Sec. 4.2 insight
+    two) enters the pool within a few steps and is never demoted, while the
+    other selected tokens change."""
+    rng = np.random.default_rng(1)
+    n, sink = 200, 17
+    hits = np.zeros(n, dtype=np.uint16)
+    hot = np.zeros(n, dtype=bool)
+    first = None
+    for t in range(40):
+        others = rng.choice(np.setdiff1d(np.arange(n - 20), [sink]), 19, replace=False)
+        sel = np.sort(np.append(others, sink))
+        hits, hot, pr, de = _bkp(hits, hot, sel, n, 20, 30)
+        if hot[sink] and first is None:
+            first = t
+        if first is not None:
+            assert hot[sink] and sink not in de
+    assert first is not None and first <= 2
