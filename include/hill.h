@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define HILL_ABI_VERSION 1
+#define HILL_ABI_VERSION 2
 
 typedef enum hill_status {
     HILL_OK = 0,
@@ -101,6 +101,15 @@ typedef struct hill_desc {
     int64_t k_stride_b, k_stride_h, k_stride_n;
     int64_t v_stride_b, v_stride_h, v_stride_n;
     int64_t s_stride_b, s_stride_r;
+    /* Selection pinning (optional; 0 and 0 give the plain top-k).  The first
+     * min(n_sink, n) tokens and the last min(n_recent, n) tokens are always
+     * selected (attention sinks and the recent window, Sec. 4.2's temporal
+     * locality and hit-rate stability); the rest of the budget takes the
+     * largest S among the other tokens, ties to the lower index.  hill_topk,
+     * hill_step and hill_step_sketch require k_sel >= the number of pinned
+     * tokens. */
+    int32_t n_sink;       /* >= 0 */
+    int32_t n_recent;     /* >= 0 */
 } hill_desc;
 
 /* ABI version of the loaded library (HILL_ABI_VERSION it was built with). */

@@ -14,7 +14,8 @@ one definition of the paper (arxiv 2602.18750):
                          (Eq. 1) or raw logits (Sec. 4.4), summed column-wise
                          into the cumulative importance S (Sec. 4.1).
 * :func:`topk`        -- the top-alpha selection (Sec. 3.1, Sec. 4.2 HIE),
-                         brute force by full sort, ties to the lower index.
+                         brute force by full sort, ties to the lower index;
+                         :func:`topk_pinned` keeps sink and recent tokens.
 * :func:`sparse_attn` -- Eq. 1 restricted to the selected tokens (Sec. 4.1,
                          workflow step 6).
 * :func:`step`        -- the three in the workflow's order.
@@ -208,6 +209,29 @@ def topk(S, k: int) -> np.ndarray:
     if rc:
         raise ValueError("hor_topk failed (%d)" % rc)
     return out
+
+
+def topk_pinned(S, k: int, n_sink: int = 0, n_recent: int = 0) -> np.ndarray:
+    """Selection that always keeps pinned tokens: the first min(n_sink, n) and
+    the last min(n_recent, n) of each row (attention sinks and the recent
+    window that Sec. 4.2's locality and hit-rate observations single out);
+    the other k - |pinned| slots take the largest S among the tokens between
+    the two windows (plain top-k there, ties to the lower index).  Returns
+    ascending indices [..., k]."""
+    S = np.asarray(S, dtype=np.float64)
+    n = S.shape[-1]
+    lo = min(int(n_sink), n)
+    hi = max(lo, n - min(int(n_recent), n))
+    pinned = np.concatenate([np.arange(lo), np.arange(hi, n)]).astype(np.int64)
+    free = int(k) - len(pinned)
+    if free < 0:
+        raise ValueError("k smaller than the pinned tokens")
+    rows = S.reshape(-1, n)
+    out = np.empty((rows.shape[0], int(k)), dtype=np.int32)
+    for i, row in enumerate(rows):
+        pick = topk(row[lo:hi][None], free)[0].astype(np.int64) + lo if free else np.empty(0, np.int64)
+        out[i] = np.sort(np.concatenate([pinned, pick]))
+    return out.reshape(S.shape[:-1] + (int(k),))
 
 
 def sparse_attn(q, k, v, idx, dtype, granularity="token", scale=None) -> np.ndarray:

@@ -35,6 +35,8 @@ struct Shape {
     int64_t ld;
     int dtype, mode, gran;
     float scale;
+    int pin_lo, pin_hi;   // tokens outside [pin_lo, pin_hi) are always selected (lo == hi: all of them)
+    int pinned;           // how many tokens that is
 };
 
 // Workspace regions, in this order, each 256-byte aligned:
@@ -128,6 +130,8 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     if ((int64_t)d->n_tokens > (int64_t)kMaxSlots * kSelChunk)
         return fail(HILL_ERR_UNSUPPORTED, "n_tokens %d exceeds the supported %d", d->n_tokens, kMaxSlots * kSelChunk);
     if (!std::isfinite(d->sm_scale)) return fail(HILL_ERR_INVALID_ARG, "sm_scale is not finite");
+    if (d->n_sink < 0 || d->n_recent < 0)
+        return fail(HILL_ERR_INVALID_ARG, "n_sink (%d) and n_recent (%d) must be >= 0", d->n_sink, d->n_recent);
     const int64_t D = d->head_dim;
     const int64_t strides16[] = {d->q_stride_b, d->q_stride_h, d->k_stride_b, d->k_stride_h,
                                  d->k_stride_n, d->v_stride_b, d->v_stride_h, d->v_stride_n};
@@ -160,6 +164,11 @@ hill_status check_desc(const hill_desc* d, Shape* s, bool uses_s = true)
     s->mode = d->score_mode;
     s->gran = d->granularity;
     s->scale = d->sm_scale != 0.0f ? d->sm_scale : 1.0f / std::sqrt((float)d->head_dim);
+    s->pin_lo = d->n_sink < d->n_tokens ? d->n_sink : d->n_tokens;
+    s->pin_hi = d->n_tokens - (d->n_recent < d->n_tokens ? d->n_recent : d->n_tokens);
+    if (s->pin_hi <= s->pin_lo) s->pin_lo = s->pin_hi = 0;   // the windows cover the row: all pinned
+    s->pinned = s->pin_lo + (d->n_tokens - s->pin_hi);
+    if (s->pin_lo == s->pin_hi) s->pinned = d->n_tokens;
     return HILL_OK;
 }
 
@@ -173,6 +182,15 @@ hill_status check_ptr(const void* p, const char* name)
 hill_status check_ksel(const Shape& s, int32_t ksel)
 {
     if (ksel < 1 || ksel > s.n) return fail(HILL_ERR_INVALID_ARG, "k_sel %d not in [1, n_tokens=%d]", ksel, s.n);
+    return HILL_OK;
+}
+
+// Selections must have room for every pinned token.
+hill_status check_pins(const Shape& s, int32_t ksel)
+{
+    if (ksel < s.pinned)
+        return fail(HILL_ERR_INVALID_ARG, "k_sel %d is smaller than the %d pinned tokens (n_sink, n_recent)", ksel,
+                    s.pinned);
     return HILL_OK;
 }
 
@@ -287,6 +305,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     u.ld = s.ld;
     u.s2 = a.s2;
     u.hist = hist;
+    u.pin_lo = s.pin_lo;
+    u.pin_hi = s.pin_hi;
 
     if (s.mode == HILL_SCORE_ATTN) {
         a.logits = at<float>(ws, L.logits);
@@ -306,7 +326,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         // one row per KV head (or a single KV head): the scan adds straight into S
         HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawS, ncu, st, scan));
         HIP_TRY(mark(ev.score_stop, st));
-        if (with_hist) HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, hist, st));
+        if (with_hist)
+            HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, s.pin_lo, s.pin_hi, hist, st));
     } else {
         a.logits = at<float>(ws, L.logits);
         HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawGroups, ncu, st, scan));
@@ -333,6 +354,8 @@ RefineArgs refine_args(const hill_desc* d, const Shape& s, const Layout& L, cons
     r.state = at<uint4>(ws, L.state);
     r.sel_list = at<int32_t>(ws, L.sel_list);
     r.sel_n = at<uint32_t>(ws, L.sel_n);
+    r.pin_lo = s.pin_lo;
+    r.pin_hi = s.pin_hi;
     return r;
 }
 
@@ -342,7 +365,8 @@ hill_status run_select(const hill_desc* d, const Shape& s, const Layout& L, cons
 {
     const RefineArgs r = refine_args(d, s, L, sacc, ksel, ws);
     HIP_TRY(launch_fill_zero(at<uint32_t>(ws, L.zero), L.zero_words, st));
-    HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, at<uint32_t>(ws, L.hist1), st));
+    HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, s.pin_lo, s.pin_hi,
+                             at<uint32_t>(ws, L.hist1), st));
     HIP_TRY(launch_topk_refine(r, s.B * s.R, st));
     HIP_TRY(launch_topk_emit_indices(r, s.B * s.R, idx, val, st));
     return HILL_OK;
@@ -399,6 +423,7 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     Shape s;
     HILL_TRY(check_desc(d, &s));
     HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_pins(s, k_sel));
     HILL_TRY(check_ptr(q, "q"));
     HILL_TRY(check_ptr(k, "k"));
     HILL_TRY(check_ptr(v, "v"));
@@ -614,7 +639,9 @@ hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t 
         r.sel_list = at<int32_t>(ws, L.sel_list);
         r.sel_n = at<uint32_t>(ws, L.sel_n);
         HIP_TRY(launch_fill_zero(at<uint32_t>(ws, L.zero), L.zero_words, st));
-        HIP_TRY(launch_topk_hist(a.v, r.s_sb, r.s_sr, d->batch, d->rows, n, at<uint32_t>(ws, L.hist1), st));
+        r.pin_lo = 0;
+        r.pin_hi = n;
+        HIP_TRY(launch_topk_hist(a.v, r.s_sb, r.s_sr, d->batch, d->rows, n, 0, n, at<uint32_t>(ws, L.hist1), st));
         HIP_TRY(launch_topk_refine(r, rows, st));
         HIP_TRY(launch_topk_emit_indices(r, rows, at<int32_t>(ws, L.flist), nullptr, st));
         HIP_TRY(launch_bkp_mark(a, rows, st));
@@ -654,6 +681,7 @@ hill_status hill_topk(const hill_desc* d, const float* s_acc, int32_t k_sel, int
     Shape s;
     HILL_TRY(check_desc(d, &s));
     HILL_TRY(check_ksel(s, k_sel));
+    HILL_TRY(check_pins(s, k_sel));
     HILL_TRY(check_ptr(s_acc, "s"));
     if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
     if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");

@@ -318,4 +318,12 @@ __device__ __forceinline__ uint32_t order_key(float f)
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Selection key of token j: pinned tokens (outside [lo, hi), with 0 <= lo <=
+// hi; lo == hi pins all) take the largest key, which no float reaches (+inf
+// maps to 0xFF800000, NaN to 0).
+__device__ __forceinline__ uint32_t select_key(float f, int j, int lo, int hi)
+{
+    return (uint32_t)(j - lo) >= (uint32_t)(hi - lo) ? 0xFFFFFFFFu : order_key(f);
+}
+
 }  // namespace hill

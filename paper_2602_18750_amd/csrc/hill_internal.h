@@ -67,6 +67,7 @@ struct UpdateArgs {
     int B, Hq, Hkv, G, R, n;
     float s2;
     uint32_t* hist;          // nullable: [B*R, kHistRow] first-digit counts (fine, coarse)
+    int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) count with the largest key (lo == hi: all)
 };
 
 struct AttnArgs {
@@ -98,6 +99,7 @@ struct RefineArgs {
     uint4* state;            // [rows] (first-digit bin, keys still needed from it, keys in it, 0)
     int32_t* sel_list;       // [rows, n] each chunk's selected tokens in order, chunk c at c*kSelChunk
     uint32_t* sel_n;         // [rows, nchunks]
+    int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) are always selected (lo == hi: all)
 };
 
 // Splits of the selected set per (sequence, KV head) for the attention pass.
@@ -171,8 +173,8 @@ inline bool update_reduces_stats(int nheads_per_row, int npart)
 }
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
-hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n,
-                            uint32_t* hist, hipStream_t st, Stamp ts = {});
+hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n, int pin_lo,
+                            int pin_hi, uint32_t* hist, hipStream_t st, Stamp ts = {});
 hipError_t launch_topk_refine(const RefineArgs& a, int rows, hipStream_t st, Stamp ts = {});
 // Selects per chunk and writes the ordered indices (and values, if val).
 hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx, float* val, hipStream_t st,

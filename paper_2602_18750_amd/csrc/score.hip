@@ -608,7 +608,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
-        if (do_hist) count_key(kh, order_key(s_new));
+        if (do_hist) count_key(kh, select_key(s_new, j, a.pin_lo, a.pin_hi));
     }
     if (do_hist) {
         __syncthreads();
@@ -654,7 +654,7 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
-        if (do_hist) count_key(kh, order_key(s_new));
+        if (do_hist) count_key(kh, select_key(s_new, j, a.pin_lo, a.pin_hi));
     }
     if (do_hist) {
         __syncthreads();

@@ -47,7 +47,8 @@ static_assert(kPerThread == 2, "load_keys reads float2");
 static_assert(kSelChunk == 16 * 32, "16 row groups of 32 tokens");
 
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict__ s, int64_t s_sb, int64_t s_sr,
-                                                        int R, int n, uint32_t* __restrict__ hist)
+                                                        int R, int n, int pin_lo, int pin_hi,
+                                                        uint32_t* __restrict__ hist)
 {
     __shared__ uint32_t lds_hist[kHistRow];
     __shared__ uint32_t list[kHistRow];
@@ -63,7 +64,7 @@ __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict_
     for (int i = 0; i < kPer; ++i) {
         const int j = blockIdx.x * kHistChunk + i * 256 + threadIdx.x;
         if (j < n) {
-            const uint32_t kk = order_key(srow[j]);
+            const uint32_t kk = select_key(srow[j], j, pin_lo, pin_hi);
             hist_add(lds_hist, list, &nlist, kk >> (32 - kHistBits));
             hist_add(lds_hist, list, &nlist, kHistBins + (kk >> 26));
         }
@@ -78,21 +79,22 @@ __device__ __forceinline__ const float* row_ptr(const RefineArgs& a, int row)
     return a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
 }
 
-// Keys of this thread's 2 consecutive tokens of chunk c (row bases 16-byte aligned).
-__device__ __forceinline__ void load_keys(const float* srow, int c, int n, uint32_t (&key)[kPerThread],
-                                          bool (&ok)[kPerThread])
+// Selection keys of this thread's 2 consecutive tokens of chunk c (row bases
+// 16-byte aligned); tokens outside [lo, hi) are pinned.
+__device__ __forceinline__ void load_keys(const float* srow, int c, int n, int lo, int hi,
+                                          uint32_t (&key)[kPerThread], bool (&ok)[kPerThread])
 {
     const int j = c * kSelChunk + threadIdx.x * kPerThread;
     if (j + kPerThread <= n) {
         const float2 x = *reinterpret_cast<const float2*>(srow + j);
-        key[0] = order_key(x.x);
-        key[1] = order_key(x.y);
+        key[0] = select_key(x.x, j, lo, hi);
+        key[1] = select_key(x.y, j + 1, lo, hi);
         ok[0] = ok[1] = true;
     } else {
 #pragma unroll
         for (int e = 0; e < kPerThread; ++e) {
             ok[e] = j + e < n;
-            key[e] = ok[e] ? order_key(srow[j + e]) : 0u;
+            key[e] = ok[e] ? select_key(srow[j + e], j + e, lo, hi) : 0u;
         }
     }
 }
@@ -189,7 +191,7 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     // the chunk's keys and the row's first-digit histogram are loaded together
     uint32_t key[kPerThread];
     bool ok[kPerThread];
-    load_keys(srow, c, a.n, key, ok);
+    load_keys(srow, c, a.n, a.pin_lo, a.pin_hi, key, ok);
     DigitHist h1;
     load_digit_hist(a.hist1 + (int64_t)row * kHistRow, h1);
     for (int i = tid; i < kHistRow; i += kThreads) hist[i] = 0u;
@@ -273,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     if constexpr (ATTN) load_queries<GC>(at, b, g, 0, qv);
     uint32_t key[kPerThread];
     bool ok[kPerThread];
-    load_keys(row_ptr(r, row), c, r.n, key, ok);
+    load_keys(row_ptr(r, row), c, r.n, r.pin_lo, r.pin_hi, key, ok);
     const uint4 s1 = r.state[row];
     DigitHist h2;
     load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
@@ -443,11 +445,12 @@ void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, S
 
 }  // namespace
 
-hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n, uint32_t* hist,
-                            hipStream_t st, Stamp ts)
+hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n, int pin_lo, int pin_hi,
+                            uint32_t* hist, hipStream_t st, Stamp ts)
 {
     dim3 grid((n + kHistChunk - 1) / kHistChunk, B * R);
-    hipExtLaunchKernelGGL(topk_hist_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, s, s_sb, s_sr, R, n, hist);
+    hipExtLaunchKernelGGL(topk_hist_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, s, s_sb, s_sr, R, n, pin_lo,
+                          pin_hi, hist);
     return hipGetLastError();
 }
 

@@ -35,6 +35,7 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
+ABI_VERSION = 2   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
@@ -69,6 +70,8 @@ class HillDesc(ctypes.Structure):
         ("v_stride_n", ctypes.c_int64),
         ("s_stride_b", ctypes.c_int64),
         ("s_stride_r", ctypes.c_int64),
+        ("n_sink", ctypes.c_int32),
+        ("n_recent", ctypes.c_int32),
     ]
 
 
@@ -134,6 +137,9 @@ def load_library(path: str = LIB_PATH):
         lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
         lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
         lib.hill_bkp_update.restype = ctypes.c_int
+        if lib.hill_abi_version() != ABI_VERSION:
+            raise RuntimeError("libhill.so has ABI version %d, this binding needs %d; rebuild it"
+                               % (lib.hill_abi_version(), ABI_VERSION))
         _lib = lib
         return lib
 
@@ -151,8 +157,11 @@ def budget_k(n: int, budget: float) -> int:
 def make_desc(q: Optional[torch.Tensor], k: Optional[torch.Tensor], v: Optional[torch.Tensor],
               s: Optional[torch.Tensor], *, mode: str = "attn", granularity: str = "token",
               n_tokens: Optional[int] = None, sm_scale: float = 0.0,
-              shape: Optional[Tuple[int, int, int, int]] = None, dtype=None) -> HillDesc:
-    """Descriptor from tensors.  ``shape`` = (B, Hq, Hkv, D) stands in when q/k are absent."""
+              shape: Optional[Tuple[int, int, int, int]] = None, dtype=None, n_sink: int = 0,
+              n_recent: int = 0) -> HillDesc:
+    """Descriptor from tensors.  ``shape`` = (B, Hq, Hkv, D) stands in when q/k are absent.
+    ``n_sink`` / ``n_recent``: tokens at the start / end of the context that
+    every selection keeps."""
     d = HillDesc()
     d.struct_size = ctypes.sizeof(HillDesc)
     if q is not None:
@@ -171,6 +180,7 @@ def make_desc(q: Optional[torch.Tensor], k: Optional[torch.Tensor], v: Optional[
     d.score_mode = MODES[mode]
     d.granularity = GRANS[granularity]
     d.sm_scale = float(sm_scale)
+    d.n_sink, d.n_recent = int(n_sink), int(n_recent)
     if q is not None:
         d.q_stride_b, d.q_stride_h = q.stride(0), q.stride(1)
         _require_unit_last(q, "q")
@@ -306,14 +316,15 @@ def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_s
 
 
 def hill_topk(s, k_sel, *, granularity="token", n_tokens=None, n_kv_heads=None, with_values=False,
-              idx_out=None, val_out=None, ws=None, stream=None):
-    """Indices [B, R, k_sel] (int32, ascending) of the k_sel largest S per row."""
+              idx_out=None, val_out=None, ws=None, stream=None, n_sink=0, n_recent=0):
+    """Indices [B, R, k_sel] (int32, ascending) of the k_sel largest S per row
+    (the first n_sink and last n_recent tokens always among them)."""
     lib = load_library()
     _device_check(s)
     B, R, _ = s.shape
     hkv = n_kv_heads if n_kv_heads is not None else R
     desc = make_desc(None, None, None, s, granularity=granularity, n_tokens=n_tokens,
-                     shape=(B, hkv, hkv, 128), dtype=torch.float16)
+                     shape=(B, hkv, hkv, 128), dtype=torch.float16, n_sink=n_sink, n_recent=n_recent)
     if idx_out is None:
         idx_out = torch.empty((B, R, k_sel), dtype=torch.int32, device=s.device)
     if with_values and val_out is None:
@@ -345,14 +356,16 @@ def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_sca
 
 def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
               sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None,
-              sketch: Optional[Sketch] = None):
+              sketch: Optional[Sketch] = None, n_sink=0, n_recent=0):
     """One decode step: S update, top-k on the new S, attention.  Returns (idx, out).
+    ``n_sink`` / ``n_recent``: pinned tokens every selection keeps.
 
     ``events``: optional HillStepEvents; then hill_step_profiled records them.
     ``sketch``: score on the int8 sketch (hill_step_sketch)."""
     lib = load_library()
     _device_check(q, k, v, s)
-    desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale)
+    desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale,
+                     n_sink=n_sink, n_recent=n_recent)
     if k_sel is None:
         if budget is None:
             raise ValueError("give k_sel or budget")
@@ -440,11 +453,11 @@ class StepCall:
     repeatedly on the same buffers (only the query pointer changes per call)."""
 
     def __init__(self, q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
-                 ws=None, stream=None, sketch: Optional[Sketch] = None):
+                 ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0):
         lib = load_library()
         _device_check(q, k, v, s)
         self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
-                              sm_scale=sm_scale)
+                              sm_scale=sm_scale, n_sink=n_sink, n_recent=n_recent)
         B, R = s.shape[0], s.shape[1]
         self.k_sel = int(k_sel)
         self.idx = torch.empty((B, R, self.k_sel), dtype=torch.int32, device=s.device)

@@ -47,16 +47,18 @@ def test_library_exports_every_declared_symbol(H):
 
 def test_abi_version_and_status_strings(H):
     lib = H.load_library()
-    assert lib.hill_abi_version() == 1
+    want = int(re.search(r"#define HILL_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
+    assert lib.hill_abi_version() == want == H.hill.ABI_VERSION
     assert lib.hill_status_str(0) == b"HILL_OK"
     assert lib.hill_status_str(3) == b"HILL_ERR_WORKSPACE"
     assert lib.hill_status_str(99) == b"HILL_ERR_UNKNOWN"
 
 
 def test_desc_layout_matches_header(H):
-    # 10 x 4-byte fields, then 10 x int64 strides
-    assert ctypes.sizeof(H.HillDesc) == 40 + 80
+    # 10 x 4-byte fields, then 10 x int64 strides, then the two pinning counts
+    assert ctypes.sizeof(H.HillDesc) == 40 + 80 + 8
     assert H.HillDesc.q_stride_b.offset == 40
+    assert H.HillDesc.n_sink.offset == 120 and H.HillDesc.n_recent.offset == 124
 
 
 FAKE = 0x10000          # 16-byte aligned, never dereferenced
@@ -286,3 +288,32 @@ def test_bkp_arguments_validate(H):
     need2 = ctypes.c_size_t()
     lib.hill_bkp_workspace_bytes(ctypes.byref(_bkp_desc(H)), ctypes.byref(need2))
     assert need2.value == need.value
+
+
+def test_desc_field_names_match_header(H):
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct hill_desc \{(.*?)\} hill_desc;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = []
+    for decl in body.split(";"):
+        decl = decl.strip()
+        if decl:
+            names += [x.strip() for x in decl.split(None, 1)[1].split(",")]
+    assert names == [f[0] for f in H.HillDesc._fields_]
+
+
+def test_pinned_tokens_need_room_in_the_budget(H):
+    lib = H.load_library()
+    d = base_desc(H)                     # n = 1000
+    need = ws_need(H, d, 10)
+    d.n_sink = -1
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 10, FAKE, None, FAKE, need, None) == INVALID
+    d.n_sink, d.n_recent = 4, 7          # 11 pinned tokens
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 10, FAKE, None, FAKE, need, None) == INVALID
+    assert b"pinned" in lib.hill_last_error()
+    assert lib.hill_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, need, None) == INVALID
+    d.n_sink, d.n_recent = 600, 600      # the windows overlap: all 1000 tokens are pinned
+    assert lib.hill_topk(ctypes.byref(d), FAKE, 999, FAKE, None, FAKE, 1 << 40, None) == INVALID
+    # attention over a given list does not select: pins do not constrain it
+    d.n_sink, d.n_recent = 4, 7
+    assert lib.hill_gather_attn(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, 16, None) == WORKSPACE

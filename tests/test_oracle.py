@@ -533,3 +533,39 @@ def test_bkp_recurring_sink_stays_hot():
         if first is not None:
             assert hot[sink] and sink not in de
     assert first is not None and first <= 2
+
+
+# ------------------------------------------------- pinned selection (sinks, recent) --
+
+def test_pinned_selection_without_pins_is_the_plain_top_k():
+    rng = np.random.default_rng(3)
+    S = rng.integers(0, 5, (4, 300)).astype(np.float64)
+    assert np.array_equal(O.topk_pinned(S, 40), O.topk(S, 40))
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.integers(1, 60), st.data())
+def test_pinned_selection_by_brute_force(n, data):
+    sink = data.draw(st.integers(0, n + 2))
+    recent = data.draw(st.integers(0, n + 2))
+    npin = min(n, min(sink, n) + min(recent, n))
+    k = data.draw(st.integers(max(1, npin), n)) if npin <= n else n
+    S = np.array(data.draw(st.lists(st.integers(-3, 3), min_size=n, max_size=n)), dtype=np.float64) / 2
+    got = O.topk_pinned(S[None], k, sink, recent)[0]
+    assert len(got) == k and np.all(np.diff(got) > 0)
+    pinned = set(range(min(sink, n))) | set(range(n - min(recent, n), n))
+    assert pinned <= set(got.tolist())
+    free = [j for j in range(n) if j not in pinned]
+    # the free slots hold the largest S among the unpinned tokens, ties to the lower index
+    want = sorted(free, key=lambda j: (-S[j], j))[:k - len(pinned)]
+    assert set(got.tolist()) - pinned == set(want)
+
+
+def test_pinned_selection_cases():
+    S = np.array([[9.0, 1, 8, 7, 0, 6, 5, 4]])
+    assert list(O.topk_pinned(S, 4, 1, 2)[0]) == [0, 2, 6, 7]     # sink 0, recent 6-7, best free: 2 (8)
+    assert list(O.topk_pinned(S, 3, 1, 2)[0]) == [0, 6, 7]        # k equals the pinned count
+    assert list(O.topk_pinned(S, 8, 6, 6)[0]) == list(range(8))   # overlapping windows pin everything
+    assert list(O.topk_pinned(S, 3, 0, 1)[0]) == [0, 2, 7]
+    with pytest.raises(ValueError):
+        O.topk_pinned(S, 2, 1, 2)
