@@ -286,6 +286,8 @@ def run_bench(args):
         "layer_step_us_probe": round(mean(total) * 1e3, 3),
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
     }
+    if not args.no_bkp:
+        res["bkp"] = bench_bkp(args, w, calls, nl_run, T, qptrs, stream)
     if not args.no_sketch:
         res["sketch"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_cpu_baseline:
@@ -294,6 +296,42 @@ def run_bench(args):
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
+
+
+def bench_bkp(args, w, calls, nl_run, T, qptrs, stream):
+    """The Bidirectional KV Cache Pools pass (Sec. 4.2 BKP) after each
+    layer's decode step, on that step's selected set: recent window = k
+    tokens (alpha * N), hot pool = 2k tokens (the window plus the top-alpha
+    by hit count).  Timed per pass with events around one probe layer per
+    step; the decode steps themselves run untimed in between."""
+    import torch
+    import paper_2602_18750_amd as H
+
+    dev = torch.device("cuda:0")
+    k = w.k_sel
+    states = [H.BkpState(w.batch, 1, w.n_tokens, dev) for _ in range(nl_run)]
+    bkps = [H.BkpCall(st, k, n_tokens=w.n_tokens, n_recent=k, capacity=2 * k, stream=stream) for st in states]
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    for i in range(args.steps):
+        t = i % T
+        probe = i % nl_run
+        for L in range(nl_run):
+            calls[L](qptrs[L][t])
+            if L == probe:
+                evs[i][0].record(stream)
+            bkps[L](calls[L].idx.data_ptr())
+            if L == probe:
+                evs[i][1].record(stream)
+    torch.cuda.synchronize()
+    us = sorted(a.elapsed_time(b) * 1e3 for a, b in evs[1:])   # the first pass fills the empty pools
+    last = bkps[(args.steps - 1) % nl_run].counts[0, 0].tolist()
+    del bkps, states
+    return {
+        "us_per_pass_median": round(us[len(us) // 2], 3),
+        "us_per_pass_mean": round(sum(us) / len(us), 3),
+        "n_recent": k, "capacity": 2 * k, "launches_per_pass": 6,
+        "last_pass_promotions": last[0], "last_pass_demotions": last[1],
+    }
 
 
 def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
@@ -569,6 +607,7 @@ def main():
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sketch", action="store_true", help="skip the int8-sketch variant of the step")
+    ap.add_argument("--no-bkp", action="store_true", help="skip timing the hot/cold pool pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")

@@ -518,7 +518,7 @@ hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8
 // ---------------------------------------------------------------- BKP pools --
 
 struct BkpLayout {
-    size_t v, flist, zero, hist1, hist2, cand_key, cand_n, state, sel_list, sel_n, end;
+    size_t v, zero, hist1, hist2, cand_key, cand_n, state, sel_list, sel_n, moves, end;
     int64_t zero_words, ld;
     int nchunks;
 };
@@ -533,8 +533,6 @@ BkpLayout bkp_layout(const hill_bkp_desc* d)
     size_t off = 0;
     L.v = off;
     off += align256(rows * (size_t)L.ld * sizeof(float));
-    L.flist = off;
-    off += align256(rows * n * sizeof(int32_t));
     L.zero = L.hist1 = off;
     L.hist2 = L.hist1 + rows * kHistRow * sizeof(uint32_t);
     const size_t zero_end = L.hist2 + rows * kHistRow * sizeof(uint32_t);
@@ -550,6 +548,8 @@ BkpLayout bkp_layout(const hill_bkp_desc* d)
     off += align256(rows * n * sizeof(int32_t));
     L.sel_n = off;
     off += align256(rows * L.nchunks * sizeof(uint32_t));
+    L.moves = off;
+    off += align256(rows * L.nchunks * sizeof(uint2));
     L.end = off;
     return L;
 }
@@ -613,16 +613,24 @@ hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t 
     a.n = n;
     a.w = d->n_recent < n ? d->n_recent : n;
     a.f = (d->capacity < n ? d->capacity : n) - a.w;
+    a.pos_shift = 0;
+    while (((n - 1) >> a.pos_shift) >= 128) ++a.pos_shift;
     a.v = at<float>(ws, L.v);
     a.ld = L.ld;
-    a.flist = at<int32_t>(ws, L.flist);
+    a.zero = at<uint32_t>(ws, L.zero);
+    a.zero_words = L.zero_words;
+    a.hist1 = at<uint32_t>(ws, L.hist1);
+    a.sel_list = at<int32_t>(ws, L.sel_list);
+    a.sel_n = at<uint32_t>(ws, L.sel_n);
+    a.nchunks = L.nchunks;
+    a.chunk_moves = at<uint2>(ws, L.moves);
     a.promote = promote;
     a.demote = demote;
     a.list_cap = list_cap;
     a.counts = counts;
     HIP_TRY(launch_bkp_hits(a, rows, st));
-    HIP_TRY(launch_bkp_rank(a, rows, st));
     if (a.f > 0) {   // frequency slots: the exact top-f of the rank values, ties to the lower index
+        HIP_TRY(launch_bkp_rank(a, rows, st));
         RefineArgs r{};
         r.s = a.v;
         r.s_sb = (int64_t)d->rows * L.ld;
@@ -638,13 +646,10 @@ hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t 
         r.state = at<uint4>(ws, L.state);
         r.sel_list = at<int32_t>(ws, L.sel_list);
         r.sel_n = at<uint32_t>(ws, L.sel_n);
-        HIP_TRY(launch_fill_zero(at<uint32_t>(ws, L.zero), L.zero_words, st));
         r.pin_lo = 0;
         r.pin_hi = n;
-        HIP_TRY(launch_topk_hist(a.v, r.s_sb, r.s_sr, d->batch, d->rows, n, 0, n, at<uint32_t>(ws, L.hist1), st));
         HIP_TRY(launch_topk_refine(r, rows, st));
-        HIP_TRY(launch_topk_emit_indices(r, rows, at<int32_t>(ws, L.flist), nullptr, st));
-        HIP_TRY(launch_bkp_mark(a, rows, st));
+        HIP_TRY(launch_topk_emit_lists(r, rows, st));
     }
     HIP_TRY(launch_bkp_lists(a, rows, st));
     return HILL_OK;

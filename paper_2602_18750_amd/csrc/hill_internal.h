@@ -141,24 +141,30 @@ hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
 hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
 // Bidirectional KV cache pools (bkp.hip).
 struct BkpArgs {
-    const int32_t* idx;   // [rows, k]
+    const int32_t* idx;       // [rows, k]
     int k;
-    uint16_t* hits;       // [B, R, >= n] strided
-    uint8_t* hot;         // same strides as hits
+    uint16_t* hits;           // [B, R, >= n] strided
+    uint8_t* hot;             // same strides as hits
     int64_t sb, sr;
-    int R, n, w, f;       // w = min(n_recent, n); f = frequency slots
-    float* v;             // [rows, ld] rank values for the selection
+    int R, n, w, f;           // w = min(n_recent, n); f = frequency slots
+    int pos_shift;            // (n - 1) >> pos_shift < 128: the rank value's position bins
+    float* v;                 // [rows, ld] rank values for the selection
     int64_t ld;
-    const int32_t* flist; // [rows, f] frequency-hot tokens
-    int32_t* promote;     // [rows, list_cap]
+    uint32_t* zero;           // histogram region cleared by bkp_hits
+    int64_t zero_words;
+    uint32_t* hist1;          // [rows, kHistRow] first-digit counts of v
+    const int32_t* sel_list;  // [rows, n] chosen tokens per 512-token chunk (topk emit)
+    const uint32_t* sel_n;    // [rows, nchunks]
+    int nchunks;
+    uint2* chunk_moves;       // [rows, nchunks] (promotions, demotions) per chunk
+    int32_t* promote;         // [rows, list_cap]
     int32_t* demote;
     int list_cap;
-    int32_t* counts;      // [rows, 2]
+    int32_t* counts;          // [rows, 2]
     __host__ __device__ int64_t off(int row) const { return (int64_t)(row / R) * sb + (int64_t)(row % R) * sr; }
 };
 hipError_t launch_bkp_hits(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_bkp_rank(const BkpArgs& a, int rows, hipStream_t st);
-hipError_t launch_bkp_mark(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_bkp_lists(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_calib_read(const void* p, int64_t bytes, int grid, uint32_t* sink, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
@@ -179,6 +185,8 @@ hipError_t launch_topk_refine(const RefineArgs& a, int rows, hipStream_t st, Sta
 // Selects per chunk and writes the ordered indices (and values, if val).
 hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx, float* val, hipStream_t st,
                                     Stamp ts = {});
+// Selects per chunk only: chunk c's tokens in order in r.sel_list, their count in r.sel_n.
+hipError_t launch_topk_emit_lists(const RefineArgs& r, int rows, hipStream_t st);
 // Selects per chunk and attends over each chunk's selected tokens: one
 // partial per (query head, chunk) in at.part_o / at.part_ml ([B*Hq, nchunks]
 // slots).  launch_merge_write then merges the partials into at.out and

@@ -470,6 +470,12 @@ hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx,
     return hipGetLastError();
 }
 
+hipError_t launch_topk_emit_lists(const RefineArgs& r, int rows, hipStream_t st)
+{
+    hipLaunchKernelGGL((topk_emit_kernel<0, 1, false>), dim3(r.nchunks, rows), dim3(kThreads), 0, st, r, AttnArgs{});
+    return hipGetLastError();
+}
+
 hipError_t launch_topk_emit_attn(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
 {
     const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;

@@ -448,6 +448,36 @@ def bkp_update(state: BkpState, idx, *, n_tokens: int, n_recent: int, capacity: 
     return promote[..., :list_cap], demote[..., :list_cap], counts
 
 
+class BkpCall:
+    """hill_bkp_update with its buffers allocated and arguments marshalled
+    once, for per-step loops (only the index pointer changes per call)."""
+
+    def __init__(self, state: BkpState, k_sel: int, *, n_tokens: int, n_recent: int, capacity: int,
+                 list_cap=None, stream=None):
+        lib = load_library()
+        _device_check(state.hits, state.hot)
+        B, R, _ = state.hits.shape
+        self.desc = bkp_desc(state, n_tokens, n_recent, capacity)
+        self.list_cap = min(int(capacity), int(n_tokens)) if list_cap is None else int(list_cap)
+        dev = state.hits.device
+        need = ctypes.c_size_t(0)
+        _check(lib.hill_bkp_workspace_bytes(ctypes.byref(self.desc), ctypes.byref(need)))
+        self.ws = torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=dev)
+        self.promote = torch.empty((B, R, max(self.list_cap, 1)), dtype=torch.int32, device=dev)
+        self.demote = torch.empty_like(self.promote)
+        self.counts = torch.empty((B, R, 2), dtype=torch.int32, device=dev)
+        P = ctypes.c_void_p
+        self._fn = lib.hill_bkp_update
+        self._k = ctypes.c_int32(int(k_sel))
+        self._post = (P(state.hits.data_ptr()), P(state.hot.data_ptr()), P(self.promote.data_ptr()),
+                      P(self.demote.data_ptr()), ctypes.c_int32(self.list_cap), P(self.counts.data_ptr()),
+                      P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        self._keep = state
+
+    def __call__(self, idx_ptr: int):
+        _check(self._fn(ctypes.byref(self.desc), ctypes.c_void_p(idx_ptr), self._k, *self._post))
+
+
 class StepCall:
     """hill_step with its arguments marshalled once, for hot loops that call it
     repeatedly on the same buffers (only the query pointer changes per call)."""

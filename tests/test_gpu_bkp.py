@@ -124,3 +124,17 @@ def test_bkp_driven_by_hill_step():
         moves.append(int(counts[0, 0, 0]))
     assert moves[0] == cap            # the empty pool fills at the first pass
     assert all(m < cap for m in moves[1:])
+
+
+def test_bkp_reads_bit_zero_and_writes_zero_or_one():
+    B, R, n, k = 1, 2, 3000, 300
+    rng = np.random.default_rng(11)
+    st = H().BkpState(B, R, n, DEV)
+    raw = rng.choice(np.array([0, 1, 2, 3, 254, 255], dtype=np.uint8), (B, R, n))
+    st.hot.copy_(torch.from_numpy(raw))
+    h0 = np.zeros((B, R, n), dtype=np.uint16)
+    idx = np.stack([np.sort(rng.permutation(n)[:k]) for _ in range(R)]).astype(np.int32).reshape(B, R, k)
+    promote, demote, counts = H().bkp_update(st, torch.from_numpy(idx).to(DEV), n_tokens=n, n_recent=30,
+                                             capacity=500)
+    ref = O.bkp_update(h0, (raw & 1).astype(bool), idx, n, 30, 500)
+    _compare(st, promote, demote, counts, ref, 500, "stray bits")
