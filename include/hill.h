@@ -258,6 +258,33 @@ hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t 
                             uint8_t* hot, int32_t* promote, int32_t* demote, int32_t list_cap, int32_t* counts,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* Adaptive Prefetch-based Pipeline (Sec. 4.3, Eqs. 2-4): the split of the KV
+ * bytes M scored per step between a hot pool (subscript c) and a cold pool
+ * (subscript s) whose scorers run in parallel, so that both paths, scoring
+ * plus moving the retained fraction, take the same time:
+ *     T_c = M_c / f_c + alpha_c * M_c / b_c  =  M_s / f_s + alpha_s * M_s / b_s = T_s,
+ * M_c + M_s = M, M_c <= m0.  With alpha_c = alpha_s = alpha this is Eq. 2 and
+ * beta = M_c / M_s is Eq. 4; separate values are the skew correction the
+ * paper applies to alpha (the hot pool holds more of the retained tokens).
+ * Host-only; no GPU work.  All rates in bytes per second, sizes in bytes. */
+typedef struct hill_app_params {
+    double f_c, f_s;            /* scoring throughput of each pool's evaluator, > 0 */
+    double b_c, b_s;            /* bandwidth moving each pool's retained KV to the attention device, > 0 */
+    double alpha_c, alpha_s;    /* retained fraction of each pool, in [0, 1] */
+    double m;                   /* M > 0: KV bytes scored per step */
+    double m0;                  /* bound on M_c (> 0), or <= 0 for none */
+} hill_app_params;
+
+typedef struct hill_app_plan {
+    double beta;                /* M_c / M_s (infinite when M_s == 0) */
+    double m_c, m_s;            /* the split */
+    double t_c, t_s;            /* the two path times of Eq. 2, seconds */
+    int32_t capped;             /* 1 if M_c was limited to m0 */
+} hill_app_plan;
+
+/* Fills *plan; HILL_ERR_INVALID_ARG for non-finite or out-of-range inputs. */
+hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan);
+
 /* Roofline calibration (measurement aid, computes nothing of the method):
  * one launch of `grid` workgroups that reads `bytes` bytes of the device
  * buffer `buf` once, each workgroup a contiguous share, with 16-byte

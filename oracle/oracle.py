@@ -25,6 +25,9 @@ one definition of the paper (arxiv 2602.18750):
 * :func:`bkp_update`  -- the hit-rate table and the hot/cold pool policy of
                          the Bidirectional KV Cache Pools (Sec. 4.2 HKM,
                          BKP (1)-(3)), plain numpy on integers.
+* :func:`app_split`   -- the Adaptive Prefetch-based Pipeline's capacity
+                         split (Sec. 4.3): Eq. 2's balance solved by
+                         bisection, with the host-memory bound Eq. 3.
 
 16-bit inputs are passed as ``numpy.uint16`` bit patterns; the oracle decodes
 them itself (:func:`decode16`).
@@ -339,3 +342,33 @@ def bkp_update(hits, hot, idx, n_tokens: int, n_recent: int, capacity: int):
             demote[b][r] = np.nonzero(old & ~new)[0]
             hot_new[b, r, :N] = new
     return hits.astype(np.uint16), hot_new, promote, demote
+
+
+def app_split(f_c, f_s, b_c, b_s, alpha_c, alpha_s, m, m0=0.0, iters=200):
+    """Sec. 4.3: choose M_c (the rest, M_s = M - M_c, in the cold pool) so
+    that the two parallel paths of Eq. 2 take equal time, each path being its
+    scoring time plus moving its retained fraction,
+        T_c(M_c) = M_c / f_c + alpha_c M_c / b_c,  T_s(M_s) = M_s / f_s + alpha_s M_s / b_s,
+    subject to M_c <= m0 (Eq. 3; m0 <= 0: no bound).  T_c - T_s grows with
+    M_c, so the balance point is found by bisection on [0, M]; the bound then
+    clips it.  Returns (beta, M_c, M_s, T_c, T_s, capped)."""
+    def t_c(x):
+        return x / f_c + alpha_c * x / b_c
+
+    def t_s(x):
+        return x / f_s + alpha_s * x / b_s
+
+    lo, hi = 0.0, float(m)
+    for _ in range(iters):
+        mid = 0.5 * (lo + hi)
+        if t_c(mid) < t_s(m - mid):
+            lo = mid
+        else:
+            hi = mid
+    mc = 0.5 * (lo + hi)
+    capped = m0 > 0 and mc > m0
+    if capped:
+        mc = float(m0)
+    ms = m - mc
+    beta = mc / ms if ms > 0 else float("inf")
+    return beta, mc, ms, t_c(mc), t_s(ms), capped

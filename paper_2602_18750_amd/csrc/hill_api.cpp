@@ -655,6 +655,34 @@ hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t 
     return HILL_OK;
 }
 
+hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan)
+{
+    if (!p || !plan) return fail(HILL_ERR_INVALID_ARG, "params or plan is NULL");
+    const double rates[] = {p->f_c, p->f_s, p->b_c, p->b_s, p->m};
+    for (double x : rates)
+        if (!std::isfinite(x) || x <= 0.0)
+            return fail(HILL_ERR_INVALID_ARG, "throughputs, bandwidths and m must be finite and > 0");
+    if (!std::isfinite(p->alpha_c) || !std::isfinite(p->alpha_s) || p->alpha_c < 0.0 || p->alpha_c > 1.0 ||
+        p->alpha_s < 0.0 || p->alpha_s > 1.0)
+        return fail(HILL_ERR_INVALID_ARG, "alpha_c and alpha_s must lie in [0, 1]");
+    if (!std::isfinite(p->m0)) return fail(HILL_ERR_INVALID_ARG, "m0 is not finite");
+    // seconds per byte along each path (Eq. 2): scoring plus moving the retained part
+    const double a_c = 1.0 / p->f_c + p->alpha_c / p->b_c;
+    const double a_s = 1.0 / p->f_s + p->alpha_s / p->b_s;
+    hill_app_plan r{};
+    r.m_c = p->m * a_s / (a_c + a_s);   // a_c * M_c == a_s * (M - M_c)
+    if (p->m0 > 0.0 && r.m_c > p->m0) {
+        r.m_c = p->m0;
+        r.capped = 1;
+    }
+    r.m_s = p->m - r.m_c;
+    r.beta = r.m_s > 0.0 ? r.m_c / r.m_s : HUGE_VAL;
+    r.t_c = a_c * r.m_c;
+    r.t_s = a_s * r.m_s;
+    *plan = r;
+    return HILL_OK;
+}
+
 hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream)
 {
     HILL_TRY(check_ptr(buf, "buf"));

@@ -39,7 +39,7 @@ ABI_VERSION = 2   # HILL_ABI_VERSION of include/hill.h that this binding's struc
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
-           "hill_bkp_update")
+           "hill_bkp_update", "hill_app_balance")
 
 
 class HillError(RuntimeError):
@@ -87,6 +87,16 @@ class BkpDesc(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("batch", ctypes.c_int32), ("rows", ctypes.c_int32),
                 ("n_tokens", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("capacity", ctypes.c_int32),
                 ("stride_b", ctypes.c_int64), ("stride_r", ctypes.c_int64)]
+
+
+class AppParams(ctypes.Structure):
+    """hill_app_params (include/hill.h)."""
+    _fields_ = [(n, ctypes.c_double) for n in ("f_c", "f_s", "b_c", "b_s", "alpha_c", "alpha_s", "m", "m0")]
+
+
+class AppPlan(ctypes.Structure):
+    """hill_app_plan (include/hill.h)."""
+    _fields_ = [(n, ctypes.c_double) for n in ("beta", "m_c", "m_s", "t_c", "t_s")] + [("capped", ctypes.c_int32)]
 
 
 _lock = threading.Lock()
@@ -137,6 +147,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
         lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
         lib.hill_bkp_update.restype = ctypes.c_int
+        lib.hill_app_balance.argtypes = [ctypes.POINTER(AppParams), ctypes.POINTER(AppPlan)]
+        lib.hill_app_balance.restype = ctypes.c_int
         if lib.hill_abi_version() != ABI_VERSION:
             raise RuntimeError("libhill.so has ABI version %d, this binding needs %d; rebuild it"
                                % (lib.hill_abi_version(), ABI_VERSION))
@@ -476,6 +488,21 @@ class BkpCall:
 
     def __call__(self, idx_ptr: int):
         _check(self._fn(ctypes.byref(self.desc), ctypes.c_void_p(idx_ptr), self._k, *self._post))
+
+
+def app_balance(*, f_c, f_s, b_c, b_s, alpha=None, alpha_c=None, alpha_s=None, m=1.0, m0=0.0) -> dict:
+    """Capacity split of the Adaptive Prefetch-based Pipeline (Sec. 4.3, Eqs.
+    2-4), computed by the library (host only).  ``alpha`` sets both retained
+    fractions; ``alpha_c`` / ``alpha_s`` give skew-corrected ones."""
+    lib = load_library()
+    ac = alpha if alpha_c is None else alpha_c
+    as_ = alpha if alpha_s is None else alpha_s
+    if ac is None or as_ is None:
+        raise ValueError("give alpha, or alpha_c and alpha_s")
+    p = AppParams(f_c, f_s, b_c, b_s, ac, as_, m, m0)
+    out = AppPlan()
+    _check(lib.hill_app_balance(ctypes.byref(p), ctypes.byref(out)))
+    return {f[0]: getattr(out, f[0]) for f in AppPlan._fields_}
 
 
 class StepCall:

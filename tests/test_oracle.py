@@ -569,3 +569,50 @@ def test_pinned_selection_cases():
     assert list(O.topk_pinned(S, 3, 0, 1)[0]) == [0, 2, 7]
     with pytest.raises(ValueError):
         O.topk_pinned(S, 2, 1, 2)
+
+
+# --------------------------------------- APP capacity split (Sec. 4.3, Eqs. 2-4) --
+
+def _eq4(f_c, f_s, b_c, b_s, a):
+    """Eq. 4 as printed: beta = B_c f_c (B_s + alpha f_s) / (B_s f_s (B_c + alpha f_c))."""
+    return b_c * f_c * (b_s + a * f_s) / (b_s * f_s * (b_c + a * f_c))
+
+
+def _sec54(f_c, f_s, b_c, b_s, a):
+    """The optimum quoted with the sensitivity analysis (Sec. 5.4)."""
+    return f_c * (b_s * b_c + a * b_c * f_s + a * b_s * f_s) / (b_s * f_s * (b_c + a * f_c))
+
+
+@settings(max_examples=200, deadline=None)
+@given(st.floats(1e8, 1e11), st.floats(1e8, 1e11), st.floats(1e8, 1e11), st.floats(1e8, 1e11), st.floats(0, 1))
+def test_app_balance_is_eq4(f_c, f_s, b_c, b_s, a):
+    beta, mc, ms, tc, ts, capped = O.app_split(f_c, f_s, b_c, b_s, a, a, 1.0)
+    assert not capped
+    assert math.isclose(beta, _eq4(f_c, f_s, b_c, b_s, a), rel_tol=1e-9)
+    assert math.isclose(tc, ts, rel_tol=1e-9) and math.isclose(mc + ms, 1.0)
+
+
+def test_app_limits_and_bound():
+    # scoring alone (nothing retained): the split follows the scoring throughputs
+    beta = O.app_split(8e9, 2e9, 1e9, 1e9, 0.0, 0.0, 1.0)[0]
+    assert math.isclose(beta, 4.0, rel_tol=1e-9)
+    # scoring free (f -> inf): the split follows the transfer bandwidths
+    beta = O.app_split(1e30, 1e30, 32e9, 8e9, 0.2, 0.2, 1.0)[0]
+    assert math.isclose(beta, 4.0, rel_tol=1e-6)
+    # identical pools split evenly
+    assert math.isclose(O.app_split(5e9, 5e9, 7e9, 7e9, 0.3, 0.3, 2.0)[1], 1.0, rel_tol=1e-9)
+    # the host-memory bound (Eq. 3) clips M_c, leaving the cold path the slower one
+    beta, mc, ms, tc, ts, capped = O.app_split(10e9, 2e9, 25e9, 6e9, 0.2, 0.2, 100.0, m0=50.0)
+    assert capped and mc == 50.0 and ms == 50.0 and beta == 1.0 and ts > tc
+    # a larger retained fraction in the hot pool (the skew correction) moves bytes to the cold pool
+    assert O.app_split(10e9, 2e9, 25e9, 6e9, 0.3, 0.1, 1.0)[1] < O.app_split(10e9, 2e9, 25e9, 6e9, 0.2, 0.2, 1.0)[1]
+
+
+def test_app_sec54_variant_differs_by_one_term():
+    """The optimum quoted in Sec. 5.4 is Eq. 4 plus alpha f_c / (B_c + alpha f_c);
+    the balance of Eq. 2 gives Eq. 4 (the reading taken)."""
+    for f_c, f_s, b_c, b_s, a in [(10e9, 2e9, 25e9, 6e9, 0.2), (3e9, 3e9, 8e9, 2e9, 0.1)]:
+        assert math.isclose(_sec54(f_c, f_s, b_c, b_s, a) - _eq4(f_c, f_s, b_c, b_s, a),
+                            a * f_c / (b_c + a * f_c), rel_tol=1e-9)
+        beta = O.app_split(f_c, f_s, b_c, b_s, a, a, 1.0)[0]
+        assert not math.isclose(beta, _sec54(f_c, f_s, b_c, b_s, a), rel_tol=1e-3)
