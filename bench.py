@@ -40,6 +40,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -107,16 +108,16 @@ def scan_kernel_bytes(B, Hq, Hkv, D, n, mode="attn"):
 
 def load_traffic(which="keys16"):
     """HBM traffic of one score_tiles launch (which = "keys16" for the scan of
-    the 16-bit keys, "sketch" for the scan of the int8 sketch) from committed
-    counter runs, only while the kernel source is unchanged since the counters
-    were taken."""
+    the 16-bit keys, "sketch" / "sketch4" for the scan of the int8 / int4
+    sketch) from committed counter runs, only while the kernel source is
+    unchanged since the counters were taken."""
     try:
         rec = json.load(open(COUNTERS_FILE))
         src = hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest()
         if rec.get("source_sha256") != src:
             return None
-        if which == "sketch":
-            return (rec.get("sketch") or {}).get("hbm_bytes_per_launch")
+        if which in ("sketch", "sketch4"):
+            return (rec.get(which) or {}).get("hbm_bytes_per_launch")
         return rec.get("hbm_bytes_per_launch")
     except (OSError, ValueError):
         return None
@@ -289,7 +290,8 @@ def run_bench(args):
     if not args.no_bkp:
         res["bkp"] = bench_bkp(args, w, calls, nl_run, T, qptrs, stream)
     if not args.no_sketch:
-        res["sketch"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
+        res["sketch"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, 8)
+        res["sketch4"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, 4)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (%.0f s budget)" % args.cpu_seconds)
         res["cpu_baseline"] = cpu_baseline(W.WORKLOADS[int(args.workload)], args.cpu_seconds)
@@ -334,16 +336,17 @@ def bench_bkp(args, w, calls, nl_run, T, qptrs, stream):
     }
 
 
-def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
-    """The same decode steps scored on the int8 key sketch (Sec. 4.4
-    asymmetric precision; selection and attention unchanged).  The sketches
-    are written once before timing, as when the cache is filled; in a decode
-    loop only the appended row is sketched per step."""
+def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=8):
+    """The same decode steps scored on the int8 (nbits 8) or int4 (nbits 4)
+    key sketch (Sec. 4.4 asymmetric precision; selection and attention
+    unchanged).  The sketches are written once before timing, as when the
+    cache is filled; in a decode loop only the appended row is sketched per
+    step."""
     import torch
     import paper_2602_18750_amd as H
 
     dev = torch.device("cuda:0")
-    sks = [H.sketch_keys(x.k) for (x, _) in layers]
+    sks = [H.sketch_keys(x.k, bits=nbits) for (x, _) in layers]
     ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
     calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L])
              for L, (x, _) in enumerate(layers)]
@@ -374,10 +377,10 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
     units = (w.n_tokens + 255) // 256
     npart = (units + 1) // 2 * 2
-    scan_bytes = (w.batch * w.n_kv_heads * w.n_tokens * (128 + 1) + w.batch * w.n_q_heads * w.n_tokens * 4
-                  + w.batch * w.n_q_heads * npart * 8)
+    scan_bytes = (w.batch * w.n_kv_heads * w.n_tokens * (128 * nbits // 8 + 1)
+                  + w.batch * w.n_q_heads * w.n_tokens * 4 + w.batch * w.n_q_heads * npart * 8)
     scan_gbs = scan_bytes / (scan * 1e-3) / 1e9
-    traffic = load_traffic("sketch")
+    traffic = load_traffic("sketch" if nbits == 8 else "sketch4")
     # selection agreement with the 16-bit path: one step from zero importance on layer 0
     x = layers[0][0]
     s16 = H.new_importance(w.batch, 1, w.n_tokens, dev)
@@ -505,14 +508,15 @@ def run_read_ceiling(args):
 
 
 def _counter_rows(directory: str, counter: str, name_part: str):
-    """Per-dispatch values of `counter` for kernels whose name contains name_part."""
+    """Per-dispatch values of `counter` for kernels whose name contains
+    name_part (a regular expression)."""
     import csv
     vals = []
     for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
         with open(path) as f:
             per = {}
             for r in csv.DictReader(f):
-                if r.get("Counter_Name") != counter or name_part not in r.get("Kernel_Name", ""):
+                if r.get("Counter_Name") != counter or not re.search(name_part, r.get("Kernel_Name", "")):
                     continue
                 key = r.get("Dispatch_Id") or r.get("Correlation_Id")
                 per[key] = per.get(key, 0.0) + float(r.get("Counter_Value", 0))
@@ -543,14 +547,15 @@ def make_counters(directory: str, command: str):
 
     rec = {"kernel": "score_tiles (16-bit keys)",
            "source_sha256": hashlib.sha256(open(SCORE_SRC, "rb").read()).hexdigest()}
-    rec.update(scan("KeysF16"))
+    rec.update(scan(r"KeysF16"))
     rec.update({
         "copy_bytes": copy_bytes,
         "copy_fetch_kib": round(cf_kib, 1),
         "copy_write_kib": round(cw_kib, 1),
         "fetch_factor": round(ff, 4),
         "write_factor": round(wf, 4),
-        "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan("KeysI8")),
+        "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan(r"KeysSketch<\d+, \d+, 8>")),
+        "sketch4": dict(kernel="score_tiles (int4 key sketch)", **scan(r"KeysSketch<\d+, \d+, 4>")),
         "command": command,
     })
     print(json.dumps(rec, indent=1))

@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define HILL_ABI_VERSION 2
+#define HILL_ABI_VERSION 3
 
 typedef enum hill_status {
     HILL_OK = 0,
@@ -181,35 +181,40 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
                                float* s, int32_t k_sel, int32_t* idx_out, float* out,
                                void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
-/* Asymmetric-precision scoring (Sec. 4.4: the evaluation runs on int8 casts
- * of the keys and the query, attention on the original 16-bit K and V).
+/* Asymmetric-precision scoring (Sec. 4.4: the evaluation runs on int8 or
+ * int4 casts of the keys and an int8 cast of the query, attention on the
+ * original 16-bit K and V).
  *
- * The sketch of a key row (sequence b, KV head g, token j) is 128 int8 codes
- * plus one exponent e (int8): e is the smallest integer with
- * max|K[b,g,j,:]| * 2^-e <= 127, clamped to [-128, 127] (-128 for an all-zero
- * row), and code i = K[b,g,j,i] * 2^-e rounded to nearest, ties to even.
- * Layouts: k8 [B, Hkv, cap, 128] int8 contiguous, 16-byte aligned; k_exp
+ * The sketch of a key row (sequence b, KV head g, token j) is 128 codes plus
+ * one exponent e (int8): with qmax = 127 (bits 8) or 7 (bits 4), e is the
+ * smallest integer with max|K[b,g,j,:]| * 2^-e <= qmax, clamped to
+ * [-128, 127] (-128 for an all-zero row), and code i = K[b,g,j,i] * 2^-e
+ * rounded to nearest, ties to even, clamped to [-qmax, qmax].
+ * Layouts: codes [B, Hkv, cap, 128] int8 (bits 8) or [B, Hkv, cap, 64] bytes
+ * (bits 4: each group of 8 codes c0..c7 is one 4-byte word whose byte i is
+ * (c_i + 8) | (c_{i+4} + 8) << 4), contiguous, 16-byte aligned; k_exp
  * [B, Hkv, cap] int8 contiguous, 4-byte aligned; cap >= n_tokens, cap a
- * multiple of 4.  The query is cast the same way per head inside the scan.
- * The score of token j for head h is (sum_i q8[h,i] * k8[j,i]) * 2^(e_q + e_k),
- * exact up to one fp32 rounding; weights, S, selection and attention are as
- * in hill_score / hill_step. */
+ * multiple of 4.  The query is cast to int8 the same way per head inside the
+ * scan.  The score of token j for head h is (sum_i q8[h,i] * code[j,i]) *
+ * 2^(e_q + e_k), exact up to one fp32 rounding; weights, S, selection and
+ * attention are as in hill_score / hill_step. */
 
-/* Writes the sketch of key rows [token_begin, token_end) of every (b, g):
- * run it over the whole cache once, then for each appended token. */
-hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap,
+/* Writes the sketch (bits 8 or 4) of key rows [token_begin, token_end) of
+ * every (b, g): run it over the whole cache once, then for each appended
+ * token. */
+hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap, int32_t bits,
                              int32_t token_begin, int32_t token_end, void* stream);
 
 /* hill_score on the sketch (no 16-bit keys read). */
 hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp,
-                              int64_t cap, float* s, void* ws, size_t ws_bytes, void* stream);
+                              int64_t cap, int32_t bits, float* s, void* ws, size_t ws_bytes, void* stream);
 
 /* hill_step whose scoring reads the sketch; selection and attention as in
  * hill_step (attention reads the 16-bit K and V of the selected tokens).
  * ev may be NULL (see hill_step_profiled). */
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v,
-                             const int8_t* k8, const int8_t* k_exp, int64_t cap, float* s, int32_t k_sel,
-                             int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
+                             const int8_t* k8, const int8_t* k_exp, int64_t cap, int32_t bits, float* s,
+                             int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                              const hill_step_events* ev);
 
 /* Bidirectional KV Cache Pools (Sec. 4.2, HKM / BKP): the per-token hit-rate

@@ -27,16 +27,18 @@
  *   (5) attention    Eq. 1 restricted to the selected set I, softmax
  *                    renormalised over I (Sec. 4.1 workflow step 6)
  *
- *   (6) asymmetric   scoring-only int8 casts of the keys and the query
- *       precision    (Sec. 4.4 "Streaming Execution and Asymmetric
- *                    Precision": Q.K^T in low precision for the evaluation
- *                    only; attention keeps the 16-bit K, V).  Readings where
- *                    the paper is silent: one power-of-two scale 2^e per key
- *                    row (sequence, KV head, token) and per query head, the
- *                    smallest e with max|x| * 2^-e <= 127; codes rounded to
- *                    nearest, ties to even; e clamped to [-128, 127] (an
- *                    all-zero row has e = -128); the score is the exact
- *                    integer dot product times 2^(e_q + e_k).
+ *   (6) asymmetric   scoring-only low-precision casts of the keys (int8 or
+ *       precision    int4) and the query (int8) (Sec. 4.4 "Streaming
+ *                    Execution and Asymmetric Precision": Q.K^T in INT8/INT4
+ *                    for the evaluation only; attention keeps the 16-bit K,
+ *                    V).  Readings where the paper is silent: one
+ *                    power-of-two scale 2^e per key row (sequence, KV head,
+ *                    token) and per query head, the smallest e with
+ *                    max|x| * 2^-e <= qmax (127 for int8, 7 for int4); codes
+ *                    rounded to nearest, ties to even, clamped to
+ *                    [-qmax, qmax]; e clamped to [-128, 127] (an all-zero row
+ *                    has e = -128); the score is the exact integer dot
+ *                    product times 2^(e_q + e_k).
  *
  * kv(h) = floor(h / G) with G = Hq / Hkv (contiguous GQA groups).
  * Row granularity: token mode (gran 0) has one row per batch element summing
@@ -155,12 +157,14 @@ int hor_logits(int B, int Hq, int Hkv, int D, int n, int dtype,
     return 0;
 }
 
-/* (6) int8 sketch of `rows` rows of D 16-bit values: codes[r, i] and one
- * exponent per row, by the rule in the header.  Every operation is exact
- * (scaling by a power of two, round-to-nearest-even of a value <= 127). */
-int hor_sketch(int64_t rows, int D, int dtype, const uint16_t *x, int8_t *codes, int8_t *exps)
+/* (6) sketch of `rows` rows of D 16-bit values with codes in [-qmax, qmax]
+ * (qmax = 127: int8, 7: int4): codes[r, i] and one exponent per row, by the
+ * rule in the header.  Every operation is exact (scaling by a power of two,
+ * round-to-nearest-even of a value <= qmax). */
+int hor_sketch(int64_t rows, int D, int dtype, int qmax, const uint16_t *x, int8_t *codes, int8_t *exps)
 {
-    if (rows < 0 || D < 1) return -1;
+    if (rows < 0 || D < 1 || (qmax != 127 && qmax != 7)) return -1;
+    const int lg = qmax == 127 ? 7 : 3;   /* qmax + 1 = 2^lg */
     double *tab = (double *)malloc(65536 * sizeof(double));
     if (!tab) return -2;
     build_table(dtype, tab);
@@ -176,15 +180,16 @@ int hor_sketch(int64_t rows, int D, int dtype, const uint16_t *x, int8_t *codes,
         if (amax > 0.0) {
             int E;
             const double m = frexp(amax, &E);       /* amax = m * 2^E, m in [0.5, 1) */
-            e = m * 128.0 <= 127.0 ? E - 7 : E - 6; /* smallest e with amax * 2^-e <= 127 */
+            /* smallest e with amax * 2^-e <= qmax: m * 2^(E-e) <= qmax */
+            e = ldexp(m, lg) <= (double)qmax ? E - lg : E - lg + 1;
             if (e < -128) e = -128;
             if (e > 127) e = 127;
         }
         exps[r] = (int8_t)e;
         for (int i = 0; i < D; ++i) {
             double c = nearbyint(ldexp(tab[xr[i]], -e));   /* default rounding: to nearest, ties to even */
-            if (c > 127.0) c = 127.0;
-            if (c < -127.0) c = -127.0;
+            if (c > qmax) c = qmax;
+            if (c < -qmax) c = -qmax;
             codes[r * D + i] = (int8_t)c;
         }
     }

@@ -95,7 +95,7 @@ def _load():
         lib.hor_sparse_attn.restype = I
         lib.hor_step.argtypes = [I, I, I, I, I, I, I, I, Dd, P, P, P, P, P, I, P, P, P]
         lib.hor_step.restype = I
-        lib.hor_sketch.argtypes = [I64, I, I, P, P, P]
+        lib.hor_sketch.argtypes = [I64, I, I, I, P, P, P]
         lib.hor_sketch.restype = I
         lib.hor_logits_i8.argtypes = [I, I, I, I, I, P, P, P, P, P]
         lib.hor_logits_i8.restype = I
@@ -152,24 +152,27 @@ def logits(q, k, dtype) -> np.ndarray:
     return out
 
 
-def sketch(x, dtype):
-    """int8 scoring sketch of the last axis of x (16-bit patterns, D = last
-    dimension): (codes int8 of x's shape, exponents int8 of x.shape[:-1]).
-    Sec. 4.4 asymmetric precision, with the power-of-two per-row scale reading."""
+def sketch(x, dtype, bits: int = 8):
+    """Scoring sketch of the last axis of x (16-bit patterns, D = last
+    dimension): (codes int8 of x's shape, exponents int8 of x.shape[:-1]);
+    codes in [-127, 127] (bits 8) or [-7, 7] (bits 4).  Sec. 4.4 asymmetric
+    precision, with the power-of-two per-row scale reading."""
     lib = _load()
     x = _u16(x)
     D = x.shape[-1]
     rows = x.size // D
+    qmax = {8: 127, 4: 7}[bits]
     codes = np.empty(x.shape, dtype=np.int8)
     exps = np.empty(x.shape[:-1], dtype=np.int8)
-    rc = lib.hor_sketch(rows, D, _code(_DTYPES, dtype), _ptr(x), _ptr(codes), _ptr(exps))
+    rc = lib.hor_sketch(rows, D, _code(_DTYPES, dtype), qmax, _ptr(x), _ptr(codes), _ptr(exps))
     if rc:
         raise ValueError("hor_sketch failed (%d)" % rc)
     return codes, exps
 
 
 def logits_i8(q8, eq, k8, ek) -> np.ndarray:
-    """Sketch logits: exact integer q8.k8 scaled by 2^(eq + ek), float64.
+    """Sketch logits: exact integer q8.k8 scaled by 2^(eq + ek), float64 (k8:
+    int8 or int4 key codes, held one per int8).
     q8 [B,Hq,D], eq [B,Hq], k8 [B,Hkv,n,D], ek [B,Hkv,n]."""
     lib = _load()
     q8, k8 = np.ascontiguousarray(q8, dtype=np.int8), np.ascontiguousarray(k8, dtype=np.int8)

@@ -239,16 +239,18 @@ T* at(void* ws, size_t off)
     return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
 }
 
-// Optional int8 key sketch scored in place of the 16-bit keys.
+// Optional int8 / int4 key sketch scored in place of the 16-bit keys.
 struct Sketch {
     const int8_t* k8 = nullptr;
     const int8_t* k_exp = nullptr;
     int64_t cap = 0;
+    int bits = 8;
 };
 
-hill_status check_sketch(const Shape& s, const int8_t* k8, const int8_t* k_exp, int64_t cap)
+hill_status check_sketch(const Shape& s, const int8_t* k8, const int8_t* k_exp, int64_t cap, int bits)
 {
     if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
+    if (bits != 8 && bits != 4) return fail(HILL_ERR_INVALID_ARG, "sketch bits %d is not 8 or 4", bits);
     if ((uintptr_t)k8 & 15u) return fail(HILL_ERR_INVALID_ARG, "sketch codes are not 16-byte aligned");
     if ((uintptr_t)k_exp & 3u) return fail(HILL_ERR_INVALID_ARG, "sketch exponents are not 4-byte aligned");
     if (cap < s.n || cap % 4) return fail(HILL_ERR_INVALID_ARG, "sketch capacity %lld must be >= n_tokens and a multiple of 4",
@@ -290,6 +292,7 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.k8 = sk.k8;
     a.k_exp = sk.k_exp;
     a.cap = sk.cap;
+    a.kbits = sk.bits;
     const int ncu = device_cus();
 
     UpdateArgs u{};
@@ -427,7 +430,7 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     HILL_TRY(check_ptr(q, "q"));
     HILL_TRY(check_ptr(k, "k"));
     HILL_TRY(check_ptr(v, "v"));
-    if (sk.k8) HILL_TRY(check_sketch(s, sk.k8, sk.k_exp, sk.cap));
+    if (sk.k8) HILL_TRY(check_sketch(s, sk.k8, sk.k_exp, sk.cap, sk.bits));
     HILL_TRY(check_ptr(s_acc, "s"));
     HILL_TRY(check_ptr(out, "out"));
     if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
@@ -490,13 +493,13 @@ hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* 
     return run_score(d, s, L, q, k, Sketch{}, s_acc, ws, false, static_cast<hipStream_t>(stream), hill_step_events{});
 }
 
-hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap,
+hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap, int32_t bits,
                              int32_t token_begin, int32_t token_end, void* stream)
 {
     Shape s;
     HILL_TRY(check_desc(d, &s, false));
     HILL_TRY(check_ptr(k, "k"));
-    HILL_TRY(check_sketch(s, k8, k_exp, cap));
+    HILL_TRY(check_sketch(s, k8, k_exp, cap, bits));
     if (token_begin < 0 || token_begin > token_end || token_end > s.n)
         return fail(HILL_ERR_INVALID_ARG, "token range [%d, %d) not inside [0, n_tokens=%d)", token_begin, token_end, s.n);
     SketchArgs a{};
@@ -511,6 +514,7 @@ hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8
     a.cap = cap;
     a.k8 = k8;
     a.k_exp = k_exp;
+    a.bits = bits;
     HIP_TRY(launch_sketch_keys(a, s.dtype, static_cast<hipStream_t>(stream)));
     return HILL_OK;
 }
@@ -695,16 +699,16 @@ hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32
 }
 
 hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp, int64_t cap,
-                              float* s_acc, void* ws, size_t ws_bytes, void* stream)
+                              int32_t bits, float* s_acc, void* ws, size_t ws_bytes, void* stream)
 {
     Shape s;
     HILL_TRY(check_desc(d, &s));
     HILL_TRY(check_ptr(q, "q"));
-    HILL_TRY(check_sketch(s, k8, k_exp, cap));
+    HILL_TRY(check_sketch(s, k8, k_exp, cap, bits));
     HILL_TRY(check_ptr(s_acc, "s"));
     const Layout L = layout_for(s, 1);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_score));
-    return run_score(d, s, L, q, nullptr, Sketch{k8, k_exp, cap}, s_acc, ws, false, static_cast<hipStream_t>(stream),
+    return run_score(d, s, L, q, nullptr, Sketch{k8, k_exp, cap, bits}, s_acc, ws, false, static_cast<hipStream_t>(stream),
                      hill_step_events{});
 }
 
@@ -755,11 +759,12 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
 }
 
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v, const int8_t* k8,
-                             const int8_t* k_exp, int64_t cap, float* s_acc, int32_t k_sel, int32_t* idx_out,
-                             float* out, void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev)
+                             const int8_t* k_exp, int64_t cap, int32_t bits, float* s_acc, int32_t k_sel,
+                             int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
+                             const hill_step_events* ev)
 {
     if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
-    return run_step(d, q, k, v, Sketch{k8, k_exp, cap}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
+    return run_step(d, q, k, v, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
 }
 
 }  // extern "C"

@@ -20,6 +20,14 @@ __device__ __forceinline__ uint4 load_stream16(const void* p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 8-byte non-temporal load (streamed int4 key codes).
+__device__ __forceinline__ uint2 load_stream8(const void* p)
+{
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    const u32x2_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x2_t*>(p));
+    return make_uint2(v.x, v.y);
+}
+
 // fp32 += a.lo*b.lo + a.hi*b.hi over packed 16-bit pairs (v_dot2c_f32_{f16,bf16}).
 template <int DT>
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c);
@@ -109,24 +117,29 @@ __device__ __forceinline__ float max16(float v)
     return fmaxf(v, dpp<0x140>(v));
 }
 
-// Exponent of the int8 scoring sketch of a row whose largest magnitude is
-// amax: the smallest e with amax * 2^-e <= 127, clamped to [-128, 127]
-// (-128 for an all-zero row).  frexp is exact.
+// Exponent of a scoring sketch with codes in [-QMAX, QMAX] (127: int8, 7:
+// int4) of a row whose largest magnitude is amax: the smallest e with
+// amax * 2^-e <= QMAX, clamped to [-128, 127] (-128 for an all-zero row).
+// frexp is exact; QMAX / (QMAX + 1) is exact in fp32.
+template <int QMAX>
 __device__ __forceinline__ int sketch_exponent(float amax)
 {
+    static_assert(QMAX == 127 || QMAX == 7, "int8 or int4 codes");
+    constexpr int kLg = QMAX == 127 ? 7 : 3;   // QMAX + 1 = 2^kLg
     if (!(amax > 0.0f)) return -128;
     int E;
     const float m = frexpf(amax, &E);   // amax = m * 2^E, m in [0.5, 1)
-    const int e = m <= 0.9921875f ? E - 7 : E - 6;
+    const int e = m <= (float)QMAX / (float)(QMAX + 1) ? E - kLg : E - kLg + 1;
     return e < -128 ? -128 : (e > 127 ? 127 : e);
 }
 
-// int8 code of x under exponent e: x * 2^-e (exact) rounded to nearest, ties
-// to even, clamped to [-127, 127].
+// Code of x under exponent e: x * 2^-e (exact) rounded to nearest, ties to
+// even, clamped to [-QMAX, QMAX].
+template <int QMAX>
 __device__ __forceinline__ int sketch_code(float x, int e)
 {
     const float r = rintf(ldexpf(x, -e));
-    return (int)fminf(fmaxf(r, -127.0f), 127.0f);
+    return (int)fminf(fmaxf(r, -(float)QMAX), (float)QMAX);
 }
 
 // Sum over each aligned group of 16 lanes; every lane of the group gets the sum.

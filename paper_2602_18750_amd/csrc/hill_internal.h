@@ -41,9 +41,11 @@ struct ScoreArgs {
     int64_t s_sb, s_sr;
     uint32_t* zero_ptr;      // nullable: words to clear for a later kernel
     int64_t zero_words;
-    const int8_t* k8;        // nullable: int8 key sketch [B,Hkv,cap,128] scored instead of k
+    const int8_t* k8;        // nullable: key sketch scored instead of k: int8 codes [B,Hkv,cap,128]
+                             //   (kbits 8) or packed int4 codes [B,Hkv,cap,64] bytes (kbits 4)
     const int8_t* k_exp;     //   its per-row exponents [B,Hkv,cap]
     int64_t cap;             //   tokens per (b, g) in the sketch, a multiple of 4
+    int kbits;               //   8 or 4
 };
 
 // int8 key sketch: codes and one power-of-two exponent per key row
@@ -52,8 +54,9 @@ struct SketchArgs {
     int64_t k_sb, k_sh, k_sn;
     int B, Hkv, t0, t1;
     int64_t cap;
-    int8_t* k8;
+    int8_t* k8;              // int8 codes [.., 128] or packed int4 codes [.., 64] bytes
     int8_t* k_exp;
+    int bits;                // 8 or 4
 };
 
 struct UpdateArgs {

@@ -115,26 +115,34 @@ struct KeysF16 {
     }
 };
 
-// int8 sketch (Sec. 4.4 asymmetric precision): lane l8 holds codes
-// [16*l8, 16*l8+16) of each of its 4 rows (one 16-byte load per row) and the
-// rows' exponents.  The queries of the group are cast to int8 the same way
-// (power-of-two scale per head, round to nearest even) once per workgroup
-// when the group changes: wave w casts heads w, w+4, ... into LDS
-// (group_query), and every wave reads its slices from there (query).  The
-// dot product is exact in int32 (|sum| < 2^24) and scaled by 2^(e_q + e_k).
+// Key sketch (Sec. 4.4 asymmetric precision), BITS = 8 or 4: lane l8 holds
+// codes [16*l8, 16*l8+16) of each of its 4 rows (one 16-byte load per row for
+// int8, one 8-byte load for int4) and the rows' exponents.  An int4 row packs
+// each group of 8 codes into one word: byte i holds code i + 8 in its low
+// nibble and code i+4 + 8 in its high nibble, so two masks give four int8
+// lanes in element order, and the +8 offset is taken off as 8 * (sum of the
+// query codes).  The queries of the group are cast to int8 (power-of-two
+// scale per head, round to nearest even) once per workgroup when the group
+// changes: wave w casts heads w, w+4, ... into LDS (group_query), and every
+// wave reads its slices from there (query).  The dot product is exact in
+// int32 (|sum| < 2^24) and scaled by 2^(e_q + e_k).
 struct QueryLds {
     int8_t q8[kMaxGroup][kHeadDim];
     int eq[kMaxGroup];
 };
 
-template <int DT, int GC>
-struct KeysI8 {
+template <int DT, int GC, int BITS>
+struct KeysSketch {
+    static_assert(BITS == 8 || BITS == 4, "int8 or int4 key codes");
     static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
     static constexpr bool kGroupQuery = true;
-    uint4 kr[kSlots][kRowsPerLane];
+    static constexpr int kRowBytes = kHeadDim * BITS / 8;
+    using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
+    Codes kr[kSlots][kRowsPerLane];
     uint32_t ek4[kSlots];   // exponents of the 4 rows, one byte each
     uint4 q8[GC];
     int eq[GC];
+    int qbias[GC];          // int4: 8 * (sum of this lane's 16 query codes)
     int q_tag = -1;
     QueryLds* ql = nullptr;
 
@@ -143,11 +151,15 @@ struct KeysI8 {
     {
         const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
         const int jr = c.j0 + rg * kRowsPerLane;
-        const int8_t* kb = a.k8 + bg * a.cap * kHeadDim + l8 * 16;
+        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + l8 * (kRowBytes / 8);
 #pragma unroll
         for (int u = 0; u < kRowsPerLane; ++u) {
             const int j = jr + u;
-            kr[SLOT][u] = j < a.n ? load_stream16(kb + (int64_t)j * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+            if constexpr (BITS == 8) {
+                kr[SLOT][u] = j < a.n ? load_stream16(kb + (int64_t)j * kRowBytes) : make_uint4(0u, 0u, 0u, 0u);
+            } else {
+                kr[SLOT][u] = j < a.n ? load_stream8(kb + (int64_t)j * kRowBytes) : make_uint2(0u, 0u);
+            }
         }
         // jr is a multiple of 4 and cap too: the 4 exponents are one aligned word inside the row
         ek4[SLOT] = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
@@ -178,8 +190,9 @@ struct KeysI8 {
     {
         float x0, x1;
         widen2<DT>(word, x0, x1);
-        const int e = sketch_exponent(wave_max(fmaxf(fabsf(x0), fabsf(x1))));
-        const uint32_t c2 = ((uint32_t)sketch_code(x0, e) & 0xffu) | (((uint32_t)sketch_code(x1, e) & 0xffu) << 8);
+        const int e = sketch_exponent<127>(wave_max(fmaxf(fabsf(x0), fabsf(x1))));
+        const uint32_t c2 =
+            ((uint32_t)sketch_code<127>(x0, e) & 0xffu) | (((uint32_t)sketch_code<127>(x1, e) & 0xffu) << 8);
         *reinterpret_cast<uint16_t*>(&ql->q8[h][2 * lane]) = (uint16_t)c2;
         if (lane == 0) ql->eq[h] = e;
     }
@@ -204,6 +217,14 @@ struct KeysI8 {
         for (int hh = 0; hh < GC; ++hh) {
             q8[hh] = *reinterpret_cast<const uint4*>(&ql->q8[hc + hh][16 * l8]);
             eq[hh] = ql->eq[hc + hh];
+            if constexpr (BITS == 4) {
+                const int ones = 0x01010101;
+                int sq = __builtin_amdgcn_sdot4((int)q8[hh].x, ones, 0, false);
+                sq = __builtin_amdgcn_sdot4((int)q8[hh].y, ones, sq, false);
+                sq = __builtin_amdgcn_sdot4((int)q8[hh].z, ones, sq, false);
+                sq = __builtin_amdgcn_sdot4((int)q8[hh].w, ones, sq, false);
+                qbias[hh] = 8 * sq;
+            }
         }
         q_tag = tag;
     }
@@ -211,11 +232,22 @@ struct KeysI8 {
     template <int SLOT>
     __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
     {
-        const uint4 k = kr[SLOT][u];
-        int d = __builtin_amdgcn_sdot4((int)k.x, (int)q8[hh].x, 0, false);
-        d = __builtin_amdgcn_sdot4((int)k.y, (int)q8[hh].y, d, false);
-        d = __builtin_amdgcn_sdot4((int)k.z, (int)q8[hh].z, d, false);
-        d = __builtin_amdgcn_sdot4((int)k.w, (int)q8[hh].w, d, false);
+        int d;
+        if constexpr (BITS == 8) {
+            const uint4 k = kr[SLOT][u];
+            d = __builtin_amdgcn_sdot4((int)k.x, (int)q8[hh].x, 0, false);
+            d = __builtin_amdgcn_sdot4((int)k.y, (int)q8[hh].y, d, false);
+            d = __builtin_amdgcn_sdot4((int)k.z, (int)q8[hh].z, d, false);
+            d = __builtin_amdgcn_sdot4((int)k.w, (int)q8[hh].w, d, false);
+        } else {
+            // codes + 8 in [1, 15]: low nibbles are elements 0..3 of a group, high nibbles 4..7
+            const uint2 k = kr[SLOT][u];
+            const uint32_t m = 0x0F0F0F0Fu;
+            d = __builtin_amdgcn_sdot4((int)(k.x & m), (int)q8[hh].x, -qbias[hh], false);
+            d = __builtin_amdgcn_sdot4((int)((k.x >> 4) & m), (int)q8[hh].y, d, false);
+            d = __builtin_amdgcn_sdot4((int)(k.y & m), (int)q8[hh].z, d, false);
+            d = __builtin_amdgcn_sdot4((int)((k.y >> 4) & m), (int)q8[hh].w, d, false);
+        }
         d = isum8(d);
         const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * u));
         return ldexpf((float)d, eq[hh] + ek);
@@ -318,7 +350,7 @@ __device__ __forceinline__ void merge_unit(const ScoreArgs& a, int bg, int unit,
 
 // Work unit: kUnitTiles consecutive wave-tiles of one (b, g); wave w takes
 // tiles w, w+4, ... of the unit.  Each workgroup walks a contiguous range of
-// units.  Keys = KeysF16 (16-bit cache) or KeysI8 (int8 sketch).
+// units.  Keys = KeysF16 (16-bit cache) or KeysSketch (int8 / int4 sketch).
 template <int GC, int OUT, typename Keys>
 __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
 {
@@ -679,8 +711,13 @@ template <int DT, int GC, int OUT>
 hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp ts)
 {
     const int64_t total = (int64_t)a.B * a.Hkv * a.npart;
-    if (a.k8) {
-        auto kernel = score_tiles_kernel<GC, OUT, KeysI8<DT, GC>>;
+    if (a.k8 && a.kbits == 4) {
+        auto kernel = score_tiles_kernel<GC, OUT, KeysSketch<DT, GC, 4>>;
+        const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+        const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+        hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+    } else if (a.k8) {
+        auto kernel = score_tiles_kernel<GC, OUT, KeysSketch<DT, GC, 8>>;
         const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
         const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
         hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);

@@ -35,7 +35,7 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
-ABI_VERSION = 2   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
+ABI_VERSION = 3   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
@@ -134,11 +134,11 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_profiled.argtypes = [D, P, P, P, P, I32, P, P, P, SZ, P, ctypes.POINTER(HillStepEvents)]
         lib.hill_step_profiled.restype = ctypes.c_int
         I64 = ctypes.c_int64
-        lib.hill_sketch_keys.argtypes = [D, P, P, P, I64, I32, I32, P]
+        lib.hill_sketch_keys.argtypes = [D, P, P, P, I64, I32, I32, I32, P]
         lib.hill_sketch_keys.restype = ctypes.c_int
-        lib.hill_score_sketch.argtypes = [D, P, P, P, I64, P, P, SZ, P]
+        lib.hill_score_sketch.argtypes = [D, P, P, P, I64, I32, P, P, SZ, P]
         lib.hill_score_sketch.restype = ctypes.c_int
-        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, P, I32, P, P, P, SZ, P,
+        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, I32, P, P, P, SZ, P,
                                          ctypes.POINTER(HillStepEvents)]
         lib.hill_step_sketch.restype = ctypes.c_int
         lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
@@ -261,33 +261,36 @@ def _device_check(*ts):
 
 
 class Sketch:
-    """int8 scoring sketch of a key cache (Sec. 4.4 asymmetric precision):
-    codes [B, Hkv, cap, 128] int8 and one exponent per row [B, Hkv, cap] int8."""
+    """Scoring sketch of a key cache (Sec. 4.4 asymmetric precision): codes
+    [B, Hkv, cap, 128] int8 (bits 8) or [B, Hkv, cap, 64] packed int4 bytes
+    (bits 4), and one exponent per row [B, Hkv, cap] int8."""
 
-    def __init__(self, codes: torch.Tensor, exps: torch.Tensor):
-        self.codes, self.exps = codes, exps
+    def __init__(self, codes: torch.Tensor, exps: torch.Tensor, bits: int = 8):
+        self.codes, self.exps, self.bits = codes, exps, int(bits)
         self.cap = codes.shape[2]
 
 
-def new_sketch(B: int, Hkv: int, cap: int, device) -> Sketch:
+def new_sketch(B: int, Hkv: int, cap: int, device, bits: int = 8) -> Sketch:
+    if bits not in (8, 4):
+        raise ValueError("bits must be 8 or 4")
     cap = (cap + 3) // 4 * 4
-    return Sketch(torch.zeros((B, Hkv, cap, 128), dtype=torch.int8, device=device),
-                  torch.full((B, Hkv, cap), -128, dtype=torch.int8, device=device))
+    return Sketch(torch.zeros((B, Hkv, cap, 128 * bits // 8), dtype=torch.int8, device=device),
+                  torch.full((B, Hkv, cap), -128, dtype=torch.int8, device=device), bits)
 
 
 def sketch_keys(k, sketch: Optional[Sketch] = None, *, token_begin=0, token_end=None, n_tokens=None,
-                stream=None) -> Sketch:
+                stream=None, bits: int = 8) -> Sketch:
     """Write the sketch of key rows [token_begin, token_end) (default: all)."""
     lib = load_library()
     _device_check(k)
     B, Hkv, ncap, D = k.shape
     if sketch is None:
-        sketch = new_sketch(B, Hkv, ncap, k.device)
+        sketch = new_sketch(B, Hkv, ncap, k.device, bits)
     n = ncap if n_tokens is None else int(n_tokens)
     t1 = n if token_end is None else int(token_end)
     desc = make_desc(None, k, None, None, n_tokens=n, shape=(B, Hkv, Hkv, D), dtype=k.dtype)
     _check(lib.hill_sketch_keys(ctypes.byref(desc), _ptr(k), _ptr(sketch.codes), _ptr(sketch.exps), sketch.cap,
-                                int(token_begin), t1, _stream_ptr(stream)))
+                                sketch.bits, int(token_begin), t1, _stream_ptr(stream)))
     return sketch
 
 
@@ -323,7 +326,7 @@ def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_s
                               _stream_ptr(stream)))
     else:
         _check(lib.hill_score_sketch(ctypes.byref(desc), _ptr(q), _ptr(sketch.codes), _ptr(sketch.exps),
-                                     sketch.cap, _ptr(s), _ptr(ws), ws.numel(), _stream_ptr(stream)))
+                                     sketch.cap, sketch.bits, _ptr(s), _ptr(ws), ws.numel(), _stream_ptr(stream)))
     return s
 
 
@@ -373,7 +376,7 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
     ``n_sink`` / ``n_recent``: pinned tokens every selection keeps.
 
     ``events``: optional HillStepEvents; then hill_step_profiled records them.
-    ``sketch``: score on the int8 sketch (hill_step_sketch)."""
+    ``sketch``: score on the int8 / int4 sketch (hill_step_sketch)."""
     lib = load_library()
     _device_check(q, k, v, s)
     desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale,
@@ -391,7 +394,8 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         ws = workspace(desc, k_sel, q.device)
     if sketch is not None:
         _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
-                                    _ptr(sketch.exps), sketch.cap, _ptr(s), int(k_sel), _ptr(idx_out), _ptr(out),
+                                    _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), int(k_sel), _ptr(idx_out),
+                                    _ptr(out),
                                     _ptr(ws), ws.numel(), _stream_ptr(stream),
                                     None if events is None else ctypes.byref(events)))
     elif events is None:
@@ -532,7 +536,8 @@ class StepCall:
             self._fn = None
             self._fn_ev = lib.hill_step_sketch   # events may be NULL
             self._post = (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
-                          ctypes.c_int64(sketch.cap), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
+                          ctypes.c_int64(sketch.cap), ctypes.c_int32(sketch.bits), P(s.data_ptr()),
+                          ctypes.c_int32(self.k_sel),
                           P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
                           ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
         self._keep = (k, v, s, sketch)

@@ -188,28 +188,38 @@ def test_sketch_entry_points_validate(H):
     d = base_desc(H)                     # n = 1000
     need = ws_need(H, d, 10)
     ok_cap = 1000
-    # sketch_keys: pointers, capacity, token range
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, None, FAKE, ok_cap, 0, 10, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, None, ok_cap, 0, 10, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE + 8, FAKE, ok_cap, 0, 10, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE + 2, ok_cap, 0, 10, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 996, 0, 10, None) == INVALID    # cap < n
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 1002, 0, 10, None) == INVALID   # cap % 4
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, 5, 4, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, -1, 4, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, 0, 1001, None) == INVALID
-    assert lib.hill_sketch_keys(ctypes.byref(d), None, FAKE, FAKE, ok_cap, 0, 10, None) == INVALID
-    # score / step on the sketch
-    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, None, FAKE, ok_cap, FAKE, FAKE, need, None) == INVALID
-    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, 996, FAKE, FAKE, need, None) == INVALID
-    assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, FAKE, FAKE, 16, None) == WORKSPACE
-    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, FAKE, 10, FAKE, FAKE,
-                                FAKE, need, None, None) == INVALID
-    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, FAKE, 10, FAKE, FAKE,
-                                FAKE, need, None, None) == INVALID
-    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, FAKE, 0, FAKE, FAKE,
-                                FAKE, need, None, None) == INVALID
-    assert lib.hill_last_error() != b""
+    for bits in (8, 4):
+        # sketch_keys: pointers, capacity, token range
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, None, FAKE, ok_cap, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, None, ok_cap, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE + 8, FAKE, ok_cap, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE + 2, ok_cap, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 996, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, 1002, bits, 0, 10, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, 5, 4, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, -1, 4, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, 0, 1001, None) == INVALID
+        assert lib.hill_sketch_keys(ctypes.byref(d), None, FAKE, FAKE, ok_cap, bits, 0, 10, None) == INVALID
+        # score / step on the sketch
+        assert lib.hill_score_sketch(ctypes.byref(d), FAKE, None, FAKE, ok_cap, bits, FAKE, FAKE, need,
+                                     None) == INVALID
+        assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, 996, bits, FAKE, FAKE, need, None) == INVALID
+        assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 16,
+                                     None) == WORKSPACE
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, bits, FAKE, 10, FAKE,
+                                    FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, bits, FAKE, 10, FAKE,
+                                    FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, 0, FAKE,
+                                    FAKE, FAKE, need, None, None) == INVALID
+    # only 8 and 4 bits exist
+    for bits in (0, 2, 6, 16):
+        assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, 0, 10, None) == INVALID
+        assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, need,
+                                     None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, 10, FAKE,
+                                    FAKE, FAKE, need, None, None) == INVALID
+    assert b"bits" in lib.hill_last_error()
 
 
 def test_head_count_limits(H):

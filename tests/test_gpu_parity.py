@@ -421,17 +421,33 @@ def test_errors_raise_and_enqueue_nothing():
 
 # ----------------------------------------------- asymmetric-precision sketch --
 
-def _sketch_ref(x_k, dt):
-    codes, exps = O.sketch(bits(x_k), dt)
+def _sketch_ref(x_k, dt, nbits=8):
+    codes, exps = O.sketch(bits(x_k), dt, bits=nbits)
     return codes, exps
 
 
+def _unpack4(packed):
+    """Codes of the library's int4 layout (include/hill.h): each group of 8
+    codes c0..c7 is one 4-byte word whose byte i is (c_i + 8) | (c_{i+4} + 8) << 4."""
+    b = packed.view(np.uint8).astype(np.int16)
+    lo, hi = (b & 15) - 8, (b >> 4) - 8                      # [..., 64]
+    lo = lo.reshape(b.shape[:-1] + (16, 4))
+    hi = hi.reshape(b.shape[:-1] + (16, 4))
+    return np.concatenate([lo, hi], axis=-1).reshape(b.shape[:-1] + (128,)).astype(np.int8)
+
+
+def _codes_of(sk):
+    c = sk.codes.cpu().numpy()
+    return c if sk.bits == 8 else _unpack4(c)
+
+
+@pytest.mark.parametrize("nbits", [8, 4])
 @pytest.mark.parametrize("dt,B,Hkv,n,t0,t1", [
     ("bf16", 1, 8, 4096, 0, 4096), ("fp16", 2, 4, 777, 0, 777), ("bf16", 2, 2, 1000, 123, 517),
     ("bf16", 1, 1, 5, 4, 5),
 ])
-def test_sketch_keys_bit_exact(dt, B, Hkv, n, t0, t1):
-    say("sketch keys", dt, B, Hkv, n, t0, t1)
+def test_sketch_keys_bit_exact(dt, B, Hkv, n, t0, t1, nbits):
+    say("sketch keys", nbits, dt, B, Hkv, n, t0, t1)
     tdt = torch.bfloat16 if dt == "bf16" else torch.float16
     g = torch.Generator().manual_seed(n + t0)
     k = torch.randn(B, Hkv, n, 128, generator=g) * torch.exp(torch.randn(1, Hkv, 1, 128, generator=g))
@@ -439,13 +455,14 @@ def test_sketch_keys_bit_exact(dt, B, Hkv, n, t0, t1):
     k[:, :, 1::89] *= 1e-30                               # tiny rows (exponent clamp)
     k[:, :, 2::53, :5] = 0.5                              # ties at half a code step in some rows
     k = k.to(tdt)
-    sk = H().sketch_keys(k.to(DEV), token_begin=t0, token_end=t1)
+    sk = H().sketch_keys(k.to(DEV), token_begin=t0, token_end=t1, bits=nbits)
     torch.cuda.synchronize()
-    codes, exps = _sketch_ref(k, dt)
-    got_c, got_e = sk.codes.cpu().numpy(), sk.exps.cpu().numpy()
+    codes, exps = _sketch_ref(k, dt, nbits)
+    got_c, got_e = _codes_of(sk), sk.exps.cpu().numpy()
     assert np.array_equal(got_c[:, :, t0:t1], codes[:, :, t0:t1])
     assert np.array_equal(got_e[:, :, t0:t1], exps[:, :, t0:t1])
-    assert not got_c[:, :, :t0].any() and not got_c[:, :, t1:].any()          # untouched outside the range
+    raw = sk.codes.cpu().numpy()
+    assert not raw[:, :, :t0].any() and not raw[:, :, t1:].any()              # untouched outside the range
     assert (got_e[:, :, :t0] == -128).all() and (got_e[:, :, t1:] == -128).all()
 
 
@@ -458,14 +475,15 @@ SKETCH_SCORE_CASES = [
 ]
 
 
+@pytest.mark.parametrize("nbits", [8, 4])
 @pytest.mark.parametrize("B,Hq,Hkv,n,dt,mode,gran", SKETCH_SCORE_CASES)
-def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran):
-    say("sketch score", B, Hq, Hkv, n, dt, mode, gran)
+def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran, nbits):
+    say("sketch score", nbits, B, Hq, Hkv, n, dt, mode, gran)
     T = 2
     x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=T, seed=n + 3 * Hq)
     q, k, v = gpu_inputs(x)
-    sk = H().sketch_keys(k)
-    k8, ek = _sketch_ref(x.k, dt)
+    sk = H().sketch_keys(k, bits=nbits)
+    k8, ek = _sketch_ref(x.k, dt, nbits)
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
@@ -477,17 +495,18 @@ def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran):
         check_scores(s.cpu().numpy(), s_ref, "sketch step %d" % t)
 
 
+@pytest.mark.parametrize("nbits", [8, 4])
 @pytest.mark.parametrize("B,nh,n,dt", [(1, 16, 1000, "bf16"), (2, 8, 4099, "fp16")])
-def test_sketch_logits_bit_exact(B, nh, n, dt):
+def test_sketch_logits_bit_exact(B, nh, n, dt, nbits):
     """A sketch logit is an integer dot product (at most 128 * 127 * 127 < 2^24
     in magnitude) times a power of two, so in fp32 it is exact.  RAW, KV-head
     rows of one head each, one step from S = 0: S is the logit itself, and the
     GPU's must equal the oracle's exact value bit for bit."""
-    say("sketch logits exact", B, nh, n, dt)
+    say("sketch logits exact", nbits, B, nh, n, dt)
     x = W.make_random(B, nh, nh, 128, n, dt, steps=1, seed=4242 + n)
     q, k, v = gpu_inputs(x)
-    sk = H().sketch_keys(k)
-    k8, ek = _sketch_ref(x.k, dt)
+    sk = H().sketch_keys(k, bits=nbits)
+    k8, ek = _sketch_ref(x.k, dt, nbits)
     q8, eq = O.sketch(bits(x.q[0]), dt)
     ref = O.logits_i8(q8, eq, k8, ek).astype(np.float32)   # exact in fp64, hence in fp32
     s = H().new_importance(B, nh, n, DEV)
@@ -497,12 +516,12 @@ def test_sketch_logits_bit_exact(B, nh, n, dt):
     assert np.array_equal(got, ref.reshape(B, nh, n))
 
 
-def _run_sketch_steps(x, k_sel, mode, gran, steps, where):
+def _run_sketch_steps(x, k_sel, mode, gran, steps, where, nbits=8):
     B, Hkv, n = x.k.shape[0], x.k.shape[1], x.k.shape[2]
     dt = dname(x.k)
     q, k, v = gpu_inputs(x)
-    sk = H().sketch_keys(k)
-    k8, ek = _sketch_ref(x.k, dt)
+    sk = H().sketch_keys(k, bits=nbits)
+    k8, ek = _sketch_ref(x.k, dt, nbits)
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
@@ -519,14 +538,16 @@ def _run_sketch_steps(x, k_sel, mode, gran, steps, where):
         check_outputs(out.cpu().numpy(), out_own, "%s step %d out" % (where, t))
 
 
+@pytest.mark.parametrize("nbits", [8, 4])
 @pytest.mark.parametrize("mode,gran", [("attn", "token"), ("attn", "kvhead"), ("raw", "token")])
-def test_step_on_sketch_matches_oracle(mode, gran):
+def test_step_on_sketch_matches_oracle(mode, gran, nbits):
     x = W.make_random(2, 32, 8, 128, 3000, "bf16", steps=3, seed=77)
-    _run_sketch_steps(x, 300, mode, gran, 3, "sketch %s/%s" % (mode, gran))
+    _run_sketch_steps(x, 300, mode, gran, 3, "sketch%d %s/%s" % (nbits, mode, gran), nbits)
 
 
-def test_step_on_sketch_config3_full_size():
+@pytest.mark.parametrize("nbits", [8, 4])
+def test_step_on_sketch_config3_full_size(nbits):
     w = W.WORKLOADS[3]
-    say("sketch config 3 layer 0, 2 steps")
+    say("sketch config 3 layer 0, 2 steps", nbits)
     x = W.make_layer(w.replace(steps=2), 0)
-    _run_sketch_steps(x, w.k_sel, "attn", "token", 2, "sketch cfg3")
+    _run_sketch_steps(x, w.k_sel, "attn", "token", 2, "sketch%d cfg3" % nbits, nbits)

@@ -616,3 +616,90 @@ def test_app_sec54_variant_differs_by_one_term():
                             a * f_c / (b_c + a * f_c), rel_tol=1e-9)
         beta = O.app_split(f_c, f_s, b_c, b_s, a, a, 1.0)[0]
         assert not math.isclose(beta, _sec54(f_c, f_s, b_c, b_s, a), rel_tol=1e-3)
+
+
+# ------------------------------------------------------- int4 key sketch (Sec. 4.4) --
+
+@pytest.mark.parametrize("dt", ["bf16", "fp16"])
+def test_sketch4_rounding_bound_range_and_minimal_exponent(dt):
+    g = torch.Generator().manual_seed(12)
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float16
+    x = torch.randn(64, 128, generator=g) * torch.exp(torch.randn(1, 128, generator=g))
+    x = (x * torch.logspace(-3, 3, 64).unsqueeze(1)).to(tdt)
+    codes, exps = O.sketch(bits(x), dt, bits=4)
+    xd = _decoded(x)
+    amax = np.abs(xd).max(axis=1)
+    e = exps.astype(np.float64)
+    step = np.exp2(e)[:, None]
+    assert np.all(np.abs(xd - codes * step) <= step / 2)
+    assert np.all(np.abs(codes) <= 7)
+    assert np.all(amax * np.exp2(-e) <= 7)
+    assert np.all(amax * np.exp2(-(e - 1)) > 7)
+    assert np.all(np.abs(codes).max(axis=1) >= 4)
+
+
+def test_sketch4_ties_to_even_and_zero_rows():
+    s = 8.0
+    row = [7 * s, 2.5 * s, 3.5 * s, -2.5 * s, 0.5 * s, -0.5 * s, 1.5 * s, -1.5 * s] + [0.0] * 120
+    over = [7.5 * s] + [6.5 * s] + [0.0] * 126                   # 7.5 needs the next exponent
+    x = torch.tensor([row, [0.0] * 128, over], dtype=torch.float32).to(torch.bfloat16)
+    codes, exps = O.sketch(bits(x), "bf16", bits=4)
+    assert exps.tolist() == [3, -128, 4]
+    assert codes[0, :8].tolist() == [7, 2, 4, -2, 0, 0, 2, -2]
+    assert not codes[1].any()
+    assert codes[2, :2].tolist() == [4, 3]                       # 3.75 -> 4, 3.25 -> 3
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n", [(1, 4, 4, 9), (2, 8, 2, 17)])
+def test_sketch4_logits_exact_when_the_cast_is_lossless(B, Hq, Hkv, n):
+    """Keys on the int4 grid (integers in [-7, 7] times 2^s, row maximum 7 * 2^s)
+    and queries on the int8 grid are cast without loss: the asymmetric-precision
+    logits equal the fp64 logits exactly."""
+    g = np.random.default_rng(B * 37 + n)
+
+    def rows(shape, qmax):
+        v = g.integers(-qmax, qmax + 1, size=shape + (128,)).astype(np.float64)
+        v[..., 0] = qmax
+        return v * np.exp2(g.integers(-6, 7, size=shape + (1,)))
+
+    q = torch.from_numpy(rows((B, Hq), 127)).to(torch.bfloat16)
+    k = torch.from_numpy(rows((B, Hkv, n), 7)).to(torch.bfloat16)
+    q8, eq = O.sketch(bits(q), "bf16")
+    k4, ek = O.sketch(bits(k), "bf16", bits=4)
+    assert np.array_equal(O.logits_i8(q8, eq, k4, ek), O.logits(bits(q), bits(k), "bf16"))
+
+
+def test_sketch4_logits_error_bound():
+    x = W.make_random(1, 8, 2, 128, 300, "bf16", seed=6)
+    q8, eq = O.sketch(bits(x.q[0]), "bf16")
+    k4, ek = O.sketch(bits(x.k), "bf16", bits=4)
+    l4 = O.logits_i8(q8, eq, k4, ek)
+    l = O.logits(bits(x.q[0]), bits(x.k), "bf16")
+    qd, kd = _decoded(x.q[0]), _decoded(x.k)
+    dq = np.exp2(eq.astype(np.float64) - 1)
+    dk = np.exp2(ek.astype(np.float64) - 1)
+    for h in range(8):
+        g = h // 4
+        bound = (np.abs(qd[0, h]).sum() * dk[0, g] + np.abs(kd[0, g]).sum(axis=1) * dq[0, h]
+                 + 128 * dq[0, h] * dk[0, g])
+        assert np.all(np.abs(l4[0, h] - l[0, h]) <= bound * (1 + 1e-12))
+
+
+@pytest.mark.parametrize("wid,floor", [(3, 0.55), (1, 0.85)])
+def test_sketch4_selection_recall_vs_full_precision(wid, floor):
+    """Quality statistic: int4 keys (int8 queries) keep most of the 16-bit
+    selection on plain keys and lose more on per-channel outliers, which a
+    per-token scale with 7 levels cannot follow (workload 3)."""
+    w = W.WORKLOADS[wid].replace(n_tokens=4096, steps=4, layers=1)
+    x = W.make_layer(w, 0)
+    k4, ek = O.sketch(bits(x.k), w.dtype, bits=4)
+    S = np.zeros((w.batch, 1, w.n_tokens))
+    S4 = np.zeros_like(S)
+    k = O.budget_k(w.n_tokens, w.budget)
+    for t in range(w.steps):
+        q8, eq = O.sketch(bits(x.q[t]), w.dtype)
+        S = O.update(O.logits(bits(x.q[t]), bits(x.k), w.dtype), S, w.n_kv_heads, "attn", "token",
+                     O.default_scale(128))
+        S4 = O.update(O.logits_i8(q8, eq, k4, ek), S4, w.n_kv_heads, "attn", "token", O.default_scale(128))
+        for b in range(w.batch):
+            assert len(np.intersect1d(O.topk(S[b:b + 1], k), O.topk(S4[b:b + 1], k))) / k >= floor
