@@ -15,6 +15,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhill.so")
+# per-kernel registers, scratch and occupancy as the compiler reports them
+RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
 SOURCES = ["hill_api.cpp", "score.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip", "bkp.hip"]
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
@@ -28,17 +30,45 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
 
 def _compile(src: str, verbose: bool) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    lang = ["-x", "hip"] if src.endswith(".hip") else []
+    lang = ["-x", "hip", "-Rpass-analysis=kernel-resource-usage"] if src.endswith(".hip") else []
     cmd = [HIPCC] + COMMON + lang + ["-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
-    errs = "\n".join(l for l in (r.stderr or "").splitlines() if "packed-fp32-ops" not in l)
+    lines = (r.stderr or "").splitlines()
+    usage = [l for l in lines if "kernel-resource-usage" in l]
+    errs = "\n".join(l for l in lines if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed on %s:\n%s" % (src, errs))
     if verbose and errs.strip():
         print(errs, flush=True)
+    with open(os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".resources"), "w") as f:
+        f.write("\n".join(usage) + "\n")
     return obj
+
+
+def _resource_report():
+    """One line per kernel: name, VGPRs, scratch bytes per lane, occupancy."""
+    rows = []
+    for src in SOURCES:
+        path = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".resources")
+        if not src.endswith(".hip") or not os.path.exists(path):
+            continue
+        cur = {}
+        for line in open(path):
+            body = line.split("remark: ", 1)[-1].split(" [-Rpass", 1)[0].strip()
+            key, _, val = body.partition(":")
+            key, val = key.strip(), val.strip()
+            if key == "Function Name":
+                cur = {"name": val, "src": src}
+                rows.append(cur)
+            elif key in ("VGPRs", "ScratchSize [bytes/lane]", "Occupancy [waves/SIMD]"):
+                cur[key.split()[0]] = val
+    with open(RESOURCES, "w") as f:
+        for r in rows:
+            f.write("%s\t%s\tvgpr=%s\tscratch=%s\toccupancy=%s\n" % (
+                r["src"], r["name"], r.get("VGPRs", "?"), r.get("ScratchSize", "?"), r.get("Occupancy", "?")))
+    return rows
 
 
 def build(verbose: bool = False) -> str:
@@ -53,6 +83,7 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s" % r.stderr)
     os.replace(tmp, LIB)
+    _resource_report()
     return LIB
 
 

@@ -71,6 +71,7 @@ template <int DT, int GC>
 struct KeysF16 {
     static constexpr int kSlots = 1;   // tiles whose loads are in flight together
     static constexpr bool kGroupQuery = false;
+    static constexpr bool kIntDot = false;
     uint4 kr[2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
@@ -136,6 +137,7 @@ struct KeysSketch {
     static_assert(BITS == 8 || BITS == 4, "int8 or int4 key codes");
     static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
     static constexpr bool kGroupQuery = true;
+    static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
     static constexpr int kRowBytes = kHeadDim * BITS / 8;
     using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
     Codes kr[kSlots][kRowsPerLane];
@@ -143,6 +145,7 @@ struct KeysSketch {
     uint4 q8[GC];
     int eq[GC];
     int qbias[GC];          // int4: 8 * (sum of this lane's 16 query codes)
+    int eq_lane = 0;        // exponent of this lane's head (lane l8 < GC holds head l8 of the chunk)
     int q_tag = -1;
     QueryLds* ql = nullptr;
 
@@ -226,11 +229,13 @@ struct KeysSketch {
                 qbias[hh] = 8 * sq;
             }
         }
+        eq_lane = ql->eq[hc + (l8 < GC ? l8 : 0)];   // from LDS: a register-array pick would be indexed
         q_tag = tag;
     }
 
+    // Exact integer q . k of row u for head hh, complete in every lane of the row group.
     template <int SLOT>
-    __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
+    __device__ __forceinline__ int idot(int u, int hh) const
     {
         int d;
         if constexpr (BITS == 8) {
@@ -248,9 +253,22 @@ struct KeysSketch {
             d = __builtin_amdgcn_sdot4((int)(k.y & m), (int)q8[hh].z, d, false);
             d = __builtin_amdgcn_sdot4((int)((k.y >> 4) & m), (int)q8[hh].w, d, false);
         }
-        d = isum8(d);
+        return isum8(d);
+    }
+
+    // The logit of an integer dot of row u for this lane's head: d * 2^(e_q + e_k), exact.
+    template <int SLOT>
+    __device__ __forceinline__ float scale(int d, int u) const
+    {
         const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * u));
-        return ldexpf((float)d, eq[hh] + ek);
+        return ldexpf((float)d, eq_lane + ek);
+    }
+
+    template <int SLOT>
+    __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
+    {
+        const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * u));
+        return ldexpf((float)idot<SLOT>(u, hh), eq[hh] + ek);
     }
 };
 
@@ -266,16 +284,30 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord
     for (int hc = 0; hc < a.G; hc += GC) {
         ks.query(a, c, hc, l8);
         float mine[kRowsPerLane];   // lane l8 == hh keeps head hh's logits
+        if constexpr (OUT == kOutLogits && Keys::kIntDot) {
+            // integer dots: each lane keeps its own head's sum and scales only that one
 #pragma unroll
-        for (int u = 0; u < kRowsPerLane; ++u) {
-            mine[u] = 0.0f;
+            for (int u = 0; u < kRowsPerLane; ++u) {
+                int mi = 0;
 #pragma unroll
-            for (int hh = 0; hh < GC; ++hh) {
-                const float d = ks.template dot<SLOT>(a, u, hh, l8);
-                if constexpr (OUT == kOutLogits)
-                    mine[u] = (l8 == hh) ? d : mine[u];
-                else
-                    rawsum[u] += d;
+                for (int hh = 0; hh < GC; ++hh) {
+                    const int d = ks.template idot<SLOT>(u, hh);
+                    mi = (l8 == hh) ? d : mi;
+                }
+                mine[u] = ks.template scale<SLOT>(mi, u);
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < kRowsPerLane; ++u) {
+                mine[u] = 0.0f;
+#pragma unroll
+                for (int hh = 0; hh < GC; ++hh) {
+                    const float d = ks.template dot<SLOT>(a, u, hh, l8);
+                    if constexpr (OUT == kOutLogits)
+                        mine[u] = (l8 == hh) ? d : mine[u];
+                    else
+                        rawsum[u] += d;
+                }
             }
         }
         if constexpr (OUT == kOutLogits) {
