@@ -287,6 +287,7 @@ def run_bench(args):
         "layer_step_us_probe": round(mean(total) * 1e3, 3),
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
     }
+    res["streamed"] = bench_streamed(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_bkp:
         res["bkp"] = bench_bkp(args, w, calls, nl_run, T, qptrs, stream)
     if not args.no_sketch:
@@ -298,6 +299,53 @@ def run_bench(args):
     else:
         res["cpu_baseline"] = None
     print(json.dumps(res), flush=True)
+
+
+def bench_streamed(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
+    """The same decode steps through hill_step_streamed (Sec. 4.2 HIE's
+    running threshold: the update lists the candidates above the previous
+    step's threshold and the selection needs no refine pass), fresh S and
+    state per layer; results are identical to hill_step's."""
+    import torch
+    import paper_2602_18750_amd as H
+
+    dev = torch.device("cuda:0")
+    ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
+    states = [H.new_stream_state(w.batch, 1, dev) for _ in layers]
+    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, stream_state=states[L])
+             for L, (x, _) in enumerate(layers)]
+    hip = HipEvents()
+    ev_sets = []
+    for _ in range(args.steps):
+        e = [hip.create() for _ in range(6)]
+        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+    for i in range(args.warmup):
+        for L in range(nl_run):
+            calls[L](qptrs[L][i % T])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        t = (args.warmup + i) % T
+        probe = i % nl_run
+        for L in range(nl_run):
+            if L == probe:
+                calls[L](qptrs[L][t], ev_sets[i][1])
+            else:
+                calls[L](qptrs[L][t])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    score = sum(hip.ms(e[0], e[2]) for e, _ in ev_sets) / len(ev_sets)
+    selattn = sum(hip.ms(e[2], e[5]) for e, _ in ev_sets) / len(ev_sets)
+    hip.close()
+    ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
+    del calls, ss, states
+    return {
+        "ms_per_step": round(ms_step, 4),
+        "value_gbps": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl / (ms_step * 1e-3) / 1e9, 2),
+        "scoring_us_per_layer_step": round(score * 1e3, 3),
+        "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
+        "launches_per_layer_step": 4,
+    }
 
 
 def bench_bkp(args, w, calls, nl_run, T, qptrs, stream):

@@ -181,6 +181,27 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
                                float* s, int32_t k_sel, int32_t* idx_out, float* out,
                                void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
+/* Streamed selection (Sec. 4.2 HIE: scores streamed as (token, score) blocks
+ * and merged against a running threshold): hill_step with the selection's
+ * refine pass replaced.  With ATTN scores S only grows from step to step, so
+ * the previous step's threshold is a lower bound on this one; the update
+ * lists every token whose first radix digit reaches that bound, and the
+ * selection resolves the exact threshold from the complete first-digit
+ * histogram and that list.  Results are identical to hill_step.
+ *
+ * state: uint32 [B, R, 8], 16-byte aligned, caller-owned, one per S buffer;
+ * zero it at the start of a sequence and whenever S is changed outside these
+ * calls.  Each call reads the bound and writes the next one.  The bound is
+ * used only while it holds (same pins, k_sel not larger and n_tokens not
+ * smaller than at the previous call; n_tokens may grow only without pins);
+ * otherwise, and on the first call, the selection reads the whole row
+ * instead, which is exact but slower.  ATTN score mode only
+ * (HILL_ERR_UNSUPPORTED otherwise).  ev: as hill_step_profiled (the select
+ * interval is empty). */
+hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s,
+                               uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
+                               size_t ws_bytes, void* stream, const hill_step_events* ev);
+
 /* Asymmetric-precision scoring (Sec. 4.4: the evaluation runs on int8 or
  * int4 casts of the keys and an int8 cast of the query, attention on the
  * original 16-bit K and V).

@@ -42,8 +42,10 @@ struct Shape {
 // Workspace regions, in this order, each 256-byte aligned:
 //   logits   ATTN [B,Hq,ld] fp32 | RAW token rows with Hkv > 1: [B,Hkv,ld] fp32 (ld = n rounded up to 4)
 //   part     ATTN [B,Hq,npart] float2 (per 256-token unit);  stats ATTN [B,Hq] float2
-//   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins; cleared by the first kernel of every call
-//            that accumulates into them)
+//   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins) | hist2x [3,rows,4096+64] (the
+//            streamed selection's further second-digit windows, hist2 continued) -- cleared by the first kernel of
+//            every call that accumulates into them
+//   scount [rows,ceil(n/256)] u32 | spairs [rows,n] uint2 (key, token) | sd0 [rows] u32 (streamed selection only)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
 //   sel_list [rows,n] i32 | sel_n [rows,nchunks] u32
 //   slots: attention partials [B,Hq,nslots,D] fp32 and [B,Hq,nslots] float2, nslots =
@@ -51,9 +53,10 @@ struct Shape {
 // Only the last region depends on k_sel.
 struct Layout {
     size_t logits, part, stats;
-    size_t zero, hist1, hist2;
-    int64_t zero_words;
+    size_t zero, hist1, hist2, hist2x;
+    int64_t zero_words, zero_words_stream;   // the streamed selection also clears hist2x
     size_t cand_key, cand_n, state, sel_list, sel_n;
+    size_t scount, spairs, sd0;   // streamed selection: pair counts (zeroed), pairs, first-digit bounds
     size_t slot_o, slot_ml;
     size_t end_score, end_topk, end_all;
     int nchunks, nsplit, per_split, nslots;
@@ -79,9 +82,17 @@ Layout layout_for(const Shape& s, int ksel)
     L.zero = off;
     L.hist1 = off;
     L.hist2 = L.hist1 + rows * kHistRow * sizeof(uint32_t);
-    const size_t zero_end = L.hist2 + rows * kHistRow * sizeof(uint32_t);
-    L.zero_words = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
+    L.hist2x = L.hist2 + rows * kHistRow * sizeof(uint32_t);
+    L.zero_words = (int64_t)((L.hist2x - L.zero) / sizeof(uint32_t));
+    const size_t zero_end = L.hist2x + rows * (kStreamBins - 1) * kHistRow * sizeof(uint32_t);
+    L.zero_words_stream = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
     off = align256(zero_end);
+    L.scount = off;
+    off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * sizeof(uint32_t));
+    L.spairs = off;
+    off += align256(rows * (size_t)s.n * sizeof(uint2));
+    L.sd0 = off;
+    off += align256(rows * sizeof(uint32_t));
     L.nchunks = (s.n + kSelChunk - 1) / kSelChunk;
     L.cand_key = off;
     off += align256(rows * (size_t)s.n * sizeof(uint32_t));
@@ -262,7 +273,7 @@ hill_status check_sketch(const Shape& s, const int8_t* k8, const int8_t* k_exp, 
 // effect (hill_step) and the counts are cleared by the first kernel.
 hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const void* q, const void* k,
                       const Sketch& sk, float* sacc, void* ws, bool with_hist, hipStream_t st,
-                      const hill_step_events& ev)
+                      const hill_step_events& ev, const uint4* stream_prev = nullptr, int ksel = 0)
 {
     const Stamp scan{static_cast<hipEvent_t>(ev.scan_start), static_cast<hipEvent_t>(ev.scan_stop)};
     const Stamp last{nullptr, static_cast<hipEvent_t>(ev.score_stop)};
@@ -288,7 +299,7 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.s_sb = d->s_stride_b;
     a.s_sr = d->s_stride_r;
     a.zero_ptr = with_hist ? at<uint32_t>(ws, L.zero) : nullptr;
-    a.zero_words = with_hist ? L.zero_words : 0;
+    a.zero_words = with_hist ? (stream_prev ? L.zero_words_stream : L.zero_words) : 0;
     a.k8 = sk.k8;
     a.k_exp = sk.k_exp;
     a.cap = sk.cap;
@@ -310,6 +321,14 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     u.hist = hist;
     u.pin_lo = s.pin_lo;
     u.pin_hi = s.pin_hi;
+    if (stream_prev) {   // streamed selection (ATTN only): candidate pairs above the previous threshold
+        u.prev = stream_prev;
+        u.spairs = at<uint2>(ws, L.spairs);
+        u.scount = at<uint32_t>(ws, L.scount);
+        u.d0 = at<uint32_t>(ws, L.sd0);
+        u.hist2 = at<uint32_t>(ws, L.hist2);
+        u.k = ksel;
+    }
 
     if (s.mode == HILL_SCORE_ATTN) {
         a.logits = at<float>(ws, L.logits);
@@ -359,6 +378,9 @@ RefineArgs refine_args(const hill_desc* d, const Shape& s, const Layout& L, cons
     r.sel_n = at<uint32_t>(ws, L.sel_n);
     r.pin_lo = s.pin_lo;
     r.pin_hi = s.pin_hi;
+    r.spairs = at<uint2>(ws, L.spairs);
+    r.scount = at<uint32_t>(ws, L.scount);
+    r.d0 = at<uint32_t>(ws, L.sd0);
     return r;
 }
 
@@ -421,7 +443,7 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
 // then emit the indices and attend over each chunk's picks in the same kernel.
 hill_status run_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk, float* s_acc,
                      int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
-                     const hill_step_events* ev)
+                     const hill_step_events* ev, uint32_t* stream_state = nullptr)
 {
     Shape s;
     HILL_TRY(check_desc(d, &s));
@@ -440,12 +462,20 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     hipStream_t st = static_cast<hipStream_t>(stream);
     const hill_step_events none{};
     const hill_step_events& e = ev ? *ev : none;
-    HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e));
-    const RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
-    HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
-                               Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
+    uint4* state4 = reinterpret_cast<uint4*>(stream_state);
+    HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e, state4, k_sel));
+    RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
     const AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
-    HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
+    if (state4) {   // no refine pass: the select interval is empty
+        HIP_TRY(mark(e.select_start, st));
+        HIP_TRY(mark(e.select_stop, st));
+        r.state_out = state4;
+        HIP_TRY(launch_topk_emit_attn_stream(r, a, s.dtype, st));
+    } else {
+        HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
+                                   Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
+        HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
+    }
     HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, Stamp{nullptr, static_cast<hipEvent_t>(e.attn_stop)}));
     return HILL_OK;
 }
@@ -756,6 +786,17 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
                                const hill_step_events* ev)
 {
     return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
+}
+
+hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc,
+                               uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes,
+                               void* stream, const hill_step_events* ev)
+{
+    if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
+    if (d->score_mode != HILL_SCORE_ATTN)
+        return fail(HILL_ERR_UNSUPPORTED, "streamed selection needs ATTN scores (S must only grow)");
+    if (!state || ((uintptr_t)state & 15u)) return fail(HILL_ERR_INVALID_ARG, "state is NULL or not 16-byte aligned");
+    return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev, state);
 }
 
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v, const int8_t* k8,

@@ -71,7 +71,25 @@ struct UpdateArgs {
     float s2;
     uint32_t* hist;          // nullable: [B*R, kHistRow] first-digit counts (fine, coarse)
     int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) count with the largest key (lo == hi: all)
+    // streamed selection (nullable prev): candidates above the previous step's threshold
+    const uint4* prev;       // [B*R, 2] caller's state (see StreamState)
+    uint2* spairs;           // [B*R, n] (key, token) of every token whose first digit >= the bound's:
+                             //   update block u's at u * kUpdChunk
+    uint32_t* scount;        // [B*R, nup] pairs of each update block (nup = ceil(n / kUpdChunk))
+    uint32_t* d0;            // [B*R] the bound's first digit | 0x80000000 if the bound held
+    uint32_t* hist2;         // [kStreamBins, B*R, kHistRow] second-digit counts of the keys in first-digit
+                             //   bin d0 + w (w = 0: the selection's usual second-digit histogram)
+    int k;                   // this step's budget
 };
+
+// Per-row state of the streamed selection, caller-owned between steps, two
+// uint4: (threshold key lower bound, k, n, valid) and (sink tokens, recent
+// tokens, 0, 0).  The bound holds while S only grows (ATTN weights) and the
+// next step keeps k <= this k, n >= this n and the same pinned tokens.
+constexpr int kStreamStateWords = 8;
+// First-digit bins above the bound (the bound's included) whose second digits
+// the update counts: the threshold rarely moves further in one step.
+constexpr int kStreamBins = 4;
 
 struct AttnArgs {
     const uint16_t* q;
@@ -103,6 +121,12 @@ struct RefineArgs {
     int32_t* sel_list;       // [rows, n] each chunk's selected tokens in order, chunk c at c*kSelChunk
     uint32_t* sel_n;         // [rows, nchunks]
     int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) are always selected (lo == hi: all)
+    // streamed selection: the update's candidate pairs replace the refine pass
+    const uint2* spairs;     // [rows, n] update block u's pairs at u * kUpdChunk
+    const uint32_t* scount;  // [rows, nup] pairs of each update block
+    const uint32_t* d0;      // [rows] the bound's first digit | 0x80000000 if the bound held
+    // hist2 continues as [kStreamBins, rows, kHistRow]: second digits of first-digit bins d0 + w
+    uint4* state_out;        // [rows, 2] this step's threshold bound, for the next step
 };
 
 // Splits of the selected set per (sequence, KV head) for the attention pass.
@@ -188,6 +212,11 @@ hipError_t launch_topk_refine(const RefineArgs& a, int rows, hipStream_t st, Sta
 // Selects per chunk and writes the ordered indices (and values, if val).
 hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx, float* val, hipStream_t st,
                                     Stamp ts = {});
+// Streamed selection + attention: the exact threshold from the first-digit
+// histogram and the update's candidate pairs (no refine pass), then as
+// launch_topk_emit_attn; writes the next step's bound to r.state_out.
+hipError_t launch_topk_emit_attn_stream(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st,
+                                        Stamp ts = {});
 // Selects per chunk only: chunk c's tokens in order in r.sel_list, their count in r.sel_n.
 hipError_t launch_topk_emit_lists(const RefineArgs& r, int rows, hipStream_t st);
 // Selects per chunk and attends over each chunk's selected tokens: one

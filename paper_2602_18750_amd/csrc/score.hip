@@ -519,6 +519,54 @@ __device__ __forceinline__ void count_key(KeyHist& h, uint32_t key)
 
 constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 
+// First-digit bound of the streamed selection for this row: the previous
+// step's threshold key, while it is still a lower bound (same pins, k not
+// larger, n not smaller; n may only grow without pins), with 0x80000000 set;
+// else 0 (no bound: every token is a candidate).
+__device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, int row)
+{
+    const uint4 p0 = a.prev[2 * row], p1 = a.prev[2 * row + 1];
+    const bool nopins = a.pin_lo == 0 && a.pin_hi == a.n;
+    const bool ok = p0.w == 1u && (uint32_t)a.k <= p0.y && (uint32_t)a.n >= p0.z &&
+                    p1.x == (uint32_t)a.pin_lo && p1.y == (uint32_t)(a.n - a.pin_hi) &&
+                    ((uint32_t)a.n == p0.z || nopins);
+    return ok ? (p0.x >> (32 - kHistBits)) | 0x80000000u : 0u;
+}
+
+// Streamed selection: the block's tokens whose first digit reaches the bound
+// go to the block's slot of the row's (key, token) list, in token order, with
+// their count; those in the bound's first-digit bin or the next few also count
+// their second digit (the threshold seldom moves further in one step).
+static_assert(kStreamBins * kCoarseBins == 256, "one window coarse bin per update thread");
+
+__device__ __forceinline__ void stream_candidates(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
+                                                  uint32_t* scratch, uint32_t* coarse)
+{
+    const uint32_t d0 = bnd & (kHistBins - 1);
+    const uint32_t dig = key >> (32 - kHistBits);
+    const bool cand = j < a.n && dig >= d0;
+    const uint32_t wdx = dig - d0;   // window bin of the key (valid when cand)
+    const bool win = cand && (bnd >> 31) && wdx < (uint32_t)kStreamBins;
+    const int64_t rows = (int64_t)a.B * a.R;
+    if (win) {   // fine bins spread out: straight to memory; the few coarse bins are summed in LDS first
+        atomicAdd(&a.hist2[((int64_t)wdx * rows + row) * kHistRow + ((key >> 8) & (kHistBins - 1))], 1u);
+        atomicAdd(&coarse[wdx * kCoarseBins + ((key >> 14) & (kCoarseBins - 1))], 1u);
+    }
+    uint32_t tot;
+    const uint32_t pos = block_excl_scan_1b(cand ? 1u : 0u, scratch, &tot);   // its barrier completes `coarse`
+    if (bnd >> 31) {
+        const int i = threadIdx.x;   // kStreamBins * kCoarseBins == 256 bins, one per thread
+        const uint32_t c = coarse[i];
+        if (c) atomicAdd(&a.hist2[((int64_t)(i / kCoarseBins) * rows + row) * kHistRow + kHistBins + i % kCoarseBins], c);
+    }
+    if (cand) a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
+    if (threadIdx.x == 0) {
+        const int nup = (a.n + kUpdChunk - 1) / kUpdChunk;
+        a.scount[(int64_t)row * nup + blockIdx.x] = tot;
+        if (blockIdx.x == 0) a.d0[row] = bnd;
+    }
+}
+
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
 // stats kernel's output, or reduced here from the unit partials.  Thread t
 // works for head t / tph (tph = 256 / nh threads per head) and folds the
@@ -618,6 +666,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     __shared__ KeyHist kh;
     __shared__ float2 red[256];
     __shared__ float2 ms[256];
+    __shared__ uint32_t sc_scratch[4];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
@@ -626,6 +675,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool do_hist = a.hist != nullptr;
     if (do_hist) key_hist_clear(kh);
+    const uint32_t bnd = a.prev ? stream_bound(a, row) : 0u;   // loaded early, used at the end
     HeadParts hp;
     load_head_parts(a, b, h0, nh, hp);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
@@ -665,19 +715,27 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
             x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
+    // streamed selection: the window's coarse bins reuse red[] (its last reader,
+    // finish_head_stats, ended with a barrier); the barrier below orders the clear
+    uint32_t* sc_coarse = reinterpret_cast<uint32_t*>(red);
+    static_assert(sizeof(red) >= kStreamBins * kCoarseBins * sizeof(uint32_t), "coarse window fits in red[]");
+    if (a.prev) sc_coarse[tid] = 0u;
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
+    uint32_t key = 0u;
     if (j < a.n) {
         const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
-        if (do_hist) count_key(kh, select_key(s_new, j, a.pin_lo, a.pin_hi));
+        key = select_key(s_new, j, a.pin_lo, a.pin_hi);
+        if (do_hist) count_key(kh, key);
     }
     if (do_hist) {
         __syncthreads();
         hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)row * kHistRow);
     }
+    if (a.prev) stream_candidates(a, row, j, key, bnd, sc_scratch, sc_coarse);   // block-uniform
 }
 
 // Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j] (same layout).

@@ -244,10 +244,75 @@ __device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int
     }
 }
 
-template <int DT, int GC, bool ATTN>
+// Streamed selection: calls f(key, token) for every (key, token) pair the
+// update listed for the row (fast: they include every key of the threshold's
+// first-digit bin), or for every token of the row with its selection key
+// (slow: the bound did not hold).  The pairs sit in per-update-block slots;
+// groups of up to 256 slots are flattened with one block scan of their counts
+// (offsets in `offs`, 256 words of LDS) and a binary search per pair, so all
+// loads of a round are in flight together.  Every thread of the block calls it.
+template <typename F>
+__device__ __forceinline__ void for_row_pairs(const RefineArgs& r, int row, bool fast, uint32_t* offs,
+                                              uint32_t* scratch, F f)
+{
+    constexpr int kU = 8;
+    const uint32_t tid = threadIdx.x;
+    if (fast) {
+        const int nup = (r.n + kUpdChunk - 1) / kUpdChunk;
+        const uint32_t* cnt = r.scount + (int64_t)row * nup;
+        const uint2* pr = r.spairs + (int64_t)row * r.n;
+        for (int g0 = 0; g0 < nup; g0 += kThreads) {
+            const int ng = min(kThreads, nup - g0);
+            const uint32_t c = (int)tid < ng ? cnt[g0 + tid] : 0u;
+            uint32_t tot;
+            const uint32_t o = block_excl_scan<kThreads>(c, scratch, &tot);
+            offs[tid] = o;
+            __syncthreads();
+            for (uint32_t i0 = 0; i0 < tot; i0 += kThreads * kU) {
+                uint2 v[kU];
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const uint32_t i = i0 + u * kThreads + tid;
+                    v[u] = make_uint2(0u, 0u);
+                    if (i < tot) {
+                        int lo = 0, hi = ng - 1;   // the last slot whose offset is <= i
+                        while (lo < hi) {
+                            const int mid = (lo + hi + 1) >> 1;
+                            if (offs[mid] <= i) lo = mid; else hi = mid - 1;
+                        }
+                        v[u] = pr[(int64_t)(g0 + lo) * kUpdChunk + (i - offs[lo])];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < kU; ++u)
+                    if (i0 + u * kThreads + tid < tot) f(v[u].x, v[u].y);
+            }
+            __syncthreads();   // offs is rewritten by the next group
+        }
+    } else {
+        const float* srow = row_ptr(r, row);
+        for (int j0 = 0; j0 < r.n; j0 += kThreads * kU) {
+            float v[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int j = j0 + u * kThreads + (int)tid;
+                v[u] = j < r.n ? srow[j] : 0.0f;
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const int j = j0 + u * kThreads + (int)tid;
+                if (j < r.n) f(select_key(v[u], j, r.pin_lo, r.pin_hi), (uint32_t)j);
+            }
+        }
+    }
+}
+
+template <int DT, int GC, bool ATTN, bool STREAM = false>
 __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnArgs at)
 {
     __shared__ uint32_t hist3[256];
+    __shared__ typename std::conditional<STREAM, uint32_t[kHistBins], uint32_t[1]>::type hist2s;
+    __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_offs;
     __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t red[kThreads / 64];
     __shared__ uint32_t res[3];
@@ -276,15 +341,89 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     uint32_t key[kPerThread];
     bool ok[kPerThread];
     load_keys(row_ptr(r, row), c, r.n, r.pin_lo, r.pin_hi, key, ok);
+    // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
+    uint32_t prefix, need;
+    int shift;
+    bool all_eq;
+    bool fast = true;   // streamed: the update's pairs hold every key of the threshold's first-digit bin
+    if constexpr (STREAM) {
+        // first digit from the complete histogram; the second from the update's
+        // histogram of the threshold's bin when it lies in the window above the
+        // bound (the bound's own bin is loaded up front), else (and the third
+        // always) from the keys of that bin in the pair list
+        DigitHist h1, h2;
+        load_digit_hist(r.hist1 + (int64_t)row * kHistRow, h1);
+        load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
+        const uint32_t bnd = r.d0[row];
+        find_digit(h1, (uint32_t)r.k, res);
+        __syncthreads();
+        const uint32_t b1 = res[0] & (kHistBins - 1), need1 = res[1], in1 = res[2];
+        const uint32_t d0 = bnd & (kHistBins - 1);
+        fast = b1 >= d0;
+        prefix = b1;
+        need = need1;
+        shift = 20;
+        all_eq = need1 == in1;
+        if (!all_eq) {
+            uint32_t b2, need2, in2;
+            const uint32_t wdx = b1 - d0;
+            if ((bnd >> 31) && fast && wdx < (uint32_t)kStreamBins) {   // block-uniform
+                if (wdx != 0)   // the threshold left the bound's bin: that bin's counts
+                    load_digit_hist(r.hist2 + ((int64_t)wdx * at.B * r.R + row) * kHistRow, h2);   // [w][rows][bins]
+                __syncthreads();   // res of the first search has been read
+                find_digit(h2, need1, res);
+                __syncthreads();
+                b2 = res[0] & (kHistBins - 1);
+                need2 = res[1];
+                in2 = res[2];
+            } else {
+                uint32_t* h2s = hist2s;
+                for (int i = tid; i < kHistBins; i += kThreads) h2s[i] = 0u;
+                __syncthreads();
+                for_row_pairs(r, row, fast, pair_offs, scan_scratch, [b1, h2s](uint32_t kk, uint32_t) {
+                    if ((kk >> 20) == b1) atomicAdd(&h2s[(kk >> 8) & (kHistBins - 1)], 1u);
+                });
+                __syncthreads();
+                find_bin<kThreads>(h2s, kHistBins, need1, scan_scratch, res);
+                b2 = res[0] & (kHistBins - 1);
+                need2 = need1 - res[1];
+                in2 = h2s[b2];
+            }
+            prefix = (b1 << 12) | b2;
+            shift = 8;
+            need = need2;
+            all_eq = need2 == in2;
+            if (!all_eq) {   // third digit (bits 7..0)
+                uint32_t* h3 = hist3;
+                for (int i = tid; i < 256; i += kThreads) h3[i] = 0u;
+                __syncthreads();
+                const uint32_t p2 = prefix;
+                for_row_pairs(r, row, fast, pair_offs, scan_scratch, [p2, h3](uint32_t kk, uint32_t) {
+                    if ((kk >> 8) == p2) atomicAdd(&h3[kk & 0xffu], 1u);
+                });
+                __syncthreads();
+                find_bin<kThreads>(h3, 256, need2, scan_scratch, res);
+                const uint32_t b3 = res[0] & 0xffu;
+                prefix = (p2 << 8) | b3;
+                shift = 0;
+                need = need2 - res[1];
+                all_eq = need == h3[b3];
+            }
+            __syncthreads();
+        }
+        if (writer && c == 0 && tid == 0) {   // lower bound of this threshold for the next step
+            r.state_out[2 * row] = make_uint4(prefix << shift, (uint32_t)r.k, (uint32_t)r.n, 1u);
+            r.state_out[2 * row + 1] = make_uint4((uint32_t)r.pin_lo, (uint32_t)(r.n - r.pin_hi), 0u, 0u);
+        }
+    } else {
     const uint4 s1 = r.state[row];
     DigitHist h2;
     load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
     const uint32_t b1 = s1.x, need1 = s1.y, in1 = s1.z;
-
-    // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
-    uint32_t prefix = b1, need = need1;
-    int shift = 20;
-    bool all_eq = need1 == in1;
+    prefix = b1;
+    need = need1;
+    shift = 20;
+    all_eq = need1 == in1;
     if (!all_eq) {
         find_digit(h2, need1, res);
         __syncthreads();
@@ -312,6 +451,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             __syncthreads();
         }
     }
+    }
 
     bool gt[kPerThread], eq[kPerThread], sel[kPerThread];
     uint32_t neq = 0;
@@ -330,7 +470,14 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         // token index (equal keys in the chunks before, then in this chunk)
         uint32_t before_chunks = 0;
         const uint32_t pf = prefix;
-        for_candidates(r, row, 0, c, [&before_chunks, pf](uint32_t kk) { before_chunks += kk == pf; });
+        if constexpr (STREAM) {
+            const uint32_t jlim = (uint32_t)c * kSelChunk;
+            for_row_pairs(r, row, fast, pair_offs, scan_scratch, [&before_chunks, pf, jlim](uint32_t kk, uint32_t j) {
+                before_chunks += (kk == pf && j < jlim) ? 1u : 0u;
+            });
+        } else {
+            for_candidates(r, row, 0, c, [&before_chunks, pf](uint32_t kk) { before_chunks += kk == pf; });
+        }
         before_chunks = wave_sum_u32(before_chunks);
         if (lane == 0) red[tid >> 6] = before_chunks;
         __syncthreads();
@@ -443,6 +590,14 @@ void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, S
     hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at);
 }
 
+template <int DT, int GC>
+void emit_attn_stream_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
+{
+    dim3 grid(r.nchunks, at.B * (at.Hkv / at.kv_per_wg));
+    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0,
+                          r, at);
+}
+
 }  // namespace
 
 hipError_t launch_topk_hist(const float* s, int64_t s_sb, int64_t s_sr, int B, int R, int n, int pin_lo, int pin_hi,
@@ -473,6 +628,27 @@ hipError_t launch_topk_emit_indices(const RefineArgs& r, int rows, int32_t* idx,
 hipError_t launch_topk_emit_lists(const RefineArgs& r, int rows, hipStream_t st)
 {
     hipLaunchKernelGGL((topk_emit_kernel<0, 1, false>), dim3(r.nchunks, rows), dim3(kThreads), 0, st, r, AttnArgs{});
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_emit_attn_stream(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
+{
+    const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
+    if (dtype == 1) {
+        switch (gc) {
+        case 8: emit_attn_stream_launch<1, 8>(r, at, st, ts); break;
+        case 4: emit_attn_stream_launch<1, 4>(r, at, st, ts); break;
+        case 2: emit_attn_stream_launch<1, 2>(r, at, st, ts); break;
+        default: emit_attn_stream_launch<1, 1>(r, at, st, ts); break;
+        }
+    } else {
+        switch (gc) {
+        case 8: emit_attn_stream_launch<0, 8>(r, at, st, ts); break;
+        case 4: emit_attn_stream_launch<0, 4>(r, at, st, ts); break;
+        case 2: emit_attn_stream_launch<0, 2>(r, at, st, ts); break;
+        default: emit_attn_stream_launch<0, 1>(r, at, st, ts); break;
+        }
+    }
     return hipGetLastError();
 }
 

@@ -39,7 +39,7 @@ ABI_VERSION = 3   # HILL_ABI_VERSION of include/hill.h that this binding's struc
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
-           "hill_bkp_update", "hill_app_balance")
+           "hill_bkp_update", "hill_app_balance", "hill_step_streamed")
 
 
 class HillError(RuntimeError):
@@ -147,6 +147,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
         lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
         lib.hill_bkp_update.restype = ctypes.c_int
+        lib.hill_step_streamed.argtypes = [D, P, P, P, P, P, I32, P, P, P, SZ, P, ctypes.POINTER(HillStepEvents)]
+        lib.hill_step_streamed.restype = ctypes.c_int
         lib.hill_app_balance.argtypes = [ctypes.POINTER(AppParams), ctypes.POINTER(AppPlan)]
         lib.hill_app_balance.restype = ctypes.c_int
         if lib.hill_abi_version() != ABI_VERSION:
@@ -369,11 +371,18 @@ def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_sca
     return out
 
 
+def new_stream_state(B: int, R: int, device) -> torch.Tensor:
+    """Zeroed state of the streamed selection for one S buffer ([B, R] rows)."""
+    return torch.zeros((B, R, 8), dtype=torch.int32, device=device)
+
+
 def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
               sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None,
-              sketch: Optional[Sketch] = None, n_sink=0, n_recent=0):
+              sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None):
     """One decode step: S update, top-k on the new S, attention.  Returns (idx, out).
     ``n_sink`` / ``n_recent``: pinned tokens every selection keeps.
+    ``stream_state``: streamed selection (hill_step_streamed) with this state
+    (from new_stream_state, kept with S across steps).
 
     ``events``: optional HillStepEvents; then hill_step_profiled records them.
     ``sketch``: score on the int8 / int4 sketch (hill_step_sketch)."""
@@ -392,7 +401,16 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
     if ws is None:
         ws = workspace(desc, k_sel, q.device)
-    if sketch is not None:
+    if stream_state is not None:
+        if sketch is not None:
+            raise ValueError("streamed selection scores the 16-bit keys")
+        _device_check(stream_state)
+        if stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8 or not stream_state.is_contiguous():
+            raise ValueError("stream_state must be a contiguous int32 [B, R, 8] tensor")
+        _check(lib.hill_step_streamed(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), _ptr(stream_state),
+                                      int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
+                                      None if events is None else ctypes.byref(events)))
+    elif sketch is not None:
         _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
                                     _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), int(k_sel), _ptr(idx_out),
                                     _ptr(out),
@@ -514,7 +532,7 @@ class StepCall:
     repeatedly on the same buffers (only the query pointer changes per call)."""
 
     def __init__(self, q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
-                 ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0):
+                 ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None):
         lib = load_library()
         _device_check(q, k, v, s)
         self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
@@ -526,7 +544,17 @@ class StepCall:
         self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
         P = ctypes.c_void_p
         self._pre = (ctypes.byref(self.desc),)
-        if sketch is None:
+        if stream_state is not None:
+            if sketch is not None:
+                raise ValueError("streamed selection scores the 16-bit keys")
+            if stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8:
+                raise ValueError("stream_state must be an int32 [B, R, 8] tensor")
+            self._fn = None
+            self._fn_ev = lib.hill_step_streamed   # events may be NULL
+            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), P(stream_state.data_ptr()),
+                          ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
+                          P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        elif sketch is None:
             self._fn = lib.hill_step
             self._fn_ev = lib.hill_step_profiled
             self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
@@ -540,7 +568,7 @@ class StepCall:
                           ctypes.c_int32(self.k_sel),
                           P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
                           ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
-        self._keep = (k, v, s, sketch)
+        self._keep = (k, v, s, sketch, stream_state)
 
     def __call__(self, q_ptr: int, events=None):
         if self._fn is None:

@@ -327,3 +327,21 @@ def test_pinned_tokens_need_room_in_the_budget(H):
     # attention over a given list does not select: pins do not constrain it
     d.n_sink, d.n_recent = 4, 7
     assert lib.hill_gather_attn(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, 16, None) == WORKSPACE
+
+
+def test_streamed_step_validates(H):
+    lib = H.load_library()
+    d = base_desc(H)
+    need = ws_need(H, d, 10)
+    args = lambda state: (ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, state, 10, FAKE, FAKE, FAKE, need, None, None)
+    assert lib.hill_step_streamed(*args(None)) == INVALID
+    assert lib.hill_step_streamed(*args(FAKE + 4)) == INVALID                 # not 16-byte aligned
+    d.score_mode = 1                                                           # RAW: S can shrink
+    assert lib.hill_step_streamed(*args(FAKE)) == UNSUPPORTED
+    d.score_mode = 0
+    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, need, None,
+                                  None) == INVALID                            # k_sel
+    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, 16, None,
+                                  None) == WORKSPACE
+    assert lib.hill_step_streamed(None, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, need, None,
+                                  None) == INVALID

@@ -1,0 +1,121 @@
+"""GPU checks of the streamed selection (hill_step_streamed; Sec. 4.2 HIE's
+running threshold): identical results to hill_step on identical inputs, step
+after step, including the cases where the bound must not be used (first
+step, a larger budget, a longer context with pins), heavy ties, and parity
+with the oracle at full size."""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2602_18750_amd import workloads as W
+from parity import check_outputs, check_scores, check_selection
+from util import bits, dname
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_18750_amd as H
+    H.load_library()
+    yield
+
+
+def H():
+    import paper_2602_18750_amd as H
+    return H
+
+
+def say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def _pair_run(x, schedule, gran="token", sink=0, recent=0):
+    """hill_step and hill_step_streamed side by side on copies of the same S;
+    schedule: list of (n_tokens, k_sel) per step.  Asserts bit-identical S,
+    indices and outputs after every step; returns the streamed state."""
+    q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    B, Hkv, ncap = k.shape[0], k.shape[1], k.shape[2]
+    R = 1 if gran == "token" else Hkv
+    s_a = H().new_importance(B, R, ncap, DEV)
+    s_b = H().new_importance(B, R, ncap, DEV)
+    state = H().new_stream_state(B, R, DEV)
+    for t, (n, ks) in enumerate(schedule):
+        i_a, o_a = H().hill_step(q[t], k, v, s_a, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent)
+        i_b, o_b = H().hill_step(q[t], k, v, s_b, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent,
+                                 stream_state=state)
+        torch.cuda.synchronize()
+        assert torch.equal(s_a, s_b), "step %d: S differs" % t
+        assert torch.equal(i_a, i_b), "step %d: indices differ" % t
+        assert torch.equal(o_a, o_b), "step %d: outputs differ" % t
+    return state
+
+
+STREAM_CASES = [
+    # B, Hq, Hkv, n, dtype, gran, steps, k, sink, recent
+    (1, 32, 8, 8192 + 77, "bf16", "token", 6, 819, 0, 0),
+    (2, 8, 2, 3000, "fp16", "kvhead", 5, 300, 0, 0),
+    (1, 32, 32, 4096, "fp16", "token", 4, 819, 0, 0),
+    (2, 16, 4, 5000, "bf16", "token", 5, 500, 4, 64),
+    (1, 4, 4, 129, "bf16", "token", 4, 13, 0, 0),
+]
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,dt,gran,steps,k,sink,recent", STREAM_CASES)
+def test_streamed_equals_plain_step(B, Hq, Hkv, n, dt, gran, steps, k, sink, recent):
+    say("streamed vs plain", B, Hq, Hkv, n, dt, gran, steps, k, sink, recent)
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=steps, seed=n + Hq + k)
+    st = _pair_run(x, [(n, k)] * steps, gran, sink, recent)
+    s0 = st.cpu().numpy().view(np.uint32)
+    assert (s0[..., 3] == 1).all() and (s0[..., 1] == k).all() and (s0[..., 2] == n).all()
+
+
+def test_streamed_bound_changes():
+    """Budget up (bound dropped), budget down (bound kept), context growth
+    without pins (bound kept) and with pins (bound dropped)."""
+    x = W.make_random(1, 16, 4, 128, 6000, "bf16", steps=8, seed=99)
+    say("streamed bound changes, no pins")
+    _pair_run(x, [(5000, 500), (5000, 700), (5000, 400), (5200, 400), (5600, 420), (6000, 400), (6000, 400),
+                  (6000, 600)])
+    say("streamed bound changes, pins")
+    _pair_run(x, [(5000, 500), (5100, 500), (5100, 500), (5300, 520), (5300, 300), (6000, 300), (6000, 300),
+                  (6000, 300)], sink=3, recent=40)
+
+
+def test_streamed_heavy_ties():
+    """Keys drawn from 40 distinct rows: equal S values across thousands of
+    tokens, so the threshold needs all three digits and the tie ranks."""
+    x = W.make_random(1, 8, 2, 128, 4096, "bf16", steps=4, seed=5)
+    g = torch.Generator().manual_seed(3)
+    pick = torch.randint(0, 40, (4096,), generator=g)
+    x.k[:, :, :, :] = x.k[:, :, pick, :].clone()
+    say("streamed heavy ties")
+    _pair_run(x, [(4096, 1000), (4096, 1000), (4096, 2047), (4096, 2047)])
+
+
+def test_streamed_workload3_full_size_matches_oracle():
+    w = W.WORKLOADS[3].replace(steps=3)
+    say("streamed workload 3 layer 0, 3 steps")
+    x = W.make_layer(w, 0)
+    dt = dname(x.k)
+    q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    s = H().new_importance(1, 1, w.n_tokens, DEV)
+    state = H().new_stream_state(1, 1, DEV)
+    s_ref = np.zeros((1, 1, w.n_tokens))
+    for t in range(w.steps):
+        idx, out = H().hill_step(q[t], k, v, s, w.k_sel, stream_state=state)
+        s_ref = O.update(O.logits(bits(x.q[t]), bits(x.k), dt), s_ref, w.n_kv_heads, "attn", "token",
+                         1 / math.sqrt(128))
+        torch.cuda.synchronize()
+        idx_g = idx.cpu().numpy()
+        check_scores(s.cpu().numpy(), s_ref, "stream step %d S" % t)
+        check_selection(idx_g, s_ref, w.k_sel, "stream step %d sel" % t)
+        out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, "token")
+        check_outputs(out.cpu().numpy(), out_own, "stream step %d out" % t)
