@@ -2,7 +2,9 @@
 """Benchmark of one decode step of HillInfer's token-importance path on one
 MI355X: for every layer, score all cached keys against the step's query and
 update the cumulative importance, select the top-k tokens, and attend over
-them (libhill ``hill_step``).
+them (libhill ``hill_step_streamed``: the selection takes the previous step's
+threshold as a running bound, Sec. 4.2 HIE; results identical to
+``hill_step``, which is timed beside it).
 
 Default workload: the Llama-3-8B-shaped 32K-context decode -- 32 layers, GQA
 32 query / 8 KV heads, head_dim 128, batch 1, 32768 cached bf16 tokens per
@@ -17,10 +19,12 @@ Prints one JSON line:
                selection + attention): K bytes per step / step time
   roofline     the key-scan kernel (score_tiles): algorithmic bytes per
                launch / its mean duration, from start/stop timestamps that
-               the kernel's own dispatch stamps into HIP events
-               (hill_step_profiled, on the library's stream), vs 8 TB/s
+               the kernel's own dispatch stamps into HIP events (the step's
+               event argument, on the library's stream), vs 8 TB/s
   scoring_*    the scoring stage (scan + normaliser + S update)
   select_attn_us_per_layer_step   selection + gather attention, per layer-step
+  plain        the same steps through hill_step (refine pass, five launches)
+  bkp          the hot/cold pool pass after each layer's step (Sec. 4.2 BKP)
   sketch       the same steps scored on the int8 key sketch (Sec. 4.4
                asymmetric precision): step time, scan roofline on its own
                bytes, selection agreement with the 16-bit path
@@ -198,7 +202,9 @@ def run_bench(args):
             layers.append((xr, H.new_importance(w.batch, 1, w.n_tokens, dev)))
     nl_run = nl * reps
     ws = H.workspace(H.make_desc(layers[0][0].q[0], layers[0][0].k, layers[0][0].v, layers[0][1]), w.k_sel, dev)
-    calls = [H.StepCall(x.q[0], x.k, x.v, s, w.k_sel, ws=ws, stream=stream) for (x, s) in layers]
+    states = [H.new_stream_state(w.batch, 1, dev) for _ in layers]   # one running bound per S buffer
+    calls = [H.StepCall(x.q[0], x.k, x.v, s, w.k_sel, ws=ws, stream=stream, stream_state=states[L])
+             for L, (x, s) in enumerate(layers)]
     qptrs = [[x.q[t].data_ptr() for t in range(T)] for (x, _) in layers]
     torch.cuda.synchronize()
 
@@ -226,11 +232,10 @@ def run_bench(args):
     t1 = time.perf_counter()
 
     # e: scan_start, scan_stop, score_stop, select_start, select_stop, attn_stop
-    scan, score, sel, selattn, total = [], [], [], [], []
+    scan, score, selattn, total = [], [], [], []
     for e, _ in ev_sets:
         scan.append(hip.ms(e[0], e[1]))
         score.append(hip.ms(e[0], e[2]))
-        sel.append(hip.ms(e[3], e[4]))
         selattn.append(hip.ms(e[2], e[5]))
         total.append(hip.ms(e[0], e[5]))
     hip.close()
@@ -265,7 +270,8 @@ def run_bench(args):
             "workload": w.name,
             "batch": w.batch, "n_q_heads": w.n_q_heads, "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
             "n_tokens": w.n_tokens, "budget": w.budget, "k_sel": w.k_sel, "layers": nl,
-            "query_steps": T, "score_mode": "attn", "granularity": "token", "parallelism": "none (1 GPU)",
+            "query_steps": T, "score_mode": "attn", "granularity": "token", "selection": "streamed",
+            "parallelism": "none (1 GPU)",
             "kv_replicas": reps,
         },
         "roofline": {
@@ -282,12 +288,11 @@ def run_bench(args):
         "scoring_gbps": round(scoring_gbs, 1),
         "scoring_frac_hbm": round(scoring_gbs / HBM_PEAK_GBS, 4),
         "scoring_us_per_layer_step": round(score_us, 3),
-        "select_kernel_us": round(mean(sel) * 1e3, 3),
         "select_attn_us_per_layer_step": round(mean(selattn) * 1e3, 3),
         "layer_step_us_probe": round(mean(total) * 1e3, 3),
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
     }
-    res["streamed"] = bench_streamed(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
+    res["plain"] = bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_bkp:
         res["bkp"] = bench_bkp(args, w, calls, nl_run, T, qptrs, stream)
     if not args.no_sketch:
@@ -301,19 +306,15 @@ def run_bench(args):
     print(json.dumps(res), flush=True)
 
 
-def bench_streamed(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
-    """The same decode steps through hill_step_streamed (Sec. 4.2 HIE's
-    running threshold: the update lists the candidates above the previous
-    step's threshold and the selection needs no refine pass), fresh S and
-    state per layer; results are identical to hill_step's."""
+def bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
+    """The same decode steps through hill_step (the selection's refine pass,
+    five launches per layer-step), fresh S per layer."""
     import torch
     import paper_2602_18750_amd as H
 
     dev = torch.device("cuda:0")
     ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
-    states = [H.new_stream_state(w.batch, 1, dev) for _ in layers]
-    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, stream_state=states[L])
-             for L, (x, _) in enumerate(layers)]
+    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream) for L, (x, _) in enumerate(layers)]
     hip = HipEvents()
     ev_sets = []
     for _ in range(args.steps):
@@ -335,16 +336,18 @@ def bench_streamed(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     score = sum(hip.ms(e[0], e[2]) for e, _ in ev_sets) / len(ev_sets)
+    sel = sum(hip.ms(e[3], e[4]) for e, _ in ev_sets) / len(ev_sets)
     selattn = sum(hip.ms(e[2], e[5]) for e, _ in ev_sets) / len(ev_sets)
     hip.close()
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
-    del calls, ss, states
+    del calls, ss
     return {
         "ms_per_step": round(ms_step, 4),
         "value_gbps": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl / (ms_step * 1e-3) / 1e9, 2),
         "scoring_us_per_layer_step": round(score * 1e3, 3),
+        "select_kernel_us": round(sel * 1e3, 3),
         "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
-        "launches_per_layer_step": 4,
+        "launches_per_layer_step": 5,
     }
 
 

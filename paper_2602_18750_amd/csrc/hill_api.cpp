@@ -84,15 +84,16 @@ Layout layout_for(const Shape& s, int ksel)
     L.hist2 = L.hist1 + rows * kHistRow * sizeof(uint32_t);
     L.hist2x = L.hist2 + rows * kHistRow * sizeof(uint32_t);
     L.zero_words = (int64_t)((L.hist2x - L.zero) / sizeof(uint32_t));
-    const size_t zero_end = L.hist2x + rows * (kStreamBins - 1) * kHistRow * sizeof(uint32_t);
+    // the streamed selection's regions exist for ATTN scores only (the only mode it runs in)
+    const size_t zero_end = L.hist2x + (attn ? rows * (kStreamBins - 1) * kHistRow * sizeof(uint32_t) : 0);
     L.zero_words_stream = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
     off = align256(zero_end);
     L.scount = off;
-    off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * sizeof(uint32_t));
+    if (attn) off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * sizeof(uint32_t));
     L.spairs = off;
-    off += align256(rows * (size_t)s.n * sizeof(uint2));
+    if (attn) off += align256(rows * (size_t)s.n * sizeof(uint2));
     L.sd0 = off;
-    off += align256(rows * sizeof(uint32_t));
+    if (attn) off += align256(rows * sizeof(uint32_t));
     L.nchunks = (s.n + kSelChunk - 1) / kSelChunk;
     L.cand_key = off;
     off += align256(rows * (size_t)s.n * sizeof(uint32_t));
