@@ -389,8 +389,8 @@ def bench_bkp(args, w, calls, nl_run, T, qptrs, stream):
 
 def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=8):
     """The same decode steps scored on the int8 (nbits 8) or int4 (nbits 4)
-    key sketch (Sec. 4.4 asymmetric precision; selection and attention
-    unchanged).  The sketches are written once before timing, as when the
+    key sketch (Sec. 4.4 asymmetric precision; the streamed selection and the
+    attention as in the main leg).  The sketches are written once before timing, as when the
     cache is filled; in a decode loop only the appended row is sketched per
     step."""
     import torch
@@ -399,8 +399,9 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
     dev = torch.device("cuda:0")
     sks = [H.sketch_keys(x.k, bits=nbits) for (x, _) in layers]
     ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
-    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L])
-             for L, (x, _) in enumerate(layers)]
+    states = [H.new_stream_state(w.batch, 1, dev) for _ in layers]
+    calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L],
+                        stream_state=states[L]) for L, (x, _) in enumerate(layers)]
     hip = HipEvents()
     ev_sets = []
     for _ in range(args.steps):
@@ -441,7 +442,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
     torch.cuda.synchronize()
     a, b = i16.cpu(), i8.cpu()
     recall = sum(len(set(a[r, 0].tolist()) & set(b[r, 0].tolist())) for r in range(w.batch)) / (w.batch * w.k_sel)
-    del calls, sks, ss
+    del calls, sks, ss, states
     return {
         "ms_per_step": round(ms_step, 4),
         "value_gbps_of_16bit_keys": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl /

@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define HILL_ABI_VERSION 3
+#define HILL_ABI_VERSION 4
 
 typedef enum hill_status {
     HILL_OK = 0,
@@ -232,11 +232,13 @@ hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k
 
 /* hill_step whose scoring reads the sketch; selection and attention as in
  * hill_step (attention reads the 16-bit K and V of the selected tokens).
- * ev may be NULL (see hill_step_profiled). */
+ * state: NULL, or the streamed selection's state (see hill_step_streamed;
+ * ATTN only), then the selection runs streamed.  ev may be NULL (see
+ * hill_step_profiled). */
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v,
                              const int8_t* k8, const int8_t* k_exp, int64_t cap, int32_t bits, float* s,
-                             int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
-                             const hill_step_events* ev);
+                             uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
+                             size_t ws_bytes, void* stream, const hill_step_events* ev);
 
 /* Bidirectional KV Cache Pools (Sec. 4.2, HKM / BKP): the per-token hit-rate
  * table and the hot/cold pool policy, run once after each decoding step (the

@@ -801,12 +801,19 @@ hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k,
 }
 
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v, const int8_t* k8,
-                             const int8_t* k_exp, int64_t cap, int32_t bits, float* s_acc, int32_t k_sel,
-                             int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
+                             const int8_t* k_exp, int64_t cap, int32_t bits, float* s_acc, uint32_t* state,
+                             int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                              const hill_step_events* ev)
 {
     if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
-    return run_step(d, q, k, v, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
+    if (state) {
+        if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
+        if (d->score_mode != HILL_SCORE_ATTN)
+            return fail(HILL_ERR_UNSUPPORTED, "streamed selection needs ATTN scores (S must only grow)");
+        if ((uintptr_t)state & 15u) return fail(HILL_ERR_INVALID_ARG, "state is not 16-byte aligned");
+    }
+    return run_step(d, q, k, v, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev,
+                    state);
 }
 
 }  // extern "C"

@@ -35,7 +35,7 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
-ABI_VERSION = 3   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
+ABI_VERSION = 4   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
@@ -138,7 +138,7 @@ def load_library(path: str = LIB_PATH):
         lib.hill_sketch_keys.restype = ctypes.c_int
         lib.hill_score_sketch.argtypes = [D, P, P, P, I64, I32, P, P, SZ, P]
         lib.hill_score_sketch.restype = ctypes.c_int
-        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, I32, P, P, P, SZ, P,
+        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, P, I32, P, P, P, SZ, P,
                                          ctypes.POINTER(HillStepEvents)]
         lib.hill_step_sketch.restype = ctypes.c_int
         lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
@@ -402,20 +402,18 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
     if ws is None:
         ws = workspace(desc, k_sel, q.device)
     if stream_state is not None:
-        if sketch is not None:
-            raise ValueError("streamed selection scores the 16-bit keys")
         _device_check(stream_state)
         if stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8 or not stream_state.is_contiguous():
             raise ValueError("stream_state must be a contiguous int32 [B, R, 8] tensor")
+    if sketch is not None:
+        _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
+                                    _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), _ptr(stream_state),
+                                    int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
+                                    None if events is None else ctypes.byref(events)))
+    elif stream_state is not None:
         _check(lib.hill_step_streamed(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), _ptr(stream_state),
                                       int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
                                       None if events is None else ctypes.byref(events)))
-    elif sketch is not None:
-        _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
-                                    _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), int(k_sel), _ptr(idx_out),
-                                    _ptr(out),
-                                    _ptr(ws), ws.numel(), _stream_ptr(stream),
-                                    None if events is None else ctypes.byref(events)))
     elif events is None:
         _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
                              _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
@@ -544,28 +542,26 @@ class StepCall:
         self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
         P = ctypes.c_void_p
         self._pre = (ctypes.byref(self.desc),)
-        if stream_state is not None:
-            if sketch is not None:
-                raise ValueError("streamed selection scores the 16-bit keys")
-            if stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8:
-                raise ValueError("stream_state must be an int32 [B, R, 8] tensor")
+        if stream_state is not None and (stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8):
+            raise ValueError("stream_state must be an int32 [B, R, 8] tensor")
+        state_ptr = P(stream_state.data_ptr() if stream_state is not None else None)
+        if sketch is not None:
             self._fn = None
-            self._fn_ev = lib.hill_step_streamed   # events may be NULL
-            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), P(stream_state.data_ptr()),
+            self._fn_ev = lib.hill_step_sketch   # events and state may be NULL
+            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
+                          ctypes.c_int64(sketch.cap), ctypes.c_int32(sketch.bits), P(s.data_ptr()), state_ptr,
                           ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
                           P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
-        elif sketch is None:
+        elif stream_state is not None:
+            self._fn = None
+            self._fn_ev = lib.hill_step_streamed   # events may be NULL
+            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), state_ptr,
+                          ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
+                          P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        else:
             self._fn = lib.hill_step
             self._fn_ev = lib.hill_step_profiled
             self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), ctypes.c_int32(self.k_sel),
-                          P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
-                          ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
-        else:
-            self._fn = None
-            self._fn_ev = lib.hill_step_sketch   # events may be NULL
-            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
-                          ctypes.c_int64(sketch.cap), ctypes.c_int32(sketch.bits), P(s.data_ptr()),
-                          ctypes.c_int32(self.k_sel),
                           P(self.idx.data_ptr()), P(self.out.data_ptr()), P(self.ws.data_ptr()),
                           ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
         self._keep = (k, v, s, sketch, stream_state)

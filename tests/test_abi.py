@@ -206,19 +206,26 @@ def test_sketch_entry_points_validate(H):
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, 996, bits, FAKE, FAKE, need, None) == INVALID
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 16,
                                      None) == WORKSPACE
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, bits, FAKE, 10, FAKE,
-                                    FAKE, FAKE, need, None, None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, bits, FAKE, 10, FAKE,
-                                    FAKE, FAKE, need, None, None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, 0, FAKE,
-                                    FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, bits, FAKE, None, 10,
+                                    FAKE, FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, bits, FAKE, None, 10,
+                                    FAKE, FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 0,
+                                    FAKE, FAKE, FAKE, need, None, None) == INVALID
+        # a streamed state must be 16-byte aligned, and needs ATTN scores
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE + 4, 10,
+                                    FAKE, FAKE, FAKE, need, None, None) == INVALID
+        d.score_mode = 1
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 10,
+                                    FAKE, FAKE, FAKE, need, None, None) == UNSUPPORTED
+        d.score_mode = 0
     # only 8 and 4 bits exist
     for bits in (0, 2, 6, 16):
         assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, 0, 10, None) == INVALID
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, need,
                                      None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, 10, FAKE,
-                                    FAKE, FAKE, need, None, None) == INVALID
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 10,
+                                    FAKE, FAKE, FAKE, need, None, None) == INVALID
     assert b"bits" in lib.hill_last_error()
 
 

@@ -119,3 +119,21 @@ def test_streamed_workload3_full_size_matches_oracle():
         check_selection(idx_g, s_ref, w.k_sel, "stream step %d sel" % t)
         out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, "token")
         check_outputs(out.cpu().numpy(), out_own, "stream step %d out" % t)
+
+
+@pytest.mark.parametrize("nbits", [8, 4])
+def test_streamed_sketch_equals_plain_sketch_step(nbits):
+    """Scoring on the int8 / int4 sketch with the streamed selection gives the
+    same S, indices and outputs as with the refine-based one."""
+    x = W.make_random(1, 32, 8, 128, 6000, "bf16", steps=5, seed=31 + nbits)
+    say("streamed sketch", nbits)
+    q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    sk = H().sketch_keys(k, bits=nbits)
+    s_a = H().new_importance(1, 1, 6000, DEV)
+    s_b = H().new_importance(1, 1, 6000, DEV)
+    state = H().new_stream_state(1, 1, DEV)
+    for t in range(5):
+        i_a, o_a = H().hill_step(q[t], k, v, s_a, 600, sketch=sk)
+        i_b, o_b = H().hill_step(q[t], k, v, s_b, 600, sketch=sk, stream_state=state)
+        torch.cuda.synchronize()
+        assert torch.equal(s_a, s_b) and torch.equal(i_a, i_b) and torch.equal(o_a, o_b), "step %d" % t
