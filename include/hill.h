@@ -192,9 +192,11 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
  * state: uint32 [B, R, 8], 16-byte aligned, caller-owned, one per S buffer;
  * zero it at the start of a sequence and whenever S is changed outside these
  * calls.  Each call reads the bound and writes the next one.  The bound is
- * used only while it holds (same pins, k_sel not larger and n_tokens not
- * smaller than at the previous call; n_tokens may grow only without pins);
- * otherwise, and on the first call, the selection reads the whole row
+ * used only while it holds: the same pins, n_tokens not smaller than at the
+ * previous call (growing only without pins), and k_sel at most the number of
+ * tokens whose first radix digit reached the previous threshold's (usually
+ * k_sel plus a few hundred, so a budget that grows with the context keeps
+ * it); otherwise, and on the first call, the selection reads the whole row
  * instead, which is exact but slower.  ATTN score mode only
  * (HILL_ERR_UNSUPPORTED otherwise).  ev: as hill_step_profiled (the select
  * interval is empty). */

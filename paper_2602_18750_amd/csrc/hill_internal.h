@@ -83,9 +83,10 @@ struct UpdateArgs {
 };
 
 // Per-row state of the streamed selection, caller-owned between steps, two
-// uint4: (threshold key lower bound, k, n, valid) and (sink tokens, recent
-// tokens, 0, 0).  The bound holds while S only grows (ATTN weights) and the
-// next step keeps k <= this k, n >= this n and the same pinned tokens.
+// uint4: (threshold key, keys whose first digit reached the threshold's, n,
+// valid) and (sink tokens, recent tokens, 0, 0).  The threshold's first digit
+// bounds the next step's from below while S only grows (ATTN weights), the
+// next budget is at most that count, n does not shrink and the pins stay.
 constexpr int kStreamStateWords = 8;
 // First-digit bins above the bound (the bound's included) whose second digits
 // the update counts: the threshold rarely moves further in one step.

@@ -519,10 +519,11 @@ __device__ __forceinline__ void count_key(KeyHist& h, uint32_t key)
 
 constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 
-// First-digit bound of the streamed selection for this row: the previous
-// step's threshold key, while it is still a lower bound (same pins, k not
-// larger, n not smaller; n may only grow without pins), with 0x80000000 set;
-// else 0 (no bound: every token is a candidate).
+// First-digit bound of the streamed selection for this row: the first digit
+// of the previous step's threshold, while the keys at or above that bin then
+// were at least this step's k (S only grows), the pins are the same and n did
+// not shrink (n may only grow without pins); with 0x80000000 set.  Else 0
+// (no bound: every token is a candidate).
 __device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, int row)
 {
     const uint4 p0 = a.prev[2 * row], p1 = a.prev[2 * row + 1];

@@ -411,8 +411,11 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             }
             __syncthreads();
         }
-        if (writer && c == 0 && tid == 0) {   // lower bound of this threshold for the next step
-            r.state_out[2 * row] = make_uint4(prefix << shift, (uint32_t)r.k, (uint32_t)r.n, 1u);
+        if (writer && c == 0 && tid == 0) {
+            // bound for the next step: the threshold's first-digit bin, with the number of keys in it or
+            // above (S only grows, so any budget up to that number keeps its threshold in or above the bin)
+            const uint32_t at_or_above = (uint32_t)r.k - need1 + in1;
+            r.state_out[2 * row] = make_uint4(prefix << shift, at_or_above, (uint32_t)r.n, 1u);
             r.state_out[2 * row + 1] = make_uint4((uint32_t)r.pin_lo, (uint32_t)(r.n - r.pin_hi), 0u, 0u);
         }
     } else {

@@ -55,7 +55,25 @@ def _pair_run(x, schedule, gran="token", sink=0, recent=0):
         assert torch.equal(s_a, s_b), "step %d: S differs" % t
         assert torch.equal(i_a, i_b), "step %d: indices differ" % t
         assert torch.equal(o_a, o_b), "step %d: outputs differ" % t
+    _check_state(state, s_b, n, ks, sink, recent)
     return state
+
+
+def _check_state(state, s, n, k, sink, recent):
+    """The state written by the last step: valid, this n, the pins, and the
+    number of tokens whose first radix digit (top 12 bits of the order key;
+    pinned tokens take the largest key) reaches the threshold's: at least k."""
+    st = state.cpu().numpy().view(np.uint32)
+    sv = s.cpu().numpy()[..., :n]
+    key = sv.view(np.uint32) | np.uint32(0x80000000)   # S >= 0: order key of a non-negative float
+    j = np.arange(n)
+    key[..., (j < sink) | (j >= n - recent)] = 0xFFFFFFFF
+    digit = (key >> 20).astype(np.int64)
+    thr = (st[..., 0] >> 20).astype(np.int64)
+    count = (digit >= thr[..., None]).sum(-1)
+    assert (st[..., 3] == 1).all() and (st[..., 2] == n).all()
+    assert (st[..., 4] == sink).all() and (st[..., 5] == recent).all()
+    assert (st[..., 1] == count).all() and (count >= k).all()
 
 
 STREAM_CASES = [
@@ -72,9 +90,7 @@ STREAM_CASES = [
 def test_streamed_equals_plain_step(B, Hq, Hkv, n, dt, gran, steps, k, sink, recent):
     say("streamed vs plain", B, Hq, Hkv, n, dt, gran, steps, k, sink, recent)
     x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=steps, seed=n + Hq + k)
-    st = _pair_run(x, [(n, k)] * steps, gran, sink, recent)
-    s0 = st.cpu().numpy().view(np.uint32)
-    assert (s0[..., 3] == 1).all() and (s0[..., 1] == k).all() and (s0[..., 2] == n).all()
+    _pair_run(x, [(n, k)] * steps, gran, sink, recent)
 
 
 def test_streamed_bound_changes():
@@ -137,3 +153,13 @@ def test_streamed_sketch_equals_plain_sketch_step(nbits):
         i_b, o_b = H().hill_step(q[t], k, v, s_b, 600, sketch=sk, stream_state=state)
         torch.cuda.synchronize()
         assert torch.equal(s_a, s_b) and torch.equal(i_a, i_b) and torch.equal(o_a, o_b), "step %d" % t
+
+
+def test_streamed_growing_context_keeps_the_bound():
+    """n grows by one token per step and k = floor(0.1 n) grows with it (the
+    decode loop's case): results equal hill_step's, and after the first steps
+    the state keeps a valid bound (its count covers the next k)."""
+    x = W.make_random(1, 16, 4, 128, 4200, "bf16", steps=40, seed=8)
+    sched = [(4000 + 5 * t, O.budget_k(4000 + 5 * t, 0.1)) for t in range(40)]
+    say("streamed growing context")
+    _pair_run(x, sched)
