@@ -16,6 +16,9 @@
 //      (2l, 2l+1) of the V row (one 4-byte load per lane: a whole 256-byte
 //      row per wave instruction) and accumulates weight * V for every head.
 //      The V loads of the first batch are issued before phase A.
+// When the scan's logits of the same keys are at hand (the fused step over
+// the 16-bit cache), the caller puts them in LDS with the list and phase A
+// is skipped: only V rows are read (attn_block_logits).
 // The four waves' outputs are added in LDS at the end, and one partial
 // (m, l, o[D]) per head is written to a slot of the partial buffer; partials
 // of all slots are merged by merge_head().
@@ -163,6 +166,59 @@ __device__ __forceinline__ void values_rows(const uint32_t (&vr)[kVBatch], int w
     }
 }
 
+// Softmax step of a block of cnt entries whose logits are in sh.p: per head
+// (one wave each), block maximum -> running maximum, exp2 weights in place
+// and their sum; ends with a barrier.
+template <int GC>
+__device__ __forceinline__ void softmax_block(int cnt, AttnLds<GC>& sh)
+{
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    for (int hh = w; hh < GC; hh += 4) {
+        float mx = -INFINITY;
+        for (int t = lane; t < cnt; t += 64) mx = fmaxf(mx, sh.p[t][hh]);
+        mx = wave_max(mx);
+        const float m_old = sh.mrun[hh];
+        const float m_new = fmaxf(m_old, mx);
+        float ls = 0.0f;
+        for (int t = lane; t < cnt; t += 64) {
+            const float e = exp2f(sh.p[t][hh] - m_new);
+            sh.p[t][hh] = e;
+            ls += e;
+        }
+        ls = wave_sum(ls);
+        if (lane == 0) {
+            const float al = m_old == -INFINITY ? 0.0f : exp2f(m_old - m_new);
+            sh.alpha[hh] = al;
+            sh.lrun[hh] = sh.lrun[hh] * al + ls;
+            sh.mrun[hh] = m_new;
+        }
+    }
+    __syncthreads();
+}
+
+// weight * V over this wave's entries w, w+4, ... of the block: the first 16
+// (and, when `two`, 32) from the rows already loaded, the rest loaded here.
+template <int DT, int GC>
+__device__ __forceinline__ void values_block(const AttnArgs& a, const uint16_t* vb, int w, int cnt, int nmine, bool two,
+                                             const uint32_t (&vr)[kVBatch], const uint32_t (&vr2)[kVBatch],
+                                             AttnAcc<GC>& acc, AttnLds<GC>& sh)
+{
+#pragma unroll
+    for (int hh = 0; hh < GC; ++hh) {
+        const float al = sh.alpha[hh];
+        acc.o[hh][0] *= al;
+        acc.o[hh][1] *= al;
+    }
+    values_rows<DT, GC>(vr, w, 0, nmine, cnt, sh.p, acc);
+    if (two) values_rows<DT, GC>(vr2, w, kVBatch, nmine, cnt, sh.p, acc);
+    for (int i0 = 2 * kVBatch; i0 < nmine; i0 += kVBatch) {   // lists longer than 128
+        uint32_t vx[kVBatch];
+        load_v_rows(a, vb, sh.tok, w + 4 * i0, cnt, vx);
+        values_rows<DT, GC>(vx, w, i0, nmine, cnt, sh.p, acc);
+    }
+}
+
 // Folds list entries [0, cnt) of sh.tok (1 <= cnt <= kAttnBlock, written and
 // made visible by a barrier before the call) into the running state.  Every
 // thread of the workgroup must call this.  The K rows are issued before the
@@ -199,43 +255,27 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
     }
     __syncthreads();
 
-    // B: per head, block maximum -> running maximum, weights and their sum
-    for (int hh = w; hh < GC; hh += 4) {
-        float mx = -INFINITY;
-        for (int t = lane; t < cnt; t += 64) mx = fmaxf(mx, sh.p[t][hh]);
-        mx = wave_max(mx);
-        const float m_old = sh.mrun[hh];
-        const float m_new = fmaxf(m_old, mx);
-        float ls = 0.0f;
-        for (int t = lane; t < cnt; t += 64) {
-            const float e = exp2f(sh.p[t][hh] - m_new);
-            sh.p[t][hh] = e;
-            ls += e;
-        }
-        ls = wave_sum(ls);
-        if (lane == 0) {
-            const float al = m_old == -INFINITY ? 0.0f : exp2f(m_old - m_new);
-            sh.alpha[hh] = al;
-            sh.lrun[hh] = sh.lrun[hh] * al + ls;
-            sh.mrun[hh] = m_new;
-        }
-    }
-    __syncthreads();
+    softmax_block<GC>(cnt, sh);
+    values_block<DT, GC>(a, vb, w, cnt, nmine, two, vr, vr2, acc, sh);
+}
 
-    // C: weight * V over this wave's entries w, w+4, ...
-#pragma unroll
-    for (int hh = 0; hh < GC; ++hh) {
-        const float al = sh.alpha[hh];
-        acc.o[hh][0] *= al;
-        acc.o[hh][1] *= al;
-    }
-    values_rows<DT, GC>(vr, w, 0, nmine, cnt, sh.p, acc);
-    if (two) values_rows<DT, GC>(vr2, w, kVBatch, nmine, cnt, sh.p, acc);
-    for (int i0 = 2 * kVBatch; i0 < nmine; i0 += kVBatch) {   // lists longer than 128
-        uint32_t vx[kVBatch];
-        load_v_rows(a, vb, sh.tok, w + 4 * i0, cnt, vx);
-        values_rows<DT, GC>(vx, w, i0, nmine, cnt, sh.p, acc);
-    }
+// attn_block with the logits already in sh.p (scaled by s2, written with
+// sh.tok before the barrier that precedes the call, after attn_begin): only
+// the V rows are read, and their loads are in flight during the softmax.
+template <int DT, int GC>
+__device__ __forceinline__ void attn_block_logits(const AttnArgs& a, int b, int g, int cnt, AttnAcc<GC>& acc,
+                                                  AttnLds<GC>& sh)
+{
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
+    const int nmine = cnt > w ? (cnt - w + 3) / 4 : 0;
+    const bool two = cnt > 4 * kVBatch;   // block-uniform
+    uint32_t vr[kVBatch], vr2[kVBatch];
+    load_v_rows(a, vb, sh.tok, w, cnt, vr);
+    if (two) load_v_rows(a, vb, sh.tok, w + 4 * kVBatch, cnt, vr2);
+    softmax_block<GC>(cnt, sh);
+    values_block<DT, GC>(a, vb, w, cnt, nmine, two, vr, vr2, acc, sh);
 }
 
 // Adds the four waves' outputs and writes the partial (m, l, o[D]) of heads

@@ -466,7 +466,11 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     uint4* state4 = reinterpret_cast<uint4*>(stream_state);
     HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e, state4, k_sel));
     RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
-    const AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
+    AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
+    if (s.mode == HILL_SCORE_ATTN && !sk.k8) {   // the scan's logits are those of the 16-bit keys: reused
+        a.logits = at<float>(ws, L.logits);
+        a.ld = s.ld;
+    }
     if (state4) {   // no refine pass: the select interval is empty
         HIP_TRY(mark(e.select_start, st));
         HIP_TRY(mark(e.select_stop, st));

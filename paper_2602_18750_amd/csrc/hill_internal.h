@@ -103,6 +103,8 @@ struct AttnArgs {
     int B, Hq, Hkv, G, R, n, ksel, nsplit, per_split;
     int kv_per_wg;           // fused select+attend, token rows: KV heads per workgroup (divides Hkv)
     float s2;
+    const float* logits;     // fused select+attend: the scan's q.k logits [B,Hq,ld] of these keys, or NULL
+    int64_t ld;
     float* part_o;           // [B,Hq,nsplit,D]
     float2* part_ml;         // [B,Hq,nsplit] (max, sum) in the exp2 domain
     float* out;              // [B,Hq,D]

@@ -307,7 +307,21 @@ __device__ __forceinline__ void for_row_pairs(const RefineArgs& r, int row, bool
     }
 }
 
-template <int DT, int GC, bool ATTN, bool STREAM = false>
+// The scan's logits of heads h0 .. h0+GC of this thread's two tokens of
+// chunk c (rows of ld floats, ld a multiple of 4; tokens past the row's end
+// read the padded tail or an earlier pair and are never selected).
+template <int GC>
+__device__ __forceinline__ void load_chunk_logits(const AttnArgs& at, int b, int h0, int c, float2 (&lg)[GC])
+{
+    const int j = min(c * kSelChunk + (int)threadIdx.x * kPerThread, (int)at.ld - 2);
+    const float* p = at.logits + ((int64_t)b * at.Hq + h0) * at.ld + j;
+#pragma unroll
+    for (int hh = 0; hh < GC; ++hh) lg[hh] = *reinterpret_cast<const float2*>(p + hh * at.ld);
+}
+
+// With LG the attention takes its logits from the scan (at.logits) instead
+// of recomputing q.k from gathered K rows.
+template <int DT, int GC, bool ATTN, bool STREAM = false, bool LG = false>
 __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnArgs at)
 {
     __shared__ uint32_t hist3[256];
@@ -336,11 +350,13 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
 
     // independent loads first: queries, this chunk's keys, the row's state and
     // second-digit histogram
-    uint4 qv[ATTN ? GC : 1];
-    if constexpr (ATTN) load_queries<GC>(at, b, g, 0, qv);
+    uint4 qv[ATTN && !LG ? GC : 1];
+    if constexpr (ATTN && !LG) load_queries<GC>(at, b, g, 0, qv);
     uint32_t key[kPerThread];
     bool ok[kPerThread];
     load_keys(row_ptr(r, row), c, r.n, r.pin_lo, r.pin_hi, key, ok);
+    float2 lgv[LG ? GC : 1];
+    if constexpr (LG) load_chunk_logits<GC>(at, b, g * at.G, c, lgv);
     // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
     uint32_t prefix, need;
     int shift;
@@ -504,24 +520,45 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     if constexpr (ATTN) {
         // attention of the group's heads over the chunk's selected tokens
         // (one partial per head in slot c), then the list is stored
+        AttnAcc<GC> acc;
+        attn_begin<GC>(acc, sh);
         uint32_t p = pos;
 #pragma unroll
-        for (int e = 0; e < kPerThread; ++e)
-            if (sel[e]) sh.tok[p++] = j0 + e;
-        __syncthreads();
-        {   // the first head chunk with the queries loaded at the start
-            AttnAcc<GC> acc;
-            attn_begin<GC>(acc, sh);
-            if (tot) attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
-            attn_finish<GC>(at, b, g, 0, acc, c, r.nchunks, sh);
+        for (int e = 0; e < kPerThread; ++e) {
+            if (sel[e]) {
+                sh.tok[p] = j0 + e;
+                if constexpr (LG) {
+#pragma unroll
+                    for (int hh = 0; hh < GC; ++hh) sh.p[p][hh] = at.s2 * (e == 0 ? lgv[hh].x : lgv[hh].y);
+                }
+                ++p;
+            }
         }
+        __syncthreads();
+        // the first head chunk with the queries (or logits) loaded at the start
+        if (tot) {
+            if constexpr (LG) attn_block_logits<DT, GC>(at, b, g, (int)tot, acc, sh);
+            else attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
+        }
+        attn_finish<GC>(at, b, g, 0, acc, c, r.nchunks, sh);
         for (int i = 1; i < ng * (at.G / GC); ++i) {   // further head chunks and KV heads
             const int gg = g + i / (at.G / GC), hc = (i % (at.G / GC)) * GC;
-            load_queries<GC>(at, b, gg, hc, qv);
-            AttnAcc<GC> acc;
-            attn_begin<GC>(acc, sh);
-            if (tot) attn_block<DT, GC>(at, b, gg, qv, (int)tot, acc, sh);
-            attn_finish<GC>(at, b, gg, hc, acc, c, r.nchunks, sh);
+            AttnAcc<GC> acc2;
+            attn_begin<GC>(acc2, sh);
+            if constexpr (LG) {   // the list's logits of these heads
+                const float* lp = at.logits + ((int64_t)b * at.Hq + gg * at.G + hc) * at.ld;
+                for (uint32_t t = tid; t < tot; t += kThreads) {
+                    const int j = sh.tok[t];
+#pragma unroll
+                    for (int hh = 0; hh < GC; ++hh) sh.p[t][hh] = at.s2 * lp[hh * at.ld + j];
+                }
+                __syncthreads();
+                if (tot) attn_block_logits<DT, GC>(at, b, gg, (int)tot, acc2, sh);
+            } else {
+                load_queries<GC>(at, b, gg, hc, qv);
+                if (tot) attn_block<DT, GC>(at, b, gg, qv, (int)tot, acc2, sh);
+            }
+            attn_finish<GC>(at, b, gg, hc, acc2, c, r.nchunks, sh);
         }
         if (writer) {
             for (uint32_t i = tid; i < tot; i += kThreads) list[i] = sh.tok[i];
@@ -586,19 +623,37 @@ __global__ __launch_bounds__(kThreads) void merge_write_kernel(RefineArgs r, Att
     }
 }
 
-template <int DT, int GC>
+template <int DT, int GC, bool STREAM, bool LG>
 void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
 {
     dim3 grid(r.nchunks, at.B * (at.Hkv / at.kv_per_wg));
-    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at);
+    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true, STREAM, LG>), grid, dim3(kThreads), 0, st, ts.start, ts.stop,
+                          0, r, at);
 }
 
-template <int DT, int GC>
-void emit_attn_stream_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
+template <int DT, bool STREAM, bool LG>
+void emit_attn_gc(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
 {
-    dim3 grid(r.nchunks, at.B * (at.Hkv / at.kv_per_wg));
-    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true, true>), grid, dim3(kThreads), 0, st, ts.start, ts.stop, 0,
-                          r, at);
+    const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
+    switch (gc) {
+    case 8: emit_attn_launch<DT, 8, STREAM, LG>(r, at, st, ts); break;
+    case 4: emit_attn_launch<DT, 4, STREAM, LG>(r, at, st, ts); break;
+    case 2: emit_attn_launch<DT, 2, STREAM, LG>(r, at, st, ts); break;
+    default: emit_attn_launch<DT, 1, STREAM, LG>(r, at, st, ts); break;
+    }
+}
+
+template <bool STREAM>
+hipError_t emit_attn_any(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
+{
+    if (dtype == 1) {
+        if (at.logits) emit_attn_gc<1, STREAM, true>(r, at, st, ts);
+        else emit_attn_gc<1, STREAM, false>(r, at, st, ts);
+    } else {
+        if (at.logits) emit_attn_gc<0, STREAM, true>(r, at, st, ts);
+        else emit_attn_gc<0, STREAM, false>(r, at, st, ts);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -636,44 +691,12 @@ hipError_t launch_topk_emit_lists(const RefineArgs& r, int rows, hipStream_t st)
 
 hipError_t launch_topk_emit_attn_stream(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
 {
-    const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
-    if (dtype == 1) {
-        switch (gc) {
-        case 8: emit_attn_stream_launch<1, 8>(r, at, st, ts); break;
-        case 4: emit_attn_stream_launch<1, 4>(r, at, st, ts); break;
-        case 2: emit_attn_stream_launch<1, 2>(r, at, st, ts); break;
-        default: emit_attn_stream_launch<1, 1>(r, at, st, ts); break;
-        }
-    } else {
-        switch (gc) {
-        case 8: emit_attn_stream_launch<0, 8>(r, at, st, ts); break;
-        case 4: emit_attn_stream_launch<0, 4>(r, at, st, ts); break;
-        case 2: emit_attn_stream_launch<0, 2>(r, at, st, ts); break;
-        default: emit_attn_stream_launch<0, 1>(r, at, st, ts); break;
-        }
-    }
-    return hipGetLastError();
+    return emit_attn_any<true>(r, at, dtype, st, ts);
 }
 
 hipError_t launch_topk_emit_attn(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
 {
-    const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
-    if (dtype == 1) {
-        switch (gc) {
-        case 8: emit_attn_launch<1, 8>(r, at, st, ts); break;
-        case 4: emit_attn_launch<1, 4>(r, at, st, ts); break;
-        case 2: emit_attn_launch<1, 2>(r, at, st, ts); break;
-        default: emit_attn_launch<1, 1>(r, at, st, ts); break;
-        }
-    } else {
-        switch (gc) {
-        case 8: emit_attn_launch<0, 8>(r, at, st, ts); break;
-        case 4: emit_attn_launch<0, 4>(r, at, st, ts); break;
-        case 2: emit_attn_launch<0, 2>(r, at, st, ts); break;
-        default: emit_attn_launch<0, 1>(r, at, st, ts); break;
-        }
-    }
-    return hipGetLastError();
+    return emit_attn_any<false>(r, at, dtype, st, ts);
 }
 
 hipError_t launch_merge_write(const RefineArgs& r, const AttnArgs& at, int32_t* idx, int rows, hipStream_t st,

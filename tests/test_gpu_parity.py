@@ -387,8 +387,9 @@ def test_step_equals_score_topk_attn_in_sequence(mode, gran):
     torch.cuda.synchronize()
     assert torch.equal(s1.cpu(), s2.cpu())
     assert torch.equal(i1.cpu(), i2.cpu())
-    # hill_step attends per 1024-token chunk, hill_gather_attn per split of the
-    # index list: same value, different fp32 summation order
+    # hill_step attends per 512-token chunk with the scan's logits (ATTN),
+    # hill_gather_attn per split of the index list with its own q.k: same
+    # value, different fp32 summation order
     o1, o2 = o1.cpu().double(), o2.cpu().double()
     assert ((o1 - o2).abs().amax(-1) <= 1e-5 * o2.abs().amax(-1)).all()
 
