@@ -69,7 +69,8 @@ struct UpdateArgs {
     int64_t s_sb, s_sr;
     int B, Hq, Hkv, G, R, n;
     float s2;
-    uint32_t* hist;          // nullable: [B*R, kHistRow] first-digit counts (fine, coarse)
+    uint32_t* hist;          // nullable: [B*R, kHistRow] first-digit counts (fine, coarse); with a
+                             // streamed bound only keys in the bound's bin or above are counted
     int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) count with the largest key (lo == hi: all)
     // streamed selection (nullable prev): candidates above the previous step's threshold
     const uint4* prev;       // [B*R, 2] caller's state (see StreamState)

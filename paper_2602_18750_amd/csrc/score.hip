@@ -677,6 +677,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const bool do_hist = a.hist != nullptr;
     if (do_hist) key_hist_clear(kh);
     const uint32_t bnd = a.prev ? stream_bound(a, row) : 0u;   // loaded early, used at the end
+    const uint32_t hist_lo = (bnd >> 31) ? (bnd & (kHistBins - 1)) : 0u;
     HeadParts hp;
     load_head_parts(a, b, h0, nh, hp);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
@@ -730,7 +731,9 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
         const float s_new = s_old + tot;
         srow[j] = s_new;
         key = select_key(s_new, j, a.pin_lo, a.pin_hi);
-        if (do_hist) count_key(kh, key);
+        // with a streamed bound the k-th key lies in the bound's first-digit bin
+        // or above, so only those bins are counted (most keys lie below it)
+        if (do_hist && (key >> (32 - kHistBits)) >= hist_lo) count_key(kh, key);
     }
     if (do_hist) {
         __syncthreads();

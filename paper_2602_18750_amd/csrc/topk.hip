@@ -363,7 +363,8 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     bool all_eq;
     bool fast = true;   // streamed: the update's pairs hold every key of the threshold's first-digit bin
     if constexpr (STREAM) {
-        // first digit from the complete histogram; the second from the update's
+        // first digit from the update's histogram (complete, or with a valid
+        // bound complete from the bound's bin upward); the second from the update's
         // histogram of the threshold's bin when it lies in the window above the
         // bound (the bound's own bin is loaded up front), else (and the third
         // always) from the keys of that bin in the pair list
