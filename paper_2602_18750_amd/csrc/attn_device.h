@@ -318,15 +318,17 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
     const float2* ml = a.part_ml + bh * nslots;
     const float* po = a.part_o + bh * nslots * kHeadDim + d;
 
-    // the first kPre of this thread's slots: loads in flight during the reductions
+    // the first kPre of this thread's slots: loads in flight during the reductions;
+    // slot tid's (m, l) is kept for both passes over the slots
     float x[kPre];
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
         const int s = grp + i * NG;
         x[i] = s < nslots ? po[(int64_t)s * kHeadDim] : 0.0f;
     }
-    float mx = -INFINITY;
-    for (int s = tid; s < nslots; s += NT) {
+    const float2 v0 = tid < nslots ? ml[tid] : make_float2(-INFINITY, 0.0f);
+    float mx = v0.y > 0.0f ? v0.x : -INFINITY;
+    for (int s = tid + NT; s < nslots; s += NT) {
         const float2 v = ml[s];
         mx = fmaxf(mx, v.y > 0.0f ? v.x : -INFINITY);
     }
@@ -338,7 +340,12 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
     for (int i = 1; i < NW; ++i) mx = fmaxf(mx, red[i]);
     __syncthreads();
     float lsum = 0.0f;
-    for (int s = tid; s < nslots; s += NT) {
+    if (tid < nslots) {
+        const float ws = v0.y > 0.0f ? exp2f(v0.x - mx) : 0.0f;
+        wsl[tid] = ws;
+        lsum = ws * v0.y;
+    }
+    for (int s = tid + NT; s < nslots; s += NT) {
         const float2 v = ml[s];
         const float ws = v.y > 0.0f ? exp2f(v.x - mx) : 0.0f;
         wsl[s] = ws;
