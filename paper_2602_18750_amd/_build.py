@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libhill.so")
 # per-kernel registers, scratch and occupancy as the compiler reports them
 RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
-SOURCES = ["hill_api.cpp", "score.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip", "bkp.hip"]
+SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip", "bkp.hip"]
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
