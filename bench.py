@@ -178,6 +178,8 @@ def run_bench(args):
     w = W.WORKLOADS[int(args.workload)]
     if args.layers:
         w = w.replace(layers=args.layers)
+    if args.n_tokens:
+        w = w.replace(n_tokens=args.n_tokens, name="%s-n%d" % (w.name, args.n_tokens))
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -627,6 +629,38 @@ def _short(name: str) -> str:
     return "".join(out)[:80]
 
 
+def _steady_state(path: str, directory: str):
+    """Median durations of the streamed decode step's four kernels (scan over
+    the 16-bit keys, update, streamed select+attend, merge), taken from the
+    launches in that order in a kernel trace, without the first third of them
+    (the first steps of every fresh S run without a bound)."""
+    import csv
+    import statistics
+    with open(path) as f:
+        rows = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
+    names = [_short(r["Kernel_Name"]) for r in rows]
+    seqs, i = [], 0
+    while i + 3 < len(rows):
+        n = names[i:i + 4]
+        if (n[0].startswith("hill::score_tiles_kernel") and "KeysF16" in n[0] and n[1] == "hill::update_attn_kernel"
+                and n[2].startswith("hill::topk_emit_kernel") and n[2].count("true") >= 2
+                and n[3] == "hill::merge_write_kernel"):
+            seqs.append(rows[i:i + 4])
+            i += 4
+        else:
+            i += 1
+    if not seqs:
+        return []
+    steady = seqs[len(seqs) // 3:]
+    out = ["## %s: streamed decode step, steady state" % os.path.relpath(path, directory),
+           "%d layer-steps in the trace, the last %d used (median µs per launch)" % (len(seqs), len(steady)),
+           "", "| kernel | median us |", "|---|---|"]
+    for k in range(4):
+        d = [(int(sq[k]["End_Timestamp"]) - int(sq[k]["Start_Timestamp"])) / 1e3 for sq in steady]
+        out.append("| %s | %.2f |" % (_short(steady[0][k]["Kernel_Name"]), statistics.median(d)))
+    return out
+
+
 def summarize(directory: str):
     """Condense rocprofv3 --stats / --pmc CSV output found under `directory`."""
     import csv
@@ -640,6 +674,8 @@ def summarize(directory: str):
                 short = _short(r.get("Name", ""))
                 lines.append("| %s | %s | %.3f | %.2f |" % (short, r.get("Calls"), float(r.get("AverageNs", 0)) / 1e3,
                                                           float(r.get("Percentage", 0))))
+    for path in sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True)):
+        lines.extend(_steady_state(path, directory))
     for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
         agg = {}
         with open(path) as f:
@@ -662,6 +698,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="3", help="1..4 (default 3: the 32K-context Llama-3-8B-shaped decode)")
     ap.add_argument("--layers", type=int, default=None)
+    ap.add_argument("--n-tokens", type=int, default=None, help="context length override (a variant of the workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sketch", action="store_true", help="skip the int8-sketch variant of the step")
     ap.add_argument("--no-bkp", action="store_true", help="skip timing the hot/cold pool pass")
