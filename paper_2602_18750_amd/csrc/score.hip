@@ -68,6 +68,7 @@ struct KeysF16 {
     static constexpr int kSlots = 1;   // tiles whose loads are in flight together
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
+    static constexpr bool kMfma = false;
     uint4 kr[2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
@@ -128,41 +129,11 @@ struct QueryLds {
     int eq[kMaxGroup];
 };
 
-template <int DT, int GC, int BITS>
-struct KeysSketch {
-    static_assert(BITS == 8 || BITS == 4, "int8 or int4 key codes");
-    static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
-    static constexpr bool kGroupQuery = true;
-    static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
-    static constexpr int kRowBytes = kHeadDim * BITS / 8;
-    using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
-    Codes kr[kSlots][kRowsPerLane];
-    uint32_t ek4[kSlots];   // exponents of the 4 rows, one byte each
-    uint4 q8[GC];
-    int eq[GC];
-    int qbias[GC];          // int4: 8 * (sum of this lane's 16 query codes)
-    int eq_lane = 0;        // exponent of this lane's head (lane l8 < GC holds head l8 of the chunk)
-    int q_tag = -1;
+// The queries of a key-sketch scan: cast once per (b, g) into LDS.
+template <int DT>
+struct SketchQuery {
     QueryLds* ql = nullptr;
-
-    template <int SLOT>
-    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
-    {
-        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
-        const int jr = c.j0 + rg * kRowsPerLane;
-        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + l8 * (kRowBytes / 8);
-#pragma unroll
-        for (int u = 0; u < kRowsPerLane; ++u) {
-            const int j = jr + u;
-            if constexpr (BITS == 8) {
-                kr[SLOT][u] = j < a.n ? load_stream16(kb + (int64_t)j * kRowBytes) : make_uint4(0u, 0u, 0u, 0u);
-            } else {
-                kr[SLOT][u] = j < a.n ? load_stream8(kb + (int64_t)j * kRowBytes) : make_uint2(0u, 0u);
-            }
-        }
-        // jr is a multiple of 4 and cap too: the 4 exponents are one aligned word inside the row
-        ek4[SLOT] = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
-    }
+    int q_tag = -1;
 
     // The raw query words of the group's first heads (wave w: heads w and
     // w + 4, lane l: elements 2l, 2l+1), fetched before the key loads so that
@@ -206,6 +177,45 @@ struct KeysSketch {
             if (w + 4 * i < a.G) cast_head(qpre[i], w + 4 * i, lane);
         for (int h = w + 4 * kQPre; h < a.G; h += 4) cast_head(*qword(a, b, g, h, lane), h, lane);
         q_tag = -1;
+    }
+
+};
+
+template <int DT, int GC, int BITS>
+struct KeysSketch : SketchQuery<DT> {
+    static_assert(BITS == 8 || BITS == 4, "int8 or int4 key codes");
+    static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
+    static constexpr bool kGroupQuery = true;
+    static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
+    static constexpr bool kMfma = false;
+    static constexpr int kRowBytes = kHeadDim * BITS / 8;
+    using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
+    using SketchQuery<DT>::ql;
+    using SketchQuery<DT>::q_tag;
+    Codes kr[kSlots][kRowsPerLane];
+    uint32_t ek4[kSlots];   // exponents of the 4 rows, one byte each
+    uint4 q8[GC];
+    int eq[GC];
+    int qbias[GC];          // int4: 8 * (sum of this lane's 16 query codes)
+    int eq_lane = 0;        // exponent of this lane's head (lane l8 < GC holds head l8 of the chunk)
+
+    template <int SLOT>
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
+        const int jr = c.j0 + rg * kRowsPerLane;
+        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + l8 * (kRowBytes / 8);
+#pragma unroll
+        for (int u = 0; u < kRowsPerLane; ++u) {
+            const int j = jr + u;
+            if constexpr (BITS == 8) {
+                kr[SLOT][u] = j < a.n ? load_stream16(kb + (int64_t)j * kRowBytes) : make_uint4(0u, 0u, 0u, 0u);
+            } else {
+                kr[SLOT][u] = j < a.n ? load_stream8(kb + (int64_t)j * kRowBytes) : make_uint2(0u, 0u);
+            }
+        }
+        // jr is a multiple of 4 and cap too: the 4 exponents are one aligned word inside the row
+        ek4[SLOT] = jr < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jr) : 0u;
     }
 
     __device__ __forceinline__ void query(const ScoreArgs& a, const TileCoord& c, int hc, int l8)
@@ -267,6 +277,160 @@ struct KeysSketch {
         return ldexpf((float)idot<SLOT>(u, hh), eq[hh] + ek);
     }
 };
+
+// Int4 key sketch on the matrix cores (ATTN logits): the scan's integer dot
+// products as v_mfma_i32_16x16x32_i8, D[row][head] = sum_k A[row][k] B[k][head]
+// over 16 rows and 16 head columns (the group's heads, zero beyond G).  Lane l
+// holds row l % 16 of a 16-row block and the 16 bytes [16*(l/16), +16) of
+// that 64-byte row (codes [32*(l/16), +32)), unpacked to int8 by two masks;
+// one load instruction thus reads 16 whole rows, i.e. 8 whole 128-byte lines.
+// The k index of the four MFMAs runs over the lane's codes in order, and the
+// query operand (head l % 16) follows the same order.  The result lands as 4
+// consecutive rows 4*(l/16) .. +3 of head l % 16 per lane, so each lane scales
+// and stores its own head's logits and the per-tile softmax pairs need two
+// cross-lane steps.  The sums are the same exact integers as on the vector
+// units, so the logits are bit-identical.  (An int8 row is a whole line, which
+// this layout would read in two half-line requests per instruction: the int8
+// sketch stays on the vector units, whose row groups read whole lines.)
+typedef int i32x4_t __attribute__((ext_vector_type(4)));
+
+template <int DT>
+struct KeysSketchMfma4 : SketchQuery<DT> {
+    static constexpr int kSlots = 2;
+    static constexpr bool kGroupQuery = true;
+    static constexpr bool kIntDot = true;
+    static constexpr bool kMfma = true;
+    static constexpr int kRowBytes = kHeadDim / 2;
+    using SketchQuery<DT>::ql;
+    using SketchQuery<DT>::q_tag;
+    uint4 kr[kSlots][2];            // [tile][16-row block]: the lane's 16 bytes of its row
+    uint32_t ek4[kSlots][2];        // exponents of rows 4*(l/16) .. +3 of each block
+    uint64_t qb[4];                 // query operand of the four MFMAs (head hc + l % 16)
+    int eq_lane = 0;                // its exponent
+    int bias = 0;                   // 8 * (sum of its 128 codes)
+
+    template <int SLOT>
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int lane = rg * 8 + l8;
+        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
+        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + 16 * (lane >> 4);
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+            const int j = c.j0 + 16 * rb + (lane & 15);
+            kr[SLOT][rb] = j < a.n ? load_stream16(kb + (int64_t)j * kRowBytes) : make_uint4(0u, 0u, 0u, 0u);
+            // rows 4*(l/16) .. +3 start at a multiple of 4 and cap is one too: one aligned word
+            const int j4 = c.j0 + 16 * rb + 4 * (lane >> 4);
+            ek4[SLOT][rb] = j4 < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + j4) : 0u;
+        }
+    }
+
+    // Query operand of heads hc .. hc+15 (lane: head hc + l % 16, the query
+    // codes of the dimensions of the lane's key codes, in the same order).
+    __device__ __forceinline__ void mquery(const ScoreArgs& a, const TileCoord& c, int hc, int lane)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+        const int h = hc + (lane & 15);
+        uint4 x = make_uint4(0u, 0u, 0u, 0u), y = make_uint4(0u, 0u, 0u, 0u);
+        eq_lane = 0;
+        if (h < a.G) {
+            const uint4* src = reinterpret_cast<const uint4*>(&ql->q8[h][32 * (lane >> 4)]);
+            x = src[0];
+            y = src[1];
+            eq_lane = ql->eq[h];
+        }
+        qb[0] = (uint64_t)x.x | ((uint64_t)x.y << 32);
+        qb[1] = (uint64_t)x.z | ((uint64_t)x.w << 32);
+        qb[2] = (uint64_t)y.x | ((uint64_t)y.y << 32);
+        qb[3] = (uint64_t)y.z | ((uint64_t)y.w << 32);
+        {   // the +8 offset of the codes: 8 * (sum of the head's 128 query codes)
+            const int ones = 0x01010101;
+            int sq = 0;
+            sq = __builtin_amdgcn_sdot4((int)x.x, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)x.y, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)x.z, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)x.w, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)y.x, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)y.y, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)y.z, ones, sq, false);
+            sq = __builtin_amdgcn_sdot4((int)y.w, ones, sq, false);
+            sq += __shfl_xor(sq, 16, 64);
+            sq += __shfl_xor(sq, 32, 64);
+            bias = 8 * sq;
+        }
+        q_tag = tag;
+    }
+
+    // Exact integer dots of the 16 rows of block rb against heads hc .. hc+15.
+    template <int SLOT>
+    __device__ __forceinline__ i32x4_t dots(int rb) const
+    {
+        i32x4_t acc = {-bias, -bias, -bias, -bias};
+#pragma unroll
+        for (int jk = 0; jk < 4; ++jk) {
+            // codes + 8 in [1, 15]: low nibbles are codes 0..3 of a word, high nibbles 4..7
+            const uint4 k = kr[SLOT][rb];
+            const uint32_t w = jk == 0 ? k.x : jk == 1 ? k.y : jk == 2 ? k.z : k.w;
+            const uint32_t m = 0x0F0F0F0Fu;
+            const uint64_t a_op = (uint64_t)(w & m) | ((uint64_t)((w >> 4) & m) << 32);
+            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8((long)a_op, (long)qb[jk], acc, 0, 0, 0);
+        }
+        return acc;
+    }
+};
+
+// One wave-tile of KeysSketchMfma (ATTN): logits of heads hc + l % 16 for
+// rows 4*(l/16) .. +3 of both 16-row blocks, stored as float4, and the tile's
+// (max, sum exp2) per head.
+template <int SLOT, typename Keys>
+__device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const TileCoord& c, int lane, Keys& ks,
+                                                  float2* tile_part)
+{
+    const int n16 = lane & 15, grp = lane >> 4;
+    for (int hc = 0; hc < a.G; hc += 16) {
+        ks.mquery(a, c, hc, lane);
+        const int h = hc + n16;
+        float mine[8], x[8];
+        float m = -INFINITY;
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+            const i32x4_t d = ks.template dots<SLOT>(rb);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int ek = (int)(int8_t)(ks.ek4[SLOT][rb] >> (8 * i));
+                mine[4 * rb + i] = ldexpf((float)d[i], ks.eq_lane + ek);
+                const int j = c.j0 + 16 * rb + 4 * grp + i;
+                x[4 * rb + i] = j < a.n ? a.s2 * mine[4 * rb + i] : -INFINITY;
+                m = fmaxf(m, x[4 * rb + i]);
+            }
+        }
+        if (h < a.G) {
+            float* lrow = a.logits + ((int64_t)c.b * a.Hq + c.g * a.G + h) * a.ld;
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                const int j = c.j0 + 16 * rb + 4 * grp;
+                if (j + 4 <= a.n) {
+                    *reinterpret_cast<float4*>(lrow + j) =
+                        make_float4(mine[4 * rb], mine[4 * rb + 1], mine[4 * rb + 2], mine[4 * rb + 3]);
+                } else {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        if (j + i < a.n) lrow[j + i] = mine[4 * rb + i];
+                }
+            }
+        }
+        // the tile's 32 rows of head h sit in lanes n16, n16 + 16, n16 + 32, n16 + 48
+        m = fmaxf(m, __shfl_xor(m, 16, 64));
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        float z = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) z += x[i] == -INFINITY ? 0.0f : exp2f(x[i] - m);
+        z += __shfl_xor(z, 16, 64);
+        z += __shfl_xor(z, 32, 64);
+        if (grp == 0 && h < a.G) tile_part[h] = make_float2(m, z);
+    }
+}
 
 template <int GC, int OUT, int SLOT, typename Keys>
 __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord& c, int rg, int l8, Keys& ks,
@@ -431,16 +595,19 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
             }
         }
         if (t0 < a.ntiles) {
-            compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
+            if constexpr (Keys::kMfma) compute_tile_mfma<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
+            else compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i0][h] = make_float2(-INFINITY, 0.0f);
         }
         if (t1 < a.ntiles) {
             if constexpr (Keys::kSlots == 1) ks.template load<0>(a, c1, rg, l8);
-            compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
+            if constexpr (Keys::kMfma) compute_tile_mfma<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
+            else compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i1][h] = make_float2(-INFINITY, 0.0f);
         }
+
         if constexpr (OUT == kOutLogits) {
             __syncthreads();
             merge_unit(a, bg, unit, tile_part);
@@ -466,6 +633,17 @@ template <int DT, int GC, int OUT>
 hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp ts)
 {
     const int64_t total = (int64_t)a.B * a.Hkv * a.npart;
+    if constexpr (OUT == kOutLogits) {
+        // int4 sketch, ATTN logits, G >= 4: integer dots on the matrix cores (with fewer heads per
+        // key the vector units' dot chains are short and faster)
+        if (a.k8 && a.kbits == 4 && a.G >= 4) {
+            auto kernel = score_tiles_kernel<1, OUT, KeysSketchMfma4<DT>>;
+            const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+            const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+            hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+            return hipGetLastError();
+        }
+    }
     if (a.k8 && a.kbits == 4) {
         auto kernel = score_tiles_kernel<GC, OUT, KeysSketch<DT, GC, 4>>;
         const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);

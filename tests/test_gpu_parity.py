@@ -517,6 +517,34 @@ def test_sketch_logits_bit_exact(B, nh, n, dt, nbits):
     assert np.array_equal(got, ref.reshape(B, nh, n))
 
 
+@pytest.mark.parametrize("nbits", [8, 4])
+@pytest.mark.parametrize("B,Hq,Hkv,n,dt", [(1, 32, 8, 1000, "bf16"), (2, 8, 8, 4099, "fp16"), (1, 32, 2, 37, "bf16"),
+                                           (1, 32, 1, 515, "fp16"), (3, 6, 2, 300, "bf16")])
+def test_sketch_attn_logits_bit_exact(B, Hq, Hkv, n, dt, nbits):
+    """ATTN scoring on the sketch (int4 with G >= 4 on the matrix cores, the
+    rest on the vector units): the logits it leaves at the start of the
+    workspace ([B, Hq, ld] fp32, ld = n rounded up to 4: the library's
+    workspace layout) must equal the oracle's exact sketch logits bit for bit,
+    for group sizes 4, 1, 16, 32 (two passes of 16 heads) and 3, and for
+    ragged n."""
+    say("sketch ATTN logits exact", nbits, B, Hq, Hkv, n, dt)
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=1, seed=5151 + n + Hq)
+    q, k, v = gpu_inputs(x)
+    sk = H().sketch_keys(k, bits=nbits)
+    k8, ek = _sketch_ref(x.k, dt, nbits)
+    q8, eq = O.sketch(bits(x.q[0]), dt)
+    ref = O.logits_i8(q8, eq, k8, ek).astype(np.float32)   # [B, Hq, n], exact
+    s = H().new_importance(B, 1, n, DEV)
+    desc = H().make_desc(q[0], k, None, s)
+    ws = H().workspace(desc, 1, DEV)
+    ws.fill_(0xFF)                                           # NaN pattern: every logit must be written
+    H().hill_score(q[0], None, s, mode="attn", granularity="token", sketch=sk, ws=ws)
+    torch.cuda.synchronize()
+    ld = (n + 3) // 4 * 4
+    got = ws[:B * Hq * ld * 4].view(torch.float32).cpu().numpy().reshape(B, Hq, ld)[:, :, :n]
+    assert np.array_equal(got, ref.reshape(B, Hq, n))
+
+
 def _run_sketch_steps(x, k_sel, mode, gran, steps, where, nbits=8):
     B, Hkv, n = x.k.shape[0], x.k.shape[1], x.k.shape[2]
     dt = dname(x.k)
