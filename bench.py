@@ -609,7 +609,7 @@ def make_counters(directory: str, command: str):
         "fetch_factor": round(ff, 4),
         "write_factor": round(wf, 4),
         "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan(r"KeysSketch<\d+, \d+, 8>")),
-        "sketch4": dict(kernel="score_tiles (int4 key sketch)", **scan(r"KeysSketch<\d+, \d+, 4>")),
+        "sketch4": dict(kernel="score_tiles (int4 key sketch)", **scan(r"KeysSketchMfma4<|KeysSketch<\d+, \d+, 4>")),
         "command": command,
     })
     print(json.dumps(rec, indent=1))
