@@ -67,7 +67,10 @@
 extern "C" {
 #endif
 
-#define HILL_ABI_VERSION 4
+#define HILL_ABI_VERSION 5
+
+/* The library exports these entry points only (built with hidden visibility). */
+#define HILL_API __attribute__((visibility("default")))
 
 typedef enum hill_status {
     HILL_OK = 0,
@@ -113,26 +116,26 @@ typedef struct hill_desc {
 } hill_desc;
 
 /* ABI version of the loaded library (HILL_ABI_VERSION it was built with). */
-int hill_abi_version(void);
+HILL_API int hill_abi_version(void);
 
 /* Static description of a status code. */
-const char* hill_status_str(int status);
+HILL_API const char* hill_status_str(int status);
 
 /* Message describing the calling thread's most recent failed call (empty
  * string if none).  Valid until the next libhill call on this thread. */
-const char* hill_last_error(void);
+HILL_API const char* hill_last_error(void);
 
 /* Workspace bytes that hill_score / hill_topk / hill_gather_attn / hill_step
  * need for this descriptor and token budget (the maximum over the four).
  * Pure host function; writes *bytes.  k_sel is only used by the attention
  * and select parts and may be any value in [1, n_tokens]. */
-hill_status hill_workspace_bytes(const hill_desc* d, int32_t k_sel, size_t* bytes);
+HILL_API hill_status hill_workspace_bytes(const hill_desc* d, int32_t k_sel, size_t* bytes);
 
 /* Importance scoring (Sec. 4.1 metric; Sec. 4.4 raw variant):
  * S[b,r,j] += sum_{h in heads(r)} w[b,h,j] for every j < n_tokens.
  * q, k: inputs.  s: in/out, the caller's cumulative importance (zero it
  * before the first step and for newly appended tokens). */
-hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* s,
+HILL_API hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* s,
                        void* ws, size_t ws_bytes, void* stream);
 
 /* Top-k selection (Sec. 3.1 top-alpha; Sec. 4.2 global top-alpha indices):
@@ -140,7 +143,7 @@ hill_status hill_score(const hill_desc* d, const void* q, const void* k, float* 
  * the lower token index, NaN below every number, -0.0 equal to +0.0.
  * idx_out: [B, R, k_sel] int32, ascending within a row.
  * val_out: nullable; if given, [B, R, k_sel] fp32 with S at those tokens. */
-hill_status hill_topk(const hill_desc* d, const float* s, int32_t k_sel,
+HILL_API hill_status hill_topk(const hill_desc* d, const float* s, int32_t k_sel,
                       int32_t* idx_out, float* val_out,
                       void* ws, size_t ws_bytes, void* stream);
 
@@ -149,7 +152,7 @@ hill_status hill_topk(const hill_desc* d, const float* s, int32_t k_sel,
  * distinct indices in [0, n_tokens) in any order (not checked on device: an
  * out-of-range index is clamped into [0, n_tokens), so it never reads out of
  * bounds, and the result is then unspecified).  out: [B, Hq, D] fp32. */
-hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v,
+HILL_API hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, const void* v,
                              const int32_t* idx, int32_t k_sel, float* out,
                              void* ws, size_t ws_bytes, void* stream);
 
@@ -157,7 +160,7 @@ hill_status hill_gather_attn(const hill_desc* d, const void* q, const void* k, c
  * update S with this query, select k_sel tokens on the updated S, attend over
  * them.  Equivalent to hill_score, hill_topk (val_out = NULL) and
  * hill_gather_attn in sequence, with fewer launches. */
-hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v,
+HILL_API hill_status hill_step(const hill_desc* d, const void* q, const void* k, const void* v,
                       float* s, int32_t k_sel, int32_t* idx_out, float* out,
                       void* ws, size_t ws_bytes, void* stream);
 
@@ -177,7 +180,7 @@ typedef struct hill_step_events {
 
 /* hill_step with kernel timestamps (ev may be NULL: then identical to hill_step).
  * Same arguments, validation and results as hill_step. */
-hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k, const void* v,
+HILL_API hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k, const void* v,
                                float* s, int32_t k_sel, int32_t* idx_out, float* out,
                                void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
@@ -196,13 +199,21 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
  * previous call (growing only without pins), and k_sel at most the number of
  * tokens whose first radix digit reached the previous threshold's (usually
  * k_sel plus a few hundred, so a budget that grows with the context keeps
- * it); otherwise, and on the first call, the selection reads the whole row
- * instead, which is exact but slower.  ATTN score mode only
- * (HILL_ERR_UNSUPPORTED otherwise).  ev: as hill_step_profiled (the select
- * interval is empty). */
-hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s,
-                               uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
-                               size_t ws_bytes, void* stream, const hill_step_events* ev);
+ * it); otherwise, and on the first call, every workgroup of the selection
+ * walks the whole row instead, which is exact but slow on long rows.
+ *
+ * flags: 0, or HILL_STREAM_RESET: this call selects through the refine pass
+ * exactly as hill_step does (no bound read, no candidate list) and writes a
+ * fresh bound from its threshold.  Use it for the first steps of a sequence
+ * (while S is young it can double from one step to the next, so the previous
+ * threshold bounds the next one only loosely) and after S was changed
+ * outside these calls; results are the same either way.  ATTN score mode
+ * only (HILL_ERR_UNSUPPORTED otherwise).  ev: as hill_step_profiled (without
+ * HILL_STREAM_RESET the select interval is empty). */
+#define HILL_STREAM_RESET 1u
+HILL_API hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s,
+                               uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out,
+                               void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
 /* Asymmetric-precision scoring (Sec. 4.4: the evaluation runs on int8 or
  * int4 casts of the keys and an int8 cast of the query, attention on the
@@ -225,22 +236,22 @@ hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k,
 /* Writes the sketch (bits 8 or 4) of key rows [token_begin, token_end) of
  * every (b, g): run it over the whole cache once, then for each appended
  * token. */
-hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap, int32_t bits,
+HILL_API hill_status hill_sketch_keys(const hill_desc* d, const void* k, int8_t* k8, int8_t* k_exp, int64_t cap, int32_t bits,
                              int32_t token_begin, int32_t token_end, void* stream);
 
 /* hill_score on the sketch (no 16-bit keys read). */
-hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp,
+HILL_API hill_status hill_score_sketch(const hill_desc* d, const void* q, const int8_t* k8, const int8_t* k_exp,
                               int64_t cap, int32_t bits, float* s, void* ws, size_t ws_bytes, void* stream);
 
 /* hill_step whose scoring reads the sketch; selection and attention as in
  * hill_step (attention reads the 16-bit K and V of the selected tokens).
  * state: NULL, or the streamed selection's state (see hill_step_streamed;
- * ATTN only), then the selection runs streamed.  ev may be NULL (see
- * hill_step_profiled). */
-hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v,
+ * ATTN only), then the selection runs streamed; flags as there (0 when
+ * state is NULL).  ev may be NULL (see hill_step_profiled). */
+HILL_API hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v,
                              const int8_t* k8, const int8_t* k_exp, int64_t cap, int32_t bits, float* s,
-                             uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
-                             size_t ws_bytes, void* stream, const hill_step_events* ev);
+                             uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out,
+                             void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
 /* Bidirectional KV Cache Pools (Sec. 4.2, HKM / BKP): the per-token hit-rate
  * table and the hot/cold pool policy, run once after each decoding step (the
@@ -275,7 +286,7 @@ typedef struct hill_bkp_desc {
 } hill_bkp_desc;
 
 /* Workspace bytes for hill_bkp_update (a pure function of the descriptor). */
-hill_status hill_bkp_workspace_bytes(const hill_bkp_desc* d, size_t* bytes);
+HILL_API hill_status hill_bkp_workspace_bytes(const hill_bkp_desc* d, size_t* bytes);
 
 /* One BKP pass.  idx: int32 [B, R, k_sel] (the layout of hill_step's
  * idx_out), indices unique within a row; entries outside [0, N) are skipped;
@@ -284,7 +295,7 @@ hill_status hill_bkp_workspace_bytes(const hill_bkp_desc* d, size_t* bytes);
  * written), both with the descriptor's strides, caller-owned, zero at the
  * start of a sequence.  promote, demote: int32 [B, R, list_cap]; counts:
  * int32 [B, R, 2].  All device pointers, asynchronous on `stream`. */
-hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t k_sel, uint16_t* hits,
+HILL_API hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx, int32_t k_sel, uint16_t* hits,
                             uint8_t* hot, int32_t* promote, int32_t* demote, int32_t list_cap, int32_t* counts,
                             void* ws, size_t ws_bytes, void* stream);
 
@@ -313,7 +324,7 @@ typedef struct hill_app_plan {
 } hill_app_plan;
 
 /* Fills *plan; HILL_ERR_INVALID_ARG for non-finite or out-of-range inputs. */
-hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan);
+HILL_API hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan);
 
 /* Roofline calibration (measurement aid, computes nothing of the method):
  * one launch of `grid` workgroups that reads `bytes` bytes of the device
@@ -321,7 +332,7 @@ hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan);
  * non-temporal loads.  buf 16-byte aligned, bytes a positive multiple of 16,
  * 1 <= grid <= 65536; sink is a device array of `grid` words that the kernel
  * may write (its contents are meaningless).  Errors as for every call. */
-hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream);
+HILL_API hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

@@ -22,7 +22,7 @@ SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", 
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
+COMMON = ["-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden", "--offload-arch=" + ARCH,
           # packed fp32 instructions stay disabled on gfx950
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wall", "-Wno-unused-result", "-I", INCLUDE, "-I", CSRC]

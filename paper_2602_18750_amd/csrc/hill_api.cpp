@@ -444,7 +444,7 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
 // then emit the indices and attend over each chunk's picks in the same kernel.
 hill_status run_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk, float* s_acc,
                      int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
-                     const hill_step_events* ev, uint32_t* stream_state = nullptr)
+                     const hill_step_events* ev, uint32_t* stream_state = nullptr, bool stream_reset = false)
 {
     Shape s;
     HILL_TRY(check_desc(d, &s));
@@ -464,19 +464,21 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     const hill_step_events none{};
     const hill_step_events& e = ev ? *ev : none;
     uint4* state4 = reinterpret_cast<uint4*>(stream_state);
-    HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e, state4, k_sel));
+    // a reset step selects through the refine pass and only writes the bound
+    HILL_TRY(run_score(d, s, L, q, k, sk, s_acc, ws, true, st, e, stream_reset ? nullptr : state4, k_sel));
     RefineArgs r = refine_args(d, s, L, s_acc, k_sel, ws);
     AttnArgs a = attn_args(d, s, L, q, k, v, idx_out, k_sel, out, ws);
     if (s.mode == HILL_SCORE_ATTN && !sk.k8) {   // the scan's logits are those of the 16-bit keys: reused
         a.logits = at<float>(ws, L.logits);
         a.ld = s.ld;
     }
-    if (state4) {   // no refine pass: the select interval is empty
+    if (state4 && !stream_reset) {   // no refine pass: the select interval is empty
         HIP_TRY(mark(e.select_start, st));
         HIP_TRY(mark(e.select_stop, st));
         r.state_out = state4;
         HIP_TRY(launch_topk_emit_attn_stream(r, a, s.dtype, st));
     } else {
+        r.state_out = state4;   // NULL, or a reset step's fresh bound
         HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
                                    Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
         HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
@@ -793,23 +795,33 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
     return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
 }
 
+static hill_status check_stream_flags(const uint32_t* state, uint32_t flags)
+{
+    if (flags & ~HILL_STREAM_RESET) return fail(HILL_ERR_INVALID_ARG, "unknown streamed-selection flags 0x%x", flags);
+    if (flags && !state) return fail(HILL_ERR_INVALID_ARG, "streamed-selection flags without a state");
+    return HILL_OK;
+}
+
 hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc,
-                               uint32_t* state, int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes,
-                               void* stream, const hill_step_events* ev)
+                               uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
+                               size_t ws_bytes, void* stream, const hill_step_events* ev)
 {
     if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
     if (d->score_mode != HILL_SCORE_ATTN)
         return fail(HILL_ERR_UNSUPPORTED, "streamed selection needs ATTN scores (S must only grow)");
     if (!state || ((uintptr_t)state & 15u)) return fail(HILL_ERR_INVALID_ARG, "state is NULL or not 16-byte aligned");
-    return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev, state);
+    HILL_TRY(check_stream_flags(state, flags));
+    return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev, state,
+                    (flags & HILL_STREAM_RESET) != 0);
 }
 
 hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, const void* v, const int8_t* k8,
                              const int8_t* k_exp, int64_t cap, int32_t bits, float* s_acc, uint32_t* state,
-                             int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
-                             const hill_step_events* ev)
+                             uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes,
+                             void* stream, const hill_step_events* ev)
 {
     if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
+    HILL_TRY(check_stream_flags(state, flags));
     if (state) {
         if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
         if (d->score_mode != HILL_SCORE_ATTN)
@@ -817,7 +829,7 @@ hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, c
         if ((uintptr_t)state & 15u) return fail(HILL_ERR_INVALID_ARG, "state is not 16-byte aligned");
     }
     return run_step(d, q, k, v, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev,
-                    state);
+                    state, (flags & HILL_STREAM_RESET) != 0);
 }
 
 }  // extern "C"

@@ -130,7 +130,8 @@ struct RefineArgs {
     const uint32_t* scount;  // [rows, nup] pairs of each update block
     const uint32_t* d0;      // [rows] the bound's first digit | 0x80000000 if the bound held
     // hist2 continues as [kStreamBins, rows, kHistRow]: second digits of first-digit bins d0 + w
-    uint4* state_out;        // [rows, 2] this step's threshold bound, for the next step
+    uint4* state_out;        // [rows, 2] this step's threshold bound, for the next step (streamed
+                             // selection; a reset step writes it from the refine pass), or NULL
 };
 
 // Splits of the selected set per (sequence, KV head) for the attention pass.

@@ -440,6 +440,10 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     DigitHist h2;
     load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
     const uint32_t b1 = s1.x, need1 = s1.y, in1 = s1.z;
+    if (r.state_out && writer && c == 0 && tid == 0) {   // a reset step of the streamed selection: its bound
+        r.state_out[2 * row] = make_uint4(b1 << 20, (uint32_t)r.k - need1 + in1, (uint32_t)r.n, 1u);
+        r.state_out[2 * row + 1] = make_uint4((uint32_t)r.pin_lo, (uint32_t)(r.n - r.pin_hi), 0u, 0u);
+    }
     prefix = b1;
     need = need1;
     shift = 20;

@@ -35,7 +35,7 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
-ABI_VERSION = 4   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
+ABI_VERSION = 5   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
@@ -138,7 +138,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_sketch_keys.restype = ctypes.c_int
         lib.hill_score_sketch.argtypes = [D, P, P, P, I64, I32, P, P, SZ, P]
         lib.hill_score_sketch.restype = ctypes.c_int
-        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, P, I32, P, P, P, SZ, P,
+        U32 = ctypes.c_uint32
+        lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, P, U32, I32, P, P, P, SZ, P,
                                          ctypes.POINTER(HillStepEvents)]
         lib.hill_step_sketch.restype = ctypes.c_int
         lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
@@ -147,7 +148,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
         lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
         lib.hill_bkp_update.restype = ctypes.c_int
-        lib.hill_step_streamed.argtypes = [D, P, P, P, P, P, I32, P, P, P, SZ, P, ctypes.POINTER(HillStepEvents)]
+        lib.hill_step_streamed.argtypes = [D, P, P, P, P, P, U32, I32, P, P, P, SZ, P,
+                                           ctypes.POINTER(HillStepEvents)]
         lib.hill_step_streamed.restype = ctypes.c_int
         lib.hill_app_balance.argtypes = [ctypes.POINTER(AppParams), ctypes.POINTER(AppPlan)]
         lib.hill_app_balance.restype = ctypes.c_int
@@ -371,6 +373,9 @@ def hill_gather_attn(q, k, v, idx, *, granularity="token", n_tokens=None, sm_sca
     return out
 
 
+HILL_STREAM_RESET = 1   # include/hill.h: select through the refine pass and write a fresh bound
+
+
 def new_stream_state(B: int, R: int, device) -> torch.Tensor:
     """Zeroed state of the streamed selection for one S buffer ([B, R] rows)."""
     return torch.zeros((B, R, 8), dtype=torch.int32, device=device)
@@ -378,11 +383,13 @@ def new_stream_state(B: int, R: int, device) -> torch.Tensor:
 
 def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="token", n_tokens=None,
               sm_scale=0.0, idx_out=None, out=None, ws=None, stream=None, events=None,
-              sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None):
+              sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None, stream_reset=False):
     """One decode step: S update, top-k on the new S, attention.  Returns (idx, out).
     ``n_sink`` / ``n_recent``: pinned tokens every selection keeps.
     ``stream_state``: streamed selection (hill_step_streamed) with this state
-    (from new_stream_state, kept with S across steps).
+    (from new_stream_state, kept with S across steps); ``stream_reset``: this
+    step selects through the refine pass and writes a fresh bound
+    (HILL_STREAM_RESET: the first steps of a sequence).
 
     ``events``: optional HillStepEvents; then hill_step_profiled records them.
     ``sketch``: score on the int8 / int4 sketch (hill_step_sketch)."""
@@ -405,15 +412,18 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         _device_check(stream_state)
         if stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8 or not stream_state.is_contiguous():
             raise ValueError("stream_state must be a contiguous int32 [B, R, 8] tensor")
+    elif stream_reset:
+        raise ValueError("stream_reset needs a stream_state")
+    flags = HILL_STREAM_RESET if stream_reset else 0
     if sketch is not None:
         _check(lib.hill_step_sketch(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(sketch.codes),
-                                    _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), _ptr(stream_state),
+                                    _ptr(sketch.exps), sketch.cap, sketch.bits, _ptr(s), _ptr(stream_state), flags,
                                     int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
                                     None if events is None else ctypes.byref(events)))
     elif stream_state is not None:
         _check(lib.hill_step_streamed(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), _ptr(stream_state),
-                                      int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
-                                      None if events is None else ctypes.byref(events)))
+                                      flags, int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(),
+                                      _stream_ptr(stream), None if events is None else ctypes.byref(events)))
     elif events is None:
         _check(lib.hill_step(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
                              _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream)))
@@ -527,10 +537,13 @@ def app_balance(*, f_c, f_s, b_c, b_s, alpha=None, alpha_c=None, alpha_s=None, m
 
 class StepCall:
     """hill_step with its arguments marshalled once, for hot loops that call it
-    repeatedly on the same buffers (only the query pointer changes per call)."""
+    repeatedly on the same buffers (only the query pointer changes per call).
+    With ``stream_state``, the first ``stream_reset_calls`` calls are reset
+    steps (HILL_STREAM_RESET), the later ones streamed."""
 
     def __init__(self, q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
-                 ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None):
+                 ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None,
+                 stream_reset_calls=3):
         lib = load_library()
         _device_check(q, k, v, s)
         self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
@@ -545,19 +558,31 @@ class StepCall:
         if stream_state is not None and (stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8):
             raise ValueError("stream_state must be an int32 [B, R, 8] tensor")
         state_ptr = P(stream_state.data_ptr() if stream_state is not None else None)
+        self._resets_left = int(stream_reset_calls) if stream_state is not None else 0
+        self._post_reset = None
         if sketch is not None:
             self._fn = None
             self._fn_ev = lib.hill_step_sketch   # events and state may be NULL
-            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
-                          ctypes.c_int64(sketch.cap), ctypes.c_int32(sketch.bits), P(s.data_ptr()), state_ptr,
-                          ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
-                          P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+
+            def post(flags):
+                return (P(k.data_ptr()), P(v.data_ptr()), P(sketch.codes.data_ptr()), P(sketch.exps.data_ptr()),
+                        ctypes.c_int64(sketch.cap), ctypes.c_int32(sketch.bits), P(s.data_ptr()), state_ptr,
+                        ctypes.c_uint32(flags), ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()),
+                        P(self.out.data_ptr()), P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()),
+                        P(_stream_ptr(stream)))
+            self._post = post(0)
+            if stream_state is not None:
+                self._post_reset = post(HILL_STREAM_RESET)
         elif stream_state is not None:
             self._fn = None
             self._fn_ev = lib.hill_step_streamed   # events may be NULL
-            self._post = (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), state_ptr,
-                          ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
-                          P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+
+            def post(flags):
+                return (P(k.data_ptr()), P(v.data_ptr()), P(s.data_ptr()), state_ptr, ctypes.c_uint32(flags),
+                        ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
+                        P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+            self._post = post(0)
+            self._post_reset = post(HILL_STREAM_RESET)
         else:
             self._fn = lib.hill_step
             self._fn_ev = lib.hill_step_profiled
@@ -568,7 +593,11 @@ class StepCall:
 
     def __call__(self, q_ptr: int, events=None):
         if self._fn is None:
-            st = self._fn_ev(*self._pre, ctypes.c_void_p(q_ptr), *self._post,
+            post = self._post
+            if self._resets_left > 0:
+                self._resets_left -= 1
+                post = self._post_reset
+            st = self._fn_ev(*self._pre, ctypes.c_void_p(q_ptr), *post,
                              None if events is None else ctypes.byref(events))
         elif events is None:
             st = self._fn(*self._pre, ctypes.c_void_p(q_ptr), *self._post)

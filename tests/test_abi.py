@@ -45,6 +45,21 @@ def test_library_exports_every_declared_symbol(H):
     assert sorted(H.hill.EXPORTS) == declared_functions()
 
 
+def test_library_exports_nothing_else(H):
+    """Built with hidden visibility: the dynamic symbol table holds the C
+    entry points of include/hill.h and no internal (C++) function."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    H.load_library()
+    lib_path = H.hill.LIB_PATH
+    out = subprocess.run([nm, "-D", "--defined-only", lib_path], capture_output=True, text=True, check=True).stdout
+    funcs = sorted(ln.split()[-1] for ln in out.splitlines() if len(ln.split()) == 3 and ln.split()[1] == "T")
+    assert funcs == declared_functions()
+
+
 def test_abi_version_and_status_strings(H):
     lib = H.load_library()
     want = int(re.search(r"#define HILL_ABI_VERSION (\d+)", open(HEADER).read()).group(1))
@@ -206,17 +221,17 @@ def test_sketch_entry_points_validate(H):
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, 996, bits, FAKE, FAKE, need, None) == INVALID
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 16,
                                      None) == WORKSPACE
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, bits, FAKE, None, 10,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, ok_cap, bits, FAKE, None, 0, 10,
                                     FAKE, FAKE, FAKE, need, None, None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, bits, FAKE, None, 10,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1002, bits, FAKE, None, 0, 10,
                                     FAKE, FAKE, FAKE, need, None, None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 0,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 0, 0,
                                     FAKE, FAKE, FAKE, need, None, None) == INVALID
         # a streamed state must be 16-byte aligned, and needs ATTN scores
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE + 4, 10,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE + 4, 0, 10,
                                     FAKE, FAKE, FAKE, need, None, None) == INVALID
         d.score_mode = 1
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 10,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, 0, 10,
                                     FAKE, FAKE, FAKE, need, None, None) == UNSUPPORTED
         d.score_mode = 0
     # only 8 and 4 bits exist
@@ -224,7 +239,7 @@ def test_sketch_entry_points_validate(H):
         assert lib.hill_sketch_keys(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, 0, 10, None) == INVALID
         assert lib.hill_score_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, ok_cap, bits, FAKE, FAKE, need,
                                      None) == INVALID
-        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 10,
+        assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, ok_cap, bits, FAKE, None, 0, 10,
                                     FAKE, FAKE, FAKE, need, None, None) == INVALID
     assert b"bits" in lib.hill_last_error()
 
@@ -340,15 +355,23 @@ def test_streamed_step_validates(H):
     lib = H.load_library()
     d = base_desc(H)
     need = ws_need(H, d, 10)
-    args = lambda state: (ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, state, 10, FAKE, FAKE, FAKE, need, None, None)
+    args = lambda state, flags=0: (ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, state, flags, 10, FAKE, FAKE, FAKE, need,
+                                   None, None)
     assert lib.hill_step_streamed(*args(None)) == INVALID
     assert lib.hill_step_streamed(*args(FAKE + 4)) == INVALID                 # not 16-byte aligned
     d.score_mode = 1                                                           # RAW: S can shrink
     assert lib.hill_step_streamed(*args(FAKE)) == UNSUPPORTED
     d.score_mode = 0
-    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, FAKE, FAKE, need, None,
+    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 0, FAKE, FAKE, FAKE, need, None,
                                   None) == INVALID                            # k_sel
-    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, 16, None,
+    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 0, 10, FAKE, FAKE, FAKE, 16, None,
                                   None) == WORKSPACE
-    assert lib.hill_step_streamed(None, FAKE, FAKE, FAKE, FAKE, FAKE, 10, FAKE, FAKE, FAKE, need, None,
+    assert lib.hill_step_streamed(None, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 10, FAKE, FAKE, FAKE, need, None,
                                   None) == INVALID
+    # flags: only HILL_STREAM_RESET exists; the reset step validates like the others
+    assert lib.hill_step_streamed(*args(FAKE, 2)) == INVALID
+    assert b"flags" in lib.hill_last_error()
+    assert lib.hill_step_streamed(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1, 10, FAKE, FAKE, FAKE, 16, None,
+                                  None) == WORKSPACE
+    assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1000, 8, FAKE, None, 1, 10,
+                                FAKE, FAKE, FAKE, need, None, None) == INVALID   # flags without a state

@@ -37,10 +37,11 @@ def say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _pair_run(x, schedule, gran="token", sink=0, recent=0):
+def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0):
     """hill_step and hill_step_streamed side by side on copies of the same S;
-    schedule: list of (n_tokens, k_sel) per step.  Asserts bit-identical S,
-    indices and outputs after every step; returns the streamed state."""
+    schedule: list of (n_tokens, k_sel) per step, the first `resets` of them
+    reset steps (HILL_STREAM_RESET).  Asserts bit-identical S, indices and
+    outputs and a valid state after every step; returns the streamed state."""
     q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
     B, Hkv, ncap = k.shape[0], k.shape[1], k.shape[2]
     R = 1 if gran == "token" else Hkv
@@ -50,12 +51,12 @@ def _pair_run(x, schedule, gran="token", sink=0, recent=0):
     for t, (n, ks) in enumerate(schedule):
         i_a, o_a = H().hill_step(q[t], k, v, s_a, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent)
         i_b, o_b = H().hill_step(q[t], k, v, s_b, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent,
-                                 stream_state=state)
+                                 stream_state=state, stream_reset=t < resets)
         torch.cuda.synchronize()
         assert torch.equal(s_a, s_b), "step %d: S differs" % t
         assert torch.equal(i_a, i_b), "step %d: indices differ" % t
         assert torch.equal(o_a, o_b), "step %d: outputs differ" % t
-    _check_state(state, s_b, n, ks, sink, recent)
+        _check_state(state, s_b, n, ks, sink, recent)
     return state
 
 
@@ -163,3 +164,18 @@ def test_streamed_growing_context_keeps_the_bound():
     sched = [(4000 + 5 * t, O.budget_k(4000 + 5 * t, 0.1)) for t in range(40)]
     say("streamed growing context")
     _pair_run(x, sched)
+
+
+@pytest.mark.parametrize("sink,recent", [(0, 0), (4, 64)])
+def test_streamed_reset_steps(sink, recent):
+    """HILL_STREAM_RESET steps select through the refine pass and write a
+    fresh bound (the same state a streamed step writes); the streamed steps
+    after them use it.  Identical results to hill_step throughout, also when
+    a reset follows streamed steps."""
+    x = W.make_random(2, 16, 4, 128, 5000, "bf16", steps=7, seed=123 + sink)
+    say("streamed reset steps", sink, recent)
+    sched = [(4800, 480), (4800, 480), (4900, 490), (4900, 490), (5000, 500), (5000, 500), (5000, 520)]
+    _pair_run(x, sched, sink=sink, recent=recent, resets=2)
+    # a later reset (k grew past the bound's count, or the caller changed S): a fresh start from any state
+    x2 = W.make_random(2, 16, 4, 128, 5000, "bf16", steps=3, seed=321 + sink)
+    _pair_run(x2, [(5000, 500), (5000, 2000), (5000, 500)], sink=sink, recent=recent, resets=1)
