@@ -60,6 +60,9 @@ SCORE_CASES = [
     # the length whose softmax partials the update reduces itself
     (1, 6, 3, 2000, "fp16", "attn", "token"),
     (1, 32, 8, 32768 + 129, "bf16", "attn", "token"),
+    # the head-count limits: 256 query heads, 128 per KV head
+    (1, 256, 2, 700, "bf16", "attn", "token"),
+    (1, 256, 256, 300, "fp16", "raw", "kvhead"),
 ]
 
 
@@ -580,3 +583,22 @@ def test_step_on_sketch_config3_full_size(nbits):
     say("sketch config 3 layer 0, 2 steps", nbits)
     x = W.make_layer(w.replace(steps=2), 0)
     _run_sketch_steps(x, w.k_sel, "attn", "token", 2, "sketch%d cfg3" % nbits, nbits)
+
+
+@pytest.mark.parametrize("Hq,Hkv,n,k,dt,gran", [(256, 2, 700, 70, "bf16", "token"), (256, 256, 300, 30, "fp16", "kvhead"),
+                                               (128, 1, 1000, 100, "bf16", "token")])
+def test_step_at_head_count_limits(Hq, Hkv, n, k, dt, gran):
+    """256 query heads, or 128 per KV head: the update reduces one head per
+    thread, the fused attention walks 16 chunks of 8 heads (or 256 KV heads),
+    and the scan passes over the group 16 times."""
+    say("head-count limits", Hq, Hkv, n, k, dt, gran)
+    x = W.make_random(1, Hq, Hkv, 128, n, dt, steps=2, seed=Hq + Hkv + n)
+    run_steps(x, k, "attn", gran, 2, where="heads %d/%d" % (Hq, Hkv))
+
+
+@pytest.mark.parametrize("nbits", [8, 4])
+def test_sketch_step_at_the_group_limit(nbits):
+    """128 query heads per KV head on the sketch: the int4 scan's matrix-core
+    form takes the group in 8 passes of 16 heads."""
+    x = W.make_random(1, 128, 1, 128, 1000, "bf16", steps=2, seed=99 + nbits)
+    _run_sketch_steps(x, 100, "attn", "token", 2, "group limit sketch%d" % nbits, nbits)
