@@ -65,11 +65,13 @@ __device__ __forceinline__ TileCoord coord(const ScoreArgs& a, int t)
 // of each of its 4 rows (two 16-byte non-temporal loads per row).
 template <int DT, int GC>
 struct KeysF16 {
-    static constexpr int kSlots = 1;   // tiles whose loads are in flight together
+    // tiles whose loads are in flight together: two where the queries take few
+    // registers (G <= 2 heads per pass keeps 4 workgroups per CU), else one
+    static constexpr int kSlots = GC <= 2 ? 2 : 1;
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
     static constexpr bool kMfma = false;
-    uint4 kr[2 * kRowsPerLane];
+    uint4 kr[kSlots][2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
 
@@ -82,11 +84,11 @@ struct KeysF16 {
             const int j = c.j0 + rg * kRowsPerLane + u;
             if (j < a.n) {
                 const uint16_t* row = kb + (int64_t)j * a.k_sn;
-                kr[2 * u] = load_stream16(row);
-                kr[2 * u + 1] = load_stream16(row + 64);
+                kr[SLOT][2 * u] = load_stream16(row);
+                kr[SLOT][2 * u + 1] = load_stream16(row + 64);
             } else {
-                kr[2 * u] = make_uint4(0u, 0u, 0u, 0u);
-                kr[2 * u + 1] = make_uint4(0u, 0u, 0u, 0u);
+                kr[SLOT][2 * u] = make_uint4(0u, 0u, 0u, 0u);
+                kr[SLOT][2 * u + 1] = make_uint4(0u, 0u, 0u, 0u);
             }
         }
     }
@@ -107,8 +109,8 @@ struct KeysF16 {
     template <int SLOT>
     __device__ __forceinline__ float dot(const ScoreArgs&, int u, int hh, int) const
     {
-        float d = dot8<DT>(kr[2 * u], qa[hh]);
-        d += dot8<DT>(kr[2 * u + 1], qb[hh]);
+        float d = dot8<DT>(kr[SLOT][2 * u], qa[hh]);
+        d += dot8<DT>(kr[SLOT][2 * u + 1], qb[hh]);
         return sum8(d);
     }
 };
