@@ -189,8 +189,9 @@ HILL_API hill_status hill_step_profiled(const hill_desc* d, const void* q, const
  * refine pass replaced.  With ATTN scores S only grows from step to step, so
  * the previous step's threshold is a lower bound on this one; the update
  * lists every token whose first radix digit reaches that bound, and the
- * selection resolves the exact threshold from the complete first-digit
- * histogram and that list.  Results are identical to hill_step.
+ * selection resolves the exact threshold from the first-digit histogram
+ * (counted from the bound's bin upward) and that list.  Results are
+ * identical to hill_step.
  *
  * state: uint32 [B, R, 8], 16-byte aligned, caller-owned, one per S buffer;
  * zero it at the start of a sequence and whenever S is changed outside these
