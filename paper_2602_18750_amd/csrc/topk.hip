@@ -18,8 +18,14 @@
 //               budget -- and stores them in token order with their count.
 //               With attention, the workgroup then attends over the chunk's
 //               selected tokens for one or more KV heads (fused gather +
-//               softmax over the list, attn_device.h) and writes one partial
-//               per query head.
+//               softmax over the list, attn_device.h; the logits are the
+//               scan's own when it read the 16-bit keys, so only V rows are
+//               gathered) and writes one partial per query head.  The
+//               streamed variant takes the first two digits from the
+//               update's histograms (the second from its window above the
+//               previous step's threshold) and, when those do not settle the
+//               threshold, walks the update's candidate pairs instead of
+//               refine's lists; it writes the bound for the next step.
 //  topk_write   places each chunk's list at its ascending-order offset (the
 //               counts of the chunks before it) in the output; in hill_step
 //               this runs inside merge_write, with the merge of the attention
