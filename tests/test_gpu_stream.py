@@ -179,3 +179,13 @@ def test_streamed_reset_steps(sink, recent):
     # a later reset (k grew past the bound's count, or the caller changed S): a fresh start from any state
     x2 = W.make_random(2, 16, 4, 128, 5000, "bf16", steps=3, seed=321 + sink)
     _pair_run(x2, [(5000, 500), (5000, 2000), (5000, 500)], sink=sink, recent=recent, resets=1)
+
+
+def test_streamed_several_kv_heads_per_workgroup():
+    """Workload 4's shape (B 4, n 131072, GQA 32/8): the select+attend kernel
+    takes four KV heads per workgroup there; the streamed steps (a reset step,
+    then streamed ones, including a growing budget) equal hill_step's."""
+    n = 131072
+    x = W.make_random(4, 32, 8, 128, n, "bf16", steps=4, seed=404, device=DEV)
+    say("streamed, several KV heads per workgroup")
+    _pair_run(x, [(n, 6553), (n, 6553), (n, 6600), (n, 6553)], resets=1)
