@@ -31,7 +31,6 @@ namespace hill {
 namespace {
 
 constexpr int kRowsPerLane = kScoreTile / 8;   // 4 rows per row group
-constexpr int kLoadsPerTile = 2 * kRowsPerLane;
 
 __global__ __launch_bounds__(256) void fill_zero_kernel(uint32_t* p, int64_t words)
 {
