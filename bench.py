@@ -25,13 +25,14 @@ Prints one JSON line:
   select_attn_us_per_layer_step   selection + gather attention, per layer-step
   plain        the same steps through hill_step (refine pass, five launches)
   bkp          the hot/cold pool pass after each layer's step (Sec. 4.2 BKP)
-  sketch       the same steps scored on the int8 key sketch (Sec. 4.4
-               asymmetric precision): step time, scan roofline on its own
-               bytes, selection agreement with the 16-bit path
+  sketch, sketch4  the same steps scored on the int8 / int4 key sketch
+               (Sec. 4.4 asymmetric precision): step time, scan roofline on
+               its own bytes, selection agreement with the 16-bit path
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
 ``--copy-calib`` (plain copy of known size, for counter calibration),
+``--read-ceiling`` (a plain streaming read at the scan's sizes),
 ``--summarize DIR`` (condense rocprofv3 output under DIR into text),
 ``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs).
 """
@@ -700,7 +701,7 @@ def main():
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--n-tokens", type=int, default=None, help="context length override (a variant of the workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-sketch", action="store_true", help="skip the int8-sketch variant of the step")
+    ap.add_argument("--no-sketch", action="store_true", help="skip the int8 / int4 sketch variants of the step")
     ap.add_argument("--no-bkp", action="store_true", help="skip timing the hot/cold pool pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
