@@ -80,3 +80,25 @@ def test_sketch_step_at_the_maximum_context(nbits):
     s_ref = O.update(O.logits_i8(q8, eq, k8, ek), np.zeros((1, 1, N_MAX)), 2, "attn", "token", 1 / math.sqrt(128))
     check_scores(s.cpu().numpy(), s_ref, "max sketch%d S" % nbits)
     check_selection(idx.cpu().numpy(), s_ref, k_sel, "max sketch%d sel" % nbits)
+
+
+@pytest.mark.parametrize("mode,gran", [("raw", "kvhead"), ("attn", "kvhead"), ("raw", "token")])
+def test_long_context_modes(mode, gran):
+    """A 262,144-token context in the other score modes and granularities
+    (RAW sums, one row per KV head), one step against the oracle."""
+    import paper_2602_18750_amd as H
+    n = 1 << 18
+    say("long context", mode, gran)
+    x = W.make_random(1, 8, 2, 128, n, "fp16", steps=1, seed=77 + len(mode) + len(gran), device=DEV)
+    k_sel = H.budget_k(n, 0.05)
+    R = 1 if gran == "token" else 2
+    s = H.new_importance(1, R, n, DEV)
+    idx, out = H.hill_step(x.q[0], x.k, x.v, s, k_sel, mode=mode, granularity=gran)
+    torch.cuda.synchronize()
+    qc, kc, vc = bits(x.q.cpu()), bits(x.k.cpu()), bits(x.v.cpu())
+    s_ref, _, _ = O.step(qc[0], kc, vc, np.zeros((1, R, n)), k_sel, "fp16", mode, gran)
+    check_scores(s.cpu().numpy(), s_ref, "long %s %s S" % (mode, gran))
+    idx_g = idx.cpu().numpy()
+    check_selection(idx_g, s_ref, k_sel, "long %s %s sel" % (mode, gran))
+    own = O.sparse_attn(qc[0], kc, vc, idx_g, "fp16", gran)
+    check_outputs(out.cpu().numpy(), own, "long %s %s out" % (mode, gran))
