@@ -45,7 +45,7 @@ struct Shape {
 //   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins) | hist2x [3,rows,4096+64] (the
 //            streamed selection's further second-digit windows, hist2 continued) -- cleared by the first kernel of
 //            every call that accumulates into them
-//   scount [rows,ceil(n/256)] u32 | spairs [rows,n] uint2 (key, token) | sd0 [rows] u32 (streamed selection only)
+//   scount [rows,ceil(n/256),8] u32 | spairs [rows,n] uint2 (key, token) | sd0 [rows] u32 (streamed selection only)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
 //   sel_list [rows,n] i32 | sel_n [rows,nchunks] u32
 //   slots: attention partials [B,Hq,nslots,D] fp32 and [B,Hq,nslots] float2, nslots =
@@ -89,7 +89,7 @@ Layout layout_for(const Shape& s, int ksel)
     L.zero_words_stream = (int64_t)((zero_end - L.zero) / sizeof(uint32_t));
     off = align256(zero_end);
     L.scount = off;
-    if (attn) off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * sizeof(uint32_t));
+    if (attn) off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * kSlotWords * sizeof(uint32_t));
     L.spairs = off;
     if (attn) off += align256(rows * (size_t)s.n * sizeof(uint2));
     L.sd0 = off;

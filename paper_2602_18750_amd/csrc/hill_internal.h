@@ -76,7 +76,7 @@ struct UpdateArgs {
     const uint4* prev;       // [B*R, 2] caller's state (see StreamState)
     uint2* spairs;           // [B*R, n] (key, token) of every token whose first digit >= the bound's:
                              //   update block u's at u * kUpdChunk
-    uint32_t* scount;        // [B*R, nup] pairs of each update block (nup = ceil(n / kUpdChunk))
+    uint32_t* scount;        // [B*R, nup, kSlotWords] pairs of each update block per class (nup = ceil(n / kUpdChunk))
     uint32_t* d0;            // [B*R] the bound's first digit | 0x80000000 if the bound held
     uint32_t* hist2;         // [kStreamBins, B*R, kHistRow] second-digit counts of the keys in first-digit
                              //   bin d0 + w (w = 0: the selection's usual second-digit histogram)
@@ -127,7 +127,7 @@ struct RefineArgs {
     int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) are always selected (lo == hi: all)
     // streamed selection: the update's candidate pairs replace the refine pass
     const uint2* spairs;     // [rows, n] update block u's pairs at u * kUpdChunk
-    const uint32_t* scount;  // [rows, nup] pairs of each update block
+    const uint32_t* scount;  // [rows, nup, kSlotWords] pairs of each update block per class
     const uint32_t* d0;      // [rows] the bound's first digit | 0x80000000 if the bound held
     // hist2 continues as [kStreamBins, rows, kHistRow]: second digits of first-digit bins d0 + w
     uint4* state_out;        // [rows, 2] this step's threshold bound, for the next step (streamed
@@ -161,6 +161,12 @@ inline int emit_kv_per_wg(int B, int Hkv, int nchunks, int R)
     while (h * 2 <= Hkv && Hkv % (h * 2) == 0 && (int64_t)B * nchunks * (Hkv / (h * 2)) >= target) h *= 2;
     return h;
 }
+// Streamed selection: the pairs of an update block are grouped in kPairClasses
+// classes (the kStreamBins window bins, then every key above the window); the
+// block's class counts take kSlotWords words.
+constexpr int kPairClasses = kStreamBins + 1;
+constexpr int kSlotWords = 8;
+static_assert(kPairClasses <= kSlotWords, "class counts fit a slot");
 constexpr int kMaxSlots = 4096;   // partial slots merged per head (splits or chunks)
 
 // Optional start/stop timestamps of one launch (hipExtLaunchKernel events).

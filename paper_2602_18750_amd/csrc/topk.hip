@@ -250,29 +250,37 @@ __device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int
     }
 }
 
-// Streamed selection: calls f(key, token) for every (key, token) pair the
-// update listed for the row (fast: they include every key of the threshold's
-// first-digit bin), or for every token of the row with its selection key
-// (slow: the bound did not hold).  The pairs sit in per-update-block slots;
-// groups of up to 256 slots are flattened with one block scan of their counts
-// (offsets in `offs`, 256 words of LDS) and a binary search per pair, so all
-// loads of a round are in flight together.  Every thread of the block calls it.
+// Streamed selection: calls f(key, token) for every (key, token) pair of
+// class cls that the update listed for the row (fast: the class holds every
+// key of the first-digit bin in question), or for every token of the row with
+// its selection key (slow: the bound did not hold).  The pairs sit in
+// per-update-block slots, grouped by class; groups of up to 256 slots are
+// flattened with one block scan of the class counts (offsets in `offs`, the
+// class's start in each slot in `starts`, 256 words of LDS each) and a binary
+// search per pair, so all loads of a round are in flight together.  Every
+// thread of the block calls it.
 template <typename F>
-__device__ __forceinline__ void for_row_pairs(const RefineArgs& r, int row, bool fast, uint32_t* offs,
-                                              uint32_t* scratch, F f)
+__device__ __forceinline__ void for_row_pairs(const RefineArgs& r, int row, bool fast, int cls, uint32_t* offs,
+                                              uint32_t* starts, uint32_t* scratch, F f)
 {
     constexpr int kU = 8;
     const uint32_t tid = threadIdx.x;
     if (fast) {
         const int nup = (r.n + kUpdChunk - 1) / kUpdChunk;
-        const uint32_t* cnt = r.scount + (int64_t)row * nup;
+        const uint32_t* cnt = r.scount + (int64_t)row * nup * kSlotWords;
         const uint2* pr = r.spairs + (int64_t)row * r.n;
         for (int g0 = 0; g0 < nup; g0 += kThreads) {
             const int ng = min(kThreads, nup - g0);
-            const uint32_t c = (int)tid < ng ? cnt[g0 + tid] : 0u;
+            uint32_t c = 0u, st = 0u;
+            if ((int)tid < ng) {
+                const uint32_t* cs = cnt + (int64_t)(g0 + tid) * kSlotWords;
+                for (int k = 0; k < cls; ++k) st += cs[k];
+                c = cs[cls];
+            }
             uint32_t tot;
             const uint32_t o = block_excl_scan<kThreads>(c, scratch, &tot);
             offs[tid] = o;
+            starts[tid] = st;
             __syncthreads();
             for (uint32_t i0 = 0; i0 < tot; i0 += kThreads * kU) {
                 uint2 v[kU];
@@ -286,14 +294,14 @@ __device__ __forceinline__ void for_row_pairs(const RefineArgs& r, int row, bool
                             const int mid = (lo + hi + 1) >> 1;
                             if (offs[mid] <= i) lo = mid; else hi = mid - 1;
                         }
-                        v[u] = pr[(int64_t)(g0 + lo) * kUpdChunk + (i - offs[lo])];
+                        v[u] = pr[(int64_t)(g0 + lo) * kUpdChunk + starts[lo] + (i - offs[lo])];
                     }
                 }
 #pragma unroll
                 for (int u = 0; u < kU; ++u)
                     if (i0 + u * kThreads + tid < tot) f(v[u].x, v[u].y);
             }
-            __syncthreads();   // offs is rewritten by the next group
+            __syncthreads();   // offs and starts are rewritten by the next group
         }
     } else {
         const float* srow = row_ptr(r, row);
@@ -333,6 +341,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     __shared__ uint32_t hist3[256];
     __shared__ typename std::conditional<STREAM, uint32_t[kHistBins], uint32_t[1]>::type hist2s;
     __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_offs;
+    __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_starts;
     __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t red[kThreads / 64];
     __shared__ uint32_t res[3];
@@ -368,6 +377,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     int shift;
     bool all_eq;
     bool fast = true;   // streamed: the update's pairs hold every key of the threshold's first-digit bin
+    int pair_cls = kStreamBins;   // streamed: the class of the update's pairs that holds that bin
     if constexpr (STREAM) {
         // first digit from the update's histogram (complete, or with a valid
         // bound complete from the bound's bin upward); the second from the update's
@@ -383,6 +393,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         const uint32_t b1 = res[0] & (kHistBins - 1), need1 = res[1], in1 = res[2];
         const uint32_t d0 = bnd & (kHistBins - 1);
         fast = b1 >= d0;
+        pair_cls = ((bnd >> 31) && b1 - d0 < (uint32_t)kStreamBins) ? (int)(b1 - d0) : kStreamBins;
         prefix = b1;
         need = need1;
         shift = 20;
@@ -403,7 +414,9 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
                 uint32_t* h2s = hist2s;
                 for (int i = tid; i < kHistBins; i += kThreads) h2s[i] = 0u;
                 __syncthreads();
-                for_row_pairs(r, row, fast, pair_offs, scan_scratch, [b1, h2s](uint32_t kk, uint32_t) {
+                // the threshold's bin lies above the window (or there is no bound): class kStreamBins
+                for_row_pairs(r, row, fast, kStreamBins, pair_offs, pair_starts, scan_scratch,
+                              [b1, h2s](uint32_t kk, uint32_t) {
                     if ((kk >> 20) == b1) atomicAdd(&h2s[(kk >> 8) & (kHistBins - 1)], 1u);
                 });
                 __syncthreads();
@@ -421,7 +434,8 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
                 for (int i = tid; i < 256; i += kThreads) h3[i] = 0u;
                 __syncthreads();
                 const uint32_t p2 = prefix;
-                for_row_pairs(r, row, fast, pair_offs, scan_scratch, [p2, h3](uint32_t kk, uint32_t) {
+                for_row_pairs(r, row, fast, pair_cls, pair_offs, pair_starts, scan_scratch,
+                              [p2, h3](uint32_t kk, uint32_t) {
                     if ((kk >> 8) == p2) atomicAdd(&h3[kk & 0xffu], 1u);
                 });
                 __syncthreads();
@@ -502,7 +516,8 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         const uint32_t pf = prefix;
         if constexpr (STREAM) {
             const uint32_t jlim = (uint32_t)c * kSelChunk;
-            for_row_pairs(r, row, fast, pair_offs, scan_scratch, [&before_chunks, pf, jlim](uint32_t kk, uint32_t j) {
+            for_row_pairs(r, row, fast, pair_cls, pair_offs, pair_starts, scan_scratch,
+                          [&before_chunks, pf, jlim](uint32_t kk, uint32_t j) {
                 before_chunks += (kk == pf && j < jlim) ? 1u : 0u;
             });
         } else {

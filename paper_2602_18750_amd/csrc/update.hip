@@ -102,37 +102,57 @@ __device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, int row)
 }
 
 // Streamed selection: the block's tokens whose first digit reaches the bound
-// go to the block's slot of the row's (key, token) list, in token order, with
-// their count; those in the bound's first-digit bin or the next few also count
-// their second digit (the threshold seldom moves further in one step).
+// go to the block's slot of the row's (key, token) list, grouped by class --
+// the key's window bin (the bound's first-digit bin or one of the next
+// kStreamBins - 1) or, for every key above the window (and for every key when
+// there is no bound), class kStreamBins -- with the counts of the classes, so
+// that a walk for one first-digit bin reads one class only.  Keys in the
+// window also count their second digit (the threshold seldom moves further
+// in one step).
 static_assert(kStreamBins * kCoarseBins == 256, "one window coarse bin per update thread");
 
 __device__ __forceinline__ void stream_candidates(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                                  uint32_t* scratch, uint32_t* coarse)
+                                                  uint32_t (*wcnt)[4], uint32_t* coarse)
 {
     const uint32_t d0 = bnd & (kHistBins - 1);
     const uint32_t dig = key >> (32 - kHistBits);
     const bool cand = j < a.n && dig >= d0;
     const uint32_t wdx = dig - d0;   // window bin of the key (valid when cand)
     const bool win = cand && (bnd >> 31) && wdx < (uint32_t)kStreamBins;
+    const int cls = win ? (int)wdx : kStreamBins;
     const int64_t rows = (int64_t)a.B * a.R;
     if (win) {   // fine bins spread out: straight to memory; the few coarse bins are summed in LDS first
         atomicAdd(&a.hist2[((int64_t)wdx * rows + row) * kHistRow + ((key >> 8) & (kHistBins - 1))], 1u);
         atomicAdd(&coarse[wdx * kCoarseBins + ((key >> 14) & (kCoarseBins - 1))], 1u);
     }
-    uint32_t tot;
-    const uint32_t pos = block_excl_scan_1b(cand ? 1u : 0u, scratch, &tot);   // its barrier completes `coarse`
+    // rank within the class: one ballot per class, wave counts through LDS
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint64_t below = (1ull << lane) - 1ull;
+    uint32_t rank = 0;
+#pragma unroll
+    for (int k = 0; k < kPairClasses; ++k) {
+        const uint64_t m = __ballot(cand && cls == k);
+        if (cand && cls == k) rank = (uint32_t)__popcll(m & below);
+        if (lane == 0) wcnt[k][w] = (uint32_t)__popcll(m);
+    }
+    __syncthreads();   // also completes `coarse`
     if (bnd >> 31) {
         const int i = threadIdx.x;   // kStreamBins * kCoarseBins == 256 bins, one per thread
         const uint32_t c = coarse[i];
         if (c) atomicAdd(&a.hist2[((int64_t)(i / kCoarseBins) * rows + row) * kHistRow + kHistBins + i % kCoarseBins], c);
     }
-    if (cand) a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
-    if (threadIdx.x == 0) {
-        const int nup = (a.n + kUpdChunk - 1) / kUpdChunk;
-        a.scount[(int64_t)row * nup + blockIdx.x] = tot;
-        if (blockIdx.x == 0) a.d0[row] = bnd;
+    if (cand) {
+        uint32_t pos = rank;
+        for (int k = 0; k < cls; ++k) pos += (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+        for (int v = 0; v < w; ++v) pos += wcnt[cls][v];
+        a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
     }
+    const int nup = (a.n + kUpdChunk - 1) / kUpdChunk;
+    if (threadIdx.x < kPairClasses) {
+        const int k = threadIdx.x;
+        a.scount[((int64_t)row * nup + blockIdx.x) * kSlotWords + k] = (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+    }
+    if (threadIdx.x == 0 && blockIdx.x == 0) a.d0[row] = bnd;
 }
 
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
@@ -234,7 +254,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     __shared__ KeyHist kh;
     __shared__ float2 red[256];
     __shared__ float2 ms[256];
-    __shared__ uint32_t sc_scratch[4];
+    __shared__ uint32_t sc_wcnt[kPairClasses][4];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
@@ -306,7 +326,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
         __syncthreads();
         hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)row * kHistRow);
     }
-    if (a.prev) stream_candidates(a, row, j, key, bnd, sc_scratch, sc_coarse);   // block-uniform
+    if (a.prev) stream_candidates(a, row, j, key, bnd, sc_wcnt, sc_coarse);   // block-uniform
 }
 
 // Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j] (same layout).
