@@ -15,14 +15,21 @@ in HBM before timing starts; the 4 GiB of K+V exceed the 256 MB Infinity
 Cache, so every layer's keys come from HBM.
 
 Prints one JSON line:
-  value        GB/s of keys scanned by the whole step (all layers, scoring +
-               selection + attention): K bytes per step / step time
+  value        scoring GB/s: the keys of one layer (B*Hkv*n*D*2 bytes) over
+               the scoring stage of one layer-step (the key scan plus the
+               normaliser and S update), with each stage's duration taken from
+               start/stop timestamps that its own dispatch stamps into HIP
+               events (one probe layer per step, on the library's stream)
+  ms_per_step  wall time of one decode step through all layers (timed region
+               bracketed by device synchronisations)
   roofline     the key-scan kernel (score_tiles): algorithmic bytes per
-               launch / its mean duration, from start/stop timestamps that
-               the kernel's own dispatch stamps into HIP events (the step's
-               event argument, on the library's stream), vs 8 TB/s
-  scoring_*    the scoring stage (scan + normaliser + S update)
-  select_attn_us_per_layer_step   selection + gather attention, per layer-step
+               launch / its mean duration (the scan stage's events) vs 8 TB/s
+  stage_us     mean duration per stage of a layer-step (scan, update,
+               select, merge; refine in the plain leg)
+  select_attn_us_per_layer_step   select + merge stages (selection, gather,
+               attention over the selected tokens, merge of the partials),
+               beside dense_decode_bound_us, the time to read all K and V of
+               a layer once at 8 TB/s
   plain        the same steps through hill_step (refine pass, five launches)
   bkp          the hot/cold pool pass after each layer's step (Sec. 4.2 BKP)
   sketch, sketch4  the same steps scored on the int8 / int4 key sketch
@@ -33,6 +40,8 @@ Prints one JSON line:
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
 ``--copy-calib`` (plain copy of known size, for counter calibration),
 ``--read-ceiling`` (a plain streaming read at the scan's sizes),
+``--selection-stats`` (heavy-hitter recall of the Qwen-7B-shaped workload and
+the step-to-step selection overlap of the AR(1) workload),
 ``--summarize DIR`` (condense rocprofv3 output under DIR into text),
 ``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs).
 """
@@ -97,6 +106,26 @@ class HipEvents:
         self.made = []
 
 
+class StageProbe:
+    """Start/stop events for every stage of one decode step (include/hill.h
+    HILL_STAGE_*), and the stage durations they measured."""
+
+    def __init__(self, hip: HipEvents, H):
+        self.hip, self.stages = hip, H.hill.STAGES
+        self.start = [hip.create() for _ in self.stages]
+        self.stop = [hip.create() for _ in self.stages]
+        self.ev = H.HillStepEvents.of([e.value for e in self.start], [e.value for e in self.stop])
+
+    def us(self, stage: str) -> float:
+        i = self.stages.index(stage)
+        return self.hip.ms(self.start[i], self.stop[i]) * 1e3
+
+
+def stage_means(probes, stages):
+    """Mean duration (us) of each named stage over the probes."""
+    return {st: sum(p.us(st) for p in probes) / len(probes) for st in stages}
+
+
 # ------------------------------------------------------------ byte counts --
 
 def scan_kernel_bytes(B, Hq, Hkv, D, n, mode="attn"):
@@ -157,10 +186,20 @@ def cpu_baseline(w, seconds: float):
             break
     kbytes = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
     per = t_total / done
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {
         "value": round(kbytes / per / 1e9, 4),
         "unit": "GB/s",
         "cores": O.num_threads(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+        "cpu_model": model,
         "kind": "oracle",
         "sample": "%d decode steps of layer 0 (B=%d, n=%d, GQA %d/%d, %s, k=%d), S carried; "
                   "%.1f ms per layer-step (score %.1f, select %.1f, attention %.1f)" % (
@@ -212,10 +251,7 @@ def run_bench(args):
     torch.cuda.synchronize()
 
     hip = HipEvents()
-    ev_sets = []
-    for _ in range(args.steps):
-        e = [hip.create() for _ in range(6)]
-        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+    probes = [StageProbe(hip, H) for _ in range(args.steps)]
 
     for i in range(args.warmup):
         for L in range(nl_run):
@@ -228,37 +264,28 @@ def run_bench(args):
         probe = i % nl_run        # one timestamped layer per step, rotating
         for L in range(nl_run):
             if L == probe:
-                calls[L](qptrs[L][t], ev_sets[i][1])
+                calls[L](qptrs[L][t], probes[i].ev)
             else:
                 calls[L](qptrs[L][t])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
 
-    # e: scan_start, scan_stop, score_stop, select_start, select_stop, attn_stop
-    scan, score, selattn, total = [], [], [], []
-    for e, _ in ev_sets:
-        scan.append(hip.ms(e[0], e[1]))
-        score.append(hip.ms(e[0], e[2]))
-        selattn.append(hip.ms(e[2], e[5]))
-        total.append(hip.ms(e[0], e[5]))
+    st = stage_means(probes, ("scan", "update", "select", "merge"))
     hip.close()
-
-    def mean(xs):
-        return sum(xs) / len(xs)
 
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)   # one decode step = nl layer-steps
     kbytes_layer = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
-    value = kbytes_layer * nl / (ms_step * 1e-3) / 1e9
+    vbytes_layer = kbytes_layer
     scan_bytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
-    scan_us = mean(scan) * 1e3
+    scan_us = st["scan"]
     achieved = scan_bytes / (scan_us * 1e-6) / 1e9
-    score_us = mean(score) * 1e3
+    score_us = st["scan"] + st["update"]
     scoring_gbs = kbytes_layer / (score_us * 1e-6) / 1e9
     traffic = load_traffic() if w.id == COUNTERS_WORKLOAD else None
 
     res = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": round(scoring_gbs, 1),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -288,12 +315,13 @@ def run_bench(args):
             "algorithmic_bytes_per_launch": scan_bytes,
             "mean_launch_us": round(scan_us, 3),
         },
-        "scoring_gbps": round(scoring_gbs, 1),
         "scoring_frac_hbm": round(scoring_gbs / HBM_PEAK_GBS, 4),
         "scoring_us_per_layer_step": round(score_us, 3),
-        "select_attn_us_per_layer_step": round(mean(selattn) * 1e3, 3),
-        "layer_step_us_probe": round(mean(total) * 1e3, 3),
+        "select_attn_us_per_layer_step": round(st["select"] + st["merge"], 3),
+        "dense_decode_bound_us": round((kbytes_layer + vbytes_layer) / (HBM_PEAK_GBS * 1e3), 3),
+        "stage_us": {k: round(v, 3) for k, v in st.items()},
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
+        "step_keys_gbps": round(kbytes_layer * nl / (ms_step * 1e-3) / 1e9, 1),
     }
     res["plain"] = bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_bkp:
@@ -319,10 +347,7 @@ def bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
     calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream) for L, (x, _) in enumerate(layers)]
     hip = HipEvents()
-    ev_sets = []
-    for _ in range(args.steps):
-        e = [hip.create() for _ in range(6)]
-        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+    probes = [StageProbe(hip, H) for _ in range(args.steps)]
     for i in range(args.warmup):
         for L in range(nl_run):
             calls[L](qptrs[L][i % T])
@@ -333,23 +358,22 @@ def bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
         probe = i % nl_run
         for L in range(nl_run):
             if L == probe:
-                calls[L](qptrs[L][t], ev_sets[i][1])
+                calls[L](qptrs[L][t], probes[i].ev)
             else:
                 calls[L](qptrs[L][t])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    score = sum(hip.ms(e[0], e[2]) for e, _ in ev_sets) / len(ev_sets)
-    sel = sum(hip.ms(e[3], e[4]) for e, _ in ev_sets) / len(ev_sets)
-    selattn = sum(hip.ms(e[2], e[5]) for e, _ in ev_sets) / len(ev_sets)
+    st = stage_means(probes, ("scan", "update", "refine", "select", "merge"))
     hip.close()
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
     del calls, ss
     return {
         "ms_per_step": round(ms_step, 4),
-        "value_gbps": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl / (ms_step * 1e-3) / 1e9, 2),
-        "scoring_us_per_layer_step": round(score * 1e3, 3),
-        "select_kernel_us": round(sel * 1e3, 3),
-        "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
+        "step_keys_gbps": round(w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2 * nl / (ms_step * 1e-3) / 1e9,
+                                1),
+        "scoring_us_per_layer_step": round(st["scan"] + st["update"], 3),
+        "select_attn_us_per_layer_step": round(st["refine"] + st["select"] + st["merge"], 3),
+        "stage_us": {k: round(v, 3) for k, v in st.items()},
         "launches_per_layer_step": 5,
     }
 
@@ -406,10 +430,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
     calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L],
                         stream_state=states[L]) for L, (x, _) in enumerate(layers)]
     hip = HipEvents()
-    ev_sets = []
-    for _ in range(args.steps):
-        e = [hip.create() for _ in range(6)]
-        ev_sets.append((e, H.HillStepEvents(*[x.value for x in e])))
+    probes = [StageProbe(hip, H) for _ in range(args.steps)]
     for i in range(args.warmup):
         for L in range(nl_run):
             calls[L](qptrs[L][i % T])
@@ -420,14 +441,15 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
         probe = i % nl_run
         for L in range(nl_run):
             if L == probe:
-                calls[L](qptrs[L][t], ev_sets[i][1])
+                calls[L](qptrs[L][t], probes[i].ev)
             else:
                 calls[L](qptrs[L][t])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    scan = sum(hip.ms(e[0], e[1]) for e, _ in ev_sets) / len(ev_sets)
-    score = sum(hip.ms(e[0], e[2]) for e, _ in ev_sets) / len(ev_sets)
-    selattn = sum(hip.ms(e[2], e[5]) for e, _ in ev_sets) / len(ev_sets)
+    st = stage_means(probes, ("scan", "update", "select", "merge"))
+    scan = st["scan"] * 1e-3                     # ms
+    score = (st["scan"] + st["update"]) * 1e-3
+    selattn = (st["select"] + st["merge"]) * 1e-3
     hip.close()
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
     units = (w.n_tokens + 255) // 256
@@ -457,6 +479,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
         "scan_traffic": traffic if w.id == COUNTERS_WORKLOAD else None,
         "scoring_us_per_layer_step": round(score * 1e3, 3),
         "select_attn_us_per_layer_step": round(selattn * 1e3, 3),
+        "stage_us": {k: round(v, 3) for k, v in st.items()},
         "selection_recall_vs_16bit": round(recall, 4),
     }
 
@@ -483,16 +506,19 @@ def run_sweep(args):
         ws = H.workspace(H.make_desc(x.q[0], x.k, x.v, s), w.k_sel, dev)
         calls = [H.StepCall(x.q[0], ks[r], vs[r], s, w.k_sel, ws=ws, stream=stream) for r in range(reps)]
         iters = max(20, reps)
-        evs = [[hip.create() for _ in range(6)] for _ in range(iters)]
+        probes = [StageProbe(hip, H) for _ in range(iters)]
         for r in range(reps):
             calls[r](x.q[0].data_ptr())
         torch.cuda.synchronize()
         for i in range(iters):
-            calls[i % reps](x.q[0].data_ptr(), H.HillStepEvents(*[e.value for e in evs[i]]))
+            calls[i % reps](x.q[0].data_ptr(), probes[i].ev)
         torch.cuda.synchronize()
-        scan = sorted(hip.ms(e[0], e[1]) for e in evs)[iters // 2]
-        score = sorted(hip.ms(e[0], e[2]) for e in evs)[iters // 2]
-        selattn = sorted(hip.ms(e[2], e[5]) for e in evs)[iters // 2]
+
+        def med(f):
+            return sorted(f(p) for p in probes)[iters // 2] * 1e-3   # ms
+        scan = med(lambda p: p.us("scan"))
+        score = med(lambda p: p.us("scan") + p.us("update"))
+        selattn = med(lambda p: p.us("refine") + p.us("select") + p.us("merge"))
         nbytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
         kbytes = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
         print(json.dumps({
@@ -505,6 +531,56 @@ def run_sweep(args):
         del calls, ks, vs, x, s
         hip.close()
         torch.cuda.empty_cache()
+
+
+def run_selection_stats(args):
+    """Statistics of the selections the path makes (not pass/fail; the GPU
+    tests hold the same figures against the oracle):
+    * Qwen-7B-shaped workload (32 layers, B 8, 4096 tokens, 5% heavy-hitter
+      keys scaled 4x): the fraction of heavy-hitter tokens inside the selected
+      set of one decode step, per layer and overall;
+    * the AR(1) workload (B 4, 131072 tokens, 16 decode steps, streamed
+      selection as in the benchmark): the overlap |I_t & I_(t-1)| / k of
+      consecutive selections per step (temporal locality, Sec. 4.2)."""
+    import torch
+    import paper_2602_18750_amd as H
+    from paper_2602_18750_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    w = W.WORKLOADS[2]
+    recalls = []
+    for L in range(w.layers):
+        x = W.make_layer(w, L, device=dev)
+        s = H.new_importance(w.batch, 1, w.n_tokens, dev)
+        idx, _ = H.hill_step(x.q[0], x.k, x.v, s, w.k_sel)
+        torch.cuda.synchronize()
+        hv = x.heavy.to(dev).long()
+        chosen = torch.zeros(w.batch, w.n_tokens, dtype=torch.bool, device=dev)
+        chosen.scatter_(1, idx[:, 0].long(), True)
+        recalls.append(float(torch.gather(chosen, 1, hv).float().mean()))
+        del x, s, idx
+    print(json.dumps({"workload": w.name, "statistic": "heavy-hitter recall in the selected set",
+                      "k_sel": w.k_sel, "heavy_per_row": int(W.HEAVY_FRACTION * w.n_tokens),
+                      "per_layer": [round(r, 4) for r in recalls],
+                      "mean": round(sum(recalls) / len(recalls), 4), "min": round(min(recalls), 4)}), flush=True)
+
+    w = W.WORKLOADS[4]
+    x = W.make_layer(w, 0, device=dev)
+    s = H.new_importance(w.batch, 1, w.n_tokens, dev)
+    state = H.new_stream_state(w.batch, 1, dev)
+    call = H.StepCall(x.q[0], x.k, x.v, s, w.k_sel, stream_state=state)
+    prev, overlap = None, []
+    for t in range(w.steps):
+        call(x.q[t].data_ptr())
+        torch.cuda.synchronize()
+        cur = torch.zeros(w.batch, w.n_tokens, dtype=torch.bool, device=dev)
+        cur.scatter_(1, call.idx[:, 0].long(), True)
+        if prev is not None:
+            overlap.append(float((cur & prev).sum(1).float().mean()) / w.k_sel)
+        prev = cur
+    print(json.dumps({"workload": w.name, "statistic": "overlap |I_t & I_(t-1)| / k of consecutive selections",
+                      "k_sel": w.k_sel, "steps": w.steps, "per_step": [round(o, 4) for o in overlap],
+                      "mean": round(sum(overlap) / len(overlap), 4)}), flush=True)
 
 
 def run_copy_calib(args):
@@ -526,12 +602,21 @@ def run_copy_calib(args):
 
 def run_read_ceiling(args):
     """What a single plain streaming-read launch reaches at the scan's sizes:
-    the library's calibration read (hill_calib_read: 16-byte non-temporal
+    the calibration read (libhill_calib.so hill_calib_read: 16-byte non-temporal
     loads, eight in flight per lane, one contiguous share per workgroup) over
     16 MiB .. 1 GiB, the best of a few grid sizes, rotated through replicas so
     that at least 1 GiB is touched between reuses; event-timed like the scan."""
     import torch
-    import paper_2602_18750_amd as H
+    from paper_2602_18750_amd import _build
+    lib = ctypes.CDLL(_build.CALIB_LIB)
+    lib.hill_calib_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    lib.hill_calib_read.restype = ctypes.c_int
+
+    def calib_read(buf, grid, sink, stream):
+        rc = lib.hill_calib_read(buf.data_ptr(), buf.numel(), grid, sink.data_ptr(), stream.cuda_stream)
+        if rc != 0:
+            raise RuntimeError("hill_calib_read failed (%d)" % rc)
+
     stream = torch.cuda.current_stream()
     sink = torch.empty(65536, dtype=torch.int32, device="cuda:0")
     for mib in (16, 32, 64, 256, 1024):
@@ -540,13 +625,13 @@ def run_read_ceiling(args):
         best = None
         for grid in (1024, 2048, 4096, 8192):
             for x in xs:
-                H.calib_read(x, grid, sink, stream=stream)
+                calib_read(x, grid, sink, stream)
             torch.cuda.synchronize()
             iters = max(20, reps)
             ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
             for i in range(iters):
                 ev[i][0].record(stream)
-                H.calib_read(xs[i % reps], grid, sink, stream=stream)
+                calib_read(xs[i % reps], grid, sink, stream)
                 ev[i][1].record(stream)
             torch.cuda.synchronize()
             ts = sorted(a.elapsed_time(b) for a, b in ev)
@@ -706,7 +791,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--copy-calib", action="store_true")
-    ap.add_argument("--read-ceiling", action="store_true", help="time a plain library streaming read at the scan's sizes")
+    ap.add_argument("--read-ceiling", action="store_true", help="time a plain streaming read at the scan's sizes")
+    ap.add_argument("--selection-stats", action="store_true",
+                    help="heavy-hitter recall (Qwen-7B-shaped) and step-to-step selection overlap (AR(1) workload)")
     ap.add_argument("--summarize", metavar="DIR")
     ap.add_argument("--counters", metavar="DIR", help="write the score_tiles traffic record from --pmc runs under DIR")
     ap.add_argument("--counters-command", default="", help="command line recorded with --counters")
@@ -728,6 +815,8 @@ def main():
         run_copy_calib(args)
     elif args.read_ceiling:
         run_read_ceiling(args)
+    elif args.selection_stats:
+        run_selection_stats(args)
     elif args.sweep:
         run_sweep(args)
     else:

@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define HILL_ABI_VERSION 5
+#define HILL_ABI_VERSION 6
 
 /* The library exports these entry points only (built with hidden visibility). */
 #define HILL_API __attribute__((visibility("default")))
@@ -164,18 +164,44 @@ HILL_API hill_status hill_step(const hill_desc* d, const void* q, const void* k,
                       float* s, int32_t k_sel, int32_t* idx_out, float* out,
                       void* ws, size_t ws_bytes, void* stream);
 
-/* Kernel timestamps for profiling hill_step.  Each non-NULL member is a
- * caller-created hipEvent_t (hipEventCreate, timing enabled) that the named
- * kernel boundary stamps: the kernels are launched with hipExtLaunchKernel's
- * start/stop events, so no extra work is enqueued and elapsed times between
- * members are GPU execution times. */
+/* Kernel timestamps for profiling a decode step.  A step runs as a chain of
+ * kernel launches on the caller's stream; each launch belongs to one stage:
+ *
+ *   HILL_STAGE_SCAN     streams the keys: q.K^T of every cached token (ATTN:
+ *                       logits and per-256-token softmax partials; RAW with
+ *                       one row per KV head: added straight into S)
+ *   HILL_STAGE_STATS    ATTN rows longer than 32768 tokens only: the softmax
+ *                       normaliser of every head
+ *   HILL_STAGE_UPDATE   S += the step's weights, and the selection's first
+ *                       radix digit histogram (RAW per-KV-head rows: only
+ *                       the histogram)
+ *   HILL_STAGE_REFINE   the threshold's first-digit bin and the second-digit
+ *                       histogram (hill_step, and reset steps of the
+ *                       streamed selection)
+ *   HILL_STAGE_SELECT   the exact threshold, each chunk's selected tokens and
+ *                       the attention partials over them
+ *   HILL_STAGE_MERGE    the partials merged into the output, the ordered
+ *                       index list written
+ *
+ * Each non-NULL start[i] / stop[i] is a caller-created hipEvent_t
+ * (hipEventCreate, timing enabled) that stage i's launch stamps when it
+ * starts / ends: the kernels are launched with hipExtLaunchKernel's start and
+ * stop events, so no extra work is enqueued, and elapsed times between them
+ * are GPU execution times.  Events of stages a call does not run are left
+ * untouched. */
+enum {
+    HILL_STAGE_SCAN = 0,
+    HILL_STAGE_STATS = 1,
+    HILL_STAGE_UPDATE = 2,
+    HILL_STAGE_REFINE = 3,
+    HILL_STAGE_SELECT = 4,
+    HILL_STAGE_MERGE = 5,
+    HILL_STAGES = 6
+};
+
 typedef struct hill_step_events {
-    void* scan_start;    /* start of the kernel that streams the keys (q.K^T) */
-    void* scan_stop;     /* end of that kernel */
-    void* score_stop;    /* end of the last kernel that updates S */
-    void* select_start;  /* start of the first selection kernel (threshold refinement) */
-    void* select_stop;   /* end of it */
-    void* attn_stop;     /* end of the last attention kernel (output written) */
+    void* start[HILL_STAGES];
+    void* stop[HILL_STAGES];
 } hill_step_events;
 
 /* hill_step with kernel timestamps (ev may be NULL: then identical to hill_step).
@@ -194,14 +220,17 @@ HILL_API hill_status hill_step_profiled(const hill_desc* d, const void* q, const
  * identical to hill_step.
  *
  * state: uint32 [B, R, 8], 16-byte aligned, caller-owned, one per S buffer;
- * zero it at the start of a sequence and whenever S is changed outside these
- * calls.  Each call reads the bound and writes the next one.  The bound is
- * used only while it holds: the same pins, n_tokens not smaller than at the
- * previous call (growing only without pins), and k_sel at most the number of
- * tokens whose first radix digit reached the previous threshold's (usually
- * k_sel plus a few hundred, so a budget that grows with the context keeps
- * it); otherwise, and on the first call, every workgroup of the selection
- * walks the whole row instead, which is exact but slow on long rows.
+ * zero it at the start of a sequence.  Each call reads the bound and writes
+ * the next one.  The bound is used only while it holds: the same pins,
+ * n_tokens not smaller than at the previous call (growing only without pins),
+ * and k_sel at most the number of tokens whose first radix digit reached the
+ * previous threshold's (usually k_sel plus a few hundred, so a budget that
+ * grows with the context keeps it); otherwise, and on the first call, every
+ * workgroup of the selection walks the whole row instead, which is exact but
+ * slow on long rows.  If S is changed outside these calls the results stay
+ * exact: when fewer than k_sel keys then reach the bound's first digit, the
+ * selection counts that digit again over the whole row (slow); a reset step
+ * after such a change avoids the walk.
  *
  * flags: 0, or HILL_STREAM_RESET: this call selects through the refine pass
  * exactly as hill_step does (no bound read, no candidate list) and writes a
@@ -210,7 +239,7 @@ HILL_API hill_status hill_step_profiled(const hill_desc* d, const void* q, const
  * threshold bounds the next one only loosely) and after S was changed
  * outside these calls; results are the same either way.  ATTN score mode
  * only (HILL_ERR_UNSUPPORTED otherwise).  ev: as hill_step_profiled (without
- * HILL_STREAM_RESET the select interval is empty). */
+ * HILL_STREAM_RESET the REFINE stage does not run). */
 #define HILL_STREAM_RESET 1u
 HILL_API hill_status hill_step_streamed(const hill_desc* d, const void* q, const void* k, const void* v, float* s,
                                uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out,
@@ -326,14 +355,6 @@ typedef struct hill_app_plan {
 
 /* Fills *plan; HILL_ERR_INVALID_ARG for non-finite or out-of-range inputs. */
 HILL_API hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan);
-
-/* Roofline calibration (measurement aid, computes nothing of the method):
- * one launch of `grid` workgroups that reads `bytes` bytes of the device
- * buffer `buf` once, each workgroup a contiguous share, with 16-byte
- * non-temporal loads.  buf 16-byte aligned, bytes a positive multiple of 16,
- * 1 <= grid <= 65536; sink is a device array of `grid` words that the kernel
- * may write (its contents are meaningless).  Errors as for every call. */
-HILL_API hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream);
 
 #ifdef __cplusplus
 }

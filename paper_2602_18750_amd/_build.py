@@ -15,10 +15,13 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhill.so")
+# the benchmark's roofline calibration read, a library of its own (not libhill's ABI)
+CALIB_LIB = os.path.join(PKG, "libhill_calib.so")
 # per-kernel registers, scratch and occupancy as the compiler reports them
 RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
-SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", "attn.hip", "calib.hip", "bkp.hip"]
+SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", "attn.hip", "bkp.hip"]
+CALIB_SOURCES = ["calib.hip"]
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -50,7 +53,7 @@ def _compile(src: str, verbose: bool) -> str:
 def _resource_report():
     """One line per kernel: name, VGPRs, scratch bytes per lane, occupancy."""
     rows = []
-    for src in SOURCES:
+    for src in SOURCES + CALIB_SOURCES:
         path = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".resources")
         if not src.endswith(".hip") or not os.path.exists(path):
             continue
@@ -71,18 +74,24 @@ def _resource_report():
     return rows
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with ThreadPoolExecutor(max_workers=len(SOURCES)) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _link(objs, lib, verbose):
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s" % r.stderr)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = SOURCES + CALIB_SOURCES
+    with ThreadPoolExecutor(max_workers=len(srcs)) as ex:
+        objs = dict(zip(srcs, ex.map(lambda s: _compile(s, verbose), srcs)))
+    _link([objs[s] for s in SOURCES], LIB, verbose)
+    _link([objs[s] for s in CALIB_SOURCES], CALIB_LIB, verbose)
     _resource_report()
     return LIB
 

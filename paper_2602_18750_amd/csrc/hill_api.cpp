@@ -240,9 +240,10 @@ int device_cus()
     return v;
 }
 
-hipError_t mark(void* ev, hipStream_t st)
+// The start / stop events of one stage of a step (include/hill.h).
+Stamp stage(const hill_step_events& ev, int i)
 {
-    return ev ? hipEventRecord(static_cast<hipEvent_t>(ev), st) : hipSuccess;
+    return Stamp{static_cast<hipEvent_t>(ev.start[i]), static_cast<hipEvent_t>(ev.stop[i])};
 }
 
 template <typename T>
@@ -276,8 +277,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
                       const Sketch& sk, float* sacc, void* ws, bool with_hist, hipStream_t st,
                       const hill_step_events& ev, const uint4* stream_prev = nullptr, int ksel = 0)
 {
-    const Stamp scan{static_cast<hipEvent_t>(ev.scan_start), static_cast<hipEvent_t>(ev.scan_stop)};
-    const Stamp last{nullptr, static_cast<hipEvent_t>(ev.score_stop)};
+    const Stamp scan = stage(ev, HILL_STAGE_SCAN);
+    const Stamp upd = stage(ev, HILL_STAGE_UPDATE);
     uint32_t* hist = with_hist ? at<uint32_t>(ws, L.hist1) : nullptr;
     ScoreArgs a{};
     a.q = static_cast<const uint16_t*>(q);
@@ -341,21 +342,21 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         u.stats = nullptr;
         if (!update_reduces_stats(s.R == 1 ? s.Hq : s.G, s.npart)) {
             float2* stats = at<float2>(ws, L.stats);
-            HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.npart, st));
+            HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.npart, st, stage(ev, HILL_STAGE_STATS)));
             u.stats = stats;
         }
-        HIP_TRY(launch_update_attn(u, st, last));
+        HIP_TRY(launch_update_attn(u, st, upd));
     } else if (s.R == s.Hkv) {
         // one row per KV head (or a single KV head): the scan adds straight into S
         HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawS, ncu, st, scan));
-        HIP_TRY(mark(ev.score_stop, st));
         if (with_hist)
-            HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, s.pin_lo, s.pin_hi, hist, st));
+            HIP_TRY(launch_topk_hist(sacc, d->s_stride_b, d->s_stride_r, s.B, s.R, s.n, s.pin_lo, s.pin_hi, hist, st,
+                                     upd));
     } else {
         a.logits = at<float>(ws, L.logits);
         HIP_TRY(launch_score_tiles(a, s.dtype, kOutRawGroups, ncu, st, scan));
         u.logits = a.logits;
-        HIP_TRY(launch_update_raw_groups(u, st, last));
+        HIP_TRY(launch_update_raw_groups(u, st, upd));
     }
     return HILL_OK;
 }
@@ -472,18 +473,15 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
         a.logits = at<float>(ws, L.logits);
         a.ld = s.ld;
     }
-    if (state4 && !stream_reset) {   // no refine pass: the select interval is empty
-        HIP_TRY(mark(e.select_start, st));
-        HIP_TRY(mark(e.select_stop, st));
+    if (state4 && !stream_reset) {   // no refine pass
         r.state_out = state4;
-        HIP_TRY(launch_topk_emit_attn_stream(r, a, s.dtype, st));
+        HIP_TRY(launch_topk_emit_attn_stream(r, a, s.dtype, st, stage(e, HILL_STAGE_SELECT)));
     } else {
         r.state_out = state4;   // NULL, or a reset step's fresh bound
-        HIP_TRY(launch_topk_refine(r, s.B * s.R, st,
-                                   Stamp{static_cast<hipEvent_t>(e.select_start), static_cast<hipEvent_t>(e.select_stop)}));
-        HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st));
+        HIP_TRY(launch_topk_refine(r, s.B * s.R, st, stage(e, HILL_STAGE_REFINE)));
+        HIP_TRY(launch_topk_emit_attn(r, a, s.dtype, st, stage(e, HILL_STAGE_SELECT)));
     }
-    HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, Stamp{nullptr, static_cast<hipEvent_t>(e.attn_stop)}));
+    HIP_TRY(launch_merge_write(r, a, idx_out, s.B * s.R, st, stage(e, HILL_STAGE_MERGE)));
     return HILL_OK;
 }
 
@@ -721,17 +719,6 @@ hill_status hill_app_balance(const hill_app_params* p, hill_app_plan* plan)
     r.t_c = a_c * r.m_c;
     r.t_s = a_s * r.m_s;
     *plan = r;
-    return HILL_OK;
-}
-
-hill_status hill_calib_read(const void* buf, int64_t bytes, int32_t grid, uint32_t* sink, void* stream)
-{
-    HILL_TRY(check_ptr(buf, "buf"));
-    if (!sink) return fail(HILL_ERR_INVALID_ARG, "sink is NULL");
-    if (bytes < 16 || bytes % 16) return fail(HILL_ERR_INVALID_ARG, "bytes %lld not a positive multiple of 16",
-                                              static_cast<long long>(bytes));
-    if (grid < 1 || grid > 65536) return fail(HILL_ERR_INVALID_ARG, "grid %d not in [1, 65536]", grid);
-    HIP_TRY(launch_calib_read(buf, bytes, grid, sink, static_cast<hipStream_t>(stream)));
     return HILL_OK;
 }
 

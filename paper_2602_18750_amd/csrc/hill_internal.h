@@ -204,9 +204,9 @@ struct BkpArgs {
 hipError_t launch_bkp_hits(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_bkp_rank(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_bkp_lists(const BkpArgs& a, int rows, hipStream_t st);
-hipError_t launch_calib_read(const void* p, int64_t bytes, int grid, uint32_t* sink, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
-hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st);
+hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st,
+                                Stamp ts = {});
 // Whether update_attn can reduce the softmax partials itself (no separate
 // softmax_stats launch): every thread then loads at most kStatLoads of them.
 inline bool update_reduces_stats(int nheads_per_row, int npart)

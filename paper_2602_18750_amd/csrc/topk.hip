@@ -390,10 +390,29 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         const uint32_t bnd = r.d0[row];
         find_digit(h1, (uint32_t)r.k, res);
         __syncthreads();
-        const uint32_t b1 = res[0] & (kHistBins - 1), need1 = res[1], in1 = res[2];
+        uint32_t b1 = res[0] & (kHistBins - 1), need1 = res[1], in1 = res[2];
         const uint32_t d0 = bnd & (kHistBins - 1);
-        fast = b1 >= d0;
-        pair_cls = ((bnd >> 31) && b1 - d0 < (uint32_t)kStreamBins) ? (int)(b1 - d0) : kStreamBins;
+        // With a bound the histogram holds only the keys from the bound's bin upward.  If fewer than
+        // k keys are there (the search then lands below the bound), S did not only grow since the
+        // bound was written -- it was changed outside these calls -- and the first digit is counted
+        // again over the whole row, whose keys the later walks then read directly (fast = false).
+        // Otherwise the k-th key lies in the counted bins and the result is exact as it is.
+        fast = b1 >= d0;   // block-uniform
+        if (!fast) {
+            uint32_t* h1s = hist2s;
+            __syncthreads();   // res of the search has been read
+            for (int i = tid; i < kHistBins; i += kThreads) h1s[i] = 0u;
+            __syncthreads();
+            for_row_pairs(r, row, false, kStreamBins, pair_offs, pair_starts, scan_scratch,
+                          [h1s](uint32_t kk, uint32_t) { atomicAdd(&h1s[kk >> 20], 1u); });
+            __syncthreads();
+            find_bin<kThreads>(h1s, kHistBins, (uint32_t)r.k, scan_scratch, res);
+            b1 = res[0] & (kHistBins - 1);
+            need1 = (uint32_t)r.k - res[1];
+            in1 = h1s[b1];
+            __syncthreads();   // res and the counts have been read before either is reused
+        }
+        pair_cls = (fast && (bnd >> 31) && b1 - d0 < (uint32_t)kStreamBins) ? (int)(b1 - d0) : kStreamBins;
         prefix = b1;
         need = need1;
         shift = 20;

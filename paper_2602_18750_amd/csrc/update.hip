@@ -377,9 +377,9 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
 
 }  // namespace
 
-hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st)
+hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st, Stamp ts)
 {
-    hipLaunchKernelGGL(softmax_stats_kernel, dim3(bh), dim3(256), 0, st, part, stats, npart);
+    hipExtLaunchKernelGGL(softmax_stats_kernel, dim3(bh), dim3(256), 0, st, ts.start, ts.stop, 0, part, stats, npart);
     return hipGetLastError();
 }
 

@@ -35,10 +35,10 @@ DTYPES = {torch.float16: 0, torch.bfloat16: 1}
 MODES = {"attn": 0, "raw": 1}
 GRANS = {"token": 0, "kvhead": 1}
 
-ABI_VERSION = 5   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
+ABI_VERSION = 6   # HILL_ABI_VERSION of include/hill.h that this binding's structures follow
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
-           "hill_score_sketch", "hill_step_sketch", "hill_calib_read", "hill_bkp_workspace_bytes",
+           "hill_score_sketch", "hill_step_sketch", "hill_bkp_workspace_bytes",
            "hill_bkp_update", "hill_app_balance", "hill_step_streamed")
 
 
@@ -75,11 +75,24 @@ class HillDesc(ctypes.Structure):
     ]
 
 
+# Stages of a decode step (include/hill.h HILL_STAGE_*), in launch order.
+STAGES = ("scan", "stats", "update", "refine", "select", "merge")
+
+
 class HillStepEvents(ctypes.Structure):
-    """Kernel timestamps for hill_step_profiled: hipEvent_t handles or None."""
-    _fields_ = [("scan_start", ctypes.c_void_p), ("scan_stop", ctypes.c_void_p), ("score_stop", ctypes.c_void_p),
-                ("select_start", ctypes.c_void_p), ("select_stop", ctypes.c_void_p),
-                ("attn_stop", ctypes.c_void_p)]
+    """Kernel timestamps of a decode step (hill_step_profiled and the streamed
+    and sketch steps): hipEvent_t handles or None, per stage, stamped by the
+    start and the end of that stage's launch."""
+    _fields_ = [("start", ctypes.c_void_p * len(STAGES)), ("stop", ctypes.c_void_p * len(STAGES))]
+
+    @classmethod
+    def of(cls, starts, stops):
+        """From two sequences of len(STAGES) event handles (ints or None)."""
+        ev = cls()
+        for i in range(len(STAGES)):
+            ev.start[i] = starts[i]
+            ev.stop[i] = stops[i]
+        return ev
 
 
 class BkpDesc(ctypes.Structure):
@@ -142,8 +155,6 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_sketch.argtypes = [D, P, P, P, P, P, I64, I32, P, P, U32, I32, P, P, P, SZ, P,
                                          ctypes.POINTER(HillStepEvents)]
         lib.hill_step_sketch.restype = ctypes.c_int
-        lib.hill_calib_read.argtypes = [P, I64, I32, P, P]
-        lib.hill_calib_read.restype = ctypes.c_int
         lib.hill_bkp_workspace_bytes.argtypes = [ctypes.POINTER(BkpDesc), ctypes.POINTER(SZ)]
         lib.hill_bkp_workspace_bytes.restype = ctypes.c_int
         lib.hill_bkp_update.argtypes = [ctypes.POINTER(BkpDesc), P, I32, P, P, P, P, I32, P, P, SZ, P]
@@ -298,18 +309,6 @@ def sketch_keys(k, sketch: Optional[Sketch] = None, *, token_begin=0, token_end=
     return sketch
 
 
-def calib_read(buf, grid: int, sink, stream=None) -> None:
-    """One launch of the library's plain streaming read over the bytes of
-    ``buf`` (roofline calibration; computes nothing of the method).  ``sink``
-    is a device int32/uint32 tensor of at least ``grid`` words."""
-    lib = load_library()
-    _device_check(buf, sink)
-    if sink.numel() < grid or sink.element_size() != 4:
-        raise ValueError("sink needs at least grid 4-byte words")
-    _check(lib.hill_calib_read(_ptr(buf), buf.numel() * buf.element_size(), int(grid), _ptr(sink),
-                               _stream_ptr(stream)))
-
-
 def hill_score(q, k, s, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0, ws=None,
                stream=None, sketch: Optional[Sketch] = None):
     """S += column-wise sum over this step's weights (in place).  With
@@ -394,7 +393,9 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
     ``events``: optional HillStepEvents; then hill_step_profiled records them.
     ``sketch``: score on the int8 / int4 sketch (hill_step_sketch)."""
     lib = load_library()
-    _device_check(q, k, v, s)
+    _device_check(q, k, v, s, ws)
+    if sketch is not None:
+        _device_check(sketch.codes, sketch.exps)
     desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale,
                      n_sink=n_sink, n_recent=n_recent)
     if k_sel is None:
@@ -545,7 +546,11 @@ class StepCall:
                  ws=None, stream=None, sketch: Optional[Sketch] = None, n_sink=0, n_recent=0, stream_state=None,
                  stream_reset_calls=3):
         lib = load_library()
-        _device_check(q, k, v, s)
+        _device_check(q, k, v, s, ws, stream_state)
+        if sketch is not None:
+            _device_check(sketch.codes, sketch.exps)
+            if not (sketch.codes.is_contiguous() and sketch.exps.is_contiguous()):
+                raise ValueError("sketch codes and exponents must be contiguous")
         self.desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens,
                               sm_scale=sm_scale, n_sink=n_sink, n_recent=n_recent)
         B, R = s.shape[0], s.shape[1]
@@ -555,8 +560,9 @@ class StepCall:
         self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
         P = ctypes.c_void_p
         self._pre = (ctypes.byref(self.desc),)
-        if stream_state is not None and (stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8):
-            raise ValueError("stream_state must be an int32 [B, R, 8] tensor")
+        if stream_state is not None and (stream_state.dtype != torch.int32 or stream_state.numel() < B * R * 8
+                                         or not stream_state.is_contiguous()):
+            raise ValueError("stream_state must be a contiguous int32 [B, R, 8] tensor")
         state_ptr = P(stream_state.data_ptr() if stream_state is not None else None)
         self._resets_left = int(stream_reset_calls) if stream_state is not None else 0
         self._post_reset = None

@@ -251,15 +251,31 @@ def test_head_count_limits(H):
     assert call_step(H, d, ws_bytes=1 << 40) == UNSUPPORTED
 
 
-def test_calib_read_validates(H):
-    lib = H.load_library()
-    assert lib.hill_calib_read(None, 1024, 4, FAKE, None) == INVALID
-    assert lib.hill_calib_read(FAKE + 8, 1024, 4, FAKE, None) == INVALID     # misaligned buffer
-    assert lib.hill_calib_read(FAKE, 1024, 4, None, None) == INVALID          # no sink
-    assert lib.hill_calib_read(FAKE, 1000, 4, FAKE, None) == INVALID          # not a multiple of 16
-    assert lib.hill_calib_read(FAKE, 0, 4, FAKE, None) == INVALID
-    assert lib.hill_calib_read(FAKE, 1024, 0, FAKE, None) == INVALID
-    assert lib.hill_calib_read(FAKE, 1024, 65537, FAKE, None) == INVALID
+def test_calib_read_is_a_separate_library(H):
+    """The benchmark's roofline calibration read lives in libhill_calib.so,
+    outside libhill's ABI; it validates its arguments before launching."""
+    from paper_2602_18750_amd import _build
+    assert not hasattr(H.load_library(), "hill_calib_read")
+    lib = ctypes.CDLL(_build.CALIB_LIB)
+    fn = lib.hill_calib_read
+    fn.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    fn.restype = ctypes.c_int
+    assert fn(None, 1024, 4, FAKE, None) == 1
+    assert fn(FAKE + 8, 1024, 4, FAKE, None) == 1     # misaligned buffer
+    assert fn(FAKE, 1024, 4, None, None) == 1          # no sink
+    assert fn(FAKE, 1000, 4, FAKE, None) == 1          # not a multiple of 16
+    assert fn(FAKE, 0, 4, FAKE, None) == 1
+    assert fn(FAKE, 1024, 0, FAKE, None) == 1
+    assert fn(FAKE, 1024, 65537, FAKE, None) == 1
+
+
+def test_step_events_layout_matches_header(H):
+    text = open(HEADER).read()
+    stages = re.findall(r"HILL_STAGE_([A-Z]+) = (\d+)", text)
+    assert [n.lower() for n, _ in stages] == list(H.hill.STAGES)
+    assert [int(v) for _, v in stages] == list(range(len(stages)))
+    assert int(re.search(r"HILL_STAGES = (\d+)", text).group(1)) == len(H.hill.STAGES)
+    assert ctypes.sizeof(H.HillStepEvents) == 2 * len(H.hill.STAGES) * ctypes.sizeof(ctypes.c_void_p)
 
 
 def _bkp_desc(H, **kw):

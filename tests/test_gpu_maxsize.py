@@ -13,7 +13,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2602_18750_amd import workloads as W
-from parity import check_outputs, check_scores, check_selection
+from parity import check_outputs, check_scores, check_selection, raw_abs_update
 from util import bits
 
 pytestmark = pytest.mark.gpu
@@ -97,7 +97,8 @@ def test_long_context_modes(mode, gran):
     torch.cuda.synchronize()
     qc, kc, vc = bits(x.q.cpu()), bits(x.k.cpu()), bits(x.v.cpu())
     s_ref, _, _ = O.step(qc[0], kc, vc, np.zeros((1, R, n)), k_sel, "fp16", mode, gran)
-    check_scores(s.cpu().numpy(), s_ref, "long %s %s S" % (mode, gran))
+    a_ref = raw_abs_update(np.zeros((1, R, n)), qc[0], kc, "fp16", 2, gran) if mode == "raw" else None
+    check_scores(s.cpu().numpy(), s_ref, "long %s %s S" % (mode, gran), abs_sum=a_ref)
     idx_g = idx.cpu().numpy()
     check_selection(idx_g, s_ref, k_sel, "long %s %s sel" % (mode, gran))
     own = O.sparse_attn(qc[0], kc, vc, idx_g, "fp16", gran)

@@ -9,7 +9,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2602_18750_amd import workloads as W
-from parity import check_outputs, check_scores, check_selection
+from parity import check_outputs, check_scores, check_selection, raw_abs_update, raw_abs_update_logits
 from util import bits, dname
 
 pytestmark = pytest.mark.gpu
@@ -75,12 +75,15 @@ def test_score_matches_oracle_over_steps(B, Hq, Hkv, n, dt, mode, gran):
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
+    a_ref = np.zeros((B, R, n)) if mode == "raw" else None
     for t in range(T):
         H().hill_score(q[t], k, s, mode=mode, granularity=gran)
         l = O.logits(bits(x.q[t]), bits(x.k), dt)
         s_ref = O.update(l, s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        if a_ref is not None:
+            a_ref = raw_abs_update(a_ref, bits(x.q[t]), bits(x.k), dt, Hkv, gran)
         torch.cuda.synchronize()
-        check_scores(s.cpu().numpy(), s_ref, "step %d" % t)
+        check_scores(s.cpu().numpy(), s_ref, "step %d" % t, abs_sum=a_ref)
 
 
 # -------------------------------------------------------------------- top-k --
@@ -192,13 +195,16 @@ def run_steps(x, k_sel, mode, gran, steps, check_every=1, where=""):
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
+    a_ref = np.zeros((B, R, n)) if mode == "raw" else None
     for t in range(steps):
         idx, out = H().hill_step(q[t], k, v, s, k_sel, mode=mode, granularity=gran)
         s_ref, idx_ref, out_ref = O.step(bits(x.q[t]), bits(x.k), bits(x.v), s_ref, k_sel, dt, mode, gran)
+        if a_ref is not None:
+            a_ref = raw_abs_update(a_ref, bits(x.q[t]), bits(x.k), dt, Hkv, gran)
         if t % check_every == 0 or t == steps - 1:
             torch.cuda.synchronize()
             idx_g = idx.cpu().numpy()
-            check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t))
+            check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t), abs_sum=a_ref)
             check_selection(idx_g, s_ref, k_sel, "%s step %d sel" % (where, t))
             out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, gran)
             check_outputs(out.cpu().numpy(), out_own, "%s step %d out" % (where, t))
@@ -491,12 +497,16 @@ def test_score_on_sketch_matches_oracle(B, Hq, Hkv, n, dt, mode, gran, nbits):
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
+    a_ref = np.zeros((B, R, n)) if mode == "raw" else None
     for t in range(T):
         H().hill_score(q[t], None, s, mode=mode, granularity=gran, sketch=sk)
         q8, eq = O.sketch(bits(x.q[t]), dt)
-        s_ref = O.update(O.logits_i8(q8, eq, k8, ek), s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        l8 = O.logits_i8(q8, eq, k8, ek)
+        s_ref = O.update(l8, s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        if a_ref is not None:
+            a_ref = raw_abs_update_logits(a_ref, l8, Hkv, gran)
         torch.cuda.synchronize()
-        check_scores(s.cpu().numpy(), s_ref, "sketch step %d" % t)
+        check_scores(s.cpu().numpy(), s_ref, "sketch step %d" % t, abs_sum=a_ref)
 
 
 @pytest.mark.parametrize("nbits", [8, 4])
@@ -557,13 +567,17 @@ def _run_sketch_steps(x, k_sel, mode, gran, steps, where, nbits=8):
     R = R_of(gran, Hkv)
     s = H().new_importance(B, R, n, DEV)
     s_ref = np.zeros((B, R, n))
+    a_ref = np.zeros((B, R, n)) if mode == "raw" else None
     for t in range(steps):
         idx, out = H().hill_step(q[t], k, v, s, k_sel, mode=mode, granularity=gran, sketch=sk)
         q8, eq = O.sketch(bits(x.q[t]), dt)
-        s_ref = O.update(O.logits_i8(q8, eq, k8, ek), s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        l8 = O.logits_i8(q8, eq, k8, ek)
+        s_ref = O.update(l8, s_ref, Hkv, mode, gran, 1 / math.sqrt(128))
+        if a_ref is not None:
+            a_ref = raw_abs_update_logits(a_ref, l8, Hkv, gran)
         torch.cuda.synchronize()
         idx_g = idx.cpu().numpy()
-        check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t))
+        check_scores(s.cpu().numpy(), s_ref, "%s step %d S" % (where, t), abs_sum=a_ref)
         check_selection(idx_g, s_ref, k_sel, "%s step %d sel" % (where, t))
         # attention reads the 16-bit K and V of the selected tokens
         out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, gran)

@@ -11,7 +11,7 @@ import torch
 
 from oracle import oracle as O
 from paper_2602_18750_amd import workloads as W
-from parity import check_outputs, check_scores, check_selection
+from parity import check_outputs, check_scores, check_selection, raw_abs_update
 from util import bits, dname
 
 pytestmark = pytest.mark.gpu
@@ -117,6 +117,7 @@ def test_step_with_pins_matches_oracle(mode, gran, sketch):
     R = 1 if gran == "token" else w.n_kv_heads
     s = H().new_importance(w.batch, R, w.n_tokens, DEV)
     s_ref = np.zeros((w.batch, R, w.n_tokens))
+    a_ref = np.zeros((w.batch, R, w.n_tokens)) if mode == "raw" else None
     sk = H().sketch_keys(k) if sketch else None
     k8, ek = O.sketch(bits(x.k), dt) if sketch else (None, None)
     for t in range(w.steps):
@@ -128,9 +129,11 @@ def test_step_with_pins_matches_oracle(mode, gran, sketch):
         else:
             l = O.logits(bits(x.q[t]), bits(x.k), dt)
         s_ref = O.update(l, s_ref, w.n_kv_heads, mode, gran, 1 / math.sqrt(128))
+        if a_ref is not None:
+            a_ref = raw_abs_update(a_ref, bits(x.q[t]), bits(x.k), dt, w.n_kv_heads, gran)
         torch.cuda.synchronize()
         idx_g = idx.cpu().numpy()
-        check_scores(s.cpu().numpy(), s_ref, "step %d S" % t)
+        check_scores(s.cpu().numpy(), s_ref, "step %d S" % t, abs_sum=a_ref)
         _check_pinned_selection(idx_g, s_ref, k_sel, sink, recent, "step %d sel" % t)
         out_own = O.sparse_attn(bits(x.q[t]), bits(x.k), bits(x.v), idx_g, dt, gran)
         check_outputs(out.cpu().numpy(), out_own, "step %d out" % t)

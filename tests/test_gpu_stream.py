@@ -37,11 +37,13 @@ def say(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0):
+def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0, mutate=None):
     """hill_step and hill_step_streamed side by side on copies of the same S;
     schedule: list of (n_tokens, k_sel) per step, the first `resets` of them
-    reset steps (HILL_STREAM_RESET).  Asserts bit-identical S, indices and
-    outputs and a valid state after every step; returns the streamed state."""
+    reset steps (HILL_STREAM_RESET); mutate: {step: f}, f(S) applied in place
+    to both copies of S before that step (a change outside the calls).
+    Asserts bit-identical S, indices and outputs and a valid state after
+    every step; returns the streamed state."""
     q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
     B, Hkv, ncap = k.shape[0], k.shape[1], k.shape[2]
     R = 1 if gran == "token" else Hkv
@@ -49,6 +51,9 @@ def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0):
     s_b = H().new_importance(B, R, ncap, DEV)
     state = H().new_stream_state(B, R, DEV)
     for t, (n, ks) in enumerate(schedule):
+        if mutate and t in mutate:
+            mutate[t](s_a)
+            mutate[t](s_b)
         i_a, o_a = H().hill_step(q[t], k, v, s_a, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent)
         i_b, o_b = H().hill_step(q[t], k, v, s_b, ks, granularity=gran, n_tokens=n, n_sink=sink, n_recent=recent,
                                  stream_state=state, stream_reset=t < resets)
@@ -104,6 +109,18 @@ def test_streamed_bound_changes():
     say("streamed bound changes, pins")
     _pair_run(x, [(5000, 500), (5100, 500), (5100, 500), (5300, 520), (5300, 300), (6000, 300), (6000, 300),
                   (6000, 300)], sink=3, recent=40)
+
+
+@pytest.mark.parametrize("factor", [0.25, 4.0, 0.0])
+def test_streamed_after_outside_change_of_s(factor):
+    """S scaled (or cleared) between streamed calls without a reset: scaled
+    down or cleared, fewer than k keys reach the bound's first digit and the
+    selection counts that digit again over the whole row; scaled up, the k-th
+    key stays in the counted bins.  Either way the results equal hill_step's,
+    and the bound written afterwards is valid again."""
+    x = W.make_random(1, 16, 4, 128, 5000, "bf16", steps=6, seed=61)
+    say("streamed after S *= %g outside the calls" % factor)
+    _pair_run(x, [(5000, 500)] * 6, resets=1, mutate={3: lambda s: s.mul_(factor)})
 
 
 def test_streamed_heavy_ties():
@@ -189,3 +206,55 @@ def test_streamed_several_kv_heads_per_workgroup():
     x = W.make_random(4, 32, 8, 128, n, "bf16", steps=4, seed=404, device=DEV)
     say("streamed, several KV heads per workgroup")
     _pair_run(x, [(n, 6553), (n, 6553), (n, 6600), (n, 6553)], resets=1)
+
+
+def test_stage_events_stamp_the_stages_that_run():
+    """hill_step_events (include/hill.h): a streamed step stamps the scan,
+    update, select and merge stages (each interval non-negative, in launch
+    order) and leaves the refine stage's events unrecorded; a reset step
+    stamps refine too."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    n_st = len(H().hill.STAGES)
+
+    def make():
+        evs = []
+        for _ in range(2 * n_st):
+            e = ctypes.c_void_p()
+            assert hip.hipEventCreate(ctypes.byref(e)) == 0
+            evs.append(e)
+        return evs
+
+    def ms(a, b):
+        out = ctypes.c_float()
+        rc = hip.hipEventElapsedTime(ctypes.byref(out), a, b)
+        return rc, out.value
+
+    x = W.make_random(1, 32, 8, 128, 5000, "bf16", steps=2, seed=17)
+    q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    s = H().new_importance(1, 1, 5000, DEV)
+    state = H().new_stream_state(1, 1, DEV)
+    stages = H().hill.STAGES
+    for t, reset in ((0, True), (1, False)):
+        evs = make()
+        ev = H().HillStepEvents.of([e.value for e in evs[:n_st]], [e.value for e in evs[n_st:]])
+        H().hill_step(q[t], k, v, s, 500, stream_state=state, stream_reset=reset, events=ev)
+        torch.cuda.synchronize()
+        ran = ["scan", "update"] + (["refine"] if reset else []) + ["select", "merge"]
+        prev_stop = None
+        for name in stages:
+            i = stages.index(name)
+            rc, dur = ms(evs[i], evs[n_st + i])
+            if name in ran:
+                assert rc == 0 and dur >= 0.0, (name, rc, dur)
+                if prev_stop is not None:
+                    rc2, gap = ms(prev_stop, evs[i])
+                    assert rc2 == 0 and gap >= 0.0, (name, gap)
+                prev_stop = evs[n_st + i]
+            else:
+                assert rc != 0, "stage %s did not run but its events were recorded" % name
+        for e in evs:
+            hip.hipEventDestroy(e)
