@@ -75,50 +75,26 @@ def log(*a):
 
 # ------------------------------------------------------------- HIP events --
 
-class HipEvents:
-    """hipEvent_t handles created through the HIP runtime (ctypes)."""
-
-    def __init__(self):
-        self.hip = ctypes.CDLL("libamdhip64.so")
-        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
-        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
-        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
-        self.made = []
-
-    def create(self):
-        e = ctypes.c_void_p()
-        rc = self.hip.hipEventCreate(ctypes.byref(e))
-        if rc != 0:
-            raise RuntimeError("hipEventCreate failed (%d)" % rc)
-        self.made.append(e)
-        return e
-
-    def ms(self, a, b) -> float:
-        out = ctypes.c_float()
-        rc = self.hip.hipEventElapsedTime(ctypes.byref(out), a, b)
-        if rc != 0:
-            raise RuntimeError("hipEventElapsedTime failed (%d)" % rc)
-        return float(out.value)
-
-    def close(self):
-        for e in self.made:
-            self.hip.hipEventDestroy(e)
-        self.made = []
-
-
 class StageProbe:
     """Start/stop events for every stage of one decode step (include/hill.h
-    HILL_STAGE_*), and the stage durations they measured."""
+    HILL_STAGE_*), and the stage durations they measured.  The events are
+    torch's (HIP events with timing, created by a first record on the
+    stream), so that they belong to the HIP runtime that torch and the
+    library share; their handles go to the library, which stamps them at the
+    start and end of each stage's launch."""
 
-    def __init__(self, hip: HipEvents, H):
-        self.hip, self.stages = hip, H.hill.STAGES
-        self.start = [hip.create() for _ in self.stages]
-        self.stop = [hip.create() for _ in self.stages]
-        self.ev = H.HillStepEvents.of([e.value for e in self.start], [e.value for e in self.stop])
+    def __init__(self, H, stream):
+        import torch
+        self.stages = H.hill.STAGES
+        self.start = [torch.cuda.Event(enable_timing=True) for _ in self.stages]
+        self.stop = [torch.cuda.Event(enable_timing=True) for _ in self.stages]
+        for e in self.start + self.stop:
+            e.record(stream)
+        self.ev = H.HillStepEvents.of([e.cuda_event for e in self.start], [e.cuda_event for e in self.stop])
 
     def us(self, stage: str) -> float:
         i = self.stages.index(stage)
-        return self.hip.ms(self.start[i], self.stop[i]) * 1e3
+        return self.start[i].elapsed_time(self.stop[i]) * 1e3
 
 
 def stage_means(probes, stages):
@@ -250,8 +226,7 @@ def run_bench(args):
     qptrs = [[x.q[t].data_ptr() for t in range(T)] for (x, _) in layers]
     torch.cuda.synchronize()
 
-    hip = HipEvents()
-    probes = [StageProbe(hip, H) for _ in range(args.steps)]
+    probes = [StageProbe(H, stream) for _ in range(args.steps)]
 
     for i in range(args.warmup):
         for L in range(nl_run):
@@ -271,7 +246,6 @@ def run_bench(args):
     t1 = time.perf_counter()
 
     st = stage_means(probes, ("scan", "update", "select", "merge"))
-    hip.close()
 
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)   # one decode step = nl layer-steps
     kbytes_layer = w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
@@ -346,8 +320,7 @@ def bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     dev = torch.device("cuda:0")
     ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in layers]
     calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream) for L, (x, _) in enumerate(layers)]
-    hip = HipEvents()
-    probes = [StageProbe(hip, H) for _ in range(args.steps)]
+    probes = [StageProbe(H, stream) for _ in range(args.steps)]
     for i in range(args.warmup):
         for L in range(nl_run):
             calls[L](qptrs[L][i % T])
@@ -364,7 +337,6 @@ def bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     st = stage_means(probes, ("scan", "update", "refine", "select", "merge"))
-    hip.close()
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
     del calls, ss
     return {
@@ -429,8 +401,7 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
     states = [H.new_stream_state(w.batch, 1, dev) for _ in layers]
     calls = [H.StepCall(x.q[0], x.k, x.v, ss[L], w.k_sel, ws=ws, stream=stream, sketch=sks[L],
                         stream_state=states[L]) for L, (x, _) in enumerate(layers)]
-    hip = HipEvents()
-    probes = [StageProbe(hip, H) for _ in range(args.steps)]
+    probes = [StageProbe(H, stream) for _ in range(args.steps)]
     for i in range(args.warmup):
         for L in range(nl_run):
             calls[L](qptrs[L][i % T])
@@ -450,7 +421,6 @@ def bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, nbits=
     scan = st["scan"] * 1e-3                     # ms
     score = (st["scan"] + st["update"]) * 1e-3
     selattn = (st["select"] + st["merge"]) * 1e-3
-    hip.close()
     ms_step = (t1 - t0) * 1e3 / (args.steps * reps)
     units = (w.n_tokens + 255) // 256
     npart = (units + 1) // 2 * 2
@@ -495,7 +465,6 @@ def run_sweep(args):
 
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    hip = HipEvents()
     for w in W.sweep_workloads():
         kv_bytes = 2 * w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
         reps = max(1, min(16, -(-(1 << 30) // kv_bytes)))
@@ -506,7 +475,7 @@ def run_sweep(args):
         ws = H.workspace(H.make_desc(x.q[0], x.k, x.v, s), w.k_sel, dev)
         calls = [H.StepCall(x.q[0], ks[r], vs[r], s, w.k_sel, ws=ws, stream=stream) for r in range(reps)]
         iters = max(20, reps)
-        probes = [StageProbe(hip, H) for _ in range(iters)]
+        probes = [StageProbe(H, stream) for _ in range(iters)]
         for r in range(reps):
             calls[r](x.q[0].data_ptr())
         torch.cuda.synchronize()
@@ -528,8 +497,7 @@ def run_sweep(args):
             "scoring_us": round(score * 1e3, 2),
             "scoring_kgbps": round(kbytes / (score * 1e-3) / 1e9, 1),
             "select_attn_us": round(selattn * 1e3, 2), "replicas": reps}), flush=True)
-        del calls, ks, vs, x, s
-        hip.close()
+        del calls, ks, vs, x, s, probes
         torch.cuda.empty_cache()
 
 
