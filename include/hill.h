@@ -245,6 +245,22 @@ HILL_API hill_status hill_step_streamed(const hill_desc* d, const void* q, const
                                uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out,
                                void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
 
+/* hill_step without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The scratch is a fixed device buffer of
+ * HILL_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends (looked up on a device's first call, never
+ * allocated by the call).  A step whose hill_workspace_bytes() exceeds it is
+ * rejected with HILL_ERR_WORKSPACE before anything is enqueued (a 32K-token
+ * GQA 32/8 step of batch 1 needs about 6 MB).  Every call on one GPU shares
+ * that GPU's buffer, whose contents the previous call left: calls ordered on
+ * one stream are fine, but calls that overlap in time on one GPU (other
+ * streams or threads) race and give undefined results.  Otherwise the same
+ * arguments, validation and results as hill_step. */
+#define HILL_NOALLOC_SCRATCH_BYTES (32u << 20)
+HILL_API hill_status hill_step_noalloc(const hill_desc* d, const void* q, const void* k, const void* v,
+                              float* s, int32_t k_sel, int32_t* idx_out, float* out, void* stream);
+
 /* Asymmetric-precision scoring (Sec. 4.4: the evaluation runs on int8 or
  * int4 casts of the keys and an int8 cast of the query, attention on the
  * original 16-bit K and V).

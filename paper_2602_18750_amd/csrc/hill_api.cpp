@@ -443,22 +443,30 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
 
 // One decode step: score (16-bit keys or the sketch), refine the threshold,
 // then emit the indices and attend over each chunk's picks in the same kernel.
+// Every argument of a decode step except the workspace.
+hill_status check_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk,
+                       const float* s_acc, int32_t k_sel, const int32_t* idx_out, const float* out, Shape* s)
+{
+    HILL_TRY(check_desc(d, s));
+    HILL_TRY(check_ksel(*s, k_sel));
+    HILL_TRY(check_pins(*s, k_sel));
+    HILL_TRY(check_ptr(q, "q"));
+    HILL_TRY(check_ptr(k, "k"));
+    HILL_TRY(check_ptr(v, "v"));
+    if (sk.k8) HILL_TRY(check_sketch(*s, sk.k8, sk.k_exp, sk.cap, sk.bits));
+    HILL_TRY(check_ptr(s_acc, "s"));
+    HILL_TRY(check_ptr(out, "out"));
+    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
+    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
+    return HILL_OK;
+}
+
 hill_status run_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk, float* s_acc,
                      int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
                      const hill_step_events* ev, uint32_t* stream_state = nullptr, bool stream_reset = false)
 {
     Shape s;
-    HILL_TRY(check_desc(d, &s));
-    HILL_TRY(check_ksel(s, k_sel));
-    HILL_TRY(check_pins(s, k_sel));
-    HILL_TRY(check_ptr(q, "q"));
-    HILL_TRY(check_ptr(k, "k"));
-    HILL_TRY(check_ptr(v, "v"));
-    if (sk.k8) HILL_TRY(check_sketch(s, sk.k8, sk.k_exp, sk.cap, sk.bits));
-    HILL_TRY(check_ptr(s_acc, "s"));
-    HILL_TRY(check_ptr(out, "out"));
-    if (!idx_out) return fail(HILL_ERR_INVALID_ARG, "idx_out is NULL");
-    if ((uintptr_t)idx_out & 3u) return fail(HILL_ERR_INVALID_ARG, "idx_out is not 4-byte aligned");
+    HILL_TRY(check_step(d, q, k, v, sk, s_acc, k_sel, idx_out, out, &s));
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -780,6 +788,21 @@ hill_status hill_step_profiled(const hill_desc* d, const void* q, const void* k,
                                const hill_step_events* ev)
 {
     return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev);
+}
+
+hill_status hill_step_noalloc(const hill_desc* d, const void* q, const void* k, const void* v, float* s_acc,
+                              int32_t k_sel, int32_t* idx_out, float* out, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, &s));
+    const size_t need = layout_for(s, k_sel).end_all;
+    if (need > kStaticScratchBytes)
+        return fail(HILL_ERR_WORKSPACE, "this step needs %zu bytes of scratch, more than the %zu of the fixed device buffer",
+                    need, (size_t)kStaticScratchBytes);
+    void* ws = nullptr;
+    const hipError_t e = static_scratch(&ws);
+    if (e != hipSuccess) return fail(HILL_ERR_HIP, "fixed device scratch: %s", hipGetErrorString(e));
+    return run_step(d, q, k, v, Sketch{}, s_acc, k_sel, idx_out, out, ws, kStaticScratchBytes, stream, nullptr);
 }
 
 static hill_status check_stream_flags(const uint32_t* state, uint32_t flags)

@@ -175,6 +175,12 @@ struct Stamp {
     hipEvent_t stop = nullptr;
 };
 
+// Fixed device scratch of hill_step_noalloc (noalloc.hip): a file-scope device
+// array of kStaticScratchBytes per GPU; *ptr receives the current device's copy
+// (its address looked up once per device, then cached).
+constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
+hipError_t static_scratch(void** ptr);
+
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
 hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
 // Bidirectional KV cache pools (bkp.hip).

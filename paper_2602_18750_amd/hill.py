@@ -39,7 +39,7 @@ ABI_VERSION = 6   # HILL_ABI_VERSION of include/hill.h that this binding's struc
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_bkp_workspace_bytes",
-           "hill_bkp_update", "hill_app_balance", "hill_step_streamed")
+           "hill_bkp_update", "hill_app_balance", "hill_step_streamed", "hill_step_noalloc")
 
 
 class HillError(RuntimeError):
@@ -162,6 +162,8 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_streamed.argtypes = [D, P, P, P, P, P, U32, I32, P, P, P, SZ, P,
                                            ctypes.POINTER(HillStepEvents)]
         lib.hill_step_streamed.restype = ctypes.c_int
+        lib.hill_step_noalloc.argtypes = [D, P, P, P, P, I32, P, P, P]
+        lib.hill_step_noalloc.restype = ctypes.c_int
         lib.hill_app_balance.argtypes = [ctypes.POINTER(AppParams), ctypes.POINTER(AppPlan)]
         lib.hill_app_balance.restype = ctypes.c_int
         if lib.hill_abi_version() != ABI_VERSION:
@@ -432,6 +434,28 @@ def hill_step(q, k, v, s, k_sel=None, *, budget=None, mode="attn", granularity="
         _check(lib.hill_step_profiled(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel),
                                       _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
                                       ctypes.byref(events)))
+    return idx_out, out
+
+
+NOALLOC_SCRATCH_BYTES = 32 << 20   # HILL_NOALLOC_SCRATCH_BYTES of include/hill.h
+
+
+def hill_step_noalloc(q, k, v, s, k_sel, *, mode="attn", granularity="token", n_tokens=None, sm_scale=0.0,
+                      idx_out=None, out=None, stream=None, n_sink=0, n_recent=0):
+    """hill_step with the library's fixed device scratch instead of a
+    workspace (hill_step_noalloc, for callers that cannot allocate; steps up
+    to NOALLOC_SCRATCH_BYTES of workspace).  Returns (idx, out)."""
+    lib = load_library()
+    _device_check(q, k, v, s, idx_out, out)
+    desc = make_desc(q, k, v, s, mode=mode, granularity=granularity, n_tokens=n_tokens, sm_scale=sm_scale,
+                     n_sink=n_sink, n_recent=n_recent)
+    B, R = s.shape[0], s.shape[1]
+    if idx_out is None:
+        idx_out = torch.empty((B, R, k_sel), dtype=torch.int32, device=s.device)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    _check(lib.hill_step_noalloc(ctypes.byref(desc), _ptr(q), _ptr(k), _ptr(v), _ptr(s), int(k_sel), _ptr(idx_out),
+                                 _ptr(out), _stream_ptr(stream)))
     return idx_out, out
 
 
