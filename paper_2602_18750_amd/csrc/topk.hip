@@ -49,7 +49,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kPerThread = kSelChunk / kThreads;   // 2 consecutive tokens per thread
-static_assert(kPerThread == 2, "load_keys reads float2");
+static_assert(kPerThread == 2, "load_s_pair reads float2");
 static_assert(kSelChunk == 16 * 32, "16 row groups of 32 tokens");
 
 __global__ __launch_bounds__(256) void topk_hist_kernel(const float* __restrict__ s, int64_t s_sb, int64_t s_sr,
@@ -85,24 +85,30 @@ __device__ __forceinline__ const float* row_ptr(const RefineArgs& a, int row)
     return a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
 }
 
-// Selection keys of this thread's 2 consecutive tokens of chunk c (row bases
-// 16-byte aligned); tokens outside [lo, hi) are pinned.
-__device__ __forceinline__ void load_keys(const float* srow, int c, int n, int lo, int hi,
-                                          uint32_t (&key)[kPerThread], bool (&ok)[kPerThread])
+// S of this thread's 2 consecutive tokens of chunk c: one unconditional
+// 8-byte load (row bases 16-byte aligned, row strides a multiple of 4 floats
+// and at least n, so the pair at an even index below n lies inside the row;
+// a pair past the end reads the row's last pair, and keys_of marks it invalid).
+// The keys are formed by keys_of() once every other load of the kernel's
+// opening is in flight: a branch around the load would make the compiler
+// wait for it before issuing anything else.
+__device__ __forceinline__ float2 load_s_pair(const float* srow, int c, int n)
 {
     const int j = c * kSelChunk + threadIdx.x * kPerThread;
-    if (j + kPerThread <= n) {
-        const float2 x = *reinterpret_cast<const float2*>(srow + j);
-        key[0] = select_key(x.x, j, lo, hi);
-        key[1] = select_key(x.y, j + 1, lo, hi);
-        ok[0] = ok[1] = true;
-    } else {
-#pragma unroll
-        for (int e = 0; e < kPerThread; ++e) {
-            ok[e] = j + e < n;
-            key[e] = ok[e] ? select_key(srow[j + e], j + e, lo, hi) : 0u;
-        }
-    }
+    const int jl = j < n ? j : ((n - 1) & ~1);
+    return *reinterpret_cast<const float2*>(srow + jl);
+}
+
+// Selection keys of the pair loaded by load_s_pair; tokens outside [lo, hi)
+// are pinned, tokens at or past n are not valid (ok false, key 0).
+__device__ __forceinline__ void keys_of(float2 x, int c, int n, int lo, int hi, uint32_t (&key)[kPerThread],
+                                        bool (&ok)[kPerThread])
+{
+    const int j = c * kSelChunk + threadIdx.x * kPerThread;
+    ok[0] = j < n;
+    ok[1] = j + 1 < n;
+    key[0] = ok[0] ? select_key(x.x, j, lo, hi) : 0u;
+    key[1] = ok[1] ? select_key(x.y, j + 1, lo, hi) : 0u;
 }
 
 // A histogram row of one 12-bit digit, loaded so that thread t holds fine
@@ -194,12 +200,13 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     const int c = blockIdx.x, row = blockIdx.y;
     const float* srow = row_ptr(a, row);
 
-    // the chunk's keys and the row's first-digit histogram are loaded together
-    uint32_t key[kPerThread];
-    bool ok[kPerThread];
-    load_keys(srow, c, a.n, a.pin_lo, a.pin_hi, key, ok);
+    // the chunk's S and the row's first-digit histogram are loaded together
+    const float2 sx = load_s_pair(srow, c, a.n);
     DigitHist h1;
     load_digit_hist(a.hist1 + (int64_t)row * kHistRow, h1);
+    uint32_t key[kPerThread];
+    bool ok[kPerThread];
+    keys_of(sx, c, a.n, a.pin_lo, a.pin_hi, key, ok);
     for (int i = tid; i < kHistRow; i += kThreads) hist[i] = 0u;
     if (tid == 0) n_cand = nlist = 0u;
     // first digit: the bin of the k-th key
@@ -367,9 +374,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     // second-digit histogram
     uint4 qv[ATTN && !LG ? GC : 1];
     if constexpr (ATTN && !LG) load_queries<GC>(at, b, g, 0, qv);
-    uint32_t key[kPerThread];
-    bool ok[kPerThread];
-    load_keys(row_ptr(r, row), c, r.n, r.pin_lo, r.pin_hi, key, ok);
+    const float2 sx = load_s_pair(row_ptr(r, row), c, r.n);
     float2 lgv[LG ? GC : 1];
     if constexpr (LG) load_chunk_logits<GC>(at, b, g * at.G, c, lgv);
     // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
@@ -516,6 +521,9 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     }
     }
 
+    uint32_t key[kPerThread];
+    bool ok[kPerThread];
+    keys_of(sx, c, r.n, r.pin_lo, r.pin_hi, key, ok);
     bool gt[kPerThread], eq[kPerThread], sel[kPerThread];
     uint32_t neq = 0;
 #pragma unroll
@@ -619,12 +627,20 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
 }
 
 // Copies the list of chunk c of a row to the output at its ascending-order
-// offset (the selected counts of the chunks before it).
+// offset (the selected counts of the chunks before it).  Every load is issued
+// before the first wait: the counts before c, this chunk's count and its list
+// entries (two per thread, at most kSelChunk; positions past the chunk's
+// tokens are clamped into it and never stored).
 __device__ __forceinline__ void write_chunk(const RefineArgs& r, int row, int c, int32_t* idx, float* val,
                                             uint32_t* red)
 {
     const int tid = threadIdx.x, lane = tid & 63;
     const uint32_t* sn = r.sel_n + (int64_t)row * r.nchunks;
+    const int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
+    const int last = min(kSelChunk, r.n - c * kSelChunk) - 1;   // the chunk's last slot
+    const int32_t e0 = list[min(tid, last)];
+    const int32_t e1 = list[min(tid + kThreads, last)];
+    const uint32_t m = sn[c];
     uint32_t before = 0;
     for (int cc = tid; cc < c; cc += kThreads) before += sn[cc];
     before = wave_sum_u32(before);
@@ -632,13 +648,14 @@ __device__ __forceinline__ void write_chunk(const RefineArgs& r, int row, int c,
     __syncthreads();
     uint32_t base = 0;
     for (int i = 0; i < kThreads / 64; ++i) base += red[i];
-    const uint32_t m = sn[c];
-    const int32_t* list = r.sel_list + (int64_t)row * r.n + (int64_t)c * kSelChunk;
     const float* srow = row_ptr(r, row);
-    for (uint32_t i = tid; i < m; i += kThreads) {
+    static_assert(kSelChunk == 2 * kThreads, "two list entries per thread");
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const uint32_t i = (uint32_t)(tid + e * kThreads);
         const uint32_t p = base + i;
-        if (p < (uint32_t)r.k) {
-            const int32_t j = list[i];
+        if (i < m && p < (uint32_t)r.k) {
+            const int32_t j = e == 0 ? e0 : e1;
             idx[(int64_t)row * r.k + p] = j;
             if (val) val[(int64_t)row * r.k + p] = srow[j];
         }

@@ -91,13 +91,14 @@ constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
 // were at least this step's k (S only grows), the pins are the same and n did
 // not shrink (n may only grow without pins); with 0x80000000 set.  Else 0
 // (no bound: every token is a candidate).
-__device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, int row)
+// p0, p1: the row's two state words, loaded by the caller with its other
+// loads (the test is branch-free, so nothing waits for them early).
+__device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, uint4 p0, uint4 p1)
 {
-    const uint4 p0 = a.prev[2 * row], p1 = a.prev[2 * row + 1];
-    const bool nopins = a.pin_lo == 0 && a.pin_hi == a.n;
-    const bool ok = p0.w == 1u && (uint32_t)a.k <= p0.y && (uint32_t)a.n >= p0.z &&
-                    p1.x == (uint32_t)a.pin_lo && p1.y == (uint32_t)(a.n - a.pin_hi) &&
-                    ((uint32_t)a.n == p0.z || nopins);
+    const bool nopins = (a.pin_lo == 0) & (a.pin_hi == a.n);
+    const bool ok = (p0.w == 1u) & ((uint32_t)a.k <= p0.y) & ((uint32_t)a.n >= p0.z) &
+                    (p1.x == (uint32_t)a.pin_lo) & (p1.y == (uint32_t)(a.n - a.pin_hi)) &
+                    (((uint32_t)a.n == p0.z) | nopins);
     return ok ? (p0.x >> (32 - kHistBits)) | 0x80000000u : 0u;
 }
 
@@ -262,27 +263,34 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bool do_hist = a.hist != nullptr;
-    if (do_hist) key_hist_clear(kh);
-    const uint32_t bnd = a.prev ? stream_bound(a, row) : 0u;   // loaded early, used at the end
-    const uint32_t hist_lo = (bnd >> 31) ? (bnd & (kHistBins - 1)) : 0u;
+    // Every load of the opening is issued before anything waits for one: the
+    // softmax partials, this thread's old S, the first batch of logits and the
+    // streamed selection's state (whose test runs only after the statistics).
     HeadParts hp;
     load_head_parts(a, b, h0, nh, hp);
     const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
     const int jc = min(j4, (int)(a.ld - 4));              // rows are padded to ld (multiple of 4)
     const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
-    // this thread's old importance, loaded with the logits
     const int j = blockIdx.x * kUpdChunk + tid;
     float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
-    const float s_old = j < a.n ? srow[j] : 0.0f;
-    // the first batch of logits is issued before the statistics are folded
+    const float s_ld = srow[min(j, a.n - 1)];             // unconditional: no branch around the load
     float4 x[kHeadBatch];
 #pragma unroll
     for (int i = 0; i < kHeadBatch; ++i) {
         const int h = w + 4 * i;
         x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+    uint4 p0 = make_uint4(0u, 0u, 0u, 0u), p1 = p0;
+    if (a.prev) {
+        p0 = a.prev[2 * row];
+        p1 = a.prev[2 * row + 1];
+    }
     __builtin_amdgcn_sched_barrier(0);
+    if (do_hist) key_hist_clear(kh);
     finish_head_stats(a, b, h0, nh, hp, red, ms);
+    const float s_old = j < a.n ? s_ld : 0.0f;
+    const uint32_t bnd = a.prev ? stream_bound(a, p0, p1) : 0u;
+    const uint32_t hist_lo = (bnd >> 31) ? (bnd & (kHistBins - 1)) : 0u;
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (int hb = w;;) {
 #pragma unroll
