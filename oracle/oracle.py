@@ -25,6 +25,8 @@ one definition of the paper (arxiv 2602.18750):
 * :func:`bkp_update`  -- the hit-rate table and the hot/cold pool policy of
                          the Bidirectional KV Cache Pools (Sec. 4.2 HKM,
                          BKP (1)-(3)), plain numpy on integers.
+* :func:`tier_apply`  -- the migration of rows between the hot and the cold
+                         pool that a BKP pass decides (Sec. 4.2 BKP (3)).
 * :func:`app_split`   -- the Adaptive Prefetch-based Pipeline's capacity
                          split (Sec. 4.3): Eq. 2's balance solved by
                          bisection, with the host-memory bound Eq. 3.
@@ -345,6 +347,57 @@ def bkp_update(hits, hot, idx, n_tokens: int, n_recent: int, capacity: int):
             demote[b][r] = np.nonzero(old & ~new)[0]
             hot_new[b, r, :N] = new
     return hits.astype(np.uint16), hot_new, promote, demote
+
+
+def tier_apply(loc, promote, demote, n_prev: int, n_tokens: int, capacity: int):
+    """The migration of one BKP pass between the two tiers (Sec. 4.2 BKP (3):
+    promoted tokens move up to the hot pool, demoted ones down to the cold
+    pool, an equal volume each way once the pool is full; the pools are
+    exclusive, so a token's K/V row lives in exactly one of them).
+
+    loc: int [B, R, >= n_tokens], the hot-pool slot of each token or -1 for
+    the cold pool, as it stood after the previous pass over n_prev tokens
+    (the pool then held min(capacity, n_prev) tokens in slots
+    0 .. min(capacity, n_prev) - 1).  promote, demote: nested lists [B][R]
+    of ascending token arrays (bkp_update's).
+
+    Slot rule (a layout of this library; the paper places rows in pools but
+    fixes no slot order): the slot of the i-th demoted token passes to the
+    i-th promoted token; promoted tokens beyond the demoted ones take the
+    slots never used before, in order, from min(capacity, n_prev).  A pass
+    must leave min(capacity, n_tokens) tokens hot, so #promote - #demote must
+    equal min(capacity, n_tokens) - min(capacity, n_prev) (else ValueError).
+
+    Returns the new loc (a copy) and the moves [B][R] as lists of
+    (token, slot, direction), direction +1 up (cold -> hot slot) and -1 down
+    (hot slot -> cold)."""
+    loc = np.array(loc, dtype=np.int64, copy=True)
+    B, R = loc.shape[0], loc.shape[1]
+    used_prev = min(int(capacity), int(n_prev))
+    used_now = min(int(capacity), int(n_tokens))
+    moves = [[None] * R for _ in range(B)]
+    for b in range(B):
+        for r in range(R):
+            pr = [int(j) for j in promote[b][r]]
+            de = [int(j) for j in demote[b][r]]
+            if len(pr) - len(de) != used_now - used_prev:
+                raise ValueError("row (%d, %d): %d promotions and %d demotions do not take the pool from %d to %d"
+                                 % (b, r, len(pr), len(de), used_prev, used_now))
+            mv = []
+            for i, j in enumerate(de):
+                slot = int(loc[b, r, j])
+                if slot < 0:
+                    raise ValueError("demoted token %d is not in the hot pool" % j)
+                mv.append((j, slot, -1))
+            for i, j in enumerate(pr):
+                if loc[b, r, j] >= 0:
+                    raise ValueError("promoted token %d is already in the hot pool" % j)
+                slot = mv[i][1] if i < len(de) else used_prev + (i - len(de))
+                mv.append((j, slot, +1))
+            for j, slot, d in mv:
+                loc[b, r, j] = slot if d > 0 else -1
+            moves[b][r] = mv
+    return loc, moves
 
 
 def app_split(f_c, f_s, b_c, b_s, alpha_c, alpha_s, m, m0=0.0, iters=200):

@@ -703,3 +703,67 @@ def test_sketch4_selection_recall_vs_full_precision(wid, floor):
         S4 = O.update(O.logits_i8(q8, eq, k4, ek), S4, w.n_kv_heads, "attn", "token", O.default_scale(128))
         for b in range(w.batch):
             assert len(np.intersect1d(O.topk(S[b:b + 1], k), O.topk(S4[b:b + 1], k))) / k >= floor
+
+
+# ------------------------------------- tier migration (Sec. 4.2 BKP (3)) --
+
+def _tier(loc, pr, de, n_prev, n, cap):
+    l2, mv = O.tier_apply(np.array(loc)[None, None], [[np.array(pr)]], [[np.array(de)]], n_prev, n, cap)
+    return list(l2[0, 0]), mv[0][0]
+
+
+def test_tier_apply_worked_cases():
+    # pool of 3 slots holding tokens 0 and 1 (n_prev 2); the context grows to 4 and the pass
+    # promotes 2 and 3 and demotes 0: token 2 takes 0's slot, token 3 the first unused slot (2)
+    loc, mv = _tier([0, 1, -1, -1], [2, 3], [0], 2, 4, 3)
+    assert loc == [-1, 1, 0, 2]
+    assert sorted(mv) == [(0, 0, -1), (2, 0, 1), (3, 2, 1)]
+    # full pool, equal volume each way: slots pass in list order
+    loc, mv = _tier([2, -1, 0, -1, 1, -1], [1, 3], [0, 4], 6, 6, 3)
+    assert loc == [-1, 2, 0, 1, -1, -1]
+    # nothing moves
+    loc, mv = _tier([0, -1, 1], [], [], 3, 3, 2)
+    assert loc == [0, -1, 1] and mv == []
+    # filling an empty pool
+    loc, mv = _tier([-1, -1, -1, -1], [0, 2, 3], [], 0, 4, 3)
+    assert loc == [0, -1, 1, 2]
+
+
+def test_tier_apply_rejects_inconsistent_lists():
+    with pytest.raises(ValueError):
+        _tier([0, 1, -1, -1], [2], [0], 2, 4, 3)          # the pool must grow by one
+    with pytest.raises(ValueError):
+        _tier([0, 1, -1, -1], [1, 2], [0], 2, 4, 3)       # 1 is hot already
+    with pytest.raises(ValueError):
+        _tier([0, 1, -1, -1], [2, 3], [3], 2, 4, 3)       # 3 is cold
+
+
+@settings(max_examples=60, deadline=None)
+@given(data=st.data())
+def test_tier_apply_follows_the_pool_over_passes(data):
+    """Many BKP passes with random selections and a growing context: after
+    every migration the tokens with a slot are exactly the pool's hot set,
+    the slots in use are exactly 0 .. min(capacity, N) - 1 with no slot
+    shared, and a token keeps its slot while it stays hot."""
+    n0 = data.draw(st.integers(1, 30))
+    cap = data.draw(st.integers(1, 25))
+    w = data.draw(st.integers(0, cap))
+    steps = data.draw(st.integers(1, 6))
+    ncap = n0 + 3 * steps
+    hits = np.zeros((1, 1, ncap), dtype=np.uint16)
+    hot = np.zeros((1, 1, ncap), dtype=bool)
+    loc = np.full((1, 1, ncap), -1, dtype=np.int64)
+    n_prev = 0
+    n = n0
+    for _ in range(steps):
+        k = data.draw(st.integers(0, n))
+        idx = np.sort(np.array(data.draw(st.permutations(list(range(n))))[:k], dtype=np.int64)).reshape(1, 1, -1)
+        hits, hot2, pr, de = O.bkp_update(hits, hot, idx, n, w, cap)
+        loc2, _ = O.tier_apply(loc, pr, de, n_prev, n, cap)
+        assert np.array_equal(loc2[0, 0, :n] >= 0, hot2[0, 0, :n])
+        slots = loc2[0, 0][loc2[0, 0] >= 0]
+        assert sorted(slots.tolist()) == list(range(min(cap, n)))
+        stay = hot[0, 0, :n] & hot2[0, 0, :n]
+        assert np.array_equal(loc2[0, 0, :n][stay], loc[0, 0, :n][stay])
+        loc, hot, n_prev = loc2, hot2, n
+        n = min(ncap, n + data.draw(st.integers(0, 3)))
