@@ -345,6 +345,60 @@ HILL_API hill_status hill_bkp_update(const hill_bkp_desc* d, const int32_t* idx,
                             uint8_t* hot, int32_t* promote, int32_t* demote, int32_t list_cap, int32_t* counts,
                             void* ws, size_t ws_bytes, void* stream);
 
+/* Tiered KV cache: the hot and cold pools of Sec. 4.2 (BKP) as two memory
+ * tiers of one node -- the hot pool's K/V rows in HBM, the cold pool's in
+ * host memory that the GPU reads and writes in place (pinned, allocated with
+ * hipHostMalloc) -- with each token's row in exactly one of them.  Scoring
+ * reads a key sketch of every token kept in HBM (the low-precision
+ * evaluation the paper runs beside its cold pool, Sec. 4.4); the attention
+ * gathers the selected tokens' rows from whichever pool holds them; after a
+ * step, hill_bkp_update decides the pools and hill_tier_apply moves the rows.
+ *
+ * Layouts.  Hot pool: K_hot, V_hot [B, Hkv, capacity, D] 16-bit rows by slot,
+ * both with the strides below (D contiguous).  Cold pool: K_cold, V_cold
+ * [B, Hkv, >= n_cap, D] rows by token position, with the hill_desc's k / v
+ * strides.  loc: int32 [B, R, n_cap] contiguous, 16-byte aligned: the slot
+ * that holds the token's row in the hot pool, or -1 (cold pool).  R = 1 in
+ * token mode (all KV heads of a token share its slot and move together) or
+ * n_kv_heads in KV-head mode (one slot table per KV head).  A pool that
+ * starts empty has loc = -1 everywhere and every row in the cold pool. */
+typedef struct hill_tier_desc {
+    uint32_t struct_size;   /* sizeof(hill_tier_desc) */
+    int32_t capacity;       /* hot-pool slots per row (b, r), >= 1 */
+    int32_t n_cap;          /* tokens per row of loc: >= n_tokens, a multiple of 4 */
+    int32_t reserved;       /* 0 */
+    int64_t hot_stride_b, hot_stride_h, hot_stride_n;   /* K_hot and V_hot strides in elements */
+} hill_tier_desc;
+
+/* One row migration after a BKP pass (Sec. 4.2 BKP (3)): promote / demote /
+ * counts are hill_bkp_update's lists for this context (d->n_tokens tokens,
+ * rows = R, capacity = the pool's), list_cap the lists' row length, at least
+ * min(capacity, n_tokens) so that no list is cut.  The i-th demoted token's
+ * row moves from its slot to the cold pool and the i-th promoted token's row
+ * from the cold pool into that slot; promoted tokens beyond the demoted ones
+ * take the slots never used before, from min(capacity, n_prev) on, where
+ * n_prev is the context of the previous pass over this pool (0 for an empty
+ * pool): the pool then holds min(capacity, n_tokens) rows in slots 0 .. that
+ * number - 1.  loc is updated.  A row whose lists do not fit that (cut lists,
+ * a pass over another context, a token out of place) is left as it was and
+ * sets bit 0 or 1 of *status (device int32, caller-cleared; nothing else
+ * writes it).  k_hot, v_hot, k_cold, v_cold: 16-byte aligned; the cold pool
+ * may be host memory.  Asynchronous on stream. */
+HILL_API hill_status hill_tier_apply(const hill_desc* d, const hill_tier_desc* t, void* k_hot, void* v_hot,
+                            void* k_cold, void* v_cold, int32_t* loc, const int32_t* promote,
+                            const int32_t* demote, int32_t list_cap, const int32_t* counts, int32_t n_prev,
+                            int32_t* status, void* stream);
+
+/* hill_step_sketch over a tiered cache: S, the selection and the outputs are
+ * those of hill_step_sketch on a cache holding every row (the same values,
+ * read from whichever pool holds them); d's k / v strides describe the cold
+ * pool.  state, flags and ev as for hill_step_sketch. */
+HILL_API hill_status hill_step_tiered(const hill_desc* d, const hill_tier_desc* t, const void* q, const void* k_hot,
+                             const void* v_hot, const void* k_cold, const void* v_cold, const int32_t* loc,
+                             const int8_t* k8, const int8_t* k_exp, int64_t cap, int32_t bits, float* s,
+                             uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out,
+                             void* ws, size_t ws_bytes, void* stream, const hill_step_events* ev);
+
 /* Adaptive Prefetch-based Pipeline (Sec. 4.3, Eqs. 2-4): the split of the KV
  * bytes M scored per step between a hot pool (subscript c) and a cold pool
  * (subscript s) whose scorers run in parallel, so that both paths, scoring

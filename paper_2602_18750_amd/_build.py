@@ -20,7 +20,7 @@ CALIB_LIB = os.path.join(PKG, "libhill_calib.so")
 # per-kernel registers, scratch and occupancy as the compiler reports them
 RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
-SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", "attn.hip", "bkp.hip", "noalloc.hip"]
+SOURCES = ["hill_api.cpp", "score.hip", "update.hip", "sketch.hip", "topk.hip", "attn.hip", "bkp.hip", "noalloc.hip", "tier.hip"]
 CALIB_SOURCES = ["calib.hip"]
 ARCH = os.environ.get("HILL_OFFLOAD_ARCH", "gfx950")
 

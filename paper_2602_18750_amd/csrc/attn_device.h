@@ -80,29 +80,85 @@ __device__ __forceinline__ uint64_t row_off(int j, int n, int64_t stride)
     return (uint64_t)(uint32_t)j * (uint32_t)stride;
 }
 
+// Where list entry t's row lies: the cache row of its token, or, in a tiered
+// cache (TIER), the hot pool's slot sloc[t] when that is >= 0 and the cold
+// pool's row of the token otherwise (sloc: the entries' slots in LDS).  cold
+// and hot are the row bases of this lane's slice for the (b, KV head).
+struct RowSrc {
+    const uint16_t* cold;
+    const uint16_t* hot;
+    int64_t cold_sn, hot_sn;
+    int n, cap;
+    const int32_t* sloc;
+};
+
+template <bool TIER>
+__device__ __forceinline__ const uint16_t* entry_row(const RowSrc& r, const int32_t* tok, int t)
+{
+    if constexpr (TIER) {
+        const int s = r.sloc[t];
+        const bool hot = s >= 0;
+        return hot ? r.hot + row_off(s, r.cap, r.hot_sn) : r.cold + row_off(tok[t], r.n, r.cold_sn);
+    }
+    return r.cold + row_off(tok[t], r.n, r.cold_sn);
+}
+
 // K rows of entries t0, t0+16, ... (kKBatch of them) for this lane's
 // 16-byte slice; entries past cnt are clamped to the last one (their logits
 // are not stored).  Unconditional loads keep the wait counters exact.
-__device__ __forceinline__ void load_k_rows(const AttnArgs& a, const uint16_t* kb, const int32_t* tok, int t0, int cnt,
+template <bool TIER = false>
+__device__ __forceinline__ void load_k_rows(const RowSrc& kr_src, const int32_t* tok, int t0, int cnt,
                                             uint4 (&kr)[kKBatch])
 {
 #pragma unroll
     for (int u = 0; u < kKBatch; ++u) {
         const int t = min(t0 + 16 * u, cnt - 1);
-        kr[u] = *reinterpret_cast<const uint4*>(kb + row_off(tok[t], a.n, a.k_sn));
+        kr[u] = *reinterpret_cast<const uint4*>(entry_row<TIER>(kr_src, tok, t));
     }
 }
 
 // V element pairs of entries t0, t0+4, ... (kVBatch of them); entries past
 // cnt are clamped to the last one (they weigh 0).
-__device__ __forceinline__ void load_v_rows(const AttnArgs& a, const uint16_t* vb, const int32_t* tok, int t0, int cnt,
+template <bool TIER = false>
+__device__ __forceinline__ void load_v_rows(const RowSrc& vr_src, const int32_t* tok, int t0, int cnt,
                                             uint32_t (&vr)[kVBatch])
 {
 #pragma unroll
     for (int i = 0; i < kVBatch; ++i) {
         const int t = min(t0 + 4 * i, cnt - 1);
-        vr[i] = *reinterpret_cast<const uint32_t*>(vb + row_off(tok[t], a.n, a.v_sn));
+        vr[i] = *reinterpret_cast<const uint32_t*>(entry_row<TIER>(vr_src, tok, t));
     }
+}
+
+// The K (lane offset 8 * l16 elements) and V (lane offset 2 * lane) row
+// sources of (b, g): the cache, or the two pools of a tiered cache with the
+// block's slots in sloc.
+__device__ __forceinline__ RowSrc k_src(const AttnArgs& a, int b, int g, const int32_t* sloc)
+{
+    const int l16 = threadIdx.x & 15;
+    RowSrc r;
+    r.cold = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
+    r.cold_sn = a.k_sn;
+    r.n = a.n;
+    r.hot = a.loc ? a.k_hot + (int64_t)b * a.hk_sb + (int64_t)g * a.hk_sh + l16 * 8 : r.cold;
+    r.hot_sn = a.hk_sn;
+    r.cap = a.cap;
+    r.sloc = sloc;
+    return r;
+}
+
+__device__ __forceinline__ RowSrc v_src(const AttnArgs& a, int b, int g, const int32_t* sloc)
+{
+    const int lane = threadIdx.x & 63;
+    RowSrc r;
+    r.cold = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
+    r.cold_sn = a.v_sn;
+    r.n = a.n;
+    r.hot = a.loc ? a.v_hot + (int64_t)b * a.hv_sb + (int64_t)g * a.hv_sh + 2 * lane : r.cold;
+    r.hot_sn = a.hv_sn;
+    r.cap = a.cap;
+    r.sloc = sloc;
+    return r;
 }
 
 // Logits of entries t0, t0+16, ... into sh.p (lane l16 == hh of the row group
@@ -199,8 +255,8 @@ __device__ __forceinline__ void softmax_block(int cnt, AttnLds<GC>& sh)
 
 // weight * V over this wave's entries w, w+4, ... of the block: the first 16
 // (and, when `two`, 32) from the rows already loaded, the rest loaded here.
-template <int DT, int GC>
-__device__ __forceinline__ void values_block(const AttnArgs& a, const uint16_t* vb, int w, int cnt, int nmine, bool two,
+template <int DT, int GC, bool TIER = false>
+__device__ __forceinline__ void values_block(const RowSrc& vs, int w, int cnt, int nmine, bool two,
                                              const uint32_t (&vr)[kVBatch], const uint32_t (&vr2)[kVBatch],
                                              AttnAcc<GC>& acc, AttnLds<GC>& sh)
 {
@@ -214,7 +270,7 @@ __device__ __forceinline__ void values_block(const AttnArgs& a, const uint16_t* 
     if (two) values_rows<DT, GC>(vr2, w, kVBatch, nmine, cnt, sh.p, acc);
     for (int i0 = 2 * kVBatch; i0 < nmine; i0 += kVBatch) {   // lists longer than 128
         uint32_t vx[kVBatch];
-        load_v_rows(a, vb, sh.tok, w + 4 * i0, cnt, vx);
+        load_v_rows<TIER>(vs, sh.tok, w + 4 * i0, cnt, vx);
         values_rows<DT, GC>(vx, w, i0, nmine, cnt, sh.p, acc);
     }
 }
@@ -223,16 +279,17 @@ __device__ __forceinline__ void values_block(const AttnArgs& a, const uint16_t* 
 // made visible by a barrier before the call) into the running state.  Every
 // thread of the workgroup must call this.  The K rows are issued before the
 // V rows, so that the logits wait for K only; every loop bound is
-// wave-uniform.
-template <int DT, int GC>
+// wave-uniform.  TIER: a tiered cache, the entries' hot-pool slots in sloc
+// (written with sh.tok).
+template <int DT, int GC, bool TIER = false>
 __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, const uint4 (&qv)[GC], int cnt,
-                                           AttnAcc<GC>& acc, AttnLds<GC>& sh)
+                                           AttnAcc<GC>& acc, AttnLds<GC>& sh, const int32_t* sloc = nullptr)
 {
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = threadIdx.x;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar control flow
-    const int rg = tid >> 4, l16 = tid & 15;
-    const uint16_t* kb = a.k + (int64_t)b * a.k_sb + (int64_t)g * a.k_sh + l16 * 8;
-    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
+    const int rg = tid >> 4;
+    const RowSrc ks = k_src(a, b, g, sloc);
+    const RowSrc vs = v_src(a, b, g, sloc);
 
     // A: logits of every entry, into sh.p.  Up to 128 entries take one round
     // trip: the K rows of entries < 64 (and < 128 when the list is longer),
@@ -240,23 +297,23 @@ __device__ __forceinline__ void attn_block(const AttnArgs& a, int b, int g, cons
     const int nmine = cnt > w ? (cnt - w + 3) / 4 : 0;   // this wave's entries w, w+4, ...
     const bool two = cnt > 16 * kKBatch;                 // block-uniform
     uint4 kr[kKBatch], kr2[kKBatch];
-    load_k_rows(a, kb, sh.tok, rg, cnt, kr);
-    if (two) load_k_rows(a, kb, sh.tok, rg + 16 * kKBatch, cnt, kr2);
+    load_k_rows<TIER>(ks, sh.tok, rg, cnt, kr);
+    if (two) load_k_rows<TIER>(ks, sh.tok, rg + 16 * kKBatch, cnt, kr2);
     __builtin_amdgcn_sched_barrier(0);   // keep the K loads ahead of the V loads in the queue
     uint32_t vr[kVBatch], vr2[kVBatch];
-    load_v_rows(a, vb, sh.tok, w, cnt, vr);
-    if (two) load_v_rows(a, vb, sh.tok, w + 4 * kVBatch, cnt, vr2);
+    load_v_rows<TIER>(vs, sh.tok, w, cnt, vr);
+    if (two) load_v_rows<TIER>(vs, sh.tok, w + 4 * kVBatch, cnt, vr2);
     logits_rows<DT, GC>(a, qv, kr, rg, cnt, (cnt - 4 * w + 15) / 16, sh.p);
     if (two) logits_rows<DT, GC>(a, qv, kr2, rg + 16 * kKBatch, cnt, (cnt - 16 * kKBatch - 4 * w + 15) / 16, sh.p);
     for (int base = 32 * kKBatch; base < cnt; base += 16 * kKBatch) {   // lists longer than 128
         uint4 kx[kKBatch];
-        load_k_rows(a, kb, sh.tok, base + rg, cnt, kx);
+        load_k_rows<TIER>(ks, sh.tok, base + rg, cnt, kx);
         logits_rows<DT, GC>(a, qv, kx, base + rg, cnt, (cnt - base - 4 * w + 15) / 16, sh.p);
     }
     __syncthreads();
 
     softmax_block<GC>(cnt, sh);
-    values_block<DT, GC>(a, vb, w, cnt, nmine, two, vr, vr2, acc, sh);
+    values_block<DT, GC, TIER>(vs, w, cnt, nmine, two, vr, vr2, acc, sh);
 }
 
 // attn_block with the logits already in sh.p (scaled by s2, written with
@@ -266,16 +323,15 @@ template <int DT, int GC>
 __device__ __forceinline__ void attn_block_logits(const AttnArgs& a, int b, int g, int cnt, AttnAcc<GC>& acc,
                                                   AttnLds<GC>& sh)
 {
-    const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint16_t* vb = a.v + (int64_t)b * a.v_sb + (int64_t)g * a.v_sh + 2 * lane;
+    const RowSrc vs = v_src(a, b, g, nullptr);
     const int nmine = cnt > w ? (cnt - w + 3) / 4 : 0;
     const bool two = cnt > 4 * kVBatch;   // block-uniform
     uint32_t vr[kVBatch], vr2[kVBatch];
-    load_v_rows(a, vb, sh.tok, w, cnt, vr);
-    if (two) load_v_rows(a, vb, sh.tok, w + 4 * kVBatch, cnt, vr2);
+    load_v_rows(vs, sh.tok, w, cnt, vr);
+    if (two) load_v_rows(vs, sh.tok, w + 4 * kVBatch, cnt, vr2);
     softmax_block<GC>(cnt, sh);
-    values_block<DT, GC>(a, vb, w, cnt, nmine, two, vr, vr2, acc, sh);
+    values_block<DT, GC>(vs, w, cnt, nmine, two, vr, vr2, acc, sh);
 }
 
 // Adds the four waves' outputs and writes the partial (m, l, o[D]) of heads

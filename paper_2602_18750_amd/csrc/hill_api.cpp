@@ -443,6 +443,49 @@ hill_status run_attn(const hill_desc* d, const Shape& s, const Layout& L, const 
 
 // One decode step: score (16-bit keys or the sketch), refine the threshold,
 // then emit the indices and attend over each chunk's picks in the same kernel.
+// Optional tiered cache of a decode step: the hot pool and the slot table
+// (the step's k and v are then the cold pool).
+struct Tier {
+    const hill_tier_desc* t = nullptr;
+    const void* k_hot = nullptr;
+    const void* v_hot = nullptr;
+    const int32_t* loc = nullptr;
+};
+
+// The cold pool may be host memory: it must be memory the GPU can reach (pinned host memory from
+// hipHostMalloc, or device memory); pageable host memory is refused here instead of faulting on the device.
+hill_status check_reachable(const void* p, const char* name)
+{
+    hipPointerAttribute_t at{};
+    if (hipPointerGetAttributes(&at, p) != hipSuccess) {
+        (void)hipGetLastError();   // clear the query's error
+        return fail(HILL_ERR_INVALID_ARG, "%s is not memory the GPU can reach (pinned host or device memory)", name);
+    }
+    if (at.type != hipMemoryTypeHost && at.type != hipMemoryTypeDevice && at.type != hipMemoryTypeManaged)
+        return fail(HILL_ERR_INVALID_ARG, "%s is not memory the GPU can reach (pinned host or device memory)", name);
+    if (at.type == hipMemoryTypeHost && at.devicePointer != p)
+        return fail(HILL_ERR_UNSUPPORTED, "%s: pinned host memory whose device address differs from its host address", name);
+    return HILL_OK;
+}
+
+hill_status check_tier(const Shape& s, const hill_tier_desc* t)
+{
+    if (!t) return fail(HILL_ERR_INVALID_ARG, "tier descriptor is NULL");
+    if (t->struct_size != sizeof(hill_tier_desc))
+        return fail(HILL_ERR_INVALID_ARG, "struct_size %u != sizeof(hill_tier_desc) %zu", t->struct_size,
+                    sizeof(hill_tier_desc));
+    if (t->capacity < 1) return fail(HILL_ERR_INVALID_ARG, "capacity %d < 1", t->capacity);
+    if (t->n_cap < s.n || t->n_cap % 4)
+        return fail(HILL_ERR_INVALID_ARG, "n_cap %d must be >= n_tokens (%d) and a multiple of 4", t->n_cap, s.n);
+    if (t->reserved != 0) return fail(HILL_ERR_INVALID_ARG, "reserved must be 0");
+    const int64_t st[] = {t->hot_stride_b, t->hot_stride_h, t->hot_stride_n};
+    for (int64_t x : st)
+        if (x < 0 || x % 8) return fail(HILL_ERR_INVALID_ARG, "hot-pool strides must be non-negative multiples of 8");
+    if (t->hot_stride_n < s.D) return fail(HILL_ERR_INVALID_ARG, "hot_stride_n < head_dim");
+    if (t->hot_stride_n > INT32_MAX) return fail(HILL_ERR_UNSUPPORTED, "hot_stride_n above 2^31 - 1 elements");
+    return HILL_OK;
+}
+
 // Every argument of a decode step except the workspace.
 hill_status check_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk,
                        const float* s_acc, int32_t k_sel, const int32_t* idx_out, const float* out, Shape* s)
@@ -463,10 +506,20 @@ hill_status check_step(const hill_desc* d, const void* q, const void* k, const v
 
 hill_status run_step(const hill_desc* d, const void* q, const void* k, const void* v, const Sketch& sk, float* s_acc,
                      int32_t k_sel, int32_t* idx_out, float* out, void* ws, size_t ws_bytes, void* stream,
-                     const hill_step_events* ev, uint32_t* stream_state = nullptr, bool stream_reset = false)
+                     const hill_step_events* ev, uint32_t* stream_state = nullptr, bool stream_reset = false,
+                     const Tier& tier = Tier{})
 {
     Shape s;
     HILL_TRY(check_step(d, q, k, v, sk, s_acc, k_sel, idx_out, out, &s));
+    if (tier.t) {
+        HILL_TRY(check_tier(s, tier.t));
+        HILL_TRY(check_ptr(tier.k_hot, "k_hot"));
+        HILL_TRY(check_ptr(tier.v_hot, "v_hot"));
+        HILL_TRY(check_ptr(tier.loc, "loc"));
+        if (!sk.k8) return fail(HILL_ERR_INVALID_ARG, "a tiered step scores on the key sketch");
+        HILL_TRY(check_reachable(k, "k_cold"));
+        HILL_TRY(check_reachable(v, "v_cold"));
+    }
     const Layout L = layout_for(s, k_sel);
     HILL_TRY(check_ws(ws, ws_bytes, L.end_all));
     hipStream_t st = static_cast<hipStream_t>(stream);
@@ -480,6 +533,16 @@ hill_status run_step(const hill_desc* d, const void* q, const void* k, const voi
     if (s.mode == HILL_SCORE_ATTN && !sk.k8) {   // the scan's logits are those of the 16-bit keys: reused
         a.logits = at<float>(ws, L.logits);
         a.ld = s.ld;
+    }
+    if (tier.t) {   // K and V rows through the slot table: the hot pool, else the cold pool (k, v)
+        a.loc = tier.loc;
+        a.loc_sr = tier.t->n_cap;
+        a.k_hot = static_cast<const uint16_t*>(tier.k_hot);
+        a.v_hot = static_cast<const uint16_t*>(tier.v_hot);
+        a.hk_sb = a.hv_sb = tier.t->hot_stride_b;
+        a.hk_sh = a.hv_sh = tier.t->hot_stride_h;
+        a.hk_sn = a.hv_sn = tier.t->hot_stride_n;
+        a.cap = tier.t->capacity;
     }
     if (state4 && !stream_reset) {   // no refine pass
         r.state_out = state4;
@@ -840,6 +903,84 @@ hill_status hill_step_sketch(const hill_desc* d, const void* q, const void* k, c
     }
     return run_step(d, q, k, v, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes, stream, ev,
                     state, (flags & HILL_STREAM_RESET) != 0);
+}
+
+hill_status hill_step_tiered(const hill_desc* d, const hill_tier_desc* t, const void* q, const void* k_hot,
+                             const void* v_hot, const void* k_cold, const void* v_cold, const int32_t* loc,
+                             const int8_t* k8, const int8_t* k_exp, int64_t cap, int32_t bits, float* s_acc,
+                             uint32_t* state, uint32_t flags, int32_t k_sel, int32_t* idx_out, float* out, void* ws,
+                             size_t ws_bytes, void* stream, const hill_step_events* ev)
+{
+    if (!t) return fail(HILL_ERR_INVALID_ARG, "tier descriptor is NULL");
+    if (!k8 || !k_exp) return fail(HILL_ERR_INVALID_ARG, "sketch codes or exponents are NULL");
+    HILL_TRY(check_stream_flags(state, flags));
+    if (state) {
+        if (!d) return fail(HILL_ERR_INVALID_ARG, "descriptor is NULL");
+        if (d->score_mode != HILL_SCORE_ATTN)
+            return fail(HILL_ERR_UNSUPPORTED, "streamed selection needs ATTN scores (S must only grow)");
+        if ((uintptr_t)state & 15u) return fail(HILL_ERR_INVALID_ARG, "state is not 16-byte aligned");
+    }
+    if (loc && ((uintptr_t)loc & 15u)) return fail(HILL_ERR_INVALID_ARG, "loc is not 16-byte aligned");
+    Tier tier;
+    tier.t = t;
+    tier.k_hot = k_hot;
+    tier.v_hot = v_hot;
+    tier.loc = loc;
+    return run_step(d, q, k_cold, v_cold, Sketch{k8, k_exp, cap, bits}, s_acc, k_sel, idx_out, out, ws, ws_bytes,
+                    stream, ev, state, (flags & HILL_STREAM_RESET) != 0, tier);
+}
+
+hill_status hill_tier_apply(const hill_desc* d, const hill_tier_desc* t, void* k_hot, void* v_hot, void* k_cold,
+                            void* v_cold, int32_t* loc, const int32_t* promote, const int32_t* demote,
+                            int32_t list_cap, const int32_t* counts, int32_t n_prev, int32_t* status, void* stream)
+{
+    Shape s;
+    HILL_TRY(check_desc(d, &s, false));
+    HILL_TRY(check_tier(s, t));
+    HILL_TRY(check_ptr(k_hot, "k_hot"));
+    HILL_TRY(check_ptr(v_hot, "v_hot"));
+    HILL_TRY(check_ptr(k_cold, "k_cold"));
+    HILL_TRY(check_ptr(v_cold, "v_cold"));
+    HILL_TRY(check_ptr(loc, "loc"));
+    if (list_cap < 1) return fail(HILL_ERR_INVALID_ARG, "list_cap %d < 1", list_cap);
+    HILL_TRY(check_reachable(k_cold, "k_cold"));
+    HILL_TRY(check_reachable(v_cold, "v_cold"));
+    if (!promote || !demote || ((uintptr_t)promote & 3u) || ((uintptr_t)demote & 3u))
+        return fail(HILL_ERR_INVALID_ARG, "promote / demote NULL or not 4-byte aligned");
+    if (!counts || ((uintptr_t)counts & 3u)) return fail(HILL_ERR_INVALID_ARG, "counts is NULL or not 4-byte aligned");
+    if (!status || ((uintptr_t)status & 3u)) return fail(HILL_ERR_INVALID_ARG, "status is NULL or not 4-byte aligned");
+    if (n_prev < 0 || n_prev > s.n)
+        return fail(HILL_ERR_INVALID_ARG, "n_prev %d not in [0, n_tokens=%d]", n_prev, s.n);
+    if ((int64_t)s.B * s.R > 65535) return fail(HILL_ERR_UNSUPPORTED, "batch * rows above 65535");
+    TierArgs a{};
+    a.k_hot = static_cast<uint16_t*>(k_hot);
+    a.v_hot = static_cast<uint16_t*>(v_hot);
+    a.k_cold = static_cast<uint16_t*>(k_cold);
+    a.v_cold = static_cast<uint16_t*>(v_cold);
+    a.hk_sb = a.hv_sb = t->hot_stride_b;
+    a.hk_sh = a.hv_sh = t->hot_stride_h;
+    a.hk_sn = a.hv_sn = t->hot_stride_n;
+    a.ck_sb = d->k_stride_b;
+    a.ck_sh = d->k_stride_h;
+    a.ck_sn = d->k_stride_n;
+    a.cv_sb = d->v_stride_b;
+    a.cv_sh = d->v_stride_h;
+    a.cv_sn = d->v_stride_n;
+    a.loc = loc;
+    a.loc_sr = t->n_cap;
+    a.promote = promote;
+    a.demote = demote;
+    a.counts = counts;
+    a.list_cap = list_cap;
+    a.R = s.R;
+    a.Hkv = s.Hkv;
+    a.n = s.n;
+    a.cap = t->capacity;
+    a.used_prev = n_prev < t->capacity ? n_prev : t->capacity;
+    a.used_now = s.n < t->capacity ? s.n : t->capacity;
+    a.status = status;
+    HIP_TRY(launch_tier_apply(a, s.B * s.R, static_cast<hipStream_t>(stream)));
+    return HILL_OK;
 }
 
 }  // extern "C"

@@ -109,7 +109,36 @@ struct AttnArgs {
     float* part_o;           // [B,Hq,nsplit,D]
     float2* part_ml;         // [B,Hq,nsplit] (max, sum) in the exp2 domain
     float* out;              // [B,Hq,D]
+    // tiered cache (nullable loc): k and v above are the cold pool (rows by token), these the hot pool
+    // (rows by slot); loc [B, R, loc_sr] holds each token's slot or -1
+    const int32_t* loc;
+    int64_t loc_sr;
+    const uint16_t* k_hot;
+    const uint16_t* v_hot;
+    int64_t hk_sb, hk_sh, hk_sn, hv_sb, hv_sh, hv_sn;
+    int cap;                 // hot-pool slots per row
 };
+
+// Row migration of a BKP pass between the hot pool (HBM slots) and the cold
+// pool (rows by token, host memory): see hill_tier_apply.
+struct TierArgs {
+    uint16_t* k_hot;
+    uint16_t* v_hot;
+    uint16_t* k_cold;
+    uint16_t* v_cold;
+    int64_t hk_sb, hk_sh, hk_sn, hv_sb, hv_sh, hv_sn;    // hot pool strides
+    int64_t ck_sb, ck_sh, ck_sn, cv_sb, cv_sh, cv_sn;    // cold pool strides
+    int32_t* loc;             // [B, R, loc_sr]
+    int64_t loc_sr;
+    const int32_t* promote;   // [B, R, list_cap]
+    const int32_t* demote;
+    const int32_t* counts;    // [B, R, 2] (promotions, demotions)
+    int list_cap;
+    int R, Hkv, n, cap;
+    int used_prev, used_now;  // slots in use before and after the pass: min(cap, n_prev), min(cap, n)
+    int32_t* status;          // set to 1 when a row's counts do not fit (that row is left as it was)
+};
+
 
 // Exact top-k over 512-token chunks of each importance row (rows = B*R).
 // Counts and lists live in the workspace.
@@ -182,6 +211,7 @@ constexpr size_t kStaticScratchBytes = (size_t)32 << 20;
 hipError_t static_scratch(void** ptr);
 
 hipError_t launch_fill_zero(uint32_t* p, int64_t words, hipStream_t st);
+hipError_t launch_tier_apply(const TierArgs& a, int rows, hipStream_t st, Stamp ts = {});
 hipError_t launch_sketch_keys(const SketchArgs& a, int dtype, hipStream_t st);
 // Bidirectional KV cache pools (bkp.hip).
 struct BkpArgs {

@@ -341,10 +341,15 @@ __device__ __forceinline__ void load_chunk_logits(const AttnArgs& at, int b, int
 }
 
 // With LG the attention takes its logits from the scan (at.logits) instead
-// of recomputing q.k from gathered K rows.
-template <int DT, int GC, bool ATTN, bool STREAM = false, bool LG = false>
+// of recomputing q.k from gathered K rows.  TIER: a tiered cache -- each
+// selected token's K and V rows are read from the hot pool's slot that
+// at.loc gives it, or from the cold pool (its row by position) when that is
+// -1; the slots of the chunk's tokens are loaded with its S.
+template <int DT, int GC, bool ATTN, bool STREAM = false, bool LG = false, bool TIER = false>
 __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnArgs at)
 {
+    static_assert(!TIER || (ATTN && !LG), "a tiered cache gathers K and V for the attention");
+    __shared__ int32_t sloc[TIER ? kAttnBlock : 1];
     __shared__ uint32_t hist3[256];
     __shared__ typename std::conditional<STREAM, uint32_t[kHistBins], uint32_t[1]>::type hist2s;
     __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_offs;
@@ -375,6 +380,11 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     uint4 qv[ATTN && !LG ? GC : 1];
     if constexpr (ATTN && !LG) load_queries<GC>(at, b, g, 0, qv);
     const float2 sx = load_s_pair(row_ptr(r, row), c, r.n);
+    int2 lv = make_int2(-1, -1);   // TIER: the hot-pool slots of this thread's two tokens
+    if constexpr (TIER) {
+        const int j = c * kSelChunk + tid * kPerThread;
+        lv = *reinterpret_cast<const int2*>(at.loc + (int64_t)row * at.loc_sr + (j < r.n ? j : ((r.n - 1) & ~1)));
+    }
     float2 lgv[LG ? GC : 1];
     if constexpr (LG) load_chunk_logits<GC>(at, b, g * at.G, c, lgv);
     // exact threshold: (key >> shift) compared with prefix; `need` keys equal to it are taken
@@ -580,6 +590,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         for (int e = 0; e < kPerThread; ++e) {
             if (sel[e]) {
                 sh.tok[p] = j0 + e;
+                if constexpr (TIER) sloc[p] = e == 0 ? lv.x : lv.y;
                 if constexpr (LG) {
 #pragma unroll
                     for (int hh = 0; hh < GC; ++hh) sh.p[p][hh] = at.s2 * (e == 0 ? lgv[hh].x : lgv[hh].y);
@@ -591,7 +602,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         // the first head chunk with the queries (or logits) loaded at the start
         if (tot) {
             if constexpr (LG) attn_block_logits<DT, GC>(at, b, g, (int)tot, acc, sh);
-            else attn_block<DT, GC>(at, b, g, qv, (int)tot, acc, sh);
+            else attn_block<DT, GC, TIER>(at, b, g, qv, (int)tot, acc, sh, sloc);
         }
         attn_finish<GC>(at, b, g, 0, acc, c, r.nchunks, sh);
         for (int i = 1; i < ng * (at.G / GC); ++i) {   // further head chunks and KV heads
@@ -609,7 +620,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
                 if (tot) attn_block_logits<DT, GC>(at, b, gg, (int)tot, acc2, sh);
             } else {
                 load_queries<GC>(at, b, gg, hc, qv);
-                if (tot) attn_block<DT, GC>(at, b, gg, qv, (int)tot, acc2, sh);
+                if (tot) attn_block<DT, GC, TIER>(at, b, gg, qv, (int)tot, acc2, sh, sloc);
             }
             attn_finish<GC>(at, b, gg, hc, acc2, c, r.nchunks, sh);
         }
@@ -685,23 +696,23 @@ __global__ __launch_bounds__(kThreads) void merge_write_kernel(RefineArgs r, Att
     }
 }
 
-template <int DT, int GC, bool STREAM, bool LG>
+template <int DT, int GC, bool STREAM, bool LG, bool TIER>
 void emit_attn_launch(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
 {
     dim3 grid(r.nchunks, at.B * (at.Hkv / at.kv_per_wg));
-    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true, STREAM, LG>), grid, dim3(kThreads), 0, st, ts.start, ts.stop,
-                          0, r, at);
+    hipExtLaunchKernelGGL((topk_emit_kernel<DT, GC, true, STREAM, LG, TIER>), grid, dim3(kThreads), 0, st, ts.start,
+                          ts.stop, 0, r, at);
 }
 
-template <int DT, bool STREAM, bool LG>
+template <int DT, bool STREAM, bool LG, bool TIER = false>
 void emit_attn_gc(const RefineArgs& r, const AttnArgs& at, hipStream_t st, Stamp ts)
 {
     const int gc = (at.G % 8 == 0) ? 8 : (at.G % 4 == 0) ? 4 : (at.G % 2 == 0) ? 2 : 1;
     switch (gc) {
-    case 8: emit_attn_launch<DT, 8, STREAM, LG>(r, at, st, ts); break;
-    case 4: emit_attn_launch<DT, 4, STREAM, LG>(r, at, st, ts); break;
-    case 2: emit_attn_launch<DT, 2, STREAM, LG>(r, at, st, ts); break;
-    default: emit_attn_launch<DT, 1, STREAM, LG>(r, at, st, ts); break;
+    case 8: emit_attn_launch<DT, 8, STREAM, LG, TIER>(r, at, st, ts); break;
+    case 4: emit_attn_launch<DT, 4, STREAM, LG, TIER>(r, at, st, ts); break;
+    case 2: emit_attn_launch<DT, 2, STREAM, LG, TIER>(r, at, st, ts); break;
+    default: emit_attn_launch<DT, 1, STREAM, LG, TIER>(r, at, st, ts); break;
     }
 }
 
@@ -709,10 +720,12 @@ template <bool STREAM>
 hipError_t emit_attn_any(const RefineArgs& r, const AttnArgs& at, int dtype, hipStream_t st, Stamp ts)
 {
     if (dtype == 1) {
-        if (at.logits) emit_attn_gc<1, STREAM, true>(r, at, st, ts);
+        if (at.loc) emit_attn_gc<1, STREAM, false, true>(r, at, st, ts);
+        else if (at.logits) emit_attn_gc<1, STREAM, true>(r, at, st, ts);
         else emit_attn_gc<1, STREAM, false>(r, at, st, ts);
     } else {
-        if (at.logits) emit_attn_gc<0, STREAM, true>(r, at, st, ts);
+        if (at.loc) emit_attn_gc<0, STREAM, false, true>(r, at, st, ts);
+        else if (at.logits) emit_attn_gc<0, STREAM, true>(r, at, st, ts);
         else emit_attn_gc<0, STREAM, false>(r, at, st, ts);
     }
     return hipGetLastError();

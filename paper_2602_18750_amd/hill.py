@@ -39,7 +39,8 @@ ABI_VERSION = 6   # HILL_ABI_VERSION of include/hill.h that this binding's struc
 EXPORTS = ("hill_abi_version", "hill_status_str", "hill_last_error", "hill_workspace_bytes", "hill_score",
            "hill_topk", "hill_gather_attn", "hill_step", "hill_step_profiled", "hill_sketch_keys",
            "hill_score_sketch", "hill_step_sketch", "hill_bkp_workspace_bytes",
-           "hill_bkp_update", "hill_app_balance", "hill_step_streamed", "hill_step_noalloc")
+           "hill_bkp_update", "hill_app_balance", "hill_step_streamed", "hill_step_noalloc", "hill_tier_apply",
+           "hill_step_tiered")
 
 
 class HillError(RuntimeError):
@@ -100,6 +101,13 @@ class BkpDesc(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_uint32), ("batch", ctypes.c_int32), ("rows", ctypes.c_int32),
                 ("n_tokens", ctypes.c_int32), ("n_recent", ctypes.c_int32), ("capacity", ctypes.c_int32),
                 ("stride_b", ctypes.c_int64), ("stride_r", ctypes.c_int64)]
+
+
+class TierDesc(ctypes.Structure):
+    """hill_tier_desc (include/hill.h)."""
+    _fields_ = [("struct_size", ctypes.c_uint32), ("capacity", ctypes.c_int32), ("n_cap", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("hot_stride_b", ctypes.c_int64), ("hot_stride_h", ctypes.c_int64),
+                ("hot_stride_n", ctypes.c_int64)]
 
 
 class AppParams(ctypes.Structure):
@@ -164,6 +172,12 @@ def load_library(path: str = LIB_PATH):
         lib.hill_step_streamed.restype = ctypes.c_int
         lib.hill_step_noalloc.argtypes = [D, P, P, P, P, I32, P, P, P]
         lib.hill_step_noalloc.restype = ctypes.c_int
+        T = ctypes.POINTER(TierDesc)
+        lib.hill_tier_apply.argtypes = [D, T, P, P, P, P, P, P, P, I32, P, I32, P, P]
+        lib.hill_tier_apply.restype = ctypes.c_int
+        lib.hill_step_tiered.argtypes = [D, T, P, P, P, P, P, P, P, P, I64, I32, P, P, U32, I32, P, P, P, SZ, P,
+                                         ctypes.POINTER(HillStepEvents)]
+        lib.hill_step_tiered.restype = ctypes.c_int
         lib.hill_app_balance.argtypes = [ctypes.POINTER(AppParams), ctypes.POINTER(AppPlan)]
         lib.hill_app_balance.restype = ctypes.c_int
         if lib.hill_abi_version() != ABI_VERSION:
@@ -543,6 +557,88 @@ class BkpCall:
 
     def __call__(self, idx_ptr: int):
         _check(self._fn(ctypes.byref(self.desc), ctypes.c_void_p(idx_ptr), self._k, *self._post))
+
+
+class TieredCache:
+    """One layer's K/V split between a hot pool in HBM (``capacity`` slot rows
+    per row (b, r)) and a cold pool in pinned host memory that the GPU reads
+    and writes in place (rows by token position), each token's rows in
+    exactly one of them, plus the key sketch of every token in HBM that the
+    step scores on (include/hill.h, tiered KV cache).  Starts with every row
+    in the cold pool (loc = -1).  ``granularity``: "token" (all KV heads of a
+    token share a slot) or "kvhead"."""
+
+    def __init__(self, k, v, capacity: int, *, granularity="token", bits=8, n_cap=None, stream=None):
+        _device_check(k, v)
+        B, Hkv, n, D = k.shape
+        self.granularity = granularity
+        self.R = 1 if granularity == "token" else Hkv
+        self.capacity = int(capacity)
+        self.n_cap = ((n if n_cap is None else int(n_cap)) + 3) // 4 * 4
+        dev = k.device
+        self.k_cold = torch.empty((B, Hkv, self.n_cap, D), dtype=k.dtype, pin_memory=True)
+        self.v_cold = torch.empty((B, Hkv, self.n_cap, D), dtype=v.dtype, pin_memory=True)
+        if not (self.k_cold.is_pinned() and self.v_cold.is_pinned()):
+            raise RuntimeError("the cold pool could not be allocated as pinned host memory")
+        self.k_cold[:, :, :n].copy_(k)
+        self.v_cold[:, :, :n].copy_(v)
+        self.k_hot = torch.zeros((B, Hkv, self.capacity, D), dtype=k.dtype, device=dev)
+        self.v_hot = torch.zeros((B, Hkv, self.capacity, D), dtype=v.dtype, device=dev)
+        self.loc = torch.full((B, self.R, self.n_cap), -1, dtype=torch.int32, device=dev)
+        self.sketch = sketch_keys(k, bits=bits, stream=stream)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.n_prev = 0   # context of the last migration (the pool holds min(capacity, n_prev) rows)
+        self.desc = TierDesc(ctypes.sizeof(TierDesc), self.capacity, self.n_cap, 0, self.k_hot.stride(0),
+                             self.k_hot.stride(1), self.k_hot.stride(2))
+
+    def step_desc(self, q, s, n_tokens, **kw) -> HillDesc:
+        return make_desc(q, self.k_cold, self.v_cold, s, granularity=self.granularity, n_tokens=n_tokens, **kw)
+
+
+def hill_tier_apply(cache: TieredCache, promote, demote, counts, *, n_tokens: int, stream=None):
+    """Moves the rows that a BKP pass over ``n_tokens`` tokens decided
+    (hill_bkp_update's promote / demote / counts) between the pools and
+    updates the slot table; records n_tokens as the pool's context."""
+    lib = load_library()
+    _device_check(promote, demote, counts)
+    q0 = torch.empty((cache.k_hot.shape[0], cache.k_hot.shape[1], cache.k_hot.shape[3]), dtype=cache.k_hot.dtype,
+                     device="meta")
+    desc = make_desc(q0, cache.k_cold, cache.v_cold, None, granularity=cache.granularity, n_tokens=n_tokens)
+    if not (promote.is_contiguous() and demote.is_contiguous() and counts.is_contiguous()):
+        raise ValueError("promote, demote and counts must be contiguous")
+    _check(lib.hill_tier_apply(ctypes.byref(desc), ctypes.byref(cache.desc), _ptr(cache.k_hot), _ptr(cache.v_hot),
+                               _ptr(cache.k_cold), _ptr(cache.v_cold), _ptr(cache.loc), _ptr(promote), _ptr(demote),
+                               int(promote.shape[-1]), _ptr(counts), int(cache.n_prev), _ptr(cache.status),
+                               _stream_ptr(stream)))
+    cache.n_prev = int(n_tokens)
+
+
+def hill_step_tiered(q, cache: TieredCache, s, k_sel, *, n_tokens=None, mode="attn", sm_scale=0.0, idx_out=None,
+                     out=None, ws=None, stream=None, events=None, stream_state=None, stream_reset=False):
+    """hill_step_sketch over a tiered cache (scores on the cache's sketch, K
+    and V of the selected tokens from whichever pool holds them).  Returns
+    (idx, out)."""
+    lib = load_library()
+    _device_check(q, s, ws, stream_state)
+    n = cache.n_cap if n_tokens is None else int(n_tokens)
+    desc = cache.step_desc(q, s, n, mode=mode, sm_scale=sm_scale)
+    B, R = s.shape[0], s.shape[1]
+    if idx_out is None:
+        idx_out = torch.empty((B, R, k_sel), dtype=torch.int32, device=s.device)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = workspace(desc, k_sel, q.device)
+    if stream_state is not None and (stream_state.dtype != torch.int32 or not stream_state.is_contiguous()):
+        raise ValueError("stream_state must be a contiguous int32 [B, R, 8] tensor")
+    flags = HILL_STREAM_RESET if stream_reset else 0
+    sk = cache.sketch
+    _check(lib.hill_step_tiered(ctypes.byref(desc), ctypes.byref(cache.desc), _ptr(q), _ptr(cache.k_hot),
+                                _ptr(cache.v_hot), _ptr(cache.k_cold), _ptr(cache.v_cold), _ptr(cache.loc),
+                                _ptr(sk.codes), _ptr(sk.exps), sk.cap, sk.bits, _ptr(s), _ptr(stream_state), flags,
+                                int(k_sel), _ptr(idx_out), _ptr(out), _ptr(ws), ws.numel(), _stream_ptr(stream),
+                                None if events is None else ctypes.byref(events)))
+    return idx_out, out
 
 
 def app_balance(*, f_c, f_s, b_c, b_s, alpha=None, alpha_c=None, alpha_s=None, m=1.0, m0=0.0) -> dict:

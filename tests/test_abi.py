@@ -391,3 +391,60 @@ def test_streamed_step_validates(H):
                                   None) == WORKSPACE
     assert lib.hill_step_sketch(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, 1000, 8, FAKE, None, 1, 10,
                                 FAKE, FAKE, FAKE, need, None, None) == INVALID   # flags without a state
+
+
+def _tier_desc(H, **kw):
+    f = dict(capacity=100, n_cap=1000, reserved=0, hot_stride_b=2 * 100 * 128, hot_stride_h=100 * 128,
+             hot_stride_n=128)
+    f.update(kw)
+    return H.TierDesc(ctypes.sizeof(H.TierDesc), f["capacity"], f["n_cap"], f["reserved"], f["hot_stride_b"],
+                      f["hot_stride_h"], f["hot_stride_n"])
+
+
+def test_tier_desc_layout_matches_header(H):
+    text = open(HEADER).read()
+    body = re.search(r"typedef struct hill_tier_desc \{(.*?)\} hill_tier_desc;", text, re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    names = []
+    for decl in body.split(";"):
+        decl = decl.strip()
+        if decl:
+            names += [x.strip() for x in decl.split(None, 1)[1].split(",")]
+    assert names == [f[0] for f in H.TierDesc._fields_]
+    assert ctypes.sizeof(H.TierDesc) == 40
+
+
+@pytest.mark.parametrize("field,value", [("capacity", 0), ("n_cap", 999), ("n_cap", 998), ("reserved", 1),
+                                         ("hot_stride_n", 64), ("hot_stride_h", 12)])
+def test_tier_arguments_validate(H, field, value):
+    """Descriptor errors of the tiered entry points come back before any
+    device query or launch (n_tokens 1000 here)."""
+    lib = H.load_library()
+    d = base_desc(H)
+    t = _tier_desc(H, **{field: value})
+    rc = lib.hill_tier_apply(ctypes.byref(d), ctypes.byref(t), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 100, FAKE, 0,
+                             FAKE, None)
+    assert rc == INVALID
+    rc = lib.hill_step_tiered(ctypes.byref(d), ctypes.byref(t), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1000,
+                              8, FAKE, None, 0, 10, FAKE, FAKE, FAKE, 1 << 40, None, None)
+    assert rc == INVALID
+
+
+def test_tier_apply_checks_its_lists_and_context(H):
+    lib = H.load_library()
+    d = base_desc(H)
+    t = _tier_desc(H)
+    args = lambda list_cap=100, n_prev=0, status=FAKE: (ctypes.byref(d), ctypes.byref(t), FAKE, FAKE, FAKE, FAKE, FAKE,
+                                                        FAKE, FAKE, list_cap, FAKE, n_prev, status, None)
+    assert lib.hill_tier_apply(*args(list_cap=0)) == INVALID
+    assert lib.hill_tier_apply(*args(status=None)) == INVALID
+    assert lib.hill_tier_apply(*args(n_prev=1001)) == INVALID       # more than n_tokens
+    assert lib.hill_tier_apply(*args(n_prev=-1)) == INVALID
+    assert lib.hill_tier_apply(None, ctypes.byref(t), *args()[2:]) == INVALID
+    assert lib.hill_tier_apply(ctypes.byref(d), None, *args()[2:]) == INVALID
+    # fake pointers pass the shape checks and are then refused as memory the GPU cannot reach
+    assert lib.hill_tier_apply(*args()) == INVALID
+    assert b"reach" in lib.hill_last_error()
+    # a tiered step scores on the sketch
+    assert lib.hill_step_tiered(ctypes.byref(d), ctypes.byref(t), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 1000,
+                                8, FAKE, None, 0, 10, FAKE, FAKE, FAKE, 1 << 40, None, None) == INVALID
