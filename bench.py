@@ -35,6 +35,10 @@ Prints one JSON line:
   sketch, sketch4  the same steps scored on the int8 / int4 key sketch
                (Sec. 4.4 asymmetric precision): step time, scan roofline on
                its own bytes, selection agreement with the 16-bit path
+  tier         the tiered cache (hot pool of 2k rows in HBM, the rest in
+               pinned host memory read in place) on 4 layers: stage times
+               beside the int8 sketch leg's, the BKP pass and the row
+               migration per layer, the share of selected rows in the hot pool
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
@@ -303,6 +307,8 @@ def run_bench(args):
     if not args.no_sketch:
         res["sketch"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, 8)
         res["sketch4"] = bench_sketch(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream, 4)
+    if not args.no_tier:
+        res["tier"] = bench_tier(args, w, layers, T, qptrs, ws, stream)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle (%.0f s budget)" % args.cpu_seconds)
         res["cpu_baseline"] = cpu_baseline(W.WORKLOADS[int(args.workload)], args.cpu_seconds)
@@ -383,6 +389,87 @@ def bench_bkp(args, w, calls, nl_run, T, qptrs, stream):
         "us_per_pass_mean": round(sum(us) / len(us), 3),
         "n_recent": k, "capacity": 2 * k, "launches_per_pass": 6,
         "last_pass_promotions": last[0], "last_pass_demotions": last[1],
+    }
+
+
+def bench_tier(args, w, layers, T, qptrs, ws, stream, n_layers=4):
+    """The tiered KV cache (Sec. 4.2 BKP with the rows moved): per layer a hot
+    pool of 2k slot rows in HBM and the cold rows in pinned host memory that
+    the attention reads in place; after each layer's decode step the BKP pass
+    over its selection and the migration of the rows it names.  The step
+    scores on the int8 sketch, so its stages compare with the int8 sketch
+    leg's (all rows in HBM).  ``n_layers`` layers, one probe layer per step
+    (stage events on its step, events around its BKP pass and its
+    migration); the first 8 steps fill the pools and stay untimed."""
+    import torch
+    import paper_2602_18750_amd as H
+
+    dev = torch.device("cuda:0")
+    k = w.k_sel
+    nt = min(n_layers, len(layers))
+    caches = [H.TieredCache(layers[L][0].k, layers[L][0].v, 2 * k, bits=8, stream=stream) for L in range(nt)]
+    ss = [H.new_importance(w.batch, 1, w.n_tokens, dev) for _ in range(nt)]
+    sts = [H.new_stream_state(w.batch, 1, dev) for _ in range(nt)]
+    steps = [H.TierStepCall(layers[L][0].q[0], caches[L], ss[L], k, n_tokens=w.n_tokens, ws=ws, stream=stream,
+                            stream_state=sts[L]) for L in range(nt)]
+    bstates = [H.BkpState(w.batch, 1, w.n_tokens, dev) for _ in range(nt)]
+    bkps = [H.BkpCall(b, k, n_tokens=w.n_tokens, n_recent=k, capacity=2 * k, stream=stream) for b in bstates]
+    moves = [H.TierApplyCall(caches[L], bkps[L], n_tokens=w.n_tokens, stream=stream) for L in range(nt)]
+    fill = 8
+    n_steps = max(args.steps, nt)
+    probes = [StageProbe(H, stream) for _ in range(n_steps)]
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_steps)]
+    snap = None
+    torch.cuda.synchronize()
+    t0 = None
+    for i in range(fill + n_steps):
+        if i == fill:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        t = i % T
+        j = i - fill
+        probe = j % nt if j >= 0 else -1
+        for L in range(nt):
+            if L == probe:
+                steps[L](qptrs[L][t], probes[j].ev)
+                if j == n_steps - 1:     # the last probe step's selection and where its rows were
+                    snap = (L, steps[L].idx.clone(), caches[L].loc.clone())
+                ev[j][0].record(stream)
+                bkps[L](steps[L].idx.data_ptr())
+                ev[j][1].record(stream)
+                moves[L]()
+                ev[j][2].record(stream)
+            else:
+                steps[L](qptrs[L][t])
+                bkps[L](steps[L].idx.data_ptr())
+                moves[L]()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    st = stage_means(probes, ("scan", "update", "select", "merge"))
+    bkp_us = sorted(a.elapsed_time(b) * 1e3 for a, b, _ in ev)
+    mig_us = sorted(b.elapsed_time(c) * 1e3 for _, b, c in ev)
+    sel, loc = snap[1].long().clamp_min(0), snap[2]
+    in_hot = float((loc.gather(2, sel) >= 0).float().mean())
+    status = int(caches[0].status.item())
+    hot_rows = [int((c.loc[0, 0] >= 0).sum()) for c in caches]
+    row_bytes = 2 * w.n_kv_heads * w.head_dim * 2    # K and V of one token
+    counts = bkps[0].counts[0, 0].tolist()
+    del steps, moves, bkps, caches
+    torch.cuda.empty_cache()
+    return {
+        "layers": nt,
+        "capacity": 2 * k, "n_recent": k, "granularity": "token",
+        "layer_step_us_wall": round((t1 - t0) * 1e6 / (n_steps * nt), 3),
+        "stage_us": {kk: round(v, 3) for kk, v in st.items()},
+        "select_attn_us_per_layer_step": round(st["select"] + st["merge"], 3),
+        "bkp_pass_us_median": round(bkp_us[len(bkp_us) // 2], 3),
+        "migration_us_median": round(mig_us[len(mig_us) // 2], 3),
+        "migration_us_mean": round(sum(mig_us) / len(mig_us), 3),
+        "last_pass_promotions": counts[0], "last_pass_demotions": counts[1],
+        "moved_bytes_last_pass": (counts[0] + counts[1]) * row_bytes,
+        "hot_rows": hot_rows,
+        "selected_in_hot_pool": round(in_hot, 4),
+        "status": status,
     }
 
 
@@ -755,6 +842,7 @@ def main():
     ap.add_argument("--n-tokens", type=int, default=None, help="context length override (a variant of the workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sketch", action="store_true", help="skip the int8 / int4 sketch variants of the step")
+    ap.add_argument("--no-tier", action="store_true", help="skip the tiered-cache leg (hot pool in HBM, cold in host)")
     ap.add_argument("--no-bkp", action="store_true", help="skip timing the hot/cold pool pass")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--sweep", action="store_true")

@@ -641,6 +641,73 @@ def hill_step_tiered(q, cache: TieredCache, s, k_sel, *, n_tokens=None, mode="at
     return idx_out, out
 
 
+class TierStepCall:
+    """hill_step_tiered with its arguments marshalled once, for per-step loops
+    (only the query pointer changes); the first ``stream_reset_calls`` calls
+    are reset steps of the streamed selection when a state is given."""
+
+    def __init__(self, q, cache: TieredCache, s, k_sel, *, n_tokens=None, ws=None, stream=None, stream_state=None,
+                 stream_reset_calls=3):
+        lib = load_library()
+        _device_check(q, s, ws, stream_state)
+        n = cache.n_cap if n_tokens is None else int(n_tokens)
+        self.desc = cache.step_desc(q, s, n)
+        B, R = s.shape[0], s.shape[1]
+        self.k_sel = int(k_sel)
+        self.idx = torch.empty((B, R, self.k_sel), dtype=torch.int32, device=s.device)
+        self.out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        self.ws = ws if ws is not None else workspace(self.desc, self.k_sel, q.device)
+        P = ctypes.c_void_p
+        sk = cache.sketch
+        self._fn = lib.hill_step_tiered
+        self._resets_left = int(stream_reset_calls) if stream_state is not None else 0
+
+        def args(flags):
+            return (ctypes.byref(self.desc), ctypes.byref(cache.desc)), \
+                   (P(cache.k_hot.data_ptr()), P(cache.v_hot.data_ptr()), P(cache.k_cold.data_ptr()),
+                    P(cache.v_cold.data_ptr()), P(cache.loc.data_ptr()), P(sk.codes.data_ptr()),
+                    P(sk.exps.data_ptr()), ctypes.c_int64(sk.cap), ctypes.c_int32(sk.bits), P(s.data_ptr()),
+                    P(stream_state.data_ptr() if stream_state is not None else None), ctypes.c_uint32(flags),
+                    ctypes.c_int32(self.k_sel), P(self.idx.data_ptr()), P(self.out.data_ptr()),
+                    P(self.ws.data_ptr()), ctypes.c_size_t(self.ws.numel()), P(_stream_ptr(stream)))
+        self._pre, self._post = args(0)
+        self._post_reset = args(HILL_STREAM_RESET)[1]
+        self._keep = (cache, s, stream_state)
+
+    def __call__(self, q_ptr: int, events=None):
+        post = self._post
+        if self._resets_left > 0:
+            self._resets_left -= 1
+            post = self._post_reset
+        st = self._fn(*self._pre, ctypes.c_void_p(q_ptr), *post, None if events is None else ctypes.byref(events))
+        if st != HILL_OK:
+            _check(st)
+
+
+class TierApplyCall:
+    """hill_tier_apply marshalled once for a cache and a BkpCall's lists (the
+    context stays n_tokens from the second call on)."""
+
+    def __init__(self, cache: TieredCache, bkp: "BkpCall", *, n_tokens: int, stream=None):
+        lib = load_library()
+        q0 = torch.empty((cache.k_hot.shape[0], cache.k_hot.shape[1], cache.k_hot.shape[3]), dtype=cache.k_hot.dtype,
+                         device="meta")
+        self.desc = make_desc(q0, cache.k_cold, cache.v_cold, None, granularity=cache.granularity, n_tokens=n_tokens)
+        P = ctypes.c_void_p
+        self._fn = lib.hill_tier_apply
+        self._cache, self._n = cache, int(n_tokens)
+        self._args = (ctypes.byref(self.desc), ctypes.byref(cache.desc), P(cache.k_hot.data_ptr()),
+                      P(cache.v_hot.data_ptr()), P(cache.k_cold.data_ptr()), P(cache.v_cold.data_ptr()),
+                      P(cache.loc.data_ptr()), P(bkp.promote.data_ptr()), P(bkp.demote.data_ptr()),
+                      ctypes.c_int32(bkp.promote.shape[-1]), P(bkp.counts.data_ptr()))
+        self._post = (P(cache.status.data_ptr()), P(_stream_ptr(stream)))
+        self._keep = bkp
+
+    def __call__(self):
+        _check(self._fn(*self._args, ctypes.c_int32(self._cache.n_prev), *self._post))
+        self._cache.n_prev = self._n
+
+
 def app_balance(*, f_c, f_s, b_c, b_s, alpha=None, alpha_c=None, alpha_s=None, m=1.0, m0=0.0) -> dict:
     """Capacity split of the Adaptive Prefetch-based Pipeline (Sec. 4.3, Eqs.
     2-4), computed by the library (host only).  ``alpha`` sets both retained
