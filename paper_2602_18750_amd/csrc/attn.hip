@@ -43,10 +43,9 @@ __global__ __launch_bounds__(256) void attn_split_kernel(AttnArgs a)
 
 __global__ __launch_bounds__(kHeadDim) void attn_combine_kernel(AttnArgs a)
 {
-    __shared__ float wsl[kMaxSlots];
     __shared__ float red[kHeadDim / 64 + 1];
     __shared__ float osum[kHeadDim];
-    merge_head<kHeadDim>(a, blockIdx.x / a.Hq, blockIdx.x % a.Hq, a.nsplit, wsl, red, osum);
+    merge_head<kHeadDim>(a, blockIdx.x / a.Hq, blockIdx.x % a.Hq, 0, a.nsplit, red, osum);
 }
 
 template <int DT>

@@ -356,37 +356,41 @@ __device__ __forceinline__ void attn_finish(const AttnArgs& a, int b, int g, int
     __syncthreads();
 }
 
-// out[b,h,:] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s over the nslots
-// partials of head h (empty slots have l = 0 and weigh 0).  Thread t sums
-// output dimension t % D over every (NT/D)-th slot; its partial loads are
-// issued before the maximum is known.  The slot weights are formed once in
-// LDS (wsl holds nslots floats), and the slot groups are added in order.
-// red holds NT/64 + 1 floats, osum NT floats.  One workgroup of NT threads
-// per (b, h).
-template <int NT>
-__device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int nslots, float* wsl, float* red,
+// out[b,h,d0:d0+DS] = sum_s e^{m_s - M} o_s / sum_s e^{m_s - M} l_s over the
+// nslots partials of head h (empty slots have l = 0 and weigh 0), for one
+// slice of DS output dimensions.  Thread t takes dimension d0 + t % DS of
+// every (NT/DS)-th slot, starting at slot t / DS: it loads those slots' o and
+// (m, l) at once, and after one block-wide maximum adds both its weighted o
+// and its weighted l; the groups' sums are then added in order.  red holds
+// NT/64 + NT/DS floats, osum NT floats.  One workgroup of NT threads per
+// (b, h, slice); every slice forms the same (M, L).
+template <int NT, int DS = kHeadDim>
+__device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int d0, int nslots, float* red,
                                            float* osum)
 {
-    constexpr int NW = NT / 64, NG = NT / kHeadDim, kPre = 32;
+    static_assert(NT % DS == 0 && kHeadDim % DS == 0, "slices tile the head and the workgroup");
+    constexpr int NW = NT / 64, NG = NT / DS, kPre = NG >= 8 ? 16 : 32;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int d = tid % kHeadDim, grp = tid / kHeadDim;
+    const int d = tid % DS, grp = tid / DS;
     const int64_t bh = (int64_t)b * a.Hq + h;
     const float2* ml = a.part_ml + bh * nslots;
-    const float* po = a.part_o + bh * nslots * kHeadDim + d;
+    const float* po = a.part_o + bh * nslots * kHeadDim + d0 + d;
 
-    // the first kPre of this thread's slots: loads in flight during the reductions;
-    // slot tid's (m, l) is kept for both passes over the slots
+    // this thread's first kPre slots: o and (m, l) in flight together
     float x[kPre];
+    float2 v[kPre];
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
         const int s = grp + i * NG;
         x[i] = s < nslots ? po[(int64_t)s * kHeadDim] : 0.0f;
+        v[i] = s < nslots ? ml[s] : make_float2(-INFINITY, 0.0f);
     }
-    const float2 v0 = tid < nslots ? ml[tid] : make_float2(-INFINITY, 0.0f);
-    float mx = v0.y > 0.0f ? v0.x : -INFINITY;
-    for (int s = tid + NT; s < nslots; s += NT) {
-        const float2 v = ml[s];
-        mx = fmaxf(mx, v.y > 0.0f ? v.x : -INFINITY);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) mx = fmaxf(mx, v[i].y > 0.0f ? v[i].x : -INFINITY);
+    for (int s = grp + kPre * NG; s < nslots; s += NG) {
+        const float2 u = ml[s];
+        mx = fmaxf(mx, u.y > 0.0f ? u.x : -INFINITY);
     }
     mx = wave_max(mx);
     if (lane == 0) red[w] = mx;
@@ -394,50 +398,38 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
     mx = red[0];
 #pragma unroll
     for (int i = 1; i < NW; ++i) mx = fmaxf(mx, red[i]);
-    __syncthreads();
-    float lsum = 0.0f;
-    if (tid < nslots) {
-        const float ws = v0.y > 0.0f ? exp2f(v0.x - mx) : 0.0f;
-        wsl[tid] = ws;
-        lsum = ws * v0.y;
-    }
-    for (int s = tid + NT; s < nslots; s += NT) {
-        const float2 v = ml[s];
-        const float ws = v.y > 0.0f ? exp2f(v.x - mx) : 0.0f;
-        wsl[s] = ws;
-        lsum += ws * v.y;
-    }
-    lsum = wave_sum(lsum);
-    if (lane == 0) red[w] = lsum;
-    __syncthreads();
-    float L = 0.0f;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) L += red[i];
-    float O = 0.0f;
+    float O = 0.0f, L = 0.0f;
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
-        const int s = grp + i * NG;
-        if (s < nslots) O += wsl[s] * x[i];
+        const float ws = v[i].y > 0.0f ? exp2f(v[i].x - mx) : 0.0f;
+        O += ws * x[i];
+        L += ws * v[i].y;
     }
     for (int s0 = grp + kPre * NG; s0 < nslots; s0 += kPre * NG) {
 #pragma unroll
         for (int i = 0; i < kPre; ++i) {
             const int s = s0 + i * NG;
             x[i] = s < nslots ? po[(int64_t)s * kHeadDim] : 0.0f;
+            v[i] = s < nslots ? ml[s] : make_float2(-INFINITY, 0.0f);
         }
 #pragma unroll
         for (int i = 0; i < kPre; ++i) {
-            const int s = s0 + i * NG;
-            if (s < nslots) O += wsl[s] * x[i];
+            const float ws = v[i].y > 0.0f ? exp2f(v[i].x - mx) : 0.0f;
+            O += ws * x[i];
+            L += ws * v[i].y;
         }
     }
     osum[tid] = O;
+    if (d == 0) red[NW + grp] = L;
     __syncthreads();
     if (grp == 0) {
-        float t = osum[d];
+        float t = osum[d], l = red[NW];
 #pragma unroll
-        for (int q = 1; q < NG; ++q) t += osum[q * kHeadDim + d];
-        a.out[bh * kHeadDim + d] = t / L;
+        for (int q = 1; q < NG; ++q) {
+            t += osum[q * DS + d];
+            l += red[NW + q];
+        }
+        a.out[bh * kHeadDim + d0 + d] = t / l;
     }
 }
 

@@ -679,19 +679,25 @@ __global__ __launch_bounds__(kThreads) void topk_write_kernel(RefineArgs r, int3
     write_chunk(r, blockIdx.y, blockIdx.x, idx, val, red);
 }
 
-// hill_step's last kernel: workgroups [0, B*Hq) merge the chunk partials of one
-// query head each; the rest copy one chunk list each into the index output.
+// hill_step's last kernel: workgroups [0, B*Hq*kMergeSlices) merge the chunk
+// partials of one slice of kHeadDim / kMergeSlices output dimensions of one
+// query head each (a slice's loads are one 128-byte line per slot; more,
+// shorter workgroups finish sooner than one per head); the rest copy one
+// chunk list each into the index output.
+constexpr int kMergeSlices = 4;
+
 __global__ __launch_bounds__(kThreads) void merge_write_kernel(RefineArgs r, AttnArgs at, int32_t* idx)
 {
-    __shared__ float wsl[kMaxSlots];
-    __shared__ float red[kThreads / 64 + 1];
+    constexpr int DS = kHeadDim / kMergeSlices;
+    __shared__ float red[kThreads / 64 + kThreads / DS];
     __shared__ float osum[kThreads];
     __shared__ uint32_t ured[kThreads / 64];
-    const int nheads = at.B * at.Hq;
-    if ((int)blockIdx.x < nheads) {
-        merge_head<kThreads>(at, blockIdx.x / at.Hq, blockIdx.x % at.Hq, r.nchunks, wsl, red, osum);
+    const int nmerge = at.B * at.Hq * kMergeSlices;
+    if ((int)blockIdx.x < nmerge) {
+        const int bh = blockIdx.x / kMergeSlices, sl = blockIdx.x % kMergeSlices;
+        merge_head<kThreads, DS>(at, bh / at.Hq, bh % at.Hq, sl * DS, r.nchunks, red, osum);
     } else {
-        const int t = blockIdx.x - nheads;
+        const int t = blockIdx.x - nmerge;
         write_chunk(r, t / r.nchunks, t % r.nchunks, idx, nullptr, ured);
     }
 }
@@ -777,7 +783,7 @@ hipError_t launch_topk_emit_attn(const RefineArgs& r, const AttnArgs& at, int dt
 hipError_t launch_merge_write(const RefineArgs& r, const AttnArgs& at, int32_t* idx, int rows, hipStream_t st,
                               Stamp ts)
 {
-    const int blocks = at.B * at.Hq + rows * r.nchunks;
+    const int blocks = at.B * at.Hq * kMergeSlices + rows * r.nchunks;
     hipExtLaunchKernelGGL(merge_write_kernel, dim3(blocks), dim3(kThreads), 0, st, ts.start, ts.stop, 0, r, at, idx);
     return hipGetLastError();
 }
