@@ -39,6 +39,9 @@ Prints one JSON line:
                pinned host memory read in place) on 4 layers: stage times
                beside the int8 sketch leg's, the BKP pass and the row
                migration per layer, the share of selected rows in the hot pool
+  kernel_traffic  calibrated HBM bytes per launch of update_attn, topk_emit
+               and merge_write beside their algorithmic bytes (committed
+               counter runs; null once their sources changed)
   cpu_baseline the CPU oracle on a bounded sample of the same workload
 
 Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
@@ -47,7 +50,8 @@ Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
 ``--selection-stats`` (heavy-hitter recall of the Qwen-7B-shaped workload and
 the step-to-step selection overlap of the AR(1) workload),
 ``--summarize DIR`` (condense rocprofv3 output under DIR into text),
-``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs).
+``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs),
+``--step-counters DIR`` (the same for update_attn, topk_emit, merge_write).
 """
 from __future__ import annotations
 
@@ -301,7 +305,10 @@ def run_bench(args):
         "layer_step_us_wall": round(ms_step * 1e3 / nl, 3),
         "step_keys_gbps": round(kbytes_layer * nl / (ms_step * 1e-3) / 1e9, 1),
     }
-    res["plain"] = bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
+    if w.id == COUNTERS_WORKLOAD:
+        res["kernel_traffic"] = load_step_traffic()
+    if not args.no_plain:
+        res["plain"] = bench_plain(args, w, layers, nl, nl_run, reps, T, qptrs, ws, stream)
     if not args.no_bkp:
         res["bkp"] = bench_bkp(args, w, calls, nl_run, T, qptrs, stream)
     if not args.no_sketch:
@@ -702,9 +709,11 @@ def run_read_ceiling(args):
         torch.cuda.empty_cache()
 
 
-def _counter_rows(directory: str, counter: str, name_part: str):
+def _counter_rows(directory: str, counter: str, name_part: str, steady: bool = False):
     """Per-dispatch values of `counter` for kernels whose name contains
-    name_part (a regular expression)."""
+    name_part (a regular expression); with `steady`, only the later half of
+    the dispatches in launch order (the bench's timed steps after as many
+    warm-up steps, which hold the reset steps of every fresh S)."""
     import csv
     vals = []
     for path in sorted(glob.glob(os.path.join(directory, "**", "*counter_collection.csv"), recursive=True)):
@@ -713,10 +722,87 @@ def _counter_rows(directory: str, counter: str, name_part: str):
             for r in csv.DictReader(f):
                 if r.get("Counter_Name") != counter or not re.search(name_part, r.get("Kernel_Name", "")):
                     continue
-                key = r.get("Dispatch_Id") or r.get("Correlation_Id")
+                key = int(r.get("Dispatch_Id") or r.get("Correlation_Id"))
                 per[key] = per.get(key, 0.0) + float(r.get("Counter_Value", 0))
-            vals.extend(per.values())
+            xs = [per[k] for k in sorted(per)]
+            vals.extend(xs[len(xs) // 2:] if steady else xs)
     return vals
+
+
+STEP_SOURCES = [os.path.join(ROOT, "paper_2602_18750_amd", "csrc", f)
+                for f in ("update.hip", "topk.hip", "attn_device.h", "hill_device.h", "hill_internal.h")]
+STEP_COUNTERS_FILE = os.path.join(ROOT, "profiles", "step_kernels_counters.json")
+
+
+def step_sources_sha() -> str:
+    h = hashlib.sha256()
+    for p in STEP_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()
+
+
+def step_algorithmic_bytes(B, Hq, Hkv, D, n, k):
+    """Algorithmic bytes per launch of the streamed step's kernels after the
+    scan (token rows, ATTN weights, 16-bit V; 512-token selection chunks,
+    256-token update blocks and scan units):
+      update_attn  the logits (Hq * 4 B per token), the scan's unit partials
+                   once, S read and written (the candidate pairs, 8 B each
+                   for the few thousand tokens at or above the bound's bin,
+                   and the sparse histogram bins are left out)
+      topk_emit    the selected tokens' V rows, the G heads' logits of every
+                   chunk (at a 5-20 % budget every 128-byte line of them holds
+                   selected tokens), S, and the (m, l, o) partials written
+      merge_write  the partials, the chunk lists and the index output, the
+                   output rows."""
+    nchunks = -(-n // 512)
+    npart = (-(-n // 256) + 1) // 2 * 2
+    parts = B * Hq * nchunks * (D + 2) * 4
+    return {
+        "update_attn": B * Hq * n * 4 + B * Hq * npart * 8 + 2 * B * n * 4,
+        "topk_emit": B * k * Hkv * D * 2 + B * Hq * n * 4 + B * n * 4 + parts,
+        "merge_write": parts + 2 * B * k * 4 + B * Hq * D * 4,
+    }
+
+
+def make_step_counters(directory: str, command: str):
+    """The HBM-traffic record of the streamed step's kernels after the scan
+    (update_attn, topk_emit streamed with the scan's logits, merge_write) at
+    workload 3, from the same four --pmc runs as make_counters (steady-state
+    dispatches only), with each kernel's algorithmic bytes and the ratio."""
+    from paper_2602_18750_amd import workloads as W
+
+    def mean(xs):
+        if not xs:
+            raise SystemExit("no dispatches found under %s" % directory)
+        return sum(xs) / len(xs)
+
+    copy_bytes = 1 << 30
+    ff = copy_bytes / (mean(_counter_rows(os.path.join(directory, "calib_fetch"), "FETCH_SIZE", "bitwise_not")) * 1024.0)
+    wf = copy_bytes / (mean(_counter_rows(os.path.join(directory, "calib_write"), "WRITE_SIZE", "bitwise_not")) * 1024.0)
+    w = W.WORKLOADS[COUNTERS_WORKLOAD]
+    alg = step_algorithmic_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens, w.k_sel)
+    names = {"update_attn": r"update_attn_kernel",
+             "topk_emit": r"topk_emit_kernel<1, 4, true, true, true, false>",
+             "merge_write": r"merge_write_kernel"}
+    rec = {"workload": w.name, "source_sha256": step_sources_sha(), "fetch_factor": round(ff, 4),
+           "write_factor": round(wf, 4), "kernels": {}, "command": command}
+    for key, pat in names.items():
+        fs = _counter_rows(os.path.join(directory, "fetch"), "FETCH_SIZE", pat, steady=True)
+        ws_ = _counter_rows(os.path.join(directory, "write"), "WRITE_SIZE", pat, steady=True)
+        hbm = mean(fs) * 1024.0 * ff + mean(ws_) * 1024.0 * wf
+        rec["kernels"][key] = {"dispatches": len(fs), "fetch_kib_per_dispatch": round(mean(fs), 1),
+                               "write_kib_per_dispatch": round(mean(ws_), 1), "hbm_bytes_per_launch": int(round(hbm)),
+                               "algorithmic_bytes_per_launch": alg[key], "traffic_over_algorithmic": round(hbm / alg[key], 3)}
+    print(json.dumps(rec, indent=1))
+
+
+def load_step_traffic():
+    """The step kernels' traffic record, while their sources are unchanged."""
+    try:
+        rec = json.load(open(STEP_COUNTERS_FILE))
+        return rec["kernels"] if rec.get("source_sha256") == step_sources_sha() else None
+    except (OSError, ValueError, KeyError):
+        return None
 
 
 def make_counters(directory: str, command: str):
@@ -852,11 +938,17 @@ def main():
                     help="heavy-hitter recall (Qwen-7B-shaped) and step-to-step selection overlap (AR(1) workload)")
     ap.add_argument("--summarize", metavar="DIR")
     ap.add_argument("--counters", metavar="DIR", help="write the score_tiles traffic record from --pmc runs under DIR")
+    ap.add_argument("--step-counters", metavar="DIR",
+                    help="write the traffic record of the step's other kernels from --pmc runs under DIR")
     ap.add_argument("--counters-command", default="", help="command line recorded with --counters")
+    ap.add_argument("--no-plain", action="store_true", help="skip the hill_step (refine pass) leg")
     args = ap.parse_args()
 
     if args.counters:
         make_counters(args.counters, args.counters_command)
+        return 0
+    if args.step_counters:
+        make_step_counters(args.step_counters, args.counters_command)
         return 0
 
     if args.summarize:
