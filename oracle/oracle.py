@@ -46,6 +46,10 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "hill_oracle.c")
 _LIB_PATH = os.path.join(_HERE, "libhill_oracle.so")
+# the same source built with AddressSanitizer and UBSan (clang), for CPU test
+# runs that preload the sanitizer runtime; selected by HILL_ORACLE_LIB
+SAN_LIB_PATH = os.path.join(_HERE, "libhill_oracle_san.so")
+CLANG = os.environ.get("HILL_CLANG", "/opt/rocm/llvm/bin/clang")
 
 F16, BF16 = 0, 1
 ATTN, RAW = 0, 1
@@ -59,17 +63,23 @@ _lock = threading.Lock()
 _lib = None
 
 
-def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (-O2, OpenMP, no fast-math)."""
-    if force or not os.path.exists(_LIB_PATH) or (
-        os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC)
-    ):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
-               "-D_POSIX_C_SOURCE=200809L", "-o", tmp, _SRC, "-lm"]
+def build(force: bool = False, sanitize: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, OpenMP, no fast-math); with
+    ``sanitize``, the sanitizer variant instead: clang, -O1, AddressSanitizer
+    and UBSan with no recovery (any finding aborts), single-threaded."""
+    out = SAN_LIB_PATH if sanitize else _LIB_PATH
+    if force or not os.path.exists(out) or os.path.getmtime(out) < os.path.getmtime(_SRC):
+        tmp = out + ".tmp%d" % os.getpid()
+        if sanitize:
+            cmd = [CLANG, "-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
+                   "-fno-sanitize-recover=all", "-Wno-unknown-pragmas", "-fPIC", "-shared", "-std=c11",
+                   "-D_POSIX_C_SOURCE=200809L", "-o", tmp, _SRC, "-lm"]
+        else:
+            cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                   "-D_POSIX_C_SOURCE=200809L", "-o", tmp, _SRC, "-lm"]
         subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+        os.replace(tmp, out)
+    return out
 
 
 def _load():
@@ -77,8 +87,10 @@ def _load():
     with _lock:
         if _lib is not None:
             return _lib
-        build()
-        lib = ctypes.CDLL(_LIB_PATH)
+        path = os.environ.get("HILL_ORACLE_LIB")
+        if path is None:
+            path = build()
+        lib = ctypes.CDLL(path)
         P = ctypes.c_void_p
         I = ctypes.c_int
         I64 = ctypes.c_int64

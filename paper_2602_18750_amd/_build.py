@@ -17,6 +17,13 @@ BUILD_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libhill.so")
 # the benchmark's roofline calibration read, a library of its own (not libhill's ABI)
 CALIB_LIB = os.path.join(PKG, "libhill_calib.so")
+# the same library with its host layer (hill_api.cpp: validation, workspace
+# layouts, launch set-up) built with AddressSanitizer and UBSan, for CPU runs
+# of the error paths with the sanitizer runtime preloaded; device code as in LIB
+HOSTSAN_LIB = os.path.join(PKG, "libhill_hostsan.so")
+# host-only sanitizer flags (each behind -Xarch_host: no GPU code is instrumented)
+HOSTSAN_FLAGS = ["-O1", "-g", "-fno-omit-frame-pointer"] + [
+    x for f in ("-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=all") for x in ("-Xarch_host", f)]
 # per-kernel registers, scratch and occupancy as the compiler reports them
 RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
@@ -83,6 +90,24 @@ def _link(objs, lib, verbose):
     if r.returncode != 0:
         raise RuntimeError("link failed:\n%s" % r.stderr)
     os.replace(tmp, lib)
+
+
+def build_host_sanitized(verbose: bool = False) -> str:
+    """HOSTSAN_LIB from hill_api.cpp built with the sanitizers and the regular
+    build's device objects (run build() first)."""
+    objs = [os.path.join(BUILD_DIR, os.path.splitext(s)[0] + ".o") for s in SOURCES if s != "hill_api.cpp"]
+    missing = [o for o in objs if not os.path.exists(o)]
+    if missing:
+        raise RuntimeError("build() first: missing %s" % ", ".join(missing))
+    obj = os.path.join(BUILD_DIR, "hill_api_hostsan.o")
+    cmd = [HIPCC] + COMMON + HOSTSAN_FLAGS + ["-c", os.path.join(CSRC, "hill_api.cpp"), "-o", obj]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on hill_api.cpp (sanitized):\n%s" % r.stderr)
+    _link([obj] + objs, HOSTSAN_LIB, verbose)
+    return HOSTSAN_LIB
 
 
 def build(verbose: bool = False) -> str:
