@@ -174,7 +174,8 @@ HILL_API hill_status hill_step(const hill_desc* d, const void* q, const void* k,
  *                       normaliser of every head
  *   HILL_STAGE_UPDATE   S += the step's weights, and the selection's first
  *                       radix digit histogram (RAW per-KV-head rows: only
- *                       the histogram)
+ *                       the histogram; a streamed step with a valid bound:
+ *                       the candidate list and its class counts instead)
  *   HILL_STAGE_REFINE   the threshold's first-digit bin and the second-digit
  *                       histogram (hill_step, and reset steps of the
  *                       streamed selection)
@@ -214,9 +215,10 @@ HILL_API hill_status hill_step_profiled(const hill_desc* d, const void* q, const
  * and merged against a running threshold): hill_step with the selection's
  * refine pass replaced.  With ATTN scores S only grows from step to step, so
  * the previous step's threshold is a lower bound on this one; the update
- * lists every token whose first radix digit reaches that bound, and the
- * selection resolves the exact threshold from the first-digit histogram
- * (counted from the bound's bin upward) and that list.  Results are
+ * lists every token whose first radix digit reaches that bound, grouped by
+ * that digit (the bound's bin, the next three, or above), and the selection
+ * resolves the exact threshold from the counts of those groups, a
+ * second-digit histogram of the four bins and the list.  Results are
  * identical to hill_step.
  *
  * state: uint32 [B, R, 8], 16-byte aligned, caller-owned, one per S buffer;

@@ -16,7 +16,7 @@ constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;    // each 12-bit digit histogram also counts its top 6 bits
 constexpr int kHistRow = kHistBins + kCoarseBins;   // words per histogram row: fine, then coarse
-constexpr int kUpdChunk = 256;     // tokens per importance-update workgroup
+constexpr int kUpdChunk = 128;     // tokens per importance-update workgroup (two per lane)
 constexpr int kHistChunk = 2048;   // tokens per standalone histogram workgroup
 constexpr int kSelChunk = 512;     // tokens per selection chunk (256 threads x 2)
 

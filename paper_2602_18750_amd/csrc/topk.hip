@@ -127,6 +127,65 @@ __device__ __forceinline__ void load_digit_hist(const uint32_t* h, DigitHist& d)
     d.coarse = h[kHistBins + (threadIdx.x & 63)];
 }
 
+// Fine bins only (the update does not count the coarse bins of a second-digit
+// histogram; derive_coarse forms them).
+__device__ __forceinline__ void load_digit_fine(const uint32_t* h, DigitHist& d)
+{
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) d.fine[i] = h[i * kThreads + threadIdx.x];
+}
+
+// Coarse bin C = the sum of fine bins 64C .. 64C+63, which are register C/4 of
+// wave C%4: every wave sums its 16 registers, the sums meet in LDS (`lds`, 64
+// words) and every lane takes coarse bin `lane`.  Every thread calls it; it
+// ends with a barrier.
+__device__ __forceinline__ void derive_coarse(DigitHist& d, uint32_t* lds)
+{
+    static_assert(kHistBins / kThreads == 16 && kThreads == 256, "16 fine registers per thread");
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) {
+        const uint32_t c = wave_sum_u32(d.fine[i]);
+        if (lane == 0) lds[4 * i + w] = c;
+    }
+    __syncthreads();
+    d.coarse = lds[lane];
+}
+
+// Streamed selection: this thread's share of the class counts of the row's
+// update blocks (blocks t, t + kThreads, ...), loads issued together.
+__device__ __forceinline__ void load_class_counts(const RefineArgs& r, int row, uint32_t (&c)[kPairClasses])
+{
+    static_assert(kPairClasses == 5 && kSlotWords == 8, "four counts in one 16-byte load, one more word");
+    const int nup = (r.n + kUpdChunk - 1) / kUpdChunk;
+    const uint32_t* base = r.scount + (int64_t)row * nup * kSlotWords;
+#pragma unroll
+    for (int k = 0; k < kPairClasses; ++k) c[k] = 0u;
+    for (int u = threadIdx.x; u < nup; u += kThreads) {
+        const uint4 v = *reinterpret_cast<const uint4*>(base + (int64_t)u * kSlotWords);
+        const uint32_t v4 = base[(int64_t)u * kSlotWords + 4];
+        c[0] += v.x;
+        c[1] += v.y;
+        c[2] += v.z;
+        c[3] += v.w;
+        c[4] += v4;
+    }
+}
+
+// Block-wide sums of the class counts (every thread gets them); one barrier.
+__device__ __forceinline__ void reduce_class_counts(uint32_t (&c)[kPairClasses], uint32_t (*red)[kThreads / 64])
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int k = 0; k < kPairClasses; ++k) {
+        const uint32_t v = wave_sum_u32(c[k]);
+        if (lane == 0) red[k][w] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kPairClasses; ++k) c[k] = (red[k][0] + red[k][1]) + (red[k][2] + red[k][3]);
+}
+
 // The bin holding the need-th largest key of the row (1 <= need <= keys in
 // the row): res[0] = bin, res[1] = keys still needed from it (need minus the
 // keys in higher bins), res[2] = keys in it.  Every wave finds the coarse bin;
@@ -357,6 +416,8 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t red[kThreads / 64];
     __shared__ uint32_t res[3];
+    __shared__ typename std::conditional<STREAM, uint32_t[kPairClasses][kThreads / 64], uint32_t[1][1]>::type cls_red;
+    __shared__ typename std::conditional<STREAM, uint32_t[kCoarseBins], uint32_t[1]>::type coarse64;
     __shared__ AttnLds<ATTN ? GC : 1> sh;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -394,31 +455,32 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     bool fast = true;   // streamed: the update's pairs hold every key of the threshold's first-digit bin
     int pair_cls = kStreamBins;   // streamed: the class of the update's pairs that holds that bin
     if constexpr (STREAM) {
-        // first digit from the update's histogram (complete, or with a valid
-        // bound complete from the bound's bin upward); the second from the update's
-        // histogram of the threshold's bin when it lies in the window above the
-        // bound (the bound's own bin is loaded up front), else (and the third
-        // always) from the keys of that bin in the pair list
-        DigitHist h1, h2;
-        load_digit_hist(r.hist1 + (int64_t)row * kHistRow, h1);
-        load_digit_hist(r.hist2 + (int64_t)row * kHistRow, h2);
+        // First digit of the k-th key.  With a valid bound (the update's d0 word) it lies in
+        // the bound's bin or above: the update's class counts of the row's pairs, summed here
+        // over its blocks, give the keys in each of the window's kStreamBins bins and above
+        // it, and only a threshold above the window needs a first-digit histogram, counted
+        // here from the above-window pairs.  If fewer than k pairs are there, S did not only
+        // grow since the bound was written -- it was changed outside these calls -- and the
+        // first digit is counted over the whole row, whose keys the later walks then read
+        // directly (fast = false).  Without a bound the update counted the row's histogram.
+        // The second digit of a threshold in the window comes from the update's histogram of
+        // that bin (the bound's own bin is loaded up front), the third (and ties) from the
+        // keys of the threshold's bin in the pair list.
+        uint32_t cnt[kPairClasses];
+        load_class_counts(r, row, cnt);
+        DigitHist h2;
+        load_digit_fine(r.hist2 + (int64_t)row * kHistRow, h2);
         const uint32_t bnd = r.d0[row];
-        find_digit(h1, (uint32_t)r.k, res);
-        __syncthreads();
-        uint32_t b1 = res[0] & (kHistBins - 1), need1 = res[1], in1 = res[2];
+        reduce_class_counts(cnt, cls_red);
         const uint32_t d0 = bnd & (kHistBins - 1);
-        // With a bound the histogram holds only the keys from the bound's bin upward.  If fewer than
-        // k keys are there (the search then lands below the bound), S did not only grow since the
-        // bound was written -- it was changed outside these calls -- and the first digit is counted
-        // again over the whole row, whose keys the later walks then read directly (fast = false).
-        // Otherwise the k-th key lies in the counted bins and the result is exact as it is.
-        fast = b1 >= d0;   // block-uniform
-        if (!fast) {
+        const bool bound = bnd >> 31;   // block-uniform
+        uint32_t b1 = 0u, need1 = 0u, in1 = 0u;
+        // first digit of the k-th key among the pairs of class cls (or the whole row when !fast)
+        auto first_digit_from_pairs = [&](int cls) {
             uint32_t* h1s = hist2s;
-            __syncthreads();   // res of the search has been read
             for (int i = tid; i < kHistBins; i += kThreads) h1s[i] = 0u;
             __syncthreads();
-            for_row_pairs(r, row, false, kStreamBins, pair_offs, pair_starts, scan_scratch,
+            for_row_pairs(r, row, fast, cls, pair_offs, pair_starts, scan_scratch,
                           [h1s](uint32_t kk, uint32_t) { atomicAdd(&h1s[kk >> 20], 1u); });
             __syncthreads();
             find_bin<kThreads>(h1s, kHistBins, (uint32_t)r.k, scan_scratch, res);
@@ -426,8 +488,42 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             need1 = (uint32_t)r.k - res[1];
             in1 = h1s[b1];
             __syncthreads();   // res and the counts have been read before either is reused
+        };
+        if (!bound) {
+            DigitHist h1;
+            load_digit_hist(r.hist1 + (int64_t)row * kHistRow, h1);
+            find_digit(h1, (uint32_t)r.k, res);
+            __syncthreads();
+            b1 = res[0] & (kHistBins - 1);
+            need1 = res[1];
+            in1 = res[2];
+            __syncthreads();   // res has been read
+        } else {
+            uint32_t total = 0u;
+#pragma unroll
+            for (int k = 0; k < kPairClasses; ++k) total += cnt[k];
+            fast = total >= (uint32_t)r.k;   // block-uniform
+            if (!fast) {
+                first_digit_from_pairs(kStreamBins);
+            } else if (cnt[kStreamBins] >= (uint32_t)r.k) {
+                first_digit_from_pairs(kStreamBins);   // above the window
+            } else {
+                uint32_t above = cnt[kStreamBins];
+                int wsel = 0;
+#pragma unroll
+                for (int wd = kStreamBins - 1; wd >= 0; --wd) {
+                    if (above + cnt[wd] >= (uint32_t)r.k) {
+                        wsel = wd;
+                        break;
+                    }
+                    above += cnt[wd];
+                }
+                b1 = d0 + (uint32_t)wsel;
+                need1 = (uint32_t)r.k - above;
+                in1 = cnt[wsel];
+            }
         }
-        pair_cls = (fast && (bnd >> 31) && b1 - d0 < (uint32_t)kStreamBins) ? (int)(b1 - d0) : kStreamBins;
+        pair_cls = (fast && bound && b1 - d0 < (uint32_t)kStreamBins) ? (int)(b1 - d0) : kStreamBins;
         prefix = b1;
         need = need1;
         shift = 20;
@@ -435,10 +531,10 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         if (!all_eq) {
             uint32_t b2, need2, in2;
             const uint32_t wdx = b1 - d0;
-            if ((bnd >> 31) && fast && wdx < (uint32_t)kStreamBins) {   // block-uniform
+            if (bound && fast && wdx < (uint32_t)kStreamBins) {   // block-uniform
                 if (wdx != 0)   // the threshold left the bound's bin: that bin's counts
-                    load_digit_hist(r.hist2 + ((int64_t)wdx * at.B * r.R + row) * kHistRow, h2);   // [w][rows][bins]
-                __syncthreads();   // res of the first search has been read
+                    load_digit_fine(r.hist2 + ((int64_t)wdx * at.B * r.R + row) * kHistRow, h2);   // [w][rows][bins]
+                derive_coarse(h2, coarse64);   // ends with a barrier (res of the first search has been read)
                 find_digit(h2, need1, res);
                 __syncthreads();
                 b2 = res[0] & (kHistBins - 1);

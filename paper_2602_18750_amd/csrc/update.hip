@@ -65,26 +65,60 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
 }
 
 // First-digit histogram of the importance keys a workgroup writes (bits
-// 31..20, and the coarse bins of bits 31..26), merged sparsely.
+// 31..20), counted in LDS without returning atomics, with a bitmap of the bins
+// touched.  The flush adds the touched bins to the row's histogram one 64-bin
+// window per instruction (a wave's lanes hold consecutive bins, so a hot
+// window costs one request per cache line, not one per bin) and derives the
+// coarse bins (bits 31..26: one window each) from the same loads, flushed
+// together at the end.
 struct KeyHist {
-    uint32_t bins[kHistRow];
-    uint32_t list[2 * kUpdChunk];
-    uint32_t nlist;
+    alignas(16) uint32_t bins[kHistBins];
+    uint32_t mark[kHistBins / 32];
+    uint32_t coarse[kCoarseBins];
 };
 
 __device__ __forceinline__ void key_hist_clear(KeyHist& h)
 {
-    for (int i = threadIdx.x; i < kHistRow; i += 256) h.bins[i] = 0u;
-    if (threadIdx.x == 0) h.nlist = 0u;
+    uint4* b4 = reinterpret_cast<uint4*>(h.bins);
+    for (int i = threadIdx.x; i < kHistBins / 4; i += 256) b4[i] = make_uint4(0u, 0u, 0u, 0u);
+    if (threadIdx.x < kHistBins / 32) h.mark[threadIdx.x] = 0u;
+    if (threadIdx.x < kCoarseBins) h.coarse[threadIdx.x] = 0u;
 }
 
 __device__ __forceinline__ void count_key(KeyHist& h, uint32_t key)
 {
-    hist_add(h.bins, h.list, &h.nlist, key >> (32 - kHistBits));
-    hist_add(h.bins, h.list, &h.nlist, kHistBins + (key >> 26));
+    const uint32_t d = key >> (32 - kHistBits);
+    atomicAdd(&h.bins[d], 1u);
+    atomicOr(&h.mark[d >> 5], 1u << (d & 31));
 }
 
-constexpr int kHeadBatch = 8;   // float4 logits loads in flight per thread
+// After a barrier; every thread calls it (it ends with a barrier of its own).
+// Wave w owns windows w, w+4, ...: lane l < 32 reads bitmap word l of them
+// (window w + 4 * (l / 2), half l % 2), one ballot names the touched windows,
+// and the wave flushes only those.  Integer atomics: order-independent.
+__device__ __forceinline__ void key_hist_flush(KeyHist& h, uint32_t* ghist)
+{
+    static_assert(kHistBins == 64 * kCoarseBins, "one coarse bin per 64-bin window");
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const uint32_t mw = lane < 32 ? h.mark[2 * (w + 4 * (lane >> 1)) + (lane & 1)] : 0u;
+    uint64_t live = __ballot(mw != 0u);   // wave-uniform
+    while (live) {
+        const int i = __builtin_ctzll(live) >> 1;
+        live &= ~(3ull << (2 * i));
+        const int c = w + 4 * i;
+        const uint32_t v = h.bins[c * 64 + lane];
+        if (v) atomicAdd(ghist + c * 64 + lane, v);
+        const uint32_t tot = wave_sum_u32(v);
+        if (lane == 0) h.coarse[c] = tot;
+    }
+    __syncthreads();
+    if (threadIdx.x < kCoarseBins) {
+        const uint32_t v = h.coarse[threadIdx.x];
+        if (v) atomicAdd(ghist + kHistBins + threadIdx.x, v);
+    }
+}
+
+constexpr int kHeadBatch = 8;   // float2 logits loads in flight per thread
 
 // First-digit bound of the streamed selection for this row: the first digit
 // of the previous step's threshold, while the keys at or above that bin then
@@ -106,46 +140,54 @@ __device__ __forceinline__ uint32_t stream_bound(const UpdateArgs& a, uint4 p0, 
 // go to the block's slot of the row's (key, token) list, grouped by class --
 // the key's window bin (the bound's first-digit bin or one of the next
 // kStreamBins - 1) or, for every key above the window (and for every key when
-// there is no bound), class kStreamBins -- with the counts of the classes, so
-// that a walk for one first-digit bin reads one class only.  Keys in the
-// window also count their second digit (the threshold seldom moves further
-// in one step).
-static_assert(kStreamBins * kCoarseBins == 256, "one window coarse bin per update thread");
+// there is no bound), class kStreamBins -- with the counts of the classes.
+// The selection sums those counts over the row's blocks to find the first
+// digit of the k-th key (with a bound it lies in the window or above), and a
+// walk for one first-digit bin reads one class only.  Keys in the window also
+// count their second digit (fine bins, straight to memory: they spread over
+// the window's 4 x 4096 bins; the threshold seldom moves further in one step).
+// Two halves around the caller's barrier: stream_rank (class, rank within the
+// class in the wave, wave counts into LDS) and stream_store (the pair at its
+// slot position, the class counts).
+struct StreamRank {
+    bool cand;
+    int cls;
+    uint32_t rank;
+};
 
-__device__ __forceinline__ void stream_candidates(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                                  uint32_t (*wcnt)[4], uint32_t* coarse)
+__device__ __forceinline__ StreamRank stream_rank(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
+                                                  uint32_t (*wcnt)[4])
 {
     const uint32_t d0 = bnd & (kHistBins - 1);
     const uint32_t dig = key >> (32 - kHistBits);
-    const bool cand = j < a.n && dig >= d0;
+    StreamRank s;
+    s.cand = j < a.n && dig >= d0;
     const uint32_t wdx = dig - d0;   // window bin of the key (valid when cand)
-    const bool win = cand && (bnd >> 31) && wdx < (uint32_t)kStreamBins;
-    const int cls = win ? (int)wdx : kStreamBins;
+    const bool win = s.cand && (bnd >> 31) && wdx < (uint32_t)kStreamBins;
+    s.cls = win ? (int)wdx : kStreamBins;
     const int64_t rows = (int64_t)a.B * a.R;
-    if (win) {   // fine bins spread out: straight to memory; the few coarse bins are summed in LDS first
-        atomicAdd(&a.hist2[((int64_t)wdx * rows + row) * kHistRow + ((key >> 8) & (kHistBins - 1))], 1u);
-        atomicAdd(&coarse[wdx * kCoarseBins + ((key >> 14) & (kCoarseBins - 1))], 1u);
-    }
+    if (win) atomicAdd(&a.hist2[((int64_t)wdx * rows + row) * kHistRow + ((key >> 8) & (kHistBins - 1))], 1u);
     // rank within the class: one ballot per class, wave counts through LDS
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const uint64_t below = (1ull << lane) - 1ull;
-    uint32_t rank = 0;
+    s.rank = 0;
 #pragma unroll
     for (int k = 0; k < kPairClasses; ++k) {
-        const uint64_t m = __ballot(cand && cls == k);
-        if (cand && cls == k) rank = (uint32_t)__popcll(m & below);
+        const uint64_t m = __ballot(s.cand && s.cls == k);
+        if (s.cand && s.cls == k) s.rank = (uint32_t)__popcll(m & below);
         if (lane == 0) wcnt[k][w] = (uint32_t)__popcll(m);
     }
-    __syncthreads();   // also completes `coarse`
-    if (bnd >> 31) {
-        const int i = threadIdx.x;   // kStreamBins * kCoarseBins == 256 bins, one per thread
-        const uint32_t c = coarse[i];
-        if (c) atomicAdd(&a.hist2[((int64_t)(i / kCoarseBins) * rows + row) * kHistRow + kHistBins + i % kCoarseBins], c);
-    }
-    if (cand) {
-        uint32_t pos = rank;
-        for (int k = 0; k < cls; ++k) pos += (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
-        for (int v = 0; v < w; ++v) pos += wcnt[cls][v];
+    return s;
+}
+
+__device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
+                                             const StreamRank& s, const uint32_t (*wcnt)[4])
+{
+    const int w = threadIdx.x >> 6;
+    if (s.cand) {
+        uint32_t pos = s.rank;
+        for (int k = 0; k < s.cls; ++k) pos += (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+        for (int v = 0; v < w; ++v) pos += wcnt[s.cls][v];
         a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
     }
     const int nup = (a.n + kUpdChunk - 1) / kUpdChunk;
@@ -158,12 +200,12 @@ __device__ __forceinline__ void stream_candidates(const UpdateArgs& a, int row, 
 
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
 // stats kernel's output, or reduced here from the unit partials.  Thread t
-// works for head t / tph (tph = 256 / nh threads per head) and folds the
-// partial pairs t % tph, + tph, ... (at most kStatLoads partials); the tph
-// results of a
-// head are then folded across lanes (DPP within a wave when tph is a power of
-// two up to 64, else in order through LDS).  The partial loads
-// are issued by load_head_parts() before the logits; every thread calls
+// works for head t / tph (tph = 256 / nh threads per head) and holds the
+// partial pairs t % tph, + tph, ... (at most kStatLoads partials); the head's
+// maximum is taken first (DPP within a wave when tph is a power of two up to
+// 64, else in order through LDS), then every pair's sum is scaled to it with
+// one exp2 and the scaled sums are added the same way.  The partial loads are
+// issued by load_head_parts() before the logits; every thread calls
 // finish_head_stats(), which ends with a barrier.
 struct HeadParts {
     float2 v[kStatLoads];
@@ -189,21 +231,19 @@ __device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int 
     }
 }
 
-// (m, z) of two disjoint sets of exp2 terms merged (z relative to m).
-__device__ __forceinline__ void merge_mz(float& m, float& z, float mo, float zo)
+// max over the aligned group of tph lanes (tph a power of two, 2..64); every
+// lane of the group gets it.  Usable for sums as well (ADD).
+template <bool ADD>
+__device__ __forceinline__ float group_fold(float v, int tph)
 {
-    const float M = fmaxf(m, mo);
-    const float a = m == -INFINITY ? 0.0f : z * exp2f(m - M);
-    const float c = mo == -INFINITY ? 0.0f : zo * exp2f(mo - M);
-    m = M;
-    z = a + c;
-}
-
-template <int CTRL>
-__device__ __forceinline__ void merge_mz_dpp(float& m, float& z)
-{
-    const float mo = dpp<CTRL>(m), zo = dpp<CTRL>(z);
-    merge_mz(m, z, mo, zo);
+    auto op = [](float x, float y) { return ADD ? x + y : fmaxf(x, y); };
+    v = op(v, dpp<0xB1>(v));                         // lane ^ 1
+    if (tph >= 4) v = op(v, dpp<0x4E>(v));           // lane ^ 2
+    if (tph >= 8) v = op(v, dpp<0x141>(v));          // mirror within 8
+    if (tph >= 16) v = op(v, dpp<0x140>(v));         // mirror within 16
+    if (tph >= 32) v = op(v, __shfl_xor(v, 16, 64));
+    if (tph >= 64) v = op(v, __shfl_xor(v, 32, 64));
+    return v;
 }
 
 __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, int h0, int nh, const HeadParts& hp,
@@ -218,40 +258,53 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
     float m = -INFINITY;
 #pragma unroll
     for (int i = 0; i < kStatLoads; ++i) m = fmaxf(m, hp.v[i].x);
+    const int tph = 256 / nh;
+    const bool dpp_path = (tph & (tph - 1)) == 0 && tph >= 2 && tph <= 64;   // block-uniform
+    if (dpp_path) {
+        m = group_fold<false>(m, tph);   // every lane is active here; groups of tph lanes are aligned
+    } else {
+        red[t].x = m;
+        __syncthreads();
+        const int hh = t / tph;
+        if (hh < nh) {
+            float M = -INFINITY;
+            for (int i = 0; i < tph; ++i) M = fmaxf(M, red[hh * tph + i].x);
+            m = M;
+        }
+        __syncthreads();   // the maxima have been read
+    }
     float z = 0.0f;
 #pragma unroll
     for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2f(hp.v[i].x - m);
-    const int tph = 256 / nh;
-    if ((tph & (tph - 1)) == 0 && tph >= 2 && tph <= 64) {
-        // every lane is active here; groups of tph lanes are aligned
-        merge_mz_dpp<0xB1>(m, z);                      // lane ^ 1
-        if (tph >= 4) merge_mz_dpp<0x4E>(m, z);        // lane ^ 2
-        if (tph >= 8) merge_mz_dpp<0x141>(m, z);       // mirror within 8
-        if (tph >= 16) merge_mz_dpp<0x140>(m, z);      // mirror within 16
-        if (tph >= 32) merge_mz(m, z, __shfl_xor(m, 16, 64), __shfl_xor(z, 16, 64));
-        if (tph >= 64) merge_mz(m, z, __shfl_xor(m, 32, 64), __shfl_xor(z, 32, 64));
+    if (dpp_path) {
+        z = group_fold<true>(z, tph);
         if (t % tph == 0 && t / tph < nh) ms[t / tph] = make_float2(m, 1.0f / z);
     } else {
-        red[t] = make_float2(m, z);
+        red[t] = make_float2(m, z);   // thread hh * tph holds the maximum of head hh
         __syncthreads();
         if (t < nh) {
-            float M = -INFINITY, Z = 0.0f;
-            for (int i = 0; i < tph; ++i) merge_mz(M, Z, red[t * tph + i].x, red[t * tph + i].y);
-            ms[t] = make_float2(M, 1.0f / Z);
+            float Z = 0.0f;
+            for (int i = 0; i < tph; ++i) Z += red[t * tph + i].y;
+            ms[t] = make_float2(red[t * tph].x, 1.0f / Z);
         }
     }
     __syncthreads();
 }
 
 // S[b,r,j] += sum_{h in heads(r)} exp2(s2*l - max_h) / sum_h   (softmax weights).
-// kUpdChunk = 256 tokens per workgroup: lane l of wave w loads tokens
-// [4l, 4l+4) of heads w, w+4, ... as float4; the four wave partials are added
-// in wave order, then each thread finishes one token and counts its first
-// selection digit in an LDS histogram.  The head statistics come from the
-// stats kernel or, for short rows, from the unit partials reduced here.
+// kUpdChunk = 128 tokens per workgroup (one workgroup per CU at a 32K-token
+// row, so the opening loads and the exponentials spread over the whole chip):
+// lane l of wave w loads tokens [2l, 2l+2) of heads w, w+4, ... as float2
+// (unconditional loads, heads clamped into the row's; heads past it weigh
+// nothing); the four wave partials are added in wave order, then thread t <
+// 128 finishes token t.  The head statistics come from the stats kernel or,
+// for short rows, from the unit partials reduced here.  The first-digit
+// histogram of the new keys (LDS, then the touched windows) is counted for
+// the refine pass and for a streamed selection without a bound; with a bound
+// the selection takes the first digit from the class counts of the pairs.
 __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
 {
-    __shared__ float4 wsum[4][64];
+    __shared__ float2 wsum[4][64];
     __shared__ KeyHist kh;
     __shared__ float2 red[256];
     __shared__ float2 ms[256];
@@ -262,124 +315,111 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     const int nh = a.R == 1 ? a.Hq : a.G;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const bool do_hist = a.hist != nullptr;
     // Every load of the opening is issued before anything waits for one: the
     // softmax partials, this thread's old S, the first batch of logits and the
     // streamed selection's state (whose test runs only after the statistics).
     HeadParts hp;
     load_head_parts(a, b, h0, nh, hp);
-    const int j4 = blockIdx.x * kUpdChunk + 4 * lane;     // first of this lane's 4 tokens
-    const int jc = min(j4, (int)(a.ld - 4));              // rows are padded to ld (multiple of 4)
+    const int j2 = blockIdx.x * kUpdChunk + 2 * lane;     // first of this lane's 2 tokens
+    const int jc = min(j2, (int)(a.ld - 2));              // rows are padded to ld (multiple of 4)
     const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
-    const int j = blockIdx.x * kUpdChunk + tid;
+    // thread tid < kUpdChunk finishes token j; the others hold no token
+    const int j = tid < kUpdChunk ? blockIdx.x * kUpdChunk + tid : a.n;
     float* srow = a.s + (int64_t)b * a.s_sb + (int64_t)r * a.s_sr;
     const float s_ld = srow[min(j, a.n - 1)];             // unconditional: no branch around the load
-    float4 x[kHeadBatch];
+    float2 x[kHeadBatch];
 #pragma unroll
-    for (int i = 0; i < kHeadBatch; ++i) {
-        const int h = w + 4 * i;
-        x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
+    for (int i = 0; i < kHeadBatch; ++i)
+        x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(w + 4 * i, nh - 1) * a.ld);
     uint4 p0 = make_uint4(0u, 0u, 0u, 0u), p1 = p0;
     if (a.prev) {
         p0 = a.prev[2 * row];
         p1 = a.prev[2 * row + 1];
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (do_hist) key_hist_clear(kh);
+    if (a.hist) key_hist_clear(kh);
     finish_head_stats(a, b, h0, nh, hp, red, ms);
     const float s_old = j < a.n ? s_ld : 0.0f;
     const uint32_t bnd = a.prev ? stream_bound(a, p0, p1) : 0u;
-    const uint32_t hist_lo = (bnd >> 31) ? (bnd & (kHistBins - 1)) : 0u;
-    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    const bool do_hist = a.hist != nullptr && !(bnd >> 31);   // block-uniform
+    float2 acc = make_float2(0.0f, 0.0f);
     for (int hb = w;;) {
+        float2 st[kHeadBatch];   // every statistics read of the batch before the first use
+#pragma unroll
+        for (int i = 0; i < kHeadBatch; ++i) st[i] = ms[min(hb + 4 * i, nh - 1)];
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
-            const int h = hb + 4 * i;
-            if (h < nh) {
-                const float2 st = ms[h];
-                acc.x += exp2f(a.s2 * x[i].x - st.x) * st.y;
-                acc.y += exp2f(a.s2 * x[i].y - st.x) * st.y;
-                acc.z += exp2f(a.s2 * x[i].z - st.x) * st.y;
-                acc.w += exp2f(a.s2 * x[i].w - st.x) * st.y;
-            }
+            const float e0 = exp2f(a.s2 * x[i].x - st[i].x) * st[i].y;
+            const float e1 = exp2f(a.s2 * x[i].y - st[i].x) * st[i].y;
+            const bool live = hb + 4 * i < nh;   // wave-uniform
+            acc.x += live ? e0 : 0.0f;
+            acc.y += live ? e1 : 0.0f;
         }
         hb += 4 * kHeadBatch;
         if (hb >= nh) break;
 #pragma unroll
-        for (int i = 0; i < kHeadBatch; ++i) {
-            const int h = hb + 4 * i;
-            x[i] = h < nh ? *reinterpret_cast<const float4*>(lg + (int64_t)h * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
-        }
+        for (int i = 0; i < kHeadBatch; ++i)
+            x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(hb + 4 * i, nh - 1) * a.ld);
     }
-    // streamed selection: the window's coarse bins reuse red[] (its last reader,
-    // finish_head_stats, ended with a barrier); the barrier below orders the clear
-    uint32_t* sc_coarse = reinterpret_cast<uint32_t*>(red);
-    static_assert(sizeof(red) >= kStreamBins * kCoarseBins * sizeof(uint32_t), "coarse window fits in red[]");
-    if (a.prev) sc_coarse[tid] = 0u;
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
     uint32_t key = 0u;
     if (j < a.n) {
-        const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
+        const float tot = ((ws[tid] + ws[128 + tid]) + ws[256 + tid]) + ws[384 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
         key = select_key(s_new, j, a.pin_lo, a.pin_hi);
-        // with a streamed bound the k-th key lies in the bound's first-digit bin
-        // or above, so only those bins are counted (most keys lie below it)
-        if (do_hist && (key >> (32 - kHistBits)) >= hist_lo) count_key(kh, key);
+        if (do_hist) count_key(kh, key);
     }
-    if (do_hist) {
-        __syncthreads();
-        hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)row * kHistRow);
-    }
-    if (a.prev) stream_candidates(a, row, j, key, bnd, sc_wcnt, sc_coarse);   // block-uniform
+    StreamRank sr{};
+    if (a.prev) sr = stream_rank(a, row, j, key, bnd, sc_wcnt);   // block-uniform
+    __syncthreads();
+    if (do_hist) key_hist_flush(kh, a.hist + (int64_t)row * kHistRow);
+    if (a.prev) stream_store(a, row, j, key, bnd, sr, sc_wcnt);
 }
 
 // Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j] (same layout).
 __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
 {
-    __shared__ float4 wsum[4][64];
+    __shared__ float2 wsum[4][64];
     __shared__ KeyHist kh;
     const int b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
     if (do_hist) key_hist_clear(kh);
-    const int j4 = blockIdx.x * kUpdChunk + 4 * lane;
-    const int jc = min(j4, (int)(a.ld - 4));
+    const int j2 = blockIdx.x * kUpdChunk + 2 * lane;
+    const int jc = min(j2, (int)(a.ld - 2));
     const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
-    const int j = blockIdx.x * kUpdChunk + tid;
+    const int j = tid < kUpdChunk ? blockIdx.x * kUpdChunk + tid : a.n;
     float* srow = a.s + (int64_t)b * a.s_sb;
     const float s_old = j < a.n ? srow[j] : 0.0f;
-    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    float2 acc = make_float2(0.0f, 0.0f);
     for (int gb = w; gb < a.Hkv; gb += 4 * kHeadBatch) {
-        float4 x[kHeadBatch];
+        float2 x[kHeadBatch];
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
             const int g = gb + 4 * i;
-            x[i] = g < a.Hkv ? *reinterpret_cast<const float4*>(gs + (int64_t)g * a.ld) : make_float4(0.f, 0.f, 0.f, 0.f);
+            x[i] = g < a.Hkv ? *reinterpret_cast<const float2*>(gs + (int64_t)g * a.ld) : make_float2(0.f, 0.f);
         }
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
             acc.x += x[i].x;
             acc.y += x[i].y;
-            acc.z += x[i].z;
-            acc.w += x[i].w;
         }
     }
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
     if (j < a.n) {
-        const float tot = ((ws[tid] + ws[256 + tid]) + ws[512 + tid]) + ws[768 + tid];
+        const float tot = ((ws[tid] + ws[128 + tid]) + ws[256 + tid]) + ws[384 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
         if (do_hist) count_key(kh, select_key(s_new, j, a.pin_lo, a.pin_hi));
     }
     if (do_hist) {
         __syncthreads();
-        hist_flush(kh.bins, kh.list, kh.nlist, a.hist + (int64_t)b * kHistRow);
+        key_hist_flush(kh, a.hist + (int64_t)b * kHistRow);
     }
 }
 
