@@ -45,7 +45,7 @@ struct Shape {
 //   zeroed   hist1 [rows,4096+64] | hist2 [rows,4096+64] (u32 fine + coarse bins) | hist2x [3,rows,4096+64] (the
 //            streamed selection's further second-digit windows, hist2 continued) -- cleared by the first kernel of
 //            every call that accumulates into them
-//   scount [rows,ceil(n/256),8] u32 | spairs [rows,n] uint2 (key, token) | sd0 [rows] u32 (streamed selection only)
+//   scount [rows,ceil(n/kUpdChunk),8] u32 | spairs [rows,n] uint2 (key, token) (streamed selection only)
 //   cand_key [rows,n] u32 | cand_n [rows,nchunks] u32 | state [rows] uint4
 //   sel_list [rows,n] i32 | sel_n [rows,nchunks] u32
 //   slots: attention partials [B,Hq,nslots,D] fp32 and [B,Hq,nslots] float2, nslots =
@@ -56,7 +56,7 @@ struct Layout {
     size_t zero, hist1, hist2, hist2x;
     int64_t zero_words, zero_words_stream;   // the streamed selection also clears hist2x
     size_t cand_key, cand_n, state, sel_list, sel_n;
-    size_t scount, spairs, sd0;   // streamed selection: pair counts (zeroed), pairs, first-digit bounds
+    size_t scount, spairs;   // streamed selection: pair counts and bound per update block, pairs
     size_t slot_o, slot_ml;
     size_t end_score, end_topk, end_all;
     int nchunks, nsplit, per_split, nslots;
@@ -92,8 +92,6 @@ Layout layout_for(const Shape& s, int ksel)
     if (attn) off += align256(rows * (size_t)((s.n + kUpdChunk - 1) / kUpdChunk) * kSlotWords * sizeof(uint32_t));
     L.spairs = off;
     if (attn) off += align256(rows * (size_t)s.n * sizeof(uint2));
-    L.sd0 = off;
-    if (attn) off += align256(rows * sizeof(uint32_t));
     L.nchunks = (s.n + kSelChunk - 1) / kSelChunk;
     L.cand_key = off;
     off += align256(rows * (size_t)s.n * sizeof(uint32_t));
@@ -327,7 +325,6 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         u.prev = stream_prev;
         u.spairs = at<uint2>(ws, L.spairs);
         u.scount = at<uint32_t>(ws, L.scount);
-        u.d0 = at<uint32_t>(ws, L.sd0);
         u.hist2 = at<uint32_t>(ws, L.hist2);
         u.k = ksel;
     }
@@ -382,7 +379,6 @@ RefineArgs refine_args(const hill_desc* d, const Shape& s, const Layout& L, cons
     r.pin_hi = s.pin_hi;
     r.spairs = at<uint2>(ws, L.spairs);
     r.scount = at<uint32_t>(ws, L.scount);
-    r.d0 = at<uint32_t>(ws, L.sd0);
     return r;
 }
 

@@ -76,8 +76,8 @@ struct UpdateArgs {
     const uint4* prev;       // [B*R, 2] caller's state (see StreamState)
     uint2* spairs;           // [B*R, n] (key, token) of every token whose first digit >= the bound's:
                              //   update block u's at u * kUpdChunk
-    uint32_t* scount;        // [B*R, nup, kSlotWords] pairs of each update block per class (nup = ceil(n / kUpdChunk))
-    uint32_t* d0;            // [B*R] the bound's first digit | 0x80000000 if the bound held
+    uint32_t* scount;        // [B*R, nup, kSlotWords] per update block: pairs per class, then the bound
+                             //   (nup = ceil(n / kUpdChunk); see kSlotWords)
     uint32_t* hist2;         // [kStreamBins, B*R, kHistRow] second-digit counts of the keys in first-digit
                              //   bin d0 + w (w = 0: the selection's usual second-digit histogram)
     int k;                   // this step's budget
@@ -156,8 +156,7 @@ struct RefineArgs {
     int pin_lo, pin_hi;      // tokens outside [pin_lo, pin_hi) are always selected (lo == hi: all)
     // streamed selection: the update's candidate pairs replace the refine pass
     const uint2* spairs;     // [rows, n] update block u's pairs at u * kUpdChunk
-    const uint32_t* scount;  // [rows, nup, kSlotWords] pairs of each update block per class
-    const uint32_t* d0;      // [rows] the bound's first digit | 0x80000000 if the bound held
+    const uint32_t* scount;  // [rows, nup, kSlotWords] per update block: pairs per class, then the bound
     // hist2 continues as [kStreamBins, rows, kHistRow]: second digits of first-digit bins d0 + w
     uint4* state_out;        // [rows, 2] this step's threshold bound, for the next step (streamed
                              // selection; a reset step writes it from the refine pass), or NULL
@@ -191,11 +190,15 @@ inline int emit_kv_per_wg(int B, int Hkv, int nchunks, int R)
     return h;
 }
 // Streamed selection: the pairs of an update block are grouped in kPairClasses
-// classes (the kStreamBins window bins, then every key above the window); the
-// block's class counts take kSlotWords words.
+// classes (the kStreamBins window bins, then every key above the window).  The
+// block's slot of kSlotWords words holds the class counts (words 0-4) and the
+// bound the update used (word 5: the previous threshold's first digit |
+// 0x80000000 if the bound held, else 0; the same in every block of a row), so
+// that the selection reads both with one pair of 16-byte loads.
 constexpr int kPairClasses = kStreamBins + 1;
 constexpr int kSlotWords = 8;
-static_assert(kPairClasses <= kSlotWords, "class counts fit a slot");
+constexpr int kSlotBound = 5;
+static_assert(kPairClasses == kSlotBound && kSlotBound < kSlotWords, "class counts, then the bound");
 constexpr int kMaxSlots = 4096;   // partial slots merged per head (splits or chunks)
 
 // Optional start/stop timestamps of one launch (hipExtLaunchKernel events).

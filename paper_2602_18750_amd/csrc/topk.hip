@@ -127,48 +127,95 @@ __device__ __forceinline__ void load_digit_hist(const uint32_t* h, DigitHist& d)
     d.coarse = h[kHistBins + (threadIdx.x & 63)];
 }
 
-// Fine bins only (the update does not count the coarse bins of a second-digit
-// histogram; derive_coarse forms them).
-__device__ __forceinline__ void load_digit_fine(const uint32_t* h, DigitHist& d)
+// A 12-bit digit histogram row held in registers from the top: thread t holds
+// bins [4096 - 16(t+1), 4096 - 16t) (four 16-byte loads), so the bin of the
+// need-th largest key is found with one block scan of the threads' totals and
+// a walk of one thread's 16 registers -- no coarse bins needed.
+struct DigitBins {
+    uint32_t v[kHistBins / kThreads];   // v[i] = bin base + i, base = 4096 - 16(t+1)
+};
+
+__device__ __forceinline__ void load_digit_bins(const uint32_t* h, DigitBins& d)
 {
+    static_assert(kHistBins / kThreads == 16, "16 bins per thread");
+    const uint4* p = reinterpret_cast<const uint4*>(h + kHistBins - 16 * ((int)threadIdx.x + 1));
 #pragma unroll
-    for (int i = 0; i < kHistBins / kThreads; ++i) d.fine[i] = h[i * kThreads + threadIdx.x];
+    for (int q = 0; q < 4; ++q) {
+        const uint4 x = p[q];
+        d.v[4 * q] = x.x;
+        d.v[4 * q + 1] = x.y;
+        d.v[4 * q + 2] = x.z;
+        d.v[4 * q + 3] = x.w;
+    }
 }
 
-// Coarse bin C = the sum of fine bins 64C .. 64C+63, which are register C/4 of
-// wave C%4: every wave sums its 16 registers, the sums meet in LDS (`lds`, 64
-// words) and every lane takes coarse bin `lane`.  Every thread calls it; it
-// ends with a barrier.
-__device__ __forceinline__ void derive_coarse(DigitHist& d, uint32_t* lds)
+// res[0] = the bin holding the need-th largest key (1 <= need <= keys in the
+// row), res[1] = keys still needed from it, res[2] = keys in it (all 0 if the
+// row holds fewer than need keys).  Every thread calls it; the caller reads
+// res after a barrier, and `scratch` (4 words) is not rewritten before it.
+__device__ __forceinline__ void find_digit_bins(const DigitBins& d, uint32_t need, uint32_t* scratch, uint32_t* res)
 {
-    static_assert(kHistBins / kThreads == 16 && kThreads == 256, "16 fine registers per thread");
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-#pragma unroll
-    for (int i = 0; i < kHistBins / kThreads; ++i) {
-        const uint32_t c = wave_sum_u32(d.fine[i]);
-        if (lane == 0) lds[4 * i + w] = c;
+    if (threadIdx.x == 0) {   // defined result even if the counts were inconsistent
+        res[0] = 0u;
+        res[1] = 0u;
+        res[2] = 0u;
     }
-    __syncthreads();
-    d.coarse = lds[lane];
+    uint32_t local = 0u;
+#pragma unroll
+    for (int i = 0; i < kHistBins / kThreads; ++i) local += d.v[i];
+    uint32_t total;
+    const uint32_t before = block_excl_scan_1b(local, scratch, &total);   // keys in the bins above this thread's
+    if (before < need && before + local >= need) {
+        const uint32_t base = (uint32_t)(kHistBins - 16 * ((int)threadIdx.x + 1));
+        uint32_t c = before, bin = base, left = 0u, in = 0u;
+        bool found = false;
+#pragma unroll
+        for (int i = kHistBins / kThreads - 1; i >= 0; --i) {   // from the top bin of the range
+            const bool hit = !found && c + d.v[i] >= need;
+            bin = hit ? base + (uint32_t)i : bin;
+            left = hit ? need - c : left;
+            in = hit ? d.v[i] : in;
+            found = found || hit;
+            c += d.v[i];
+        }
+        res[0] = bin;
+        res[1] = left;
+        res[2] = in;
+    }
 }
 
 // Streamed selection: this thread's share of the class counts of the row's
-// update blocks (blocks t, t + kThreads, ...), loads issued together.
-__device__ __forceinline__ void load_class_counts(const RefineArgs& r, int row, uint32_t (&c)[kPairClasses])
+// update blocks, and the bound they were listed against.  The first slot
+// (block t, clamped) is one pair of unconditional 16-byte loads issued with the
+// kernel's other opening loads; blocks t + kThreads, ... (rows longer than
+// kThreads update blocks) are added by add_class_counts after those.
+__device__ __forceinline__ uint32_t load_class_counts(const RefineArgs& r, int row, uint32_t (&c)[kPairClasses])
 {
-    static_assert(kPairClasses == 5 && kSlotWords == 8, "four counts in one 16-byte load, one more word");
+    static_assert(kPairClasses == 5 && kSlotWords == 8 && kSlotBound == 5, "counts 0-3, then count 4 and the bound");
+    const int nup = (r.n + kUpdChunk - 1) / kUpdChunk;
+    const uint4* slot = reinterpret_cast<const uint4*>(r.scount + ((int64_t)row * nup + min((int)threadIdx.x, nup - 1)) *
+                                                                       kSlotWords);
+    const uint4 lo = slot[0], hi = slot[1];
+    const bool ok = (int)threadIdx.x < nup;
+    c[0] = ok ? lo.x : 0u;
+    c[1] = ok ? lo.y : 0u;
+    c[2] = ok ? lo.z : 0u;
+    c[3] = ok ? lo.w : 0u;
+    c[4] = ok ? hi.x : 0u;
+    return hi.y;   // every block of the row wrote the same bound
+}
+
+__device__ __forceinline__ void add_class_counts(const RefineArgs& r, int row, uint32_t (&c)[kPairClasses])
+{
     const int nup = (r.n + kUpdChunk - 1) / kUpdChunk;
     const uint32_t* base = r.scount + (int64_t)row * nup * kSlotWords;
-#pragma unroll
-    for (int k = 0; k < kPairClasses; ++k) c[k] = 0u;
-    for (int u = threadIdx.x; u < nup; u += kThreads) {
+    for (int u = threadIdx.x + kThreads; u < nup; u += kThreads) {
         const uint4 v = *reinterpret_cast<const uint4*>(base + (int64_t)u * kSlotWords);
-        const uint32_t v4 = base[(int64_t)u * kSlotWords + 4];
         c[0] += v.x;
         c[1] += v.y;
         c[2] += v.z;
         c[3] += v.w;
-        c[4] += v4;
+        c[4] += base[(int64_t)u * kSlotWords + 4];
     }
 }
 
@@ -417,7 +464,6 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     __shared__ uint32_t red[kThreads / 64];
     __shared__ uint32_t res[3];
     __shared__ typename std::conditional<STREAM, uint32_t[kPairClasses][kThreads / 64], uint32_t[1][1]>::type cls_red;
-    __shared__ typename std::conditional<STREAM, uint32_t[kCoarseBins], uint32_t[1]>::type coarse64;
     __shared__ AttnLds<ATTN ? GC : 1> sh;
 
     const int tid = threadIdx.x, lane = tid & 63;
@@ -455,7 +501,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     bool fast = true;   // streamed: the update's pairs hold every key of the threshold's first-digit bin
     int pair_cls = kStreamBins;   // streamed: the class of the update's pairs that holds that bin
     if constexpr (STREAM) {
-        // First digit of the k-th key.  With a valid bound (the update's d0 word) it lies in
+        // First digit of the k-th key.  With a valid bound (the one the update used) it lies in
         // the bound's bin or above: the update's class counts of the row's pairs, summed here
         // over its blocks, give the keys in each of the window's kStreamBins bins and above
         // it, and only a threshold above the window needs a first-digit histogram, counted
@@ -467,10 +513,13 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         // that bin (the bound's own bin is loaded up front), the third (and ties) from the
         // keys of the threshold's bin in the pair list.
         uint32_t cnt[kPairClasses];
-        load_class_counts(r, row, cnt);
-        DigitHist h2;
-        load_digit_fine(r.hist2 + (int64_t)row * kHistRow, h2);
-        const uint32_t bnd = r.d0[row];
+        const uint32_t bnd = load_class_counts(r, row, cnt);
+        // the threshold mostly stays in the bound's bin or moves one bin up: both bins' counts
+        // are loaded with the opening loads
+        DigitBins h2, h2n;
+        load_digit_bins(r.hist2 + (int64_t)row * kHistRow, h2);
+        load_digit_bins(r.hist2 + ((int64_t)at.B * r.R + row) * kHistRow, h2n);   // [w][rows][bins]
+        add_class_counts(r, row, cnt);
         reduce_class_counts(cnt, cls_red);
         const uint32_t d0 = bnd & (kHistBins - 1);
         const bool bound = bnd >> 31;   // block-uniform
@@ -490,9 +539,9 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             __syncthreads();   // res and the counts have been read before either is reused
         };
         if (!bound) {
-            DigitHist h1;
-            load_digit_hist(r.hist1 + (int64_t)row * kHistRow, h1);
-            find_digit(h1, (uint32_t)r.k, res);
+            DigitBins h1;
+            load_digit_bins(r.hist1 + (int64_t)row * kHistRow, h1);
+            find_digit_bins(h1, (uint32_t)r.k, scan_scratch, res);
             __syncthreads();
             b1 = res[0] & (kHistBins - 1);
             need1 = res[1];
@@ -532,10 +581,13 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             uint32_t b2, need2, in2;
             const uint32_t wdx = b1 - d0;
             if (bound && fast && wdx < (uint32_t)kStreamBins) {   // block-uniform
-                if (wdx != 0)   // the threshold left the bound's bin: that bin's counts
-                    load_digit_fine(r.hist2 + ((int64_t)wdx * at.B * r.R + row) * kHistRow, h2);   // [w][rows][bins]
-                derive_coarse(h2, coarse64);   // ends with a barrier (res of the first search has been read)
-                find_digit(h2, need1, res);
+                if (wdx == 1) {
+#pragma unroll
+                    for (int i = 0; i < kHistBins / kThreads; ++i) h2.v[i] = h2n.v[i];
+                } else if (wdx > 1) {   // the threshold moved further: that bin's counts
+                    load_digit_bins(r.hist2 + ((int64_t)wdx * at.B * r.R + row) * kHistRow, h2);
+                }
+                find_digit_bins(h2, need1, scan_scratch, res);
                 __syncthreads();
                 b2 = res[0] & (kHistBins - 1);
                 need2 = res[1];

@@ -191,11 +191,15 @@ __device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j
         a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
     }
     const int nup = (a.n + kUpdChunk - 1) / kUpdChunk;
-    if (threadIdx.x < kPairClasses) {
-        const int k = threadIdx.x;
-        a.scount[((int64_t)row * nup + blockIdx.x) * kSlotWords + k] = (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+    if (threadIdx.x == 0) {
+        uint32_t c[kPairClasses];
+#pragma unroll
+        for (int k = 0; k < kPairClasses; ++k) c[k] = (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+        uint4* slot = reinterpret_cast<uint4*>(a.scount + ((int64_t)row * nup + blockIdx.x) * kSlotWords);
+        static_assert(kSlotWords == 8 && kPairClasses == 5, "two 16-byte words per slot");
+        slot[0] = make_uint4(c[0], c[1], c[2], c[3]);
+        slot[1] = make_uint4(c[4], bnd, 0u, 0u);
     }
-    if (threadIdx.x == 0 && blockIdx.x == 0) a.d0[row] = bnd;
 }
 
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
