@@ -11,7 +11,8 @@ constexpr int kHeadDim = 128;      // D supported by every kernel
 constexpr int kScoreTile = 32;     // tokens per scoring wave-tile
 constexpr int kUnitTiles = 8;      // wave-tiles per scoring workgroup unit (softmax partial granularity)
 constexpr int kMaxGroup = 128;     // query heads per KV head supported
-constexpr int kStatLoads = 16;     // softmax partials per thread when the update reduces them itself
+constexpr int kUpdThreads = 512;   // threads per importance-update workgroup (two waves per SIMD)
+constexpr int kStatLoads = 8;      // softmax partials per thread when the update reduces them itself
 constexpr int kHistBits = 12;      // first radix digit of the selection keys
 constexpr int kHistBins = 1 << kHistBits;
 constexpr int kCoarseBins = 64;    // each 12-bit digit histogram also counts its top 6 bits
@@ -251,7 +252,7 @@ hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int n
 inline bool update_reduces_stats(int nheads_per_row, int npart)
 {
     if (nheads_per_row < 1 || nheads_per_row > 256) return false;
-    const int tph = 256 / nheads_per_row;
+    const int tph = kUpdThreads / nheads_per_row;
     return (int64_t)npart <= (int64_t)kStatLoads * tph;
 }
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {});

@@ -70,17 +70,18 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
 // window per instruction (a wave's lanes hold consecutive bins, so a hot
 // window costs one request per cache line, not one per bin) and derives the
 // coarse bins (bits 31..26: one window each) from the same loads, flushed
-// together at the end.
+// together at the end.  NT: threads of the workgroup (256 or 512).
 struct KeyHist {
     alignas(16) uint32_t bins[kHistBins];
     uint32_t mark[kHistBins / 32];
     uint32_t coarse[kCoarseBins];
 };
 
+template <int NT>
 __device__ __forceinline__ void key_hist_clear(KeyHist& h)
 {
     uint4* b4 = reinterpret_cast<uint4*>(h.bins);
-    for (int i = threadIdx.x; i < kHistBins / 4; i += 256) b4[i] = make_uint4(0u, 0u, 0u, 0u);
+    for (int i = threadIdx.x; i < kHistBins / 4; i += NT) b4[i] = make_uint4(0u, 0u, 0u, 0u);
     if (threadIdx.x < kHistBins / 32) h.mark[threadIdx.x] = 0u;
     if (threadIdx.x < kCoarseBins) h.coarse[threadIdx.x] = 0u;
 }
@@ -93,19 +94,22 @@ __device__ __forceinline__ void count_key(KeyHist& h, uint32_t key)
 }
 
 // After a barrier; every thread calls it (it ends with a barrier of its own).
-// Wave w owns windows w, w+4, ...: lane l < 32 reads bitmap word l of them
-// (window w + 4 * (l / 2), half l % 2), one ballot names the touched windows,
-// and the wave flushes only those.  Integer atomics: order-independent.
+// Wave w of the NW = NT/64 waves owns windows w, w+NW, ...: lane l < 2*64/NW
+// reads bitmap word l of them (window w + NW * (l / 2), half l % 2), one
+// ballot names the touched windows, and the wave flushes only those.
+// Integer atomics: order-independent.
+template <int NT>
 __device__ __forceinline__ void key_hist_flush(KeyHist& h, uint32_t* ghist)
 {
     static_assert(kHistBins == 64 * kCoarseBins, "one coarse bin per 64-bin window");
+    constexpr int NW = NT / 64, kWords = 2 * kCoarseBins / NW;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const uint32_t mw = lane < 32 ? h.mark[2 * (w + 4 * (lane >> 1)) + (lane & 1)] : 0u;
+    const uint32_t mw = lane < kWords ? h.mark[2 * (w + NW * (lane >> 1)) + (lane & 1)] : 0u;
     uint64_t live = __ballot(mw != 0u);   // wave-uniform
     while (live) {
         const int i = __builtin_ctzll(live) >> 1;
         live &= ~(3ull << (2 * i));
-        const int c = w + 4 * i;
+        const int c = w + NW * i;
         const uint32_t v = h.bins[c * 64 + lane];
         if (v) atomicAdd(ghist + c * 64 + lane, v);
         const uint32_t tot = wave_sum_u32(v);
@@ -118,7 +122,9 @@ __device__ __forceinline__ void key_hist_flush(KeyHist& h, uint32_t* ghist)
     }
 }
 
-constexpr int kHeadBatch = 8;   // float2 logits loads in flight per thread
+constexpr int kHeadBatch = 4;   // float2 logits loads in flight per thread (update_attn)
+constexpr int kRawBatch = 8;    // float2 group-sum loads in flight per thread (update_raw_groups)
+constexpr int kUpdWaves = kUpdThreads / 64;
 
 // First-digit bound of the streamed selection for this row: the first digit
 // of the previous step's threshold, while the keys at or above that bin then
@@ -156,7 +162,7 @@ struct StreamRank {
 };
 
 __device__ __forceinline__ StreamRank stream_rank(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                                  uint32_t (*wcnt)[4])
+                                                  uint32_t (*wcnt)[kUpdWaves])
 {
     const uint32_t d0 = bnd & (kHistBins - 1);
     const uint32_t dig = key >> (32 - kHistBits);
@@ -180,13 +186,21 @@ __device__ __forceinline__ StreamRank stream_rank(const UpdateArgs& a, int row, 
     return s;
 }
 
+__device__ __forceinline__ uint32_t class_total(const uint32_t (*wcnt)[kUpdWaves], int k)
+{
+    uint32_t t = 0u;
+#pragma unroll
+    for (int v = 0; v < kUpdWaves; ++v) t += wcnt[k][v];
+    return t;
+}
+
 __device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                             const StreamRank& s, const uint32_t (*wcnt)[4])
+                                             const StreamRank& s, const uint32_t (*wcnt)[kUpdWaves])
 {
     const int w = threadIdx.x >> 6;
     if (s.cand) {
         uint32_t pos = s.rank;
-        for (int k = 0; k < s.cls; ++k) pos += (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+        for (int k = 0; k < s.cls; ++k) pos += class_total(wcnt, k);
         for (int v = 0; v < w; ++v) pos += wcnt[s.cls][v];
         a.spairs[(int64_t)row * a.n + (int64_t)blockIdx.x * kUpdChunk + pos] = make_uint2(key, (uint32_t)j);
     }
@@ -194,7 +208,7 @@ __device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j
     if (threadIdx.x == 0) {
         uint32_t c[kPairClasses];
 #pragma unroll
-        for (int k = 0; k < kPairClasses; ++k) c[k] = (wcnt[k][0] + wcnt[k][1]) + (wcnt[k][2] + wcnt[k][3]);
+        for (int k = 0; k < kPairClasses; ++k) c[k] = class_total(wcnt, k);
         uint4* slot = reinterpret_cast<uint4*>(a.scount + ((int64_t)row * nup + blockIdx.x) * kSlotWords);
         static_assert(kSlotWords == 8 && kPairClasses == 5, "two 16-byte words per slot");
         slot[0] = make_uint4(c[0], c[1], c[2], c[3]);
@@ -204,20 +218,20 @@ __device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j
 
 // (max, 1/sum) of heads h0 .. h0+nh of sequence b into ms[]: copied from the
 // stats kernel's output, or reduced here from the unit partials.  Thread t
-// works for head t / tph (tph = 256 / nh threads per head) and holds the
-// partial pairs t % tph, + tph, ... (at most kStatLoads partials); the head's
-// maximum is taken first (DPP within a wave when tph is a power of two up to
-// 64, else in order through LDS), then every pair's sum is scaled to it with
-// one exp2 and the scaled sums are added the same way.  The partial loads are
-// issued by load_head_parts() before the logits; every thread calls
-// finish_head_stats(), which ends with a barrier.
+// works for head t / tph (tph = kUpdThreads / nh threads per head) and holds
+// the partial pairs t % tph, + tph, ... (at most kStatLoads partials); the
+// head's maximum is taken first (DPP within a wave when tph is a power of two
+// up to 64, else through LDS by one thread per head), then every pair's sum is
+// scaled to it with one exp2 and the scaled sums are added the same way.  The
+// partial loads are issued by load_head_parts() before the logits; every
+// thread calls finish_head_stats(), which ends with a barrier.
 struct HeadParts {
     float2 v[kStatLoads];
 };
 
 __device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int h0, int nh, HeadParts& hp)
 {
-    const int tph = nh <= 256 ? 256 / nh : 1;
+    const int tph = nh <= kUpdThreads ? kUpdThreads / nh : 1;
     const int t = threadIdx.x, hh = t / tph, sub = t % tph;
     const bool active = a.stats == nullptr && hh < nh;
     // npart is even and the rows 16-byte aligned: pairs of partials per load
@@ -235,8 +249,8 @@ __device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int 
     }
 }
 
-// max over the aligned group of tph lanes (tph a power of two, 2..64); every
-// lane of the group gets it.  Usable for sums as well (ADD).
+// max (or, ADD, sum) over the aligned group of tph lanes (tph a power of two,
+// 2..64); every lane of the group gets it.
 template <bool ADD>
 __device__ __forceinline__ float group_fold(float v, int tph)
 {
@@ -250,6 +264,7 @@ __device__ __forceinline__ float group_fold(float v, int tph)
     return v;
 }
 
+// red: kUpdThreads float2 of LDS; ms: the heads' (max, 1/sum)
 __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, int h0, int nh, const HeadParts& hp,
                                                   float2* red, float2* ms)
 {
@@ -262,57 +277,59 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
     float m = -INFINITY;
 #pragma unroll
     for (int i = 0; i < kStatLoads; ++i) m = fmaxf(m, hp.v[i].x);
-    const int tph = 256 / nh;
+    const int tph = kUpdThreads / nh;
+    const int hh = t / tph;
     const bool dpp_path = (tph & (tph - 1)) == 0 && tph >= 2 && tph <= 64;   // block-uniform
     if (dpp_path) {
         m = group_fold<false>(m, tph);   // every lane is active here; groups of tph lanes are aligned
     } else {
         red[t].x = m;
         __syncthreads();
-        const int hh = t / tph;
-        if (hh < nh) {
+        if (t < nh) {
             float M = -INFINITY;
-            for (int i = 0; i < tph; ++i) M = fmaxf(M, red[hh * tph + i].x);
-            m = M;
+            for (int i = 0; i < tph; ++i) M = fmaxf(M, red[t * tph + i].x);
+            ms[t].x = M;
         }
-        __syncthreads();   // the maxima have been read
+        __syncthreads();
+        m = hh < nh ? ms[hh].x : -INFINITY;
     }
     float z = 0.0f;
 #pragma unroll
     for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2f(hp.v[i].x - m);
     if (dpp_path) {
         z = group_fold<true>(z, tph);
-        if (t % tph == 0 && t / tph < nh) ms[t / tph] = make_float2(m, 1.0f / z);
+        if (t % tph == 0 && hh < nh) ms[hh] = make_float2(m, 1.0f / z);
     } else {
-        red[t] = make_float2(m, z);   // thread hh * tph holds the maximum of head hh
+        red[t].y = z;
         __syncthreads();
         if (t < nh) {
             float Z = 0.0f;
             for (int i = 0; i < tph; ++i) Z += red[t * tph + i].y;
-            ms[t] = make_float2(red[t * tph].x, 1.0f / Z);
+            ms[t].y = 1.0f / Z;
         }
     }
     __syncthreads();
 }
 
 // S[b,r,j] += sum_{h in heads(r)} exp2(s2*l - max_h) / sum_h   (softmax weights).
-// kUpdChunk = 128 tokens per workgroup (one workgroup per CU at a 32K-token
-// row, so the opening loads and the exponentials spread over the whole chip):
-// lane l of wave w loads tokens [2l, 2l+2) of heads w, w+4, ... as float2
-// (unconditional loads, heads clamped into the row's; heads past it weigh
-// nothing); the four wave partials are added in wave order, then thread t <
-// 128 finishes token t.  The head statistics come from the stats kernel or,
-// for short rows, from the unit partials reduced here.  The first-digit
-// histogram of the new keys (LDS, then the touched windows) is counted for
-// the refine pass and for a streamed selection without a bound; with a bound
-// the selection takes the first digit from the class counts of the pairs.
-__global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
+// kUpdChunk = 128 tokens per workgroup of kUpdThreads = 512 threads (one
+// workgroup per CU at a 32K-token row, two waves per SIMD to hide the
+// latency of the short dependent chains): lane l of wave w loads tokens
+// [2l, 2l+2) of heads w, w+8, ... as float2 (unconditional loads, heads
+// clamped into the row's; heads past it weigh nothing); the eight wave
+// partials are added in wave order, then thread t < 128 finishes token t.
+// The head statistics come from the stats kernel or, for short rows, from the
+// unit partials reduced here.  The first-digit histogram of the new keys
+// (LDS, then the touched windows) is counted for the refine pass and for a
+// streamed selection without a bound; with a bound the selection takes the
+// first digit from the class counts of the pairs.
+__global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
 {
-    __shared__ float2 wsum[4][64];
+    __shared__ float2 wsum[kUpdWaves][64];
     __shared__ KeyHist kh;
-    __shared__ float2 red[256];
+    __shared__ float2 red[kUpdThreads];
     __shared__ float2 ms[256];
-    __shared__ uint32_t sc_wcnt[kPairClasses][4];
+    __shared__ uint32_t sc_wcnt[kPairClasses][kUpdWaves];
     const int row = blockIdx.y;          // b * R + r
     const int b = row / a.R, r = row % a.R;
     const int h0 = a.R == 1 ? 0 : r * a.G;
@@ -334,14 +351,14 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     float2 x[kHeadBatch];
 #pragma unroll
     for (int i = 0; i < kHeadBatch; ++i)
-        x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(w + 4 * i, nh - 1) * a.ld);
+        x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(w + kUpdWaves * i, nh - 1) * a.ld);
     uint4 p0 = make_uint4(0u, 0u, 0u, 0u), p1 = p0;
     if (a.prev) {
         p0 = a.prev[2 * row];
         p1 = a.prev[2 * row + 1];
     }
     __builtin_amdgcn_sched_barrier(0);
-    if (a.hist) key_hist_clear(kh);
+    if (a.hist) key_hist_clear<kUpdThreads>(kh);
     finish_head_stats(a, b, h0, nh, hp, red, ms);
     const float s_old = j < a.n ? s_ld : 0.0f;
     const uint32_t bnd = a.prev ? stream_bound(a, p0, p1) : 0u;
@@ -350,27 +367,29 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     for (int hb = w;;) {
         float2 st[kHeadBatch];   // every statistics read of the batch before the first use
 #pragma unroll
-        for (int i = 0; i < kHeadBatch; ++i) st[i] = ms[min(hb + 4 * i, nh - 1)];
+        for (int i = 0; i < kHeadBatch; ++i) st[i] = ms[min(hb + kUpdWaves * i, nh - 1)];
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
             const float e0 = exp2f(a.s2 * x[i].x - st[i].x) * st[i].y;
             const float e1 = exp2f(a.s2 * x[i].y - st[i].x) * st[i].y;
-            const bool live = hb + 4 * i < nh;   // wave-uniform
+            const bool live = hb + kUpdWaves * i < nh;   // wave-uniform
             acc.x += live ? e0 : 0.0f;
             acc.y += live ? e1 : 0.0f;
         }
-        hb += 4 * kHeadBatch;
+        hb += kUpdWaves * kHeadBatch;
         if (hb >= nh) break;
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i)
-            x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(hb + 4 * i, nh - 1) * a.ld);
+            x[i] = *reinterpret_cast<const float2*>(lg + (int64_t)min(hb + kUpdWaves * i, nh - 1) * a.ld);
     }
     wsum[w][lane] = acc;
     __syncthreads();
     const float* ws = reinterpret_cast<const float*>(&wsum[0][0]);
     uint32_t key = 0u;
     if (j < a.n) {
-        const float tot = ((ws[tid] + ws[128 + tid]) + ws[256 + tid]) + ws[384 + tid];
+        float tot = ws[tid];
+#pragma unroll
+        for (int v = 1; v < kUpdWaves; ++v) tot += ws[v * 2 * 64 + tid];
         const float s_new = s_old + tot;
         srow[j] = s_new;
         key = select_key(s_new, j, a.pin_lo, a.pin_hi);
@@ -379,7 +398,7 @@ __global__ __launch_bounds__(256) void update_attn_kernel(UpdateArgs a)
     StreamRank sr{};
     if (a.prev) sr = stream_rank(a, row, j, key, bnd, sc_wcnt);   // block-uniform
     __syncthreads();
-    if (do_hist) key_hist_flush(kh, a.hist + (int64_t)row * kHistRow);
+    if (do_hist) key_hist_flush<kUpdThreads>(kh, a.hist + (int64_t)row * kHistRow);
     if (a.prev) stream_store(a, row, j, key, bnd, sr, sc_wcnt);
 }
 
@@ -391,7 +410,7 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
     const int b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const bool do_hist = a.hist != nullptr;
-    if (do_hist) key_hist_clear(kh);
+    if (do_hist) key_hist_clear<256>(kh);
     const int j2 = blockIdx.x * kUpdChunk + 2 * lane;
     const int jc = min(j2, (int)(a.ld - 2));
     const float* gs = a.logits + (int64_t)b * a.Hkv * a.ld + jc;
@@ -399,15 +418,15 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
     float* srow = a.s + (int64_t)b * a.s_sb;
     const float s_old = j < a.n ? srow[j] : 0.0f;
     float2 acc = make_float2(0.0f, 0.0f);
-    for (int gb = w; gb < a.Hkv; gb += 4 * kHeadBatch) {
-        float2 x[kHeadBatch];
+    for (int gb = w; gb < a.Hkv; gb += 4 * kRawBatch) {
+        float2 x[kRawBatch];
 #pragma unroll
-        for (int i = 0; i < kHeadBatch; ++i) {
+        for (int i = 0; i < kRawBatch; ++i) {
             const int g = gb + 4 * i;
             x[i] = g < a.Hkv ? *reinterpret_cast<const float2*>(gs + (int64_t)g * a.ld) : make_float2(0.f, 0.f);
         }
 #pragma unroll
-        for (int i = 0; i < kHeadBatch; ++i) {
+        for (int i = 0; i < kRawBatch; ++i) {
             acc.x += x[i].x;
             acc.y += x[i].y;
         }
@@ -423,7 +442,7 @@ __global__ __launch_bounds__(256) void update_raw_groups_kernel(UpdateArgs a)
     }
     if (do_hist) {
         __syncthreads();
-        key_hist_flush(kh, a.hist + (int64_t)b * kHistRow);
+        key_hist_flush<256>(kh, a.hist + (int64_t)b * kHistRow);
     }
 }
 
@@ -438,7 +457,7 @@ hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int n
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts)
 {
     dim3 grid((a.n + kUpdChunk - 1) / kUpdChunk, a.B * a.R);
-    hipExtLaunchKernelGGL(update_attn_kernel, grid, dim3(256), 0, st, ts.start, ts.stop, 0, a);
+    hipExtLaunchKernelGGL(update_attn_kernel, grid, dim3(kUpdThreads), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
 
