@@ -20,6 +20,16 @@ __device__ __forceinline__ uint4 load_stream16(const void* p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 16-byte non-temporal store: the scan's logits go to memory as they are written
+// instead of staying dirty in L2 until the kernel's end, where their write-back
+// delayed the next launch.
+__device__ __forceinline__ void store_stream16(float* p, float4 v)
+{
+    typedef float f32x4_t __attribute__((ext_vector_type(4)));
+    const f32x4_t x = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
+}
+
 // 8-byte non-temporal load (streamed int4 key codes).
 __device__ __forceinline__ uint2 load_stream8(const void* p)
 {
