@@ -744,7 +744,7 @@ def step_sources_sha() -> str:
 def step_algorithmic_bytes(B, Hq, Hkv, D, n, k):
     """Algorithmic bytes per launch of the streamed step's kernels after the
     scan (token rows, ATTN weights, 16-bit V; 512-token selection chunks,
-    256-token update blocks and scan units):
+    128-token update blocks, 256-token scan units):
       update_attn  the logits (Hq * 4 B per token), the scan's unit partials
                    once, S read and written (the candidate pairs, 8 B each
                    for the few thousand tokens at or above the bound's bin,
