@@ -304,6 +304,10 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
     a.k_exp = sk.k_exp;
     a.cap = sk.cap;
     a.kbits = sk.bits;
+    {   // bytes of keys (or sketch codes) this scan reads
+        const int64_t row_bytes = sk.k8 ? (sk.bits == 4 ? 64 : 128) : (int64_t)kHeadDim * 2;
+        a.nt_logits = (int64_t)s.B * s.Hkv * s.n * row_bytes <= kNtLogitsMaxKeyBytes;
+    }
     const int ncu = device_cus();
 
     UpdateArgs u{};

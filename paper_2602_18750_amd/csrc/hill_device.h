@@ -20,9 +20,9 @@ __device__ __forceinline__ uint4 load_stream16(const void* p)
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
-// 16-byte non-temporal store: the scan's logits go to memory as they are written
-// instead of staying dirty in L2 until the kernel's end, where their write-back
-// delayed the next launch.
+// 16-byte non-temporal store: the logits of a short scan go to memory as they
+// are written instead of staying dirty in L2 until the kernel's end, where
+// their write-back delayed the next launch.
 __device__ __forceinline__ void store_stream16(float* p, float4 v)
 {
     typedef float f32x4_t __attribute__((ext_vector_type(4)));

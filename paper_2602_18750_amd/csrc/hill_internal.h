@@ -47,7 +47,14 @@ struct ScoreArgs {
     const int8_t* k_exp;     //   its per-row exponents [B,Hkv,cap]
     int64_t cap;             //   tokens per (b, g) in the sketch, a multiple of 4
     int kbits;               //   8 or 4
+    int nt_logits;           // logits written with non-temporal stores (short launches, see kNtLogitsMaxKeyBytes)
 };
+
+// A scan reading at most this many key bytes writes its logits with non-temporal stores: in such a short
+// launch the end-of-kernel write-back of logits left dirty in L2 delays the next kernel by ~2 us (32K tokens,
+// B = 1: -0.8 us per layer-step); longer launches evict and write them back while they run, and there the
+// non-temporal stores cost more read bandwidth than they save (256 MiB - 4 GiB of keys: 1-3 % slower).
+constexpr int64_t kNtLogitsMaxKeyBytes = 96ll << 20;
 
 // int8 key sketch: codes and one power-of-two exponent per key row
 struct SketchArgs {

@@ -412,7 +412,9 @@ __device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const Tile
             for (int rb = 0; rb < 2; ++rb) {
                 const int j = c.j0 + 16 * rb + 4 * grp;
                 if (j + 4 <= a.n) {
-                    store_stream16(lrow + j, make_float4(mine[4 * rb], mine[4 * rb + 1], mine[4 * rb + 2], mine[4 * rb + 3]));
+                    const float4 v4 = make_float4(mine[4 * rb], mine[4 * rb + 1], mine[4 * rb + 2], mine[4 * rb + 3]);
+                    if (a.nt_logits) store_stream16(lrow + j, v4);
+                    else *reinterpret_cast<float4*>(lrow + j) = v4;
                 } else {
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
@@ -482,7 +484,9 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord
             }
             if (l8 < GC) {
                 if (jr + kRowsPerLane <= a.n) {
-                    store_stream16(lrow, make_float4(mine[0], mine[1], mine[2], mine[3]));
+                    const float4 v4 = make_float4(mine[0], mine[1], mine[2], mine[3]);
+                    if (a.nt_logits) store_stream16(lrow, v4);
+                    else *reinterpret_cast<float4*>(lrow) = v4;
                 } else {
 #pragma unroll
                     for (int u = 0; u < kRowsPerLane; ++u)
