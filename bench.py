@@ -49,7 +49,8 @@ Other modes: ``--sweep`` (27-cell throughput sweep, one line per cell),
 ``--read-ceiling`` (a plain streaming read at the scan's sizes),
 ``--selection-stats`` (heavy-hitter recall of the Qwen-7B-shaped workload and
 the step-to-step selection overlap of the AR(1) workload),
-``--summarize DIR`` (condense rocprofv3 output under DIR into text),
+``--summarize DIR`` (condense rocprofv3 output under DIR into text), ``--summarize-sweep DIR`` (per-cell kernel
+medians of a rocprofv3 kernel trace of ``--sweep``),
 ``--counters DIR`` (score_tiles HBM traffic from rocprofv3 --pmc runs),
 ``--step-counters DIR`` (the same for update_attn, topk_emit, merge_write).
 """
@@ -918,6 +919,48 @@ def summarize(directory: str):
     print("\n".join(lines))
 
 
+def summarize_sweep(directory: str):
+    """Per-cell kernel durations of `bench.py --sweep` from a rocprofv3 kernel
+    trace under `directory`: the sweep's cells run in workloads.sweep_workloads()
+    order, each as `replicas` warm-up steps and max(20, replicas) timed steps of
+    hill_step (scan, update, refine, select+attend, merge); per cell the median
+    duration of each kernel over the timed steps, and the scan's roofline
+    fraction (its algorithmic bytes over that median, against 8 TB/s)."""
+    import csv
+    import statistics
+    from paper_2602_18750_amd import workloads as W
+
+    path = sorted(glob.glob(os.path.join(directory, "**", "*kernel_trace.csv"), recursive=True))
+    if not path:
+        raise SystemExit("no kernel trace under %s" % directory)
+    with open(path[0]) as f:
+        rows = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
+    kinds = (("scan", "score_tiles_kernel"), ("update", "update_attn_kernel"), ("refine", "topk_refine_kernel"),
+             ("select", "topk_emit_kernel"), ("merge", "merge_write_kernel"))
+    seqs = {k: [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in rows if pat in r["Kernel_Name"]]
+            for k, pat in kinds}
+    pos = {k: 0 for k, _ in kinds}
+    out = ["| cell (B, n, α) | k | scan µs | scan GB/s | frac of 8 TB/s | update µs | refine µs | select µs | merge µs |",
+           "|---|---|---|---|---|---|---|---|---|"]
+    for w in W.sweep_workloads():
+        kv_bytes = 2 * w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
+        reps = max(1, min(16, -(-(1 << 30) // kv_bytes)))
+        iters = max(20, reps)
+        med = {}
+        for k, _ in kinds:
+            xs = seqs[k][pos[k] + reps:pos[k] + reps + iters]
+            pos[k] += reps + iters
+            if len(xs) != iters:
+                raise SystemExit("trace holds fewer %s launches than the sweep makes" % k)
+            med[k] = statistics.median(xs)
+        nbytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
+        gbs = nbytes / (med["scan"] * 1e-6) / 1e9
+        out.append("| %d, %dK, %d%% | %d | %.2f | %.0f | %.3f | %.2f | %.2f | %.2f | %.2f |" % (
+            w.batch, w.n_tokens // 1024, round(w.budget * 100), w.k_sel, med["scan"], gbs, gbs / HBM_PEAK_GBS,
+            med["update"], med["refine"], med["select"], med["merge"]))
+    print("\n".join(out))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -937,6 +980,7 @@ def main():
     ap.add_argument("--selection-stats", action="store_true",
                     help="heavy-hitter recall (Qwen-7B-shaped) and step-to-step selection overlap (AR(1) workload)")
     ap.add_argument("--summarize", metavar="DIR")
+    ap.add_argument("--summarize-sweep", metavar="DIR", help="per-cell kernel medians of a rocprofv3 trace of --sweep")
     ap.add_argument("--counters", metavar="DIR", help="write the score_tiles traffic record from --pmc runs under DIR")
     ap.add_argument("--step-counters", metavar="DIR",
                     help="write the traffic record of the step's other kernels from --pmc runs under DIR")
@@ -953,6 +997,9 @@ def main():
 
     if args.summarize:
         summarize(args.summarize)
+        return 0
+    if args.summarize_sweep:
+        summarize_sweep(args.summarize_sweep)
         return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
