@@ -935,29 +935,38 @@ def summarize_sweep(directory: str):
         raise SystemExit("no kernel trace under %s" % directory)
     with open(path[0]) as f:
         rows = sorted(csv.DictReader(f), key=lambda r: int(r["Start_Timestamp"]))
-    kinds = (("scan", "score_tiles_kernel"), ("update", "update_attn_kernel"), ("refine", "topk_refine_kernel"),
-             ("select", "topk_emit_kernel"), ("merge", "merge_write_kernel"))
-    seqs = {k: [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3 for r in rows if pat in r["Kernel_Name"]]
-            for k, pat in kinds}
-    pos = {k: 0 for k, _ in kinds}
-    out = ["| cell (B, n, α) | k | scan µs | scan GB/s | frac of 8 TB/s | update µs | refine µs | select µs | merge µs |",
-           "|---|---|---|---|---|---|---|---|---|"]
+    kinds = (("scan", "score_tiles_kernel"), ("stats", "softmax_stats_kernel"), ("update", "update_attn_kernel"),
+             ("refine", "topk_refine_kernel"), ("select", "topk_emit_kernel"), ("merge", "merge_write_kernel"))
+    # one step per scan launch: the kernels up to the next scan belong to it
+    # (softmax_stats runs only where the update does not reduce the partials)
+    steps = []
+    for r in rows:
+        for k, pat in kinds:
+            if pat in r["Kernel_Name"]:
+                if k == "scan":
+                    steps.append({})
+                elif not steps:
+                    raise SystemExit("trace starts with a %s launch before any scan" % k)
+                steps[-1][k] = steps[-1].get(k, 0.0) + (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3
+                break
+    pos = 0
+    out = ["| cell (B, n, α) | k | scan µs | scan GB/s | frac of 8 TB/s | stats µs | update µs | refine µs | select µs | "
+           "merge µs | step µs |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
     for w in W.sweep_workloads():
         kv_bytes = 2 * w.batch * w.n_kv_heads * w.n_tokens * w.head_dim * 2
         reps = max(1, min(16, -(-(1 << 30) // kv_bytes)))
         iters = max(20, reps)
-        med = {}
-        for k, _ in kinds:
-            xs = seqs[k][pos[k] + reps:pos[k] + reps + iters]
-            pos[k] += reps + iters
-            if len(xs) != iters:
-                raise SystemExit("trace holds fewer %s launches than the sweep makes" % k)
-            med[k] = statistics.median(xs)
+        cell = steps[pos + reps:pos + reps + iters]
+        pos += reps + iters
+        if len(cell) != iters:
+            raise SystemExit("trace holds fewer steps than the sweep makes")
+        med = {k: statistics.median(st.get(k, 0.0) for st in cell) for k, _ in kinds}
         nbytes = scan_kernel_bytes(w.batch, w.n_q_heads, w.n_kv_heads, w.head_dim, w.n_tokens)
         gbs = nbytes / (med["scan"] * 1e-6) / 1e9
-        out.append("| %d, %dK, %d%% | %d | %.2f | %.0f | %.3f | %.2f | %.2f | %.2f | %.2f |" % (
+        out.append("| %d, %dK, %d%% | %d | %.2f | %.0f | %.3f | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f |" % (
             w.batch, w.n_tokens // 1024, round(w.budget * 100), w.k_sel, med["scan"], gbs, gbs / HBM_PEAK_GBS,
-            med["update"], med["refine"], med["select"], med["merge"]))
+            med["stats"], med["update"], med["refine"], med["select"], med["merge"], sum(med.values())))
     print("\n".join(out))
 
 

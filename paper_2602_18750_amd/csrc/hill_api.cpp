@@ -341,7 +341,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         u.part = a.part;
         u.npart = s.npart;
         u.stats = nullptr;
-        if (!update_reduces_stats(s.R == 1 ? s.Hq : s.G, s.npart)) {
+        const int64_t update_blocks = (int64_t)s.B * s.R * ((s.n + kUpdChunk - 1) / kUpdChunk);
+        if (!update_reduces_stats(s.R == 1 ? s.Hq : s.G, s.npart, update_blocks)) {
             float2* stats = at<float2>(ws, L.stats);
             HIP_TRY(launch_softmax_stats(a.part, stats, s.B * s.Hq, s.npart, st, stage(ev, HILL_STAGE_STATS)));
             u.stats = stats;

@@ -254,13 +254,19 @@ hipError_t launch_bkp_lists(const BkpArgs& a, int rows, hipStream_t st);
 hipError_t launch_score_tiles(const ScoreArgs& a, int dtype, ScoreOut out, int ncu, hipStream_t st, Stamp ts = {});
 hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int npart, hipStream_t st,
                                 Stamp ts = {});
-// Whether update_attn can reduce the softmax partials itself (no separate
-// softmax_stats launch): every thread then loads at most kStatLoads of them.
-inline bool update_reduces_stats(int nheads_per_row, int npart)
+// Whether update_attn reduces the softmax partials itself (no separate
+// softmax_stats launch): every thread then loads at most kStatLoads of them,
+// and every update workgroup re-reads its row's partials. The extra launch
+// costs about 4 us; the re-reads it saves cost about 0.05 us per MiB (8 x 32K
+// tokens, 64 MiB: about 3 us; 32 x 32K, 256 MiB: about 12.5 us), so calls
+// re-reading more than kStatRereadMax bytes take the separate launch.
+constexpr int64_t kStatRereadMax = 128ll << 20;
+inline bool update_reduces_stats(int nheads_per_row, int npart, int64_t update_blocks)
 {
     if (nheads_per_row < 1 || nheads_per_row > 256) return false;
     const int tph = kUpdThreads / nheads_per_row;
-    return (int64_t)npart <= (int64_t)kStatLoads * tph;
+    return (int64_t)npart <= (int64_t)kStatLoads * tph &&
+           update_blocks * npart * nheads_per_row * (int64_t)sizeof(float2) <= kStatRereadMax;
 }
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts = {});
 hipError_t launch_update_raw_groups(const UpdateArgs& a, hipStream_t st, Stamp ts = {});

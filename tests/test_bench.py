@@ -59,11 +59,13 @@ def test_steady_state_table(tmp_path):
 
 
 def test_sweep_summary_maps_launches_to_cells(tmp_path):
-    """--summarize-sweep walks the trace in sweep order: per cell its warm-up
-    steps (replicas) are skipped and the medians of the timed steps are kept;
-    a cell's scan GB/s are its algorithmic bytes over that median."""
+    """--summarize-sweep walks the trace in sweep order, one step per scan
+    launch: per cell its warm-up steps (replicas) are skipped and the medians
+    of the timed steps are kept; a softmax_stats launch counts where a step has
+    one; a cell's scan GB/s are its algorithmic bytes over that median."""
     from paper_2602_18750_amd import workloads as W
     names = {"scan": "void hill::score_tiles_kernel<4, 0, hill::KeysF16<1, 4> >(hill::ScoreArgs)",
+             "stats": "hill::softmax_stats_kernel(float2 const*, float2*, int, int)",
              "update": "hill::update_attn_kernel(hill::UpdateArgs)",
              "refine": "hill::topk_refine_kernel(hill::RefineArgs)",
              "select": "void hill::topk_emit_kernel<1, 4, true, false, true, false>(hill::RefineArgs, hill::AttnArgs)",
@@ -75,8 +77,11 @@ def test_sweep_summary_maps_launches_to_cells(tmp_path):
         for i in range(reps + max(20, reps)):
             warm = i < reps
             # warm-up steps take 10x longer: they must not reach the medians
-            seq += [(names["scan"], (1000 + ci) * (10 if warm else 1)), (names["update"], 2000),
-                    (names["refine"], 3000), (names["select"], 4000 + ci), (names["merge"], 5000)]
+            seq += [(names["scan"], (1000 + ci) * (10 if warm else 1))]
+            if w.n_tokens > 32768:   # some steps reduce the partials in a launch of their own
+                seq += [(names["stats"], 700)]
+            seq += [(names["update"], 2000), (names["refine"], 3000), (names["select"], 4000 + ci),
+                    (names["merge"], 5000)]
     _trace(tmp_path / "s_kernel_trace.csv", seq)
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--summarize-sweep", str(tmp_path)],
                        capture_output=True, text=True, cwd=ROOT, timeout=120)
@@ -84,8 +89,10 @@ def test_sweep_summary_maps_launches_to_cells(tmp_path):
     rows = [l for l in r.stdout.splitlines() if l.startswith("| ") and "K," in l]
     assert len(rows) == 27
     first = [c.strip() for c in rows[0].split("|")[1:-1]]
-    assert first[0] == "1, 8K, 5%" and first[2] == "1.00" and first[5] == "2.00" and first[7] == "4.00"
+    assert first[0] == "1, 8K, 5%" and first[2] == "1.00" and first[5] == "0.00" and first[6] == "2.00"
+    assert first[8] == "4.00" and first[10] == "%.2f" % (1.0 + 2.0 + 3.0 + 4.0 + 5.0)
     nbytes = bench.scan_kernel_bytes(1, 32, 8, 128, 8192)
     assert first[3] == "%.0f" % (nbytes / 1e-6 / 1e9)
     last = [c.strip() for c in rows[-1].split("|")[1:-1]]
-    assert last[0] == "32, 64K, 20%" and last[2] == "%.2f" % ((1000 + 26) * 1e-3) and last[7] == "%.2f" % ((4000 + 26) * 1e-3)
+    assert last[0] == "32, 64K, 20%" and last[2] == "%.2f" % ((1000 + 26) * 1e-3) and last[8] == "%.2f" % ((4000 + 26) * 1e-3)
+    assert last[5] == "0.70" and last[6] == "2.00"
