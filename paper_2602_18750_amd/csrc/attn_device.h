@@ -238,13 +238,13 @@ __device__ __forceinline__ void softmax_block(int cnt, AttnLds<GC>& sh)
         const float m_new = fmaxf(m_old, mx);
         float ls = 0.0f;
         for (int t = lane; t < cnt; t += 64) {
-            const float e = exp2f(sh.p[t][hh] - m_new);
+            const float e = exp2_ftz(sh.p[t][hh] - m_new);
             sh.p[t][hh] = e;
             ls += e;
         }
         ls = wave_sum(ls);
         if (lane == 0) {
-            const float al = m_old == -INFINITY ? 0.0f : exp2f(m_old - m_new);
+            const float al = m_old == -INFINITY ? 0.0f : exp2_ftz(m_old - m_new);
             sh.alpha[hh] = al;
             sh.lrun[hh] = sh.lrun[hh] * al + ls;
             sh.mrun[hh] = m_new;
@@ -401,7 +401,7 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
     float O = 0.0f, L = 0.0f;
 #pragma unroll
     for (int i = 0; i < kPre; ++i) {
-        const float ws = v[i].y > 0.0f ? exp2f(v[i].x - mx) : 0.0f;
+        const float ws = v[i].y > 0.0f ? exp2_ftz(v[i].x - mx) : 0.0f;
         O += ws * x[i];
         L += ws * v[i].y;
     }
@@ -414,7 +414,7 @@ __device__ __forceinline__ void merge_head(const AttnArgs& a, int b, int h, int 
         }
 #pragma unroll
         for (int i = 0; i < kPre; ++i) {
-            const float ws = v[i].y > 0.0f ? exp2f(v[i].x - mx) : 0.0f;
+            const float ws = v[i].y > 0.0f ? exp2_ftz(v[i].x - mx) : 0.0f;
             O += ws * x[i];
             L += ws * v[i].y;
         }

@@ -30,6 +30,15 @@ __device__ __forceinline__ void store_stream16(float* p, float4 v)
     __builtin_nontemporal_store(x, reinterpret_cast<f32x4_t*>(p));
 }
 
+// 2^x on the transcendental unit alone (v_exp_f32, about 1 ulp), without the
+// range scaling that keeps results below 2^-126 denormal: those come out as
+// zero.  Every caller exponentiates relative to a maximum (softmax weights,
+// rescaled partial sums), so such a term is below 2^-126 of the sum it joins.
+__device__ __forceinline__ float exp2_ftz(float x)
+{
+    return __builtin_amdgcn_exp2f(x);
+}
+
 // 8-byte non-temporal load (streamed int4 key codes).
 __device__ __forceinline__ uint2 load_stream8(const void* p)
 {

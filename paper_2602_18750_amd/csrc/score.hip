@@ -427,7 +427,7 @@ __device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const Tile
         m = fmaxf(m, __shfl_xor(m, 32, 64));
         float z = 0.0f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) z += x[i] == -INFINITY ? 0.0f : exp2f(x[i] - m);
+        for (int i = 0; i < 8; ++i) z += x[i] == -INFINITY ? 0.0f : exp2_ftz(x[i] - m);
         z += __shfl_xor(z, 16, 64);
         z += __shfl_xor(z, 32, 64);
         if (grp == 0 && h < a.G) tile_part[h] = make_float2(m, z);
@@ -499,7 +499,7 @@ __device__ __forceinline__ void compute_tile(const ScoreArgs& a, const TileCoord
             m = fmaxf(m, __shfl_xor(m, 32, 64));
             float z = 0.0f;
 #pragma unroll
-            for (int u = 0; u < kRowsPerLane; ++u) z += jr + u < a.n ? exp2f(x[u] - m) : 0.0f;
+            for (int u = 0; u < kRowsPerLane; ++u) z += jr + u < a.n ? exp2_ftz(x[u] - m) : 0.0f;
             z += __shfl_xor(z, 8, 64);
             z += __shfl_xor(z, 16, 64);
             z += __shfl_xor(z, 32, 64);
@@ -539,7 +539,7 @@ __device__ __forceinline__ void merge_unit(const ScoreArgs& a, int bg, int unit,
     float z = 0.0f;
 #pragma unroll
     for (int i = 0; i < kUnitTiles; ++i)
-        z += tp[i][h].x == -INFINITY ? 0.0f : tp[i][h].y * exp2f(tp[i][h].x - m);
+        z += tp[i][h].x == -INFINITY ? 0.0f : tp[i][h].y * exp2_ftz(tp[i][h].x - m);
     const int b = bg / a.Hkv, g = bg % a.Hkv;
     a.part[((int64_t)b * a.Hq + g * a.G + h) * a.npart + unit] = make_float2(m, z);
 }

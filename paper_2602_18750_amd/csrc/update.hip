@@ -43,12 +43,12 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
         for (int u = 0; u < kBatch; ++u) {
             if (v[u].x == -INFINITY) continue;
             const float mn = fmaxf(m, v[u].x);
-            z = z * exp2f(m - mn) + v[u].y * exp2f(v[u].x - mn);
+            z = z * exp2_ftz(m - mn) + v[u].y * exp2_ftz(v[u].x - mn);
             m = mn;
         }
     }
     const float mw = wave_max(m);
-    z = m > -INFINITY ? z * exp2f(m - mw) : 0.0f;
+    z = m > -INFINITY ? z * exp2_ftz(m - mw) : 0.0f;
     z = wave_sum(z);
     if (lane == 0) {
         red_m[w] = mw;
@@ -59,7 +59,7 @@ __global__ __launch_bounds__(256) void softmax_stats_kernel(const float2* __rest
         float M = red_m[0];
         for (int i = 1; i < 4; ++i) M = fmaxf(M, red_m[i]);
         float Z = 0.0f;
-        for (int i = 0; i < 4; ++i) Z += red_m[i] > -INFINITY ? red_z[i] * exp2f(red_m[i] - M) : 0.0f;
+        for (int i = 0; i < 4; ++i) Z += red_m[i] > -INFINITY ? red_z[i] * exp2_ftz(red_m[i] - M) : 0.0f;
         stats[bh] = make_float2(M, 1.0f / Z);
     }
 }
@@ -295,7 +295,7 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
     }
     float z = 0.0f;
 #pragma unroll
-    for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2f(hp.v[i].x - m);
+    for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2_ftz(hp.v[i].x - m);
     if (dpp_path) {
         z = group_fold<true>(z, tph);
         if (t % tph == 0 && hh < nh) ms[hh] = make_float2(m, 1.0f / z);
@@ -370,8 +370,8 @@ __global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
         for (int i = 0; i < kHeadBatch; ++i) st[i] = ms[min(hb + kUpdWaves * i, nh - 1)];
 #pragma unroll
         for (int i = 0; i < kHeadBatch; ++i) {
-            const float e0 = exp2f(a.s2 * x[i].x - st[i].x) * st[i].y;
-            const float e1 = exp2f(a.s2 * x[i].y - st[i].x) * st[i].y;
+            const float e0 = exp2_ftz(a.s2 * x[i].x - st[i].x) * st[i].y;
+            const float e1 = exp2_ftz(a.s2 * x[i].y - st[i].x) * st[i].y;
             const bool live = hb + kUpdWaves * i < nh;   // wave-uniform
             acc.x += live ? e0 : 0.0f;
             acc.y += live ? e1 : 0.0f;
