@@ -340,6 +340,8 @@ hill_status run_score(const hill_desc* d, const Shape& s, const Layout& L, const
         u.logits = a.logits;
         u.part = a.part;
         u.npart = s.npart;
+        u.tph = kUpdThreads / (s.R == 1 ? s.Hq : s.G);   // heads per row <= 256 (validated)
+        u.inv_tph = 1.0f / (float)u.tph;
         u.stats = nullptr;
         const int64_t update_blocks = (int64_t)s.B * s.R * ((s.n + kUpdChunk - 1) / kUpdChunk);
         if (!update_reduces_stats(s.R == 1 ? s.Hq : s.G, s.npart, update_blocks)) {

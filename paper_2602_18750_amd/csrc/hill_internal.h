@@ -73,6 +73,8 @@ struct UpdateArgs {
     const float2* stats;     // ATTN: [B,Hq] (max, 1/sum) in the exp2 domain, or null: then
     const float2* part;      //   the kernel reduces the [B,Hq,npart] unit partials itself
     int npart;
+    int tph;                 // update_attn: threads per head in the reduction (kUpdThreads / heads per row)
+    float inv_tph;           //   and 1 / tph
     float* s;
     int64_t s_sb, s_sr;
     int B, Hq, Hkv, G, R, n;

@@ -229,20 +229,32 @@ struct HeadParts {
     float2 v[kStatLoads];
 };
 
-__device__ __forceinline__ void load_head_parts(const UpdateArgs& a, int b, int h0, int nh, HeadParts& hp)
+// Thread t's head among the heads of a row (tph threads each, set by the
+// host with its reciprocal): t / tph as a float product, exact for t < 512 and
+// tph <= 512 -- (t + 1/2) / tph lies at least 1/(2 tph) from an integer, far
+// more than the product's rounding.
+__device__ __forceinline__ int head_of_thread(const UpdateArgs& a, int t)
 {
-    const int tph = nh <= kUpdThreads ? kUpdThreads / nh : 1;
-    const int t = threadIdx.x, hh = t / tph, sub = t % tph;
+    return (int)(((float)t + 0.5f) * a.inv_tph);
+}
+
+// p: the row's first head's partials (uniform); hh, sub: this thread's head
+// and its place among the head's threads.
+__device__ __forceinline__ void load_head_parts(const UpdateArgs& a, const float2* p2, int hh, int sub, int nh,
+                                                HeadParts& hp)
+{
+    const int tph = a.tph;
     const bool active = a.stats == nullptr && hh < nh;
-    // npart is even and the rows 16-byte aligned: pairs of partials per load
-    const float4* p = reinterpret_cast<const float4*>(a.part + ((int64_t)b * a.Hq + h0 + (active ? hh : 0)) * a.npart);
+    // npart is even and the rows 16-byte aligned: pairs of partials per load;
+    // per-thread offsets in 32 bits (at most 256 heads x 2^20 partials)
     const int npair = a.npart / 2;
+    const float4* p = reinterpret_cast<const float4*>(p2) + (uint32_t)((active ? hh : 0) * npair);
 #pragma unroll
     for (int i = 0; i < kStatLoads / 2; ++i) {
         // consecutive lanes read consecutive pairs; unconditional (clamped)
         // loads, invalid ones replaced afterwards
         const int idx = sub + i * tph;
-        const float4 v = p[min(idx, npair - 1)];
+        const float4 v = p[(uint32_t)min(idx, npair - 1)];
         const bool ok = active && idx < npair;
         hp.v[2 * i] = ok ? make_float2(v.x, v.y) : make_float2(-INFINITY, 0.0f);
         hp.v[2 * i + 1] = ok ? make_float2(v.z, v.w) : make_float2(-INFINITY, 0.0f);
@@ -265,8 +277,8 @@ __device__ __forceinline__ float group_fold(float v, int tph)
 }
 
 // red: kUpdThreads float2 of LDS; ms: the heads' (max, 1/sum)
-__device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, int h0, int nh, const HeadParts& hp,
-                                                  float2* red, float2* ms)
+__device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, int h0, int nh, int hh,
+                                                  const HeadParts& hp, float2* red, float2* ms)
 {
     const int t = threadIdx.x;
     if (a.stats) {
@@ -277,8 +289,7 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
     float m = -INFINITY;
 #pragma unroll
     for (int i = 0; i < kStatLoads; ++i) m = fmaxf(m, hp.v[i].x);
-    const int tph = kUpdThreads / nh;
-    const int hh = t / tph;
+    const int tph = a.tph;
     const bool dpp_path = (tph & (tph - 1)) == 0 && tph >= 2 && tph <= 64;   // block-uniform
     if (dpp_path) {
         m = group_fold<false>(m, tph);   // every lane is active here; groups of tph lanes are aligned
@@ -298,7 +309,7 @@ __device__ __forceinline__ void finish_head_stats(const UpdateArgs& a, int b, in
     for (int i = 0; i < kStatLoads; ++i) z += hp.v[i].x == -INFINITY ? 0.0f : hp.v[i].y * exp2_ftz(hp.v[i].x - m);
     if (dpp_path) {
         z = group_fold<true>(z, tph);
-        if (t % tph == 0 && hh < nh) ms[hh] = make_float2(m, 1.0f / z);
+        if (t == hh * tph && hh < nh) ms[hh] = make_float2(m, 1.0f / z);
     } else {
         red[t].y = z;
         __syncthreads();
@@ -330,17 +341,18 @@ __global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
     __shared__ float2 red[kUpdThreads];
     __shared__ float2 ms[256];
     __shared__ uint32_t sc_wcnt[kPairClasses][kUpdWaves];
-    const int row = blockIdx.y;          // b * R + r
-    const int b = row / a.R, r = row % a.R;
+    const int r = blockIdx.y, b = blockIdx.z;
+    const int row = b * a.R + r;
     const int h0 = a.R == 1 ? 0 : r * a.G;
     const int nh = a.R == 1 ? a.Hq : a.G;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int hh = head_of_thread(a, tid);                // this thread's head in the statistics
     // Every load of the opening is issued before anything waits for one: the
     // softmax partials, this thread's old S, the first batch of logits and the
     // streamed selection's state (whose test runs only after the statistics).
     HeadParts hp;
-    load_head_parts(a, b, h0, nh, hp);
+    load_head_parts(a, a.part + ((int64_t)b * a.Hq + h0) * a.npart, hh, tid - hh * a.tph, nh, hp);
     const int j2 = blockIdx.x * kUpdChunk + 2 * lane;     // first of this lane's 2 tokens
     const int jc = min(j2, (int)(a.ld - 2));              // rows are padded to ld (multiple of 4)
     const float* lg = a.logits + ((int64_t)b * a.Hq + h0) * a.ld + jc;
@@ -359,7 +371,7 @@ __global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
     }
     __builtin_amdgcn_sched_barrier(0);
     if (a.hist) key_hist_clear<kUpdThreads>(kh);
-    finish_head_stats(a, b, h0, nh, hp, red, ms);
+    finish_head_stats(a, b, h0, nh, hh, hp, red, ms);
     const float s_old = j < a.n ? s_ld : 0.0f;
     const uint32_t bnd = a.prev ? stream_bound(a, p0, p1) : 0u;
     const bool do_hist = a.hist != nullptr && !(bnd >> 31);   // block-uniform
@@ -456,7 +468,9 @@ hipError_t launch_softmax_stats(const float2* part, float2* stats, int bh, int n
 
 hipError_t launch_update_attn(const UpdateArgs& a, hipStream_t st, Stamp ts)
 {
-    dim3 grid((a.n + kUpdChunk - 1) / kUpdChunk, a.B * a.R);
+    const int nh = a.R == 1 ? a.Hq : a.G;
+    if (nh < 1 || a.tph != kUpdThreads / nh || a.B > 65535 || a.R > 65535) return hipErrorInvalidValue;
+    dim3 grid((a.n + kUpdChunk - 1) / kUpdChunk, a.R, a.B);
     hipExtLaunchKernelGGL(update_attn_kernel, grid, dim3(kUpdThreads), 0, st, ts.start, ts.stop, 0, a);
     return hipGetLastError();
 }
