@@ -125,6 +125,8 @@ __device__ __forceinline__ void key_hist_flush(KeyHist& h, uint32_t* ghist)
 constexpr int kHeadBatch = 4;   // float2 logits loads in flight per thread (update_attn)
 constexpr int kRawBatch = 8;    // float2 group-sum loads in flight per thread (update_raw_groups)
 constexpr int kUpdWaves = kUpdThreads / 64;
+constexpr int kTokWaves = kUpdChunk / 64;   // waves whose threads finish a token (thread t < kUpdChunk)
+static_assert(kUpdChunk % 64 == 0 && kTokWaves <= kUpdWaves, "whole waves of tokens");
 
 // First-digit bound of the streamed selection for this row: the first digit
 // of the previous step's threshold, while the keys at or above that bin then
@@ -162,7 +164,7 @@ struct StreamRank {
 };
 
 __device__ __forceinline__ StreamRank stream_rank(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                                  uint32_t (*wcnt)[kUpdWaves])
+                                                  uint32_t (*wcnt)[kTokWaves])
 {
     const uint32_t d0 = bnd & (kHistBins - 1);
     const uint32_t dig = key >> (32 - kHistBits);
@@ -186,16 +188,16 @@ __device__ __forceinline__ StreamRank stream_rank(const UpdateArgs& a, int row, 
     return s;
 }
 
-__device__ __forceinline__ uint32_t class_total(const uint32_t (*wcnt)[kUpdWaves], int k)
+__device__ __forceinline__ uint32_t class_total(const uint32_t (*wcnt)[kTokWaves], int k)
 {
     uint32_t t = 0u;
 #pragma unroll
-    for (int v = 0; v < kUpdWaves; ++v) t += wcnt[k][v];
+    for (int v = 0; v < kTokWaves; ++v) t += wcnt[k][v];
     return t;
 }
 
 __device__ __forceinline__ void stream_store(const UpdateArgs& a, int row, int j, uint32_t key, uint32_t bnd,
-                                             const StreamRank& s, const uint32_t (*wcnt)[kUpdWaves])
+                                             const StreamRank& s, const uint32_t (*wcnt)[kTokWaves])
 {
     const int w = threadIdx.x >> 6;
     if (s.cand) {
@@ -340,7 +342,7 @@ __global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
     __shared__ KeyHist kh;
     __shared__ float2 red[kUpdThreads];
     __shared__ float2 ms[256];
-    __shared__ uint32_t sc_wcnt[kPairClasses][kUpdWaves];
+    __shared__ uint32_t sc_wcnt[kPairClasses][kTokWaves];
     const int r = blockIdx.y, b = blockIdx.z;
     const int row = b * a.R + r;
     const int h0 = a.R == 1 ? 0 : r * a.G;
@@ -407,11 +409,13 @@ __global__ __launch_bounds__(kUpdThreads) void update_attn_kernel(UpdateArgs a)
         key = select_key(s_new, j, a.pin_lo, a.pin_hi);
         if (do_hist) count_key(kh, key);
     }
+    // the streamed selection's ranks and pairs: the token waves only (the others
+    // would share SIMDs with them for nothing)
     StreamRank sr{};
-    if (a.prev) sr = stream_rank(a, row, j, key, bnd, sc_wcnt);   // block-uniform
+    if (a.prev && w < kTokWaves) sr = stream_rank(a, row, j, key, bnd, sc_wcnt);   // wave-uniform
     __syncthreads();
     if (do_hist) key_hist_flush<kUpdThreads>(kh, a.hist + (int64_t)row * kHistRow);
-    if (a.prev) stream_store(a, row, j, key, bnd, sr, sc_wcnt);
+    if (a.prev && w < kTokWaves) stream_store(a, row, j, key, bnd, sr, sc_wcnt);
 }
 
 // Token rows, RAW mode, Hkv > 1: S[b,0,j] += sum_g groupsum[b,g,j] (same layout).
