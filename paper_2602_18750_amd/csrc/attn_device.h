@@ -32,11 +32,15 @@ namespace hill {
 constexpr int kAttnBlock = 512;   // list entries per LDS block
 constexpr int kKBatch = 4;        // K rows per row group per batch (64 entries)
 constexpr int kVBatch = 16;       // V rows per wave per batch (64 entries)
+// Zero weights after a block's last entry: a wave's batch of eight entries
+// reaches at most 30 entries past the block's count, which then weigh 0
+// without a per-entry test.
+constexpr int kWeightPad = 32;
 
 template <int GC>
 struct AttnLds {
     int32_t tok[kAttnBlock];          // token index of each entry of the block
-    float p[kAttnBlock][GC];          // logits, then exp2 weights
+    float p[kAttnBlock + kWeightPad][GC];   // logits, then exp2 weights (0 past the block's entries)
     float mrun[GC], lrun[GC], alpha[GC];
     float o[4][GC][kHeadDim];         // per-wave outputs, added at the end
 };
@@ -184,7 +188,9 @@ __device__ __forceinline__ void logits_rows(const AttnArgs& a, const uint4 (&qv)
 }
 
 // weight * V of this wave's entries idx0 .. idx0+N-1 (entry w + 4*idx) into
-// the accumulators; entries at or past nmine weigh 0.
+// the accumulators; entries at or past nmine lie past the block's count,
+// where softmax_block left zero weights (their V registers hold a clamped,
+// valid row).
 template <int DT, int GC>
 __device__ __forceinline__ void values_rows(const uint32_t (&vr)[kVBatch], int w, int idx0, int nmine, int cnt,
                                             const float (*p)[GC], AttnAcc<GC>& acc)
@@ -195,7 +201,7 @@ __device__ __forceinline__ void values_rows(const uint32_t (&vr)[kVBatch], int w
 #pragma unroll
         for (int i = c0; i < c0 + 8; ++i) {
             const int idx = idx0 + i;
-            const int tc = min(w + 4 * idx, cnt - 1);
+            const int tc = w + 4 * idx;   // < cnt + kWeightPad
             float v0, v1;
             widen2<DT>(vr[i], v0, v1);
             float pw[GC];
@@ -214,9 +220,8 @@ __device__ __forceinline__ void values_rows(const uint32_t (&vr)[kVBatch], int w
             }
 #pragma unroll
             for (int hh = 0; hh < GC; ++hh) {
-                const float pv = idx < nmine ? pw[hh] : 0.0f;
-                acc.o[hh][0] += pv * v0;
-                acc.o[hh][1] += pv * v1;
+                acc.o[hh][0] += pw[hh] * v0;
+                acc.o[hh][1] += pw[hh] * v1;
             }
         }
     }
@@ -243,6 +248,7 @@ __device__ __forceinline__ void softmax_block(int cnt, AttnLds<GC>& sh)
             ls += e;
         }
         ls = wave_sum(ls);
+        if (lane < kWeightPad) sh.p[cnt + lane][hh] = 0.0f;   // entries past the block weigh 0
         if (lane == 0) {
             const float al = m_old == -INFINITY ? 0.0f : exp2_ftz(m_old - m_new);
             sh.alpha[hh] = al;

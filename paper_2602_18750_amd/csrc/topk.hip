@@ -220,9 +220,33 @@ __device__ __forceinline__ void add_class_counts(const RefineArgs& r, int row, u
 }
 
 // Block-wide sums of the class counts (every thread gets them); one barrier.
-__device__ __forceinline__ void reduce_class_counts(uint32_t (&c)[kPairClasses], uint32_t (*red)[kThreads / 64])
+// packed (block-uniform): every thread holds one block's counts (at most
+// kUpdChunk each) and the row at most kThreads blocks, so every sum stays
+// below 2^16 and two counts share a word.
+__device__ __forceinline__ void reduce_class_counts(uint32_t (&c)[kPairClasses], uint32_t (*red)[kThreads / 64],
+                                                    bool packed)
 {
+    static_assert(kPairClasses == 5 && kThreads * kUpdChunk < 65536, "three packed sums");
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    if (packed) {
+        const uint32_t v0 = wave_sum_u32(c[0] | (c[1] << 16));
+        const uint32_t v1 = wave_sum_u32(c[2] | (c[3] << 16));
+        const uint32_t v2 = wave_sum_u32(c[4]);
+        if (lane == 0) {
+            red[0][w] = v0;
+            red[1][w] = v1;
+            red[2][w] = v2;
+        }
+        __syncthreads();
+        const uint32_t t0 = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+        const uint32_t t1 = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+        c[0] = t0 & 0xffffu;
+        c[1] = t0 >> 16;
+        c[2] = t1 & 0xffffu;
+        c[3] = t1 >> 16;
+        c[4] = (red[2][0] + red[2][1]) + (red[2][2] + red[2][3]);
+        return;
+    }
 #pragma unroll
     for (int k = 0; k < kPairClasses; ++k) {
         const uint32_t v = wave_sum_u32(c[k]);
@@ -520,7 +544,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         load_digit_bins(r.hist2 + (int64_t)row * kHistRow, h2);
         load_digit_bins(r.hist2 + ((int64_t)at.B * r.R + row) * kHistRow, h2n);   // [w][rows][bins]
         add_class_counts(r, row, cnt);
-        reduce_class_counts(cnt, cls_red);
+        reduce_class_counts(cnt, cls_red, (r.n + kUpdChunk - 1) / kUpdChunk <= kThreads);
         const uint32_t d0 = bnd & (kHistBins - 1);
         const bool bound = bnd >> 31;   // block-uniform
         uint32_t b1 = 0u, need1 = 0u, in1 = 0u;
