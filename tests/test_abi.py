@@ -448,3 +448,17 @@ def test_tier_apply_checks_its_lists_and_context(H):
     # a tiered step scores on the sketch
     assert lib.hill_step_tiered(ctypes.byref(d), ctypes.byref(t), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, None, 1000,
                                 8, FAKE, None, 0, 10, FAKE, FAKE, FAKE, 1 << 40, None, None) == INVALID
+
+
+def test_stepcall_rejects_host_tensors(H):
+    """StepCall checks where its tensors live before anything reaches the
+    library: host tensors raise ValueError in the constructor (a host pointer
+    taken for a device one would fault the GPU at the first launch)."""
+    import torch
+    q = torch.zeros((1, 4, 128), dtype=torch.bfloat16)
+    k = torch.zeros((1, 2, 64, 128), dtype=torch.bfloat16)
+    s = torch.zeros((1, 1, 64))
+    with pytest.raises(ValueError, match="GPU tensors only"):
+        H.StepCall(q, k, k, s, 8)
+    with pytest.raises(ValueError, match="GPU tensors only"):
+        H.StepCall(q, k, k, s, 8, stream_state=torch.zeros((1, 1, 8), dtype=torch.int32))

@@ -173,6 +173,21 @@ def test_streamed_sketch_equals_plain_sketch_step(nbits):
         assert torch.equal(s_a, s_b) and torch.equal(i_a, i_b) and torch.equal(o_a, o_b), "step %d" % t
 
 
+def test_stepcall_rejects_a_host_or_strided_state():
+    """Device inputs with a stream state on the host, or one that is not
+    contiguous: ValueError from StepCall's constructor, before any launch."""
+    x = W.make_random(1, 8, 2, 128, 1000, "bf16", steps=1, seed=3)
+    q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
+    s = H().new_importance(1, 1, 1000, DEV)
+    with pytest.raises(ValueError, match="GPU tensors only"):
+        H().StepCall(q[0], k, v, s, 100, stream_state=H().new_stream_state(1, 1, DEV).cpu())
+    strided = torch.zeros((1, 1, 16), dtype=torch.int32, device=DEV)[:, :, ::2]
+    with pytest.raises(ValueError, match="contiguous"):
+        H().StepCall(q[0], k, v, s, 100, stream_state=strided)
+    torch.cuda.synchronize()
+    assert not s.any(), "a rejected StepCall must not have launched anything"
+
+
 def test_streamed_growing_context_keeps_the_bound():
     """n grows by one token per step and k = floor(0.1 n) grows with it (the
     decode loop's case): results equal hill_step's, and after the first steps
