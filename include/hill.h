@@ -170,8 +170,10 @@ HILL_API hill_status hill_step(const hill_desc* d, const void* q, const void* k,
  *   HILL_STAGE_SCAN     streams the keys: q.K^T of every cached token (ATTN:
  *                       logits and per-256-token softmax partials; RAW with
  *                       one row per KV head: added straight into S)
- *   HILL_STAGE_STATS    ATTN rows longer than 32768 tokens only: the softmax
- *                       normaliser of every head
+ *   HILL_STAGE_STATS    ATTN only, for rows longer than 32768 tokens or calls
+ *                       whose update would re-read more than 128 MiB of
+ *                       softmax partials (e.g. 32 sequences of 32768
+ *                       tokens): the softmax normaliser of every head
  *   HILL_STAGE_UPDATE   S += the step's weights, and the selection's first
  *                       radix digit histogram (RAW per-KV-head rows: only
  *                       the histogram; a streamed step with a valid bound:
