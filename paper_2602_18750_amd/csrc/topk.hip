@@ -373,17 +373,46 @@ __global__ __launch_bounds__(kThreads) void topk_refine_kernel(RefineArgs a)
     if (tid == 0) a.cand_n[(int64_t)row * a.nchunks + c] = n_cand;
 }
 
-// Calls f(key) for every candidate of chunks [c0, c1) of a row, all threads
-// of the block in parallel (one chunk list per wave pass).
+// Calls f(key) for every candidate of chunks [c0, c1) of a row.  Groups of
+// up to kThreads chunks are flattened with one block scan of their counts
+// (offsets in `offs`, kThreads words of LDS) and a binary search per key, so
+// all loads of a round are in flight together instead of one chunk after
+// another.  Every thread of the block calls it.
 template <typename F>
-__device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int c0, int c1, F f)
+__device__ __forceinline__ void for_candidates(const RefineArgs& a, int row, int c0, int c1, uint32_t* offs,
+                                               uint32_t* scratch, F f)
 {
-    const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    constexpr int kU = 8;
+    const uint32_t tid = threadIdx.x;
     const uint32_t* cn = a.cand_n + (int64_t)row * a.nchunks;
     const uint32_t* cl = a.cand_key + (int64_t)row * a.n;
-    for (int cc = c0 + w; cc < c1; cc += kThreads / 64) {
-        const uint32_t m = cn[cc];
-        for (uint32_t i = lane; i < m; i += 64) f(cl[(int64_t)cc * kSelChunk + i]);
+    for (int g0 = c0; g0 < c1; g0 += kThreads) {
+        const int ng = min(kThreads, c1 - g0);
+        const uint32_t m = (int)tid < ng ? cn[g0 + tid] : 0u;
+        uint32_t tot;
+        const uint32_t o = block_excl_scan<kThreads>(m, scratch, &tot);
+        offs[tid] = o;
+        __syncthreads();
+        for (uint32_t i0 = 0; i0 < tot; i0 += kThreads * kU) {
+            uint32_t v[kU];
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                const uint32_t i = i0 + u * kThreads + tid;
+                v[u] = 0u;
+                if (i < tot) {
+                    int lo = 0, hi = ng - 1;   // the last chunk whose offset is <= i
+                    while (lo < hi) {
+                        const int mid = (lo + hi + 1) >> 1;
+                        if (offs[mid] <= i) lo = mid; else hi = mid - 1;
+                    }
+                    v[u] = cl[(int64_t)(g0 + lo) * kSelChunk + (i - offs[lo])];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kU; ++u)
+                if (i0 + u * kThreads + tid < tot) f(v[u]);
+        }
+        __syncthreads();   // offs is rewritten by the next group
     }
 }
 
@@ -482,7 +511,7 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
     __shared__ int32_t sloc[TIER ? kAttnBlock : 1];
     __shared__ uint32_t hist3[256];
     __shared__ typename std::conditional<STREAM, uint32_t[kHistBins], uint32_t[1]>::type hist2s;
-    __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_offs;
+    __shared__ uint32_t pair_offs[kThreads];   // also the chunk offsets of the candidate walks
     __shared__ typename std::conditional<STREAM, uint32_t[kThreads], uint32_t[1]>::type pair_starts;
     __shared__ uint32_t scan_scratch[kThreads / 64 + 1];
     __shared__ uint32_t red[kThreads / 64];
@@ -636,21 +665,34 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
             need = need2;
             all_eq = need2 == in2;
             if (!all_eq) {   // third digit (bits 7..0)
-                uint32_t* h3 = hist3;
-                for (int i = tid; i < 256; i += kThreads) h3[i] = 0u;
-                __syncthreads();
+                // needed only by workgroups holding a key of the threshold's 24-bit bin (and by the
+                // one that writes the next step's bound): elsewhere the keys above that bin are
+                // exactly the selected ones
                 const uint32_t p2 = prefix;
-                for_row_pairs(r, row, fast, pair_cls, pair_offs, pair_starts, scan_scratch,
-                              [p2, h3](uint32_t kk, uint32_t) {
-                    if ((kk >> 8) == p2) atomicAdd(&h3[kk & 0xffu], 1u);
-                });
-                __syncthreads();
-                find_bin<kThreads>(h3, 256, need2, scan_scratch, res);
-                const uint32_t b3 = res[0] & 0xffu;
-                prefix = (p2 << 8) | b3;
-                shift = 0;
-                need = need2 - res[1];
-                all_eq = need == h3[b3];
+                uint32_t kx[kPerThread];
+                bool okx[kPerThread];
+                keys_of(sx, c, r.n, r.pin_lo, r.pin_hi, kx, okx);
+                bool mine = writer && c == 0;
+#pragma unroll
+                for (int e = 0; e < kPerThread; ++e) mine = mine || (okx[e] && (kx[e] >> 8) == p2);
+                if (__syncthreads_or(mine)) {   // block-uniform
+                    uint32_t* h3 = hist3;
+                    for (int i = tid; i < 256; i += kThreads) h3[i] = 0u;
+                    __syncthreads();
+                    for_row_pairs(r, row, fast, pair_cls, pair_offs, pair_starts, scan_scratch,
+                                  [p2, h3](uint32_t kk, uint32_t) {
+                        if ((kk >> 8) == p2) atomicAdd(&h3[kk & 0xffu], 1u);
+                    });
+                    __syncthreads();
+                    find_bin<kThreads>(h3, 256, need2, scan_scratch, res);
+                    const uint32_t b3 = res[0] & 0xffu;
+                    prefix = (p2 << 8) | b3;
+                    shift = 0;
+                    need = need2 - res[1];
+                    all_eq = need == h3[b3];
+                } else {
+                    all_eq = true;   // no key of this chunk ties with the threshold at 24 bits
+                }
             }
             __syncthreads();
         }
@@ -685,20 +727,32 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
         need = need2;
         all_eq = need2 == in2;
         if (!all_eq) {   // third digit (bits 7..0) from the candidate lists
-            for (int i = tid; i < 256; i += kThreads) hist3[i] = 0u;
-            __syncthreads();
+            // only workgroups holding a key of the threshold's 24-bit bin need it (elsewhere the
+            // keys above that bin are exactly the selected ones)
             const uint32_t p2 = prefix;
-            for_candidates(r, row, 0, r.nchunks, [p2](uint32_t kk) {
-                if ((kk >> 8) == p2) atomicAdd(&hist3[kk & 0xffu], 1u);
-            });
-            __syncthreads();
-            find_bin<kThreads>(hist3, 256, need2, scan_scratch, res);
-            const uint32_t b3 = res[0] & 0xffu;
-            prefix = (p2 << 8) | b3;
-            shift = 0;
-            need = need2 - res[1];
-            all_eq = need == hist3[b3];
-            __syncthreads();
+            uint32_t kx[kPerThread];
+            bool okx[kPerThread];
+            keys_of(sx, c, r.n, r.pin_lo, r.pin_hi, kx, okx);
+            bool mine = false;
+#pragma unroll
+            for (int e = 0; e < kPerThread; ++e) mine = mine || (okx[e] && (kx[e] >> 8) == p2);
+            if (__syncthreads_or(mine)) {   // block-uniform
+                for (int i = tid; i < 256; i += kThreads) hist3[i] = 0u;
+                __syncthreads();
+                for_candidates(r, row, 0, r.nchunks, pair_offs, scan_scratch, [p2](uint32_t kk) {
+                    if ((kk >> 8) == p2) atomicAdd(&hist3[kk & 0xffu], 1u);
+                });
+                __syncthreads();
+                find_bin<kThreads>(hist3, 256, need2, scan_scratch, res);
+                const uint32_t b3 = res[0] & 0xffu;
+                prefix = (p2 << 8) | b3;
+                shift = 0;
+                need = need2 - res[1];
+                all_eq = need == hist3[b3];
+                __syncthreads();
+            } else {
+                all_eq = true;   // no key of this chunk ties with the threshold at 24 bits
+            }
         }
     }
     }
@@ -730,7 +784,8 @@ __global__ __launch_bounds__(kThreads) void topk_emit_kernel(RefineArgs r, AttnA
                 before_chunks += (kk == pf && j < jlim) ? 1u : 0u;
             });
         } else {
-            for_candidates(r, row, 0, c, [&before_chunks, pf](uint32_t kk) { before_chunks += kk == pf; });
+            for_candidates(r, row, 0, c, pair_offs, scan_scratch,
+                           [&before_chunks, pf](uint32_t kk) { before_chunks += kk == pf; });
         }
         before_chunks = wave_sum_u32(before_chunks);
         if (lane == 0) red[tid >> 6] = before_chunks;
