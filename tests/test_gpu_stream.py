@@ -43,7 +43,9 @@ def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0, mutate=None
     reset steps (HILL_STREAM_RESET); mutate: {step: f}, f(S) applied in place
     to both copies of S before that step (a change outside the calls).
     Asserts bit-identical S, indices and outputs and a valid state after
-    every step; returns the streamed state."""
+    every step, and that the indices are the oracle's top-k of the GPU's own
+    S (with the pins; equal keys to the lower token index, R7).  Returns the
+    streamed state."""
     q, k, v = x.q.to(DEV), x.k.to(DEV), x.v.to(DEV)
     B, Hkv, ncap = k.shape[0], k.shape[1], k.shape[2]
     R = 1 if gran == "token" else Hkv
@@ -61,6 +63,10 @@ def _pair_run(x, schedule, gran="token", sink=0, recent=0, resets=0, mutate=None
         assert torch.equal(s_a, s_b), "step %d: S differs" % t
         assert torch.equal(i_a, i_b), "step %d: indices differ" % t
         assert torch.equal(o_a, o_b), "step %d: outputs differ" % t
+        sv = s_b.cpu().numpy()[..., :n].astype(np.float64).reshape(-1, n)
+        ref = O.topk_pinned(sv, ks, sink, recent) if (sink or recent) else O.topk(sv, ks)
+        assert np.array_equal(i_b.cpu().numpy(), ref.reshape(i_b.shape)), \
+            "step %d: not the top-k of the step's own S" % t
         _check_state(state, s_b, n, ks, sink, recent)
     return state
 
@@ -132,6 +138,20 @@ def test_streamed_heavy_ties():
     x.k[:, :, :, :] = x.k[:, :, pick, :].clone()
     say("streamed heavy ties")
     _pair_run(x, [(4096, 1000), (4096, 1000), (4096, 2047), (4096, 2047)])
+
+
+def test_heavy_ties_over_more_than_256_chunks():
+    """The same over 140,000 tokens (274 selection chunks, so the walks over
+    the chunks' candidate lists take two groups of 256) with the threshold
+    inside a tie group spread over all chunks: both paths' indices equal the
+    oracle's top-k of the step's own S, lower index first among equal keys."""
+    n = 140000
+    x = W.make_random(1, 8, 2, 128, n, "bf16", steps=3, seed=17)
+    g = torch.Generator().manual_seed(4)
+    pick = torch.randint(0, 60, (n,), generator=g)
+    x.k[:, :, :, :] = x.k[:, :, pick, :].clone()
+    say("heavy ties, 140000 tokens")
+    _pair_run(x, [(n, 40000), (n, 40000), (n, 70001)])
 
 
 def test_streamed_workload3_full_size_matches_oracle():
