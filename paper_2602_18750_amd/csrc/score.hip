@@ -18,7 +18,9 @@
 // pair per head.  Queries stay in registers while (b, g) stays the same.
 // Latency is hidden by occupancy (four workgroups per CU) rather than by
 // double-buffering, which costs more registers than it returns.  Partial dot
-// products are combined by three DPP adds.
+// products are combined by three DPP adds.  ATTN logits with G >= 4 heads per
+// KV head take the dots on the matrix cores instead (KeysF16Mfma: the same
+// tiles, units and whole-line loads, a different lane-to-element map).
 #include <hip/hip_ext.h>
 
 #include <type_traits>
@@ -70,6 +72,7 @@ struct KeysF16 {
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
     static constexpr bool kMfma = false;
+    static constexpr bool kMfma16 = false;
     uint4 kr[kSlots][2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
@@ -189,6 +192,7 @@ struct KeysSketch : SketchQuery<DT> {
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
     static constexpr bool kMfma = false;
+    static constexpr bool kMfma16 = false;
     static constexpr int kRowBytes = kHeadDim * BITS / 8;
     using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
     using SketchQuery<DT>::ql;
@@ -301,6 +305,7 @@ struct KeysSketchMfma4 : SketchQuery<DT> {
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;
     static constexpr bool kMfma = true;
+    static constexpr bool kMfma16 = false;
     static constexpr int kRowBytes = kHeadDim / 2;
     using SketchQuery<DT>::ql;
     using SketchQuery<DT>::q_tag;
@@ -381,6 +386,98 @@ struct KeysSketchMfma4 : SketchQuery<DT> {
     }
 };
 
+// 16-bit keys on the matrix cores (ATTN logits, G >= 4): the dot products as
+// v_mfma_f32_16x16x32_{bf16,f16}, D[row][col] = sum_k A[row][k] B[k][col].
+// A row of the 16-row operand is half a key row: row 4q + 2u + p of group gr
+// (gr = 0..3) holds the 16-byte chunks of parity p (chunks 2m + p of the 16 in
+// the 256-byte row) of token 8q + 4u + gr of the tile; lane l (row l % 16,
+// quarter c = l / 16) loads chunk 8s + 2c + p for line s = 0, 1 (one MFMA per
+// line).  The 8 lanes of a token thus read its whole 128-byte line s in one
+// load instruction.  Column 2h + p' of the query operand holds the parity-p'
+// chunks of head hc + h (8 heads per pass, zero beyond G), in the same order,
+// so D[(t, p)][(h, p)] is the parity-p half of q_h . K_t and the two halves
+// sit in neighbouring lanes (columns 2h, 2h + 1) of the same output row pair.
+// One DPP add joins them: even lanes finish token 8q + gr, odd lanes token
+// 8q + 4 + gr (q = l / 16), so over the four groups a lane holds 4
+// consecutive tokens of its head and stores them as one float4.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+
+template <int DT>
+__device__ __forceinline__ f32x4_t mfma16(const uint4& a, const uint4& b, f32x4_t acc)
+{
+    if constexpr (DT == 1)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+    else
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b),
+                                                      acc, 0, 0, 0);
+}
+
+constexpr int kMfmaHeads = 8;   // heads per pass of KeysF16Mfma (two columns each)
+
+template <int DT>
+struct KeysF16Mfma {
+    static constexpr int kSlots = 1;
+    static constexpr bool kGroupQuery = false;
+    static constexpr bool kIntDot = false;
+    static constexpr bool kMfma = false;
+    static constexpr bool kMfma16 = true;
+    uint4 kr[kSlots][8];   // [tile][2 * group + line]: the lane's 16-byte chunk
+    uint4 qb[2];           // query operand per line (column l % 16)
+    int q_tag = -1;
+
+    template <int SLOT>
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int lane = rg * 8 + l8;
+        const int i = lane & 15, q = i >> 2, u = (i >> 1) & 1, p = i & 1;
+        const uint16_t* kb = a.k + (int64_t)c.b * a.k_sb + (int64_t)c.g * a.k_sh + (2 * (lane >> 4) + p) * 8;
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            const int j = c.j0 + 8 * q + 4 * u + gr;
+            const uint16_t* row = kb + (int64_t)j * a.k_sn;
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+                kr[SLOT][2 * gr + s] = j < a.n ? load_stream16(row + 64 * s) : make_uint4(0u, 0u, 0u, 0u);
+        }
+    }
+
+    // Query operand of heads hc .. hc+7: column 2h + p' of lane l = l % 16 holds
+    // the chunks 8s + 2c + p' (c = l / 16) of head hc + h, zero beyond G.
+    __device__ __forceinline__ void mquery(const ScoreArgs& a, const TileCoord& c, int hc, int lane)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+        const int col = lane & 15, h = hc + (col >> 1);
+        const int e0 = (2 * (lane >> 4) + (col & 1)) * 8;
+        const uint16_t* qr = a.q + (int64_t)c.b * a.q_sb + (int64_t)(c.g * a.G + min(h, a.G - 1)) * a.q_sh + e0;
+#pragma unroll
+        for (int s = 0; s < 2; ++s)
+            qb[s] = h < a.G ? *reinterpret_cast<const uint4*>(qr + 64 * s) : make_uint4(0u, 0u, 0u, 0u);
+        q_tag = tag;
+    }
+
+    // Raw logits of this lane's 4 tokens (see above) for head hc + (l % 16) / 2.
+    template <int SLOT>
+    __device__ __forceinline__ void dots(int lane, float (&out)[4]) const
+    {
+        const bool odd = lane & 1;
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+            acc = mfma16<DT>(kr[SLOT][2 * gr], qb[0], acc);
+            acc = mfma16<DT>(kr[SLOT][2 * gr + 1], qb[1], acc);
+            // even lane (p' = 0): its row pair u = 0 half + the odd neighbour's;
+            // odd lane (p' = 1): its u = 1 half + the even neighbour's
+            const float own = odd ? acc[3] : acc[0];
+            const float send = odd ? acc[1] : acc[2];
+            out[gr] = own + dpp<0xB1>(send);
+        }
+    }
+};
+
 // One wave-tile of KeysSketchMfma (ATTN): logits of heads hc + l % 16 for
 // rows 4*(l/16) .. +3 of both 16-row blocks, stored as float4, and the tile's
 // (max, sum exp2) per head.
@@ -431,6 +528,50 @@ __device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const Tile
         z += __shfl_xor(z, 16, 64);
         z += __shfl_xor(z, 32, 64);
         if (grp == 0 && h < a.G) tile_part[h] = make_float2(m, z);
+    }
+}
+
+// One wave-tile of KeysF16Mfma (ATTN): lane l holds head hc + (l % 16) / 2
+// for tokens j0 + 8*(l/16) + 4*(l & 1) .. +3; the head's 32 tokens sit in
+// lanes l ^ 1, l ^ 16, l ^ 32.
+template <int SLOT, typename Keys>
+__device__ __forceinline__ void compute_tile_mfma16(const ScoreArgs& a, const TileCoord& c, int lane, Keys& ks,
+                                                    float2* tile_part)
+{
+    const int jt = c.j0 + 8 * (lane >> 4) + 4 * (lane & 1);   // this lane's first token
+    for (int hc = 0; hc < a.G; hc += kMfmaHeads) {
+        ks.mquery(a, c, hc, lane);
+        const int h = hc + ((lane & 15) >> 1);
+        float mine[4], x[4];
+        ks.template dots<SLOT>(lane, mine);
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            x[i] = jt + i < a.n ? a.s2 * mine[i] : -INFINITY;
+            m = fmaxf(m, x[i]);
+        }
+        if (h < a.G) {
+            float* lrow = a.logits + ((int64_t)c.b * a.Hq + c.g * a.G + h) * a.ld + jt;
+            if (jt + 4 <= a.n) {
+                const float4 v4 = make_float4(mine[0], mine[1], mine[2], mine[3]);
+                if (a.nt_logits) store_stream16(lrow, v4);
+                else *reinterpret_cast<float4*>(lrow) = v4;
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    if (jt + i < a.n) lrow[i] = mine[i];
+            }
+        }
+        m = fmaxf(m, dpp<0xB1>(m));
+        m = fmaxf(m, __shfl_xor(m, 16, 64));
+        m = fmaxf(m, __shfl_xor(m, 32, 64));
+        float z = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) z += jt + i < a.n ? exp2_ftz(x[i] - m) : 0.0f;
+        z += dpp<0xB1>(z);
+        z += __shfl_xor(z, 16, 64);
+        z += __shfl_xor(z, 32, 64);
+        if (lane < 16 && !(lane & 1) && h < a.G) tile_part[h] = make_float2(m, z);
     }
 }
 
@@ -600,6 +741,7 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
         }
         if (t0 < a.ntiles) {
             if constexpr (Keys::kMfma) compute_tile_mfma<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
+            else if constexpr (Keys::kMfma16) compute_tile_mfma16<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
             else compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i0][h] = make_float2(-INFINITY, 0.0f);
@@ -607,6 +749,8 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
         if (t1 < a.ntiles) {
             if constexpr (Keys::kSlots == 1) ks.template load<0>(a, c1, rg, l8);
             if constexpr (Keys::kMfma) compute_tile_mfma<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
+            else if constexpr (Keys::kMfma16)
+                compute_tile_mfma16<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
             else compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i1][h] = make_float2(-INFINITY, 0.0f);
@@ -642,6 +786,14 @@ hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp 
         // key the vector units' dot chains are short and faster)
         if (a.k8 && a.kbits == 4 && a.G >= 4) {
             auto kernel = score_tiles_kernel<1, OUT, KeysSketchMfma4<DT>>;
+            const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+            const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+            hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+            return hipGetLastError();
+        }
+        // 16-bit keys, G >= 4: the dots on the matrix cores as well
+        if (!a.k8 && a.G >= 4) {
+            auto kernel = score_tiles_kernel<1, OUT, KeysF16Mfma<DT>>;
             const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
             const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
             hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
