@@ -72,7 +72,7 @@ struct KeysF16 {
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
     static constexpr bool kMfma = false;
-    static constexpr bool kMfma16 = false;
+    static constexpr bool kMfmaSplit = false;
     uint4 kr[kSlots][2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
     int q_tag = -1;
@@ -192,7 +192,7 @@ struct KeysSketch : SketchQuery<DT> {
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
     static constexpr bool kMfma = false;
-    static constexpr bool kMfma16 = false;
+    static constexpr bool kMfmaSplit = false;
     static constexpr int kRowBytes = kHeadDim * BITS / 8;
     using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
     using SketchQuery<DT>::ql;
@@ -296,7 +296,7 @@ struct KeysSketch : SketchQuery<DT> {
 // cross-lane steps.  The sums are the same exact integers as on the vector
 // units, so the logits are bit-identical.  (An int8 row is a whole line, which
 // this layout would read in two half-line requests per instruction: the int8
-// sketch stays on the vector units, whose row groups read whole lines.)
+// sketch uses the split-row layout of KeysSketchMfma8 instead.)
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
 
 template <int DT>
@@ -305,7 +305,7 @@ struct KeysSketchMfma4 : SketchQuery<DT> {
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;
     static constexpr bool kMfma = true;
-    static constexpr bool kMfma16 = false;
+    static constexpr bool kMfmaSplit = false;
     static constexpr int kRowBytes = kHeadDim / 2;
     using SketchQuery<DT>::ql;
     using SketchQuery<DT>::q_tag;
@@ -423,7 +423,7 @@ struct KeysF16Mfma {
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
     static constexpr bool kMfma = false;
-    static constexpr bool kMfma16 = true;
+    static constexpr bool kMfmaSplit = true;
     uint4 kr[kSlots][8];   // [tile][2 * group + line]: the lane's 16-byte chunk
     uint4 qb[2];           // query operand per line (column l % 16)
     int q_tag = -1;
@@ -530,6 +530,83 @@ __device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const Tile
         if (grp == 0 && h < a.G) tile_part[h] = make_float2(m, z);
     }
 }
+
+// Int8 key sketch on the matrix cores (ATTN logits, G >= 4), in the split-row
+// layout of KeysF16Mfma: row 4q + 2u + p of group gr holds the 16-byte chunks
+// 2c + p (c = 0..3) of token 8q + 4u + gr's 128-byte code row, so one load
+// instruction reads 8 whole rows, and each lane's 16 bytes feed two
+// v_mfma_i32_16x16x32_i8 (its low and high 8 codes).  The integer halves are
+// joined by one DPP add and scaled by 2^(e_q + e_k) as on the vector units:
+// the logits are the same exact values.
+template <int DT>
+struct KeysSketchMfma8 : SketchQuery<DT> {
+    static constexpr int kSlots = 2;
+    static constexpr bool kGroupQuery = true;
+    static constexpr bool kIntDot = true;
+    static constexpr bool kMfma = false;
+    static constexpr bool kMfmaSplit = true;
+    using SketchQuery<DT>::ql;
+    using SketchQuery<DT>::q_tag;
+    uint4 kr[kSlots][4];       // [tile][group]: the lane's 16 code bytes
+    uint32_t ek4[kSlots];      // exponents of the lane's 4 output tokens
+    uint64_t qb[2];            // query operand of the two MFMAs (column l % 16)
+    int eq_lane = 0;           // exponent of the lane's head
+
+    template <int SLOT>
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int lane = rg * 8 + l8;
+        const int i = lane & 15, q = i >> 2, u = (i >> 1) & 1, p = i & 1;
+        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
+        const int8_t* kb = a.k8 + bg * a.cap * kHeadDim + (2 * (lane >> 4) + p) * 16;
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            const int j = c.j0 + 8 * q + 4 * u + gr;
+            kr[SLOT][gr] = j < a.n ? load_stream16(kb + (int64_t)j * kHeadDim) : make_uint4(0u, 0u, 0u, 0u);
+        }
+        // the output tokens start at a multiple of 4 and cap is one too: one aligned word
+        const int jt = c.j0 + 8 * (lane >> 4) + 4 * (lane & 1);
+        ek4[SLOT] = jt < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jt) : 0u;
+    }
+
+    // Query operand of heads hc .. hc+7 (column 2h + p': the codes of chunk
+    // 2c + p' of head hc + h, zero beyond G) and the lane's head exponent.
+    __device__ __forceinline__ void mquery(const ScoreArgs& a, const TileCoord& c, int hc, int lane)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+        const int col = lane & 15, h = hc + (col >> 1);
+        uint4 x = make_uint4(0u, 0u, 0u, 0u);
+        eq_lane = 0;
+        if (h < a.G) {
+            x = *reinterpret_cast<const uint4*>(&ql->q8[h][(2 * (lane >> 4) + (col & 1)) * 16]);
+            eq_lane = ql->eq[h];
+        }
+        qb[0] = (uint64_t)x.x | ((uint64_t)x.y << 32);
+        qb[1] = (uint64_t)x.z | ((uint64_t)x.w << 32);
+        q_tag = tag;
+    }
+
+    template <int SLOT>
+    __device__ __forceinline__ void dots(int lane, float (&out)[4]) const
+    {
+        const bool odd = lane & 1;
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            const uint4 k = kr[SLOT][gr];
+            i32x4_t acc = {0, 0, 0, 0};
+            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8((long)((uint64_t)k.x | ((uint64_t)k.y << 32)), (long)qb[0],
+                                                        acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8((long)((uint64_t)k.z | ((uint64_t)k.w << 32)), (long)qb[1],
+                                                        acc, 0, 0, 0);
+            const int own = odd ? acc[3] : acc[0];
+            const int send = odd ? acc[1] : acc[2];
+            const int d = own + __builtin_amdgcn_update_dpp(0, send, 0xB1, 0xF, 0xF, false);
+            const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * gr));
+            out[gr] = ldexpf((float)d, eq_lane + ek);
+        }
+    }
+};
 
 // One wave-tile of KeysF16Mfma (ATTN): lane l holds head hc + (l % 16) / 2
 // for tokens j0 + 8*(l/16) + 4*(l & 1) .. +3; the head's 32 tokens sit in
@@ -741,7 +818,7 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
         }
         if (t0 < a.ntiles) {
             if constexpr (Keys::kMfma) compute_tile_mfma<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
-            else if constexpr (Keys::kMfma16) compute_tile_mfma16<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
+            else if constexpr (Keys::kMfmaSplit) compute_tile_mfma16<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
             else compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i0][h] = make_float2(-INFINITY, 0.0f);
@@ -749,7 +826,7 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
         if (t1 < a.ntiles) {
             if constexpr (Keys::kSlots == 1) ks.template load<0>(a, c1, rg, l8);
             if constexpr (Keys::kMfma) compute_tile_mfma<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
-            else if constexpr (Keys::kMfma16)
+            else if constexpr (Keys::kMfmaSplit)
                 compute_tile_mfma16<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
             else compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
         } else if constexpr (OUT == kOutLogits) {
@@ -786,6 +863,13 @@ hipError_t launch_score_inst(const ScoreArgs& a, int ncu, hipStream_t st, Stamp 
         // key the vector units' dot chains are short and faster)
         if (a.k8 && a.kbits == 4 && a.G >= 4) {
             auto kernel = score_tiles_kernel<1, OUT, KeysSketchMfma4<DT>>;
+            const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
+            const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
+            hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
+            return hipGetLastError();
+        }
+        if (a.k8 && a.kbits == 8 && a.G >= 4) {
+            auto kernel = score_tiles_kernel<1, OUT, KeysSketchMfma8<DT>>;
             const int64_t cap = (int64_t)ncu * resident_per_cu(kernel);
             const int64_t grid = total < cap ? (total < 1 ? 1 : total) : cap;
             hipExtLaunchKernelGGL(kernel, dim3((unsigned)grid), dim3(256), 0, st, ts.start, ts.stop, 0, a);
