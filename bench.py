@@ -821,7 +821,7 @@ def make_counters(directory: str, command: str):
     ff = copy_bytes / (cf_kib * 1024.0)
     wf = copy_bytes / (cw_kib * 1024.0)
 
-    def scan(keys):   # the score_tiles instantiation over `keys` (KeysF16 or KeysI8)
+    def scan(keys):   # the score_tiles instantiations matching `keys` (a regular expression)
         f_kib = mean(_counter_rows(os.path.join(directory, "fetch"), "FETCH_SIZE", keys))
         w_kib = mean(_counter_rows(os.path.join(directory, "write"), "WRITE_SIZE", keys))
         return {"fetch_kib_per_dispatch": round(f_kib, 1), "write_kib_per_dispatch": round(w_kib, 1),
@@ -836,7 +836,7 @@ def make_counters(directory: str, command: str):
         "copy_write_kib": round(cw_kib, 1),
         "fetch_factor": round(ff, 4),
         "write_factor": round(wf, 4),
-        "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan(r"KeysSketch<\d+, \d+, 8>")),
+        "sketch": dict(kernel="score_tiles (int8 key sketch)", **scan(r"KeysSketchMfma8<|KeysSketch<\d+, \d+, 8>")),
         "sketch4": dict(kernel="score_tiles (int4 key sketch)", **scan(r"KeysSketchMfma4<|KeysSketch<\d+, \d+, 4>")),
         "command": command,
     })
