@@ -63,6 +63,11 @@ SCORE_CASES = [
     # the head-count limits: 256 query heads, 128 per KV head
     (1, 256, 2, 700, "bf16", "attn", "token"),
     (1, 256, 256, 300, "fp16", "raw", "kvhead"),
+    # matrix-core scan (ATTN, G >= 4) with group sizes that leave query columns
+    # empty (G = 5, 7) or take a second pass of 8 heads (G = 12), ragged lengths
+    (2, 10, 2, 1001, "bf16", "attn", "token"),
+    (1, 7, 1, 35, "bf16", "attn", "token"),
+    (1, 12, 1, 333, "fp16", "attn", "kvhead"),
 ]
 
 
@@ -211,6 +216,18 @@ def run_steps(x, k_sel, mode, gran, steps, check_every=1, where=""):
             if np.array_equal(idx_g, idx_ref):
                 check_outputs(out.cpu().numpy(), out_ref, "%s step %d out(direct)" % (where, t))
     return s, idx, out
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,n,k,dt,gran", [(2, 10, 2, 1001, 100, "bf16", "token"),
+                                                   (1, 12, 1, 333, 40, "fp16", "kvhead"),
+                                                   (1, 7, 1, 35, 9, "bf16", "token")])
+def test_step_with_uneven_group_sizes(B, Hq, Hkv, n, k, dt, gran):
+    """hill_step where the matrix-core scan leaves query columns empty (G = 5,
+    7) or takes two passes (G = 12); the select+attend kernel then takes the
+    scan's logits of those heads."""
+    say("uneven group", B, Hq, Hkv, n, k, dt, gran)
+    x = W.make_random(B, Hq, Hkv, 128, n, dt, steps=3, seed=n + Hq)
+    run_steps(x, k, "attn", gran, 3, where="G %d" % (Hq // Hkv))
 
 
 @pytest.mark.parametrize("mode,gran", [("attn", "token"), ("attn", "kvhead"), ("raw", "token"),
@@ -485,6 +502,9 @@ SKETCH_SCORE_CASES = [
     (2, 8, 2, 1001, "fp16", "attn", "kvhead"),
     (1, 32, 32, 777, "fp16", "raw", "token"),
     (2, 16, 4, 2049, "bf16", "raw", "kvhead"),
+    # the int8 matrix-core scan with empty query columns or two passes, ragged lengths
+    (2, 10, 2, 1001, "fp16", "attn", "token"),
+    (1, 12, 1, 333, "bf16", "attn", "kvhead"),
 ]
 
 
