@@ -786,6 +786,10 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
     const int u_end = min(u + per, total);
 
     static_assert(kUnitTiles == 8, "each wave takes two tiles of a unit");
+    // one tile in flight per wave: the next unit's first tile is requested
+    // before this unit's merge, so its barriers overlap that load
+    constexpr bool kAhead = !Keys::kGroupQuery && Keys::kSlots == 1;
+    bool ahead = false;
     Keys ks;
     int cur_bg = -1;
     for (; u < u_end; ++u) {
@@ -811,7 +815,7 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
                 cur_bg = bg;
             }
         } else {
-            if (t0 < a.ntiles) ks.template load<0>(a, c0, rg, l8);
+            if (t0 < a.ntiles && !ahead) ks.template load<0>(a, c0, rg, l8);
             if constexpr (Keys::kSlots == 2) {   // both tiles in flight at once
                 if (t1 < a.ntiles) ks.template load<1>(a, c1, rg, l8);
             }
@@ -831,6 +835,13 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
             else compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i1][h] = make_float2(-INFINITY, 0.0f);
+        }
+        if constexpr (kAhead) {
+            ahead = u + 1 < u_end;   // workgroup-uniform
+            if (ahead) {
+                const int un = u + 1, tn = (un % a.npart) * kUnitTiles + i0;
+                if (tn < a.ntiles) ks.template load<0>(a, coord(a, (un / a.npart) * a.ntiles + tn), rg, l8);
+            }
         }
 
         if constexpr (OUT == kOutLogits) {
