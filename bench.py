@@ -686,6 +686,7 @@ def run_read_ceiling(args):
         reps = max(1, min(16, 1024 // mib))
         xs = [torch.empty(mib << 20, dtype=torch.uint8, device="cuda:0").fill_(r + 1) for r in range(reps)]
         best = None
+        per_grid = {}
         for grid in (1024, 2048, 4096, 8192):
             for x in xs:
                 calib_read(x, grid, sink, stream)
@@ -699,12 +700,14 @@ def run_read_ceiling(args):
             torch.cuda.synchronize()
             ts = sorted(a.elapsed_time(b) for a, b in ev)
             med = ts[len(ts) // 2]
+            per_grid[grid] = round(med * 1e3, 2)
             if best is None or med < best[0]:
                 best = (med, grid)
         med, grid = best
         gbs = (mib << 20) / (med * 1e-3) / 1e9
         print(json.dumps({"read_mib": mib, "kernel": "hill_calib_read", "grid": grid, "median_us": round(med * 1e3, 2),
-                          "gbps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "replicas": reps}),
+                          "gbps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "replicas": reps,
+                          "median_us_per_grid": per_grid}),
               flush=True)
         del xs
         torch.cuda.empty_cache()
