@@ -71,7 +71,6 @@ struct KeysF16 {
     static constexpr int kSlots = GC <= 2 ? 2 : 1;
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
-    static constexpr bool kMfma = false;
     static constexpr bool kMfmaSplit = false;
     uint4 kr[kSlots][2 * kRowsPerLane];
     uint4 qa[GC], qb[GC];
@@ -191,7 +190,6 @@ struct KeysSketch : SketchQuery<DT> {
     static constexpr int kSlots = 2;   // a wave's two tiles of a unit are loaded together
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;   // idot + scale: one conversion per row for the lane's head
-    static constexpr bool kMfma = false;
     static constexpr bool kMfmaSplit = false;
     static constexpr int kRowBytes = kHeadDim * BITS / 8;
     using Codes = typename std::conditional<BITS == 8, uint4, uint2>::type;
@@ -283,108 +281,7 @@ struct KeysSketch : SketchQuery<DT> {
     }
 };
 
-// Int4 key sketch on the matrix cores (ATTN logits): the scan's integer dot
-// products as v_mfma_i32_16x16x32_i8, D[row][head] = sum_k A[row][k] B[k][head]
-// over 16 rows and 16 head columns (the group's heads, zero beyond G).  Lane l
-// holds row l % 16 of a 16-row block and the 16 bytes [16*(l/16), +16) of
-// that 64-byte row (codes [32*(l/16), +32)), unpacked to int8 by two masks;
-// one load instruction thus reads 16 whole rows, i.e. 8 whole 128-byte lines.
-// The k index of the four MFMAs runs over the lane's codes in order, and the
-// query operand (head l % 16) follows the same order.  The result lands as 4
-// consecutive rows 4*(l/16) .. +3 of head l % 16 per lane, so each lane scales
-// and stores its own head's logits and the per-tile softmax pairs need two
-// cross-lane steps.  The sums are the same exact integers as on the vector
-// units, so the logits are bit-identical.  (An int8 row is a whole line, which
-// this layout would read in two half-line requests per instruction: the int8
-// sketch uses the split-row layout of KeysSketchMfma8 instead.)
 typedef int i32x4_t __attribute__((ext_vector_type(4)));
-
-template <int DT>
-struct KeysSketchMfma4 : SketchQuery<DT> {
-    static constexpr int kSlots = 2;
-    static constexpr bool kGroupQuery = true;
-    static constexpr bool kIntDot = true;
-    static constexpr bool kMfma = true;
-    static constexpr bool kMfmaSplit = false;
-    static constexpr int kRowBytes = kHeadDim / 2;
-    using SketchQuery<DT>::ql;
-    using SketchQuery<DT>::q_tag;
-    uint4 kr[kSlots][2];            // [tile][16-row block]: the lane's 16 bytes of its row
-    uint32_t ek4[kSlots][2];        // exponents of rows 4*(l/16) .. +3 of each block
-    uint64_t qb[4];                 // query operand of the four MFMAs (head hc + l % 16)
-    int eq_lane = 0;                // its exponent
-    int bias = 0;                   // 8 * (sum of its 128 codes)
-
-    template <int SLOT>
-    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
-    {
-        const int lane = rg * 8 + l8;
-        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
-        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + 16 * (lane >> 4);
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            const int j = c.j0 + 16 * rb + (lane & 15);
-            kr[SLOT][rb] = j < a.n ? load_stream16(kb + (int64_t)j * kRowBytes) : make_uint4(0u, 0u, 0u, 0u);
-            // rows 4*(l/16) .. +3 start at a multiple of 4 and cap is one too: one aligned word
-            const int j4 = c.j0 + 16 * rb + 4 * (lane >> 4);
-            ek4[SLOT][rb] = j4 < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + j4) : 0u;
-        }
-    }
-
-    // Query operand of heads hc .. hc+15 (lane: head hc + l % 16, the query
-    // codes of the dimensions of the lane's key codes, in the same order).
-    __device__ __forceinline__ void mquery(const ScoreArgs& a, const TileCoord& c, int hc, int lane)
-    {
-        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
-        if (tag == q_tag) return;
-        const int h = hc + (lane & 15);
-        uint4 x = make_uint4(0u, 0u, 0u, 0u), y = make_uint4(0u, 0u, 0u, 0u);
-        eq_lane = 0;
-        if (h < a.G) {
-            const uint4* src = reinterpret_cast<const uint4*>(&ql->q8[h][32 * (lane >> 4)]);
-            x = src[0];
-            y = src[1];
-            eq_lane = ql->eq[h];
-        }
-        qb[0] = (uint64_t)x.x | ((uint64_t)x.y << 32);
-        qb[1] = (uint64_t)x.z | ((uint64_t)x.w << 32);
-        qb[2] = (uint64_t)y.x | ((uint64_t)y.y << 32);
-        qb[3] = (uint64_t)y.z | ((uint64_t)y.w << 32);
-        {   // the +8 offset of the codes: 8 * (sum of the head's 128 query codes)
-            const int ones = 0x01010101;
-            int sq = 0;
-            sq = __builtin_amdgcn_sdot4((int)x.x, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)x.y, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)x.z, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)x.w, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)y.x, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)y.y, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)y.z, ones, sq, false);
-            sq = __builtin_amdgcn_sdot4((int)y.w, ones, sq, false);
-            sq += __shfl_xor(sq, 16, 64);
-            sq += __shfl_xor(sq, 32, 64);
-            bias = 8 * sq;
-        }
-        q_tag = tag;
-    }
-
-    // Exact integer dots of the 16 rows of block rb against heads hc .. hc+15.
-    template <int SLOT>
-    __device__ __forceinline__ i32x4_t dots(int rb) const
-    {
-        i32x4_t acc = {-bias, -bias, -bias, -bias};
-#pragma unroll
-        for (int jk = 0; jk < 4; ++jk) {
-            // codes + 8 in [1, 15]: low nibbles are codes 0..3 of a word, high nibbles 4..7
-            const uint4 k = kr[SLOT][rb];
-            const uint32_t w = jk == 0 ? k.x : jk == 1 ? k.y : jk == 2 ? k.z : k.w;
-            const uint32_t m = 0x0F0F0F0Fu;
-            const uint64_t a_op = (uint64_t)(w & m) | ((uint64_t)((w >> 4) & m) << 32);
-            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8((long)a_op, (long)qb[jk], acc, 0, 0, 0);
-        }
-        return acc;
-    }
-};
 
 // 16-bit keys on the matrix cores (ATTN logits, G >= 4): the dot products as
 // v_mfma_f32_16x16x32_{bf16,f16}, D[row][col] = sum_k A[row][k] B[k][col].
@@ -422,7 +319,6 @@ struct KeysF16Mfma {
     static constexpr int kSlots = 1;
     static constexpr bool kGroupQuery = false;
     static constexpr bool kIntDot = false;
-    static constexpr bool kMfma = false;
     static constexpr bool kMfmaSplit = true;
     uint4 kr[kSlots][8];   // [tile][2 * group + line]: the lane's 16-byte chunk
     uint4 qb[2];           // query operand per line (column l % 16)
@@ -478,59 +374,6 @@ struct KeysF16Mfma {
     }
 };
 
-// One wave-tile of KeysSketchMfma (ATTN): logits of heads hc + l % 16 for
-// rows 4*(l/16) .. +3 of both 16-row blocks, stored as float4, and the tile's
-// (max, sum exp2) per head.
-template <int SLOT, typename Keys>
-__device__ __forceinline__ void compute_tile_mfma(const ScoreArgs& a, const TileCoord& c, int lane, Keys& ks,
-                                                  float2* tile_part)
-{
-    const int n16 = lane & 15, grp = lane >> 4;
-    for (int hc = 0; hc < a.G; hc += 16) {
-        ks.mquery(a, c, hc, lane);
-        const int h = hc + n16;
-        float mine[8], x[8];
-        float m = -INFINITY;
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            const i32x4_t d = ks.template dots<SLOT>(rb);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int ek = (int)(int8_t)(ks.ek4[SLOT][rb] >> (8 * i));
-                mine[4 * rb + i] = ldexpf((float)d[i], ks.eq_lane + ek);
-                const int j = c.j0 + 16 * rb + 4 * grp + i;
-                x[4 * rb + i] = j < a.n ? a.s2 * mine[4 * rb + i] : -INFINITY;
-                m = fmaxf(m, x[4 * rb + i]);
-            }
-        }
-        if (h < a.G) {
-            float* lrow = a.logits + ((int64_t)c.b * a.Hq + c.g * a.G + h) * a.ld;
-#pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                const int j = c.j0 + 16 * rb + 4 * grp;
-                if (j + 4 <= a.n) {
-                    const float4 v4 = make_float4(mine[4 * rb], mine[4 * rb + 1], mine[4 * rb + 2], mine[4 * rb + 3]);
-                    if (a.nt_logits) store_stream16(lrow + j, v4);
-                    else *reinterpret_cast<float4*>(lrow + j) = v4;
-                } else {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        if (j + i < a.n) lrow[j + i] = mine[4 * rb + i];
-                }
-            }
-        }
-        // the tile's 32 rows of head h sit in lanes n16, n16 + 16, n16 + 32, n16 + 48
-        m = fmaxf(m, __shfl_xor(m, 16, 64));
-        m = fmaxf(m, __shfl_xor(m, 32, 64));
-        float z = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) z += x[i] == -INFINITY ? 0.0f : exp2_ftz(x[i] - m);
-        z += __shfl_xor(z, 16, 64);
-        z += __shfl_xor(z, 32, 64);
-        if (grp == 0 && h < a.G) tile_part[h] = make_float2(m, z);
-    }
-}
-
 // Int8 key sketch on the matrix cores (ATTN logits, G >= 4), in the split-row
 // layout of KeysF16Mfma: row 4q + 2u + p of group gr holds the 16-byte chunks
 // 2c + p (c = 0..3) of token 8q + 4u + gr's 128-byte code row, so one load
@@ -543,7 +386,6 @@ struct KeysSketchMfma8 : SketchQuery<DT> {
     static constexpr int kSlots = 2;
     static constexpr bool kGroupQuery = true;
     static constexpr bool kIntDot = true;
-    static constexpr bool kMfma = false;
     static constexpr bool kMfmaSplit = true;
     using SketchQuery<DT>::ql;
     using SketchQuery<DT>::q_tag;
@@ -604,6 +446,107 @@ struct KeysSketchMfma8 : SketchQuery<DT> {
             const int d = own + __builtin_amdgcn_update_dpp(0, send, 0xB1, 0xF, 0xF, false);
             const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * gr));
             out[gr] = ldexpf((float)d, eq_lane + ek);
+        }
+    }
+};
+
+// Int4 key sketch on the matrix cores (ATTN logits, G >= 4), split-row layout.
+// A 64-byte code row packs each group of 8 codes into one word (byte i holds
+// code i + 8 in its low nibble and code i+4 + 8 in its high nibble), so two
+// masks turn a word into 8 int8 operands in element order.  Row 4q + 2u + p of
+// group gr's 16-row operand holds the 16-byte chunks p and p + 2 of token
+// 8q + 2gr + u, lane quarter c its 8 bytes at 16p + 8(c & 1) + 32(c >> 1): one
+// load instruction reads 8 whole rows, i.e. the 4 whole 128-byte lines of 4
+// token pairs.  Column 2h + p' of the query operand holds head hc + h's codes
+// in the same order, and each column's accumulator starts at -8 times the sum
+// of those codes (the +8 of the key codes).  One DPP add joins a token's two
+// halves (even lanes: token 8q + 2gr, odd lanes 8q + 2gr + 1); one DPP
+// exchange of two sums per group then leaves 4 consecutive tokens per lane
+// (even lanes 8q .. +3, odd lanes 8q + 4 .. +7), scaled by 2^(e_q + e_k) as on
+// the vector units: the same exact logits.
+template <int DT>
+struct KeysSketchMfma4 : SketchQuery<DT> {
+    static constexpr int kSlots = 2;
+    static constexpr bool kGroupQuery = true;
+    static constexpr bool kIntDot = true;
+    static constexpr bool kMfmaSplit = true;
+    static constexpr int kRowBytes = kHeadDim / 2;
+    using SketchQuery<DT>::ql;
+    using SketchQuery<DT>::q_tag;
+    uint2 kr[kSlots][4];       // [tile][group]: the lane's 8 code bytes (two words)
+    uint32_t ek4[kSlots];      // exponents of the lane's 4 output tokens
+    uint64_t qb[2];            // query operand of the two MFMAs (column l % 16)
+    int eq_lane = 0;           // exponent of the lane's head
+    int bias = 0;              // 8 * (sum of the column's 64 query codes)
+
+    template <int SLOT>
+    __device__ __forceinline__ void load(const ScoreArgs& a, const TileCoord& c, int rg, int l8)
+    {
+        const int lane = rg * 8 + l8;
+        const int i = lane & 15, q = i >> 2, u = (i >> 1) & 1, p = i & 1, qc = lane >> 4;
+        const int64_t bg = (int64_t)c.b * a.Hkv + c.g;
+        const int8_t* kb = a.k8 + bg * a.cap * kRowBytes + 16 * p + 8 * (qc & 1) + 32 * (qc >> 1);
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            const int j = c.j0 + 8 * q + 2 * gr + u;
+            kr[SLOT][gr] = j < a.n ? load_stream8(kb + (int64_t)j * kRowBytes) : make_uint2(0u, 0u);
+        }
+        // the output tokens start at a multiple of 4 and cap is one too: one aligned word
+        const int jt = c.j0 + 8 * qc + 4 * (lane & 1);
+        ek4[SLOT] = jt < a.n ? *reinterpret_cast<const uint32_t*>(a.k_exp + bg * a.cap + jt) : 0u;
+    }
+
+    __device__ __forceinline__ void mquery(const ScoreArgs& a, const TileCoord& c, int hc, int lane)
+    {
+        const int tag = (c.b * a.Hkv + c.g) * a.G + hc;
+        if (tag == q_tag) return;
+        const int col = lane & 15, h = hc + (col >> 1), qc = lane >> 4;
+        uint4 x = make_uint4(0u, 0u, 0u, 0u);
+        eq_lane = 0;
+        if (h < a.G) {
+            // codes of the lane's key bytes: 2 per byte, at 2 * (16p' + 8(c & 1) + 32(c >> 1))
+            x = *reinterpret_cast<const uint4*>(&ql->q8[h][32 * (col & 1) + 16 * (qc & 1) + 64 * (qc >> 1)]);
+            eq_lane = ql->eq[h];
+        }
+        qb[0] = (uint64_t)x.x | ((uint64_t)x.y << 32);
+        qb[1] = (uint64_t)x.z | ((uint64_t)x.w << 32);
+        const int ones = 0x01010101;
+        int sq = __builtin_amdgcn_sdot4((int)x.x, ones, 0, false);
+        sq = __builtin_amdgcn_sdot4((int)x.y, ones, sq, false);
+        sq = __builtin_amdgcn_sdot4((int)x.z, ones, sq, false);
+        sq = __builtin_amdgcn_sdot4((int)x.w, ones, sq, false);
+        sq += __shfl_xor(sq, 16, 64);
+        sq += __shfl_xor(sq, 32, 64);
+        bias = 8 * sq;
+        q_tag = tag;
+    }
+
+    template <int SLOT>
+    __device__ __forceinline__ void dots(int lane, float (&out)[4]) const
+    {
+        const bool odd = lane & 1;
+        const uint32_t m = 0x0F0F0F0Fu;
+        int v[4];
+#pragma unroll
+        for (int gr = 0; gr < 4; ++gr) {
+            const uint2 k = kr[SLOT][gr];
+            i32x4_t acc = {-bias, -bias, -bias, -bias};
+            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8(
+                (long)((uint64_t)(k.x & m) | ((uint64_t)((k.x >> 4) & m) << 32)), (long)qb[0], acc, 0, 0, 0);
+            acc = __builtin_amdgcn_mfma_i32_16x16x32_i8(
+                (long)((uint64_t)(k.y & m) | ((uint64_t)((k.y >> 4) & m) << 32)), (long)qb[1], acc, 0, 0, 0);
+            const int own = odd ? acc[3] : acc[0];
+            const int send = odd ? acc[1] : acc[2];
+            v[gr] = own + __builtin_amdgcn_update_dpp(0, send, 0xB1, 0xF, 0xF, false);
+        }
+        // even lanes hold tokens 0, 2, 4, 6 of the lane's 8 (q = l / 16), odd lanes 1, 3, 5, 7
+        const int ra = __builtin_amdgcn_update_dpp(0, odd ? v[0] : v[2], 0xB1, 0xF, 0xF, false);
+        const int rb = __builtin_amdgcn_update_dpp(0, odd ? v[1] : v[3], 0xB1, 0xF, 0xF, false);
+        const int d[4] = {odd ? ra : v[0], odd ? v[2] : ra, odd ? rb : v[1], odd ? v[3] : rb};
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int ek = (int)(int8_t)(ek4[SLOT] >> (8 * t));
+            out[t] = ldexpf((float)d[t], eq_lane + ek);
         }
     }
 };
@@ -821,16 +764,14 @@ __global__ __launch_bounds__(256) void score_tiles_kernel(ScoreArgs a)
             }
         }
         if (t0 < a.ntiles) {
-            if constexpr (Keys::kMfma) compute_tile_mfma<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
-            else if constexpr (Keys::kMfmaSplit) compute_tile_mfma16<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
+            if constexpr (Keys::kMfmaSplit) compute_tile_mfma16<0>(a, c0, rg * 8 + l8, ks, tile_part[i0]);
             else compute_tile<GC, OUT, 0>(a, c0, rg, l8, ks, tile_part[i0]);
         } else if constexpr (OUT == kOutLogits) {
             for (int h = lane; h < a.G; h += 64) tile_part[i0][h] = make_float2(-INFINITY, 0.0f);
         }
         if (t1 < a.ntiles) {
             if constexpr (Keys::kSlots == 1) ks.template load<0>(a, c1, rg, l8);
-            if constexpr (Keys::kMfma) compute_tile_mfma<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
-            else if constexpr (Keys::kMfmaSplit)
+            if constexpr (Keys::kMfmaSplit)
                 compute_tile_mfma16<Keys::kSlots - 1>(a, c1, rg * 8 + l8, ks, tile_part[i1]);
             else compute_tile<GC, OUT, Keys::kSlots - 1>(a, c1, rg, l8, ks, tile_part[i1]);
         } else if constexpr (OUT == kOutLogits) {
